@@ -1,0 +1,183 @@
+"""Pins of the bucketing oracle, the seeded router and the FLOP/byte accounting."""
+import json
+import math
+import os
+
+import numpy as np
+import pytest
+
+from lxsynth import make_problem, config, route_gaussian, make_x, f32_to_bf16_bits
+from oracle import bucket as B
+from paper_2608_07814_amd import accounting as A
+from helpers import random_routing, tiny_tree, tiny_flat
+
+
+def _structure(layer):
+    parents = [lv.parent for lv in layer.levels]
+    n_nodes = [layer.n_anchors] + [lv.n_nodes for lv in layer.levels]
+    return parents, n_nodes
+
+
+def _eq(a, b):
+    for la, lb in zip(a, b):
+        for key in ("row_token", "offsets", "slot_row"):
+            assert np.array_equal(la[key], lb[key]), key
+
+
+@pytest.mark.parametrize("kind", ["flat", "flat_shuffled", "tree", "dense"])
+@pytest.mark.parametrize("seed", [0, 1])
+def test_bucket_definition_equals_bruteforce(kind, seed):
+    if kind == "flat":
+        layer = tiny_flat(E=12, C=3)
+    elif kind == "flat_shuffled":
+        layer = tiny_flat(E=12, C=4, shuffle=True)
+    elif kind == "tree":
+        layer = tiny_tree(E=16, n_roots=2, subs=2)
+    else:
+        layer = tiny_flat(E=5, C=5)
+        layer.levels = []
+    parents, n_nodes = _structure(layer)
+    ids, _ = random_routing(23, 4, layer.E, 200 + seed, allow_dupes=True, drop_frac=0.15,
+                            bad_frac=0.05)
+    a, fa = B.bucket(parents, n_nodes, layer.E, ids)
+    b, fb = B.bucket_bruteforce(parents, n_nodes, layer.E, ids)
+    assert fa == fb == B.FLAG_BAD_ID
+    _eq(a, b)
+
+
+def test_bucket_invariants_cfg1_shape():
+    p = make_problem(1, T=512)
+    parents, n_nodes = _structure(p.layer)
+    ids = p.routing.topk_ids
+    lv, flag = B.bucket(parents, n_nodes, p.layer.E, ids)
+    assert flag == 0
+    T, k = ids.shape
+    for li, arrs in enumerate(lv):
+        off, rt, sr = arrs["offsets"], arrs["row_token"], arrs["slot_row"]
+        assert off[0] == 0 and off[-1] == rt.size and np.all(np.diff(off) >= 0)
+        for n in range(n_nodes[li]):
+            seg = rt[off[n]:off[n + 1]]
+            assert np.all(np.diff(seg) > 0)     # unique, ascending tokens per node
+        tok = np.repeat(np.arange(T), k)
+        assert np.all(sr >= 0)                   # Gaussian routing drops nothing
+        assert np.array_equal(rt[sr], tok)       # each slot's row is its token's row
+        # every row is referenced by at least one slot
+        assert np.array_equal(np.unique(sr), np.arange(rt.size))
+    # experts level: distinct ids per token, so every slot is its own row
+    assert lv[-1]["row_token"].size == T * k
+    # anchors level: row count = unique (token, cluster) pairs
+    cl = p.layer.levels[0].parent[ids]
+    assert lv[0]["row_token"].size == sum(len(set(r)) for r in cl.tolist())
+
+
+def test_bucket_empty_and_all_dropped():
+    layer = tiny_flat(E=6, C=2)
+    parents, n_nodes = _structure(layer)
+    for ids in (np.zeros((0, 3), np.int32), np.full((4, 3), -1, np.int32)):
+        lv, flag = B.bucket(parents, n_nodes, layer.E, ids)
+        assert flag == 0
+        for li, arrs in enumerate(lv):
+            assert arrs["row_token"].size == 0
+            assert np.all(arrs["offsets"] == 0) and arrs["offsets"].size == n_nodes[li] + 1
+            assert np.all(arrs["slot_row"] == -1)
+
+
+def test_bucket_single_hot_expert():
+    """Every token routed to the same expert: one node per level has all rows."""
+    layer = tiny_flat(E=6, C=2)
+    parents, n_nodes = _structure(layer)
+    ids = np.full((9, 2), 4, np.int32)
+    ids[:, 1] = -1
+    lv, _ = B.bucket(parents, n_nodes, layer.E, ids)
+    assert np.array_equal(lv[1]["offsets"], [0, 0, 0, 0, 0, 9, 9])
+    assert np.array_equal(lv[0]["offsets"], [0, 0, 9])
+    assert np.array_equal(lv[1]["row_token"], np.arange(9))
+
+
+# ------------------------------------------------------------------ router
+@pytest.mark.parametrize("cfg", [0, 1, 4])
+def test_router_topk_and_weights(cfg):
+    c = config(cfg, T=64)
+    x = make_x(c["T"], c["d"], c["dtype"], 7)
+    r = route_gaussian(x, c["dtype"], c["E"], c["k"], 7)
+    ids, w = r.topk_ids, r.topk_weights
+    assert ids.shape == (64, c["k"]) and w.dtype == np.float32
+    assert np.all(np.abs(w.astype(np.float64).sum(1) - 1) < 1e-6)
+    assert np.all(w > 0) and np.all(np.diff(w, axis=1) <= 0)
+    for row in ids:
+        assert len(set(row.tolist())) == c["k"]
+    # brute-force top-k of the same logits
+    rng = np.random.default_rng(np.random.SeedSequence(7).spawn(8)[1])
+    w_r = rng.standard_normal((c["d"], c["E"])) / math.sqrt(c["d"])
+    xv = (x.astype(np.uint32) << 16).view(np.float32) if c["dtype"] == "bf16" else x
+    logits = xv.astype(np.float64) @ w_r
+    for t in range(8):
+        lst = sorted(range(c["E"]), key=lambda e: (-logits[t, e], e))[:c["k"]]
+        assert ids[t].tolist() == lst
+        ex = np.exp(logits[t, lst] - logits[t, lst].max())
+        assert np.allclose(w[t], ex / ex.sum(), rtol=1e-6)
+
+
+def test_community_routing_structure():
+    p = make_problem(3, T=2000)
+    ids = p.routing.topk_ids
+    cl = p.layer.levels[0].parent
+    assert all(len(set(r)) == 8 for r in ids.tolist())
+    # most slots share the token's most common cluster (p_home = 0.7 plus chance)
+    home_share = np.mean([np.bincount(cl[r], minlength=32).max() / 8 for r in ids])
+    assert 0.45 < home_share < 0.75
+    assert np.all(np.abs(p.routing.topk_weights.sum(1) - 1) < 1e-6)
+
+
+def test_bf16_rounding_is_rne():
+    vals = np.array([1.0, 1.0 + 2**-8, 1.0 + 3 * 2**-9, -2.5, 3.0e-3], dtype=np.float32)
+    bits = f32_to_bf16_bits(vals)
+    back = (bits.astype(np.uint32) << 16).view(np.float32)
+    # 1 + 2^-8 is a tie between 1 and 1 + 2^-7 -> even mantissa (1.0)
+    assert back[0] == 1.0 and back[1] == 1.0 and back[2] == np.float32(1 + 2**-7)
+    assert back[3] == -2.5
+    # half an ulp of bf16 in [2^-9, 2^-8): 2^-8 * 2^-9
+    assert abs(float(back[4]) - float(vals[4])) <= 2.0**-17
+
+
+def test_weight_scale_rule():
+    """||A B||_F is about 0.3 ||W_dom||_F for every projection."""
+    layer = tiny_flat(E=4, C=1, d=256, f=128, r=16, seed=3)
+    lv = layer.levels[0]
+    ratios = []
+    for m in range(lv.n_factors):
+        for a, b, w in ((lv.a_gate, lv.b_gate, layer.anchor_gate), (lv.a_down, lv.b_down, layer.anchor_down)):
+            ratios.append(np.linalg.norm(a[m].astype(np.float64) @ b[m]) / np.linalg.norm(w[0]))
+    assert 0.25 < np.mean(ratios) < 0.35
+
+
+# -------------------------------------------------------------- accounting
+def test_accounting_matches_paper_fig_flops(root):
+    g = json.load(open(os.path.join(root, "tests", "golden", "paper_fig_flops.json")))
+    s, pr = g["shape"], g["printed"]
+    c = A.per_token_projection_cost(s["k"], s["I"], s["H"], s["r"], s["bytes_per_elem"])
+    assert round(c["dense_matrix_bytes"] / 1e6) == pr["dense_matrix_MB"]
+    assert round(c["factor_pair_bytes"] / 1e6, 1) == pr["factor_pair_MB"]
+    assert round(c["original_flops"] / 1e6) == pr["original_MFLOPs"]
+    assert round(c["original_bytes"] / 1e6) == pr["original_MB"]
+    assert round(c["amortized_flops"] / 1e6) == pr["amortized_MFLOPs"]
+    assert round(c["amortized_bytes"] / 1e6) == pr["amortized_MB"]
+    sp = A.closed_form_speedup(s["k"], s["I"], s["H"], s["r"])
+    assert round(sp, 1) == pr["speedup_approx"]
+    assert abs(sp - c["original_flops"] / c["amortized_flops"]) < 1e-12
+    # batch-1 arithmetic intensity of one bf16 projection: 2 FLOP per 2-byte weight
+    assert round(c["original_flops"] / c["original_bytes"]) == pr["arithmetic_intensity_flop_per_byte_approx"]
+
+
+def test_algorithmic_counts_from_buckets():
+    p = make_problem(1, T=256)
+    parents, n_nodes = _structure(p.layer)
+    lv, _ = B.bucket(parents, n_nodes, p.layer.E, p.routing.topk_ids)
+    rows = A.level_rows_from_buckets([l["offsets"] for l in lv],
+                                     [None, p.layer.levels[0].factor_of], [0, 64])
+    c = A.algorithmic_counts(2048, 768, rows, 256, 8)
+    U = rows[0].rows
+    S_nd = int((p.layer.levels[0].factor_of[p.routing.topk_ids] >= 0).sum())
+    assert rows[1].rows == S_nd
+    assert c["flops"] == 6 * 2048 * 768 * U + 6 * 64 * (2048 + 768) * S_nd
+    assert c["gate_up_flops"] == 4 * 2048 * 768 * U
