@@ -1,0 +1,208 @@
+/*
+ * lorex.h -- C ABI of the LorExperts / BTExperts MoE-layer forward for MI355X.
+ *
+ * The operation (arXiv 2608.07814):
+ *   Sec. 3 "Representation": the E experts of one MoE layer are partitioned
+ *   into clusters; each cluster keeps one full-precision dominant expert and
+ *   every other member m is stored as a rank-r correction of it, per
+ *   projection:  W_m = W_dom + A_m B_m  (A output-side, B input-side).
+ *   Sec. 5 / Fig. tree (BTExperts): anchors and corrections may be nested in a
+ *   tree whose leaves are the experts; an expert's weights are the anchor plus
+ *   the corrections of every node on its path.
+ *   The router is unchanged (Fig. overview): top-k ids and weights are inputs.
+ *   Expert FFN: y = W_down (silu(W_gate x) * (W_up x)), no biases.
+ *   out[t] = sum_j topk_weights[t][j] * y_{topk_ids[t][j]}(x_t).
+ *   Sec. 5.1 "Amortized forward pass": terms shared by co-selected experts are
+ *   computed once per token; the library applies each anchor's gate/up once
+ *   per (token, anchor), each node's correction once per (token, node), and by
+ *   linearity each down projection once to the routing-weighted sum of the
+ *   activations below it.
+ *
+ * Conventions for every entry point:
+ *   - All array arguments are DEVICE pointers to caller-owned memory (the
+ *     layer descriptor structs themselves live on the host and are read during
+ *     the call only). The library never allocates, frees or retains memory.
+ *   - Weights use nn.Linear layout [out][in], input dimension contiguous.
+ *     Every array is dense row-major; pointers must be 16-byte aligned.
+ *   - x and all weights share one dtype (LX_BF16 or LX_F32). bf16 inputs are
+ *     multiplied with fp32 accumulation; fp32 inputs use fp32 arithmetic.
+ *     d and f must be multiples of 8 (LX_ERR_UNSUPPORTED otherwise), and so
+ *     must every correction rank of a bf16 layer.
+ *   - topk_ids [T][k] int32: -1 marks a dropped slot (contributes nothing);
+ *     an id < -1 or >= E is invalid: it is dropped and LX_DEVFLAG_BAD_ID is
+ *     raised in the workspace (read it with lx_read_device_status). Duplicate
+ *     ids in a row are legal and act as independent slots.
+ *   - topk_weights [T][k] fp32 are used as given (never renormalized).
+ *   - out [T][d] is fully overwritten (LX_F32 or LX_BF16).
+ *   - `workspace` is device memory of at least the size the matching
+ *     *_workspace_bytes function returns; its contents need no initialization.
+ *   - `stream` is a hipStream_t (NULL = the default stream). Every call is
+ *     asynchronous on that stream; inputs must stay valid until the stream's
+ *     work completes. The library keeps no mutable global state apart from the
+ *     optional kernel-timing records, so calls with distinct workspaces may
+ *     run concurrently.
+ *   - T = 0 is a valid no-op. Host-side argument errors are returned before
+ *     anything is enqueued; the message is available from lx_last_error().
+ */
+#ifndef LOREX_H
+#define LOREX_H
+
+#include <stddef.h>
+#include <stdint.h>
+
+#ifdef __cplusplus
+extern "C" {
+#endif
+
+typedef enum lx_status {
+  LX_OK = 0,
+  LX_ERR_INVALID_ARGUMENT = 1,   /* null/misaligned pointer, bad size or count */
+  LX_ERR_UNSUPPORTED = 2,        /* valid but not implemented (e.g. d % 8 != 0 in bf16) */
+  LX_ERR_WORKSPACE_TOO_SMALL = 3,
+  LX_ERR_HIP = 4                 /* a HIP runtime call failed */
+} lx_status;
+
+typedef enum lx_dtype { LX_F32 = 0, LX_BF16 = 1 } lx_dtype;
+
+#define LX_MAX_LEVELS 4      /* correction levels below the anchors */
+#define LX_MAX_K 32          /* largest supported top-k */
+#define LX_MAX_NODES 8192    /* largest node count of any level (incl. E) */
+
+/* Device-side status bits, accumulated in the workspace by each call. */
+#define LX_DEVFLAG_BAD_ID 1u     /* a topk id < -1 or >= E (slot dropped) */
+#define LX_DEVFLAG_BAD_TREE 2u   /* a parent or factor index out of range
+                                    (the node's expert slots are dropped or the
+                                    correction ignored) */
+
+/* One correction level of a tree (Sec. 5, Fig. tree). Node i of this level is
+ * its parent's weights plus, when factor_of[i] >= 0, the rank-`rank` product
+ * of factor pair factor_of[i]:
+ *   gate: A_gate[m] (f x rank) * B_gate[m] (rank x d)
+ *   up:   A_up[m]   (f x rank) * B_up[m]   (rank x d)
+ *   down: A_down[m] (d x rank) * B_down[m] (rank x f)            */
+typedef struct lx_level {
+  int32_t n_nodes;           /* nodes of this level */
+  int32_t rank;              /* rank of its corrections (multiple of 8 for bf16) */
+  int32_t n_factors;         /* factor pairs stored */
+  const int32_t* parent;     /* [n_nodes] node index one level up */
+  const int32_t* factor_of;  /* [n_nodes] factor pair index, or -1 (no correction) */
+  const void* a_gate;        /* [n_factors][f][rank] */
+  const void* b_gate;        /* [n_factors][rank][d] */
+  const void* a_up;          /* [n_factors][f][rank] */
+  const void* b_up;          /* [n_factors][rank][d] */
+  const void* a_down;        /* [n_factors][d][rank] */
+  const void* b_down;        /* [n_factors][rank][f] */
+} lx_level;
+
+/* A BTExperts tree (Sec. 5): dense anchors, then n_levels correction levels;
+ * the nodes of the last level are the E experts (levels[n_levels-1].n_nodes
+ * must equal E; with n_levels = 0 the anchors are the experts). */
+typedef struct lx_tree_layer {
+  int32_t E, d, f;
+  lx_dtype dtype;
+  int32_t n_anchors;
+  const void* anchor_gate;   /* [n_anchors][f][d] */
+  const void* anchor_up;     /* [n_anchors][f][d] */
+  const void* anchor_down;   /* [n_anchors][d][f] */
+  int32_t n_levels;          /* 0 .. LX_MAX_LEVELS */
+  lx_level levels[LX_MAX_LEVELS];
+} lx_tree_layer;
+
+/* A flat LorExperts layer (Sec. 3 "Representation"): C clusters, one dominant
+ * per cluster, members W_dom + A B with rank r. Equivalent to a tree with one
+ * correction level whose parent map is cluster_of. */
+typedef struct lx_flat_layer {
+  int32_t E, C, d, f, r, M;  /* experts, clusters, hidden, intermediate, rank, factor pairs */
+  lx_dtype dtype;
+  const int32_t* cluster_of; /* [E] cluster of each expert */
+  const int32_t* factor_of;  /* [E] factor pair of each expert, -1 for a dominant */
+  const void* dom_gate;      /* [C][f][d] */
+  const void* dom_up;        /* [C][f][d] */
+  const void* dom_down;      /* [C][d][f] */
+  const void* a_gate;        /* [M][f][r] */
+  const void* b_gate;        /* [M][r][d] */
+  const void* a_up;          /* [M][f][r] */
+  const void* b_up;          /* [M][r][d] */
+  const void* a_down;        /* [M][d][r] */
+  const void* b_down;        /* [M][r][f] */
+} lx_flat_layer;
+
+/* An uncompressed MoE layer (every expert stored in full): the comparator the
+ * compressed layers are measured against, computed with the same kernels and
+ * precision policy. */
+typedef struct lx_dense_layer {
+  int32_t E, d, f;
+  lx_dtype dtype;
+  const void* w_gate;        /* [E][f][d] */
+  const void* w_up;          /* [E][f][d] */
+  const void* w_down;        /* [E][d][f] */
+} lx_dense_layer;
+
+/* Human-readable name of a status code (static string). */
+const char* lx_status_string(lx_status s);
+/* Message of the last failed call on this thread ("" if none). */
+const char* lx_last_error(void);
+/* Library version, major*10000 + minor*100 + patch. */
+int32_t lx_version(void);
+
+/* Workspace bytes needed by one forward call with T tokens and top-k k.
+ * Returns 0 and sets lx_last_error() if the descriptor or sizes are invalid
+ * (only sizes and counts are inspected; no device memory is read). */
+size_t lx_moe_workspace_bytes(const lx_flat_layer* layer, int32_t T, int32_t k);
+size_t lx_moe_tree_workspace_bytes(const lx_tree_layer* layer, int32_t T, int32_t k);
+size_t lx_dense_moe_workspace_bytes(const lx_dense_layer* layer, int32_t T, int32_t k);
+
+/* Flat LorExperts forward (Sec. 3 representation, Sec. 5.1 amortization).
+ * x [T][d] (layer dtype); out [T][d] (out_dtype). */
+lx_status lx_moe_forward(const lx_flat_layer* layer, int32_t T, int32_t k,
+                         const void* x, const int32_t* topk_ids,
+                         const float* topk_weights, void* out, lx_dtype out_dtype,
+                         void* workspace, size_t workspace_bytes, void* stream);
+
+/* BTExperts tree forward (Sec. 5); same arguments as lx_moe_forward. */
+lx_status lx_moe_forward_tree(const lx_tree_layer* layer, int32_t T, int32_t k,
+                              const void* x, const int32_t* topk_ids,
+                              const float* topk_weights, void* out, lx_dtype out_dtype,
+                              void* workspace, size_t workspace_bytes, void* stream);
+
+/* Uncompressed top-k SwiGLU MoE (comparator); same arguments. */
+lx_status lx_dense_moe_forward(const lx_dense_layer* layer, int32_t T, int32_t k,
+                               const void* x, const int32_t* topk_ids,
+                               const float* topk_weights, void* out, lx_dtype out_dtype,
+                               void* workspace, size_t workspace_bytes, void* stream);
+
+/* Routing bucketing alone (the first step of every forward), exposing the
+ * arrays of one tree level `level` (0 = anchors, n_levels = experts):
+ *   row_token   [T * min(k, N_level)] (only the first node_offsets[N] entries
+ *               are written): tokens of the unique (token, node) pairs, sorted
+ *               by (node, token);
+ *   node_offsets [N_level + 1]: exclusive prefix sum of rows per node;
+ *   slot_row    [T * k]: row of the pair (t, node of slot t*k+j), or -1 for a
+ *               dropped or invalid slot.
+ * Deterministic: equal inputs give bit-identical arrays. Any of the three
+ * output pointers may be NULL. Uses the forward's workspace size. */
+lx_status lx_bucket(const lx_tree_layer* layer, int32_t T, int32_t k,
+                    const int32_t* topk_ids, int32_t level, int32_t* row_token,
+                    int32_t* node_offsets, int32_t* slot_row, void* workspace,
+                    size_t workspace_bytes, void* stream);
+
+/* Device status bits (LX_DEVFLAG_*) of the last call that used `workspace`.
+ * Synchronizes `stream`. */
+lx_status lx_read_device_status(const void* workspace, void* stream, uint32_t* flags);
+
+/* Optional kernel timing. While enabled, every kernel the library launches is
+ * bracketed by HIP events recorded on the launch stream. lx_profile_collect
+ * waits for the recorded events and adds their durations to per-kernel
+ * totals; lx_profile_entry reads total i (name is a static string). Not
+ * thread-safe; meant for benchmarks. */
+lx_status lx_profile_enable(int32_t on);
+lx_status lx_profile_collect(void);
+int32_t lx_profile_count(void);
+lx_status lx_profile_entry(int32_t i, const char** name, int64_t* launches, double* total_ms);
+lx_status lx_profile_reset(void);
+
+#ifdef __cplusplus
+}
+#endif
+
+#endif /* LOREX_H */

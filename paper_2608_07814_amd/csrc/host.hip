@@ -1,0 +1,609 @@
+// Host side of the C ABI: argument validation, workspace planning, and the
+// launch sequence of one forward (everything is enqueued on the caller's
+// stream; the host never waits on the device).
+//
+// Launch sequence for a tree with L correction levels (a flat LorExperts
+// layer is L = 1, the dense comparator L = 0):
+//   prepare                ancestors per level, validated factor indices
+//   bucket hist/scan/place unique (token, node) rows per level, tile tables
+//   level 0 gate|up GEMM   X[rows0] * [G_a; U_a]^T, once per (token, anchor)
+//   per level l >= 1       z = X[rows_l] * [B_gate; B_up]^T, dgu = z * [A_gate; A_up]^T
+//   swiglu_reduce          h = silu(g) * u per distinct expert, weighted sums per row
+//   level 0 down GEMM      hbar0 * D_a^T, once per (token, anchor)
+//   per level l >= 1       v = hbar_l * B_down^T, y_l = v * A_down^T
+//   combine                out[t] = sum of the token's rows over all levels
+#include <algorithm>
+#include <map>
+#include <string>
+#include <vector>
+
+#include "lx_internal.h"
+
+namespace lx {
+namespace {
+
+thread_local std::string g_err;
+
+lx_status fail(lx_status s, const std::string& msg) {
+  g_err = msg;
+  return s;
+}
+
+// ------------------------------------------------------------ kernel timing
+struct ProfRec {
+  const char* name;
+  hipEvent_t a, b;
+};
+bool g_prof = false;
+std::vector<ProfRec> g_pending;
+std::vector<hipEvent_t> g_pool;
+std::vector<std::pair<const char*, std::pair<int64_t, double>>> g_tot;
+
+hipEvent_t pool_get() {
+  if (!g_pool.empty()) {
+    hipEvent_t e = g_pool.back();
+    g_pool.pop_back();
+    return e;
+  }
+  hipEvent_t e = nullptr;
+  if (hipEventCreate(&e) != hipSuccess) return nullptr;
+  return e;
+}
+
+struct Timed {
+  const char* name;
+  hipStream_t s;
+  hipEvent_t a = nullptr, b = nullptr;
+  Timed(const char* n, hipStream_t st) : name(n), s(st) {
+    if (g_prof) {
+      a = pool_get();
+      b = pool_get();
+      if (a) (void)hipEventRecord(a, s);
+    }
+  }
+  void done() {
+    if (g_prof && a && b) {
+      (void)hipEventRecord(b, s);
+      g_pending.push_back({name, a, b});
+    }
+  }
+};
+
+#define LX_LAUNCH(NAME, CALL)                                                          \
+  do {                                                                                 \
+    Timed _t(NAME, stream);                                                            \
+    hipError_t _e = (CALL);                                                            \
+    _t.done();                                                                         \
+    if (_e != hipSuccess)                                                              \
+      return fail(LX_ERR_HIP, std::string(NAME) + ": " + hipGetErrorString(_e));       \
+  } while (0)
+
+// --------------------------------------------------------------- planning
+size_t align_up(size_t x) { return (x + 255) & ~size_t(255); }
+
+struct LevelPlan {
+  int N = 0, rank = 0, nfac = 0, bm = 0;
+  int64_t rows_max = 0, tiles_max = 0;
+  size_t hist, offsets, row_token, slot_row, tiles, n_tiles, fac;
+  size_t gu, z, hbar, v, y;
+};
+
+struct Plan {
+  int T, k, E, L, d, f, NT;
+  LevelPlan lv[kMaxLvl];
+  size_t flags, anc, total;
+};
+
+int level_nodes(const lx_tree_layer& t, int l) { return l == 0 ? t.n_anchors : t.levels[l - 1].n_nodes; }
+
+Plan make_plan(const lx_tree_layer& t, int T, int k) {
+  Plan p{};
+  p.T = T;
+  p.k = k;
+  p.E = t.E;
+  p.L = t.n_levels;
+  p.d = t.d;
+  p.f = t.f;
+  p.NT = (T + kTokTile - 1) / kTokTile;
+  size_t off = 0;
+  auto take = [&](size_t bytes) {
+    const size_t o = off;
+    off = align_up(off + std::max<size_t>(bytes, 16));
+    return o;
+  };
+  p.flags = take(16);  // first: lx_read_device_status reads offset 0
+  p.anc = take((size_t)(p.L + 1) * p.E * 4);
+  const size_t tk = (size_t)T * k;
+  for (int l = 0; l <= p.L; ++l) {
+    LevelPlan& q = p.lv[l];
+    q.N = level_nodes(t, l);
+    q.rank = l == 0 ? 0 : t.levels[l - 1].rank;
+    q.nfac = l == 0 ? q.N : t.levels[l - 1].n_factors;
+    q.bm = gemm_bm(t.dtype);
+    q.rows_max = (int64_t)T * std::min(k, q.N);
+    q.tiles_max = q.rows_max / q.bm + q.N + 1;
+    q.hist = take((size_t)q.N * p.NT * 4);
+    q.offsets = take((size_t)(q.N + 1) * 4);
+    q.row_token = take((size_t)q.rows_max * 4);
+    q.slot_row = take(tk * 4);
+    q.tiles = take((size_t)q.tiles_max * sizeof(TileEntry));
+    q.n_tiles = take(4);
+    q.fac = take((size_t)q.N * 4);
+    const size_t R = (size_t)q.rows_max;
+    const bool work = l == 0 || q.nfac > 0;
+    q.gu = take(work ? R * 2 * p.f * 4 : 0);
+    q.z = take(l > 0 && work ? R * 2 * q.rank * 4 : 0);
+    q.hbar = take(work ? R * p.f * 4 : 0);
+    q.v = take(l > 0 && work ? R * q.rank * 4 : 0);
+    q.y = take(work ? R * p.d * 4 : 0);
+  }
+  p.total = off;
+  return p;
+}
+
+// -------------------------------------------------------------- validation
+bool aligned(const void* p, size_t a) { return ((uintptr_t)p % a) == 0; }
+
+lx_status check_layer(const lx_tree_layer* t) {
+  if (!t) return fail(LX_ERR_INVALID_ARGUMENT, "layer is null");
+  if (t->dtype != LX_F32 && t->dtype != LX_BF16) return fail(LX_ERR_INVALID_ARGUMENT, "bad dtype");
+  if (t->E < 1 || t->d < 1 || t->f < 1 || t->n_anchors < 1)
+    return fail(LX_ERR_INVALID_ARGUMENT, "E, d, f and n_anchors must be positive");
+  if (t->n_levels < 0 || t->n_levels > LX_MAX_LEVELS)
+    return fail(LX_ERR_INVALID_ARGUMENT, "n_levels out of range");
+  if (t->E > LX_MAX_NODES || t->n_anchors > LX_MAX_NODES)
+    return fail(LX_ERR_UNSUPPORTED, "more nodes than LX_MAX_NODES");
+  if (t->d % 8 || t->f % 8) return fail(LX_ERR_UNSUPPORTED, "d and f must be multiples of 8");
+  if ((int64_t)t->f * t->d > ((int64_t)1 << 31)) return fail(LX_ERR_UNSUPPORTED, "f*d too large");
+  const int last = t->n_levels == 0 ? t->n_anchors : t->levels[t->n_levels - 1].n_nodes;
+  if (last != t->E) return fail(LX_ERR_INVALID_ARGUMENT, "the last level must have E nodes");
+  const void* aw[3] = {t->anchor_gate, t->anchor_up, t->anchor_down};
+  for (const void* q : aw)
+    if (!q || !aligned(q, 16)) return fail(LX_ERR_INVALID_ARGUMENT, "anchor weights null or not 16-byte aligned");
+  for (int l = 0; l < t->n_levels; ++l) {
+    const lx_level& v = t->levels[l];
+    if (v.n_nodes < 1 || v.n_nodes > LX_MAX_NODES) return fail(LX_ERR_INVALID_ARGUMENT, "level node count out of range");
+    if (v.n_factors < 0) return fail(LX_ERR_INVALID_ARGUMENT, "negative n_factors");
+    if (!v.parent || !v.factor_of || !aligned(v.parent, 4) || !aligned(v.factor_of, 4))
+      return fail(LX_ERR_INVALID_ARGUMENT, "level parent/factor_of null or misaligned");
+    if (v.n_factors > 0) {
+      if (v.rank < 1) return fail(LX_ERR_INVALID_ARGUMENT, "rank must be positive");
+      if (t->dtype == LX_BF16 && v.rank % 8) return fail(LX_ERR_UNSUPPORTED, "bf16 ranks must be multiples of 8");
+      const void* fw[6] = {v.a_gate, v.b_gate, v.a_up, v.b_up, v.a_down, v.b_down};
+      for (const void* q : fw)
+        if (!q || !aligned(q, 16)) return fail(LX_ERR_INVALID_ARGUMENT, "factor arrays null or not 16-byte aligned");
+    }
+  }
+  return LX_OK;
+}
+
+lx_status check_call(const lx_tree_layer* t, int T, int k) {
+  lx_status s = check_layer(t);
+  if (s != LX_OK) return s;
+  if (T < 0) return fail(LX_ERR_INVALID_ARGUMENT, "T must be >= 0");
+  if (k < 1 || k > LX_MAX_K) return fail(LX_ERR_INVALID_ARGUMENT, "k must be in [1, LX_MAX_K]");
+  if ((int64_t)T * k >= ((int64_t)1 << 31)) return fail(LX_ERR_UNSUPPORTED, "T*k too large");
+  return LX_OK;
+}
+
+lx_tree_layer flat_to_tree(const lx_flat_layer& F) {
+  lx_tree_layer t{};
+  t.E = F.E;
+  t.d = F.d;
+  t.f = F.f;
+  t.dtype = F.dtype;
+  t.n_anchors = F.C;
+  t.anchor_gate = F.dom_gate;
+  t.anchor_up = F.dom_up;
+  t.anchor_down = F.dom_down;
+  t.n_levels = 1;
+  lx_level& v = t.levels[0];
+  v.n_nodes = F.E;
+  v.rank = F.r;
+  v.n_factors = F.M;
+  v.parent = F.cluster_of;
+  v.factor_of = F.factor_of;
+  v.a_gate = F.a_gate;
+  v.b_gate = F.b_gate;
+  v.a_up = F.a_up;
+  v.b_up = F.b_up;
+  v.a_down = F.a_down;
+  v.b_down = F.b_down;
+  return t;
+}
+
+lx_tree_layer dense_to_tree(const lx_dense_layer& D) {
+  lx_tree_layer t{};
+  t.E = D.E;
+  t.d = D.d;
+  t.f = D.f;
+  t.dtype = D.dtype;
+  t.n_anchors = D.E;
+  t.anchor_gate = D.w_gate;
+  t.anchor_up = D.w_up;
+  t.anchor_down = D.w_down;
+  t.n_levels = 0;
+  return t;
+}
+
+const char* kLowIn[kMaxLvl] = {"", "lowrank_gate_up_in_l1", "lowrank_gate_up_in_l2", "lowrank_gate_up_in_l3",
+                               "lowrank_gate_up_in_l4"};
+const char* kLowOut[kMaxLvl] = {"", "lowrank_gate_up_out_l1", "lowrank_gate_up_out_l2",
+                                "lowrank_gate_up_out_l3", "lowrank_gate_up_out_l4"};
+const char* kDownIn[kMaxLvl] = {"", "lowrank_down_in_l1", "lowrank_down_in_l2", "lowrank_down_in_l3",
+                                "lowrank_down_in_l4"};
+const char* kDownOut[kMaxLvl] = {"", "lowrank_down_out_l1", "lowrank_down_out_l2", "lowrank_down_out_l3",
+                                 "lowrank_down_out_l4"};
+
+enum Stop { RUN_ALL, RUN_BUCKET };
+
+// The whole forward (or just the bucketing) of a validated tree.
+lx_status run(const lx_tree_layer& t, int T, int k, const void* x, const int32_t* ids, const float* w,
+              void* out, lx_dtype out_dtype, void* ws, size_t ws_bytes, hipStream_t stream, Stop stop,
+              Plan* plan_out = nullptr) {
+  lx_status st = check_call(&t, T, k);
+  if (st != LX_OK) return st;
+  if (stop == RUN_ALL && out_dtype != LX_F32 && out_dtype != LX_BF16)
+    return fail(LX_ERR_INVALID_ARGUMENT, "bad out_dtype");
+  if (T > 0) {
+    if (!ids || !aligned(ids, 4)) return fail(LX_ERR_INVALID_ARGUMENT, "topk_ids null or misaligned");
+    if (stop == RUN_ALL) {
+      if (!x || !aligned(x, 16)) return fail(LX_ERR_INVALID_ARGUMENT, "x null or not 16-byte aligned");
+      if (!w || !aligned(w, 4)) return fail(LX_ERR_INVALID_ARGUMENT, "topk_weights null or misaligned");
+      if (!out || !aligned(out, 16)) return fail(LX_ERR_INVALID_ARGUMENT, "out null or not 16-byte aligned");
+    }
+  }
+  const Plan P = make_plan(t, T, k);
+  if (plan_out) *plan_out = P;
+  if (!ws || !aligned(ws, 16)) return fail(LX_ERR_INVALID_ARGUMENT, "workspace null or not 16-byte aligned");
+  if (ws_bytes < P.total) return fail(LX_ERR_WORKSPACE_TOO_SMALL, "workspace smaller than required");
+  char* W = (char*)ws;
+  const int L = P.L, E = P.E, d = P.d, f = P.f;
+
+  PrepareArgs pa{};
+  pa.E = E;
+  pa.L = L;
+  pa.anc = (int32_t*)(W + P.anc);
+  pa.flags = (uint32_t*)(W + P.flags);
+  for (int l = 0; l <= L; ++l) {
+    pa.n_nodes[l] = P.lv[l].N;
+    if (l > 0) {
+      pa.n_factors[l] = t.levels[l - 1].n_factors;
+      pa.parent[l] = t.levels[l - 1].parent;
+      pa.factor_of[l] = t.levels[l - 1].factor_of;
+      pa.fac[l] = (int32_t*)(W + P.lv[l].fac);
+    }
+  }
+  LX_LAUNCH("bucket_prepare", launch_prepare(pa, stream));
+  if (T == 0) return LX_OK;
+
+  BucketArgs ba{};
+  ba.T = T;
+  ba.k = k;
+  ba.E = E;
+  ba.L = L;
+  ba.n_tok_tiles = P.NT;
+  ba.ids = ids;
+  ba.anc = pa.anc;
+  ba.flags = pa.flags;
+  for (int l = 0; l <= L; ++l) {
+    const LevelPlan& q = P.lv[l];
+    BucketLevel& b = ba.lv[l];
+    b.n_nodes = q.N;
+    b.bm = q.bm;
+    b.work_all = l == 0;
+    b.fac = l > 0 ? (const int32_t*)(W + q.fac) : nullptr;
+    b.hist = (int32_t*)(W + q.hist);
+    b.offsets = (int32_t*)(W + q.offsets);
+    b.row_token = (int32_t*)(W + q.row_token);
+    b.slot_row = (int32_t*)(W + q.slot_row);
+    b.tiles = (TileEntry*)(W + q.tiles);
+    b.n_tiles = (int32_t*)(W + q.n_tiles);
+  }
+  LX_LAUNCH("bucket_hist", launch_bucket_hist(ba, stream));
+  LX_LAUNCH("bucket_scan", launch_bucket_scan(ba, stream));
+  LX_LAUNCH("bucket_place", launch_bucket_place(ba, stream));
+  if (stop == RUN_BUCKET) return LX_OK;
+
+  const lx_dtype dt = t.dtype;
+  const int esz = dt == LX_BF16 ? 2 : 4;
+  (void)esz;
+
+  // anchor gate|up, once per (token, anchor)
+  {
+    const LevelPlan& q = P.lv[0];
+    GemmArgs g{};
+    g.tiles = ba.lv[0].tiles;
+    g.n_tiles = ba.lv[0].n_tiles;
+    g.A = x;
+    g.lda = d;
+    g.a_rows = ba.lv[0].row_token;
+    g.B[0] = t.anchor_gate;
+    g.B[1] = t.anchor_up;
+    g.b_stride[0] = g.b_stride[1] = (int64_t)f * d;
+    g.ncols[0] = g.ncols[1] = f;
+    g.K = d;
+    g.C = (float*)(W + q.gu);
+    g.ldc = 2 * (int64_t)f;
+    g.c_coloff[1] = f;
+    LX_LAUNCH("anchor_gate_up", launch_gemm(g, dt, A_BF16, (int)q.tiles_max, stream));
+  }
+  // correction gate|up per level: z = B x, then A z
+  for (int l = 1; l <= L; ++l) {
+    const LevelPlan& q = P.lv[l];
+    const lx_level& v = t.levels[l - 1];
+    if (v.n_factors == 0) continue;
+    const int r = v.rank;
+    GemmArgs g{};
+    g.tiles = ba.lv[l].tiles;
+    g.n_tiles = ba.lv[l].n_tiles;
+    g.A = x;
+    g.lda = d;
+    g.a_rows = ba.lv[l].row_token;
+    g.B[0] = v.b_gate;
+    g.B[1] = v.b_up;
+    g.b_stride[0] = g.b_stride[1] = (int64_t)r * d;
+    g.ncols[0] = g.ncols[1] = r;
+    g.K = d;
+    g.C = (float*)(W + q.z);
+    g.ldc = 2 * (int64_t)r;
+    g.c_coloff[1] = r;
+    LX_LAUNCH(kLowIn[l], launch_gemm(g, dt, A_BF16, (int)q.tiles_max, stream));
+    GemmArgs h{};
+    h.tiles = g.tiles;
+    h.n_tiles = g.n_tiles;
+    h.A = W + q.z;
+    h.lda = 2 * (int64_t)r;
+    h.a_koff[1] = r;
+    h.B[0] = v.a_gate;
+    h.B[1] = v.a_up;
+    h.b_stride[0] = h.b_stride[1] = (int64_t)f * r;
+    h.ncols[0] = h.ncols[1] = f;
+    h.K = r;
+    h.C = (float*)(W + q.gu);
+    h.ldc = 2 * (int64_t)f;
+    h.c_coloff[1] = f;
+    LX_LAUNCH(kLowOut[l], launch_gemm(h, dt, A_F32_HILO, (int)q.tiles_max, stream));
+  }
+
+  TokenArgs ta{};
+  ta.T = T;
+  ta.k = k;
+  ta.E = E;
+  ta.L = L;
+  ta.d = d;
+  ta.f = f;
+  ta.ids = ids;
+  ta.w = w;
+  ta.anc = pa.anc;
+  ta.gu0 = (const float*)(W + P.lv[0].gu);
+  for (int l = 0; l <= L; ++l) {
+    const LevelPlan& q = P.lv[l];
+    ta.slot_row[l] = ba.lv[l].slot_row;
+    ta.fac[l] = l > 0 ? (const int32_t*)(W + q.fac) : nullptr;
+    ta.dgu[l] = (const float*)(W + q.gu);
+    ta.hbar[l] = (float*)(W + q.hbar);
+    ta.y[l] = (const float*)(W + q.y);
+  }
+  ta.out = out;
+  ta.out_dtype = out_dtype;
+  LX_LAUNCH("swiglu_reduce", launch_swiglu_reduce(ta, stream));
+
+  // anchor down, once per (token, anchor), on the weighted activation sums
+  {
+    const LevelPlan& q = P.lv[0];
+    GemmArgs g{};
+    g.tiles = ba.lv[0].tiles;
+    g.n_tiles = ba.lv[0].n_tiles;
+    g.A = W + q.hbar;
+    g.lda = f;
+    g.B[0] = t.anchor_down;
+    g.b_stride[0] = (int64_t)d * f;
+    g.ncols[0] = d;
+    g.K = f;
+    g.C = (float*)(W + q.y);
+    g.ldc = d;
+    LX_LAUNCH("anchor_down", launch_gemm(g, dt, A_F32_HILO, (int)q.tiles_max, stream));
+  }
+  for (int l = 1; l <= L; ++l) {
+    const LevelPlan& q = P.lv[l];
+    const lx_level& v = t.levels[l - 1];
+    if (v.n_factors == 0) continue;
+    const int r = v.rank;
+    GemmArgs g{};
+    g.tiles = ba.lv[l].tiles;
+    g.n_tiles = ba.lv[l].n_tiles;
+    g.A = W + q.hbar;
+    g.lda = f;
+    g.B[0] = v.b_down;
+    g.b_stride[0] = (int64_t)r * f;
+    g.ncols[0] = r;
+    g.K = f;
+    g.C = (float*)(W + q.v);
+    g.ldc = r;
+    LX_LAUNCH(kDownIn[l], launch_gemm(g, dt, A_F32_HILO, (int)q.tiles_max, stream));
+    GemmArgs h{};
+    h.tiles = g.tiles;
+    h.n_tiles = g.n_tiles;
+    h.A = W + q.v;
+    h.lda = r;
+    h.B[0] = v.a_down;
+    h.b_stride[0] = (int64_t)d * r;
+    h.ncols[0] = d;
+    h.K = r;
+    h.C = (float*)(W + q.y);
+    h.ldc = d;
+    LX_LAUNCH(kDownOut[l], launch_gemm(h, dt, A_F32_HILO, (int)q.tiles_max, stream));
+  }
+  LX_LAUNCH("combine", launch_combine(ta, stream));
+  return LX_OK;
+}
+
+lx_status check_flat(const lx_flat_layer* F) {
+  if (!F) return fail(LX_ERR_INVALID_ARGUMENT, "layer is null");
+  if (F->C < 1 || F->M < 0) return fail(LX_ERR_INVALID_ARGUMENT, "C must be positive and M non-negative");
+  return LX_OK;
+}
+
+lx_status check_dense(const lx_dense_layer* D) {
+  if (!D) return fail(LX_ERR_INVALID_ARGUMENT, "layer is null");
+  return LX_OK;
+}
+
+}  // namespace
+}  // namespace lx
+
+using namespace lx;
+
+extern "C" {
+
+const char* lx_status_string(lx_status s) {
+  switch (s) {
+    case LX_OK: return "LX_OK";
+    case LX_ERR_INVALID_ARGUMENT: return "LX_ERR_INVALID_ARGUMENT";
+    case LX_ERR_UNSUPPORTED: return "LX_ERR_UNSUPPORTED";
+    case LX_ERR_WORKSPACE_TOO_SMALL: return "LX_ERR_WORKSPACE_TOO_SMALL";
+    case LX_ERR_HIP: return "LX_ERR_HIP";
+  }
+  return "LX_ERR_UNKNOWN";
+}
+
+const char* lx_last_error(void) { return g_err.c_str(); }
+
+int32_t lx_version(void) { return 100; }
+
+size_t lx_moe_tree_workspace_bytes(const lx_tree_layer* layer, int32_t T, int32_t k) {
+  if (check_call(layer, T, k) != LX_OK) return 0;
+  return make_plan(*layer, T, k).total;
+}
+
+size_t lx_moe_workspace_bytes(const lx_flat_layer* layer, int32_t T, int32_t k) {
+  if (check_flat(layer) != LX_OK) return 0;
+  const lx_tree_layer t = flat_to_tree(*layer);
+  return lx_moe_tree_workspace_bytes(&t, T, k);
+}
+
+size_t lx_dense_moe_workspace_bytes(const lx_dense_layer* layer, int32_t T, int32_t k) {
+  if (check_dense(layer) != LX_OK) return 0;
+  const lx_tree_layer t = dense_to_tree(*layer);
+  return lx_moe_tree_workspace_bytes(&t, T, k);
+}
+
+lx_status lx_moe_forward_tree(const lx_tree_layer* layer, int32_t T, int32_t k, const void* x,
+                              const int32_t* topk_ids, const float* topk_weights, void* out,
+                              lx_dtype out_dtype, void* workspace, size_t workspace_bytes, void* stream) {
+  g_err.clear();
+  if (!layer) return fail(LX_ERR_INVALID_ARGUMENT, "layer is null");
+  return run(*layer, T, k, x, topk_ids, topk_weights, out, out_dtype, workspace, workspace_bytes,
+             (hipStream_t)stream, RUN_ALL);
+}
+
+lx_status lx_moe_forward(const lx_flat_layer* layer, int32_t T, int32_t k, const void* x,
+                         const int32_t* topk_ids, const float* topk_weights, void* out, lx_dtype out_dtype,
+                         void* workspace, size_t workspace_bytes, void* stream) {
+  g_err.clear();
+  lx_status s = check_flat(layer);
+  if (s != LX_OK) return s;
+  const lx_tree_layer t = flat_to_tree(*layer);
+  return run(t, T, k, x, topk_ids, topk_weights, out, out_dtype, workspace, workspace_bytes,
+             (hipStream_t)stream, RUN_ALL);
+}
+
+lx_status lx_dense_moe_forward(const lx_dense_layer* layer, int32_t T, int32_t k, const void* x,
+                               const int32_t* topk_ids, const float* topk_weights, void* out,
+                               lx_dtype out_dtype, void* workspace, size_t workspace_bytes, void* stream) {
+  g_err.clear();
+  lx_status s = check_dense(layer);
+  if (s != LX_OK) return s;
+  const lx_tree_layer t = dense_to_tree(*layer);
+  return run(t, T, k, x, topk_ids, topk_weights, out, out_dtype, workspace, workspace_bytes,
+             (hipStream_t)stream, RUN_ALL);
+}
+
+lx_status lx_bucket(const lx_tree_layer* layer, int32_t T, int32_t k, const int32_t* topk_ids, int32_t level,
+                    int32_t* row_token, int32_t* node_offsets, int32_t* slot_row, void* workspace,
+                    size_t workspace_bytes, void* stream) {
+  g_err.clear();
+  if (!layer) return fail(LX_ERR_INVALID_ARGUMENT, "layer is null");
+  if (level < 0 || level > layer->n_levels) return fail(LX_ERR_INVALID_ARGUMENT, "level out of range");
+  Plan P{};
+  hipStream_t s = (hipStream_t)stream;
+  lx_status st = run(*layer, T, k, nullptr, topk_ids, nullptr, nullptr, LX_F32, workspace, workspace_bytes, s,
+                     RUN_BUCKET, &P);
+  if (st != LX_OK) return st;
+  const LevelPlan& q = P.lv[level];
+  const char* W = (const char*)workspace;
+  hipError_t e = hipSuccess;
+  if (T == 0) {
+    // no bucketing ran: the level has no rows
+    if (node_offsets) e = hipMemsetAsync(node_offsets, 0, (size_t)(q.N + 1) * 4, s);
+    if (e != hipSuccess) return fail(LX_ERR_HIP, hipGetErrorString(e));
+    return LX_OK;
+  }
+  if (row_token && q.rows_max > 0)
+    e = hipMemcpyAsync(row_token, W + q.row_token, (size_t)q.rows_max * 4, hipMemcpyDeviceToDevice, s);
+  if (e == hipSuccess && node_offsets)
+    e = hipMemcpyAsync(node_offsets, W + q.offsets, (size_t)(q.N + 1) * 4, hipMemcpyDeviceToDevice, s);
+  if (e == hipSuccess && slot_row)
+    e = hipMemcpyAsync(slot_row, W + q.slot_row, (size_t)T * k * 4, hipMemcpyDeviceToDevice, s);
+  if (e != hipSuccess) return fail(LX_ERR_HIP, hipGetErrorString(e));
+  return LX_OK;
+}
+
+lx_status lx_read_device_status(const void* workspace, void* stream, uint32_t* flags) {
+  g_err.clear();
+  if (!workspace || !flags) return fail(LX_ERR_INVALID_ARGUMENT, "null argument");
+  hipStream_t s = (hipStream_t)stream;
+  uint32_t v = 0;
+  hipError_t e = hipMemcpyAsync(&v, workspace, sizeof(v), hipMemcpyDeviceToHost, s);
+  if (e == hipSuccess) e = hipStreamSynchronize(s);
+  if (e != hipSuccess) return fail(LX_ERR_HIP, hipGetErrorString(e));
+  *flags = v;
+  return LX_OK;
+}
+
+lx_status lx_profile_enable(int32_t on) {
+  g_prof = on != 0;
+  return LX_OK;
+}
+
+lx_status lx_profile_collect(void) {
+  for (const ProfRec& r : g_pending) {
+    float ms = 0.f;
+    hipError_t e = hipEventSynchronize(r.b);
+    if (e == hipSuccess) e = hipEventElapsedTime(&ms, r.a, r.b);
+    if (e != hipSuccess) return fail(LX_ERR_HIP, hipGetErrorString(e));
+    auto it = std::find_if(g_tot.begin(), g_tot.end(),
+                           [&](const std::pair<const char*, std::pair<int64_t, double>>& p) {
+                             return std::string(p.first) == r.name;
+                           });
+    if (it == g_tot.end()) {
+      g_tot.push_back({r.name, {1, (double)ms}});
+    } else {
+      it->second.first += 1;
+      it->second.second += ms;
+    }
+    g_pool.push_back(r.a);
+    g_pool.push_back(r.b);
+  }
+  g_pending.clear();
+  return LX_OK;
+}
+
+int32_t lx_profile_count(void) { return (int32_t)g_tot.size(); }
+
+lx_status lx_profile_entry(int32_t i, const char** name, int64_t* launches, double* total_ms) {
+  if (i < 0 || i >= (int32_t)g_tot.size()) return fail(LX_ERR_INVALID_ARGUMENT, "profile index out of range");
+  if (name) *name = g_tot[i].first;
+  if (launches) *launches = g_tot[i].second.first;
+  if (total_ms) *total_ms = g_tot[i].second.second;
+  return LX_OK;
+}
+
+lx_status lx_profile_reset(void) {
+  lx_profile_collect();
+  g_tot.clear();
+  return LX_OK;
+}
+
+}  // extern "C"

@@ -1,0 +1,245 @@
+// Routing bucketing (first step of the forward).
+//
+// The amortized forward (Sec. 5.1) computes each shared term once per token:
+// the anchor's gate/up once per (token, anchor), each node's correction once
+// per (token, node). Bucketing lists those unique (token, node) pairs for
+// every tree level, sorted by (node, token), and maps every routing slot to
+// its row. The result is a pure function of the inputs (no atomics decide an
+// order), so it is bit-identical run to run.
+//
+// Three passes over 64-token tiles (one wavefront each):
+//   hist  : per (level, tile) a 64-bit LDS mask per node marks the tile's
+//           tokens that reach the node; popcounts give hist[node][tile];
+//   scan  : per level, an exclusive scan of hist in (node, tile) order gives
+//           each (node, tile) its first row; node offsets and the GEMM tile
+//           table follow;
+//   place : the masks are rebuilt; a token's row inside its (node, tile)
+//           segment is the popcount of the mask bits below its lane.
+#include "lx_internal.h"
+
+namespace lx {
+namespace {
+
+// Ancestors of every expert at every level and validated factor indices.
+// Single workgroup: it also zeroes the status word before anything else runs.
+__global__ __launch_bounds__(1024) void k_prepare(PrepareArgs a) {
+  __shared__ uint32_t s_bad;
+  if (threadIdx.x == 0) s_bad = 0;
+  __syncthreads();
+  uint32_t bad = 0;
+  const int E = a.E, L = a.L;
+  for (int e = threadIdx.x; e < E; e += blockDim.x) {
+    int n = e;
+    bool ok = true;
+    a.anc[(int64_t)L * E + e] = e;
+    for (int l = L; l >= 1; --l) {
+      const int p = a.parent[l][n];
+      if (p < 0 || p >= a.n_nodes[l - 1]) {
+        ok = false;
+        break;
+      }
+      n = p;
+      a.anc[(int64_t)(l - 1) * E + e] = n;
+    }
+    if (!ok) {
+      bad |= LX_DEVFLAG_BAD_TREE;
+      for (int l = 0; l <= L; ++l) a.anc[(int64_t)l * E + e] = -1;
+    }
+  }
+  for (int l = 1; l <= L; ++l) {
+    for (int n = threadIdx.x; n < a.n_nodes[l]; n += blockDim.x) {
+      int m = a.factor_of[l][n];
+      if (m < -1 || m >= a.n_factors[l]) {
+        bad |= LX_DEVFLAG_BAD_TREE;
+        m = -1;
+      }
+      a.fac[l][n] = m;
+    }
+  }
+  if (bad) atomicOr(&s_bad, bad);
+  __syncthreads();
+  if (threadIdx.x == 0) *a.flags = s_bad;
+}
+
+__device__ inline int node_of(const BucketArgs& a, int l, int e) {
+  if (e < 0 || e >= a.E) return -1;
+  return a.anc[(int64_t)l * a.E + e];
+}
+
+__device__ inline void build_masks(const BucketArgs& a, int l, int tt,
+                                   unsigned long long* s_mask, int n_nodes) {
+  const int lane = threadIdx.x;
+  for (int n = lane; n < n_nodes; n += 64) s_mask[n] = 0ull;
+  __syncthreads();
+  const int t = tt * kTokTile + lane;
+  if (t < a.T) {
+    for (int j = 0; j < a.k; ++j) {
+      const int n = node_of(a, l, a.ids[(int64_t)t * a.k + j]);
+      if (n >= 0) atomicOr(&s_mask[n], 1ull << lane);
+    }
+  }
+  __syncthreads();
+}
+
+__global__ __launch_bounds__(64) void k_bucket_hist(BucketArgs a) {
+  extern __shared__ unsigned long long s_mask[];
+  const int l = blockIdx.y, tt = blockIdx.x, lane = threadIdx.x;
+  const int N = a.lv[l].n_nodes;
+  build_masks(a, l, tt, s_mask, N);
+  int32_t* hist = a.lv[l].hist;
+  for (int n = lane; n < N; n += 64)
+    hist[(int64_t)n * a.n_tok_tiles + tt] = __popcll(s_mask[n]);
+  if (l == 0) {
+    const int t = tt * kTokTile + lane;
+    bool bad = false;
+    if (t < a.T)
+      for (int j = 0; j < a.k; ++j) {
+        const int e = a.ids[(int64_t)t * a.k + j];
+        bad |= (e < -1 || e >= a.E);
+      }
+    if (bad) atomicOr(a.flags, (uint32_t)LX_DEVFLAG_BAD_ID);
+  }
+}
+
+// Exclusive scan of one value per thread across a 1024-thread block.
+__device__ inline int block_exscan(int v, int* s_wave, int& total) {
+  const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
+  const int nwaves = blockDim.x >> 6;
+  int incl = v;
+  for (int o = 1; o < 64; o <<= 1) {
+    const int u = __shfl_up(incl, o, 64);
+    if (lane >= o) incl += u;
+  }
+  if (lane == 63) s_wave[wave] = incl;
+  __syncthreads();
+  if (threadIdx.x < 64) {
+    int w = threadIdx.x < nwaves ? s_wave[threadIdx.x] : 0;
+    int wi = w;
+    for (int o = 1; o < 64; o <<= 1) {
+      const int u = __shfl_up(wi, o, 64);
+      if (threadIdx.x >= o) wi += u;
+    }
+    if (threadIdx.x < nwaves) s_wave[threadIdx.x] = wi - w;
+    if (threadIdx.x == nwaves - 1) s_wave[63] = wi;
+  }
+  __syncthreads();
+  const int res = s_wave[wave] + incl - v;
+  total = s_wave[63];
+  __syncthreads();
+  return res;
+}
+
+__global__ __launch_bounds__(1024) void k_bucket_scan(BucketArgs a) {
+  __shared__ int s_wave[64];
+  const int l = blockIdx.x;
+  const BucketLevel lv = a.lv[l];
+  const int N = lv.n_nodes, NT = a.n_tok_tiles;
+  const int64_t total = (int64_t)N * NT;
+  const int nth = blockDim.x, tid = threadIdx.x;
+
+  // 1. exclusive scan of hist in (node, tile) order, in place
+  const int64_t chunk = (total + nth - 1) / nth;
+  const int64_t b = (int64_t)tid * chunk;
+  const int64_t e = b + chunk < total ? b + chunk : total;
+  int local = 0;
+  for (int64_t i = b; i < e; ++i) local += lv.hist[i];
+  int grand = 0;
+  int run = block_exscan(local, s_wave, grand);
+  for (int64_t i = b; i < e; ++i) {
+    const int h = lv.hist[i];
+    lv.hist[i] = run;
+    run += h;
+  }
+  __syncthreads();
+
+  // 2. node offsets
+  for (int n = tid; n < N; n += nth) lv.offsets[n] = NT > 0 ? lv.hist[(int64_t)n * NT] : 0;
+  if (tid == 0) lv.offsets[N] = grand;
+  __syncthreads();
+
+  // 3. GEMM tile table over the nodes that do work, in node order
+  const int nchunk = (N + nth - 1) / nth;
+  const int nb = tid * nchunk;
+  const int ne = nb + nchunk < N ? nb + nchunk : N;
+  int my_tiles = 0;
+  for (int n = nb; n < ne; ++n) {
+    const bool work = lv.work_all || lv.fac[n] >= 0;
+    const int cnt = lv.offsets[n + 1] - lv.offsets[n];
+    if (work && cnt > 0) my_tiles += (cnt + lv.bm - 1) / lv.bm;
+  }
+  int ntiles = 0;
+  int tpos = block_exscan(my_tiles, s_wave, ntiles);
+  for (int n = nb; n < ne; ++n) {
+    const bool work = lv.work_all || lv.fac[n] >= 0;
+    const int off = lv.offsets[n];
+    const int cnt = lv.offsets[n + 1] - off;
+    if (!work || cnt == 0) continue;
+    const int widx = lv.work_all ? n : lv.fac[n];
+    for (int r = 0; r < cnt; r += lv.bm) {
+      TileEntry te;
+      te.widx = widx;
+      te.row0 = off + r;
+      te.nrows = cnt - r < lv.bm ? cnt - r : lv.bm;
+      te.node = n;
+      lv.tiles[tpos++] = te;
+    }
+  }
+  if (tid == 0) *lv.n_tiles = ntiles;
+}
+
+__global__ __launch_bounds__(64) void k_bucket_place(BucketArgs a) {
+  extern __shared__ unsigned long long s_mask[];
+  __shared__ int s_node[kTokTile][LX_MAX_K];
+  const int l = blockIdx.y, tt = blockIdx.x, lane = threadIdx.x;
+  const BucketLevel& lv = a.lv[l];
+  build_masks(a, l, tt, s_mask, lv.n_nodes);
+  const int t = tt * kTokTile + lane;
+  if (t >= a.T) return;
+  const unsigned long long below = (1ull << lane) - 1ull;
+  for (int j = 0; j < a.k; ++j) {
+    const int64_t s = (int64_t)t * a.k + j;
+    const int n = node_of(a, l, a.ids[s]);
+    s_node[lane][j] = n;
+    if (n < 0) {
+      lv.slot_row[s] = -1;
+      continue;
+    }
+    const int row = lv.hist[(int64_t)n * a.n_tok_tiles + tt] + __popcll(s_mask[n] & below);
+    lv.slot_row[s] = row;
+    bool first = true;
+    for (int j2 = 0; j2 < j; ++j2) first &= (s_node[lane][j2] != n);
+    if (first) lv.row_token[row] = t;
+  }
+}
+
+}  // namespace
+
+static size_t mask_lds_bytes(const BucketArgs& a) {
+  int mx = 1;
+  for (int l = 0; l <= a.L; ++l) mx = a.lv[l].n_nodes > mx ? a.lv[l].n_nodes : mx;
+  return (size_t)mx * sizeof(unsigned long long);
+}
+
+hipError_t launch_prepare(const PrepareArgs& a, hipStream_t s) {
+  hipLaunchKernelGGL(k_prepare, dim3(1), dim3(1024), 0, s, a);
+  return hipGetLastError();
+}
+
+hipError_t launch_bucket_hist(const BucketArgs& a, hipStream_t s) {
+  if (a.n_tok_tiles == 0) return hipSuccess;
+  hipLaunchKernelGGL(k_bucket_hist, dim3(a.n_tok_tiles, a.L + 1), dim3(64), mask_lds_bytes(a), s, a);
+  return hipGetLastError();
+}
+
+hipError_t launch_bucket_scan(const BucketArgs& a, hipStream_t s) {
+  hipLaunchKernelGGL(k_bucket_scan, dim3(a.L + 1), dim3(1024), 0, s, a);
+  return hipGetLastError();
+}
+
+hipError_t launch_bucket_place(const BucketArgs& a, hipStream_t s) {
+  if (a.n_tok_tiles == 0) return hipSuccess;
+  hipLaunchKernelGGL(k_bucket_place, dim3(a.n_tok_tiles, a.L + 1), dim3(64), mask_lds_bytes(a), s, a);
+  return hipGetLastError();
+}
+
+}  // namespace lx

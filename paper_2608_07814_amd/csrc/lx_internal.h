@@ -1,0 +1,109 @@
+// Internal declarations shared by the host orchestration and the kernel files.
+#pragma once
+
+#include <hip/hip_runtime.h>
+#include <stdint.h>
+#include <stddef.h>
+
+#include "lorex.h"
+
+namespace lx {
+
+constexpr int kTokTile = 64;          // tokens per bucketing tile (one wavefront)
+constexpr int kMaxLvl = LX_MAX_LEVELS + 1;  // anchor level + correction levels
+
+// One GEMM tile: rows [row0, row0 + nrows) of the level's row list, all
+// belonging to `node`, whose weights are at index `widx` of the weight arrays.
+struct TileEntry {
+  int32_t widx;
+  int32_t row0;
+  int32_t nrows;
+  int32_t node;
+};
+
+// ---------------------------------------------------------------- bucketing
+struct BucketLevel {
+  int32_t n_nodes;
+  int32_t bm;              // GEMM tile height the tile table is built for
+  int32_t work_all;        // 1: every node does GEMM work (anchor level)
+  const int32_t* fac;      // validated factor index per node (-1 none)
+  int32_t* hist;           // [n_nodes][n_tok_tiles], scanned in place
+  int32_t* offsets;        // [n_nodes + 1]
+  int32_t* row_token;      // [rows_max]
+  int32_t* slot_row;       // [T * k]
+  TileEntry* tiles;        // [tiles_max]
+  int32_t* n_tiles;        // [1]
+};
+
+struct BucketArgs {
+  int32_t T, k, E, L;      // L = number of correction levels
+  int32_t n_tok_tiles;
+  const int32_t* ids;      // [T * k]
+  const int32_t* anc;      // [(L + 1) * E] ancestor per level, -1 = invalid expert
+  uint32_t* flags;
+  BucketLevel lv[kMaxLvl];
+};
+
+struct PrepareArgs {
+  int32_t E, L;
+  int32_t n_nodes[kMaxLvl];            // n_nodes[0] = anchors
+  int32_t n_factors[kMaxLvl];          // per correction level (index 0 unused)
+  const int32_t* parent[kMaxLvl];      // parent[l] for l >= 1
+  const int32_t* factor_of[kMaxLvl];   // factor_of[l] for l >= 1
+  int32_t* anc;                        // out [(L + 1) * E]
+  int32_t* fac[kMaxLvl];               // out, validated factor index (l >= 1)
+  uint32_t* flags;
+};
+
+hipError_t launch_prepare(const PrepareArgs& a, hipStream_t s);
+hipError_t launch_bucket_hist(const BucketArgs& a, hipStream_t s);
+hipError_t launch_bucket_scan(const BucketArgs& a, hipStream_t s);
+hipError_t launch_bucket_place(const BucketArgs& a, hipStream_t s);
+
+// ---------------------------------------------------------------- GEMM
+// C[row, coloff[p] + n] = sum_k A[arow(row), akoff[p] + k] * B_p[widx][n][k]
+// for the tiles of a row list; two weight "parts" share the A rows (e.g. the
+// gate and up projections of one anchor).
+struct GemmArgs {
+  const TileEntry* tiles;
+  const int32_t* n_tiles;
+  const void* A;
+  int64_t lda;
+  const int32_t* a_rows;     // gather map row -> A row, or null (identity)
+  int32_t a_koff[2];
+  const void* B[2];
+  int64_t b_stride[2];       // elements between consecutive weight indices
+  int32_t ncols[2];          // output columns of each part
+  int32_t K;
+  float* C;
+  int64_t ldc;
+  int32_t c_coloff[2];
+};
+
+enum AMode { A_BF16 = 0, A_F32_HILO = 1 };
+
+// Grid: x = upper bound on tiles, y = BN-tiles of part 0 then of part 1.
+int gemm_bm(lx_dtype dt);
+int gemm_bn(lx_dtype dt);
+hipError_t launch_gemm(const GemmArgs& g, lx_dtype dt, AMode am, int grid_x, hipStream_t s);
+
+// ---------------------------------------------------------------- elementwise
+struct TokenArgs {
+  int32_t T, k, E, L, d, f;
+  const int32_t* ids;
+  const float* w;
+  const int32_t* anc;                  // [(L + 1) * E]
+  const int32_t* fac[kMaxLvl];         // validated factor index per node (l >= 1)
+  const int32_t* slot_row[kMaxLvl];
+  const float* gu0;                    // [rows0][2f] anchor gate|up
+  const float* dgu[kMaxLvl];           // [rows_l][2f] correction gate|up (l >= 1)
+  float* hbar[kMaxLvl];                // [rows_l][f] weighted activation sums
+  const float* y[kMaxLvl];             // [rows_l][d] down outputs per level
+  void* out;
+  lx_dtype out_dtype;
+};
+
+hipError_t launch_swiglu_reduce(const TokenArgs& a, hipStream_t s);
+hipError_t launch_combine(const TokenArgs& a, hipStream_t s);
+
+}  // namespace lx

@@ -1,0 +1,333 @@
+"""Thin Python binding of liblorex.so (ctypes): argument marshalling only.
+
+Every step of the forward runs in the library's HIP kernels; torch is used for
+device memory (tensors whose ``data_ptr()`` is passed down) and for the
+current stream. The library is loaded on first use; a missing library raises.
+"""
+from __future__ import annotations
+
+import ctypes
+import os
+from dataclasses import dataclass, field
+from typing import Optional
+
+import numpy as np
+import torch
+
+_PKG = os.path.dirname(os.path.abspath(__file__))
+LIB_PATH = os.path.join(_PKG, "liblorex.so")
+
+LX_OK, LX_ERR_INVALID_ARGUMENT, LX_ERR_UNSUPPORTED, LX_ERR_WORKSPACE_TOO_SMALL, LX_ERR_HIP = range(5)
+LX_F32, LX_BF16 = 0, 1
+LX_MAX_LEVELS = 4
+LX_MAX_K = 32
+LX_MAX_NODES = 8192
+LX_DEVFLAG_BAD_ID = 1
+LX_DEVFLAG_BAD_TREE = 2
+
+_c_void = ctypes.c_void_p
+_c_i32 = ctypes.c_int32
+
+
+class LxLevel(ctypes.Structure):
+    _fields_ = [("n_nodes", _c_i32), ("rank", _c_i32), ("n_factors", _c_i32),
+                ("parent", _c_void), ("factor_of", _c_void),
+                ("a_gate", _c_void), ("b_gate", _c_void), ("a_up", _c_void), ("b_up", _c_void),
+                ("a_down", _c_void), ("b_down", _c_void)]
+
+
+class LxTreeLayer(ctypes.Structure):
+    _fields_ = [("E", _c_i32), ("d", _c_i32), ("f", _c_i32), ("dtype", _c_i32),
+                ("n_anchors", _c_i32), ("anchor_gate", _c_void), ("anchor_up", _c_void),
+                ("anchor_down", _c_void), ("n_levels", _c_i32),
+                ("levels", LxLevel * LX_MAX_LEVELS)]
+
+
+class LxFlatLayer(ctypes.Structure):
+    _fields_ = [("E", _c_i32), ("C", _c_i32), ("d", _c_i32), ("f", _c_i32), ("r", _c_i32),
+                ("M", _c_i32), ("dtype", _c_i32), ("cluster_of", _c_void), ("factor_of", _c_void),
+                ("dom_gate", _c_void), ("dom_up", _c_void), ("dom_down", _c_void),
+                ("a_gate", _c_void), ("b_gate", _c_void), ("a_up", _c_void), ("b_up", _c_void),
+                ("a_down", _c_void), ("b_down", _c_void)]
+
+
+class LxDenseLayer(ctypes.Structure):
+    _fields_ = [("E", _c_i32), ("d", _c_i32), ("f", _c_i32), ("dtype", _c_i32),
+                ("w_gate", _c_void), ("w_up", _c_void), ("w_down", _c_void)]
+
+
+EXPORTS = {
+    "lx_status_string": (ctypes.c_char_p, [_c_i32]),
+    "lx_last_error": (ctypes.c_char_p, []),
+    "lx_version": (_c_i32, []),
+    "lx_moe_workspace_bytes": (ctypes.c_size_t, [ctypes.POINTER(LxFlatLayer), _c_i32, _c_i32]),
+    "lx_moe_tree_workspace_bytes": (ctypes.c_size_t, [ctypes.POINTER(LxTreeLayer), _c_i32, _c_i32]),
+    "lx_dense_moe_workspace_bytes": (ctypes.c_size_t, [ctypes.POINTER(LxDenseLayer), _c_i32, _c_i32]),
+    "lx_moe_forward": (_c_i32, [ctypes.POINTER(LxFlatLayer), _c_i32, _c_i32, _c_void, _c_void, _c_void,
+                                _c_void, _c_i32, _c_void, ctypes.c_size_t, _c_void]),
+    "lx_moe_forward_tree": (_c_i32, [ctypes.POINTER(LxTreeLayer), _c_i32, _c_i32, _c_void, _c_void,
+                                     _c_void, _c_void, _c_i32, _c_void, ctypes.c_size_t, _c_void]),
+    "lx_dense_moe_forward": (_c_i32, [ctypes.POINTER(LxDenseLayer), _c_i32, _c_i32, _c_void, _c_void,
+                                      _c_void, _c_void, _c_i32, _c_void, ctypes.c_size_t, _c_void]),
+    "lx_bucket": (_c_i32, [ctypes.POINTER(LxTreeLayer), _c_i32, _c_i32, _c_void, _c_i32, _c_void,
+                           _c_void, _c_void, _c_void, ctypes.c_size_t, _c_void]),
+    "lx_read_device_status": (_c_i32, [_c_void, _c_void, ctypes.POINTER(ctypes.c_uint32)]),
+    "lx_profile_enable": (_c_i32, [_c_i32]),
+    "lx_profile_collect": (_c_i32, []),
+    "lx_profile_count": (_c_i32, []),
+    "lx_profile_entry": (_c_i32, [_c_i32, ctypes.POINTER(ctypes.c_char_p), ctypes.POINTER(ctypes.c_int64),
+                                  ctypes.POINTER(ctypes.c_double)]),
+    "lx_profile_reset": (_c_i32, []),
+}
+
+_LIB: Optional[ctypes.CDLL] = None
+
+
+class LorexError(RuntimeError):
+    def __init__(self, status: int, msg: str):
+        super().__init__(f"{status_string(status)}: {msg}")
+        self.status = status
+
+
+def lib() -> ctypes.CDLL:
+    """Load liblorex.so (once). Raises if it has not been built."""
+    global _LIB
+    if _LIB is None:
+        if not os.path.exists(LIB_PATH):
+            raise RuntimeError(f"{LIB_PATH} is missing: build it with "
+                               "`python -m paper_2608_07814_amd.build`")
+        L = ctypes.CDLL(LIB_PATH)
+        for name, (res, args) in EXPORTS.items():
+            fn = getattr(L, name)
+            fn.restype = res
+            fn.argtypes = args
+        _LIB = L
+    return _LIB
+
+
+def status_string(s: int) -> str:
+    return lib().lx_status_string(s).decode()
+
+
+def _check(status: int):
+    if status != LX_OK:
+        raise LorexError(status, lib().lx_last_error().decode())
+
+
+def _ptr(t: Optional[torch.Tensor]) -> Optional[int]:
+    return None if t is None else t.data_ptr()
+
+
+def _stream(stream=None) -> int:
+    if stream is None:
+        stream = torch.cuda.current_stream()
+    return stream.cuda_stream
+
+
+# ----------------------------------------------------------- device layers
+def _dev_array(a, dtype: str, device) -> torch.Tensor:
+    """numpy host array (bf16 bits as uint16, fp32, int32) -> device tensor."""
+    if isinstance(a, torch.Tensor):
+        return a.to(device).contiguous()
+    a = np.ascontiguousarray(a)
+    if a.dtype == np.uint16:
+        return torch.from_numpy(a.view(np.int16)).to(device).view(torch.bfloat16)
+    return torch.from_numpy(a).to(device)
+
+
+@dataclass
+class DeviceLevel:
+    parent: torch.Tensor
+    factor_of: torch.Tensor
+    rank: int
+    a_gate: torch.Tensor
+    b_gate: torch.Tensor
+    a_up: torch.Tensor
+    b_up: torch.Tensor
+    a_down: torch.Tensor
+    b_down: torch.Tensor
+
+    @property
+    def n_nodes(self) -> int:
+        return int(self.parent.shape[0])
+
+    @property
+    def n_factors(self) -> int:
+        return int(self.a_gate.shape[0])
+
+
+@dataclass
+class DeviceLayer:
+    """A layer's arrays in device memory plus the C descriptor that points at them."""
+    E: int
+    d: int
+    f: int
+    dtype: str
+    anchor_gate: torch.Tensor
+    anchor_up: torch.Tensor
+    anchor_down: torch.Tensor
+    levels: list = field(default_factory=list)
+
+    @property
+    def lx_dtype(self) -> int:
+        return LX_BF16 if self.dtype == "bf16" else LX_F32
+
+    @property
+    def n_anchors(self) -> int:
+        return int(self.anchor_gate.shape[0])
+
+    def tree_struct(self) -> LxTreeLayer:
+        s = LxTreeLayer()
+        s.E, s.d, s.f, s.dtype = self.E, self.d, self.f, self.lx_dtype
+        s.n_anchors = self.n_anchors
+        s.anchor_gate, s.anchor_up, s.anchor_down = (_ptr(self.anchor_gate), _ptr(self.anchor_up),
+                                                     _ptr(self.anchor_down))
+        s.n_levels = len(self.levels)
+        for i, lv in enumerate(self.levels):
+            c = s.levels[i]
+            c.n_nodes, c.rank, c.n_factors = lv.n_nodes, lv.rank, lv.n_factors
+            c.parent, c.factor_of = _ptr(lv.parent), _ptr(lv.factor_of)
+            c.a_gate, c.b_gate, c.a_up, c.b_up, c.a_down, c.b_down = (
+                _ptr(lv.a_gate), _ptr(lv.b_gate), _ptr(lv.a_up), _ptr(lv.b_up),
+                _ptr(lv.a_down), _ptr(lv.b_down))
+        return s
+
+    def flat_struct(self) -> LxFlatLayer:
+        if len(self.levels) != 1:
+            raise ValueError("a flat layer has exactly one correction level")
+        lv = self.levels[0]
+        s = LxFlatLayer()
+        s.E, s.C, s.d, s.f, s.r, s.M, s.dtype = (self.E, self.n_anchors, self.d, self.f, lv.rank,
+                                                 lv.n_factors, self.lx_dtype)
+        s.cluster_of, s.factor_of = _ptr(lv.parent), _ptr(lv.factor_of)
+        s.dom_gate, s.dom_up, s.dom_down = (_ptr(self.anchor_gate), _ptr(self.anchor_up),
+                                            _ptr(self.anchor_down))
+        s.a_gate, s.b_gate, s.a_up, s.b_up, s.a_down, s.b_down = (
+            _ptr(lv.a_gate), _ptr(lv.b_gate), _ptr(lv.a_up), _ptr(lv.b_up), _ptr(lv.a_down),
+            _ptr(lv.b_down))
+        return s
+
+    def dense_struct(self) -> LxDenseLayer:
+        if self.levels:
+            raise ValueError("a dense layer has no correction levels")
+        s = LxDenseLayer()
+        s.E, s.d, s.f, s.dtype = self.E, self.d, self.f, self.lx_dtype
+        s.w_gate, s.w_up, s.w_down = _ptr(self.anchor_gate), _ptr(self.anchor_up), _ptr(self.anchor_down)
+        return s
+
+
+def to_device(layer, device="cuda") -> DeviceLayer:
+    """Copy a host layer (fields as in ``lxsynth.Layer``) to device tensors."""
+    dt = layer.dtype
+    levels = []
+    for lv in layer.levels:
+        levels.append(DeviceLevel(
+            parent=_dev_array(np.asarray(lv.parent, dtype=np.int32), dt, device),
+            factor_of=_dev_array(np.asarray(lv.factor_of, dtype=np.int32), dt, device),
+            rank=int(lv.rank),
+            **{n: _dev_array(getattr(lv, n), dt, device)
+               for n in ("a_gate", "b_gate", "a_up", "b_up", "a_down", "b_down")}))
+    return DeviceLayer(E=int(layer.E), d=int(layer.d), f=int(layer.f), dtype=dt,
+                       anchor_gate=_dev_array(layer.anchor_gate, dt, device),
+                       anchor_up=_dev_array(layer.anchor_up, dt, device),
+                       anchor_down=_dev_array(layer.anchor_down, dt, device), levels=levels)
+
+
+# ----------------------------------------------------------------- calls
+def workspace_bytes(layer: DeviceLayer, T: int, k: int, kind: str = "tree") -> int:
+    L = lib()
+    if kind == "flat":
+        n = L.lx_moe_workspace_bytes(ctypes.byref(layer.flat_struct()), T, k)
+    elif kind == "dense":
+        n = L.lx_dense_moe_workspace_bytes(ctypes.byref(layer.dense_struct()), T, k)
+    else:
+        n = L.lx_moe_tree_workspace_bytes(ctypes.byref(layer.tree_struct()), T, k)
+    if n == 0:
+        raise LorexError(LX_ERR_INVALID_ARGUMENT, L.lx_last_error().decode())
+    return int(n)
+
+
+def alloc_workspace(layer: DeviceLayer, T: int, k: int, kind: str = "tree", device="cuda"):
+    return torch.empty(workspace_bytes(layer, T, k, kind), dtype=torch.uint8, device=device)
+
+
+def forward(layer: DeviceLayer, x: torch.Tensor, topk_ids: torch.Tensor, topk_weights: torch.Tensor,
+            out: Optional[torch.Tensor] = None, out_dtype: int = LX_F32,
+            workspace: Optional[torch.Tensor] = None, kind: Optional[str] = None, stream=None):
+    """One MoE-layer forward. ``kind``: "flat" (lx_moe_forward), "tree"
+    (lx_moe_forward_tree) or "dense" (lx_dense_moe_forward); default: flat
+    for one correction level, dense for none, tree otherwise."""
+    T, k = int(topk_ids.shape[0]), int(topk_ids.shape[1]) if topk_ids.dim() == 2 else 1
+    if kind is None:
+        kind = {0: "dense", 1: "flat"}.get(len(layer.levels), "tree")
+    if out is None:
+        out = torch.empty(T, layer.d, device=x.device,
+                          dtype=torch.float32 if out_dtype == LX_F32 else torch.bfloat16)
+    if workspace is None:
+        workspace = alloc_workspace(layer, T, k, kind, x.device)
+    for name, t in (("x", x), ("topk_ids", topk_ids), ("topk_weights", topk_weights), ("out", out)):
+        if not t.is_contiguous():
+            raise ValueError(f"{name} must be contiguous")
+    if topk_ids.dtype != torch.int32 or topk_weights.dtype != torch.float32:
+        raise ValueError("topk_ids must be int32 and topk_weights float32")
+    L = lib()
+    args = (T, k, _ptr(x), _ptr(topk_ids), _ptr(topk_weights), _ptr(out), out_dtype,
+            _ptr(workspace), workspace.numel(), _stream(stream))
+    if kind == "flat":
+        st = L.lx_moe_forward(ctypes.byref(layer.flat_struct()), *args)
+    elif kind == "dense":
+        st = L.lx_dense_moe_forward(ctypes.byref(layer.dense_struct()), *args)
+    else:
+        st = L.lx_moe_forward_tree(ctypes.byref(layer.tree_struct()), *args)
+    _check(st)
+    return out
+
+
+def bucket(layer: DeviceLayer, topk_ids: torch.Tensor, level: int,
+           workspace: Optional[torch.Tensor] = None, stream=None):
+    """Bucketing arrays of one tree level: (row_token, node_offsets, slot_row).
+    ``row_token`` is trimmed to the row count."""
+    T, k = int(topk_ids.shape[0]), int(topk_ids.shape[1])
+    N = layer.n_anchors if level == 0 else layer.levels[level - 1].n_nodes
+    dev = topk_ids.device
+    if workspace is None:
+        workspace = alloc_workspace(layer, T, k, "tree", dev)
+    row_token = torch.empty(max(T * min(k, N), 1), dtype=torch.int32, device=dev)
+    offsets = torch.empty(N + 1, dtype=torch.int32, device=dev)
+    slot_row = torch.empty(max(T * k, 1), dtype=torch.int32, device=dev)
+    st = lib().lx_bucket(ctypes.byref(layer.tree_struct()), T, k, _ptr(topk_ids), level,
+                         _ptr(row_token), _ptr(offsets), _ptr(slot_row), _ptr(workspace),
+                         workspace.numel(), _stream(stream))
+    _check(st)
+    torch.cuda.current_stream().synchronize() if stream is None else stream.synchronize()
+    n = int(offsets[-1].item())
+    return row_token[:n], offsets, slot_row[:T * k]
+
+
+def read_device_status(workspace: torch.Tensor, stream=None) -> int:
+    v = ctypes.c_uint32(0)
+    _check(lib().lx_read_device_status(_ptr(workspace), _stream(stream), ctypes.byref(v)))
+    return int(v.value)
+
+
+# ------------------------------------------------------------ kernel timing
+def profile_enable(on: bool = True):
+    _check(lib().lx_profile_enable(1 if on else 0))
+
+
+def profile_reset():
+    _check(lib().lx_profile_reset())
+
+
+def profile_read() -> dict:
+    """{kernel name: (launches, total ms)} after waiting for pending events."""
+    L = lib()
+    _check(L.lx_profile_collect())
+    out = {}
+    for i in range(L.lx_profile_count()):
+        name = ctypes.c_char_p()
+        n = ctypes.c_int64()
+        ms = ctypes.c_double()
+        _check(L.lx_profile_entry(i, ctypes.byref(name), ctypes.byref(n), ctypes.byref(ms)))
+        out[name.value.decode()] = (int(n.value), float(ms.value))
+    return out

@@ -1,0 +1,68 @@
+"""Helpers for GPU tests: run the HIP path through the C ABI on seeded inputs."""
+from __future__ import annotations
+
+import sys
+
+import numpy as np
+import pytest
+import torch
+
+from paper_2608_07814_amd import lorex as lx
+
+# max|diff| <= TOL * RMS(oracle) for bf16 inputs with fp32 accumulation
+TOL_BF16 = 1e-2
+# fp32 end to end: a tighter self-check that catches logic slips
+TOL_F32 = 1e-4
+
+
+def require_gpu():
+    if not torch.cuda.is_available():
+        pytest.skip("no GPU")
+    lx.lib()  # raises if the library is missing: no fallback exists
+
+
+def say(*a):
+    print(*a, file=sys.stderr, flush=True)
+
+
+def dev_inputs(problem, device="cuda"):
+    x = problem.x
+    if problem.layer.dtype == "bf16":
+        xt = torch.from_numpy(x.view(np.int16)).to(device).view(torch.bfloat16)
+    else:
+        xt = torch.from_numpy(x).to(device)
+    ids = torch.from_numpy(np.ascontiguousarray(problem.routing.topk_ids, dtype=np.int32)).to(device)
+    w = torch.from_numpy(np.ascontiguousarray(problem.routing.topk_weights, dtype=np.float32)).to(device)
+    return xt, ids, w
+
+
+def gpu_forward(problem, kind=None, out_dtype=lx.LX_F32, dev_layer=None, ids=None, w=None,
+                return_ws=False):
+    dl = dev_layer if dev_layer is not None else lx.to_device(problem.layer)
+    xt, ids_d, w_d = dev_inputs(problem)
+    if ids is not None:
+        ids_d = torch.from_numpy(np.ascontiguousarray(ids, dtype=np.int32)).cuda()
+    if w is not None:
+        w_d = torch.from_numpy(np.ascontiguousarray(w, dtype=np.float32)).cuda()
+    T, k = ids_d.shape
+    kind = kind or {0: "dense", 1: "flat"}.get(len(dl.levels), "tree")
+    ws = lx.alloc_workspace(dl, T, k, kind)
+    out = lx.forward(dl, xt, ids_d, w_d, out_dtype=out_dtype, workspace=ws, kind=kind)
+    torch.cuda.synchronize()
+    res = out.float().cpu().numpy().astype(np.float64)
+    return (res, ws) if return_ws else res
+
+
+def err_ratio(got, ref) -> float:
+    ref = np.asarray(ref, dtype=np.float64)
+    rms = float(np.sqrt(np.mean(ref * ref)))
+    return float(np.max(np.abs(np.asarray(got) - ref))) / (rms if rms > 0 else 1.0)
+
+
+def sample_tokens(T, n, seed):
+    """n distinct tokens including the first and the last (ragged tail)."""
+    if T <= n:
+        return np.arange(T)
+    rng = np.random.default_rng(seed)
+    mid = rng.choice(np.arange(1, T - 1), size=n - 2, replace=False)
+    return np.unique(np.concatenate([[0, T - 1], mid]))

@@ -18,11 +18,11 @@ def rel_max_err(got, ref) -> float:
     return float(np.max(np.abs(got - ref))) / rms if ref.size else 0.0
 
 
-def tiny_flat(E=6, C=2, d=8, f=12, r=3, dtype="f32", seed=5, shuffle=False):
+def tiny_flat(E=6, C=2, d=8, f=16, r=3, dtype="f32", seed=5, shuffle=False):
     return make_layer_flat(E, C, d, f, r, dtype, seed, shuffle=shuffle)
 
 
-def tiny_tree(E=8, d=8, f=6, n_roots=1, subs=2, r_sub=3, r_leaf=2, dtype="f32", seed=6):
+def tiny_tree(E=8, d=8, f=8, n_roots=1, subs=2, r_sub=3, r_leaf=2, dtype="f32", seed=6):
     return make_layer_tree(E, d, f, n_roots, subs, r_sub, r_leaf, dtype, seed)
 
 

@@ -1,0 +1,118 @@
+"""The C ABI on the CPU: library loads, exports every declared entry point, and
+host-side validation and workspace planning behave as documented. No call
+here reaches a kernel launch (no GPU in this environment)."""
+import ctypes
+import os
+import re
+
+import pytest
+
+from paper_2608_07814_amd import lorex as lx
+
+FAKE = 0x10000  # a 16-byte-aligned address that is never dereferenced
+
+
+@pytest.fixture(scope="module")
+def L(root):
+    if not os.path.exists(lx.LIB_PATH):
+        from paper_2608_07814_amd import build
+        build.build()
+    return lx.lib()
+
+
+def _declared(root):
+    src = open(os.path.join(root, "include", "lorex.h")).read()
+    src = re.sub(r"/\*.*?\*/", "", src, flags=re.S)
+    return sorted(set(re.findall(r"\b(lx_[a-z_]+)\s*\(", src)))
+
+
+def test_every_declared_symbol_is_exported(L, root):
+    names = _declared(root)
+    assert len(names) == len(lx.EXPORTS) == 16
+    for n in names:
+        assert hasattr(L, n), n
+        assert n in lx.EXPORTS, n
+
+
+def test_status_strings_and_version(L):
+    assert lx.status_string(lx.LX_OK) == "LX_OK"
+    assert lx.status_string(lx.LX_ERR_WORKSPACE_TOO_SMALL) == "LX_ERR_WORKSPACE_TOO_SMALL"
+    assert L.lx_version() >= 100
+
+
+def _tree(E=128, C=16, d=2048, f=768, r=64, levels=1, dtype=lx.LX_BF16, M=None):
+    s = lx.LxTreeLayer()
+    s.E, s.d, s.f, s.dtype = E, d, f, dtype
+    s.n_anchors = C if levels else E
+    s.anchor_gate = s.anchor_up = s.anchor_down = FAKE
+    s.n_levels = levels
+    for i in range(levels):
+        c = s.levels[i]
+        c.n_nodes = E
+        c.rank = r
+        c.n_factors = E - C if M is None else M
+        c.parent = c.factor_of = FAKE
+        c.a_gate = c.b_gate = c.a_up = c.b_up = c.a_down = c.b_down = FAKE
+    return s
+
+
+def test_workspace_bytes_valid_and_monotone(L):
+    s = _tree()
+    sizes = [L.lx_moe_tree_workspace_bytes(ctypes.byref(s), T, 8) for T in (0, 1, 64, 4096)]
+    assert all(n > 0 for n in sizes)
+    assert sizes == sorted(sizes) and sizes[3] > sizes[2] > sizes[1]
+    # a flat descriptor plans the same workspace as its one-level tree
+    f = lx.LxFlatLayer()
+    f.E, f.C, f.d, f.f, f.r, f.M, f.dtype = 128, 16, 2048, 768, 64, 112, lx.LX_BF16
+    for n in ("cluster_of", "factor_of", "dom_gate", "dom_up", "dom_down", "a_gate", "b_gate",
+              "a_up", "b_up", "a_down", "b_down"):
+        setattr(f, n, FAKE)
+    assert L.lx_moe_workspace_bytes(ctypes.byref(f), 4096, 8) == sizes[3]
+    dn = lx.LxDenseLayer()
+    dn.E, dn.d, dn.f, dn.dtype = 128, 2048, 768, lx.LX_BF16
+    dn.w_gate = dn.w_up = dn.w_down = FAKE
+    assert L.lx_dense_moe_workspace_bytes(ctypes.byref(dn), 4096, 8) > 0
+
+
+@pytest.mark.parametrize("mut,code", [
+    (lambda s: setattr(s, "d", 2044), lx.LX_ERR_UNSUPPORTED),          # d % 8
+    (lambda s: setattr(s.levels[0], "rank", 60), lx.LX_ERR_UNSUPPORTED),  # bf16 rank % 8
+    (lambda s: setattr(s.levels[0], "n_nodes", 127), lx.LX_ERR_INVALID_ARGUMENT),  # last level != E
+    (lambda s: setattr(s, "anchor_up", FAKE + 4), lx.LX_ERR_INVALID_ARGUMENT),     # misaligned
+    (lambda s: setattr(s.levels[0], "a_down", None), lx.LX_ERR_INVALID_ARGUMENT),  # null factor
+    (lambda s: setattr(s, "n_levels", 5), lx.LX_ERR_INVALID_ARGUMENT),
+    (lambda s: setattr(s, "E", 9000), lx.LX_ERR_UNSUPPORTED),
+])
+def test_descriptor_validation(L, mut, code):
+    s = _tree()
+    mut(s)
+    assert L.lx_moe_tree_workspace_bytes(ctypes.byref(s), 64, 8) == 0
+    st = L.lx_moe_forward_tree(ctypes.byref(s), 64, 8, FAKE, FAKE, FAKE, FAKE, lx.LX_F32, FAKE,
+                               1 << 40, None)
+    assert st == code, (lx.status_string(st), L.lx_last_error())
+    assert L.lx_last_error().decode()
+
+
+def test_call_validation(L):
+    s = _tree()
+    need = L.lx_moe_tree_workspace_bytes(ctypes.byref(s), 64, 8)
+    call = lambda T, k, x=FAKE, ids=FAKE, w=FAKE, out=FAKE, od=lx.LX_F32, ws=FAKE, n=need: \
+        L.lx_moe_forward_tree(ctypes.byref(s), T, k, x, ids, w, out, od, ws, n, None)
+    assert call(64, 0) == lx.LX_ERR_INVALID_ARGUMENT
+    assert call(64, 33) == lx.LX_ERR_INVALID_ARGUMENT
+    assert call(-1, 8) == lx.LX_ERR_INVALID_ARGUMENT
+    assert call(64, 8, x=None) == lx.LX_ERR_INVALID_ARGUMENT
+    assert call(64, 8, ids=None) == lx.LX_ERR_INVALID_ARGUMENT
+    assert call(64, 8, out=FAKE + 8) == lx.LX_ERR_INVALID_ARGUMENT
+    assert call(64, 8, od=7) == lx.LX_ERR_INVALID_ARGUMENT
+    assert call(64, 8, ws=None) == lx.LX_ERR_INVALID_ARGUMENT
+    assert call(64, 8, n=need - 1) == lx.LX_ERR_WORKSPACE_TOO_SMALL
+    assert L.lx_bucket(ctypes.byref(s), 64, 8, FAKE, 2, None, None, None, FAKE, need, None) \
+        == lx.LX_ERR_INVALID_ARGUMENT
+    assert L.lx_read_device_status(None, None, None) == lx.LX_ERR_INVALID_ARGUMENT
+
+
+def test_profile_entries_empty(L):
+    assert L.lx_profile_reset() == lx.LX_OK
+    assert L.lx_profile_count() == 0
+    assert L.lx_profile_entry(0, None, None, None) == lx.LX_ERR_INVALID_ARGUMENT

@@ -1,0 +1,86 @@
+"""GPU bucketing vs the oracle's definition: bit-exact arrays at every level."""
+import numpy as np
+import pytest
+import torch
+
+from lxsynth import make_problem
+from oracle import bucket as B
+from paper_2608_07814_amd import lorex as lx
+from gpu_util import require_gpu, say
+from helpers import tiny_flat, tiny_tree, random_routing
+
+pytestmark = pytest.mark.gpu
+
+
+def _structure(layer):
+    return [lv.parent for lv in layer.levels], [layer.n_anchors] + [lv.n_nodes for lv in layer.levels]
+
+
+def _check(layer, ids, expect_flag=0):
+    require_gpu()
+    dl = lx.to_device(layer)
+    ids_d = torch.from_numpy(np.ascontiguousarray(ids, dtype=np.int32)).cuda()
+    T, k = ids.shape
+    ws = lx.alloc_workspace(dl, T, k, "tree")
+    parents, n_nodes = _structure(layer)
+    ref, rflag = B.bucket(parents, n_nodes, layer.E, ids)
+    assert rflag == expect_flag
+    for li in range(layer.n_levels + 1):
+        rt, off, sr = lx.bucket(dl, ids_d, li, workspace=ws)
+        assert np.array_equal(off.cpu().numpy(), ref[li]["offsets"]), f"offsets level {li}"
+        assert np.array_equal(rt.cpu().numpy(), ref[li]["row_token"]), f"row_token level {li}"
+        assert np.array_equal(sr.cpu().numpy(), ref[li]["slot_row"]), f"slot_row level {li}"
+    assert lx.read_device_status(ws) & lx.LX_DEVFLAG_BAD_ID == expect_flag
+
+
+@pytest.mark.parametrize("cfg,T", [(0, 16), (1, 4096), (2, 64), (3, 2000), (4, 1000)])
+def test_bucket_configs(cfg, T):
+    say(f"bucket cfg{cfg} T={T}")
+    p = make_problem(cfg, T=T)
+    _check(p.layer, p.routing.topk_ids)
+
+
+@pytest.mark.parametrize("case", ["dupes_drops_bad", "all_dropped", "one_hot_expert", "T1", "ragged",
+                                  "shuffled", "dense"])
+def test_bucket_adversarial(case):
+    say(f"bucket adversarial {case}")
+    flag = 0
+    if case == "dupes_drops_bad":
+        layer = tiny_flat(E=12, C=3)
+        ids, _ = random_routing(150, 6, 12, 9, allow_dupes=True, drop_frac=0.2, bad_frac=0.05)
+        flag = lx.LX_DEVFLAG_BAD_ID
+    elif case == "all_dropped":
+        layer = tiny_flat(E=12, C=3)
+        ids = np.full((70, 4), -1, np.int32)
+    elif case == "one_hot_expert":
+        layer = tiny_flat(E=12, C=3)
+        ids = np.full((300, 3), 7, np.int32)
+        ids[:, 1] = 2
+        ids[::3, 2] = -1
+    elif case == "T1":
+        layer = tiny_tree(E=16, n_roots=2, subs=2)
+        ids = np.array([[3, 15, 4, 3]], np.int32)
+    elif case == "ragged":
+        layer = tiny_tree(E=16, n_roots=2, subs=2)
+        ids, _ = random_routing(129, 5, 16, 10)
+    elif case == "shuffled":
+        layer = tiny_flat(E=40, C=8, shuffle=True)
+        ids, _ = random_routing(333, 8, 40, 11)
+    else:
+        layer = tiny_flat(E=10, C=10)
+        layer.levels = []
+        ids, _ = random_routing(100, 4, 10, 12)
+    _check(layer, ids, flag)
+
+
+def test_bucket_deterministic():
+    require_gpu()
+    p = make_problem(1, T=4096)
+    dl = lx.to_device(p.layer)
+    ids_d = torch.from_numpy(p.routing.topk_ids).cuda()
+    ws = lx.alloc_workspace(dl, 4096, 8, "tree")
+    a = [t.cpu().numpy() for t in lx.bucket(dl, ids_d, 0, workspace=ws)]
+    for _ in range(3):
+        b = [t.cpu().numpy() for t in lx.bucket(dl, ids_d, 0, workspace=ws)]
+        for x, y in zip(a, b):
+            assert np.array_equal(x, y)

@@ -1,0 +1,226 @@
+"""GPU forward vs the fp64 oracle, element by element.
+
+Bar: max|diff| <= 1e-2 * RMS(oracle output) for bf16 inputs (fp32 output);
+fp32 layers additionally meet 1e-4 * RMS. Full-size configurations are checked
+on sampled tokens (including the first and last token) in the same launch
+configuration the benchmark times.
+"""
+import numpy as np
+import pytest
+import torch
+
+from lxsynth import make_problem, make_layer_flat
+from oracle import moe as O
+from paper_2608_07814_amd import lorex as lx
+from gpu_util import (TOL_BF16, TOL_F32, require_gpu, say, gpu_forward, err_ratio, sample_tokens,
+                      dev_inputs)
+from helpers import tiny_flat, tiny_tree, random_routing, zero_level
+
+pytestmark = pytest.mark.gpu
+
+
+def _oracle(p, tokens=None):
+    return O.moe_forward(p.layer, p.x, p.routing.topk_ids, p.routing.topk_weights, tokens=tokens)
+
+
+def test_cfg0_fp32_full():
+    require_gpu()
+    say("forward cfg0 fp32")
+    p = make_problem(0)
+    got = gpu_forward(p)
+    e = err_ratio(got, _oracle(p))
+    say(f"  cfg0 err/RMS = {e:.3e}")
+    assert e <= TOL_F32
+
+
+@pytest.mark.parametrize("seed", [1, 101, 201])
+def test_cfg1_shapes_full_compare(seed):
+    """30B-A3B-class flat layer at T=256 (several tiles, ragged last tile)."""
+    require_gpu()
+    say(f"forward cfg1 T=256 seed={seed}")
+    p = make_problem(1, seed=seed, T=256)
+    got = gpu_forward(p)
+    e = err_ratio(got, _oracle(p))
+    say(f"  err/RMS = {e:.3e}")
+    assert e <= TOL_BF16
+
+
+def test_cfg1_full_size_sampled():
+    """T=4096, the benchmark's workload and launch configuration."""
+    require_gpu()
+    say("forward cfg1 T=4096 sampled")
+    p = make_problem(1)
+    got = gpu_forward(p)
+    tok = sample_tokens(p.T, 48, 7)
+    e = err_ratio(got[tok], _oracle(p, tok))
+    say(f"  err/RMS = {e:.3e}")
+    assert e <= TOL_BF16
+    assert np.all(np.isfinite(got))
+
+
+def test_cfg2_decode_full():
+    require_gpu()
+    say("forward cfg2 T=64")
+    p = make_problem(2)
+    got = gpu_forward(p)
+    e = err_ratio(got, _oracle(p))
+    say(f"  err/RMS = {e:.3e}")
+    assert e <= TOL_BF16
+
+
+def test_cfg3_community():
+    require_gpu()
+    say("forward cfg3 T=300")
+    p = make_problem(3, T=300)
+    got = gpu_forward(p)
+    e = err_ratio(got, _oracle(p))
+    say(f"  err/RMS = {e:.3e}")
+    assert e <= TOL_BF16
+
+
+def test_cfg3_full_size_sampled():
+    require_gpu()
+    say("forward cfg3 T=16384 sampled")
+    p = make_problem(3)
+    got = gpu_forward(p)
+    tok = sample_tokens(p.T, 24, 8)
+    e = err_ratio(got[tok], _oracle(p, tok))
+    say(f"  err/RMS = {e:.3e}")
+    assert e <= TOL_BF16
+
+
+def test_cfg4_tree_small():
+    require_gpu()
+    say("forward cfg4 T=8")
+    p = make_problem(4, T=8)
+    got = gpu_forward(p)
+    e = err_ratio(got, _oracle(p))
+    say(f"  err/RMS = {e:.3e}")
+    assert e <= TOL_BF16
+
+
+def test_cfg4_tree_full_size_sampled():
+    require_gpu()
+    say("forward cfg4 T=8192 sampled")
+    p = make_problem(4)
+    got = gpu_forward(p)
+    tok = sample_tokens(p.T, 6, 9)
+    e = err_ratio(got[tok], _oracle(p, tok))
+    say(f"  err/RMS = {e:.3e}")
+    assert e <= TOL_BF16
+
+
+# ------------------------------------------------------------ edge cases
+def _tiny_problem(layer, T, k, seed, dtype=None, **kw):
+    from lxsynth import Problem, Routing
+    rng = np.random.default_rng(seed)
+    x = rng.standard_normal((T, layer.d)).astype(np.float32)
+    if layer.dtype == "bf16":
+        from lxsynth import f32_to_bf16_bits
+        x = f32_to_bf16_bits(x)
+    ids, w = random_routing(T, k, layer.E, seed + 1, **kw)
+    return Problem(cfg={}, seed=seed, layer=layer, x=x, routing=Routing(ids, w))
+
+
+@pytest.mark.parametrize("dtype", ["f32", "bf16"])
+def test_dropped_duplicate_and_bad_ids(dtype):
+    require_gpu()
+    say(f"edge ids {dtype}")
+    layer = make_layer_flat(12, 3, 64, 96, 16, dtype, 5)
+    p = _tiny_problem(layer, 77, 5, 3, allow_dupes=True, drop_frac=0.2, bad_frac=0.05)
+    got, ws = gpu_forward(p, return_ws=True)
+    ref, flag = O.moe_forward(p.layer, p.x, p.routing.topk_ids, p.routing.topk_weights,
+                              return_flag=True)
+    assert flag == O.FLAG_BAD_ID
+    assert lx.read_device_status(ws) & lx.LX_DEVFLAG_BAD_ID
+    assert err_ratio(got, ref) <= (TOL_F32 if dtype == "f32" else TOL_BF16)
+
+
+def test_all_dropped_gives_zero_and_T1():
+    require_gpu()
+    say("edge all dropped / T=1")
+    layer = make_layer_flat(8, 2, 64, 128, 8, "bf16", 6)
+    p = _tiny_problem(layer, 9, 2, 4)
+    got = gpu_forward(p, ids=np.full((9, 2), -1, np.int32))
+    assert np.all(got == 0)
+    p1 = _tiny_problem(layer, 1, 2, 5)
+    assert err_ratio(gpu_forward(p1), _oracle(p1)) <= TOL_BF16
+
+
+def test_T0_is_noop():
+    require_gpu()
+    layer = make_layer_flat(8, 2, 64, 128, 8, "bf16", 6)
+    dl = lx.to_device(layer)
+    x = torch.empty(0, 64, dtype=torch.bfloat16, device="cuda")
+    ids = torch.empty(0, 2, dtype=torch.int32, device="cuda")
+    w = torch.empty(0, 2, dtype=torch.float32, device="cuda")
+    out = lx.forward(dl, x, ids, w)
+    torch.cuda.synchronize()
+    assert out.shape == (0, 64)
+
+
+def test_hot_expert_and_empty_clusters():
+    """Every token on the same two experts: most clusters and experts empty,
+    one group spans many tiles."""
+    require_gpu()
+    say("edge hot expert")
+    layer = make_layer_flat(16, 4, 128, 256, 16, "bf16", 7)
+    p = _tiny_problem(layer, 700, 2, 6)
+    ids = np.stack([np.full(700, 5), np.full(700, 6)], 1).astype(np.int32)
+    p.routing.topk_ids[:] = ids
+    assert err_ratio(gpu_forward(p), _oracle(p)) <= TOL_BF16
+
+
+def test_shuffled_clusters_and_bf16_output():
+    require_gpu()
+    say("edge shuffled clusters, bf16 out")
+    layer = make_layer_flat(32, 8, 256, 128, 32, "bf16", 8, shuffle=True)
+    p = _tiny_problem(layer, 200, 6, 9)
+    ref = _oracle(p)
+    assert err_ratio(gpu_forward(p), ref) <= TOL_BF16
+    got16 = gpu_forward(p, out_dtype=lx.LX_BF16)
+    # bf16 rounding of the output alone is ~2^-9 relative per element
+    assert err_ratio(got16, ref) <= 4e-2
+
+
+def test_flat_tree_and_determinism():
+    """lx_moe_forward and lx_moe_forward_tree on the same flat layer agree
+    bitwise, and repeated calls are bitwise identical (no atomics)."""
+    require_gpu()
+    say("flat vs tree api, determinism")
+    p = make_problem(1, T=512)
+    dl = lx.to_device(p.layer)
+    a = gpu_forward(p, kind="flat", dev_layer=dl)
+    b = gpu_forward(p, kind="tree", dev_layer=dl)
+    c = gpu_forward(p, kind="flat", dev_layer=dl)
+    assert np.array_equal(a, b) and np.array_equal(a, c)
+
+
+def test_zero_corrections_on_gpu():
+    require_gpu()
+    say("zero corrections")
+    p = make_problem(1, T=128)
+    p.layer = zero_level(p.layer, 0)
+    assert err_ratio(gpu_forward(p), _oracle(p)) <= TOL_BF16
+
+
+def test_tree_generic_levels():
+    """A three-level tree with some factor-less nodes, fp32 and bf16."""
+    require_gpu()
+    say("generic tree")
+    for dtype in ("f32", "bf16"):
+        layer = tiny_tree(E=32, d=64, f=48, n_roots=2, subs=2, r_sub=16, r_leaf=8, dtype=dtype, seed=12)
+        layer.levels[0].factor_of[1] = -1
+        layer.levels[1].factor_of[3:9] = -1
+        p = _tiny_problem(layer, 90, 6, 13, drop_frac=0.1)
+        assert err_ratio(gpu_forward(p), _oracle(p)) <= (TOL_F32 if dtype == "f32" else TOL_BF16)
+
+
+def test_dense_comparator():
+    """L = 0: the uncompressed MoE through lx_dense_moe_forward."""
+    require_gpu()
+    say("dense comparator")
+    layer = make_layer_flat(16, 16, 256, 128, 8, "bf16", 14)
+    layer.levels = []
+    p = _tiny_problem(layer, 300, 4, 15)
+    assert err_ratio(gpu_forward(p, kind="dense"), _oracle(p)) <= TOL_BF16
