@@ -1,0 +1,303 @@
+#!/usr/bin/env python3
+"""MoE-layer forward benchmark of the LorExperts / BTExperts hot path on one GPU.
+
+Default workload: the flat LorExperts layer at 30B-A3B-class shape (d=2048,
+f=768, E=128 in 16 clusters of 8, top-8, rank 64, bf16, T=4096 tokens, seeded
+synthetic inputs, Gaussian router). One step = one call of lx_moe_forward
+(bucketing included, router excluded: ids and weights are inputs), with all
+inputs resident in HBM.
+
+Prints ONE JSON line: tokens/s of the whole layer, the roofline of the
+dominant kernel (per-kernel durations from HIP events recorded around each
+launch on the launch stream, over K further steps), the uncompressed
+dense-expert comparator on the same shapes, and the CPU oracle timed on a
+bounded token sample.
+
+  python bench.py [--gpus 1] [--steps K] [--warmup W] [--config I]
+"""
+from __future__ import annotations
+
+import argparse
+import hashlib
+import json
+import os
+import sys
+import time
+
+ROOT = os.path.dirname(os.path.abspath(__file__))
+sys.path.insert(0, ROOT)
+
+PEAK_BF16_FLOPS = 2.5e15     # MI355X dense bf16 MFMA
+PEAK_HBM_BYTES = 8.0e12      # MI355X HBM3E
+RIDGE = PEAK_BF16_FLOPS / PEAK_HBM_BYTES
+
+
+def parse():
+    ap = argparse.ArgumentParser()
+    ap.add_argument("--gpus", type=int, default=1)
+    ap.add_argument("--steps", type=int, default=200)
+    ap.add_argument("--warmup", type=int, default=20)
+    ap.add_argument("--config", type=int, default=1)
+    ap.add_argument("--seed", type=int, default=None)
+    ap.add_argument("--no-dense", action="store_true", help="skip the dense comparator")
+    ap.add_argument("--no-cpu", action="store_true", help="skip the CPU oracle baseline")
+    ap.add_argument("--cpu-tokens", type=int, default=4096)
+    ap.add_argument("--copy-calibration", action="store_true",
+                    help="only run a plain 1 GiB device-to-device copy 5 times (scales the "
+                         "FETCH_SIZE / WRITE_SIZE counters to bytes)")
+    return ap.parse_args()
+
+
+def copy_calibration(torch):
+    n = 1 << 30
+    src = torch.ones(n, dtype=torch.uint8, device="cuda")
+    dst = torch.empty_like(src)
+    torch.cuda.synchronize()
+    e0 = torch.cuda.Event(enable_timing=True)
+    e1 = torch.cuda.Event(enable_timing=True)
+    e0.record()
+    for _ in range(5):
+        dst.copy_(src)
+    e1.record()
+    torch.cuda.synchronize()
+    ms = e0.elapsed_time(e1) / 5
+    print(json.dumps({"copy_bytes": n, "ms": round(ms, 4), "read_plus_write_GBps": round(2 * n / ms / 1e6, 1)}),
+          flush=True)
+
+
+def kernel_work(name, P, rows, touched):
+    """Algorithmic (flops, bytes) of one launch of kernel ``name``.
+
+    rows[l] / touched[l]: rows doing work and distinct nodes touched at level l.
+    Bytes: the weights the launch must read (touched nodes once, bf16) plus
+    its algorithmic activation input read once (x: T*d bf16; the per-row
+    fp32 intermediates are not counted).
+    """
+    d, f, T = P["d"], P["f"], P["T"]
+    if name == "anchor_gate_up":
+        return 4 * d * f * rows[0], 2 * f * d * 2 * touched[0] + T * d * 2
+    if name == "anchor_down":
+        return 2 * d * f * rows[0], d * f * 2 * touched[0]
+    for tag in ("lowrank_gate_up_in_l", "lowrank_gate_up_out_l", "lowrank_down_in_l",
+                "lowrank_down_out_l"):
+        if name.startswith(tag):
+            l = int(name[len(tag):])
+            r = P["ranks"][l]
+            if tag == "lowrank_gate_up_in_l":
+                return 4 * r * d * rows[l], 2 * r * d * 2 * touched[l] + T * d * 2
+            if tag == "lowrank_gate_up_out_l":
+                return 4 * r * f * rows[l], 2 * f * r * 2 * touched[l]
+            if tag == "lowrank_down_in_l":
+                return 2 * r * f * rows[l], r * f * 2 * touched[l]
+            return 2 * r * d * rows[l], d * r * 2 * touched[l]
+    return 0, 0
+
+
+def source_sha():
+    h = hashlib.sha256()
+    for fn in sorted(os.listdir(os.path.join(ROOT, "paper_2608_07814_amd", "csrc"))):
+        with open(os.path.join(ROOT, "paper_2608_07814_amd", "csrc", fn), "rb") as fh:
+            h.update(fn.encode())
+            h.update(fh.read())
+    return h.hexdigest()[:16]
+
+
+def load_traffic(kernel, workload):
+    """HBM bytes per launch from committed rocprofv3 counter runs, if they were
+    taken on the current kernel sources; else None."""
+    path = os.path.join(ROOT, "profiles", "traffic.json")
+    if not os.path.exists(path):
+        return None
+    try:
+        db = json.load(open(path))
+        ent = db.get(f"{kernel}@{workload}")
+        if not ent or ent.get("source_sha") != source_sha():
+            return None
+        return ent["fetch_bytes_per_launch"] + ent["write_bytes_per_launch"]
+    except Exception:
+        return None
+
+
+def time_steps(fn, steps, warmup, torch):
+    for _ in range(warmup):
+        fn()
+    torch.cuda.synchronize()
+    e0 = torch.cuda.Event(enable_timing=True)
+    e1 = torch.cuda.Event(enable_timing=True)
+    w0 = time.perf_counter()
+    e0.record()
+    for _ in range(steps):
+        fn()
+    e1.record()
+    torch.cuda.synchronize()
+    wall = time.perf_counter() - w0
+    return e0.elapsed_time(e1) / steps, wall
+
+
+def main():
+    a = parse()
+    if a.gpus != 1:
+        print(f"bench.py runs on one GPU only (asked for --gpus {a.gpus}); this build has no "
+              "multi-GPU path.", file=sys.stderr)
+        sys.exit(2)
+    import numpy as np
+    import torch
+
+    from lxsynth import make_problem
+    from paper_2608_07814_amd import accounting as acc
+    from paper_2608_07814_amd import lorex as lx
+
+    if not torch.cuda.is_available():
+        print("bench.py needs a GPU", file=sys.stderr)
+        sys.exit(3)
+    torch.cuda.set_device(0)
+    if a.copy_calibration:
+        copy_calibration(torch)
+        return
+    p = make_problem(a.config, seed=a.seed)
+    cfg = p.cfg
+    T, k = p.T, p.k
+    layer = p.layer
+    dl = lx.to_device(layer)
+    if layer.dtype == "bf16":
+        xd = torch.from_numpy(p.x.view(np.int16)).cuda().view(torch.bfloat16)
+    else:
+        xd = torch.from_numpy(p.x).cuda()
+    ids = torch.from_numpy(p.routing.topk_ids).cuda()
+    w = torch.from_numpy(p.routing.topk_weights).cuda()
+    kind = "flat" if layer.n_levels == 1 else "tree"
+    ws = lx.alloc_workspace(dl, T, k, kind)
+    out = torch.empty(T, layer.d, dtype=torch.float32, device="cuda")
+    call = lx.PreparedCall(dl, xd, ids, w, out, ws, kind)
+
+    ms, wall = time_steps(call, a.steps, a.warmup, torch)
+    tokens_per_s = T / (ms * 1e-3)
+
+    # per-kernel durations: HIP events around every launch, same stream
+    lx.profile_reset()
+    lx.profile_enable(True)
+    for _ in range(a.steps):
+        call()
+    torch.cuda.synchronize()
+    prof = lx.profile_read()
+    lx.profile_enable(False)
+
+    # bucket counts (outside the timed regions) for the algorithmic counts
+    n_lv = layer.n_levels
+    rows, touched = [], []
+    for l in range(n_lv + 1):
+        _, off, _ = lx.bucket(dl, ids, l, workspace=ws)
+        cnt = np.diff(off.cpu().numpy().astype(np.int64))
+        if l > 0:
+            cnt = np.where(layer.levels[l - 1].factor_of >= 0, cnt, 0)
+        rows.append(int(cnt.sum()))
+        touched.append(int((cnt > 0).sum()))
+    ranks = [0] + [lv.rank for lv in layer.levels]
+    lvrows = [acc.LevelRows(rank=ranks[l], rows=rows[l], nodes_touched=touched[l])
+              for l in range(n_lv + 1)]
+    work = acc.algorithmic_counts(layer.d, layer.f, lvrows, T, k)
+    P = dict(d=layer.d, f=layer.f, T=T, ranks=ranks)
+
+    kernels = {}
+    for name, (n, tot) in prof.items():
+        fl, by = kernel_work(name, P, rows, touched)
+        avg_ms = tot / max(n, 1)
+        kernels[name] = dict(launches=n, avg_us=round(avg_ms * 1e3, 3),
+                             share=None, alg_tflops=round(fl / (avg_ms * 1e-3) / 1e12, 2) if fl else None,
+                             alg_gbps=round(by / (avg_ms * 1e-3) / 1e9, 1) if by else None)
+    tot_all = sum(v[1] for v in prof.values())
+    for name, (n, tot) in prof.items():
+        kernels[name]["share"] = round(tot / tot_all, 4)
+    dom = max(prof.items(), key=lambda kv: kv[1][1])[0]
+    fl, by = kernel_work(dom, P, rows, touched)
+    dom_avg_s = prof[dom][1] / prof[dom][0] * 1e-3
+    workload = cfg["name"]
+    if fl and fl / max(by, 1) >= RIDGE:
+        roof = dict(bound="mfma", achieved=round(fl / dom_avg_s / 1e12, 2), peak=PEAK_BF16_FLOPS / 1e12,
+                    unit="TFLOP/s", frac=round(fl / dom_avg_s / PEAK_BF16_FLOPS, 4))
+    else:
+        roof = dict(bound="hbm", achieved=round(by / dom_avg_s / 1e9, 1), peak=PEAK_HBM_BYTES / 1e9,
+                    unit="GB/s", frac=round(by / dom_avg_s / PEAK_HBM_BYTES, 4))
+    roof["kernel"] = dom
+    roof["alg_flops_per_launch"] = fl
+    roof["alg_bytes_per_launch"] = by
+    roof["avg_launch_us"] = round(dom_avg_s * 1e6, 3)
+    roof["traffic"] = load_traffic(dom, workload)
+
+    step_s = ms * 1e-3
+    layer_perf = dict(alg_gflop=round(work["flops"] / 1e9, 2), alg_mbytes=round(work["bytes"] / 1e6, 1),
+                      alg_tflops=round(work["flops"] / step_s / 1e12, 2),
+                      frac_bf16_peak=round(work["flops"] / step_s / PEAK_BF16_FLOPS, 4),
+                      alg_gbps=round(work["bytes"] / step_s / 1e9, 1),
+                      frac_hbm_peak=round(work["bytes"] / step_s / PEAK_HBM_BYTES, 4),
+                      rows_per_level=rows, nodes_touched=touched)
+
+    dense = None
+    if not a.no_dense and kind == "flat":
+        # uncompressed comparator: every expert dom + A B rounded to bf16 (setup, untimed)
+        lv = dl.levels[0]
+        cl = lv.parent.long()
+        fo = lv.factor_of.long()
+        wg = dl.anchor_gate[cl].float()
+        wu = dl.anchor_up[cl].float()
+        wd = dl.anchor_down[cl].float()
+        m = fo >= 0
+        fi = fo[m]
+        wg[m] += torch.bmm(lv.a_gate[fi].float(), lv.b_gate[fi].float())
+        wu[m] += torch.bmm(lv.a_up[fi].float(), lv.b_up[fi].float())
+        wd[m] += torch.bmm(lv.a_down[fi].float(), lv.b_down[fi].float())
+        dd = lx.DeviceLayer(E=layer.E, d=layer.d, f=layer.f, dtype="bf16",
+                            anchor_gate=wg.bfloat16().contiguous(), anchor_up=wu.bfloat16().contiguous(),
+                            anchor_down=wd.bfloat16().contiguous(), levels=[])
+        del wg, wu, wd
+        wsd = lx.alloc_workspace(dd, T, k, "dense")
+        outd = torch.empty_like(out)
+        dcall = lx.PreparedCall(dd, xd, ids, w, outd, wsd, "dense")
+        dms, _ = time_steps(dcall, a.steps, a.warmup, torch)
+        dense = dict(tokens_per_s=round(T / (dms * 1e-3), 1), ms_per_step=round(dms, 4),
+                     speedup_of_compressed=round(dms / ms, 3),
+                     alg_gflop=round(6 * layer.d * layer.f * T * k / 1e9, 2))
+        del dd, wsd, outd
+
+    cpu = None
+    if not a.no_cpu:
+        from threadpoolctl import threadpool_info
+        from oracle import moe as O
+        n = min(a.cpu_tokens, T)
+        t0 = time.perf_counter()
+        O.moe_forward(layer, p.x, p.routing.topk_ids, p.routing.topk_weights, tokens=np.arange(n))
+        dt = time.perf_counter() - t0
+        threads = max([i.get("num_threads", 1) for i in threadpool_info()] or [1])
+        cpu = dict(value=round(n / dt, 2), unit="tokens/s", cores=int(threads), kind="oracle",
+                   sample=f"first {n} of {T} tokens of the same workload, fp64 numpy oracle "
+                          f"(dense reconstruction of every routed expert + per-slot SwiGLU), "
+                          f"{dt:.1f} s wall", nproc=os.cpu_count())
+
+    res = {
+        "metric": "MoE-layer tokens/s (LorExperts forward, bucketing included)",
+        "value": round(tokens_per_s, 1),
+        "unit": "tokens/s",
+        "n_gpus": 1,
+        "steps": a.steps,
+        "warmup": a.warmup,
+        "ms_per_step": round(ms, 4),
+        "wall_s_timed": round(wall, 3),
+        "higher_is_better": True,
+        "scaling": "weak",
+        "vs_baseline": None,
+        "dtype": "bf16",
+        "data": "synthetic (seeded; Gaussian or community routing; random-init weights)",
+        "config": {"workload": workload, "T": T, "d": layer.d, "f": layer.f, "E": layer.E,
+                   "k": k, "anchors": layer.n_anchors, "ranks": ranks[1:], "layer": kind,
+                   "seed": p.seed, "out_dtype": "f32"},
+        "roofline": roof,
+        "layer_roofline": layer_perf,
+        "kernels": kernels,
+        "dense_comparator": dense,
+        "cpu_baseline": cpu,
+    }
+    print(json.dumps(res), flush=True)
+
+
+if __name__ == "__main__":
+    main()

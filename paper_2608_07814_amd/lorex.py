@@ -331,3 +331,28 @@ def profile_read() -> dict:
         _check(L.lx_profile_entry(i, ctypes.byref(name), ctypes.byref(n), ctypes.byref(ms)))
         out[name.value.decode()] = (int(n.value), float(ms.value))
     return out
+
+
+class PreparedCall:
+    """A forward call with every argument marshalled once; ``__call__`` only
+    re-issues the C call (for timing loops)."""
+
+    def __init__(self, layer: DeviceLayer, x: torch.Tensor, topk_ids: torch.Tensor,
+                 topk_weights: torch.Tensor, out: torch.Tensor, workspace: torch.Tensor,
+                 kind: str, out_dtype: int = LX_F32, stream=None):
+        L = lib()
+        self._keep = (layer, x, topk_ids, topk_weights, out, workspace)
+        if kind == "flat":
+            self._desc, self._fn = layer.flat_struct(), L.lx_moe_forward
+        elif kind == "dense":
+            self._desc, self._fn = layer.dense_struct(), L.lx_dense_moe_forward
+        else:
+            self._desc, self._fn = layer.tree_struct(), L.lx_moe_forward_tree
+        T, k = int(topk_ids.shape[0]), int(topk_ids.shape[1])
+        self._args = (ctypes.byref(self._desc), T, k, _ptr(x), _ptr(topk_ids), _ptr(topk_weights),
+                      _ptr(out), out_dtype, _ptr(workspace), workspace.numel(), _stream(stream))
+
+    def __call__(self):
+        st = self._fn(*self._args)
+        if st != LX_OK:
+            _check(st)
