@@ -82,9 +82,9 @@ struct Timed {
 size_t align_up(size_t x) { return (x + 255) & ~size_t(255); }
 
 struct LevelPlan {
-  int N = 0, rank = 0, nfac = 0, bm = 0;
-  int64_t rows_max = 0, tiles_max = 0;
-  size_t hist, offsets, row_token, slot_row, tiles, n_tiles, fac;
+  int N = 0, rank = 0, nfac = 0, bm = 0, bm2 = 0;
+  int64_t rows_max = 0, tiles_max = 0, tiles2_max = 0;
+  size_t hist, offsets, row_token, slot_row, tiles, n_tiles, tiles2, n_tiles2, fac;
   size_t gu, z, hbar, v, y;
 };
 
@@ -120,14 +120,18 @@ Plan make_plan(const lx_tree_layer& t, int T, int k) {
     q.rank = l == 0 ? 0 : t.levels[l - 1].rank;
     q.nfac = l == 0 ? q.N : t.levels[l - 1].n_factors;
     q.bm = gemm_bm(t.dtype);
+    q.bm2 = gemm_big_bm();
     q.rows_max = (int64_t)T * std::min(k, q.N);
     q.tiles_max = q.rows_max / q.bm + q.N + 1;
+    q.tiles2_max = q.rows_max / q.bm2 + q.N + 1;
     q.hist = take((size_t)q.N * p.NT * 4);
     q.offsets = take((size_t)(q.N + 1) * 4);
     q.row_token = take((size_t)q.rows_max * 4);
     q.slot_row = take(tk * 4);
     q.tiles = take((size_t)q.tiles_max * sizeof(TileEntry));
     q.n_tiles = take(4);
+    q.tiles2 = take((size_t)q.tiles2_max * sizeof(TileEntry));
+    q.n_tiles2 = take(4);
     q.fac = take((size_t)q.N * 4);
     const size_t R = (size_t)q.rows_max;
     const bool work = l == 0 || q.nfac > 0;
@@ -291,6 +295,7 @@ lx_status run(const lx_tree_layer& t, int T, int k, const void* x, const int32_t
     BucketLevel& b = ba.lv[l];
     b.n_nodes = q.N;
     b.bm = q.bm;
+    b.bm2 = q.bm2;
     b.work_all = l == 0;
     b.fac = l > 0 ? (const int32_t*)(W + q.fac) : nullptr;
     b.hist = (int32_t*)(W + q.hist);
@@ -299,6 +304,8 @@ lx_status run(const lx_tree_layer& t, int T, int k, const void* x, const int32_t
     b.slot_row = (int32_t*)(W + q.slot_row);
     b.tiles = (TileEntry*)(W + q.tiles);
     b.n_tiles = (int32_t*)(W + q.n_tiles);
+    b.tiles2 = (TileEntry*)(W + q.tiles2);
+    b.n_tiles2 = (int32_t*)(W + q.n_tiles2);
   }
   LX_LAUNCH("bucket_hist", launch_bucket_hist(ba, stream));
   LX_LAUNCH("bucket_scan", launch_bucket_scan(ba, stream));
@@ -326,7 +333,13 @@ lx_status run(const lx_tree_layer& t, int T, int k, const void* x, const int32_t
     g.C = (float*)(W + q.gu);
     g.ldc = 2 * (int64_t)f;
     g.c_coloff[1] = f;
-    LX_LAUNCH("anchor_gate_up", launch_gemm(g, dt, A_BF16, (int)q.tiles_max, stream));
+    if (dt == LX_BF16 && gemm_big_ok(g, T)) {
+      g.tiles = ba.lv[0].tiles2;
+      g.n_tiles = ba.lv[0].n_tiles2;
+      LX_LAUNCH("anchor_gate_up", launch_gemm_big(g, 256, (int)q.tiles2_max, stream));
+    } else {
+      LX_LAUNCH("anchor_gate_up", launch_gemm(g, dt, A_BF16, (int)q.tiles_max, stream));
+    }
   }
   // correction gate|up per level: z = B x, then A z
   for (int l = 1; l <= L; ++l) {
@@ -387,10 +400,31 @@ lx_status run(const lx_tree_layer& t, int T, int k, const void* x, const int32_t
   }
   ta.out = out;
   ta.out_dtype = out_dtype;
+  // bf16 layers keep the anchor-level activation sums as a bf16 (hi, lo) pair
+  // so the down projection runs on the large-tile bf16 kernel
+  GemmArgs gdown{};
+  {
+    const LevelPlan& q = P.lv[0];
+    gdown.tiles = ba.lv[0].tiles2;
+    gdown.n_tiles = ba.lv[0].n_tiles2;
+    gdown.A = W + q.hbar;
+    gdown.lda = 2 * (int64_t)f;
+    gdown.B[0] = gdown.B[1] = t.anchor_down;
+    gdown.b_stride[0] = gdown.b_stride[1] = (int64_t)d * f;
+    gdown.ncols[0] = d;
+    gdown.K = 2 * f;
+    gdown.Kb = f;
+    gdown.C = (float*)(W + q.y);
+    gdown.ldc = d;
+  }
+  const bool down_big = dt == LX_BF16 && gemm_big_ok(gdown, P.lv[0].rows_max);
+  ta.hbar0_hilo = down_big ? 1 : 0;
   LX_LAUNCH("swiglu_reduce", launch_swiglu_reduce(ta, stream));
 
   // anchor down, once per (token, anchor), on the weighted activation sums
-  {
+  if (down_big) {
+    LX_LAUNCH("anchor_down", launch_gemm_big(gdown, 256, (int)P.lv[0].tiles2_max, stream));
+  } else {
     const LevelPlan& q = P.lv[0];
     GemmArgs g{};
     g.tiles = ba.lv[0].tiles;

@@ -157,34 +157,39 @@ __global__ __launch_bounds__(1024) void k_bucket_scan(BucketArgs a) {
   if (tid == 0) lv.offsets[N] = grand;
   __syncthreads();
 
-  // 3. GEMM tile table over the nodes that do work, in node order
+  // 3. GEMM tile tables over the nodes that do work, in node order: one for
+  //    tile height bm, one for bm2
   const int nchunk = (N + nth - 1) / nth;
   const int nb = tid * nchunk;
   const int ne = nb + nchunk < N ? nb + nchunk : N;
-  int my_tiles = 0;
-  for (int n = nb; n < ne; ++n) {
-    const bool work = lv.work_all || lv.fac[n] >= 0;
-    const int cnt = lv.offsets[n + 1] - lv.offsets[n];
-    if (work && cnt > 0) my_tiles += (cnt + lv.bm - 1) / lv.bm;
-  }
-  int ntiles = 0;
-  int tpos = block_exscan(my_tiles, s_wave, ntiles);
-  for (int n = nb; n < ne; ++n) {
-    const bool work = lv.work_all || lv.fac[n] >= 0;
-    const int off = lv.offsets[n];
-    const int cnt = lv.offsets[n + 1] - off;
-    if (!work || cnt == 0) continue;
-    const int widx = lv.work_all ? n : lv.fac[n];
-    for (int r = 0; r < cnt; r += lv.bm) {
-      TileEntry te;
-      te.widx = widx;
-      te.row0 = off + r;
-      te.nrows = cnt - r < lv.bm ? cnt - r : lv.bm;
-      te.node = n;
-      lv.tiles[tpos++] = te;
+  for (int tab = 0; tab < 2; ++tab) {
+    const int bm = tab == 0 ? lv.bm : lv.bm2;
+    TileEntry* tiles = tab == 0 ? lv.tiles : lv.tiles2;
+    int my_tiles = 0;
+    for (int n = nb; n < ne; ++n) {
+      const bool work = lv.work_all || lv.fac[n] >= 0;
+      const int cnt = lv.offsets[n + 1] - lv.offsets[n];
+      if (work && cnt > 0) my_tiles += (cnt + bm - 1) / bm;
     }
+    int ntiles = 0;
+    int tpos = block_exscan(my_tiles, s_wave, ntiles);
+    for (int n = nb; n < ne; ++n) {
+      const bool work = lv.work_all || lv.fac[n] >= 0;
+      const int off = lv.offsets[n];
+      const int cnt = lv.offsets[n + 1] - off;
+      if (!work || cnt == 0) continue;
+      const int widx = lv.work_all ? n : lv.fac[n];
+      for (int r = 0; r < cnt; r += bm) {
+        TileEntry te;
+        te.widx = widx;
+        te.row0 = off + r;
+        te.nrows = cnt - r < bm ? cnt - r : bm;
+        te.node = n;
+        tiles[tpos++] = te;
+      }
+    }
+    if (tid == 0) *(tab == 0 ? lv.n_tiles : lv.n_tiles2) = ntiles;
   }
-  if (tid == 0) *lv.n_tiles = ntiles;
 }
 
 __global__ __launch_bounds__(64) void k_bucket_place(BucketArgs a) {

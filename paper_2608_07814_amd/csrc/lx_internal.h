@@ -25,6 +25,7 @@ struct TileEntry {
 struct BucketLevel {
   int32_t n_nodes;
   int32_t bm;              // GEMM tile height the tile table is built for
+  int32_t bm2;             // tile height of the second table (large-tile GEMMs)
   int32_t work_all;        // 1: every node does GEMM work (anchor level)
   const int32_t* fac;      // validated factor index per node (-1 none)
   int32_t* hist;           // [n_nodes][n_tok_tiles], scanned in place
@@ -33,6 +34,8 @@ struct BucketLevel {
   int32_t* slot_row;       // [T * k]
   TileEntry* tiles;        // [tiles_max]
   int32_t* n_tiles;        // [1]
+  TileEntry* tiles2;       // [tiles2_max]
+  int32_t* n_tiles2;       // [1]
 };
 
 struct BucketArgs {
@@ -74,7 +77,10 @@ struct GemmArgs {
   const void* B[2];
   int64_t b_stride[2];       // elements between consecutive weight indices
   int32_t ncols[2];          // output columns of each part
-  int32_t K;
+  int32_t K;                 // reduction length of A
+  int32_t Kb;                // row length of W (0: K). When Kb < K the weight
+                             // columns repeat with period Kb: A = [A_hi | A_lo]
+                             // against the same W, i.e. C = (A_hi + A_lo) W^T
   float* C;
   int64_t ldc;
   int32_t c_coloff[2];
@@ -87,6 +93,13 @@ int gemm_bm(lx_dtype dt);
 int gemm_bn(lx_dtype dt);
 hipError_t launch_gemm(const GemmArgs& g, lx_dtype dt, AMode am, int grid_x, hipStream_t s);
 
+// Large-tile kernel (256-row tiles, direct HBM->LDS loads). Applicable when
+// A is bf16, K and Kb are multiples of 64, the two parts share A columns and
+// write adjacent output columns, and A's element count fits in 31 bits.
+int gemm_big_bm();
+bool gemm_big_ok(const GemmArgs& g, int64_t a_rows_total);
+hipError_t launch_gemm_big(const GemmArgs& g, int bn, int grid_tiles, hipStream_t s);
+
 // ---------------------------------------------------------------- elementwise
 struct TokenArgs {
   int32_t T, k, E, L, d, f;
@@ -98,6 +111,9 @@ struct TokenArgs {
   const float* gu0;                    // [rows0][2f] anchor gate|up
   const float* dgu[kMaxLvl];           // [rows_l][2f] correction gate|up (l >= 1)
   float* hbar[kMaxLvl];                // [rows_l][f] weighted activation sums
+                                       // (level 0 of a bf16 layer: [rows][2f] bf16,
+                                       //  hi half then lo half)
+  int32_t hbar0_hilo;
   const float* y[kMaxLvl];             // [rows_l][d] down outputs per level
   void* out;
   lx_dtype out_dtype;
