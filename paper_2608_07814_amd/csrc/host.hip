@@ -120,7 +120,7 @@ Plan make_plan(const lx_tree_layer& t, int T, int k) {
     q.rank = l == 0 ? 0 : t.levels[l - 1].rank;
     q.nfac = l == 0 ? q.N : t.levels[l - 1].n_factors;
     q.bm = gemm_bm(t.dtype);
-    q.bm2 = gemm_big_bm();
+    q.bm2 = kBigBM;
     q.rows_max = (int64_t)T * std::min(k, q.N);
     q.tiles_max = q.rows_max / q.bm + q.N + 1;
     q.tiles2_max = q.rows_max / q.bm2 + q.N + 1;
@@ -313,15 +313,92 @@ lx_status run(const lx_tree_layer& t, int T, int k, const void* x, const int32_t
   if (stop == RUN_BUCKET) return LX_OK;
 
   const lx_dtype dt = t.dtype;
-  const int esz = dt == LX_BF16 ? 2 : 4;
-  (void)esz;
+  const int64_t two31 = (int64_t)1 << 31;
 
+  // "Fast" levels keep every GEMM-feeding intermediate as a bf16 (hi, lo)
+  // pair and run all their GEMMs on the large-tile kernel; other levels use
+  // fp32 intermediates and the register-staged kernel (hi/lo split on load).
+  bool fast[kMaxLvl] = {};
+  fast[0] = dt == LX_BF16 && d % 64 == 0 && f % 64 == 0 && (int64_t)T * d < two31 &&
+            P.lv[0].rows_max * 2 * f < two31;
+  for (int l = 1; l <= L; ++l) {
+    const int r = t.levels[l - 1].rank;
+    const int64_t R = P.lv[l].rows_max;
+    // rank multiple of 64: every 64-wide K-slab of a (hi | lo) operand lies
+    // inside one half, so its weight columns stay inside the weight row
+    fast[l] = fast[0] && r % 64 == 0 && R * 2 * f < two31 && R * 4 * r < two31;
+  }
+  auto big = [&](const char* name, GemmArgs g, int l, int bm, int bn, bool hilo,
+                 int64_t a_rows_total) -> lx_status {
+    const LevelPlan& q = P.lv[l];
+    if (!gemm_big_ok(g, bn, a_rows_total))
+      return fail(LX_ERR_UNSUPPORTED, std::string(name) + ": shape not supported by the large-tile GEMM");
+    g.tiles = bm == kBigBM ? ba.lv[l].tiles2 : ba.lv[l].tiles;
+    g.n_tiles = bm == kBigBM ? ba.lv[l].n_tiles2 : ba.lv[l].n_tiles;
+    if (!g.B[1]) g.B[1] = g.B[0];
+    LX_LAUNCH(name, launch_gemm_big(g, bm, bn, hilo, (int)(bm == kBigBM ? q.tiles2_max : q.tiles_max), stream));
+    return LX_OK;
+  };
+  auto small = [&](const char* name, GemmArgs g, int l, AMode am) -> lx_status {
+    g.tiles = ba.lv[l].tiles;
+    g.n_tiles = ba.lv[l].n_tiles;
+    LX_LAUNCH(name, launch_gemm(g, dt, am, (int)P.lv[l].tiles_max, stream));
+    return LX_OK;
+  };
+#define LX_TRY(X)                  \
+  do {                             \
+    const lx_status s_ = (X);      \
+    if (s_ != LX_OK) return s_;    \
+  } while (0)
+
+  // correction gate|up per level: z = B x (once per (token, node)), dgu = A z
+  for (int l = 1; l <= L; ++l) {
+    const LevelPlan& q = P.lv[l];
+    const lx_level& v = t.levels[l - 1];
+    if (v.n_factors == 0) continue;
+    const int r = v.rank;
+    GemmArgs g{};
+    g.A = x;
+    g.lda = d;
+    g.a_rows = ba.lv[l].row_token;
+    g.B[0] = v.b_gate;
+    g.B[1] = v.b_up;
+    g.b_stride[0] = g.b_stride[1] = (int64_t)r * d;
+    g.ncols[0] = g.ncols[1] = r;
+    g.K = d;
+    g.C = (float*)(W + q.z);
+    GemmArgs h{};
+    h.B[0] = v.a_gate;
+    h.B[1] = v.a_up;
+    h.b_stride[0] = h.b_stride[1] = (int64_t)f * r;
+    h.ncols[0] = h.ncols[1] = f;
+    h.A = W + q.z;
+    h.C = (float*)(W + q.gu);
+    h.ldc = 2 * (int64_t)f;
+    h.c_coloff[1] = f;
+    if (fast[l]) {
+      g.ldc = 4 * (int64_t)r;  // [gate hi | gate lo | up hi | up lo], bf16
+      LX_TRY(big(kLowIn[l], g, l, 128, 2 * r <= 128 ? 128 : 256, true, T));
+      h.lda = 4 * (int64_t)r;
+      h.a_koff[1] = 2 * r;
+      h.K = 2 * r;
+      h.Kb = r;
+      // gate and up read different z columns: tiles must not straddle them
+      LX_TRY(big(kLowOut[l], h, l, kBigBM, f % 256 == 0 ? 256 : f % 128 == 0 ? 128 : 64, false, q.rows_max));
+    } else {
+      g.ldc = 2 * (int64_t)r;
+      g.c_coloff[1] = r;
+      LX_TRY(small(kLowIn[l], g, l, A_BF16));
+      h.lda = 2 * (int64_t)r;
+      h.a_koff[1] = r;
+      h.K = r;
+      LX_TRY(small(kLowOut[l], h, l, A_F32_HILO));
+    }
+  }
   // anchor gate|up, once per (token, anchor)
   {
     const LevelPlan& q = P.lv[0];
     GemmArgs g{};
-    g.tiles = ba.lv[0].tiles;
-    g.n_tiles = ba.lv[0].n_tiles;
     g.A = x;
     g.lda = d;
     g.a_rows = ba.lv[0].row_token;
@@ -333,50 +410,10 @@ lx_status run(const lx_tree_layer& t, int T, int k, const void* x, const int32_t
     g.C = (float*)(W + q.gu);
     g.ldc = 2 * (int64_t)f;
     g.c_coloff[1] = f;
-    if (dt == LX_BF16 && gemm_big_ok(g, T)) {
-      g.tiles = ba.lv[0].tiles2;
-      g.n_tiles = ba.lv[0].n_tiles2;
-      LX_LAUNCH("anchor_gate_up", launch_gemm_big(g, 256, (int)q.tiles2_max, stream));
-    } else {
-      LX_LAUNCH("anchor_gate_up", launch_gemm(g, dt, A_BF16, (int)q.tiles_max, stream));
-    }
-  }
-  // correction gate|up per level: z = B x, then A z
-  for (int l = 1; l <= L; ++l) {
-    const LevelPlan& q = P.lv[l];
-    const lx_level& v = t.levels[l - 1];
-    if (v.n_factors == 0) continue;
-    const int r = v.rank;
-    GemmArgs g{};
-    g.tiles = ba.lv[l].tiles;
-    g.n_tiles = ba.lv[l].n_tiles;
-    g.A = x;
-    g.lda = d;
-    g.a_rows = ba.lv[l].row_token;
-    g.B[0] = v.b_gate;
-    g.B[1] = v.b_up;
-    g.b_stride[0] = g.b_stride[1] = (int64_t)r * d;
-    g.ncols[0] = g.ncols[1] = r;
-    g.K = d;
-    g.C = (float*)(W + q.z);
-    g.ldc = 2 * (int64_t)r;
-    g.c_coloff[1] = r;
-    LX_LAUNCH(kLowIn[l], launch_gemm(g, dt, A_BF16, (int)q.tiles_max, stream));
-    GemmArgs h{};
-    h.tiles = g.tiles;
-    h.n_tiles = g.n_tiles;
-    h.A = W + q.z;
-    h.lda = 2 * (int64_t)r;
-    h.a_koff[1] = r;
-    h.B[0] = v.a_gate;
-    h.B[1] = v.a_up;
-    h.b_stride[0] = h.b_stride[1] = (int64_t)f * r;
-    h.ncols[0] = h.ncols[1] = f;
-    h.K = r;
-    h.C = (float*)(W + q.gu);
-    h.ldc = 2 * (int64_t)f;
-    h.c_coloff[1] = f;
-    LX_LAUNCH(kLowOut[l], launch_gemm(h, dt, A_F32_HILO, (int)q.tiles_max, stream));
+    if (fast[0])
+      LX_TRY(big("anchor_gate_up", g, 0, kBigBM, 256, false, T));
+    else
+      LX_TRY(small("anchor_gate_up", g, 0, A_BF16));
   }
 
   TokenArgs ta{};
@@ -396,79 +433,74 @@ lx_status run(const lx_tree_layer& t, int T, int k, const void* x, const int32_t
     ta.fac[l] = l > 0 ? (const int32_t*)(W + q.fac) : nullptr;
     ta.dgu[l] = (const float*)(W + q.gu);
     ta.hbar[l] = (float*)(W + q.hbar);
+    ta.hbar_hilo[l] = fast[l] ? 1 : 0;
     ta.y[l] = (const float*)(W + q.y);
   }
   ta.out = out;
   ta.out_dtype = out_dtype;
-  // bf16 layers keep the anchor-level activation sums as a bf16 (hi, lo) pair
-  // so the down projection runs on the large-tile bf16 kernel
-  GemmArgs gdown{};
-  {
-    const LevelPlan& q = P.lv[0];
-    gdown.tiles = ba.lv[0].tiles2;
-    gdown.n_tiles = ba.lv[0].n_tiles2;
-    gdown.A = W + q.hbar;
-    gdown.lda = 2 * (int64_t)f;
-    gdown.B[0] = gdown.B[1] = t.anchor_down;
-    gdown.b_stride[0] = gdown.b_stride[1] = (int64_t)d * f;
-    gdown.ncols[0] = d;
-    gdown.K = 2 * f;
-    gdown.Kb = f;
-    gdown.C = (float*)(W + q.y);
-    gdown.ldc = d;
-  }
-  const bool down_big = dt == LX_BF16 && gemm_big_ok(gdown, P.lv[0].rows_max);
-  ta.hbar0_hilo = down_big ? 1 : 0;
   LX_LAUNCH("swiglu_reduce", launch_swiglu_reduce(ta, stream));
 
   // anchor down, once per (token, anchor), on the weighted activation sums
-  if (down_big) {
-    LX_LAUNCH("anchor_down", launch_gemm_big(gdown, 256, (int)P.lv[0].tiles2_max, stream));
-  } else {
+  {
     const LevelPlan& q = P.lv[0];
     GemmArgs g{};
-    g.tiles = ba.lv[0].tiles;
-    g.n_tiles = ba.lv[0].n_tiles;
     g.A = W + q.hbar;
-    g.lda = f;
     g.B[0] = t.anchor_down;
     g.b_stride[0] = (int64_t)d * f;
     g.ncols[0] = d;
-    g.K = f;
     g.C = (float*)(W + q.y);
     g.ldc = d;
-    LX_LAUNCH("anchor_down", launch_gemm(g, dt, A_F32_HILO, (int)q.tiles_max, stream));
+    if (fast[0]) {
+      g.lda = 2 * (int64_t)f;
+      g.K = 2 * f;
+      g.Kb = f;
+      LX_TRY(big("anchor_down", g, 0, kBigBM, 256, false, q.rows_max));
+    } else {
+      g.lda = f;
+      g.K = f;
+      LX_TRY(small("anchor_down", g, 0, A_F32_HILO));
+    }
   }
+  // correction down per level: v = B_down hbar, y = A_down v
   for (int l = 1; l <= L; ++l) {
     const LevelPlan& q = P.lv[l];
     const lx_level& v = t.levels[l - 1];
     if (v.n_factors == 0) continue;
     const int r = v.rank;
     GemmArgs g{};
-    g.tiles = ba.lv[l].tiles;
-    g.n_tiles = ba.lv[l].n_tiles;
     g.A = W + q.hbar;
-    g.lda = f;
     g.B[0] = v.b_down;
     g.b_stride[0] = (int64_t)r * f;
     g.ncols[0] = r;
-    g.K = f;
     g.C = (float*)(W + q.v);
-    g.ldc = r;
-    LX_LAUNCH(kDownIn[l], launch_gemm(g, dt, A_F32_HILO, (int)q.tiles_max, stream));
     GemmArgs h{};
-    h.tiles = g.tiles;
-    h.n_tiles = g.n_tiles;
     h.A = W + q.v;
-    h.lda = r;
     h.B[0] = v.a_down;
     h.b_stride[0] = (int64_t)d * r;
     h.ncols[0] = d;
-    h.K = r;
     h.C = (float*)(W + q.y);
     h.ldc = d;
-    LX_LAUNCH(kDownOut[l], launch_gemm(h, dt, A_F32_HILO, (int)q.tiles_max, stream));
+    if (fast[l]) {
+      g.lda = 2 * (int64_t)f;
+      g.K = 2 * f;
+      g.Kb = f;
+      g.ldc = 2 * (int64_t)r;  // [hi | lo], bf16
+      LX_TRY(big(kDownIn[l], g, l, 128, r <= 64 ? 64 : 128, true, q.rows_max));
+      h.lda = 2 * (int64_t)r;
+      h.K = 2 * r;
+      h.Kb = r;
+      LX_TRY(big(kDownOut[l], h, l, kBigBM, 256, false, q.rows_max));
+    } else {
+      g.lda = f;
+      g.K = f;
+      g.ldc = r;
+      LX_TRY(small(kDownIn[l], g, l, A_F32_HILO));
+      h.lda = r;
+      h.K = r;
+      LX_TRY(small(kDownOut[l], h, l, A_F32_HILO));
+    }
   }
+#undef LX_TRY
   LX_LAUNCH("combine", launch_combine(ta, stream));
   return LX_OK;
 }

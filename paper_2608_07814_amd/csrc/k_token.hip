@@ -75,12 +75,12 @@ __global__ __launch_bounds__(256) void k_swiglu_reduce(TokenArgs a) {
       const float h = m.w[j] * (g / (1.f + expf(-g))) * u;
       for (int l = 0; l <= L; ++l) {
         if (!m.work[l][j]) continue;
-        if (l == 0 && a.hbar0_hilo) {
+        if (a.hbar_hilo[l]) {
           // bf16 pair: hi at column i, lo = bf16(sum - hi) at column f + i.
           // The running sum is rebuilt as hi + lo, which is exact to ~2^-17.
-          __bf16* hb = (__bf16*)a.hbar[0] + (int64_t)m.row[0][j] * ld;
+          __bf16* hb = (__bf16*)a.hbar[l] + (int64_t)m.row[l][j] * ld;
           float sum = h;
-          if (!m.first[0][j]) sum += (float)hb[i] + (float)hb[f + i];
+          if (!m.first[l][j]) sum += (float)hb[i] + (float)hb[f + i];
           const __bf16 hi = (__bf16)sum;
           hb[i] = hi;
           hb[f + i] = (__bf16)(sum - (float)hi);

@@ -93,12 +93,17 @@ int gemm_bm(lx_dtype dt);
 int gemm_bn(lx_dtype dt);
 hipError_t launch_gemm(const GemmArgs& g, lx_dtype dt, AMode am, int grid_x, hipStream_t s);
 
-// Large-tile kernel (256-row tiles, direct HBM->LDS loads). Applicable when
-// A is bf16, K and Kb are multiples of 64, the two parts share A columns and
-// write adjacent output columns, and A's element count fits in 31 bits.
-int gemm_big_bm();
-bool gemm_big_ok(const GemmArgs& g, int64_t a_rows_total);
-hipError_t launch_gemm_big(const GemmArgs& g, int bn, int grid_tiles, hipStream_t s);
+// Large-tile kernel (BM x BN tiles, direct HBM->LDS loads). Applicable when A
+// is bf16, K and Kb are multiples of 64, the parts either share A columns or
+// the part boundary is a multiple of BN, and A's element count fits in 31
+// bits. fp32 output is written at columns [0, ncols[0] + ncols[1]) of C (the
+// parts adjacent); bf16 (hi, lo) output writes part p's hi values at columns
+// base_p + c and lo values at base_p + ncols[p] + c, base_0 = 0,
+// base_1 = 2 ncols[0] (ldc in bf16 elements).
+constexpr int kBigBM = 256;
+bool gemm_big_ok(const GemmArgs& g, int bn, int64_t a_rows_total);
+hipError_t launch_gemm_big(const GemmArgs& g, int bm, int bn, bool out_hilo, int grid_tiles,
+                           hipStream_t s);
 
 // ---------------------------------------------------------------- elementwise
 struct TokenArgs {
@@ -110,10 +115,10 @@ struct TokenArgs {
   const int32_t* slot_row[kMaxLvl];
   const float* gu0;                    // [rows0][2f] anchor gate|up
   const float* dgu[kMaxLvl];           // [rows_l][2f] correction gate|up (l >= 1)
-  float* hbar[kMaxLvl];                // [rows_l][f] weighted activation sums
-                                       // (level 0 of a bf16 layer: [rows][2f] bf16,
-                                       //  hi half then lo half)
-  int32_t hbar0_hilo;
+  float* hbar[kMaxLvl];                // [rows_l][f] fp32 weighted activation sums, or
+                                       // [rows_l][2f] bf16 (hi half, lo half) when
+                                       // hbar_hilo[l]
+  int32_t hbar_hilo[kMaxLvl];
   const float* y[kMaxLvl];             // [rows_l][d] down outputs per level
   void* out;
   lx_dtype out_dtype;

@@ -13,6 +13,11 @@ from paper_2608_07814_amd import lorex as lx
 TOL_BF16 = 1e-2
 # fp32 end to end: a tighter self-check that catches logic slips
 TOL_F32 = 1e-4
+# The library's precision policy (bf16 hi+lo pairs for every fp32
+# intermediate that feeds a GEMM) lands near 2e-5 * RMS; this looser design
+# bound catches a lost lo half or a mis-indexed K-slab well before the
+# acceptance bar would.
+TOL_DESIGN = 1e-3
 
 
 def require_gpu():

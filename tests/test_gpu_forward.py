@@ -12,7 +12,7 @@ import torch
 from lxsynth import make_problem, make_layer_flat
 from oracle import moe as O
 from paper_2608_07814_amd import lorex as lx
-from gpu_util import (TOL_BF16, TOL_F32, require_gpu, say, gpu_forward, err_ratio, sample_tokens,
+from gpu_util import (TOL_BF16, TOL_F32, TOL_DESIGN, require_gpu, say, gpu_forward, err_ratio, sample_tokens,
                       dev_inputs)
 from helpers import tiny_flat, tiny_tree, random_routing, zero_level
 
@@ -43,6 +43,7 @@ def test_cfg1_shapes_full_compare(seed):
     e = err_ratio(got, _oracle(p))
     say(f"  err/RMS = {e:.3e}")
     assert e <= TOL_BF16
+    assert e <= TOL_DESIGN
 
 
 def test_cfg1_full_size_sampled():
@@ -55,6 +56,7 @@ def test_cfg1_full_size_sampled():
     e = err_ratio(got[tok], _oracle(p, tok))
     say(f"  err/RMS = {e:.3e}")
     assert e <= TOL_BF16
+    assert e <= TOL_DESIGN
     assert np.all(np.isfinite(got))
 
 
@@ -66,6 +68,7 @@ def test_cfg2_decode_full():
     e = err_ratio(got, _oracle(p))
     say(f"  err/RMS = {e:.3e}")
     assert e <= TOL_BF16
+    assert e <= TOL_DESIGN
 
 
 def test_cfg3_community():
@@ -76,6 +79,7 @@ def test_cfg3_community():
     e = err_ratio(got, _oracle(p))
     say(f"  err/RMS = {e:.3e}")
     assert e <= TOL_BF16
+    assert e <= TOL_DESIGN
 
 
 def test_cfg3_full_size_sampled():
@@ -87,6 +91,7 @@ def test_cfg3_full_size_sampled():
     e = err_ratio(got[tok], _oracle(p, tok))
     say(f"  err/RMS = {e:.3e}")
     assert e <= TOL_BF16
+    assert e <= TOL_DESIGN
 
 
 def test_cfg4_tree_small():
@@ -97,6 +102,7 @@ def test_cfg4_tree_small():
     e = err_ratio(got, _oracle(p))
     say(f"  err/RMS = {e:.3e}")
     assert e <= TOL_BF16
+    assert e <= TOL_DESIGN
 
 
 def test_cfg4_tree_full_size_sampled():
@@ -108,6 +114,7 @@ def test_cfg4_tree_full_size_sampled():
     e = err_ratio(got[tok], _oracle(p, tok))
     say(f"  err/RMS = {e:.3e}")
     assert e <= TOL_BF16
+    assert e <= TOL_DESIGN
 
 
 # ------------------------------------------------------------ edge cases
