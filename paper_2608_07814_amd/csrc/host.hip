@@ -84,14 +84,14 @@ size_t align_up(size_t x) { return (x + 255) & ~size_t(255); }
 struct LevelPlan {
   int N = 0, rank = 0, nfac = 0, bm = 0, bm2 = 0;
   int64_t rows_max = 0, tiles_max = 0, tiles2_max = 0;
-  size_t hist, offsets, row_token, slot_row, tiles, n_tiles, tiles2, n_tiles2, fac;
+  size_t hist, offsets, row_token, slot_row, slot_flags, tiles, n_tiles, tiles2, n_tiles2, fac;
   size_t gu, z, hbar, v, y;
 };
 
 struct Plan {
   int T, k, E, L, d, f, NT;
   LevelPlan lv[kMaxLvl];
-  size_t flags, anc, total;
+  size_t flags, anc, slot_wsum, total;
 };
 
 int level_nodes(const lx_tree_layer& t, int l) { return l == 0 ? t.n_anchors : t.levels[l - 1].n_nodes; }
@@ -114,6 +114,7 @@ Plan make_plan(const lx_tree_layer& t, int T, int k) {
   p.flags = take(16);  // first: lx_read_device_status reads offset 0
   p.anc = take((size_t)(p.L + 1) * p.E * 4);
   const size_t tk = (size_t)T * k;
+  p.slot_wsum = take(tk * 4);
   for (int l = 0; l <= p.L; ++l) {
     LevelPlan& q = p.lv[l];
     q.N = level_nodes(t, l);
@@ -128,6 +129,7 @@ Plan make_plan(const lx_tree_layer& t, int T, int k) {
     q.offsets = take((size_t)(q.N + 1) * 4);
     q.row_token = take((size_t)q.rows_max * 4);
     q.slot_row = take(tk * 4);
+    q.slot_flags = take(tk);
     q.tiles = take((size_t)q.tiles_max * sizeof(TileEntry));
     q.n_tiles = take(4);
     q.tiles2 = take((size_t)q.tiles2_max * sizeof(TileEntry));
@@ -288,6 +290,8 @@ lx_status run(const lx_tree_layer& t, int T, int k, const void* x, const int32_t
   ba.L = L;
   ba.n_tok_tiles = P.NT;
   ba.ids = ids;
+  ba.w = w;
+  ba.slot_wsum = (float*)(W + P.slot_wsum);
   ba.anc = pa.anc;
   ba.flags = pa.flags;
   for (int l = 0; l <= L; ++l) {
@@ -302,6 +306,7 @@ lx_status run(const lx_tree_layer& t, int T, int k, const void* x, const int32_t
     b.offsets = (int32_t*)(W + q.offsets);
     b.row_token = (int32_t*)(W + q.row_token);
     b.slot_row = (int32_t*)(W + q.slot_row);
+    b.slot_flags = (uint8_t*)(W + q.slot_flags);
     b.tiles = (TileEntry*)(W + q.tiles);
     b.n_tiles = (int32_t*)(W + q.n_tiles);
     b.tiles2 = (TileEntry*)(W + q.tiles2);
@@ -423,14 +428,12 @@ lx_status run(const lx_tree_layer& t, int T, int k, const void* x, const int32_t
   ta.L = L;
   ta.d = d;
   ta.f = f;
-  ta.ids = ids;
-  ta.w = w;
-  ta.anc = pa.anc;
+  ta.slot_wsum = ba.slot_wsum;
   ta.gu0 = (const float*)(W + P.lv[0].gu);
   for (int l = 0; l <= L; ++l) {
     const LevelPlan& q = P.lv[l];
     ta.slot_row[l] = ba.lv[l].slot_row;
-    ta.fac[l] = l > 0 ? (const int32_t*)(W + q.fac) : nullptr;
+    ta.slot_flags[l] = ba.lv[l].slot_flags;
     ta.dgu[l] = (const float*)(W + q.gu);
     ta.hbar[l] = (float*)(W + q.hbar);
     ta.hbar_hilo[l] = fast[l] ? 1 : 0;

@@ -201,12 +201,14 @@ __global__ __launch_bounds__(64) void k_bucket_place(BucketArgs a) {
   const int t = tt * kTokTile + lane;
   if (t >= a.T) return;
   const unsigned long long below = (1ull << lane) - 1ull;
+  const int64_t base = (int64_t)t * a.k;
   for (int j = 0; j < a.k; ++j) {
-    const int64_t s = (int64_t)t * a.k + j;
+    const int64_t s = base + j;
     const int n = node_of(a, l, a.ids[s]);
     s_node[lane][j] = n;
     if (n < 0) {
       lv.slot_row[s] = -1;
+      lv.slot_flags[s] = 0;
       continue;
     }
     const int row = lv.hist[(int64_t)n * a.n_tok_tiles + tt] + __popcll(s_mask[n] & below);
@@ -214,6 +216,21 @@ __global__ __launch_bounds__(64) void k_bucket_place(BucketArgs a) {
     bool first = true;
     for (int j2 = 0; j2 < j; ++j2) first &= (s_node[lane][j2] != n);
     if (first) lv.row_token[row] = t;
+    const bool work = lv.work_all || lv.fac[n] >= 0;
+    lv.slot_flags[s] = (uint8_t)((first ? 1 : 0) | (work ? 2 : 0));
+  }
+  // expert level: summed weight of each distinct expert, on its first slot
+  if (l == a.L && a.w) {
+    for (int j = 0; j < a.k; ++j) {
+      const int n = s_node[lane][j];
+      bool first = n >= 0;
+      for (int j2 = 0; j2 < j; ++j2) first &= (s_node[lane][j2] != n);
+      float ws = 0.f;
+      if (first)
+        for (int j2 = j; j2 < a.k; ++j2)
+          if (s_node[lane][j2] == n) ws += a.w[base + j2];
+      a.slot_wsum[base + j] = ws;
+    }
   }
 }
 

@@ -32,6 +32,8 @@ struct BucketLevel {
   int32_t* offsets;        // [n_nodes + 1]
   int32_t* row_token;      // [rows_max]
   int32_t* slot_row;       // [T * k]
+  uint8_t* slot_flags;     // [T * k] bit0: first slot of its row, bit1: the row's
+                           // node does work at this level (always at level 0)
   TileEntry* tiles;        // [tiles_max]
   int32_t* n_tiles;        // [1]
   TileEntry* tiles2;       // [tiles2_max]
@@ -42,6 +44,9 @@ struct BucketArgs {
   int32_t T, k, E, L;      // L = number of correction levels
   int32_t n_tok_tiles;
   const int32_t* ids;      // [T * k]
+  const float* w;          // [T * k] routing weights, or null (bucketing only)
+  float* slot_wsum;        // [T * k] at the expert level: a distinct expert's first
+                           // slot holds the sum of its slots' weights, others 0
   const int32_t* anc;      // [(L + 1) * E] ancestor per level, -1 = invalid expert
   uint32_t* flags;
   BucketLevel lv[kMaxLvl];
@@ -108,11 +113,9 @@ hipError_t launch_gemm_big(const GemmArgs& g, int bm, int bn, bool out_hilo, int
 // ---------------------------------------------------------------- elementwise
 struct TokenArgs {
   int32_t T, k, E, L, d, f;
-  const int32_t* ids;
-  const float* w;
-  const int32_t* anc;                  // [(L + 1) * E]
-  const int32_t* fac[kMaxLvl];         // validated factor index per node (l >= 1)
   const int32_t* slot_row[kMaxLvl];
+  const uint8_t* slot_flags[kMaxLvl];
+  const float* slot_wsum;
   const float* gu0;                    // [rows0][2f] anchor gate|up
   const float* dgu[kMaxLvl];           // [rows_l][2f] correction gate|up (l >= 1)
   float* hbar[kMaxLvl];                // [rows_l][f] fp32 weighted activation sums, or
