@@ -22,16 +22,25 @@
 //     an fp32 intermediate at bf16 MFMA rate;
 //   * output either fp32, or a bf16 (hi, lo) pair ready to feed the next GEMM
 //     as its two K-halves;
+//   * persistent: the grid is at most one workgroup per compute unit and each
+//     workgroup loops over (tile, n-tile) work items, so the epilogue of one
+//     item and the prologue loads of the next are not separated by a
+//     workgroup launch;
 //   * XCD-aware order: workgroups are dispatched round-robin over the 8 XCDs;
-//     the kernel renumbers them so each XCD receives a contiguous range of
-//     (tile, n-tile) work, i.e. neighbours that share A rows and weight slabs
-//     share one L2.
+//     each XCD's workgroups take a contiguous range of work items, i.e.
+//     neighbours that share A rows and weight slabs share one L2;
+//   * epilogue through LDS: each wavefront transposes its accumulator block
+//     so that every lane stores 4 consecutive columns of one row (16-byte
+//     fp32 or 8-byte bf16 stores).
 #include "lx_internal.h"
+
+#include <mutex>
 
 namespace lx {
 namespace {
 
 typedef __bf16 bf16x8 __attribute__((ext_vector_type(8)));
+typedef __bf16 bf16x4 __attribute__((ext_vector_type(4)));
 typedef float f32x16 __attribute__((ext_vector_type(16)));
 typedef uint16_t u16;
 typedef __attribute__((address_space(3))) void lds_void_t;
@@ -46,10 +55,11 @@ __device__ __forceinline__ int lds_off2(int row, int kc) { return row * BK2 + ((
 // load is issued through inline asm so that the only waits on it are the
 // explicit per-stage vmcnt waits below (the compiler's own tracking of LDS
 // DMA would otherwise serialize consecutive loads). M0 is written here only;
-// nothing else in these kernels uses it.
+// nothing else in these kernels uses it. The s_nop is the one wait state the
+// GFX9 family requires between an SALU write of M0 and an LDS-DMA load.
 __device__ __forceinline__ void load_lds16(const void* gptr, const void* lds_dst) {
   const uint32_t lds = (uint32_t)(uintptr_t)(lds_void_t*)lds_dst;
-  asm volatile("s_mov_b32 m0, %1\n\tglobal_load_lds_dwordx4 %0, off"
+  asm volatile("s_mov_b32 m0, %1\n\ts_nop 0\n\tglobal_load_lds_dwordx4 %0, off"
                :
                : "v"(gptr), "s"(__builtin_amdgcn_readfirstlane(lds))
                : "memory");
@@ -81,92 +91,101 @@ void k_gemm_big(GemmArgs p, int ntn) {
   constexpr int A_ROUNDS = BM * 8 / NTHR2;  // 16-byte chunks per thread per slab
   constexpr int B_ROUNDS = BN * 8 / NTHR2;
   constexpr int ROUNDS = A_ROUNDS + B_ROUNDS;
+  // LDS: stage 0 = [A | B], stage 1 = [A | B]; the epilogue reuses it.
+  constexpr int SA = BM * BK2, SB = BN * BK2;
+  __shared__ __attribute__((aligned(1024))) u16 smem[2 * (SA + SB)];
+  u16* const sA0 = smem;
+  u16* const sB0 = smem + SA;
+  u16* const sA1 = smem + SA + SB;
+  u16* const sB1 = smem + 2 * SA + SB;
 
-  // ---- which (tile, n-tile) this workgroup computes (XCD-contiguous order)
+  // Work items (tile, n-tile) [0, real): XCD x owns the contiguous range
+  // [xbeg, xend); its mx workgroups take every mx-th item of it. The host
+  // launches either one workgroup per item or a multiple of 8 workgroups, so
+  // every XCD with items has at least one workgroup.
   const int real = *p.n_tiles * ntn;
-  const int P = blockIdx.x;
-  if (P >= real) return;
   const int q = real / NXCD, rmd = real % NXCD;
-  const int x = P % NXCD, idx = P / NXCD;
-  const int Lg = x * q + (x < rmd ? x : rmd) + idx;
-  const int ti = Lg / ntn, nt = Lg % ntn;
-
-  // The two weight parts form one column range [0, ncol): column n < ncols[0]
-  // is row n of part 0, otherwise row n - ncols[0] of part 1.
-  const TileEntry te = p.tiles[ti];
-  const int n0 = nt * BN;
+  const int x = blockIdx.x % NXCD;
+  const int xbeg = x * q + (x < rmd ? x : rmd);
+  const int xend = xbeg + q + (x < rmd ? 1 : 0);
+  const int mx = ((int)gridDim.x - x + NXCD - 1) / NXCD;
   const int ncol = p.ncols[0] + p.ncols[1];
   const int K = p.K;
   const int Kb = p.Kb > 0 ? p.Kb : K;
-  const int tpart = n0 < p.ncols[0] ? 0 : 1;
-  const int akoff = p.a_koff[tpart];
-  const u16* __restrict__ Bw0 = (const u16*)p.B[0] + (int64_t)te.widx * p.b_stride[0];
-  const u16* __restrict__ Bw1 = (const u16*)p.B[1] + (int64_t)te.widx * p.b_stride[1];
+  const int nk = K / BK2;
   const u16* __restrict__ Ab = (const u16*)p.A;
 
-  __shared__ __attribute__((aligned(1024))) u16 sA0[BM * BK2];
-  __shared__ __attribute__((aligned(1024))) u16 sA1[BM * BK2];
-  __shared__ __attribute__((aligned(1024))) u16 sB0[BN * BK2];
-  __shared__ __attribute__((aligned(1024))) u16 sB1[BN * BK2];
+  for (int Lg = xbeg + (int)blockIdx.x / NXCD; Lg < xend; Lg += mx) {
+    // The empty asm makes the lane index opaque per item, so the per-lane
+    // address arithmetic below is recomputed each item instead of being
+    // hoisted out of the item loop (where it would not fit in registers).
+    int tid = threadIdx.x;
+    asm volatile("" : "+v"(tid));
+    const int wave = tid >> 6, lane = tid & 63;
+    const int wm = wave >> 1, wn = wave & 1;
+    const int ti = Lg / ntn, nt = Lg % ntn;
 
-  const int tid = threadIdx.x;
-  const int wave = tid >> 6, lane = tid & 63;
+    // The two weight parts form one column range [0, ncol): column n < ncols[0]
+    // is row n of part 0, otherwise row n - ncols[0] of part 1.
+    const TileEntry te = p.tiles[ti];
+    const int n0 = nt * BN;
+    const int tpart = n0 < p.ncols[0] ? 0 : 1;
+    const int akoff = p.a_koff[tpart];
+    const u16* __restrict__ Bw0 = (const u16*)p.B[0] + (int64_t)te.widx * p.b_stride[0];
+    const u16* __restrict__ Bw1 = (const u16*)p.B[1] + (int64_t)te.widx * p.b_stride[1];
 
-  // Per-thread source offsets (elements, chunk offset folded in) for each
-  // 16-byte chunk it loads. LDS slot P = round*256 + tid holds row P>>3,
-  // physical chunk P&7, i.e. logical chunk (P&7) ^ swz(row). 32-bit A
-  // offsets: the host routes A operands with 2^31 or more elements elsewhere.
-  uint32_t aoff[A_ROUNDS];
+    // Per-thread source offsets (elements, chunk offset folded in) for each
+    // 16-byte chunk it loads. LDS slot P = round*256 + tid holds row P>>3,
+    // physical chunk P&7, i.e. logical chunk (P&7) ^ swz(row). 32-bit A
+    // offsets: the host routes A operands with 2^31 or more elements elsewhere.
+    uint32_t aoff[A_ROUNDS];
 #pragma unroll
-  for (int j = 0; j < A_ROUNDS; ++j) {
-    const int Ps = j * NTHR2 + tid;
-    const int row = Ps >> 3;
-    const int c = (Ps & 7) ^ swz2(row);
-    const int r = row < te.nrows ? row : te.nrows - 1;
-    const int src = p.a_rows ? p.a_rows[te.row0 + r] : te.row0 + r;
-    aoff[j] = (uint32_t)src * (uint32_t)p.lda + (uint32_t)(akoff + c * 8);
-  }
-  const u16* bptr[B_ROUNDS];
+    for (int j = 0; j < A_ROUNDS; ++j) {
+      const int Ps = j * NTHR2 + tid;
+      const int row = Ps >> 3;
+      const int c = (Ps & 7) ^ swz2(row);
+      const int r = row < te.nrows ? row : te.nrows - 1;
+      const int src = p.a_rows ? p.a_rows[te.row0 + r] : te.row0 + r;
+      aoff[j] = (uint32_t)src * (uint32_t)p.lda + (uint32_t)(akoff + c * 8);
+    }
+    const u16* bptr[B_ROUNDS];
 #pragma unroll
-  for (int j = 0; j < B_ROUNDS; ++j) {
-    const int Ps = j * NTHR2 + tid;
-    const int row = Ps >> 3;
-    const int c = (Ps & 7) ^ swz2(row);
-    const int n = n0 + row < ncol ? n0 + row : ncol - 1;
-    bptr[j] = (n < p.ncols[0] ? Bw0 + (int64_t)n * Kb : Bw1 + (int64_t)(n - p.ncols[0]) * Kb) + c * 8;
-  }
+    for (int j = 0; j < B_ROUNDS; ++j) {
+      const int Ps = j * NTHR2 + tid;
+      const int row = Ps >> 3;
+      const int c = (Ps & 7) ^ swz2(row);
+      const int n = n0 + row < ncol ? n0 + row : ncol - 1;
+      bptr[j] = (n < p.ncols[0] ? Bw0 + (int64_t)n * Kb : Bw1 + (int64_t)(n - p.ncols[0]) * Kb) + c * 8;
+    }
 
-#define LX_ISSUE(SA, SB, K0)                                                        \
+#define LX_ISSUE(SA_, SB_, K0)                                                      \
   do {                                                                              \
     const int kb_ = (K0) % Kb;                                                      \
     _Pragma("unroll") for (int j = 0; j < A_ROUNDS; ++j)                            \
-        load_lds16(Ab + (aoff[j] + (uint32_t)(K0)), &SA[(j * NTHR2 + wave * 64) * 8]); \
+        load_lds16(Ab + (aoff[j] + (uint32_t)(K0)), &SA_[(j * NTHR2 + wave * 64) * 8]); \
     _Pragma("unroll") for (int j = 0; j < B_ROUNDS; ++j)                            \
-        load_lds16(bptr[j] + kb_, &SB[(j * NTHR2 + wave * 64) * 8]);                \
+        load_lds16(bptr[j] + kb_, &SB_[(j * NTHR2 + wave * 64) * 8]);               \
   } while (0)
 
-  f32x16 acc[MI][NI];
+    f32x16 acc[MI][NI];
 #pragma unroll
-  for (int mi = 0; mi < MI; ++mi)
+    for (int mi = 0; mi < MI; ++mi)
 #pragma unroll
-    for (int ni = 0; ni < NI; ++ni)
+      for (int ni = 0; ni < NI; ++ni)
 #pragma unroll
-      for (int i = 0; i < 16; ++i) acc[mi][ni][i] = 0.f;
+        for (int i = 0; i < 16; ++i) acc[mi][ni][i] = 0.f;
 
-  const int wm = wave >> 1, wn = wave & 1;
-  const int nk = K / BK2;
-
-  // One K-slab of MFMAs from stage (SA, SB), fragments double-buffered in
-  // registers: the LDS reads of k-step s+1 are issued before the MFMAs of
-  // step s (pinned by scheduling fences).
-  bf16x8 fa0[MI], fb0[NI], fa1[MI], fb1[NI];
-#define LX_FRAG(SA, SB, KS, FA, FB)                                                 \
+    // One K-slab of MFMAs from stage (SA_, SB_), fragments double-buffered in
+    // registers: the LDS reads of k-step s+1 are issued before the MFMAs of
+    // step s (pinned by scheduling fences).
+    bf16x8 fa0[MI], fb0[NI], fa1[MI], fb1[NI];
+#define LX_FRAG(SA_, SB_, KS, FA, FB)                                               \
   do {                                                                              \
     const int kc_ = (KS) * 2 + (lane >> 5);                                         \
     _Pragma("unroll") for (int mi = 0; mi < MI; ++mi)                               \
-      FA[mi] = *(const bf16x8*)&SA[lds_off2(wm * WM + mi * 32 + (lane & 31), kc_)]; \
+      FA[mi] = *(const bf16x8*)&SA_[lds_off2(wm * WM + mi * 32 + (lane & 31), kc_)]; \
     _Pragma("unroll") for (int ni = 0; ni < NI; ++ni)                               \
-      FB[ni] = *(const bf16x8*)&SB[lds_off2(wn * WN + ni * 32 + (lane & 31), kc_)]; \
+      FB[ni] = *(const bf16x8*)&SB_[lds_off2(wn * WN + ni * 32 + (lane & 31), kc_)]; \
   } while (0)
 #define LX_MFMAS(FA, FB)                                                            \
   do {                                                                              \
@@ -174,92 +193,108 @@ void k_gemm_big(GemmArgs p, int ntn) {
       _Pragma("unroll") for (int ni = 0; ni < NI; ++ni)                             \
         acc[mi][ni] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(FA[mi], FB[ni], acc[mi][ni], 0, 0, 0); \
   } while (0)
-#define LX_COMPUTE(SA, SB)                                                          \
+#define LX_COMPUTE(SA_, SB_)                                                        \
   do {                                                                              \
-    LX_FRAG(SA, SB, 0, fa0, fb0);                                                   \
+    LX_FRAG(SA_, SB_, 0, fa0, fb0);                                                 \
     __builtin_amdgcn_sched_barrier(0);                                              \
-    LX_FRAG(SA, SB, 1, fa1, fb1);                                                   \
+    LX_FRAG(SA_, SB_, 1, fa1, fb1);                                                 \
     __builtin_amdgcn_sched_barrier(0);                                              \
     LX_MFMAS(fa0, fb0);                                                             \
     __builtin_amdgcn_sched_barrier(0);                                              \
-    LX_FRAG(SA, SB, 2, fa0, fb0);                                                   \
+    LX_FRAG(SA_, SB_, 2, fa0, fb0);                                                 \
     __builtin_amdgcn_sched_barrier(0);                                              \
     LX_MFMAS(fa1, fb1);                                                             \
     __builtin_amdgcn_sched_barrier(0);                                              \
-    LX_FRAG(SA, SB, 3, fa1, fb1);                                                   \
+    LX_FRAG(SA_, SB_, 3, fa1, fb1);                                                 \
     __builtin_amdgcn_sched_barrier(0);                                              \
     LX_MFMAS(fa0, fb0);                                                             \
     __builtin_amdgcn_sched_barrier(0);                                              \
     LX_MFMAS(fa1, fb1);                                                             \
   } while (0)
 
-  LX_ISSUE(sA0, sB0, 0);
-  if (nk > 1) LX_ISSUE(sA1, sB1, BK2);
-  int kt = 0;
-  // Slabs kt (stage 0) and kt + 1 (stage 1) are in flight at the top of
-  // every iteration; one loop exit keeps the accumulators in place.
-  for (; kt + 1 < nk; kt += 2) {
-    wait_vmcnt<ROUNDS>();
-    bar();
-    LX_COMPUTE(sA0, sB0);
-    bar();
-    const bool more0 = kt + 2 < nk;
-    if (more0) LX_ISSUE(sA0, sB0, (kt + 2) * BK2);
-    if (more0)
+    LX_ISSUE(sA0, sB0, 0);
+    if (nk > 1) LX_ISSUE(sA1, sB1, BK2);
+    int kt = 0;
+    // Slabs kt (stage 0) and kt + 1 (stage 1) are in flight at the top of
+    // every iteration; one loop exit keeps the accumulators in place.
+    for (; kt + 1 < nk; kt += 2) {
       wait_vmcnt<ROUNDS>();
-    else
+      bar();
+      LX_COMPUTE(sA0, sB0);
+      bar();
+      const bool more0 = kt + 2 < nk;
+      if (more0) LX_ISSUE(sA0, sB0, (kt + 2) * BK2);
+      if (more0)
+        wait_vmcnt<ROUNDS>();
+      else
+        wait_vmcnt<0>();
+      bar();
+      LX_COMPUTE(sA1, sB1);
+      bar();
+      if (kt + 3 < nk) LX_ISSUE(sA1, sB1, (kt + 3) * BK2);
+    }
+    if (kt < nk) {  // odd slab count: the last slab is in stage 0
       wait_vmcnt<0>();
-    bar();
-    LX_COMPUTE(sA1, sB1);
-    bar();
-    if (kt + 3 < nk) LX_ISSUE(sA1, sB1, (kt + 3) * BK2);
-  }
-  if (kt < nk) {  // odd slab count: the last slab is in stage 0
-    wait_vmcnt<0>();
-    bar();
-    LX_COMPUTE(sA0, sB0);
-  }
+      bar();
+      LX_COMPUTE(sA0, sB0);
+      bar();
+    }
 #undef LX_ISSUE
 #undef LX_COMPUTE
 #undef LX_FRAG
 #undef LX_MFMAS
 
-  // 32x32 accumulator layout: lane holds column (lane & 31) and rows
-  // 8*(i/4) + 4*(lane/32) + (i%4) for i = 0..15.
+    // Epilogue. 32x32 accumulator layout: lane holds column (lane & 31) and
+    // rows 8*(i/4) + 4*(lane/32) + (i%4) for i = 0..15. Each wavefront writes
+    // its 32 x WN block of one mi into its own LDS region (row pitch WN + 4
+    // floats), then reads it back as 4 consecutive columns per lane. All
+    // stages are free here (every wavefront passed the barrier above).
+    {
+      constexpr int PITCH = WN + 4;
+      constexpr int LPR = WN / 4;    // lanes per row
+      constexpr int RPP = 64 / LPR;  // rows per pass
+      static_assert(4 * 32 * PITCH * 4 <= (int)sizeof(smem), "epilogue LDS");
+      float* const ep = (float*)smem + wave * (32 * PITCH);
+      const int c4 = (lane % LPR) * 4;
+      const int col = n0 + wn * WN + c4;
 #pragma unroll
-  for (int ni = 0; ni < NI; ++ni) {
-    const int col = n0 + wn * WN + ni * 32 + (lane & 31);
-    if (col >= ncol) continue;
-    if (OUT_HILO) {
-      // part p, local column c -> hi at base_p + c, lo at base_p + ncols[p] + c
-      const int pp = col < p.ncols[0] ? 0 : 1;
-      const int c = pp ? col - p.ncols[0] : col;
-      const int hi_col = (pp ? 2 * p.ncols[0] : 0) + c;
-      const int lo_col = hi_col + p.ncols[pp];
-      __bf16* __restrict__ C = (__bf16*)p.C;
+      for (int mi = 0; mi < MI; ++mi) {
 #pragma unroll
-      for (int mi = 0; mi < MI; ++mi)
+        for (int ni = 0; ni < NI; ++ni)
 #pragma unroll
-        for (int i = 0; i < 16; ++i) {
-          const int r = wm * WM + mi * 32 + 8 * (i >> 2) + 4 * (lane >> 5) + (i & 3);
-          if (r < te.nrows) {
-            const float v = acc[mi][ni][i];
-            const __bf16 h = (__bf16)v;
-            __bf16* rowp = C + (int64_t)(te.row0 + r) * p.ldc;
-            rowp[hi_col] = h;
-            rowp[lo_col] = (__bf16)(v - (float)h);
+          for (int i = 0; i < 16; ++i)
+            ep[(8 * (i >> 2) + 4 * (lane >> 5) + (i & 3)) * PITCH + ni * 32 + (lane & 31)] = acc[mi][ni][i];
+#pragma unroll
+        for (int ps = 0; ps < 32 / RPP; ++ps) {
+          const int rr = ps * RPP + lane / LPR;
+          const float4 v = *(const float4*)&ep[rr * PITCH + c4];
+          const int r = wm * WM + mi * 32 + rr;
+          if (r >= te.nrows || col >= ncol) continue;
+          if (OUT_HILO) {
+            // part p, local column c -> hi at base_p + c, lo at base_p + ncols[p] + c
+            const int pp = col < p.ncols[0] ? 0 : 1;
+            const int c = pp ? col - p.ncols[0] : col;
+            const int hi_col = (pp ? 2 * p.ncols[0] : 0) + c;
+            const int lo_col = hi_col + p.ncols[pp];
+            bf16x4 h, l;
+            h[0] = (__bf16)v.x;
+            h[1] = (__bf16)v.y;
+            h[2] = (__bf16)v.z;
+            h[3] = (__bf16)v.w;
+            l[0] = (__bf16)(v.x - (float)h[0]);
+            l[1] = (__bf16)(v.y - (float)h[1]);
+            l[2] = (__bf16)(v.z - (float)h[2]);
+            l[3] = (__bf16)(v.w - (float)h[3]);
+            __bf16* const rowp = (__bf16*)p.C + (int64_t)(te.row0 + r) * p.ldc;
+            *(bf16x4*)(rowp + hi_col) = h;
+            *(bf16x4*)(rowp + lo_col) = l;
+          } else {
+            *(float4*)(p.C + (int64_t)(te.row0 + r) * p.ldc + col) = v;
           }
         }
-    } else {
-      float* __restrict__ C = p.C + col;
-#pragma unroll
-      for (int mi = 0; mi < MI; ++mi)
-#pragma unroll
-        for (int i = 0; i < 16; ++i) {
-          const int r = wm * WM + mi * 32 + 8 * (i >> 2) + 4 * (lane >> 5) + (i & 3);
-          if (r < te.nrows) C[(int64_t)(te.row0 + r) * p.ldc] = acc[mi][ni][i];
-        }
+      }
     }
+    bar();  // the next item's loads overwrite the epilogue's LDS
   }
 }
 
@@ -280,13 +315,35 @@ bool gemm_big_ok(const GemmArgs& g, int bn, int64_t a_rows_total) {
   if (g.K <= 0 || g.K % BK2 || Kb % BK2 || g.K % Kb) return false;
   if (g.a_koff[0] + g.K > g.lda || (g.ncols[1] > 0 && g.a_koff[1] + g.K > g.lda)) return false;
   if (g.ncols[1] > 0 && g.a_koff[0] != g.a_koff[1] && g.ncols[0] % bn) return false;
+  // the epilogue stores 4 consecutive columns per lane
+  if (g.ncols[0] % 4 || g.ncols[1] % 4 || g.ldc % 4 || ((uintptr_t)g.C & 15)) return false;
   return a_rows_total * g.lda < ((int64_t)1 << 31);
 }
 
+namespace {
+// Persistent grid cap: the largest multiple of 8 not above the device's
+// compute-unit count (one 128 KB-LDS workgroup fits per compute unit).
+int grid_cap() {
+  static std::mutex mu;
+  static int cap[64] = {};
+  int dev = 0;
+  if (hipGetDevice(&dev) != hipSuccess || dev < 0 || dev >= 64) return 256;
+  std::lock_guard<std::mutex> lk(mu);
+  if (!cap[dev]) {
+    int n = 0;
+    if (hipDeviceGetAttribute(&n, hipDeviceAttributeMultiprocessorCount, dev) != hipSuccess || n < 8) n = 256;
+    cap[dev] = n / NXCD * NXCD;
+  }
+  return cap[dev];
+}
+}  // namespace
+
 hipError_t launch_gemm_big(const GemmArgs& g, int bm, int bn, bool out_hilo, int grid_tiles, hipStream_t s) {
   const int ntn = (g.ncols[0] + g.ncols[1] + bn - 1) / bn;
-  const int grid = grid_tiles * ntn;
+  int grid = grid_tiles * ntn;  // upper bound on work items
   if (grid <= 0) return hipSuccess;
+  const int cap = grid_cap();
+  if (grid > cap) grid = cap;
   if (bm == 256) {
     if (bn == 256) return launch_bn<256, 256>(g, out_hilo, grid, ntn, s);
     if (bn == 128) return launch_bn<256, 128>(g, out_hilo, grid, ntn, s);
