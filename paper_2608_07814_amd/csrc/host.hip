@@ -82,9 +82,11 @@ struct Timed {
 size_t align_up(size_t x) { return (x + 255) & ~size_t(255); }
 
 struct LevelPlan {
-  int N = 0, rank = 0, nfac = 0, bm = 0, bm2 = 0;
-  int64_t rows_max = 0, tiles_max = 0, tiles2_max = 0;
-  size_t hist, offsets, row_token, slot_row, slot_flags, tiles, n_tiles, tiles2, n_tiles2, fac;
+  int N = 0, rank = 0, nfac = 0;
+  int bm[kNumTab] = {};
+  int64_t rows_max = 0, tiles_max[kNumTab] = {};
+  size_t hist, offsets, row_token, slot_row, slot_flags, fac;
+  size_t tiles[kNumTab], n_tiles[kNumTab];
   size_t gu, z, hbar, v, y;
 };
 
@@ -120,20 +122,20 @@ Plan make_plan(const lx_tree_layer& t, int T, int k) {
     q.N = level_nodes(t, l);
     q.rank = l == 0 ? 0 : t.levels[l - 1].rank;
     q.nfac = l == 0 ? q.N : t.levels[l - 1].n_factors;
-    q.bm = gemm_bm(t.dtype);
-    q.bm2 = kBigBM;
+    q.bm[kTabSmall] = gemm_bm(t.dtype);
+    q.bm[kTabBig] = kBigBM;
+    q.bm[kTabSkinny] = kSkinnyBM;
     q.rows_max = (int64_t)T * std::min(k, q.N);
-    q.tiles_max = q.rows_max / q.bm + q.N + 1;
-    q.tiles2_max = q.rows_max / q.bm2 + q.N + 1;
+    for (int b = 0; b < kNumTab; ++b) q.tiles_max[b] = q.rows_max / q.bm[b] + q.N + 1;
     q.hist = take((size_t)q.N * p.NT * 4);
     q.offsets = take((size_t)(q.N + 1) * 4);
     q.row_token = take((size_t)q.rows_max * 4);
     q.slot_row = take(tk * 4);
     q.slot_flags = take(tk);
-    q.tiles = take((size_t)q.tiles_max * sizeof(TileEntry));
-    q.n_tiles = take(4);
-    q.tiles2 = take((size_t)q.tiles2_max * sizeof(TileEntry));
-    q.n_tiles2 = take(4);
+    for (int b = 0; b < kNumTab; ++b) {
+      q.tiles[b] = take((size_t)q.tiles_max[b] * sizeof(TileEntry));
+      q.n_tiles[b] = take(4);
+    }
     q.fac = take((size_t)q.N * 4);
     const size_t R = (size_t)q.rows_max;
     const bool work = l == 0 || q.nfac > 0;
@@ -298,8 +300,7 @@ lx_status run(const lx_tree_layer& t, int T, int k, const void* x, const int32_t
     const LevelPlan& q = P.lv[l];
     BucketLevel& b = ba.lv[l];
     b.n_nodes = q.N;
-    b.bm = q.bm;
-    b.bm2 = q.bm2;
+    for (int i = 0; i < kNumTab; ++i) b.tile_bm[i] = q.bm[i];
     b.work_all = l == 0;
     b.fac = l > 0 ? (const int32_t*)(W + q.fac) : nullptr;
     b.hist = (int32_t*)(W + q.hist);
@@ -307,10 +308,10 @@ lx_status run(const lx_tree_layer& t, int T, int k, const void* x, const int32_t
     b.row_token = (int32_t*)(W + q.row_token);
     b.slot_row = (int32_t*)(W + q.slot_row);
     b.slot_flags = (uint8_t*)(W + q.slot_flags);
-    b.tiles = (TileEntry*)(W + q.tiles);
-    b.n_tiles = (int32_t*)(W + q.n_tiles);
-    b.tiles2 = (TileEntry*)(W + q.tiles2);
-    b.n_tiles2 = (int32_t*)(W + q.n_tiles2);
+    for (int i = 0; i < kNumTab; ++i) {
+      b.tiles[i] = (TileEntry*)(W + q.tiles[i]);
+      b.n_tiles[i] = (int32_t*)(W + q.n_tiles[i]);
+    }
   }
   LX_LAUNCH("bucket_hist", launch_bucket_hist(ba, stream));
   LX_LAUNCH("bucket_scan", launch_bucket_scan(ba, stream));
@@ -333,21 +334,34 @@ lx_status run(const lx_tree_layer& t, int T, int k, const void* x, const int32_t
     // inside one half, so its weight columns stay inside the weight row
     fast[l] = fast[0] && r % 64 == 0 && R * 2 * f < two31 && R * 4 * r < two31;
   }
+  // Levels with few rows per node (decode-sized batches) stream their
+  // weights through the skinny kernel; the large tiles would spend their
+  // time on MFMA work over padding rows.
+  bool skinny[kMaxLvl] = {};
+  for (int l = 0; l <= L; ++l) skinny[l] = P.lv[l].rows_max / std::max(P.lv[l].N, 1) <= 64;
   auto big = [&](const char* name, GemmArgs g, int l, int bm, int bn, bool hilo,
                  int64_t a_rows_total) -> lx_status {
     const LevelPlan& q = P.lv[l];
+    if (!g.B[1]) g.B[1] = g.B[0];
+    if (skinny[l] && gemm_big_ok(g, kSkinnyBN, a_rows_total)) {
+      g.tiles = ba.lv[l].tiles[kTabSkinny];
+      g.n_tiles = ba.lv[l].n_tiles[kTabSkinny];
+      LX_LAUNCH(name, launch_gemm_skinny(g, hilo, (int)q.tiles_max[kTabSkinny], stream));
+      return LX_OK;
+    }
     if (!gemm_big_ok(g, bn, a_rows_total))
       return fail(LX_ERR_UNSUPPORTED, std::string(name) + ": shape not supported by the large-tile GEMM");
-    g.tiles = bm == kBigBM ? ba.lv[l].tiles2 : ba.lv[l].tiles;
-    g.n_tiles = bm == kBigBM ? ba.lv[l].n_tiles2 : ba.lv[l].n_tiles;
-    if (!g.B[1]) g.B[1] = g.B[0];
-    LX_LAUNCH(name, launch_gemm_big(g, bm, bn, hilo, (int)(bm == kBigBM ? q.tiles2_max : q.tiles_max), stream));
+    const int tab = bm == kBigBM ? kTabBig : kTabSmall;
+    if (q.bm[tab] != bm) return fail(LX_ERR_UNSUPPORTED, std::string(name) + ": no tile table for this height");
+    g.tiles = ba.lv[l].tiles[tab];
+    g.n_tiles = ba.lv[l].n_tiles[tab];
+    LX_LAUNCH(name, launch_gemm_big(g, bm, bn, hilo, (int)q.tiles_max[tab], stream));
     return LX_OK;
   };
   auto small = [&](const char* name, GemmArgs g, int l, AMode am) -> lx_status {
-    g.tiles = ba.lv[l].tiles;
-    g.n_tiles = ba.lv[l].n_tiles;
-    LX_LAUNCH(name, launch_gemm(g, dt, am, (int)P.lv[l].tiles_max, stream));
+    g.tiles = ba.lv[l].tiles[kTabSmall];
+    g.n_tiles = ba.lv[l].n_tiles[kTabSmall];
+    LX_LAUNCH(name, launch_gemm(g, dt, am, (int)P.lv[l].tiles_max[kTabSmall], stream));
     return LX_OK;
   };
 #define LX_TRY(X)                  \

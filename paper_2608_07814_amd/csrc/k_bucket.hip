@@ -157,14 +157,14 @@ __global__ __launch_bounds__(1024) void k_bucket_scan(BucketArgs a) {
   if (tid == 0) lv.offsets[N] = grand;
   __syncthreads();
 
-  // 3. GEMM tile tables over the nodes that do work, in node order: one for
-  //    tile height bm, one for bm2
+  // 3. GEMM tile tables over the nodes that do work, in node order, one per
+  //    tile height
   const int nchunk = (N + nth - 1) / nth;
   const int nb = tid * nchunk;
   const int ne = nb + nchunk < N ? nb + nchunk : N;
-  for (int tab = 0; tab < 2; ++tab) {
-    const int bm = tab == 0 ? lv.bm : lv.bm2;
-    TileEntry* tiles = tab == 0 ? lv.tiles : lv.tiles2;
+  for (int tab = 0; tab < kNumTab; ++tab) {
+    const int bm = lv.tile_bm[tab];
+    TileEntry* tiles = lv.tiles[tab];
     int my_tiles = 0;
     for (int n = nb; n < ne; ++n) {
       const bool work = lv.work_all || lv.fac[n] >= 0;
@@ -188,7 +188,7 @@ __global__ __launch_bounds__(1024) void k_bucket_scan(BucketArgs a) {
         tiles[tpos++] = te;
       }
     }
-    if (tid == 0) *(tab == 0 ? lv.n_tiles : lv.n_tiles2) = ntiles;
+    if (tid == 0) *lv.n_tiles[tab] = ntiles;
   }
 }
 

@@ -72,6 +72,9 @@ __device__ __forceinline__ void wait_vmcnt() {
   __builtin_amdgcn_s_waitcnt((N & 0xF) | ((N >> 4) << 14) | (0x7 << 4) | (0xF << 8));
 }
 
+// s_waitcnt with only the LDS/scalar-memory counter constrained to 0.
+__device__ __forceinline__ void wait_lgkm0() { __builtin_amdgcn_s_waitcnt(0xF | (0x7 << 4) | (0x3 << 14)); }
+
 // Barrier without a memory fence: the fence of __syncthreads() would drain
 // the next slab's in-flight loads. Each wavefront first waits for its own
 // loads of the slab (vmcnt), so after the barrier the whole slab is in LDS.
@@ -298,6 +301,161 @@ void k_gemm_big(GemmArgs p, int ntn) {
   }
 }
 
+// ---------------------------------------------------------------- skinny
+// 32 x 64 output tile per 128-thread workgroup (two wavefronts, one 32x32
+// MFMA block each), K-slabs of 64 through a 4-stage LDS ring (48 KB, so
+// three workgroups fit per compute unit). Three slabs are in flight while one
+// is consumed: with few rows per tile the kernel streams weights and is bound
+// by HBM, not by the MFMAs.
+constexpr int SK_THR = 128, SK_NST = 4;
+
+template <int R>
+__device__ __forceinline__ void wait_slabs(int ahead) {
+  if (ahead >= 3)
+    wait_vmcnt<3 * R>();
+  else if (ahead == 2)
+    wait_vmcnt<2 * R>();
+  else if (ahead == 1)
+    wait_vmcnt<R>();
+  else
+    wait_vmcnt<0>();
+}
+
+template <bool OUT_HILO>
+__global__ __launch_bounds__(SK_THR) void k_gemm_skinny(GemmArgs p, int ntn) {
+  constexpr int BM = kSkinnyBM, BN = kSkinnyBN;
+  constexpr int A_ROUNDS = BM * 8 / SK_THR, B_ROUNDS = BN * 8 / SK_THR;
+  constexpr int R = A_ROUNDS + B_ROUNDS;
+  constexpr int SA = BM * BK2, STAGE = (BM + BN) * BK2;
+  __shared__ __attribute__((aligned(1024))) u16 smem[SK_NST * STAGE];
+
+  // one work item per workgroup, XCD-contiguous order (grid >= items)
+  const int real = *p.n_tiles * ntn;
+  const int q = real / NXCD, rmd = real % NXCD;
+  const int x = blockIdx.x % NXCD;
+  const int Lg = x * q + (x < rmd ? x : rmd) + (int)blockIdx.x / NXCD;
+  if (Lg >= x * q + (x < rmd ? x : rmd) + q + (x < rmd ? 1 : 0)) return;
+  const int ti = Lg / ntn, nt = Lg % ntn;
+
+  const int tid = threadIdx.x;
+  const int wave = tid >> 6, lane = tid & 63;
+  const TileEntry te = p.tiles[ti];
+  const int n0 = nt * BN;
+  const int ncol = p.ncols[0] + p.ncols[1];
+  const int K = p.K;
+  const int Kb = p.Kb > 0 ? p.Kb : K;
+  const int nk = K / BK2;
+  const int tpart = n0 < p.ncols[0] ? 0 : 1;
+  const int akoff = p.a_koff[tpart];
+  const u16* __restrict__ Ab = (const u16*)p.A;
+  const u16* __restrict__ Bw0 = (const u16*)p.B[0] + (int64_t)te.widx * p.b_stride[0];
+  const u16* __restrict__ Bw1 = (const u16*)p.B[1] + (int64_t)te.widx * p.b_stride[1];
+
+  // LDS slot P = round * 128 + tid holds row P >> 3, physical chunk P & 7
+  // (logical chunk (P & 7) ^ swz(row)); rows past the tile are clamped.
+  uint32_t aoff[A_ROUNDS];
+#pragma unroll
+  for (int j = 0; j < A_ROUNDS; ++j) {
+    const int Ps = j * SK_THR + tid;
+    const int row = Ps >> 3;
+    const int c = (Ps & 7) ^ swz2(row);
+    const int r = row < te.nrows ? row : te.nrows - 1;
+    const int src = p.a_rows ? p.a_rows[te.row0 + r] : te.row0 + r;
+    aoff[j] = (uint32_t)src * (uint32_t)p.lda + (uint32_t)(akoff + c * 8);
+  }
+  const u16* bptr[B_ROUNDS];
+#pragma unroll
+  for (int j = 0; j < B_ROUNDS; ++j) {
+    const int Ps = j * SK_THR + tid;
+    const int row = Ps >> 3;
+    const int c = (Ps & 7) ^ swz2(row);
+    const int n = n0 + row < ncol ? n0 + row : ncol - 1;
+    bptr[j] = (n < p.ncols[0] ? Bw0 + (int64_t)n * Kb : Bw1 + (int64_t)(n - p.ncols[0]) * Kb) + c * 8;
+  }
+  auto issue = [&](int st, int k0) {
+    u16* const sA = smem + st * STAGE;
+    const int kb = k0 % Kb;
+#pragma unroll
+    for (int j = 0; j < A_ROUNDS; ++j) load_lds16(Ab + (aoff[j] + (uint32_t)k0), sA + (j * SK_THR + wave * 64) * 8);
+#pragma unroll
+    for (int j = 0; j < B_ROUNDS; ++j) load_lds16(bptr[j] + kb, sA + SA + (j * SK_THR + wave * 64) * 8);
+  };
+
+  f32x16 acc;
+#pragma unroll
+  for (int i = 0; i < 16; ++i) acc[i] = 0.f;
+  auto compute = [&](int st) {
+    const u16* const sA = smem + st * STAGE;
+    const u16* const sB = sA + SA;
+    const int ra = lane & 31, rb = wave * 32 + (lane & 31);
+    bf16x8 fa[4], fb[4];
+#pragma unroll
+    for (int ks = 0; ks < 4; ++ks) {
+      const int kc = ks * 2 + (lane >> 5);
+      fa[ks] = *(const bf16x8*)&sA[lds_off2(ra, kc)];
+      fb[ks] = *(const bf16x8*)&sB[lds_off2(rb, kc)];
+    }
+#pragma unroll
+    for (int ks = 0; ks < 4; ++ks) acc = __builtin_amdgcn_mfma_f32_32x32x16_bf16(fa[ks], fb[ks], acc, 0, 0, 0);
+  };
+
+  // Slab kt lives in stage kt % 4. Slabs 0..3 are issued up front; after the
+  // barrier that follows slab kt's compute, stage kt % 4 is free and slab
+  // kt + 4 goes there.
+  const int npre = nk < SK_NST ? nk : SK_NST;
+  for (int i = 0; i < npre; ++i) issue(i, i * BK2);
+  wait_slabs<R>(npre - 1);
+  bar();
+  for (int kt = 0; kt < nk; ++kt) {
+    compute(kt & (SK_NST - 1));
+    if (kt + 1 < nk) {
+      // slabs issued so far: 0 .. min(kt + 3, nk - 1); wait for kt + 1
+      const int last = kt + 3 < nk - 1 ? kt + 3 : nk - 1;
+      wait_slabs<R>(last - (kt + 1));
+      wait_lgkm0();
+      bar();
+      if (kt + SK_NST < nk) issue(kt & (SK_NST - 1), (kt + SK_NST) * BK2);
+    }
+  }
+  wait_lgkm0();
+  bar();  // every wavefront is done with the stages: the epilogue reuses them
+
+  // Epilogue: 32 x 32 block per wavefront through LDS (pitch 36 floats), then
+  // 4 consecutive columns per lane.
+  constexpr int PITCH = 36, LPR = 8, RPP = 8;
+  float* const ep = (float*)smem + wave * (32 * PITCH);
+#pragma unroll
+  for (int i = 0; i < 16; ++i) ep[(8 * (i >> 2) + 4 * (lane >> 5) + (i & 3)) * PITCH + (lane & 31)] = acc[i];
+  const int c4 = (lane % LPR) * 4;
+  const int col = n0 + wave * 32 + c4;
+#pragma unroll
+  for (int ps = 0; ps < 32 / RPP; ++ps) {
+    const int r = ps * RPP + lane / LPR;
+    const float4 v = *(const float4*)&ep[r * PITCH + c4];
+    if (r >= te.nrows || col >= ncol) continue;
+    if (OUT_HILO) {
+      const int pp = col < p.ncols[0] ? 0 : 1;
+      const int c = pp ? col - p.ncols[0] : col;
+      const int hi_col = (pp ? 2 * p.ncols[0] : 0) + c;
+      const int lo_col = hi_col + p.ncols[pp];
+      bf16x4 h, l;
+      h[0] = (__bf16)v.x;
+      h[1] = (__bf16)v.y;
+      h[2] = (__bf16)v.z;
+      h[3] = (__bf16)v.w;
+      l[0] = (__bf16)(v.x - (float)h[0]);
+      l[1] = (__bf16)(v.y - (float)h[1]);
+      l[2] = (__bf16)(v.z - (float)h[2]);
+      l[3] = (__bf16)(v.w - (float)h[3]);
+      __bf16* const rowp = (__bf16*)p.C + (int64_t)(te.row0 + r) * p.ldc;
+      *(bf16x4*)(rowp + hi_col) = h;
+      *(bf16x4*)(rowp + lo_col) = l;
+    } else {
+      *(float4*)(p.C + (int64_t)(te.row0 + r) * p.ldc + col) = v;
+    }
+  }
+}
+
 template <int BM, int BN>
 hipError_t launch_bn(const GemmArgs& g, bool hilo, int grid, int ntn, hipStream_t s) {
   if (hilo)
@@ -352,6 +510,17 @@ hipError_t launch_gemm_big(const GemmArgs& g, int bm, int bn, bool out_hilo, int
   if (bn == 256) return launch_bn<128, 256>(g, out_hilo, grid, ntn, s);
   if (bn == 128) return launch_bn<128, 128>(g, out_hilo, grid, ntn, s);
   return launch_bn<128, 64>(g, out_hilo, grid, ntn, s);
+}
+
+hipError_t launch_gemm_skinny(const GemmArgs& g, bool out_hilo, int grid_tiles, hipStream_t s) {
+  const int ntn = (g.ncols[0] + g.ncols[1] + kSkinnyBN - 1) / kSkinnyBN;
+  const int grid = grid_tiles * ntn;  // >= work items: one item per workgroup
+  if (grid <= 0) return hipSuccess;
+  if (out_hilo)
+    hipLaunchKernelGGL(k_gemm_skinny<true>, dim3(grid), dim3(SK_THR), 0, s, g, ntn);
+  else
+    hipLaunchKernelGGL(k_gemm_skinny<false>, dim3(grid), dim3(SK_THR), 0, s, g, ntn);
+  return hipGetLastError();
 }
 
 }  // namespace lx

@@ -22,10 +22,13 @@ struct TileEntry {
 };
 
 // ---------------------------------------------------------------- bucketing
+// GEMM tile tables built by the bucketing, one per tile height: the
+// register-staged kernel, the large-tile kernel and the skinny kernel.
+constexpr int kTabSmall = 0, kTabBig = 1, kTabSkinny = 2, kNumTab = 3;
+
 struct BucketLevel {
   int32_t n_nodes;
-  int32_t bm;              // GEMM tile height the tile table is built for
-  int32_t bm2;             // tile height of the second table (large-tile GEMMs)
+  int32_t tile_bm[kNumTab];  // tile height of each table
   int32_t work_all;        // 1: every node does GEMM work (anchor level)
   const int32_t* fac;      // validated factor index per node (-1 none)
   int32_t* hist;           // [n_nodes][n_tok_tiles], scanned in place
@@ -34,10 +37,8 @@ struct BucketLevel {
   int32_t* slot_row;       // [T * k]
   uint8_t* slot_flags;     // [T * k] bit0: first slot of its row, bit1: the row's
                            // node does work at this level (always at level 0)
-  TileEntry* tiles;        // [tiles_max]
-  int32_t* n_tiles;        // [1]
-  TileEntry* tiles2;       // [tiles2_max]
-  int32_t* n_tiles2;       // [1]
+  TileEntry* tiles[kNumTab];  // [tiles_max of the table]
+  int32_t* n_tiles[kNumTab];  // [1] each
 };
 
 struct BucketArgs {
@@ -109,6 +110,14 @@ constexpr int kBigBM = 256;
 bool gemm_big_ok(const GemmArgs& g, int bn, int64_t a_rows_total);
 hipError_t launch_gemm_big(const GemmArgs& g, int bm, int bn, bool out_hilo, int grid_tiles,
                            hipStream_t s);
+
+// Skinny kernel for levels with few rows per node (decode-sized batches):
+// 32-row tiles, 64 output columns per workgroup, a 4-stage LDS ring and
+// several workgroups per compute unit, so weight streaming is limited by
+// HBM rather than by MFMA work on padding rows. Same operand conventions and
+// applicability as the large-tile kernel (with bn = kSkinnyBN).
+constexpr int kSkinnyBM = 32, kSkinnyBN = 64;
+hipError_t launch_gemm_skinny(const GemmArgs& g, bool out_hilo, int grid_tiles, hipStream_t s);
 
 // ---------------------------------------------------------------- elementwise
 struct TokenArgs {
