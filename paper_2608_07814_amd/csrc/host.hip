@@ -14,6 +14,7 @@
 //   combine                out[t] = sum of the token's rows over all levels
 #include <algorithm>
 #include <map>
+#include <mutex>
 #include <string>
 #include <vector>
 
@@ -69,9 +70,11 @@ struct Timed {
   }
 };
 
+// Launches go to `lstream` (the caller's stream, or the auxiliary stream
+// while an independent correction chain is being enqueued).
 #define LX_LAUNCH(NAME, CALL)                                                          \
   do {                                                                                 \
-    Timed _t(NAME, stream);                                                            \
+    Timed _t(NAME, lstream);                                                           \
     hipError_t _e = (CALL);                                                            \
     _t.done();                                                                         \
     if (_e != hipSuccess)                                                              \
@@ -243,6 +246,63 @@ const char* kDownIn[kMaxLvl] = {"", "lowrank_down_in_l1", "lowrank_down_in_l2", 
 const char* kDownOut[kMaxLvl] = {"", "lowrank_down_out_l1", "lowrank_down_out_l2", "lowrank_down_out_l3",
                                  "lowrank_down_out_l4"};
 
+// ------------------------------------------------------- auxiliary stream
+// The correction-level GEMM chains do not depend on the anchor GEMMs, so
+// they are enqueued on a second stream of the same device (default
+// priority) between an event fork and join on the caller's stream; the
+// hardware then fills compute units left idle by one chain with the other
+// (the tail of the persistent anchor GEMM; decode-sized batches, where both
+// chains stream weights). The mutex serialises the fork/join event use of
+// concurrent callers on one device.
+struct Aux {
+  std::mutex mu;
+  hipStream_t s = nullptr;
+  hipEvent_t fork = nullptr, join = nullptr;
+  bool ok = false;
+};
+
+Aux* aux_for_current_device() {
+  static std::mutex mu;
+  static Aux aux[64];
+  int dev = 0;
+  if (hipGetDevice(&dev) != hipSuccess || dev < 0 || dev >= 64) return nullptr;
+  std::lock_guard<std::mutex> lk(mu);
+  Aux& a = aux[dev];
+  if (!a.ok && !a.s) {
+    if (hipStreamCreateWithFlags(&a.s, hipStreamNonBlocking) != hipSuccess ||
+        hipEventCreateWithFlags(&a.fork, hipEventDisableTiming) != hipSuccess ||
+        hipEventCreateWithFlags(&a.join, hipEventDisableTiming) != hipSuccess)
+      return nullptr;
+    a.ok = true;
+  }
+  return a.ok ? &a : nullptr;
+}
+
+// Fork/join of the auxiliary stream around one independent chain. The
+// destructor joins an open fork, so an early error return still leaves the
+// caller's stream ordered after everything that was enqueued.
+struct ForkJoin {
+  Aux* aux;
+  hipStream_t main;
+  bool open = false;
+  ForkJoin(Aux* a, hipStream_t m) : aux(a), main(m) {}
+  hipError_t fork() {
+    if (!aux) return hipSuccess;
+    hipError_t e = hipEventRecord(aux->fork, main);
+    if (e == hipSuccess) e = hipStreamWaitEvent(aux->s, aux->fork, 0);
+    open = e == hipSuccess;
+    return e;
+  }
+  hipError_t join() {
+    if (!aux || !open) return hipSuccess;
+    open = false;
+    hipError_t e = hipEventRecord(aux->join, aux->s);
+    if (e == hipSuccess) e = hipStreamWaitEvent(main, aux->join, 0);
+    return e;
+  }
+  ~ForkJoin() { (void)join(); }
+};
+
 enum Stop { RUN_ALL, RUN_BUCKET };
 
 // The whole forward (or just the bucketing) of a validated tree.
@@ -267,6 +327,7 @@ lx_status run(const lx_tree_layer& t, int T, int k, const void* x, const int32_t
   if (ws_bytes < P.total) return fail(LX_ERR_WORKSPACE_TOO_SMALL, "workspace smaller than required");
   char* W = (char*)ws;
   const int L = P.L, E = P.E, d = P.d, f = P.f;
+  hipStream_t lstream = stream;
 
   PrepareArgs pa{};
   pa.E = E;
@@ -282,8 +343,10 @@ lx_status run(const lx_tree_layer& t, int T, int k, const void* x, const int32_t
       pa.fac[l] = (int32_t*)(W + P.lv[l].fac);
     }
   }
-  LX_LAUNCH("bucket_prepare", launch_prepare(pa, stream));
-  if (T == 0) return LX_OK;
+  if (T == 0) {  // nothing to route: the status word is still reset
+    LX_LAUNCH("bucket_prepare", launch_prepare(pa, lstream));
+    return LX_OK;
+  }
 
   BucketArgs ba{};
   ba.T = T;
@@ -313,9 +376,14 @@ lx_status run(const lx_tree_layer& t, int T, int k, const void* x, const int32_t
       b.n_tiles[i] = (int32_t*)(W + q.n_tiles[i]);
     }
   }
-  LX_LAUNCH("bucket_hist", launch_bucket_hist(ba, stream));
-  LX_LAUNCH("bucket_scan", launch_bucket_scan(ba, stream));
-  LX_LAUNCH("bucket_place", launch_bucket_place(ba, stream));
+  if (bucket_small_ok(ba)) {
+    LX_LAUNCH("bucket_small", launch_bucket_small(pa, ba, lstream));
+  } else {
+    LX_LAUNCH("bucket_prepare", launch_prepare(pa, lstream));
+    LX_LAUNCH("bucket_hist", launch_bucket_hist(ba, lstream));
+    LX_LAUNCH("bucket_scan", launch_bucket_scan(ba, lstream));
+    LX_LAUNCH("bucket_place", launch_bucket_place(ba, lstream));
+  }
   if (stop == RUN_BUCKET) return LX_OK;
 
   const lx_dtype dt = t.dtype;
@@ -346,7 +414,7 @@ lx_status run(const lx_tree_layer& t, int T, int k, const void* x, const int32_t
     if (skinny[l] && gemm_big_ok(g, kSkinnyBN, a_rows_total)) {
       g.tiles = ba.lv[l].tiles[kTabSkinny];
       g.n_tiles = ba.lv[l].n_tiles[kTabSkinny];
-      LX_LAUNCH(name, launch_gemm_skinny(g, hilo, (int)q.tiles_max[kTabSkinny], stream));
+      LX_LAUNCH(name, launch_gemm_skinny(g, hilo, (int)q.tiles_max[kTabSkinny], lstream));
       return LX_OK;
     }
     if (!gemm_big_ok(g, bn, a_rows_total))
@@ -355,13 +423,13 @@ lx_status run(const lx_tree_layer& t, int T, int k, const void* x, const int32_t
     if (q.bm[tab] != bm) return fail(LX_ERR_UNSUPPORTED, std::string(name) + ": no tile table for this height");
     g.tiles = ba.lv[l].tiles[tab];
     g.n_tiles = ba.lv[l].n_tiles[tab];
-    LX_LAUNCH(name, launch_gemm_big(g, bm, bn, hilo, (int)q.tiles_max[tab], stream));
+    LX_LAUNCH(name, launch_gemm_big(g, bm, bn, hilo, (int)q.tiles_max[tab], lstream));
     return LX_OK;
   };
   auto small = [&](const char* name, GemmArgs g, int l, AMode am) -> lx_status {
     g.tiles = ba.lv[l].tiles[kTabSmall];
     g.n_tiles = ba.lv[l].n_tiles[kTabSmall];
-    LX_LAUNCH(name, launch_gemm(g, dt, am, (int)P.lv[l].tiles_max[kTabSmall], stream));
+    LX_LAUNCH(name, launch_gemm(g, dt, am, (int)P.lv[l].tiles_max[kTabSmall], lstream));
     return LX_OK;
   };
 #define LX_TRY(X)                  \
@@ -369,6 +437,26 @@ lx_status run(const lx_tree_layer& t, int T, int k, const void* x, const int32_t
     const lx_status s_ = (X);      \
     if (s_ != LX_OK) return s_;    \
   } while (0)
+
+#define LX_HIP(X)                                                        \
+  do {                                                                   \
+    const hipError_t e_ = (X);                                           \
+    if (e_ != hipSuccess) return fail(LX_ERR_HIP, hipGetErrorString(e_)); \
+  } while (0)
+
+  // The correction chains go to the auxiliary stream, concurrently with the
+  // anchor GEMMs on the caller's stream, when the anchor level is large
+  // enough to run on the persistent kernel (for decode-sized batches the
+  // cross-stream event latency outweighs the overlap). Per-kernel timing
+  // runs serialised so that each kernel's duration is its own.
+  bool any_fac = false;
+  for (int l = 1; l <= L; ++l) any_fac |= t.levels[l - 1].n_factors > 0;
+  Aux* const aux = any_fac && !skinny[0] && !g_prof ? aux_for_current_device() : nullptr;
+  std::unique_lock<std::mutex> aux_lock;
+  if (aux) aux_lock = std::unique_lock<std::mutex>(aux->mu);
+  ForkJoin fj_up(aux, stream), fj_down(aux, stream);
+  LX_HIP(fj_up.fork());
+  if (aux) lstream = aux->s;
 
   // correction gate|up per level: z = B x (once per (token, node)), dgu = A z
   for (int l = 1; l <= L; ++l) {
@@ -414,6 +502,7 @@ lx_status run(const lx_tree_layer& t, int T, int k, const void* x, const int32_t
       LX_TRY(small(kLowOut[l], h, l, A_F32_HILO));
     }
   }
+  lstream = stream;
   // anchor gate|up, once per (token, anchor)
   {
     const LevelPlan& q = P.lv[0];
@@ -455,7 +544,9 @@ lx_status run(const lx_tree_layer& t, int T, int k, const void* x, const int32_t
   }
   ta.out = out;
   ta.out_dtype = out_dtype;
-  LX_LAUNCH("swiglu_reduce", launch_swiglu_reduce(ta, stream));
+  LX_HIP(fj_up.join());
+  LX_LAUNCH("swiglu_reduce", launch_swiglu_reduce(ta, lstream));
+  LX_HIP(fj_down.fork());
 
   // anchor down, once per (token, anchor), on the weighted activation sums
   {
@@ -479,6 +570,7 @@ lx_status run(const lx_tree_layer& t, int T, int k, const void* x, const int32_t
     }
   }
   // correction down per level: v = B_down hbar, y = A_down v
+  if (aux) lstream = aux->s;
   for (int l = 1; l <= L; ++l) {
     const LevelPlan& q = P.lv[l];
     const lx_level& v = t.levels[l - 1];
@@ -518,7 +610,10 @@ lx_status run(const lx_tree_layer& t, int T, int k, const void* x, const int32_t
     }
   }
 #undef LX_TRY
-  LX_LAUNCH("combine", launch_combine(ta, stream));
+  lstream = stream;
+  LX_HIP(fj_down.join());
+  LX_LAUNCH("combine", launch_combine(ta, lstream));
+#undef LX_HIP
   return LX_OK;
 }
 

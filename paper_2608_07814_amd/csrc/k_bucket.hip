@@ -20,12 +20,13 @@
 namespace lx {
 namespace {
 
+constexpr int kSmallMaxNodes = 2048;  // single-workgroup path: nodes and experts per level
+
 // Ancestors of every expert at every level and validated factor indices.
 // Single workgroup: it also zeroes the status word before anything else runs.
-__global__ __launch_bounds__(1024) void k_prepare(PrepareArgs a) {
-  __shared__ uint32_t s_bad;
-  if (threadIdx.x == 0) s_bad = 0;
-  __syncthreads();
+// Ancestors of every expert at every level and validated factor indices,
+// by one workgroup; returns this thread's tree-error bits.
+__device__ inline uint32_t prepare_tables(const PrepareArgs& a) {
   uint32_t bad = 0;
   const int E = a.E, L = a.L;
   for (int e = threadIdx.x; e < E; e += blockDim.x) {
@@ -56,6 +57,15 @@ __global__ __launch_bounds__(1024) void k_prepare(PrepareArgs a) {
       a.fac[l][n] = m;
     }
   }
+  return bad;
+}
+
+// Single workgroup: it also zeroes the status word before anything else runs.
+__global__ __launch_bounds__(1024) void k_prepare(PrepareArgs a) {
+  __shared__ uint32_t s_bad;
+  if (threadIdx.x == 0) s_bad = 0;
+  __syncthreads();
+  const uint32_t bad = prepare_tables(a);
   if (bad) atomicOr(&s_bad, bad);
   __syncthreads();
   if (threadIdx.x == 0) *a.flags = s_bad;
@@ -129,6 +139,46 @@ __device__ inline int block_exscan(int v, int* s_wave, int& total) {
   return res;
 }
 
+// GEMM tile tables over the nodes that do work, in node order, one per tile
+// height. off / fac: the level's node offsets and validated factor indices
+// (global or LDS), complete and visible to the whole workgroup.
+__device__ inline void build_tile_tables(const BucketLevel& lv, const int32_t* off, const int32_t* fac,
+                                         int* s_wave) {
+  const int N = lv.n_nodes;
+  const int nth = blockDim.x, tid = threadIdx.x;
+  const int nchunk = (N + nth - 1) / nth;
+  const int nb = tid * nchunk;
+  const int ne = nb + nchunk < N ? nb + nchunk : N;
+  for (int tab = 0; tab < kNumTab; ++tab) {
+    const int bm = lv.tile_bm[tab];
+    TileEntry* tiles = lv.tiles[tab];
+    int my_tiles = 0;
+    for (int n = nb; n < ne; ++n) {
+      const bool work = lv.work_all || fac[n] >= 0;
+      const int cnt = off[n + 1] - off[n];
+      if (work && cnt > 0) my_tiles += (cnt + bm - 1) / bm;
+    }
+    int ntiles = 0;
+    int tpos = block_exscan(my_tiles, s_wave, ntiles);
+    for (int n = nb; n < ne; ++n) {
+      const bool work = lv.work_all || fac[n] >= 0;
+      const int o = off[n];
+      const int cnt = off[n + 1] - o;
+      if (!work || cnt == 0) continue;
+      const int widx = lv.work_all ? n : fac[n];
+      for (int r = 0; r < cnt; r += bm) {
+        TileEntry te;
+        te.widx = widx;
+        te.row0 = o + r;
+        te.nrows = cnt - r < bm ? cnt - r : bm;
+        te.node = n;
+        tiles[tpos++] = te;
+      }
+    }
+    if (tid == 0) *lv.n_tiles[tab] = ntiles;
+  }
+}
+
 __global__ __launch_bounds__(1024) void k_bucket_scan(BucketArgs a) {
   __shared__ int s_wave[64];
   const int l = blockIdx.x;
@@ -157,39 +207,7 @@ __global__ __launch_bounds__(1024) void k_bucket_scan(BucketArgs a) {
   if (tid == 0) lv.offsets[N] = grand;
   __syncthreads();
 
-  // 3. GEMM tile tables over the nodes that do work, in node order, one per
-  //    tile height
-  const int nchunk = (N + nth - 1) / nth;
-  const int nb = tid * nchunk;
-  const int ne = nb + nchunk < N ? nb + nchunk : N;
-  for (int tab = 0; tab < kNumTab; ++tab) {
-    const int bm = lv.tile_bm[tab];
-    TileEntry* tiles = lv.tiles[tab];
-    int my_tiles = 0;
-    for (int n = nb; n < ne; ++n) {
-      const bool work = lv.work_all || lv.fac[n] >= 0;
-      const int cnt = lv.offsets[n + 1] - lv.offsets[n];
-      if (work && cnt > 0) my_tiles += (cnt + bm - 1) / bm;
-    }
-    int ntiles = 0;
-    int tpos = block_exscan(my_tiles, s_wave, ntiles);
-    for (int n = nb; n < ne; ++n) {
-      const bool work = lv.work_all || lv.fac[n] >= 0;
-      const int off = lv.offsets[n];
-      const int cnt = lv.offsets[n + 1] - off;
-      if (!work || cnt == 0) continue;
-      const int widx = lv.work_all ? n : lv.fac[n];
-      for (int r = 0; r < cnt; r += bm) {
-        TileEntry te;
-        te.widx = widx;
-        te.row0 = off + r;
-        te.nrows = cnt - r < bm ? cnt - r : bm;
-        te.node = n;
-        tiles[tpos++] = te;
-      }
-    }
-    if (tid == 0) *lv.n_tiles[tab] = ntiles;
-  }
+  build_tile_tables(lv, lv.offsets, lv.fac, s_wave);
 }
 
 __global__ __launch_bounds__(64) void k_bucket_place(BucketArgs a) {
@@ -234,6 +252,128 @@ __global__ __launch_bounds__(64) void k_bucket_place(BucketArgs a) {
   }
 }
 
+// Whole bucketing of a batch of at most 64 tokens in one workgroup, with
+// every table it consults kept in LDS: per level the node of each expert
+// (walking the parent arrays to the root, so a broken path invalidates the
+// expert at every level, as in k_prepare) and the validated factor indices;
+// then one 64-bit token mask per node (the batch is one token tile), node
+// offsets, tile tables and slot placement, one thread per routing slot. Same
+// results as the four-pass path with one token tile.
+struct SmallLds {
+  unsigned long long mask[kSmallMaxNodes];
+  int32_t off[kSmallMaxNodes + 1];
+  int32_t fac[kSmallMaxNodes];
+  int32_t anc[kSmallMaxNodes];  // node of each expert at the current level
+  int32_t node[kTokTile * LX_MAX_K];
+  int32_t ids[kTokTile * LX_MAX_K];
+  int wave[64];
+  uint32_t bad;
+};
+
+__global__ __launch_bounds__(1024) void k_bucket_small(PrepareArgs pa, BucketArgs a) {
+  extern __shared__ __attribute__((aligned(16))) unsigned char s_raw[];
+  SmallLds& S = *(SmallLds*)s_raw;
+  const int tid = threadIdx.x, nth = blockDim.x;
+  const int T = a.T, k = a.k, TK = T * k, E = a.E, L = a.L;
+  if (tid == 0) S.bad = 0;
+  uint32_t bad = 0;
+  for (int s = tid; s < TK; s += nth) {
+    const int e = a.ids[s];
+    S.ids[s] = e;
+    if (e < -1 || e >= E) bad |= LX_DEVFLAG_BAD_ID;
+  }
+  __syncthreads();
+
+  for (int l = 0; l <= L; ++l) {
+    const BucketLevel& lv = a.lv[l];
+    const int N = lv.n_nodes;
+    for (int e = tid; e < E; e += nth) {
+      int n = e, at = l == L ? e : -1;
+      bool ok = true;
+      for (int q = L; q >= 1; --q) {
+        const int p = pa.parent[q][n];
+        if (p < 0 || p >= pa.n_nodes[q - 1]) {
+          ok = false;
+          break;
+        }
+        n = p;
+        if (q - 1 == l) at = n;
+      }
+      if (!ok) bad |= LX_DEVFLAG_BAD_TREE;
+      S.anc[e] = ok ? at : -1;
+    }
+    for (int n = tid; n < N; n += nth) {
+      S.mask[n] = 0ull;
+      int m = -1;
+      if (l > 0) {
+        m = pa.factor_of[l][n];
+        if (m < -1 || m >= pa.n_factors[l]) {
+          bad |= LX_DEVFLAG_BAD_TREE;
+          m = -1;
+        }
+      }
+      S.fac[n] = m;
+    }
+    __syncthreads();
+    for (int s = tid; s < TK; s += nth) {
+      const int e = S.ids[s];
+      const int n = e >= 0 && e < E ? S.anc[e] : -1;
+      S.node[s] = n;
+      if (n >= 0) atomicOr(&S.mask[n], 1ull << (s / k));
+    }
+    __syncthreads();
+    // node offsets: exclusive scan of the per-node token counts
+    const int nchunk = (N + nth - 1) / nth;
+    const int nb = tid * nchunk;
+    const int ne = nb + nchunk < N ? nb + nchunk : N;
+    int local = 0;
+    for (int n = nb; n < ne; ++n) local += __popcll(S.mask[n]);
+    int total = 0;
+    int run = block_exscan(local, S.wave, total);
+    for (int n = nb; n < ne; ++n) {
+      S.off[n] = run;
+      lv.hist[n] = run;
+      lv.offsets[n] = run;
+      run += __popcll(S.mask[n]);
+    }
+    if (tid == 0) {
+      S.off[N] = total;
+      lv.offsets[N] = total;
+    }
+    __syncthreads();
+    build_tile_tables(lv, S.off, S.fac, S.wave);
+    for (int s = tid; s < TK; s += nth) {
+      const int t = s / k, j = s - t * k;
+      const int n = S.node[s];
+      if (n < 0) {
+        lv.slot_row[s] = -1;
+        lv.slot_flags[s] = 0;
+        if (l == L && a.w) a.slot_wsum[s] = 0.f;
+        continue;
+      }
+      const int row = S.off[n] + __popcll(S.mask[n] & ((1ull << t) - 1ull));
+      lv.slot_row[s] = row;
+      bool first = true;
+      for (int j2 = 0; j2 < j; ++j2) first &= (S.node[t * k + j2] != n);
+      if (first) lv.row_token[row] = t;
+      const bool work = lv.work_all || S.fac[n] >= 0;
+      lv.slot_flags[s] = (uint8_t)((first ? 1 : 0) | (work ? 2 : 0));
+      // expert level: summed weight of each distinct expert, on its first slot
+      if (l == L && a.w) {
+        float ws = 0.f;
+        if (first)
+          for (int j2 = j; j2 < k; ++j2)
+            if (S.node[t * k + j2] == n) ws += a.w[(int64_t)t * k + j2];
+        a.slot_wsum[s] = ws;
+      }
+    }
+    __syncthreads();  // the LDS tables are rebuilt for the next level
+  }
+  if (bad) atomicOr(&S.bad, bad);
+  __syncthreads();
+  if (tid == 0) *a.flags = S.bad;
+}
+
 }  // namespace
 
 static size_t mask_lds_bytes(const BucketArgs& a) {
@@ -244,6 +384,18 @@ static size_t mask_lds_bytes(const BucketArgs& a) {
 
 hipError_t launch_prepare(const PrepareArgs& a, hipStream_t s) {
   hipLaunchKernelGGL(k_prepare, dim3(1), dim3(1024), 0, s, a);
+  return hipGetLastError();
+}
+
+bool bucket_small_ok(const BucketArgs& a) {
+  if (a.T < 1 || a.T > kTokTile || a.k > LX_MAX_K || a.E > kSmallMaxNodes) return false;
+  for (int l = 0; l <= a.L; ++l)
+    if (a.lv[l].n_nodes > kSmallMaxNodes) return false;
+  return true;
+}
+
+hipError_t launch_bucket_small(const PrepareArgs& pa, const BucketArgs& a, hipStream_t s) {
+  hipLaunchKernelGGL(k_bucket_small, dim3(1), dim3(1024), sizeof(SmallLds), s, pa, a);
   return hipGetLastError();
 }
 

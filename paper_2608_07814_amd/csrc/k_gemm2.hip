@@ -161,11 +161,17 @@ void k_gemm_big(GemmArgs p, int ntn) {
       bptr[j] = (n < p.ncols[0] ? Bw0 + (int64_t)n * Kb : Bw1 + (int64_t)(n - p.ncols[0]) * Kb) + c * 8;
     }
 
-#define LX_ISSUE(SA_, SB_, K0)                                                      \
+    // Slab kt covers A columns [ka, ka + 64) and weight columns [kb, kb + 64)
+    // with the K periods interleaved: slab kt = q * nper + per reads period
+    // per of weight slab q, so the periods that reuse one weight slab (hi and
+    // lo halves) run back to back and the second read hits in cache.
+    const int nper = K / Kb;
+#define LX_ISSUE(SA_, SB_, KT)                                                      \
   do {                                                                              \
-    const int kb_ = (K0) % Kb;                                                      \
+    const int q_ = (KT) / nper, per_ = (KT) - q_ * nper;                            \
+    const int kb_ = q_ * BK2, ka_ = per_ * Kb + kb_;                                \
     _Pragma("unroll") for (int j = 0; j < A_ROUNDS; ++j)                            \
-        load_lds16(Ab + (aoff[j] + (uint32_t)(K0)), &SA_[(j * NTHR2 + wave * 64) * 8]); \
+        load_lds16(Ab + (aoff[j] + (uint32_t)ka_), &SA_[(j * NTHR2 + wave * 64) * 8]); \
     _Pragma("unroll") for (int j = 0; j < B_ROUNDS; ++j)                            \
         load_lds16(bptr[j] + kb_, &SB_[(j * NTHR2 + wave * 64) * 8]);               \
   } while (0)
@@ -216,7 +222,7 @@ void k_gemm_big(GemmArgs p, int ntn) {
   } while (0)
 
     LX_ISSUE(sA0, sB0, 0);
-    if (nk > 1) LX_ISSUE(sA1, sB1, BK2);
+    if (nk > 1) LX_ISSUE(sA1, sB1, 1);
     int kt = 0;
     // Slabs kt (stage 0) and kt + 1 (stage 1) are in flight at the top of
     // every iteration; one loop exit keeps the accumulators in place.
@@ -226,7 +232,7 @@ void k_gemm_big(GemmArgs p, int ntn) {
       LX_COMPUTE(sA0, sB0);
       bar();
       const bool more0 = kt + 2 < nk;
-      if (more0) LX_ISSUE(sA0, sB0, (kt + 2) * BK2);
+      if (more0) LX_ISSUE(sA0, sB0, kt + 2);
       if (more0)
         wait_vmcnt<ROUNDS>();
       else
@@ -234,7 +240,7 @@ void k_gemm_big(GemmArgs p, int ntn) {
       bar();
       LX_COMPUTE(sA1, sB1);
       bar();
-      if (kt + 3 < nk) LX_ISSUE(sA1, sB1, (kt + 3) * BK2);
+      if (kt + 3 < nk) LX_ISSUE(sA1, sB1, kt + 3);
     }
     if (kt < nk) {  // odd slab count: the last slab is in stage 0
       wait_vmcnt<0>();
@@ -372,11 +378,14 @@ __global__ __launch_bounds__(SK_THR) void k_gemm_skinny(GemmArgs p, int ntn) {
     const int n = n0 + row < ncol ? n0 + row : ncol - 1;
     bptr[j] = (n < p.ncols[0] ? Bw0 + (int64_t)n * Kb : Bw1 + (int64_t)(n - p.ncols[0]) * Kb) + c * 8;
   }
-  auto issue = [&](int st, int k0) {
+  // slab kt: period kt % nper of weight slab kt / nper (as in k_gemm_big)
+  const int nper = K / Kb;
+  auto issue = [&](int st, int kt) {
     u16* const sA = smem + st * STAGE;
-    const int kb = k0 % Kb;
+    const int q = kt / nper, per = kt - q * nper;
+    const int kb = q * BK2, ka = per * Kb + kb;
 #pragma unroll
-    for (int j = 0; j < A_ROUNDS; ++j) load_lds16(Ab + (aoff[j] + (uint32_t)k0), sA + (j * SK_THR + wave * 64) * 8);
+    for (int j = 0; j < A_ROUNDS; ++j) load_lds16(Ab + (aoff[j] + (uint32_t)ka), sA + (j * SK_THR + wave * 64) * 8);
 #pragma unroll
     for (int j = 0; j < B_ROUNDS; ++j) load_lds16(bptr[j] + kb, sA + SA + (j * SK_THR + wave * 64) * 8);
   };
@@ -403,7 +412,7 @@ __global__ __launch_bounds__(SK_THR) void k_gemm_skinny(GemmArgs p, int ntn) {
   // barrier that follows slab kt's compute, stage kt % 4 is free and slab
   // kt + 4 goes there.
   const int npre = nk < SK_NST ? nk : SK_NST;
-  for (int i = 0; i < npre; ++i) issue(i, i * BK2);
+  for (int i = 0; i < npre; ++i) issue(i, i);
   wait_slabs<R>(npre - 1);
   bar();
   for (int kt = 0; kt < nk; ++kt) {
@@ -414,7 +423,7 @@ __global__ __launch_bounds__(SK_THR) void k_gemm_skinny(GemmArgs p, int ntn) {
       wait_slabs<R>(last - (kt + 1));
       wait_lgkm0();
       bar();
-      if (kt + SK_NST < nk) issue(kt & (SK_NST - 1), (kt + SK_NST) * BK2);
+      if (kt + SK_NST < nk) issue(kt & (SK_NST - 1), kt + SK_NST);
     }
   }
   wait_lgkm0();

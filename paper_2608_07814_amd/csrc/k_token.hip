@@ -1,19 +1,20 @@
 // Per-token kernels: SwiGLU with the amortized weighted reduction, and the
-// deterministic combine. One workgroup per token; every thread owns 4
-// consecutive neurons (SwiGLU) or output columns (combine), so all accesses
-// are 16-byte vectors.
+// deterministic combine. One 64-thread workgroup per (token, 256-column
+// chunk); every thread owns 4 consecutive neurons (SwiGLU) or output columns
+// (combine), so all accesses are 16-byte vectors and small batches still
+// spread over many workgroups.
 //
 // For a token t with selected experts e_j (j ascending), every tree level l
 // has one row per distinct level-l node among the e_j (from the bucketing,
 // which also marks each slot's first-of-row and has-work bits and stores each
 // distinct expert's summed routing weight on its first slot).
-//   swiglu_reduce: for each anchor row of t, for each distinct expert under it
+//   swiglu_reduce: for each distinct expert of t
 //       g = anchor gate row + sum over levels of the node's gate correction,
 //       u likewise, h = w * silu(g) * u;
-//     h is summed in registers into the anchor row's hbar0 (one write per
-//     row) and accumulated into hbar_l[row_l] of every correction level whose
-//     node carries a factor. By linearity the down projections then run once
-//     per row (Sec. 5.1 amortized forward).
+//     every level-l row of t then gets hbar_l[row] = sum of the h of the
+//     experts under it, in slot order (the anchor level always, correction
+//     levels where the node carries a factor). By linearity the down
+//     projections then run once per row (Sec. 5.1 amortized forward).
 //   combine: out[t] = sum over levels, over t's rows of the level, of that
 //     level's down-projection output row, in a fixed order (level, then slot)
 //     with no atomics, so the result is bit-reproducible.
@@ -71,81 +72,96 @@ __device__ __forceinline__ void hbar_store(void* base, bool hilo, int row, int c
     *(float4*)((float*)base + (int64_t)row * f + c) = v;
   }
 }
-__device__ __forceinline__ float4 hbar_load(const void* base, bool hilo, int row, int c, int f) {
-  if (hilo) {
-    const __bf16* hb = (const __bf16*)base + (int64_t)row * 2 * f;
-    const bf16x4 hi = *(const bf16x4*)(hb + c);
-    const bf16x4 lo = *(const bf16x4*)(hb + f + c);
-    return make_float4((float)hi[0] + (float)lo[0], (float)hi[1] + (float)lo[1],
-                       (float)hi[2] + (float)lo[2], (float)hi[3] + (float)lo[3]);
-  }
-  return ld4((const float*)base + (int64_t)row * f + c);
-}
+constexpr int kTokThr = 64, kTokCols = 4 * kTokThr;
+constexpr int kSlotGroups = 16;  // SwiGLU: up to 16 slots processed side by side
 
-__global__ __launch_bounds__(256) void k_swiglu_reduce(TokenArgs a) {
+// Phase 1: every distinct expert of token t (first slot of its leaf row)
+// gets h = w * silu(g) * u for this thread's 4 neurons, one slot group per
+// slot, all loads in flight together; h goes to LDS. Phase 2: each row of
+// each level is summed in slot order by the thread group of its first slot
+// and stored once (no read-modify-write of the sums in memory).
+__global__ __launch_bounds__(kTokThr * kSlotGroups) void k_swiglu_reduce(TokenArgs a) {
   __shared__ TokenMeta m;
+  extern __shared__ float4 s_h[];  // [k][kTokThr]
   const int t = blockIdx.x;
   token_meta(a, t, m);
   __syncthreads();
   const int k = a.k, L = a.L, f = a.f;
   const int64_t ld = 2 * (int64_t)f;
-  for (int c = threadIdx.x * 4; c < f; c += blockDim.x * 4) {
-    for (int j0 = 0; j0 < k; ++j0) {
-      if (!(m.fl[0][j0] & 1)) continue;  // start of an anchor row of t
-      const int r0 = m.row[0][j0];
-      const float* g0 = a.gu0 + r0 * ld;
-      const float4 gb = ld4(g0 + c), ub = ld4(g0 + f + c);
+  const int lane = threadIdx.x % kTokThr, sg = threadIdx.x / kTokThr;
+  const int nsg = blockDim.x / kTokThr;
+  const int c = (blockIdx.y * kTokThr + lane) * 4;
+  const bool colok = c < f;
+  for (int j = sg; j < k && colok; j += nsg) {
+    if (!(m.fl[L][j] & 1)) continue;  // not the first slot of a valid expert
+    const float* g0 = a.gu0 + m.row[0][j] * ld;
+    float4 g = ld4(g0 + c), u = ld4(g0 + f + c);
+    for (int l = 1; l <= L; ++l) {
+      if (!(m.fl[l][j] & 2)) continue;
+      const float* dg = a.dgu[l] + m.row[l][j] * ld;
+      add4(g, ld4(dg + c));
+      add4(u, ld4(dg + f + c));
+    }
+    const float w = m.w[j];
+    s_h[j * kTokThr + lane] = make_float4(w * silu_mul(g.x, u.x), w * silu_mul(g.y, u.y),
+                                          w * silu_mul(g.z, u.z), w * silu_mul(g.w, u.w));
+  }
+  __syncthreads();
+  if (!colok) return;
+  for (int j0 = sg; j0 < k; j0 += nsg) {
+    for (int l = 0; l <= L; ++l) {
+      const unsigned char fl0 = m.fl[l][j0];
+      if ((fl0 & 3) != 3) continue;  // j0 starts a level-l row that does work
+      const int r = m.row[l][j0];
       float4 hs = make_float4(0.f, 0.f, 0.f, 0.f);
-      for (int j = j0; j < k; ++j) {
-        // the row's distinct experts: same anchor row, first slot of the expert
-        if (m.row[0][j] != r0 || !(m.fl[L][j] & 1)) continue;
-        float4 g = gb, u = ub;
-        for (int l = 1; l <= L; ++l) {
-          if (!(m.fl[l][j] & 2)) continue;
-          const float* dg = a.dgu[l] + m.row[l][j] * ld;
-          add4(g, ld4(dg + c));
-          add4(u, ld4(dg + f + c));
-        }
-        const float w = m.w[j];
-        const float4 h = make_float4(w * silu_mul(g.x, u.x), w * silu_mul(g.y, u.y),
-                                     w * silu_mul(g.z, u.z), w * silu_mul(g.w, u.w));
-        add4(hs, h);
-        for (int l = 1; l <= L; ++l) {
-          const unsigned char fl = m.fl[l][j];
-          if (!(fl & 2)) continue;
-          float4 v = h;
-          if (!(fl & 1)) add4(v, hbar_load(a.hbar[l], a.hbar_hilo[l], m.row[l][j], c, f));
-          hbar_store(a.hbar[l], a.hbar_hilo[l], m.row[l][j], c, f, v);
-        }
-      }
-      hbar_store(a.hbar[0], a.hbar_hilo[0], r0, c, f, hs);
+      for (int j = j0; j < k; ++j)
+        if (m.row[l][j] == r && (m.fl[L][j] & 1)) add4(hs, s_h[j * kTokThr + lane]);
+      hbar_store(a.hbar[l], a.hbar_hilo[l], r, c, f, hs);
     }
   }
 }
 
-__global__ __launch_bounds__(256) void k_combine(TokenArgs a) {
+// Combine: the token's rows to sum (first slot of a row that does work), in
+// (level, slot) order, are listed once; each thread then loads 8 rows at a
+// time before adding them in that order.
+__global__ __launch_bounds__(kTokThr) void k_combine(TokenArgs a) {
   __shared__ TokenMeta m;
+  __shared__ const float* s_rows[kMaxLvl * LX_MAX_K];
+  __shared__ int s_n;
   const int t = blockIdx.x;
   token_meta(a, t, m);
   __syncthreads();
   const int k = a.k, L = a.L, d = a.d;
-  for (int c = threadIdx.x * 4; c < d; c += blockDim.x * 4) {
-    float4 acc = make_float4(0.f, 0.f, 0.f, 0.f);
+  if (threadIdx.x == 0) {
+    int n = 0;
     for (int l = 0; l <= L; ++l)
-      for (int j = 0; j < k; ++j) {
-        if ((m.fl[l][j] & 3) != 3) continue;  // first slot of a row that does work
-        add4(acc, ld4(a.y[l] + (int64_t)m.row[l][j] * d + c));
-      }
-    if (a.out_dtype == LX_F32) {
-      *(float4*)((float*)a.out + (int64_t)t * d + c) = acc;
-    } else {
-      bf16x4 o;
-      o[0] = (__bf16)acc.x;
-      o[1] = (__bf16)acc.y;
-      o[2] = (__bf16)acc.z;
-      o[3] = (__bf16)acc.w;
-      *(bf16x4*)((uint16_t*)a.out + (int64_t)t * d + c) = o;
-    }
+      for (int j = 0; j < k; ++j)
+        if ((m.fl[l][j] & 3) == 3) s_rows[n++] = a.y[l] + (int64_t)m.row[l][j] * d;
+    s_n = n;
+  }
+  __syncthreads();
+  const int c = (blockIdx.y * blockDim.x + threadIdx.x) * 4;
+  if (c >= d) return;
+  const int n = s_n;
+  float4 acc = make_float4(0.f, 0.f, 0.f, 0.f);
+  for (int b = 0; b < n; b += 8) {
+    float4 v[8];
+#pragma unroll
+    for (int i = 0; i < 8; ++i)
+      if (b + i < n) v[i] = ld4(s_rows[b + i] + c);
+#pragma unroll
+    for (int i = 0; i < 8; ++i)
+      if (b + i < n) add4(acc, v[i]);
+  }
+  if (a.out_dtype == LX_F32) {
+    *(float4*)((float*)a.out + (int64_t)t * d + c) = acc;
+  } else {
+    bf16x4 o;
+    o[0] = (__bf16)acc.x;
+    o[1] = (__bf16)acc.y;
+    o[2] = (__bf16)acc.z;
+    o[3] = (__bf16)acc.w;
+    *(bf16x4*)((uint16_t*)a.out + (int64_t)t * d + c) = o;
   }
 }
 
@@ -153,15 +169,15 @@ __global__ __launch_bounds__(256) void k_combine(TokenArgs a) {
 
 hipError_t launch_swiglu_reduce(const TokenArgs& a, hipStream_t s) {
   if (a.T == 0) return hipSuccess;
-  const int threads = a.f / 4 >= 256 ? 256 : ((a.f / 4 + 63) / 64) * 64;
-  hipLaunchKernelGGL(k_swiglu_reduce, dim3(a.T), dim3(threads), 0, s, a);
+  const int groups = a.k < kSlotGroups ? a.k : kSlotGroups;
+  hipLaunchKernelGGL(k_swiglu_reduce, dim3(a.T, (a.f + kTokCols - 1) / kTokCols), dim3(kTokThr * groups),
+                     (size_t)a.k * kTokThr * sizeof(float4), s, a);
   return hipGetLastError();
 }
 
 hipError_t launch_combine(const TokenArgs& a, hipStream_t s) {
   if (a.T == 0) return hipSuccess;
-  const int threads = a.d / 4 >= 256 ? 256 : ((a.d / 4 + 63) / 64) * 64;
-  hipLaunchKernelGGL(k_combine, dim3(a.T), dim3(threads), 0, s, a);
+  hipLaunchKernelGGL(k_combine, dim3(a.T, (a.d + kTokCols - 1) / kTokCols), dim3(kTokThr), 0, s, a);
   return hipGetLastError();
 }
 

@@ -68,6 +68,9 @@ hipError_t launch_prepare(const PrepareArgs& a, hipStream_t s);
 hipError_t launch_bucket_hist(const BucketArgs& a, hipStream_t s);
 hipError_t launch_bucket_scan(const BucketArgs& a, hipStream_t s);
 hipError_t launch_bucket_place(const BucketArgs& a, hipStream_t s);
+// Batches of 1..64 tokens: prepare + hist + scan + place in one workgroup.
+bool bucket_small_ok(const BucketArgs& a);
+hipError_t launch_bucket_small(const PrepareArgs& pa, const BucketArgs& a, hipStream_t s);
 
 // ---------------------------------------------------------------- GEMM
 // C[row, coloff[p] + n] = sum_k A[arow(row), akoff[p] + k] * B_p[widx][n][k]

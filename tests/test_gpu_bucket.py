@@ -40,23 +40,36 @@ def test_bucket_configs(cfg, T):
     _check(p.layer, p.routing.topk_ids)
 
 
+# Batches of at most 64 tokens take the single-workgroup path, larger ones
+# the four-pass path; the "small_" cases cover the former.
 @pytest.mark.parametrize("case", ["dupes_drops_bad", "all_dropped", "one_hot_expert", "T1", "ragged",
-                                  "shuffled", "dense"])
+                                  "shuffled", "dense", "small_dupes_drops_bad", "small_all_dropped",
+                                  "small_one_hot_expert", "small_tree", "small_k32"])
 def test_bucket_adversarial(case):
     say(f"bucket adversarial {case}")
     flag = 0
+    small = case.startswith("small_")
+    if small:
+        case = case[len("small_"):]
     if case == "dupes_drops_bad":
         layer = tiny_flat(E=12, C=3)
-        ids, _ = random_routing(150, 6, 12, 9, allow_dupes=True, drop_frac=0.2, bad_frac=0.05)
+        ids, _ = random_routing(50 if small else 150, 6, 12, 9, allow_dupes=True, drop_frac=0.2, bad_frac=0.05)
         flag = lx.LX_DEVFLAG_BAD_ID
     elif case == "all_dropped":
         layer = tiny_flat(E=12, C=3)
-        ids = np.full((70, 4), -1, np.int32)
+        ids = np.full((40 if small else 70, 4), -1, np.int32)
     elif case == "one_hot_expert":
         layer = tiny_flat(E=12, C=3)
-        ids = np.full((300, 3), 7, np.int32)
+        T = 64 if small else 300
+        ids = np.full((T, 3), 7, np.int32)
         ids[:, 1] = 2
         ids[::3, 2] = -1
+    elif case == "tree":
+        layer = tiny_tree(E=16, n_roots=2, subs=2)
+        ids, _ = random_routing(33, 5, 16, 13, allow_dupes=True, drop_frac=0.1)
+    elif case == "k32":
+        layer = tiny_flat(E=40, C=8, shuffle=True)
+        ids, _ = random_routing(64, 32, 40, 14, allow_dupes=True)
     elif case == "T1":
         layer = tiny_tree(E=16, n_roots=2, subs=2)
         ids = np.array([[3, 15, 4, 3]], np.int32)

@@ -71,6 +71,19 @@ def test_cfg2_decode_full():
     assert e <= TOL_DESIGN
 
 
+def test_decode_shape_duplicates_and_drops():
+    """Decode-sized batch on fast levels (skinny GEMMs, single-workgroup
+    bucketing) with duplicate and dropped slots."""
+    require_gpu()
+    say("forward decode dupes/drops")
+    layer = make_layer_flat(32, 4, 256, 192, 64, "bf16", 21)
+    p = _tiny_problem(layer, 48, 8, 22, allow_dupes=True, drop_frac=0.15)
+    e = err_ratio(gpu_forward(p), _oracle(p))
+    say(f"  err/RMS = {e:.3e}")
+    assert e <= TOL_BF16
+    assert e <= TOL_DESIGN
+
+
 def test_cfg3_community():
     require_gpu()
     say("forward cfg3 T=300")
@@ -129,12 +142,13 @@ def _tiny_problem(layer, T, k, seed, dtype=None, **kw):
     return Problem(cfg={}, seed=seed, layer=layer, x=x, routing=Routing(ids, w))
 
 
-@pytest.mark.parametrize("dtype", ["f32", "bf16"])
-def test_dropped_duplicate_and_bad_ids(dtype):
+@pytest.mark.parametrize("dtype,T", [("f32", 77), ("bf16", 77), ("bf16", 40)])
+def test_dropped_duplicate_and_bad_ids(dtype, T):
+    """T=40 takes the single-workgroup bucketing, T=77 the four-pass one."""
     require_gpu()
-    say(f"edge ids {dtype}")
+    say(f"edge ids {dtype} T={T}")
     layer = make_layer_flat(12, 3, 64, 96, 16, dtype, 5)
-    p = _tiny_problem(layer, 77, 5, 3, allow_dupes=True, drop_frac=0.2, bad_frac=0.05)
+    p = _tiny_problem(layer, T, 5, 3, allow_dupes=True, drop_frac=0.2, bad_frac=0.05)
     got, ws = gpu_forward(p, return_ws=True)
     ref, flag = O.moe_forward(p.layer, p.x, p.routing.topk_ids, p.routing.topk_weights,
                               return_flag=True)
