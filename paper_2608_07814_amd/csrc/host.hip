@@ -348,6 +348,28 @@ lx_status run(const lx_tree_layer& t, int T, int k, const void* x, const int32_t
     return LX_OK;
   }
 
+  const lx_dtype dt = t.dtype;
+  const int64_t two31 = (int64_t)1 << 31;
+  // "Fast" levels keep every GEMM-feeding intermediate as a bf16 (hi, lo)
+  // pair and run all their GEMMs on the large-tile or skinny kernel; other
+  // levels use fp32 intermediates and the register-staged kernel (hi/lo
+  // split on load).
+  bool fast[kMaxLvl] = {};
+  fast[0] = dt == LX_BF16 && d % 64 == 0 && f % 64 == 0 && (int64_t)T * d < two31 &&
+            P.lv[0].rows_max * 2 * f < two31;
+  for (int l = 1; l <= L; ++l) {
+    const int r = t.levels[l - 1].rank;
+    const int64_t R = P.lv[l].rows_max;
+    // rank multiple of 64: every 64-wide K-slab of a (hi | lo) operand lies
+    // inside one half, so its weight columns stay inside the weight row
+    fast[l] = fast[0] && r % 64 == 0 && R * 2 * f < two31 && R * 4 * r < two31;
+  }
+  // Fast levels with few rows per node (decode-sized batches) stream their
+  // weights through the skinny kernel; the large tiles would spend their
+  // time on MFMA work over padding rows.
+  bool skinny[kMaxLvl] = {};
+  for (int l = 0; l <= L; ++l) skinny[l] = fast[l] && P.lv[l].rows_max / std::max(P.lv[l].N, 1) <= 64;
+
   BucketArgs ba{};
   ba.T = T;
   ba.k = k;
@@ -364,6 +386,9 @@ lx_status run(const lx_tree_layer& t, int T, int k, const void* x, const int32_t
     BucketLevel& b = ba.lv[l];
     b.n_nodes = q.N;
     for (int i = 0; i < kNumTab; ++i) b.tile_bm[i] = q.bm[i];
+    // skinny levels use only the skinny table; others the register-staged
+    // (also 128-row large-tile) and 256-row tables
+    b.tab_mask = skinny[l] ? 1u << kTabSkinny : (1u << kTabSmall) | (1u << kTabBig);
     b.work_all = l == 0;
     b.fac = l > 0 ? (const int32_t*)(W + q.fac) : nullptr;
     b.hist = (int32_t*)(W + q.hist);
@@ -386,32 +411,13 @@ lx_status run(const lx_tree_layer& t, int T, int k, const void* x, const int32_t
   }
   if (stop == RUN_BUCKET) return LX_OK;
 
-  const lx_dtype dt = t.dtype;
-  const int64_t two31 = (int64_t)1 << 31;
-
-  // "Fast" levels keep every GEMM-feeding intermediate as a bf16 (hi, lo)
-  // pair and run all their GEMMs on the large-tile kernel; other levels use
-  // fp32 intermediates and the register-staged kernel (hi/lo split on load).
-  bool fast[kMaxLvl] = {};
-  fast[0] = dt == LX_BF16 && d % 64 == 0 && f % 64 == 0 && (int64_t)T * d < two31 &&
-            P.lv[0].rows_max * 2 * f < two31;
-  for (int l = 1; l <= L; ++l) {
-    const int r = t.levels[l - 1].rank;
-    const int64_t R = P.lv[l].rows_max;
-    // rank multiple of 64: every 64-wide K-slab of a (hi | lo) operand lies
-    // inside one half, so its weight columns stay inside the weight row
-    fast[l] = fast[0] && r % 64 == 0 && R * 2 * f < two31 && R * 4 * r < two31;
-  }
-  // Levels with few rows per node (decode-sized batches) stream their
-  // weights through the skinny kernel; the large tiles would spend their
-  // time on MFMA work over padding rows.
-  bool skinny[kMaxLvl] = {};
-  for (int l = 0; l <= L; ++l) skinny[l] = P.lv[l].rows_max / std::max(P.lv[l].N, 1) <= 64;
   auto big = [&](const char* name, GemmArgs g, int l, int bm, int bn, bool hilo,
                  int64_t a_rows_total) -> lx_status {
     const LevelPlan& q = P.lv[l];
     if (!g.B[1]) g.B[1] = g.B[0];
-    if (skinny[l] && gemm_big_ok(g, kSkinnyBN, a_rows_total)) {
+    if (skinny[l]) {
+      if (!gemm_big_ok(g, kSkinnyBN, a_rows_total))
+        return fail(LX_ERR_UNSUPPORTED, std::string(name) + ": shape not supported by the skinny GEMM");
       g.tiles = ba.lv[l].tiles[kTabSkinny];
       g.n_tiles = ba.lv[l].n_tiles[kTabSkinny];
       LX_LAUNCH(name, launch_gemm_skinny(g, hilo, (int)q.tiles_max[kTabSkinny], lstream));

@@ -20,7 +20,9 @@
 namespace lx {
 namespace {
 
-constexpr int kSmallMaxNodes = 2048;  // single-workgroup path: nodes and experts per level
+// single-workgroup path: nodes (and experts) per level, and tree nodes in all
+// correction levels together
+constexpr int kSmallMaxNodes = 1024, kSmallMaxTree = 1024;
 
 // Ancestors of every expert at every level and validated factor indices.
 // Single workgroup: it also zeroes the status word before anything else runs.
@@ -150,6 +152,7 @@ __device__ inline void build_tile_tables(const BucketLevel& lv, const int32_t* o
   const int nb = tid * nchunk;
   const int ne = nb + nchunk < N ? nb + nchunk : N;
   for (int tab = 0; tab < kNumTab; ++tab) {
+    if (!((lv.tab_mask >> tab) & 1u)) continue;  // uniform across the workgroup
     const int bm = lv.tile_bm[tab];
     TileEntry* tiles = lv.tiles[tab];
     int my_tiles = 0;
@@ -252,61 +255,107 @@ __global__ __launch_bounds__(64) void k_bucket_place(BucketArgs a) {
   }
 }
 
-// Whole bucketing of a batch of at most 64 tokens in one workgroup, with
-// every table it consults kept in LDS: per level the node of each expert
-// (walking the parent arrays to the root, so a broken path invalidates the
-// expert at every level, as in k_prepare) and the validated factor indices;
-// then one 64-bit token mask per node (the batch is one token tile), node
-// offsets, tile tables and slot placement, one thread per routing slot. Same
-// results as the four-pass path with one token tile.
+// Whole bucketing of a batch of at most 64 tokens in one workgroup. All
+// global inputs are read into LDS once; then per level three phases, each
+// ended by one barrier:
+//   A  every thread: the node of each routing slot (walking the parent
+//      arrays to the root, so a broken path invalidates the expert at every
+//      level, as in k_prepare), one 64-bit token mask per node (the batch is
+//      one token tile), validated factor indices;
+//   B  wavefront 0 alone (no barriers): node offsets and the tile tables by
+//      wavefront-wide scans;
+//   C  every thread: slot placement, one thread per routing slot.
+// Same results as the four-pass path with one token tile.
 struct SmallLds {
-  unsigned long long mask[kSmallMaxNodes];
+  unsigned long long mask[2][kSmallMaxNodes];  // alternate levels
   int32_t off[kSmallMaxNodes + 1];
   int32_t fac[kSmallMaxNodes];
-  int32_t anc[kSmallMaxNodes];  // node of each expert at the current level
+  int32_t par[kSmallMaxTree];   // parent arrays of levels 1..L, concatenated
+  int32_t fo[kSmallMaxTree];    // factor_of arrays of levels 1..L, concatenated
   int32_t node[kTokTile * LX_MAX_K];
   int32_t ids[kTokTile * LX_MAX_K];
-  int wave[64];
+  float w[kTokTile * LX_MAX_K];
+  int32_t base[kMaxLvl];        // offset of level l's arrays in par / fo
   uint32_t bad;
 };
+
+// Node of expert e at level l, or -1 (invalid id or broken path to the root).
+__device__ inline int small_node(const SmallLds& S, const PrepareArgs& pa, int L, int E, int e, int l) {
+  if (e < 0 || e >= E) return -1;
+  int n = e, at = l == L ? e : -1;
+  for (int q = L; q >= 1; --q) {
+    const int p = S.par[S.base[q] + n];
+    if (p < 0 || p >= pa.n_nodes[q - 1]) return -1;
+    n = p;
+    if (q - 1 == l) at = n;
+  }
+  return at;
+}
+
+// Workgroup barrier for LDS communication only: waits for this wave's LDS
+// operations, not for its global stores (which nothing in the workgroup
+// reads back), unlike __syncthreads().
+__device__ __forceinline__ void lds_barrier() {
+  asm volatile("" ::: "memory");
+  __builtin_amdgcn_s_waitcnt(0xF | (0x7 << 4) | (0x3 << 14));  // lgkmcnt(0)
+  __builtin_amdgcn_s_barrier();
+  asm volatile("" ::: "memory");
+}
+
+__device__ inline int wave_exscan(int v, int& total) {
+  const int lane = threadIdx.x & 63;
+  int incl = v;
+  for (int o = 1; o < 64; o <<= 1) {
+    const int u = __shfl_up(incl, o, 64);
+    if (lane >= o) incl += u;
+  }
+  total = __shfl(incl, 63, 64);
+  return incl - v;
+}
 
 __global__ __launch_bounds__(1024) void k_bucket_small(PrepareArgs pa, BucketArgs a) {
   extern __shared__ __attribute__((aligned(16))) unsigned char s_raw[];
   SmallLds& S = *(SmallLds*)s_raw;
   const int tid = threadIdx.x, nth = blockDim.x;
   const int T = a.T, k = a.k, TK = T * k, E = a.E, L = a.L;
-  if (tid == 0) S.bad = 0;
+  if (tid == 0) {
+    S.bad = 0;
+    int o = 0;
+    for (int l = 1; l <= L; ++l) {
+      S.base[l] = o;
+      o += pa.n_nodes[l];
+    }
+  }
+  lds_barrier();
   uint32_t bad = 0;
   for (int s = tid; s < TK; s += nth) {
     const int e = a.ids[s];
     S.ids[s] = e;
+    S.w[s] = a.w ? a.w[s] : 0.f;
     if (e < -1 || e >= E) bad |= LX_DEVFLAG_BAD_ID;
   }
-  __syncthreads();
+  for (int l = 1; l <= L; ++l)
+    for (int n = tid; n < pa.n_nodes[l]; n += nth) {
+      S.par[S.base[l] + n] = pa.parent[l][n];
+      S.fo[S.base[l] + n] = pa.factor_of[l][n];
+    }
+  for (int n = tid; n < a.lv[0].n_nodes; n += nth) S.mask[0][n] = 0ull;
+  lds_barrier();
 
   for (int l = 0; l <= L; ++l) {
     const BucketLevel& lv = a.lv[l];
     const int N = lv.n_nodes;
-    for (int e = tid; e < E; e += nth) {
-      int n = e, at = l == L ? e : -1;
-      bool ok = true;
-      for (int q = L; q >= 1; --q) {
-        const int p = pa.parent[q][n];
-        if (p < 0 || p >= pa.n_nodes[q - 1]) {
-          ok = false;
-          break;
-        }
-        n = p;
-        if (q - 1 == l) at = n;
-      }
-      if (!ok) bad |= LX_DEVFLAG_BAD_TREE;
-      S.anc[e] = ok ? at : -1;
+    unsigned long long* const mask = S.mask[l & 1];
+    // A
+    for (int s = tid; s < TK; s += nth) {
+      const int n = small_node(S, pa, L, E, S.ids[s], l);
+      S.node[s] = n;
+      if (n >= 0) atomicOr(&mask[n], 1ull << (s / k));
     }
     for (int n = tid; n < N; n += nth) {
-      S.mask[n] = 0ull;
       int m = -1;
       if (l > 0) {
-        m = pa.factor_of[l][n];
+        m = S.fo[S.base[l] + n];
         if (m < -1 || m >= pa.n_factors[l]) {
           bad |= LX_DEVFLAG_BAD_TREE;
           m = -1;
@@ -314,34 +363,62 @@ __global__ __launch_bounds__(1024) void k_bucket_small(PrepareArgs pa, BucketArg
       }
       S.fac[n] = m;
     }
-    __syncthreads();
-    for (int s = tid; s < TK; s += nth) {
-      const int e = S.ids[s];
-      const int n = e >= 0 && e < E ? S.anc[e] : -1;
-      S.node[s] = n;
-      if (n >= 0) atomicOr(&S.mask[n], 1ull << (s / k));
+    if (l == 0)  // tree check of every expert, routed or not
+      for (int e = tid; e < E; e += nth)
+        if (L > 0 && small_node(S, pa, L, E, e, 0) < 0) bad |= LX_DEVFLAG_BAD_TREE;
+    lds_barrier();
+    // B
+    if (tid < 64) {
+      const int per = (N + 63) / 64;
+      const int nb = tid * per, ne = nb + per < N ? nb + per : N;
+      int local = 0;
+      for (int n = nb; n < ne; ++n) local += __popcll(mask[n]);
+      int total = 0;
+      int run = wave_exscan(local, total);
+      for (int n = nb; n < ne; ++n) {
+        S.off[n] = run;
+        lv.hist[n] = run;
+        lv.offsets[n] = run;
+        run += __popcll(mask[n]);
+      }
+      if (tid == 0) {
+        S.off[N] = total;
+        lv.offsets[N] = total;
+      }
+      // S.off[ne] is read below but written by the next lane: keep the
+      // compiler from hoisting reads above the writes (a wavefront's LDS
+      // accesses execute in program order)
+      asm volatile("" ::: "memory");
+      __builtin_amdgcn_wave_barrier();
+      asm volatile("" ::: "memory");
+      for (int tab = 0; tab < kNumTab; ++tab) {
+        if (!((lv.tab_mask >> tab) & 1u)) continue;
+        const int bm = lv.tile_bm[tab];
+        int mine = 0;
+        for (int n = nb; n < ne; ++n) {
+          const int cnt = S.off[n + 1] - S.off[n];
+          if ((lv.work_all || S.fac[n] >= 0) && cnt > 0) mine += (cnt + bm - 1) / bm;
+        }
+        int ntiles = 0;
+        int tpos = wave_exscan(mine, ntiles);
+        for (int n = nb; n < ne; ++n) {
+          const int o = S.off[n], cnt = S.off[n + 1] - o;
+          if (!(lv.work_all || S.fac[n] >= 0) || cnt == 0) continue;
+          const int widx = lv.work_all ? n : S.fac[n];
+          for (int r = 0; r < cnt; r += bm) {
+            TileEntry te;
+            te.widx = widx;
+            te.row0 = o + r;
+            te.nrows = cnt - r < bm ? cnt - r : bm;
+            te.node = n;
+            lv.tiles[tab][tpos++] = te;
+          }
+        }
+        if (tid == 0) *lv.n_tiles[tab] = ntiles;
+      }
     }
-    __syncthreads();
-    // node offsets: exclusive scan of the per-node token counts
-    const int nchunk = (N + nth - 1) / nth;
-    const int nb = tid * nchunk;
-    const int ne = nb + nchunk < N ? nb + nchunk : N;
-    int local = 0;
-    for (int n = nb; n < ne; ++n) local += __popcll(S.mask[n]);
-    int total = 0;
-    int run = block_exscan(local, S.wave, total);
-    for (int n = nb; n < ne; ++n) {
-      S.off[n] = run;
-      lv.hist[n] = run;
-      lv.offsets[n] = run;
-      run += __popcll(S.mask[n]);
-    }
-    if (tid == 0) {
-      S.off[N] = total;
-      lv.offsets[N] = total;
-    }
-    __syncthreads();
-    build_tile_tables(lv, S.off, S.fac, S.wave);
+    lds_barrier();
+    // C
     for (int s = tid; s < TK; s += nth) {
       const int t = s / k, j = s - t * k;
       const int n = S.node[s];
@@ -351,7 +428,7 @@ __global__ __launch_bounds__(1024) void k_bucket_small(PrepareArgs pa, BucketArg
         if (l == L && a.w) a.slot_wsum[s] = 0.f;
         continue;
       }
-      const int row = S.off[n] + __popcll(S.mask[n] & ((1ull << t) - 1ull));
+      const int row = S.off[n] + __popcll(mask[n] & ((1ull << t) - 1ull));
       lv.slot_row[s] = row;
       bool first = true;
       for (int j2 = 0; j2 < j; ++j2) first &= (S.node[t * k + j2] != n);
@@ -363,14 +440,16 @@ __global__ __launch_bounds__(1024) void k_bucket_small(PrepareArgs pa, BucketArg
         float ws = 0.f;
         if (first)
           for (int j2 = j; j2 < k; ++j2)
-            if (S.node[t * k + j2] == n) ws += a.w[(int64_t)t * k + j2];
+            if (S.node[t * k + j2] == n) ws += S.w[t * k + j2];
         a.slot_wsum[s] = ws;
       }
     }
-    __syncthreads();  // the LDS tables are rebuilt for the next level
+    if (l < L)  // the next level's mask buffer (last read two phases ago)
+      for (int n = tid; n < a.lv[l + 1].n_nodes; n += nth) S.mask[(l + 1) & 1][n] = 0ull;
+    lds_barrier();
   }
   if (bad) atomicOr(&S.bad, bad);
-  __syncthreads();
+  lds_barrier();
   if (tid == 0) *a.flags = S.bad;
 }
 
@@ -389,9 +468,12 @@ hipError_t launch_prepare(const PrepareArgs& a, hipStream_t s) {
 
 bool bucket_small_ok(const BucketArgs& a) {
   if (a.T < 1 || a.T > kTokTile || a.k > LX_MAX_K || a.E > kSmallMaxNodes) return false;
-  for (int l = 0; l <= a.L; ++l)
+  int tree = 0;
+  for (int l = 0; l <= a.L; ++l) {
     if (a.lv[l].n_nodes > kSmallMaxNodes) return false;
-  return true;
+    if (l > 0) tree += a.lv[l].n_nodes;
+  }
+  return tree <= kSmallMaxTree;
 }
 
 hipError_t launch_bucket_small(const PrepareArgs& pa, const BucketArgs& a, hipStream_t s) {

@@ -29,6 +29,7 @@ constexpr int kTabSmall = 0, kTabBig = 1, kTabSkinny = 2, kNumTab = 3;
 struct BucketLevel {
   int32_t n_nodes;
   int32_t tile_bm[kNumTab];  // tile height of each table
+  uint32_t tab_mask;         // bit b: table b is needed (built) at this level
   int32_t work_all;        // 1: every node does GEMM work (anchor level)
   const int32_t* fac;      // validated factor index per node (-1 none)
   int32_t* hist;           // [n_nodes][n_tok_tiles], scanned in place
