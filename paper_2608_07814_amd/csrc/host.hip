@@ -1,14 +1,16 @@
 // Host side of the C ABI: argument validation, workspace planning, and the
 // launch sequence of one forward (everything is enqueued on the caller's
-// stream; the host never waits on the device).
+// stream, with the correction chains of large batches forked onto an
+// auxiliary stream and joined back; the host never waits on the device).
 //
 // Launch sequence for a tree with L correction levels (a flat LorExperts
 // layer is L = 1, the dense comparator L = 0):
-//   prepare                ancestors per level, validated factor indices
-//   bucket hist/scan/place unique (token, node) rows per level, tile tables
-//   level 0 gate|up GEMM   X[rows0] * [G_a; U_a]^T, once per (token, anchor)
+//   bucketing              unique (token, node) rows per level, slot flags,
+//                          tile tables (one kernel for <= 64 tokens, else
+//                          prepare / hist / scan / place)
 //   per level l >= 1       z = X[rows_l] * [B_gate; B_up]^T, dgu = z * [A_gate; A_up]^T
-//   swiglu_reduce          h = silu(g) * u per distinct expert, weighted sums per row
+//   level 0 gate|up GEMM   X[rows0] * [G_a; U_a]^T, once per (token, anchor)
+//   swiglu_reduce          h = w * silu(g) * u per distinct expert, sums per row
 //   level 0 down GEMM      hbar0 * D_a^T, once per (token, anchor)
 //   per level l >= 1       v = hbar_l * B_down^T, y_l = v * A_down^T
 //   combine                out[t] = sum of the token's rows over all levels
