@@ -5,7 +5,9 @@ Default workload: the flat LorExperts layer at 30B-A3B-class shape (d=2048,
 f=768, E=128 in 16 clusters of 8, top-8, rank 64, bf16, T=4096 tokens, seeded
 synthetic inputs, Gaussian router). One step = one call of lx_moe_forward
 (bucketing included, router excluded: ids and weights are inputs), with all
-inputs resident in HBM.
+inputs resident in HBM; consecutive steps use independent copies of the
+layer weights (round-robin over --rotate copies), so no step finds the
+previous step's weights in the last-level cache.
 
 Prints ONE JSON line: tokens/s of the whole layer, the roofline of the
 dominant kernel (per-kernel durations from HIP events recorded around each
@@ -43,6 +45,10 @@ def parse():
     ap.add_argument("--no-cpu", action="store_true", help="skip the CPU oracle baseline")
     ap.add_argument("--cpu-tokens", type=int, default=4096)
     ap.add_argument("--cpu-seconds", type=float, default=10.0)
+    ap.add_argument("--rotate", type=int, default=5,
+                    help="independent device copies of the layer weights, used round-robin by the "
+                         "timed steps so that the 256 MB last-level cache cannot hold one step's weights "
+                         "for the next (1 = a single copy)")
     ap.add_argument("--copy-calibration", action="store_true",
                     help="only run a plain 1 GiB device-to-device copy 5 times (scales the "
                          "FETCH_SIZE / WRITE_SIZE counters to bytes)")
@@ -119,6 +125,39 @@ def load_traffic(kernel, workload):
         return None
 
 
+def clone_layer(dl):
+    """Independent device copy of a DeviceLayer's weights (same routing structure)."""
+    import dataclasses
+    names = ("a_gate", "b_gate", "a_up", "b_up", "a_down", "b_down")
+    levels = [dataclasses.replace(lv, **{n: getattr(lv, n).clone() for n in names}) for lv in dl.levels]
+    return dataclasses.replace(dl, anchor_gate=dl.anchor_gate.clone(), anchor_up=dl.anchor_up.clone(),
+                               anchor_down=dl.anchor_down.clone(), levels=levels)
+
+
+def rotating(calls):
+    """One step = the next prepared call, round-robin over the weight copies."""
+    state = [0]
+
+    def step():
+        calls[state[0]]()
+        state[0] = (state[0] + 1) % len(calls)
+    return step
+
+
+def step_percentiles(fn, steps, torch):
+    """p10 / median / p90 of single-step times (events around each step)."""
+    import numpy as np
+    ev = [(torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)) for _ in range(steps)]
+    for a, b in ev:
+        a.record()
+        fn()
+        b.record()
+    torch.cuda.synchronize()
+    t = np.array([a.elapsed_time(b) for a, b in ev])
+    return dict(p10=round(float(np.percentile(t, 10)), 4), median=round(float(np.median(t)), 4),
+                p90=round(float(np.percentile(t, 90)), 4))
+
+
 def time_steps(fn, steps, warmup, torch):
     for _ in range(warmup):
         fn()
@@ -169,10 +208,12 @@ def main():
     kind = "flat" if layer.n_levels == 1 else "tree"
     ws = lx.alloc_workspace(dl, T, k, kind)
     out = torch.empty(T, layer.d, dtype=torch.float32, device="cuda")
-    call = lx.PreparedCall(dl, xd, ids, w, out, ws, kind)
+    copies = [dl] + [clone_layer(dl) for _ in range(max(a.rotate, 1) - 1)]
+    call = rotating([lx.PreparedCall(c, xd, ids, w, out, ws, kind) for c in copies])
 
     ms, wall = time_steps(call, a.steps, a.warmup, torch)
     tokens_per_s = T / (ms * 1e-3)
+    pct = step_percentiles(call, min(a.steps, 100), torch)
 
     # per-kernel durations: HIP events around every launch, same stream
     lx.profile_reset()
@@ -253,12 +294,13 @@ def main():
         del wg, wu, wd
         wsd = lx.alloc_workspace(dd, T, k, "dense")
         outd = torch.empty_like(out)
-        dcall = lx.PreparedCall(dd, xd, ids, w, outd, wsd, "dense")
+        dcopies = [dd] + [clone_layer(dd) for _ in range(max(a.rotate, 1) - 1)]
+        dcall = rotating([lx.PreparedCall(c, xd, ids, w, outd, wsd, "dense") for c in dcopies])
         dms, _ = time_steps(dcall, a.steps, a.warmup, torch)
         dense = dict(tokens_per_s=round(T / (dms * 1e-3), 1), ms_per_step=round(dms, 4),
                      speedup_of_compressed=round(dms / ms, 3),
                      alg_gflop=round(6 * layer.d * layer.f * T * k / 1e9, 2))
-        del dd, wsd, outd
+        del dd, dcopies, dcall, wsd, outd
 
     cpu = None
     if not a.no_cpu:
@@ -287,6 +329,8 @@ def main():
         "steps": a.steps,
         "warmup": a.warmup,
         "ms_per_step": round(ms, 4),
+        "step_ms": pct,
+        "weight_copies": len(copies),
         "wall_s_timed": round(wall, 3),
         "higher_is_better": True,
         "scaling": "weak",
