@@ -73,13 +73,17 @@ def copy_calibration(torch):
 
 
 def kernel_work(name, P, rows, touched):
-    """Algorithmic (flops, bytes) of one launch of kernel ``name``.
+    """Algorithmic (flops, bytes) of one launch of kernel ``name`` (a batched
+    launch "a+b" counts the sum of its parts).
 
     rows[l] / touched[l]: rows doing work and distinct nodes touched at level l.
     Bytes: the weights the launch must read (touched nodes once, bf16) plus
     its algorithmic activation input read once (x: T*d bf16; the per-row
     fp32 intermediates are not counted).
     """
+    if "+" in name:
+        parts = [kernel_work(n, P, rows, touched) for n in name.split("+")]
+        return sum(p[0] for p in parts), sum(p[1] for p in parts)
     d, f, T = P["d"], P["f"], P["T"]
     if name == "anchor_gate_up":
         return 4 * d * f * rows[0], 2 * f * d * 2 * touched[0] + T * d * 2

@@ -15,6 +15,7 @@
 //   per level l >= 1       v = hbar_l * B_down^T, y_l = v * A_down^T
 //   combine                out[t] = sum of the token's rows over all levels
 #include <algorithm>
+#include <deque>
 #include <map>
 #include <mutex>
 #include <string>
@@ -305,6 +306,17 @@ struct ForkJoin {
   ~ForkJoin() { (void)join(); }
 };
 
+// Stable C string for a launch name built at run time (batched launches).
+const char* intern_name(const std::string& n) {
+  static std::mutex mu;
+  static std::deque<std::string> names;
+  std::lock_guard<std::mutex> lk(mu);
+  for (const std::string& s : names)
+    if (s == n) return s.c_str();
+  names.push_back(n);
+  return names.back().c_str();
+}
+
 enum Stop { RUN_ALL, RUN_BUCKET };
 
 // The whole forward (or just the bucketing) of a validated tree.
@@ -413,6 +425,38 @@ lx_status run(const lx_tree_layer& t, int T, int k, const void* x, const int32_t
   }
   if (stop == RUN_BUCKET) return LX_OK;
 
+  // Decode-sized batches (every level with GEMM work on the skinny kernel):
+  // the independent products of one phase share a launch.
+  bool batch_mode = true;
+  for (int l = 0; l <= L; ++l) {
+    const bool work = l == 0 || t.levels[l - 1].n_factors > 0;
+    if (work && !skinny[l]) batch_mode = false;
+  }
+  struct Pend {
+    GemmArgs g;
+    bool hilo;
+    int tiles;
+    const char* name;
+  };
+  Pend pend[kSkinnyMaxProblems];
+  int npend = 0;
+  auto flush = [&]() -> lx_status {
+    if (npend == 0) return LX_OK;
+    GemmArgs g[kSkinnyMaxProblems];
+    bool hilo[kSkinnyMaxProblems];
+    int tiles[kSkinnyMaxProblems];
+    std::string name;
+    for (int i = 0; i < npend; ++i) {
+      g[i] = pend[i].g;
+      hilo[i] = pend[i].hilo;
+      tiles[i] = pend[i].tiles;
+      name += (i ? "+" : "") + std::string(pend[i].name);
+    }
+    const int n = npend;
+    npend = 0;
+    LX_LAUNCH(intern_name(name), launch_gemm_skinny_batch(g, hilo, tiles, n, lstream));
+    return LX_OK;
+  };
   auto big = [&](const char* name, GemmArgs g, int l, int bm, int bn, bool hilo,
                  int64_t a_rows_total) -> lx_status {
     const LevelPlan& q = P.lv[l];
@@ -422,6 +466,14 @@ lx_status run(const lx_tree_layer& t, int T, int k, const void* x, const int32_t
         return fail(LX_ERR_UNSUPPORTED, std::string(name) + ": shape not supported by the skinny GEMM");
       g.tiles = ba.lv[l].tiles[kTabSkinny];
       g.n_tiles = ba.lv[l].n_tiles[kTabSkinny];
+      if (batch_mode) {
+        if (npend == kSkinnyMaxProblems) {
+          const lx_status st = flush();
+          if (st != LX_OK) return st;
+        }
+        pend[npend++] = Pend{g, hilo, (int)q.tiles_max[kTabSkinny], name};
+        return LX_OK;
+      }
       LX_LAUNCH(name, launch_gemm_skinny(g, hilo, (int)q.tiles_max[kTabSkinny], lstream));
       return LX_OK;
     }
@@ -455,18 +507,20 @@ lx_status run(const lx_tree_layer& t, int T, int k, const void* x, const int32_t
   // The correction chains go to the auxiliary stream, concurrently with the
   // anchor GEMMs on the caller's stream, when the anchor level is large
   // enough to run on the persistent kernel (for decode-sized batches the
-  // cross-stream event latency outweighs the overlap). Per-kernel timing
-  // runs serialised so that each kernel's duration is its own.
+  // cross-stream event latency outweighs the overlap; those batch their
+  // launches instead). Per-kernel timing runs serialised so that each
+  // kernel's duration is its own.
   bool any_fac = false;
   for (int l = 1; l <= L; ++l) any_fac |= t.levels[l - 1].n_factors > 0;
   Aux* const aux = any_fac && !skinny[0] && !g_prof ? aux_for_current_device() : nullptr;
   std::unique_lock<std::mutex> aux_lock;
   if (aux) aux_lock = std::unique_lock<std::mutex>(aux->mu);
   ForkJoin fj_up(aux, stream), fj_down(aux, stream);
+  hipStream_t const side = aux ? aux->s : stream;
   LX_HIP(fj_up.fork());
-  if (aux) lstream = aux->s;
 
-  // correction gate|up per level: z = B x (once per (token, node)), dgu = A z
+  // correction gate|up per level, part 1: z = B x (once per (token, node))
+  lstream = side;
   for (int l = 1; l <= L; ++l) {
     const LevelPlan& q = P.lv[l];
     const lx_level& v = t.levels[l - 1];
@@ -482,36 +536,17 @@ lx_status run(const lx_tree_layer& t, int T, int k, const void* x, const int32_t
     g.ncols[0] = g.ncols[1] = r;
     g.K = d;
     g.C = (float*)(W + q.z);
-    GemmArgs h{};
-    h.B[0] = v.a_gate;
-    h.B[1] = v.a_up;
-    h.b_stride[0] = h.b_stride[1] = (int64_t)f * r;
-    h.ncols[0] = h.ncols[1] = f;
-    h.A = W + q.z;
-    h.C = (float*)(W + q.gu);
-    h.ldc = 2 * (int64_t)f;
-    h.c_coloff[1] = f;
     if (fast[l]) {
       g.ldc = 4 * (int64_t)r;  // [gate hi | gate lo | up hi | up lo], bf16
       LX_TRY(big(kLowIn[l], g, l, 128, 2 * r <= 128 ? 128 : 256, true, T));
-      h.lda = 4 * (int64_t)r;
-      h.a_koff[1] = 2 * r;
-      h.K = 2 * r;
-      h.Kb = r;
-      // gate and up read different z columns: tiles must not straddle them
-      LX_TRY(big(kLowOut[l], h, l, kBigBM, f % 256 == 0 ? 256 : f % 128 == 0 ? 128 : 64, false, q.rows_max));
     } else {
       g.ldc = 2 * (int64_t)r;
       g.c_coloff[1] = r;
       LX_TRY(small(kLowIn[l], g, l, A_BF16));
-      h.lda = 2 * (int64_t)r;
-      h.a_koff[1] = r;
-      h.K = r;
-      LX_TRY(small(kLowOut[l], h, l, A_F32_HILO));
     }
   }
-  lstream = stream;
   // anchor gate|up, once per (token, anchor)
+  lstream = stream;
   {
     const LevelPlan& q = P.lv[0];
     GemmArgs g{};
@@ -531,6 +566,39 @@ lx_status run(const lx_tree_layer& t, int T, int k, const void* x, const int32_t
     else
       LX_TRY(small("anchor_gate_up", g, 0, A_BF16));
   }
+  LX_TRY(flush());
+  // correction gate|up per level, part 2: dgu = A z
+  lstream = side;
+  for (int l = 1; l <= L; ++l) {
+    const LevelPlan& q = P.lv[l];
+    const lx_level& v = t.levels[l - 1];
+    if (v.n_factors == 0) continue;
+    const int r = v.rank;
+    GemmArgs h{};
+    h.B[0] = v.a_gate;
+    h.B[1] = v.a_up;
+    h.b_stride[0] = h.b_stride[1] = (int64_t)f * r;
+    h.ncols[0] = h.ncols[1] = f;
+    h.A = W + q.z;
+    h.C = (float*)(W + q.gu);
+    h.ldc = 2 * (int64_t)f;
+    h.c_coloff[1] = f;
+    if (fast[l]) {
+      h.lda = 4 * (int64_t)r;
+      h.a_koff[1] = 2 * r;
+      h.K = 2 * r;
+      h.Kb = r;
+      // gate and up read different z columns: tiles must not straddle them
+      LX_TRY(big(kLowOut[l], h, l, kBigBM, f % 256 == 0 ? 256 : f % 128 == 0 ? 128 : 64, false, q.rows_max));
+    } else {
+      h.lda = 2 * (int64_t)r;
+      h.a_koff[1] = r;
+      h.K = r;
+      LX_TRY(small(kLowOut[l], h, l, A_F32_HILO));
+    }
+  }
+  LX_TRY(flush());
+  lstream = stream;
 
   TokenArgs ta{};
   ta.T = T;
@@ -577,8 +645,8 @@ lx_status run(const lx_tree_layer& t, int T, int k, const void* x, const int32_t
       LX_TRY(small("anchor_down", g, 0, A_F32_HILO));
     }
   }
-  // correction down per level: v = B_down hbar, y = A_down v
-  if (aux) lstream = aux->s;
+  // correction down per level, part 1: v = B_down hbar
+  lstream = side;
   for (int l = 1; l <= L; ++l) {
     const LevelPlan& q = P.lv[l];
     const lx_level& v = t.levels[l - 1];
@@ -590,6 +658,26 @@ lx_status run(const lx_tree_layer& t, int T, int k, const void* x, const int32_t
     g.b_stride[0] = (int64_t)r * f;
     g.ncols[0] = r;
     g.C = (float*)(W + q.v);
+    if (fast[l]) {
+      g.lda = 2 * (int64_t)f;
+      g.K = 2 * f;
+      g.Kb = f;
+      g.ldc = 2 * (int64_t)r;  // [hi | lo], bf16
+      LX_TRY(big(kDownIn[l], g, l, 128, r <= 64 ? 64 : 128, true, q.rows_max));
+    } else {
+      g.lda = f;
+      g.K = f;
+      g.ldc = r;
+      LX_TRY(small(kDownIn[l], g, l, A_F32_HILO));
+    }
+  }
+  LX_TRY(flush());
+  // correction down per level, part 2: y = A_down v
+  for (int l = 1; l <= L; ++l) {
+    const LevelPlan& q = P.lv[l];
+    const lx_level& v = t.levels[l - 1];
+    if (v.n_factors == 0) continue;
+    const int r = v.rank;
     GemmArgs h{};
     h.A = W + q.v;
     h.B[0] = v.a_down;
@@ -598,25 +686,17 @@ lx_status run(const lx_tree_layer& t, int T, int k, const void* x, const int32_t
     h.C = (float*)(W + q.y);
     h.ldc = d;
     if (fast[l]) {
-      g.lda = 2 * (int64_t)f;
-      g.K = 2 * f;
-      g.Kb = f;
-      g.ldc = 2 * (int64_t)r;  // [hi | lo], bf16
-      LX_TRY(big(kDownIn[l], g, l, 128, r <= 64 ? 64 : 128, true, q.rows_max));
       h.lda = 2 * (int64_t)r;
       h.K = 2 * r;
       h.Kb = r;
       LX_TRY(big(kDownOut[l], h, l, kBigBM, 256, false, q.rows_max));
     } else {
-      g.lda = f;
-      g.K = f;
-      g.ldc = r;
-      LX_TRY(small(kDownIn[l], g, l, A_F32_HILO));
       h.lda = r;
       h.K = r;
       LX_TRY(small(kDownOut[l], h, l, A_F32_HILO));
     }
   }
+  LX_TRY(flush());
 #undef LX_TRY
   lstream = stream;
   LX_HIP(fj_down.join());

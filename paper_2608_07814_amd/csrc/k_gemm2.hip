@@ -85,6 +85,19 @@ __device__ __forceinline__ void bar() {
   asm volatile("" ::: "memory");
 }
 
+// s_waitcnt allowing `ahead` slabs of R loads each to stay in flight.
+template <int R>
+__device__ __forceinline__ void wait_slabs(int ahead) {
+  if (ahead >= 3)
+    wait_vmcnt<3 * R>();
+  else if (ahead == 2)
+    wait_vmcnt<2 * R>();
+  else if (ahead == 1)
+    wait_vmcnt<R>();
+  else
+    wait_vmcnt<0>();
+}
+
 template <int BM, int BN, bool OUT_HILO>
 __global__ __launch_bounds__(NTHR2, 1) __attribute__((amdgpu_waves_per_eu(1, 1)))
 void k_gemm_big(GemmArgs p, int ntn) {
@@ -94,9 +107,14 @@ void k_gemm_big(GemmArgs p, int ntn) {
   constexpr int A_ROUNDS = BM * 8 / NTHR2;  // 16-byte chunks per thread per slab
   constexpr int B_ROUNDS = BN * 8 / NTHR2;
   constexpr int ROUNDS = A_ROUNDS + B_ROUNDS;
-  // LDS: stage 0 = [A | B], stage 1 = [A | B]; the epilogue reuses it.
+  // LDS: NST stages of [A | B] within 128 KB (2 for 256x256 tiles, up to 4
+  // for the smaller ones, which stream more bytes per MFMA and need more
+  // slabs in flight); the epilogue reuses it.
   constexpr int SA = BM * BK2, SB = BN * BK2;
-  __shared__ __attribute__((aligned(1024))) u16 smem[2 * (SA + SB)];
+  constexpr int NST_FIT = 65536 / (SA + SB);
+  constexpr int NST = NST_FIT > 4 ? 4 : NST_FIT;
+  static_assert(NST >= 2, "two stages must fit");
+  __shared__ __attribute__((aligned(1024))) u16 smem[NST * (SA + SB)];
   u16* const sA0 = smem;
   u16* const sB0 = smem + SA;
   u16* const sA1 = smem + SA + SB;
@@ -171,9 +189,9 @@ void k_gemm_big(GemmArgs p, int ntn) {
     const int q_ = (KT) / nper, per_ = (KT) - q_ * nper;                            \
     const int kb_ = q_ * BK2, ka_ = per_ * Kb + kb_;                                \
     _Pragma("unroll") for (int j = 0; j < A_ROUNDS; ++j)                            \
-        load_lds16(Ab + (aoff[j] + (uint32_t)ka_), &SA_[(j * NTHR2 + wave * 64) * 8]); \
+        load_lds16(Ab + (aoff[j] + (uint32_t)ka_), &(SA_)[(j * NTHR2 + wave * 64) * 8]); \
     _Pragma("unroll") for (int j = 0; j < B_ROUNDS; ++j)                            \
-        load_lds16(bptr[j] + kb_, &SB_[(j * NTHR2 + wave * 64) * 8]);               \
+        load_lds16(bptr[j] + kb_, &(SB_)[(j * NTHR2 + wave * 64) * 8]);             \
   } while (0)
 
     f32x16 acc[MI][NI];
@@ -192,9 +210,9 @@ void k_gemm_big(GemmArgs p, int ntn) {
   do {                                                                              \
     const int kc_ = (KS) * 2 + (lane >> 5);                                         \
     _Pragma("unroll") for (int mi = 0; mi < MI; ++mi)                               \
-      FA[mi] = *(const bf16x8*)&SA_[lds_off2(wm * WM + mi * 32 + (lane & 31), kc_)]; \
+      FA[mi] = *(const bf16x8*)&(SA_)[lds_off2(wm * WM + mi * 32 + (lane & 31), kc_)]; \
     _Pragma("unroll") for (int ni = 0; ni < NI; ++ni)                               \
-      FB[ni] = *(const bf16x8*)&SB_[lds_off2(wn * WN + ni * 32 + (lane & 31), kc_)]; \
+      FB[ni] = *(const bf16x8*)&(SB_)[lds_off2(wn * WN + ni * 32 + (lane & 31), kc_)]; \
   } while (0)
 #define LX_MFMAS(FA, FB)                                                            \
   do {                                                                              \
@@ -221,6 +239,28 @@ void k_gemm_big(GemmArgs p, int ntn) {
     LX_MFMAS(fa1, fb1);                                                             \
   } while (0)
 
+    if constexpr (NST > 2) {
+      // Ring of NST stages, one barrier per slab: slab kt lives in stage
+      // kt % NST; after the barrier that follows slab kt's compute every
+      // wavefront is done with that stage and slab kt + NST goes there.
+      const int npre = nk < NST ? nk : NST;
+      for (int i = 0; i < npre; ++i) LX_ISSUE(smem + i * (SA + SB), smem + i * (SA + SB) + SA, i);
+      wait_slabs<ROUNDS>(npre - 1);
+      bar();
+      for (int kt = 0; kt < nk; ++kt) {
+        const int st = kt % NST;
+        u16* const cA = smem + st * (SA + SB);
+        u16* const cB = cA + SA;
+        LX_COMPUTE(cA, cB);
+        if (kt + 1 < nk) {
+          const int last = kt + NST - 1 < nk - 1 ? kt + NST - 1 : nk - 1;
+          wait_slabs<ROUNDS>(last - (kt + 1));
+          bar();
+          if (kt + NST < nk) LX_ISSUE(cA, cB, kt + NST);
+        }
+      }
+      bar();
+    } else {
     LX_ISSUE(sA0, sB0, 0);
     if (nk > 1) LX_ISSUE(sA1, sB1, 1);
     int kt = 0;
@@ -247,6 +287,7 @@ void k_gemm_big(GemmArgs p, int ntn) {
       bar();
       LX_COMPUTE(sA0, sB0);
       bar();
+    }
     }
 #undef LX_ISSUE
 #undef LX_COMPUTE
@@ -315,31 +356,30 @@ void k_gemm_big(GemmArgs p, int ntn) {
 // by HBM, not by the MFMAs.
 constexpr int SK_THR = 128, SK_NST = 4;
 
-template <int R>
-__device__ __forceinline__ void wait_slabs(int ahead) {
-  if (ahead >= 3)
-    wait_vmcnt<3 * R>();
-  else if (ahead == 2)
-    wait_vmcnt<2 * R>();
-  else if (ahead == 1)
-    wait_vmcnt<R>();
-  else
-    wait_vmcnt<0>();
-}
 
-template <bool OUT_HILO>
-__global__ __launch_bounds__(SK_THR) void k_gemm_skinny(GemmArgs p, int ntn) {
+// Several independent GEMMs in one launch (e.g. the anchor and correction
+// products that read the same input rows): problem i owns workgroups
+// [base[i], base[i+1]); every base is a multiple of 8, so the XCD of a
+// workgroup is its index within the problem modulo 8.
+__global__ __launch_bounds__(SK_THR) void k_gemm_skinny(SkinnyBatch b) {
   constexpr int BM = kSkinnyBM, BN = kSkinnyBN;
   constexpr int A_ROUNDS = BM * 8 / SK_THR, B_ROUNDS = BN * 8 / SK_THR;
   constexpr int R = A_ROUNDS + B_ROUNDS;
   constexpr int SA = BM * BK2, STAGE = (BM + BN) * BK2;
   __shared__ __attribute__((aligned(1024))) u16 smem[SK_NST * STAGE];
 
-  // one work item per workgroup, XCD-contiguous order (grid >= items)
+  int pi = 0;
+  while (pi + 1 < b.n && (int)blockIdx.x >= b.base[pi + 1]) ++pi;
+  const GemmArgs& p = b.g[pi];
+  const int ntn = b.ntn[pi];
+  const bool out_hilo = b.hilo[pi] != 0;
+  const int wg = (int)blockIdx.x - b.base[pi];
+
+  // one work item per workgroup, XCD-contiguous order (workgroups >= items)
   const int real = *p.n_tiles * ntn;
   const int q = real / NXCD, rmd = real % NXCD;
-  const int x = blockIdx.x % NXCD;
-  const int Lg = x * q + (x < rmd ? x : rmd) + (int)blockIdx.x / NXCD;
+  const int x = wg % NXCD;
+  const int Lg = x * q + (x < rmd ? x : rmd) + wg / NXCD;
   if (Lg >= x * q + (x < rmd ? x : rmd) + q + (x < rmd ? 1 : 0)) return;
   const int ti = Lg / ntn, nt = Lg % ntn;
 
@@ -442,7 +482,7 @@ __global__ __launch_bounds__(SK_THR) void k_gemm_skinny(GemmArgs p, int ntn) {
     const int r = ps * RPP + lane / LPR;
     const float4 v = *(const float4*)&ep[r * PITCH + c4];
     if (r >= te.nrows || col >= ncol) continue;
-    if (OUT_HILO) {
+    if (out_hilo) {
       const int pp = col < p.ncols[0] ? 0 : 1;
       const int c = pp ? col - p.ncols[0] : col;
       const int hi_col = (pp ? 2 * p.ncols[0] : 0) + c;
@@ -521,15 +561,28 @@ hipError_t launch_gemm_big(const GemmArgs& g, int bm, int bn, bool out_hilo, int
   return launch_bn<128, 64>(g, out_hilo, grid, ntn, s);
 }
 
-hipError_t launch_gemm_skinny(const GemmArgs& g, bool out_hilo, int grid_tiles, hipStream_t s) {
-  const int ntn = (g.ncols[0] + g.ncols[1] + kSkinnyBN - 1) / kSkinnyBN;
-  const int grid = grid_tiles * ntn;  // >= work items: one item per workgroup
-  if (grid <= 0) return hipSuccess;
-  if (out_hilo)
-    hipLaunchKernelGGL(k_gemm_skinny<true>, dim3(grid), dim3(SK_THR), 0, s, g, ntn);
-  else
-    hipLaunchKernelGGL(k_gemm_skinny<false>, dim3(grid), dim3(SK_THR), 0, s, g, ntn);
+hipError_t launch_gemm_skinny_batch(const GemmArgs* g, const bool* out_hilo, const int* grid_tiles, int n,
+                                    hipStream_t s) {
+  if (n < 1 || n > kSkinnyMaxProblems) return hipErrorInvalidValue;
+  SkinnyBatch b{};
+  int wg = 0;
+  for (int i = 0; i < n; ++i) {
+    b.g[i] = g[i];
+    b.ntn[i] = (g[i].ncols[0] + g[i].ncols[1] + kSkinnyBN - 1) / kSkinnyBN;
+    b.hilo[i] = out_hilo[i] ? 1 : 0;
+    b.base[i] = wg;
+    const int items = grid_tiles[i] * b.ntn[i];  // >= work items of problem i
+    wg += (items + NXCD - 1) / NXCD * NXCD;
+  }
+  b.base[n] = wg;
+  b.n = n;
+  if (wg <= 0) return hipSuccess;
+  hipLaunchKernelGGL(k_gemm_skinny, dim3(wg), dim3(SK_THR), 0, s, b);
   return hipGetLastError();
+}
+
+hipError_t launch_gemm_skinny(const GemmArgs& g, bool out_hilo, int grid_tiles, hipStream_t s) {
+  return launch_gemm_skinny_batch(&g, &out_hilo, &grid_tiles, 1, s);
 }
 
 }  // namespace lx

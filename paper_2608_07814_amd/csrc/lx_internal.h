@@ -122,6 +122,17 @@ hipError_t launch_gemm_big(const GemmArgs& g, int bm, int bn, bool out_hilo, int
 // applicability as the large-tile kernel (with bn = kSkinnyBN).
 constexpr int kSkinnyBM = 32, kSkinnyBN = 64;
 hipError_t launch_gemm_skinny(const GemmArgs& g, bool out_hilo, int grid_tiles, hipStream_t s);
+// Up to kSkinnyMaxProblems independent skinny GEMMs in one launch.
+constexpr int kSkinnyMaxProblems = 1 + LX_MAX_LEVELS;
+struct SkinnyBatch {
+  GemmArgs g[kSkinnyMaxProblems];
+  int32_t ntn[kSkinnyMaxProblems];
+  int32_t hilo[kSkinnyMaxProblems];
+  int32_t base[kSkinnyMaxProblems + 1];  // first workgroup of each problem
+  int32_t n;
+};
+hipError_t launch_gemm_skinny_batch(const GemmArgs* g, const bool* out_hilo, const int* grid_tiles, int n,
+                                    hipStream_t s);
 
 // ---------------------------------------------------------------- elementwise
 struct TokenArgs {
