@@ -34,6 +34,7 @@
 //     fp32 or 8-byte bf16 stores).
 #include "lx_internal.h"
 
+#include <algorithm>
 #include <mutex>
 
 namespace lx {
@@ -350,17 +351,19 @@ void k_gemm_big(GemmArgs p, int ntn) {
 
 // ---------------------------------------------------------------- skinny
 // 32 x 64 output tile per 128-thread workgroup (two wavefronts, one 32x32
-// MFMA block each), K-slabs of 64 through a 4-stage LDS ring (48 KB, so
-// three workgroups fit per compute unit). Three slabs are in flight while one
-// is consumed: with few rows per tile the kernel streams weights and is bound
-// by HBM, not by the MFMAs.
-constexpr int SK_THR = 128, SK_NST = 4;
+// MFMA block each), K-slabs of 64 through an LDS ring of SK_NST stages: 4
+// (48 KB, three workgroups per compute unit, three slabs in flight while one
+// is consumed), or 2 for products whose K is at most two slabs (24 KB, six
+// workgroups per compute unit). With few rows per tile the kernel streams
+// weights and is bound by HBM, not by the MFMAs.
+constexpr int SK_THR = 128;
 
 
 // Several independent GEMMs in one launch (e.g. the anchor and correction
 // products that read the same input rows): problem i owns workgroups
 // [base[i], base[i+1]); every base is a multiple of 8, so the XCD of a
 // workgroup is its index within the problem modulo 8.
+template <int SK_NST>
 __global__ __launch_bounds__(SK_THR) void k_gemm_skinny(SkinnyBatch b) {
   constexpr int BM = kSkinnyBM, BN = kSkinnyBN;
   constexpr int A_ROUNDS = BM * 8 / SK_THR, B_ROUNDS = BN * 8 / SK_THR;
@@ -448,9 +451,10 @@ __global__ __launch_bounds__(SK_THR) void k_gemm_skinny(SkinnyBatch b) {
     for (int ks = 0; ks < 4; ++ks) acc = __builtin_amdgcn_mfma_f32_32x32x16_bf16(fa[ks], fb[ks], acc, 0, 0, 0);
   };
 
-  // Slab kt lives in stage kt % 4. Slabs 0..3 are issued up front; after the
-  // barrier that follows slab kt's compute, stage kt % 4 is free and slab
-  // kt + 4 goes there.
+  // Slab kt lives in stage kt % SK_NST. Slabs 0 .. SK_NST-1 are issued up
+  // front; after the barrier that follows slab kt's compute, stage
+  // kt % SK_NST is free and slab kt + SK_NST goes there.
+  static_assert((SK_NST & (SK_NST - 1)) == 0, "power-of-two ring");
   const int npre = nk < SK_NST ? nk : SK_NST;
   for (int i = 0; i < npre; ++i) issue(i, i);
   wait_slabs<R>(npre - 1);
@@ -458,8 +462,8 @@ __global__ __launch_bounds__(SK_THR) void k_gemm_skinny(SkinnyBatch b) {
   for (int kt = 0; kt < nk; ++kt) {
     compute(kt & (SK_NST - 1));
     if (kt + 1 < nk) {
-      // slabs issued so far: 0 .. min(kt + 3, nk - 1); wait for kt + 1
-      const int last = kt + 3 < nk - 1 ? kt + 3 : nk - 1;
+      // slabs issued so far: 0 .. min(kt + SK_NST - 1, nk - 1); wait for kt + 1
+      const int last = kt + SK_NST - 1 < nk - 1 ? kt + SK_NST - 1 : nk - 1;
       wait_slabs<R>(last - (kt + 1));
       wait_lgkm0();
       bar();
@@ -577,7 +581,12 @@ hipError_t launch_gemm_skinny_batch(const GemmArgs* g, const bool* out_hilo, con
   b.base[n] = wg;
   b.n = n;
   if (wg <= 0) return hipSuccess;
-  hipLaunchKernelGGL(k_gemm_skinny, dim3(wg), dim3(SK_THR), 0, s, b);
+  int max_nk = 0;
+  for (int i = 0; i < n; ++i) max_nk = std::max(max_nk, g[i].K / BK2);
+  if (max_nk <= 2)
+    hipLaunchKernelGGL(k_gemm_skinny<2>, dim3(wg), dim3(SK_THR), 0, s, b);
+  else
+    hipLaunchKernelGGL(k_gemm_skinny<4>, dim3(wg), dim3(SK_THR), 0, s, b);
   return hipGetLastError();
 }
 
