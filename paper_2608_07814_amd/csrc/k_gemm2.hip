@@ -1,9 +1,9 @@
 // Large-tile grouped GEMM for gfx950: C = A * W^T over the rows of one tree
 // level, for bf16 A whose K is a multiple of 64.
 //
-//   * BM x BN output tile (BM = 128 or 256, BN = 64, 128 or 256) per
-//     256-thread workgroup; the 4 wavefronts form a 2 x 2 grid, each owning
-//     (BM/2) x (BN/2) as MFMA 32x32x16 blocks (accumulators in AGPRs);
+//   * BM x BN output tile (BM = 128 or 256, BN = 64, 128 or 256); 256x256
+//     tiles use 8 wavefronts (2 x 4 grid of 128x64 blocks, two per SIMD),
+//     the others 4 (2 x 2 grid), each block as MFMA 32x32x16 sub-blocks;
 //   * both operands go HBM -> LDS with global_load_lds_dwordx4 (16 B per lane,
 //     no staging registers) into a 2-stage LDS ring, so the next K-slab
 //     streams in while the current one feeds the MFMAs; inside a slab the
@@ -46,7 +46,7 @@ typedef float f32x16 __attribute__((ext_vector_type(16)));
 typedef uint16_t u16;
 typedef __attribute__((address_space(3))) void lds_void_t;
 
-constexpr int BK2 = 64, NTHR2 = 256, NXCD = 8;
+constexpr int BK2 = 64, NXCD = 8;
 
 __device__ __forceinline__ int swz2(int row) { return (row ^ (row >> 3)) & 7; }
 __device__ __forceinline__ int lds_off2(int row, int kc) { return row * BK2 + ((kc ^ swz2(row)) << 3); }
@@ -99,14 +99,27 @@ __device__ __forceinline__ void wait_slabs(int ahead) {
     wait_vmcnt<0>();
 }
 
+// Wavefronts per workgroup: 8 for 256x256 tiles (two per SIMD in a 2x4 grid
+// of 128x64 blocks, so one wavefront's LDS and barrier waits are covered by
+// the other's MFMAs), else 4 (one per SIMD, a 2x2 grid).
+template <int BM, int BN>
+struct BigCfg {
+  static constexpr int NW = (BM == 256 && BN == 256) ? 8 : 4;
+  static constexpr int WGN = NW / 2;  // wavefronts along N
+  static constexpr int NTHR = NW * 64;
+  static constexpr int WPE = NW / 4;  // wavefronts per SIMD
+};
+
 template <int BM, int BN, bool OUT_HILO>
-__global__ __launch_bounds__(NTHR2, 1) __attribute__((amdgpu_waves_per_eu(1, 1)))
+__global__ __launch_bounds__((BigCfg<BM, BN>::NTHR), 1)
+__attribute__((amdgpu_waves_per_eu(BigCfg<BM, BN>::WPE, BigCfg<BM, BN>::WPE)))
 void k_gemm_big(GemmArgs p, int ntn) {
+  constexpr int NTHR = BigCfg<BM, BN>::NTHR, WGN = BigCfg<BM, BN>::WGN;
   constexpr int MI = BM / 64;              // 32-row MFMA blocks per wavefront
-  constexpr int NI = BN / 64;              // 32-column MFMA blocks per wavefront
-  constexpr int WM = BM / 2, WN = BN / 2;
-  constexpr int A_ROUNDS = BM * 8 / NTHR2;  // 16-byte chunks per thread per slab
-  constexpr int B_ROUNDS = BN * 8 / NTHR2;
+  constexpr int NI = BN / (32 * WGN);      // 32-column MFMA blocks per wavefront
+  constexpr int WM = BM / 2, WN = BN / WGN;
+  constexpr int A_ROUNDS = BM * 8 / NTHR;  // 16-byte chunks per thread per slab
+  constexpr int B_ROUNDS = BN * 8 / NTHR;
   constexpr int ROUNDS = A_ROUNDS + B_ROUNDS;
   // LDS: NST stages of [A | B] within 128 KB (2 for 256x256 tiles, up to 4
   // for the smaller ones, which stream more bytes per MFMA and need more
@@ -144,7 +157,7 @@ void k_gemm_big(GemmArgs p, int ntn) {
     int tid = threadIdx.x;
     asm volatile("" : "+v"(tid));
     const int wave = tid >> 6, lane = tid & 63;
-    const int wm = wave >> 1, wn = wave & 1;
+    const int wm = wave / WGN, wn = wave % WGN;
     const int ti = Lg / ntn, nt = Lg % ntn;
 
     // The two weight parts form one column range [0, ncol): column n < ncols[0]
@@ -163,7 +176,7 @@ void k_gemm_big(GemmArgs p, int ntn) {
     uint32_t aoff[A_ROUNDS];
 #pragma unroll
     for (int j = 0; j < A_ROUNDS; ++j) {
-      const int Ps = j * NTHR2 + tid;
+      const int Ps = j * NTHR + tid;
       const int row = Ps >> 3;
       const int c = (Ps & 7) ^ swz2(row);
       const int r = row < te.nrows ? row : te.nrows - 1;
@@ -173,7 +186,7 @@ void k_gemm_big(GemmArgs p, int ntn) {
     const u16* bptr[B_ROUNDS];
 #pragma unroll
     for (int j = 0; j < B_ROUNDS; ++j) {
-      const int Ps = j * NTHR2 + tid;
+      const int Ps = j * NTHR + tid;
       const int row = Ps >> 3;
       const int c = (Ps & 7) ^ swz2(row);
       const int n = n0 + row < ncol ? n0 + row : ncol - 1;
@@ -190,9 +203,9 @@ void k_gemm_big(GemmArgs p, int ntn) {
     const int q_ = (KT) / nper, per_ = (KT) - q_ * nper;                            \
     const int kb_ = q_ * BK2, ka_ = per_ * Kb + kb_;                                \
     _Pragma("unroll") for (int j = 0; j < A_ROUNDS; ++j)                            \
-        load_lds16(Ab + (aoff[j] + (uint32_t)ka_), &(SA_)[(j * NTHR2 + wave * 64) * 8]); \
+        load_lds16(Ab + (aoff[j] + (uint32_t)ka_), &(SA_)[(j * NTHR + wave * 64) * 8]);  \
     _Pragma("unroll") for (int j = 0; j < B_ROUNDS; ++j)                            \
-        load_lds16(bptr[j] + kb_, &(SB_)[(j * NTHR2 + wave * 64) * 8]);             \
+        load_lds16(bptr[j] + kb_, &(SB_)[(j * NTHR + wave * 64) * 8]);              \
   } while (0)
 
     f32x16 acc[MI][NI];
@@ -223,6 +236,15 @@ void k_gemm_big(GemmArgs p, int ntn) {
   } while (0)
 #define LX_COMPUTE(SA_, SB_)                                                        \
   do {                                                                              \
+    if constexpr (BigCfg<BM, BN>::WPE > 1) {                                        \
+      /* two wavefronts per SIMD cover each other's LDS latency: single */          \
+      /* fragment buffer, fewer registers */                                        \
+      _Pragma("unroll") for (int ks_ = 0; ks_ < 4; ++ks_) {                         \
+        LX_FRAG(SA_, SB_, ks_, fa0, fb0);                                           \
+        LX_MFMAS(fa0, fb0);                                                         \
+      }                                                                             \
+      break;                                                                        \
+    }                                                                               \
     LX_FRAG(SA_, SB_, 0, fa0, fb0);                                                 \
     __builtin_amdgcn_sched_barrier(0);                                              \
     LX_FRAG(SA_, SB_, 1, fa1, fb1);                                                 \
@@ -304,7 +326,7 @@ void k_gemm_big(GemmArgs p, int ntn) {
       constexpr int PITCH = WN + 4;
       constexpr int LPR = WN / 4;    // lanes per row
       constexpr int RPP = 64 / LPR;  // rows per pass
-      static_assert(4 * 32 * PITCH * 4 <= (int)sizeof(smem), "epilogue LDS");
+      static_assert(BigCfg<BM, BN>::NW * 32 * PITCH * 4 <= (int)sizeof(smem), "epilogue LDS");
       float* const ep = (float*)smem + wave * (32 * PITCH);
       const int c4 = (lane % LPR) * 4;
       const int col = n0 + wn * WN + c4;
@@ -512,9 +534,9 @@ __global__ __launch_bounds__(SK_THR) void k_gemm_skinny(SkinnyBatch b) {
 template <int BM, int BN>
 hipError_t launch_bn(const GemmArgs& g, bool hilo, int grid, int ntn, hipStream_t s) {
   if (hilo)
-    hipLaunchKernelGGL((k_gemm_big<BM, BN, true>), dim3(grid), dim3(NTHR2), 0, s, g, ntn);
+    hipLaunchKernelGGL((k_gemm_big<BM, BN, true>), dim3(grid), dim3(BigCfg<BM, BN>::NTHR), 0, s, g, ntn);
   else
-    hipLaunchKernelGGL((k_gemm_big<BM, BN, false>), dim3(grid), dim3(NTHR2), 0, s, g, ntn);
+    hipLaunchKernelGGL((k_gemm_big<BM, BN, false>), dim3(grid), dim3(BigCfg<BM, BN>::NTHR), 0, s, g, ntn);
   return hipGetLastError();
 }
 
