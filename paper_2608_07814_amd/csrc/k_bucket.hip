@@ -23,6 +23,17 @@ namespace {
 // single-workgroup path: nodes (and experts) per level, and tree nodes in all
 // correction levels together
 constexpr int kSmallMaxNodes = 1024, kSmallMaxTree = 1024;
+constexpr int kPlaceThr = 256;  // placement: threads per 64-token tile
+
+// Workgroup barrier for LDS communication only: waits for this wave's LDS
+// operations, not for its global stores (which nothing in the workgroup
+// reads back), unlike __syncthreads().
+__device__ __forceinline__ void lds_barrier() {
+  asm volatile("" ::: "memory");
+  __builtin_amdgcn_s_waitcnt(0xF | (0x7 << 4) | (0x3 << 14));  // lgkmcnt(0)
+  __builtin_amdgcn_s_barrier();
+  asm volatile("" ::: "memory");
+}
 
 // Ancestors of every expert at every level and validated factor indices.
 // Single workgroup: it also zeroes the status word before anything else runs.
@@ -113,7 +124,8 @@ __global__ __launch_bounds__(64) void k_bucket_hist(BucketArgs a) {
   }
 }
 
-// Exclusive scan of one value per thread across a 1024-thread block.
+// Exclusive scan of one value per thread across the workgroup (LDS only:
+// callers' pending global stores are not waited for).
 __device__ inline int block_exscan(int v, int* s_wave, int& total) {
   const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
   const int nwaves = blockDim.x >> 6;
@@ -123,7 +135,7 @@ __device__ inline int block_exscan(int v, int* s_wave, int& total) {
     if (lane >= o) incl += u;
   }
   if (lane == 63) s_wave[wave] = incl;
-  __syncthreads();
+  lds_barrier();
   if (threadIdx.x < 64) {
     int w = threadIdx.x < nwaves ? s_wave[threadIdx.x] : 0;
     int wi = w;
@@ -134,10 +146,10 @@ __device__ inline int block_exscan(int v, int* s_wave, int& total) {
     if (threadIdx.x < nwaves) s_wave[threadIdx.x] = wi - w;
     if (threadIdx.x == nwaves - 1) s_wave[63] = wi;
   }
-  __syncthreads();
+  lds_barrier();
   const int res = s_wave[wave] + incl - v;
   total = s_wave[63];
-  __syncthreads();
+  lds_barrier();
   return res;
 }
 
@@ -184,73 +196,101 @@ __device__ inline void build_tile_tables(const BucketLevel& lv, const int32_t* o
 
 __global__ __launch_bounds__(1024) void k_bucket_scan(BucketArgs a) {
   __shared__ int s_wave[64];
+  extern __shared__ int s_off[];  // [N + 1] node offsets
   const int l = blockIdx.x;
-  const BucketLevel lv = a.lv[l];
+  const BucketLevel& lv = a.lv[l];
   const int N = lv.n_nodes, NT = a.n_tok_tiles;
   const int64_t total = (int64_t)N * NT;
   const int nth = blockDim.x, tid = threadIdx.x;
 
-  // 1. exclusive scan of hist in (node, tile) order, in place
+  // exclusive scan of hist in (node, tile) order, in place; entry (n, 0)
+  // is node n's offset (kept in LDS for the tile tables)
+  // Each thread's chunk is read CH entries at a time with all loads in
+  // flight (a dependent load per entry would serialise on memory latency);
+  // chunks of at most CH entries stay in registers between the two passes.
+  constexpr int CH = 16;
   const int64_t chunk = (total + nth - 1) / nth;
   const int64_t b = (int64_t)tid * chunk;
   const int64_t e = b + chunk < total ? b + chunk : total;
+  int v[CH];
   int local = 0;
-  for (int64_t i = b; i < e; ++i) local += lv.hist[i];
+  for (int64_t c0 = b; c0 < e; c0 += CH) {
+#pragma unroll
+    for (int u = 0; u < CH; ++u) v[u] = c0 + u < e ? lv.hist[c0 + u] : 0;
+#pragma unroll
+    for (int u = 0; u < CH; ++u) local += v[u];
+  }
   int grand = 0;
   int run = block_exscan(local, s_wave, grand);
-  for (int64_t i = b; i < e; ++i) {
-    const int h = lv.hist[i];
-    lv.hist[i] = run;
-    run += h;
+  // (node, tile) of entry b, advanced incrementally (no division per entry)
+  int node = (int)(b / NT), tile = (int)(b - (int64_t)node * NT);
+  for (int64_t c0 = b; c0 < e; c0 += CH) {
+    if (e - b > CH) {  // chunk larger than the register cache: reload
+#pragma unroll
+      for (int u = 0; u < CH; ++u) v[u] = c0 + u < e ? lv.hist[c0 + u] : 0;
+    }
+#pragma unroll
+    for (int u = 0; u < CH; ++u) {
+      const int64_t i = c0 + u;
+      if (i < e) {
+        lv.hist[i] = run;
+        if (tile == 0) s_off[node] = run;
+        run += v[u];
+        if (++tile == NT) {
+          tile = 0;
+          ++node;
+        }
+      }
+    }
   }
-  __syncthreads();
-
-  // 2. node offsets
-  for (int n = tid; n < N; n += nth) lv.offsets[n] = NT > 0 ? lv.hist[(int64_t)n * NT] : 0;
-  if (tid == 0) lv.offsets[N] = grand;
-  __syncthreads();
-
-  build_tile_tables(lv, lv.offsets, lv.fac, s_wave);
+  if (tid == 0) s_off[N] = grand;
+  lds_barrier();
+  for (int n = tid; n <= N; n += nth) lv.offsets[n] = s_off[n];
+  build_tile_tables(lv, s_off, lv.fac, s_wave);
 }
 
-__global__ __launch_bounds__(64) void k_bucket_place(BucketArgs a) {
+// One thread per routing slot of the tile's 64 tokens.
+__global__ __launch_bounds__(kPlaceThr) void k_bucket_place(BucketArgs a) {
   extern __shared__ unsigned long long s_mask[];
-  __shared__ int s_node[kTokTile][LX_MAX_K];
-  const int l = blockIdx.y, tt = blockIdx.x, lane = threadIdx.x;
+  __shared__ int s_node[kTokTile * LX_MAX_K];
+  const int l = blockIdx.y, tt = blockIdx.x, tid = threadIdx.x;
   const BucketLevel& lv = a.lv[l];
-  build_masks(a, l, tt, s_mask, lv.n_nodes);
-  const int t = tt * kTokTile + lane;
-  if (t >= a.T) return;
-  const unsigned long long below = (1ull << lane) - 1ull;
-  const int64_t base = (int64_t)t * a.k;
-  for (int j = 0; j < a.k; ++j) {
-    const int64_t s = base + j;
-    const int n = node_of(a, l, a.ids[s]);
-    s_node[lane][j] = n;
+  const int N = lv.n_nodes, k = a.k;
+  const int t0 = tt * kTokTile;
+  const int nt = a.T - t0 < kTokTile ? a.T - t0 : kTokTile;
+  const int TK = nt * k;
+  for (int n = tid; n < N; n += blockDim.x) s_mask[n] = 0ull;
+  lds_barrier();
+  for (int s = tid; s < TK; s += blockDim.x) {
+    const int n = node_of(a, l, a.ids[(int64_t)t0 * k + s]);
+    s_node[s] = n;
+    if (n >= 0) atomicOr(&s_mask[n], 1ull << (s / k));
+  }
+  lds_barrier();
+  for (int s = tid; s < TK; s += blockDim.x) {
+    const int t = s / k, j = s - t * k;
+    const int64_t gs = (int64_t)t0 * k + s;
+    const int n = s_node[s];
     if (n < 0) {
-      lv.slot_row[s] = -1;
-      lv.slot_flags[s] = 0;
+      lv.slot_row[gs] = -1;
+      lv.slot_flags[gs] = 0;
+      if (l == a.L && a.w) a.slot_wsum[gs] = 0.f;
       continue;
     }
-    const int row = lv.hist[(int64_t)n * a.n_tok_tiles + tt] + __popcll(s_mask[n] & below);
-    lv.slot_row[s] = row;
+    const int row = lv.hist[(int64_t)n * a.n_tok_tiles + tt] + __popcll(s_mask[n] & ((1ull << t) - 1ull));
+    lv.slot_row[gs] = row;
     bool first = true;
-    for (int j2 = 0; j2 < j; ++j2) first &= (s_node[lane][j2] != n);
-    if (first) lv.row_token[row] = t;
+    for (int j2 = 0; j2 < j; ++j2) first &= (s_node[t * k + j2] != n);
+    if (first) lv.row_token[row] = t0 + t;
     const bool work = lv.work_all || lv.fac[n] >= 0;
-    lv.slot_flags[s] = (uint8_t)((first ? 1 : 0) | (work ? 2 : 0));
-  }
-  // expert level: summed weight of each distinct expert, on its first slot
-  if (l == a.L && a.w) {
-    for (int j = 0; j < a.k; ++j) {
-      const int n = s_node[lane][j];
-      bool first = n >= 0;
-      for (int j2 = 0; j2 < j; ++j2) first &= (s_node[lane][j2] != n);
+    lv.slot_flags[gs] = (uint8_t)((first ? 1 : 0) | (work ? 2 : 0));
+    // expert level: summed weight of each distinct expert, on its first slot
+    if (l == a.L && a.w) {
       float ws = 0.f;
       if (first)
-        for (int j2 = j; j2 < a.k; ++j2)
-          if (s_node[lane][j2] == n) ws += a.w[base + j2];
-      a.slot_wsum[base + j] = ws;
+        for (int j2 = j; j2 < k; ++j2)
+          if (s_node[t * k + j2] == n) ws += a.w[(int64_t)(t0 + t) * k + j2];
+      a.slot_wsum[gs] = ws;
     }
   }
 }
@@ -292,15 +332,6 @@ __device__ inline int small_node(const SmallLds& S, const PrepareArgs& pa, int L
   return at;
 }
 
-// Workgroup barrier for LDS communication only: waits for this wave's LDS
-// operations, not for its global stores (which nothing in the workgroup
-// reads back), unlike __syncthreads().
-__device__ __forceinline__ void lds_barrier() {
-  asm volatile("" ::: "memory");
-  __builtin_amdgcn_s_waitcnt(0xF | (0x7 << 4) | (0x3 << 14));  // lgkmcnt(0)
-  __builtin_amdgcn_s_barrier();
-  asm volatile("" ::: "memory");
-}
 
 __device__ inline int wave_exscan(int v, int& total) {
   const int lane = threadIdx.x & 63;
@@ -488,13 +519,15 @@ hipError_t launch_bucket_hist(const BucketArgs& a, hipStream_t s) {
 }
 
 hipError_t launch_bucket_scan(const BucketArgs& a, hipStream_t s) {
-  hipLaunchKernelGGL(k_bucket_scan, dim3(a.L + 1), dim3(1024), 0, s, a);
+  int mx = 1;
+  for (int l = 0; l <= a.L; ++l) mx = a.lv[l].n_nodes > mx ? a.lv[l].n_nodes : mx;
+  hipLaunchKernelGGL(k_bucket_scan, dim3(a.L + 1), dim3(1024), (size_t)(mx + 1) * sizeof(int), s, a);
   return hipGetLastError();
 }
 
 hipError_t launch_bucket_place(const BucketArgs& a, hipStream_t s) {
   if (a.n_tok_tiles == 0) return hipSuccess;
-  hipLaunchKernelGGL(k_bucket_place, dim3(a.n_tok_tiles, a.L + 1), dim3(64), mask_lds_bytes(a), s, a);
+  hipLaunchKernelGGL(k_bucket_place, dim3(a.n_tok_tiles, a.L + 1), dim3(kPlaceThr), mask_lds_bytes(a), s, a);
   return hipGetLastError();
 }
 
