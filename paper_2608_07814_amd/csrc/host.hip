@@ -538,7 +538,7 @@ lx_status run(const lx_tree_layer& t, int T, int k, const void* x, const int32_t
     g.C = (float*)(W + q.z);
     if (fast[l]) {
       g.ldc = 4 * (int64_t)r;  // [gate hi | gate lo | up hi | up lo], bf16
-      LX_TRY(big(kLowIn[l], g, l, 128, 2 * r <= 128 ? 128 : 256, true, T));
+      LX_TRY(big(kLowIn[l], g, l, kBigBM, 2 * r <= 128 ? 128 : 256, true, T));
     } else {
       g.ldc = 2 * (int64_t)r;
       g.c_coloff[1] = r;
@@ -663,7 +663,7 @@ lx_status run(const lx_tree_layer& t, int T, int k, const void* x, const int32_t
       g.K = 2 * f;
       g.Kb = f;
       g.ldc = 2 * (int64_t)r;  // [hi | lo], bf16
-      LX_TRY(big(kDownIn[l], g, l, 128, r <= 64 ? 64 : 128, true, q.rows_max));
+      LX_TRY(big(kDownIn[l], g, l, kBigBM, r <= 64 ? 64 : 128, true, q.rows_max));
     } else {
       g.lda = f;
       g.K = f;
