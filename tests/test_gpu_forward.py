@@ -118,6 +118,19 @@ def test_cfg4_tree_small():
     assert e <= TOL_DESIGN
 
 
+def test_cfg4_tree_mixed_kernels():
+    """T=100: the root level runs on the large-tile kernel while the sub and
+    leaf levels (few rows per node) run on the skinny kernel."""
+    require_gpu()
+    say("forward cfg4 T=100")
+    p = make_problem(4, T=100)
+    got = gpu_forward(p)
+    e = err_ratio(got, _oracle(p))
+    say(f"  err/RMS = {e:.3e}")
+    assert e <= TOL_BF16
+    assert e <= TOL_DESIGN
+
+
 def test_cfg4_tree_full_size_sampled():
     require_gpu()
     say("forward cfg4 T=8192 sampled")
