@@ -100,6 +100,13 @@ struct Plan {
   int T, k, E, L, d, f, NT;
   LevelPlan lv[kMaxLvl];
   size_t flags, anc, slot_wsum, total;
+  // kernel choice per level (shapes only): "fast" levels keep every
+  // GEMM-feeding intermediate as a bf16 (hi, lo) pair and run on the
+  // large-tile or skinny kernel; "skinny" ones (few rows per node) on the
+  // skinny kernel; batch: every level with GEMM work is skinny (the
+  // independent products of a phase share a launch).
+  bool fast[kMaxLvl] = {}, skinny[kMaxLvl] = {};
+  bool batch = false;
 };
 
 int level_nodes(const lx_tree_layer& t, int l) { return l == 0 ? t.n_anchors : t.levels[l - 1].n_nodes; }
@@ -119,6 +126,30 @@ Plan make_plan(const lx_tree_layer& t, int T, int k) {
     off = align_up(off + std::max<size_t>(bytes, 16));
     return o;
   };
+  {
+    const int64_t two31 = (int64_t)1 << 31;
+    const int64_t rows0 = (int64_t)T * std::min(k, t.n_anchors);
+    p.fast[0] = t.dtype == LX_BF16 && p.d % 64 == 0 && p.f % 64 == 0 && (int64_t)T * p.d < two31 &&
+                rows0 * 2 * p.f < two31;
+    for (int l = 1; l <= p.L; ++l) {
+      const int r = t.levels[l - 1].rank;
+      const int64_t R = (int64_t)T * std::min(k, t.levels[l - 1].n_nodes);
+      // rank multiple of 64: every 64-wide K-slab of a (hi | lo) operand lies
+      // inside one half, so its weight columns stay inside the weight row
+      p.fast[l] = p.fast[0] && r % 64 == 0 && R * 2 * p.f < two31 && R * 4 * r < two31;
+    }
+    // Fast levels with few rows per node (decode-sized batches) stream their
+    // weights through the skinny kernel; the large tiles would spend their
+    // time on MFMA work over padding rows.
+    p.batch = true;
+    for (int l = 0; l <= p.L; ++l) {
+      const int N = level_nodes(t, l);
+      const int64_t R = (int64_t)T * std::min(k, N);
+      p.skinny[l] = p.fast[l] && R / std::max(N, 1) <= 64;
+      const bool work = l == 0 || t.levels[l - 1].n_factors > 0;
+      if (work && !p.skinny[l]) p.batch = false;
+    }
+  }
   p.flags = take(16);  // first: lx_read_device_status reads offset 0
   p.anc = take((size_t)(p.L + 1) * p.E * 4);
   const size_t tk = (size_t)T * k;
@@ -363,26 +394,8 @@ lx_status run(const lx_tree_layer& t, int T, int k, const void* x, const int32_t
   }
 
   const lx_dtype dt = t.dtype;
-  const int64_t two31 = (int64_t)1 << 31;
-  // "Fast" levels keep every GEMM-feeding intermediate as a bf16 (hi, lo)
-  // pair and run all their GEMMs on the large-tile or skinny kernel; other
-  // levels use fp32 intermediates and the register-staged kernel (hi/lo
-  // split on load).
-  bool fast[kMaxLvl] = {};
-  fast[0] = dt == LX_BF16 && d % 64 == 0 && f % 64 == 0 && (int64_t)T * d < two31 &&
-            P.lv[0].rows_max * 2 * f < two31;
-  for (int l = 1; l <= L; ++l) {
-    const int r = t.levels[l - 1].rank;
-    const int64_t R = P.lv[l].rows_max;
-    // rank multiple of 64: every 64-wide K-slab of a (hi | lo) operand lies
-    // inside one half, so its weight columns stay inside the weight row
-    fast[l] = fast[0] && r % 64 == 0 && R * 2 * f < two31 && R * 4 * r < two31;
-  }
-  // Fast levels with few rows per node (decode-sized batches) stream their
-  // weights through the skinny kernel; the large tiles would spend their
-  // time on MFMA work over padding rows.
-  bool skinny[kMaxLvl] = {};
-  for (int l = 0; l <= L; ++l) skinny[l] = fast[l] && P.lv[l].rows_max / std::max(P.lv[l].N, 1) <= 64;
+  const bool* const fast = P.fast;
+  const bool* const skinny = P.skinny;
 
   BucketArgs ba{};
   ba.T = T;
@@ -427,11 +440,7 @@ lx_status run(const lx_tree_layer& t, int T, int k, const void* x, const int32_t
 
   // Decode-sized batches (every level with GEMM work on the skinny kernel):
   // the independent products of one phase share a launch.
-  bool batch_mode = true;
-  for (int l = 0; l <= L; ++l) {
-    const bool work = l == 0 || t.levels[l - 1].n_factors > 0;
-    if (work && !skinny[l]) batch_mode = false;
-  }
+  const bool batch_mode = P.batch;
   struct Pend {
     GemmArgs g;
     bool hilo;
