@@ -50,6 +50,14 @@ constexpr int BK2 = 64, NXCD = 8;
 
 __device__ __forceinline__ int swz2(int row) { return (row ^ (row >> 3)) & 7; }
 __device__ __forceinline__ int lds_off2(int row, int kc) { return row * BK2 + ((kc ^ swz2(row)) << 3); }
+// Large-tile swizzle: rows r and r + 1 share a 256-byte bank window, so the
+// 16 lanes a ds_read_b128 serves together (rows r..r+15, one chunk) land on
+// 16 distinct 16-byte bank groups when the chunk is XORed with (row / 2) % 8.
+// Every fragment row of a lane (row = 32 * i + (lane % 32) + a multiple of 64)
+// has the same swizzle, so a lane's k-step offsets are shared by all its
+// fragments and the row steps become immediate offsets.
+__device__ __forceinline__ int swzb(int row) { return (row >> 1) & 7; }
+__device__ __forceinline__ int lds_offb(int row, int kc) { return row * BK2 + ((kc ^ swzb(row)) << 3); }
 
 // One 16-byte direct HBM -> LDS load per lane: lane i writes LDS bytes
 // [lds_base + 16 i, lds_base + 16 i + 16). lds_base must be wave-uniform. The
@@ -178,7 +186,7 @@ void k_gemm_big(GemmArgs p, int ntn) {
     for (int j = 0; j < A_ROUNDS; ++j) {
       const int Ps = j * NTHR + tid;
       const int row = Ps >> 3;
-      const int c = (Ps & 7) ^ swz2(row);
+      const int c = (Ps & 7) ^ swzb(row);
       const int r = row < te.nrows ? row : te.nrows - 1;
       const int src = p.a_rows ? p.a_rows[te.row0 + r] : te.row0 + r;
       aoff[j] = (uint32_t)src * (uint32_t)p.lda + (uint32_t)(akoff + c * 8);
@@ -188,7 +196,7 @@ void k_gemm_big(GemmArgs p, int ntn) {
     for (int j = 0; j < B_ROUNDS; ++j) {
       const int Ps = j * NTHR + tid;
       const int row = Ps >> 3;
-      const int c = (Ps & 7) ^ swz2(row);
+      const int c = (Ps & 7) ^ swzb(row);
       const int n = n0 + row < ncol ? n0 + row : ncol - 1;
       bptr[j] = (n < p.ncols[0] ? Bw0 + (int64_t)n * Kb : Bw1 + (int64_t)(n - p.ncols[0]) * Kb) + c * 8;
     }
@@ -224,9 +232,9 @@ void k_gemm_big(GemmArgs p, int ntn) {
   do {                                                                              \
     const int kc_ = (KS) * 2 + (lane >> 5);                                         \
     _Pragma("unroll") for (int mi = 0; mi < MI; ++mi)                               \
-      FA[mi] = *(const bf16x8*)&(SA_)[lds_off2(wm * WM + mi * 32 + (lane & 31), kc_)]; \
+      FA[mi] = *(const bf16x8*)&(SA_)[lds_offb(wm * WM + mi * 32 + (lane & 31), kc_)]; \
     _Pragma("unroll") for (int ni = 0; ni < NI; ++ni)                               \
-      FB[ni] = *(const bf16x8*)&(SB_)[lds_off2(wn * WN + ni * 32 + (lane & 31), kc_)]; \
+      FB[ni] = *(const bf16x8*)&(SB_)[lds_offb(wn * WN + ni * 32 + (lane & 31), kc_)]; \
   } while (0)
 #define LX_MFMAS(FA, FB)                                                            \
   do {                                                                              \
@@ -236,15 +244,6 @@ void k_gemm_big(GemmArgs p, int ntn) {
   } while (0)
 #define LX_COMPUTE(SA_, SB_)                                                        \
   do {                                                                              \
-    if constexpr (BigCfg<BM, BN>::WPE > 1) {                                        \
-      /* two wavefronts per SIMD cover each other's LDS latency: single */          \
-      /* fragment buffer, fewer registers */                                        \
-      _Pragma("unroll") for (int ks_ = 0; ks_ < 4; ++ks_) {                         \
-        LX_FRAG(SA_, SB_, ks_, fa0, fb0);                                           \
-        LX_MFMAS(fa0, fb0);                                                         \
-      }                                                                             \
-      break;                                                                        \
-    }                                                                               \
     LX_FRAG(SA_, SB_, 0, fa0, fb0);                                                 \
     __builtin_amdgcn_sched_barrier(0);                                              \
     LX_FRAG(SA_, SB_, 1, fa1, fb1);                                                 \

@@ -1,8 +1,7 @@
 // Per-token kernels: SwiGLU with the amortized weighted reduction, and the
-// deterministic combine. One 64-thread workgroup per (token, 256-column
-// chunk); every thread owns 4 consecutive neurons (SwiGLU) or output columns
-// (combine), so all accesses are 16-byte vectors and small batches still
-// spread over many workgroups.
+// deterministic combine. SwiGLU runs one workgroup per (token, 256-neuron
+// chunk), combine one per token; every thread owns 4 consecutive neurons
+// (SwiGLU) or output columns (combine), so all accesses are 16-byte vectors.
 //
 // For a token t with selected experts e_j (j ascending), every tree level l
 // has one row per distinct level-l node among the e_j (from the bucketing,
@@ -121,47 +120,63 @@ __global__ __launch_bounds__(kTokThr * kSlotGroups) void k_swiglu_reduce(TokenAr
   }
 }
 
-// Combine: the token's rows to sum (first slot of a row that does work), in
-// (level, slot) order, are listed once; each thread then loads 8 rows at a
-// time before adding them in that order.
-__global__ __launch_bounds__(kTokThr) void k_combine(TokenArgs a) {
-  __shared__ TokenMeta m;
+// Combine, one workgroup per token (whole output rows, so every row of the
+// token is read as one contiguous stretch): wavefront 0 lists the token's rows
+// to sum (first slot of a row that does work) in (level, slot) order with a
+// ballot compaction; then every thread sums its 4 columns over that list, 16
+// row loads in flight at a time, adding in list order.
+constexpr int kCombMaxThr = 512;
+__global__ __launch_bounds__(kCombMaxThr) void k_combine(TokenArgs a) {
   __shared__ const float* s_rows[kMaxLvl * LX_MAX_K];
   __shared__ int s_n;
   const int t = blockIdx.x;
-  token_meta(a, t, m);
-  __syncthreads();
   const int k = a.k, L = a.L, d = a.d;
-  if (threadIdx.x == 0) {
-    int n = 0;
-    for (int l = 0; l <= L; ++l)
-      for (int j = 0; j < k; ++j)
-        if ((m.fl[l][j] & 3) == 3) s_rows[n++] = a.y[l] + (int64_t)m.row[l][j] * d;
-    s_n = n;
+  if (threadIdx.x < 64) {
+    const int lane = threadIdx.x;
+    const int nq = (L + 1) * k;
+    int base = 0;
+    for (int q0 = 0; q0 < nq; q0 += 64) {
+      const int q = q0 + lane;
+      bool take = false;
+      const float* ptr = nullptr;
+      if (q < nq) {
+        const int l = q / k, j = q - l * k;
+        const int64_t sl = (int64_t)t * k + j;
+        const int row = a.slot_row[l][sl];  // loaded alongside the flags
+        if ((a.slot_flags[l][sl] & 3) == 3) {
+          take = true;
+          ptr = a.y[l] + (int64_t)row * d;
+        }
+      }
+      const uint64_t bal = __ballot(take);
+      if (take) s_rows[base + __popcll(bal & ((1ull << lane) - 1))] = ptr;
+      base += __popcll(bal);
+    }
+    if (lane == 0) s_n = base;
   }
   __syncthreads();
-  const int c = (blockIdx.y * blockDim.x + threadIdx.x) * 4;
-  if (c >= d) return;
   const int n = s_n;
-  float4 acc = make_float4(0.f, 0.f, 0.f, 0.f);
-  for (int b = 0; b < n; b += 8) {
-    float4 v[8];
+  for (int c = threadIdx.x * 4; c < d; c += blockDim.x * 4) {
+    float4 acc = make_float4(0.f, 0.f, 0.f, 0.f);
+    for (int b = 0; b < n; b += 16) {
+      float4 v[16];
 #pragma unroll
-    for (int i = 0; i < 8; ++i)
-      if (b + i < n) v[i] = ld4(s_rows[b + i] + c);
+      for (int i = 0; i < 16; ++i)
+        if (b + i < n) v[i] = ld4(s_rows[b + i] + c);
 #pragma unroll
-    for (int i = 0; i < 8; ++i)
-      if (b + i < n) add4(acc, v[i]);
-  }
-  if (a.out_dtype == LX_F32) {
-    *(float4*)((float*)a.out + (int64_t)t * d + c) = acc;
-  } else {
-    bf16x4 o;
-    o[0] = (__bf16)acc.x;
-    o[1] = (__bf16)acc.y;
-    o[2] = (__bf16)acc.z;
-    o[3] = (__bf16)acc.w;
-    *(bf16x4*)((uint16_t*)a.out + (int64_t)t * d + c) = o;
+      for (int i = 0; i < 16; ++i)
+        if (b + i < n) add4(acc, v[i]);
+    }
+    if (a.out_dtype == LX_F32) {
+      *(float4*)((float*)a.out + (int64_t)t * d + c) = acc;
+    } else {
+      bf16x4 o;
+      o[0] = (__bf16)acc.x;
+      o[1] = (__bf16)acc.y;
+      o[2] = (__bf16)acc.z;
+      o[3] = (__bf16)acc.w;
+      *(bf16x4*)((uint16_t*)a.out + (int64_t)t * d + c) = o;
+    }
   }
 }
 
@@ -177,7 +192,9 @@ hipError_t launch_swiglu_reduce(const TokenArgs& a, hipStream_t s) {
 
 hipError_t launch_combine(const TokenArgs& a, hipStream_t s) {
   if (a.T == 0) return hipSuccess;
-  hipLaunchKernelGGL(k_combine, dim3(a.T, (a.d + kTokCols - 1) / kTokCols), dim3(kTokThr), 0, s, a);
+  int thr = (a.d / 4 + 63) / 64 * 64;
+  thr = thr < 64 ? 64 : thr > kCombMaxThr ? kCombMaxThr : thr;
+  hipLaunchKernelGGL(k_combine, dim3(a.T), dim3(thr), 0, s, a);
   return hipGetLastError();
 }
 
