@@ -443,7 +443,7 @@ lx_status run(const lx_tree_layer& t, int T, int k, const void* x, const int32_t
   const bool batch_mode = P.batch;
   struct Pend {
     GemmArgs g;
-    bool hilo;
+    int ofmt;
     int tiles;
     const char* name;
   };
@@ -452,21 +452,21 @@ lx_status run(const lx_tree_layer& t, int T, int k, const void* x, const int32_t
   auto flush = [&]() -> lx_status {
     if (npend == 0) return LX_OK;
     GemmArgs g[kSkinnyMaxProblems];
-    bool hilo[kSkinnyMaxProblems];
+    int ofmt[kSkinnyMaxProblems];
     int tiles[kSkinnyMaxProblems];
     std::string name;
     for (int i = 0; i < npend; ++i) {
       g[i] = pend[i].g;
-      hilo[i] = pend[i].hilo;
+      ofmt[i] = pend[i].ofmt;
       tiles[i] = pend[i].tiles;
       name += (i ? "+" : "") + std::string(pend[i].name);
     }
     const int n = npend;
     npend = 0;
-    LX_LAUNCH(intern_name(name), launch_gemm_skinny_batch(g, hilo, tiles, n, lstream));
+    LX_LAUNCH(intern_name(name), launch_gemm_skinny_batch(g, ofmt, tiles, n, lstream));
     return LX_OK;
   };
-  auto big = [&](const char* name, GemmArgs g, int l, int bm, int bn, bool hilo,
+  auto big = [&](const char* name, GemmArgs g, int l, int bm, int bn, int ofmt,
                  int64_t a_rows_total) -> lx_status {
     const LevelPlan& q = P.lv[l];
     if (!g.B[1]) g.B[1] = g.B[0];
@@ -480,10 +480,10 @@ lx_status run(const lx_tree_layer& t, int T, int k, const void* x, const int32_t
           const lx_status st = flush();
           if (st != LX_OK) return st;
         }
-        pend[npend++] = Pend{g, hilo, (int)q.tiles_max[kTabSkinny], name};
+        pend[npend++] = Pend{g, ofmt, (int)q.tiles_max[kTabSkinny], name};
         return LX_OK;
       }
-      LX_LAUNCH(name, launch_gemm_skinny(g, hilo, (int)q.tiles_max[kTabSkinny], lstream));
+      LX_LAUNCH(name, launch_gemm_skinny(g, ofmt, (int)q.tiles_max[kTabSkinny], lstream));
       return LX_OK;
     }
     if (!gemm_big_ok(g, bn, a_rows_total))
@@ -492,7 +492,7 @@ lx_status run(const lx_tree_layer& t, int T, int k, const void* x, const int32_t
     if (q.bm[tab] != bm) return fail(LX_ERR_UNSUPPORTED, std::string(name) + ": no tile table for this height");
     g.tiles = ba.lv[l].tiles[tab];
     g.n_tiles = ba.lv[l].n_tiles[tab];
-    LX_LAUNCH(name, launch_gemm_big(g, bm, bn, hilo, (int)q.tiles_max[tab], lstream));
+    LX_LAUNCH(name, launch_gemm_big(g, bm, bn, ofmt, (int)q.tiles_max[tab], lstream));
     return LX_OK;
   };
   auto small = [&](const char* name, GemmArgs g, int l, AMode am) -> lx_status {
@@ -547,7 +547,7 @@ lx_status run(const lx_tree_layer& t, int T, int k, const void* x, const int32_t
     g.C = (float*)(W + q.z);
     if (fast[l]) {
       g.ldc = 4 * (int64_t)r;  // [gate hi | gate lo | up hi | up lo], bf16
-      LX_TRY(big(kLowIn[l], g, l, kBigBM, 2 * r <= 128 ? 128 : 256, true, T));
+      LX_TRY(big(kLowIn[l], g, l, kBigBM, 2 * r <= 128 ? 128 : 256, OUT_HILO, T));
     } else {
       g.ldc = 2 * (int64_t)r;
       g.c_coloff[1] = r;
@@ -571,7 +571,7 @@ lx_status run(const lx_tree_layer& t, int T, int k, const void* x, const int32_t
     g.ldc = 2 * (int64_t)f;
     g.c_coloff[1] = f;
     if (fast[0])
-      LX_TRY(big("anchor_gate_up", g, 0, kBigBM, 256, false, T));
+      LX_TRY(big("anchor_gate_up", g, 0, kBigBM, 256, OUT_F24, T));
     else
       LX_TRY(small("anchor_gate_up", g, 0, A_BF16));
   }
@@ -598,7 +598,7 @@ lx_status run(const lx_tree_layer& t, int T, int k, const void* x, const int32_t
       h.K = 2 * r;
       h.Kb = r;
       // gate and up read different z columns: tiles must not straddle them
-      LX_TRY(big(kLowOut[l], h, l, kBigBM, f % 256 == 0 ? 256 : f % 128 == 0 ? 128 : 64, false, q.rows_max));
+      LX_TRY(big(kLowOut[l], h, l, kBigBM, f % 256 == 0 ? 256 : f % 128 == 0 ? 128 : 64, OUT_F24, q.rows_max));
     } else {
       h.lda = 2 * (int64_t)r;
       h.a_koff[1] = r;
@@ -625,6 +625,7 @@ lx_status run(const lx_tree_layer& t, int T, int k, const void* x, const int32_t
     ta.dgu[l] = (const float*)(W + q.gu);
     ta.hbar[l] = (float*)(W + q.hbar);
     ta.hbar_hilo[l] = fast[l] ? 1 : 0;
+    ta.f24[l] = fast[l] ? 1 : 0;
     ta.y[l] = (const float*)(W + q.y);
   }
   ta.out = out;
@@ -647,7 +648,7 @@ lx_status run(const lx_tree_layer& t, int T, int k, const void* x, const int32_t
       g.lda = 2 * (int64_t)f;
       g.K = 2 * f;
       g.Kb = f;
-      LX_TRY(big("anchor_down", g, 0, kBigBM, 256, false, q.rows_max));
+      LX_TRY(big("anchor_down", g, 0, kBigBM, 256, OUT_F24, q.rows_max));
     } else {
       g.lda = f;
       g.K = f;
@@ -672,7 +673,7 @@ lx_status run(const lx_tree_layer& t, int T, int k, const void* x, const int32_t
       g.K = 2 * f;
       g.Kb = f;
       g.ldc = 2 * (int64_t)r;  // [hi | lo], bf16
-      LX_TRY(big(kDownIn[l], g, l, kBigBM, r <= 64 ? 64 : 128, true, q.rows_max));
+      LX_TRY(big(kDownIn[l], g, l, kBigBM, r <= 64 ? 64 : 128, OUT_HILO, q.rows_max));
     } else {
       g.lda = f;
       g.K = f;
@@ -698,7 +699,7 @@ lx_status run(const lx_tree_layer& t, int T, int k, const void* x, const int32_t
       h.lda = 2 * (int64_t)r;
       h.K = 2 * r;
       h.Kb = r;
-      LX_TRY(big(kDownOut[l], h, l, kBigBM, 256, false, q.rows_max));
+      LX_TRY(big(kDownOut[l], h, l, kBigBM, 256, OUT_F24, q.rows_max));
     } else {
       h.lda = r;
       h.K = r;

@@ -20,8 +20,8 @@
 //   * K may be a multiple of the weights' row length Kb: A = [A_hi | A_lo]
 //     against the same W, i.e. C = (A_hi + A_lo) W^T, which keeps ~16 bits of
 //     an fp32 intermediate at bf16 MFMA rate;
-//   * output either fp32, or a bf16 (hi, lo) pair ready to feed the next GEMM
-//     as its two K-halves;
+//   * output fp32, a bf16 (hi, lo) pair ready to feed the next GEMM as its
+//     two K-halves, or f24 (rows read back only by the elementwise kernels);
 //   * persistent: the grid is at most one workgroup per compute unit and each
 //     workgroup loops over (tile, n-tile) work items, so the epilogue of one
 //     item and the prologue loads of the next are not separated by a
@@ -118,7 +118,7 @@ struct BigCfg {
   static constexpr int WPE = NW / 4;  // wavefronts per SIMD
 };
 
-template <int BM, int BN, bool OUT_HILO>
+template <int BM, int BN, int OUT>
 __global__ __launch_bounds__((BigCfg<BM, BN>::NTHR), 1)
 __attribute__((amdgpu_waves_per_eu(BigCfg<BM, BN>::WPE, BigCfg<BM, BN>::WPE)))
 void k_gemm_big(GemmArgs p, int ntn) {
@@ -342,7 +342,7 @@ void k_gemm_big(GemmArgs p, int ntn) {
           const float4 v = *(const float4*)&ep[rr * PITCH + c4];
           const int r = wm * WM + mi * 32 + rr;
           if (r >= te.nrows || col >= ncol) continue;
-          if (OUT_HILO) {
+          if (OUT == OUT_HILO) {
             // part p, local column c -> hi at base_p + c, lo at base_p + ncols[p] + c
             const int pp = col < p.ncols[0] ? 0 : 1;
             const int c = pp ? col - p.ncols[0] : col;
@@ -360,6 +360,8 @@ void k_gemm_big(GemmArgs p, int ntn) {
             __bf16* const rowp = (__bf16*)p.C + (int64_t)(te.row0 + r) * p.ldc;
             *(bf16x4*)(rowp + hi_col) = h;
             *(bf16x4*)(rowp + lo_col) = l;
+          } else if (OUT == OUT_F24) {
+            *(F24x4*)((uint8_t*)p.C + ((int64_t)(te.row0 + r) * p.ldc + col) * 3) = f24_pack(v);
           } else {
             *(float4*)(p.C + (int64_t)(te.row0 + r) * p.ldc + col) = v;
           }
@@ -396,7 +398,7 @@ __global__ __launch_bounds__(SK_THR) void k_gemm_skinny(SkinnyBatch b) {
   while (pi + 1 < b.n && (int)blockIdx.x >= b.base[pi + 1]) ++pi;
   const GemmArgs& p = b.g[pi];
   const int ntn = b.ntn[pi];
-  const bool out_hilo = b.hilo[pi] != 0;
+  const int ofmt = b.ofmt[pi];
   const int wg = (int)blockIdx.x - b.base[pi];
 
   // one work item per workgroup, XCD-contiguous order (workgroups >= items)
@@ -507,7 +509,7 @@ __global__ __launch_bounds__(SK_THR) void k_gemm_skinny(SkinnyBatch b) {
     const int r = ps * RPP + lane / LPR;
     const float4 v = *(const float4*)&ep[r * PITCH + c4];
     if (r >= te.nrows || col >= ncol) continue;
-    if (out_hilo) {
+    if (ofmt == OUT_HILO) {
       const int pp = col < p.ncols[0] ? 0 : 1;
       const int c = pp ? col - p.ncols[0] : col;
       const int hi_col = (pp ? 2 * p.ncols[0] : 0) + c;
@@ -524,6 +526,8 @@ __global__ __launch_bounds__(SK_THR) void k_gemm_skinny(SkinnyBatch b) {
       __bf16* const rowp = (__bf16*)p.C + (int64_t)(te.row0 + r) * p.ldc;
       *(bf16x4*)(rowp + hi_col) = h;
       *(bf16x4*)(rowp + lo_col) = l;
+    } else if (ofmt == OUT_F24) {
+      *(F24x4*)((uint8_t*)p.C + ((int64_t)(te.row0 + r) * p.ldc + col) * 3) = f24_pack(v);
     } else {
       *(float4*)(p.C + (int64_t)(te.row0 + r) * p.ldc + col) = v;
     }
@@ -531,11 +535,13 @@ __global__ __launch_bounds__(SK_THR) void k_gemm_skinny(SkinnyBatch b) {
 }
 
 template <int BM, int BN>
-hipError_t launch_bn(const GemmArgs& g, bool hilo, int grid, int ntn, hipStream_t s) {
-  if (hilo)
-    hipLaunchKernelGGL((k_gemm_big<BM, BN, true>), dim3(grid), dim3(BigCfg<BM, BN>::NTHR), 0, s, g, ntn);
+hipError_t launch_bn(const GemmArgs& g, int ofmt, int grid, int ntn, hipStream_t s) {
+  if (ofmt == OUT_HILO)
+    hipLaunchKernelGGL((k_gemm_big<BM, BN, OUT_HILO>), dim3(grid), dim3(BigCfg<BM, BN>::NTHR), 0, s, g, ntn);
+  else if (ofmt == OUT_F24)
+    hipLaunchKernelGGL((k_gemm_big<BM, BN, OUT_F24>), dim3(grid), dim3(BigCfg<BM, BN>::NTHR), 0, s, g, ntn);
   else
-    hipLaunchKernelGGL((k_gemm_big<BM, BN, false>), dim3(grid), dim3(BigCfg<BM, BN>::NTHR), 0, s, g, ntn);
+    hipLaunchKernelGGL((k_gemm_big<BM, BN, OUT_F32>), dim3(grid), dim3(BigCfg<BM, BN>::NTHR), 0, s, g, ntn);
   return hipGetLastError();
 }
 
@@ -570,23 +576,23 @@ int grid_cap() {
 }
 }  // namespace
 
-hipError_t launch_gemm_big(const GemmArgs& g, int bm, int bn, bool out_hilo, int grid_tiles, hipStream_t s) {
+hipError_t launch_gemm_big(const GemmArgs& g, int bm, int bn, int ofmt, int grid_tiles, hipStream_t s) {
   const int ntn = (g.ncols[0] + g.ncols[1] + bn - 1) / bn;
   int grid = grid_tiles * ntn;  // upper bound on work items
   if (grid <= 0) return hipSuccess;
   const int cap = grid_cap();
   if (grid > cap) grid = cap;
   if (bm == 256) {
-    if (bn == 256) return launch_bn<256, 256>(g, out_hilo, grid, ntn, s);
-    if (bn == 128) return launch_bn<256, 128>(g, out_hilo, grid, ntn, s);
-    return launch_bn<256, 64>(g, out_hilo, grid, ntn, s);
+    if (bn == 256) return launch_bn<256, 256>(g, ofmt, grid, ntn, s);
+    if (bn == 128) return launch_bn<256, 128>(g, ofmt, grid, ntn, s);
+    return launch_bn<256, 64>(g, ofmt, grid, ntn, s);
   }
-  if (bn == 256) return launch_bn<128, 256>(g, out_hilo, grid, ntn, s);
-  if (bn == 128) return launch_bn<128, 128>(g, out_hilo, grid, ntn, s);
-  return launch_bn<128, 64>(g, out_hilo, grid, ntn, s);
+  if (bn == 256) return launch_bn<128, 256>(g, ofmt, grid, ntn, s);
+  if (bn == 128) return launch_bn<128, 128>(g, ofmt, grid, ntn, s);
+  return launch_bn<128, 64>(g, ofmt, grid, ntn, s);
 }
 
-hipError_t launch_gemm_skinny_batch(const GemmArgs* g, const bool* out_hilo, const int* grid_tiles, int n,
+hipError_t launch_gemm_skinny_batch(const GemmArgs* g, const int* ofmt, const int* grid_tiles, int n,
                                     hipStream_t s) {
   if (n < 1 || n > kSkinnyMaxProblems) return hipErrorInvalidValue;
   SkinnyBatch b{};
@@ -594,7 +600,7 @@ hipError_t launch_gemm_skinny_batch(const GemmArgs* g, const bool* out_hilo, con
   for (int i = 0; i < n; ++i) {
     b.g[i] = g[i];
     b.ntn[i] = (g[i].ncols[0] + g[i].ncols[1] + kSkinnyBN - 1) / kSkinnyBN;
-    b.hilo[i] = out_hilo[i] ? 1 : 0;
+    b.ofmt[i] = ofmt[i];
     b.base[i] = wg;
     const int items = grid_tiles[i] * b.ntn[i];  // >= work items of problem i
     wg += (items + NXCD - 1) / NXCD * NXCD;
@@ -611,8 +617,8 @@ hipError_t launch_gemm_skinny_batch(const GemmArgs* g, const bool* out_hilo, con
   return hipGetLastError();
 }
 
-hipError_t launch_gemm_skinny(const GemmArgs& g, bool out_hilo, int grid_tiles, hipStream_t s) {
-  return launch_gemm_skinny_batch(&g, &out_hilo, &grid_tiles, 1, s);
+hipError_t launch_gemm_skinny(const GemmArgs& g, int ofmt, int grid_tiles, hipStream_t s) {
+  return launch_gemm_skinny_batch(&g, &ofmt, &grid_tiles, 1, s);
 }
 
 }  // namespace lx

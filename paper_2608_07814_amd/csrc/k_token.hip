@@ -1,7 +1,9 @@
 // Per-token kernels: SwiGLU with the amortized weighted reduction, and the
 // deterministic combine. SwiGLU runs one workgroup per (token, 256-neuron
 // chunk), combine one per token; every thread owns 4 consecutive neurons
-// (SwiGLU) or output columns (combine), so all accesses are 16-byte vectors.
+// (SwiGLU) or output columns (combine), so every access is one vector: 16
+// bytes of fp32, or 12 bytes of f24 (the format of the gate|up and down rows
+// written by the bf16 GEMM kernels).
 //
 // For a token t with selected experts e_j (j ascending), every tree level l
 // has one row per distinct level-l node among the e_j (from the bucketing,
@@ -18,6 +20,8 @@
 //     level's down-projection output row, in a fixed order (level, then slot)
 //     with no atomics, so the result is bit-reproducible.
 #include "lx_internal.h"
+
+#include <type_traits>
 
 namespace lx {
 namespace {
@@ -43,6 +47,12 @@ __device__ inline void token_meta(const TokenArgs& a, int t, TokenMeta& m) {
 }
 
 __device__ __forceinline__ float4 ld4(const float* p) { return *(const float4*)p; }
+// 4 consecutive values at column c of row `row` (row length ld values) of an
+// fp32 or f24 matrix.
+__device__ __forceinline__ float4 ldrow4(const float* base, bool f24, int64_t row, int64_t ld, int c) {
+  if (f24) return f24_unpack(*(const F24x4*)((const uint8_t*)base + (row * ld + c) * 3));
+  return *(const float4*)(base + row * ld + c);
+}
 __device__ __forceinline__ void add4(float4& a, const float4& b) {
   a.x += b.x;
   a.y += b.y;
@@ -93,13 +103,13 @@ __global__ __launch_bounds__(kTokThr * kSlotGroups) void k_swiglu_reduce(TokenAr
   const bool colok = c < f;
   for (int j = sg; j < k && colok; j += nsg) {
     if (!(m.fl[L][j] & 1)) continue;  // not the first slot of a valid expert
-    const float* g0 = a.gu0 + m.row[0][j] * ld;
-    float4 g = ld4(g0 + c), u = ld4(g0 + f + c);
+    const bool f0 = a.f24[0] != 0;
+    float4 g = ldrow4(a.gu0, f0, m.row[0][j], ld, c), u = ldrow4(a.gu0, f0, m.row[0][j], ld, f + c);
     for (int l = 1; l <= L; ++l) {
       if (!(m.fl[l][j] & 2)) continue;
-      const float* dg = a.dgu[l] + m.row[l][j] * ld;
-      add4(g, ld4(dg + c));
-      add4(u, ld4(dg + f + c));
+      const bool fl = a.f24[l] != 0;
+      add4(g, ldrow4(a.dgu[l], fl, m.row[l][j], ld, c));
+      add4(u, ldrow4(a.dgu[l], fl, m.row[l][j], ld, f + c));
     }
     const float w = m.w[j];
     s_h[j * kTokThr + lane] = make_float4(w * silu_mul(g.x, u.x), w * silu_mul(g.y, u.y),
@@ -124,10 +134,12 @@ __global__ __launch_bounds__(kTokThr * kSlotGroups) void k_swiglu_reduce(TokenAr
 // token is read as one contiguous stretch): wavefront 0 lists the token's rows
 // to sum (first slot of a row that does work) in (level, slot) order with a
 // ballot compaction; then every thread sums its 4 columns over that list, 16
-// row loads in flight at a time, adding in list order.
+// row loads in flight at a time, adding in list order. Rows are fp32 or f24
+// per level; s_rows holds each row's first byte and s_f24 its format.
 constexpr int kCombMaxThr = 512;
 __global__ __launch_bounds__(kCombMaxThr) void k_combine(TokenArgs a) {
-  __shared__ const float* s_rows[kMaxLvl * LX_MAX_K];
+  __shared__ const uint8_t* s_rows[kMaxLvl * LX_MAX_K];
+  __shared__ uint8_t s_f24[kMaxLvl * LX_MAX_K];
   __shared__ int s_n;
   const int t = blockIdx.x;
   const int k = a.k, L = a.L, d = a.d;
@@ -137,19 +149,24 @@ __global__ __launch_bounds__(kCombMaxThr) void k_combine(TokenArgs a) {
     int base = 0;
     for (int q0 = 0; q0 < nq; q0 += 64) {
       const int q = q0 + lane;
-      bool take = false;
-      const float* ptr = nullptr;
+      bool take = false, f24 = false;
+      const uint8_t* ptr = nullptr;
       if (q < nq) {
         const int l = q / k, j = q - l * k;
         const int64_t sl = (int64_t)t * k + j;
         const int row = a.slot_row[l][sl];  // loaded alongside the flags
         if ((a.slot_flags[l][sl] & 3) == 3) {
           take = true;
-          ptr = a.y[l] + (int64_t)row * d;
+          f24 = a.f24[l] != 0;
+          ptr = (const uint8_t*)a.y[l] + (int64_t)row * d * (f24 ? 3 : 4);
         }
       }
       const uint64_t bal = __ballot(take);
-      if (take) s_rows[base + __popcll(bal & ((1ull << lane) - 1))] = ptr;
+      if (take) {
+        const int at = base + __popcll(bal & ((1ull << lane) - 1));
+        s_rows[at] = ptr;
+        s_f24[at] = f24 ? 1 : 0;
+      }
       base += __popcll(bal);
     }
     if (lane == 0) s_n = base;
@@ -162,7 +179,9 @@ __global__ __launch_bounds__(kCombMaxThr) void k_combine(TokenArgs a) {
       float4 v[16];
 #pragma unroll
       for (int i = 0; i < 16; ++i)
-        if (b + i < n) v[i] = ld4(s_rows[b + i] + c);
+        if (b + i < n)
+          v[i] = s_f24[b + i] ? f24_unpack(*(const F24x4*)(s_rows[b + i] + c * 3))
+                              : *(const float4*)(s_rows[b + i] + c * 4);
 #pragma unroll
       for (int i = 0; i < 16; ++i)
         if (b + i < n) add4(acc, v[i]);
@@ -180,10 +199,180 @@ __global__ __launch_bounds__(kCombMaxThr) void k_combine(TokenArgs a) {
   }
 }
 
+// Fast paths for k <= 8 slots and NL <= 2 correction levels (the flat layer
+// and the two-level tree): one workgroup per (token, column block) and no
+// LDS or barriers. The token's slot metadata is read with wavefront-uniform
+// (scalar) loads, every thread issues the loads of all its slots at once,
+// and the sums run over registers in the same order as the general kernels.
+constexpr int kFastK = 8, kFastL = 2, kFastThr = 256;
+
+// Slot metadata of token t for slots j < kFastK (rows and flags per level,
+// summed weights): lane j of every wavefront loads slot j, then each value is
+// broadcast from its lane, so the results are wavefront-uniform (absent
+// slots: row -1, flags 0).
+template <int NL>
+__device__ __forceinline__ void token_meta_fast(const TokenArgs& a, int t, int (&row)[NL + 1][kFastK],
+                                                int (&fl)[NL + 1][kFastK], float (&w)[kFastK]) {
+  const int lane = threadIdx.x & 63;
+  const bool on = lane < a.k;
+  const int64_t s = (int64_t)t * a.k + lane;
+  int rv[NL + 1], fv[NL + 1];
+#pragma unroll
+  for (int l = 0; l <= NL; ++l) {
+    rv[l] = on ? a.slot_row[l][s] : -1;
+    fv[l] = on ? a.slot_flags[l][s] : 0;
+  }
+  const float wv = on ? a.slot_wsum[s] : 0.f;
+#pragma unroll
+  for (int j = 0; j < kFastK; ++j) {
+#pragma unroll
+    for (int l = 0; l <= NL; ++l) {
+      row[l][j] = __builtin_amdgcn_readlane(rv[l], j);
+      fl[l][j] = __builtin_amdgcn_readlane(fv[l], j);
+    }
+    w[j] = __builtin_bit_cast(float, __builtin_amdgcn_readlane(__builtin_bit_cast(int, wv), j));
+  }
+}
+
+// Raw row segment (4 values at column c): loaded in one pass, converted in a
+// later one, so every load of a thread is in flight before the first use.
+template <bool F24>
+struct Raw4 {
+  using T = typename std::conditional<F24, F24x4, float4>::type;
+  T v;
+};
+template <bool F24>
+__device__ __forceinline__ Raw4<F24> ldraw(const float* base, int64_t row, int64_t ld, int c) {
+  Raw4<F24> r;
+  if constexpr (F24)
+    r.v = *(const F24x4*)((const uint8_t*)base + (row * ld + c) * 3);
+  else
+    r.v = *(const float4*)(base + row * ld + c);
+  return r;
+}
+template <bool F24>
+__device__ __forceinline__ float4 cvt(const Raw4<F24>& r) {
+  if constexpr (F24)
+    return f24_unpack(r.v);
+  else
+    return r.v;
+}
+
+template <int NL, bool F24>
+__global__ __launch_bounds__(kFastThr) void k_swiglu_fast(TokenArgs a) {
+  const int t = blockIdx.x, k = a.k, f = a.f;
+  const int c = (blockIdx.y * blockDim.x + threadIdx.x) * 4;
+  if (c >= f) return;
+  const int64_t ld = 2 * (int64_t)f;
+  int row[NL + 1][kFastK], fl[NL + 1][kFastK];
+  float w[kFastK];
+  token_meta_fast<NL>(a, t, row, fl, w);
+  // loads of every distinct expert's gate|up rows, then h = w silu(g) u
+  Raw4<F24> gv[kFastK][NL + 1], uv[kFastK][NL + 1];
+#pragma unroll
+  for (int j = 0; j < kFastK; ++j) {
+    if (!(fl[NL][j] & 1)) continue;
+    gv[j][0] = ldraw<F24>(a.gu0, row[0][j], ld, c);
+    uv[j][0] = ldraw<F24>(a.gu0, row[0][j], ld, f + c);
+#pragma unroll
+    for (int l = 1; l <= NL; ++l) {
+      if (!(fl[l][j] & 2)) continue;
+      gv[j][l] = ldraw<F24>(a.dgu[l], row[l][j], ld, c);
+      uv[j][l] = ldraw<F24>(a.dgu[l], row[l][j], ld, f + c);
+    }
+  }
+  float4 h[kFastK];
+#pragma unroll
+  for (int j = 0; j < kFastK; ++j) {
+    h[j] = make_float4(0.f, 0.f, 0.f, 0.f);
+    if (!(fl[NL][j] & 1)) continue;
+    float4 g = cvt<F24>(gv[j][0]), u = cvt<F24>(uv[j][0]);
+#pragma unroll
+    for (int l = 1; l <= NL; ++l) {
+      if (!(fl[l][j] & 2)) continue;
+      add4(g, cvt<F24>(gv[j][l]));
+      add4(u, cvt<F24>(uv[j][l]));
+    }
+    h[j] = make_float4(w[j] * silu_mul(g.x, u.x), w[j] * silu_mul(g.y, u.y), w[j] * silu_mul(g.z, u.z),
+                       w[j] * silu_mul(g.w, u.w));
+  }
+  // each level-l row that does work: the sum of its experts' h in slot order
+#pragma unroll
+  for (int l = 0; l <= NL; ++l)
+#pragma unroll
+    for (int j0 = 0; j0 < kFastK; ++j0) {
+      if ((fl[l][j0] & 3) != 3) continue;
+      float4 hs = make_float4(0.f, 0.f, 0.f, 0.f);
+#pragma unroll
+      for (int j = j0; j < kFastK; ++j)
+        if (row[l][j] == row[l][j0] && (fl[NL][j] & 1)) add4(hs, h[j]);
+      hbar_store(a.hbar[l], a.hbar_hilo[l], row[l][j0], c, f, hs);
+    }
+}
+
+template <int NL, bool F24>
+__global__ __launch_bounds__(kFastThr) void k_combine_fast(TokenArgs a) {
+  const int t = blockIdx.x, k = a.k, d = a.d;
+  const int c = (blockIdx.y * blockDim.x + threadIdx.x) * 4;
+  if (c >= d) return;
+  int row[NL + 1][kFastK], fl[NL + 1][kFastK];
+  float w[kFastK];
+  token_meta_fast<NL>(a, t, row, fl, w);
+  Raw4<F24> v[NL + 1][kFastK];
+#pragma unroll
+  for (int l = 0; l <= NL; ++l)
+#pragma unroll
+    for (int j = 0; j < kFastK; ++j)
+      if ((fl[l][j] & 3) == 3) v[l][j] = ldraw<F24>(a.y[l], row[l][j], d, c);
+  float4 acc = make_float4(0.f, 0.f, 0.f, 0.f);
+#pragma unroll
+  for (int l = 0; l <= NL; ++l)
+#pragma unroll
+    for (int j = 0; j < kFastK; ++j)
+      if ((fl[l][j] & 3) == 3) add4(acc, cvt<F24>(v[l][j]));
+  if (a.out_dtype == LX_F32) {
+    *(float4*)((float*)a.out + (int64_t)t * d + c) = acc;
+  } else {
+    bf16x4 o;
+    o[0] = (__bf16)acc.x;
+    o[1] = (__bf16)acc.y;
+    o[2] = (__bf16)acc.z;
+    o[3] = (__bf16)acc.w;
+    *(bf16x4*)((uint16_t*)a.out + (int64_t)t * d + c) = o;
+  }
+}
+
+// Threads per workgroup for n 4-column groups: whole wavefronts, at most kFastThr.
+int fast_threads(int cols) {
+  const int g = (cols / 4 + 63) / 64 * 64;
+  return g < 64 ? 64 : g > kFastThr ? kFastThr : g;
+}
+
 }  // namespace
+
+// The fast paths need one row format on every level (all f24 or all fp32).
+static int uniform_fmt(const TokenArgs& a) {
+  for (int l = 1; l <= a.L; ++l)
+    if (a.f24[l] != a.f24[0]) return -1;
+  return a.f24[0] ? 1 : 0;
+}
 
 hipError_t launch_swiglu_reduce(const TokenArgs& a, hipStream_t s) {
   if (a.T == 0) return hipSuccess;
+  const int fmt = uniform_fmt(a);
+  if (a.k <= kFastK && a.L >= 1 && a.L <= kFastL && fmt >= 0) {
+    const int thr = fast_threads(a.f);
+    const dim3 grid(a.T, (a.f / 4 + thr - 1) / thr);
+    if (a.L == 1 && fmt)
+      hipLaunchKernelGGL((k_swiglu_fast<1, true>), grid, dim3(thr), 0, s, a);
+    else if (a.L == 1)
+      hipLaunchKernelGGL((k_swiglu_fast<1, false>), grid, dim3(thr), 0, s, a);
+    else if (fmt)
+      hipLaunchKernelGGL((k_swiglu_fast<2, true>), grid, dim3(thr), 0, s, a);
+    else
+      hipLaunchKernelGGL((k_swiglu_fast<2, false>), grid, dim3(thr), 0, s, a);
+    return hipGetLastError();
+  }
   const int groups = a.k < kSlotGroups ? a.k : kSlotGroups;
   hipLaunchKernelGGL(k_swiglu_reduce, dim3(a.T, (a.f + kTokCols - 1) / kTokCols), dim3(kTokThr * groups),
                      (size_t)a.k * kTokThr * sizeof(float4), s, a);
@@ -192,6 +381,20 @@ hipError_t launch_swiglu_reduce(const TokenArgs& a, hipStream_t s) {
 
 hipError_t launch_combine(const TokenArgs& a, hipStream_t s) {
   if (a.T == 0) return hipSuccess;
+  const int fmt = uniform_fmt(a);
+  if (a.k <= kFastK && a.L <= kFastL && fmt >= 0) {
+    const int thr = fast_threads(a.d);
+    const dim3 grid(a.T, (a.d / 4 + thr - 1) / thr);
+    switch (a.L * 2 + fmt) {
+      case 0: hipLaunchKernelGGL((k_combine_fast<0, false>), grid, dim3(thr), 0, s, a); break;
+      case 1: hipLaunchKernelGGL((k_combine_fast<0, true>), grid, dim3(thr), 0, s, a); break;
+      case 2: hipLaunchKernelGGL((k_combine_fast<1, false>), grid, dim3(thr), 0, s, a); break;
+      case 3: hipLaunchKernelGGL((k_combine_fast<1, true>), grid, dim3(thr), 0, s, a); break;
+      case 4: hipLaunchKernelGGL((k_combine_fast<2, false>), grid, dim3(thr), 0, s, a); break;
+      default: hipLaunchKernelGGL((k_combine_fast<2, true>), grid, dim3(thr), 0, s, a); break;
+    }
+    return hipGetLastError();
+  }
   int thr = (a.d / 4 + 63) / 64 * 64;
   thr = thr < 64 ? 64 : thr > kCombMaxThr ? kCombMaxThr : thr;
   hipLaunchKernelGGL(k_combine, dim3(a.T), dim3(thr), 0, s, a);

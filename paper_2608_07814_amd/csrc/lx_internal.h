@@ -9,6 +9,35 @@
 
 namespace lx {
 
+// ---------------------------------------------------------------- f24 rows
+// Intermediates that only the elementwise kernels read back (gate|up
+// outputs, down outputs) are stored as 24-bit floats: sign, exponent and the
+// top 15 mantissa bits of the fp32 value, rounded to nearest even (relative
+// error at most 2^-16, the precision of a bf16 hi + lo pair, in 3 bytes
+// instead of 4). Four consecutive values occupy 12 bytes; a row of n values
+// (n a multiple of 4) is 3n bytes.
+struct __attribute__((packed, aligned(4))) F24x4 {
+  uint32_t a, b, c;
+};
+
+__device__ __forceinline__ uint32_t f24_round(float x) {
+  const uint32_t u = __float_as_uint(x);
+  return (u + 0x7Fu + ((u >> 8) & 1u)) >> 8;
+}
+
+__device__ __forceinline__ F24x4 f24_pack(float4 v) {
+  const uint32_t p = f24_round(v.x), q = f24_round(v.y), r = f24_round(v.z), s = f24_round(v.w);
+  return F24x4{p | (q << 24), (q >> 8) | (r << 16), (r >> 16) | (s << 8)};
+}
+
+__device__ __forceinline__ float4 f24_unpack(F24x4 w) {
+  return make_float4(__uint_as_float(w.a << 8), __uint_as_float(((w.a >> 24) | (w.b << 8)) << 8),
+                     __uint_as_float(((w.b >> 16) | (w.c << 16)) << 8), __uint_as_float(w.c & 0xFFFFFF00u));
+}
+
+// Output format of a GEMM: fp32, a bf16 (hi, lo) pair, or f24.
+enum OutFmt { OUT_F32 = 0, OUT_HILO = 1, OUT_F24 = 2 };
+
 constexpr int kTokTile = 64;          // tokens per bucketing tile (one wavefront)
 constexpr int kMaxLvl = LX_MAX_LEVELS + 1;  // anchor level + correction levels
 
@@ -106,13 +135,14 @@ hipError_t launch_gemm(const GemmArgs& g, lx_dtype dt, AMode am, int grid_x, hip
 // Large-tile kernel (BM x BN tiles, direct HBM->LDS loads). Applicable when A
 // is bf16, K and Kb are multiples of 64, the parts either share A columns or
 // the part boundary is a multiple of BN, and A's element count fits in 31
-// bits. fp32 output is written at columns [0, ncols[0] + ncols[1]) of C (the
-// parts adjacent); bf16 (hi, lo) output writes part p's hi values at columns
-// base_p + c and lo values at base_p + ncols[p] + c, base_0 = 0,
-// base_1 = 2 ncols[0] (ldc in bf16 elements).
+// bits. fp32 and f24 output is written at columns [0, ncols[0] + ncols[1]) of
+// C (the parts adjacent; ldc in values, an f24 row is 3 ldc bytes); bf16
+// (hi, lo) output writes part p's hi values at columns base_p + c and lo
+// values at base_p + ncols[p] + c, base_0 = 0, base_1 = 2 ncols[0] (ldc in
+// bf16 elements).
 constexpr int kBigBM = 256;
 bool gemm_big_ok(const GemmArgs& g, int bn, int64_t a_rows_total);
-hipError_t launch_gemm_big(const GemmArgs& g, int bm, int bn, bool out_hilo, int grid_tiles,
+hipError_t launch_gemm_big(const GemmArgs& g, int bm, int bn, int ofmt, int grid_tiles,
                            hipStream_t s);
 
 // Skinny kernel for levels with few rows per node (decode-sized batches):
@@ -121,17 +151,17 @@ hipError_t launch_gemm_big(const GemmArgs& g, int bm, int bn, bool out_hilo, int
 // HBM rather than by MFMA work on padding rows. Same operand conventions and
 // applicability as the large-tile kernel (with bn = kSkinnyBN).
 constexpr int kSkinnyBM = 32, kSkinnyBN = 64;
-hipError_t launch_gemm_skinny(const GemmArgs& g, bool out_hilo, int grid_tiles, hipStream_t s);
+hipError_t launch_gemm_skinny(const GemmArgs& g, int ofmt, int grid_tiles, hipStream_t s);
 // Up to kSkinnyMaxProblems independent skinny GEMMs in one launch.
 constexpr int kSkinnyMaxProblems = 1 + LX_MAX_LEVELS;
 struct SkinnyBatch {
   GemmArgs g[kSkinnyMaxProblems];
   int32_t ntn[kSkinnyMaxProblems];
-  int32_t hilo[kSkinnyMaxProblems];
+  int32_t ofmt[kSkinnyMaxProblems];  // OutFmt
   int32_t base[kSkinnyMaxProblems + 1];  // first workgroup of each problem
   int32_t n;
 };
-hipError_t launch_gemm_skinny_batch(const GemmArgs* g, const bool* out_hilo, const int* grid_tiles, int n,
+hipError_t launch_gemm_skinny_batch(const GemmArgs* g, const int* ofmt, const int* grid_tiles, int n,
                                     hipStream_t s);
 
 // ---------------------------------------------------------------- elementwise
@@ -142,6 +172,8 @@ struct TokenArgs {
   const float* slot_wsum;
   const float* gu0;                    // [rows0][2f] anchor gate|up
   const float* dgu[kMaxLvl];           // [rows_l][2f] correction gate|up (l >= 1)
+  int32_t f24[kMaxLvl];                // level l's gate|up and down rows are f24
+                                       // (else fp32)
   float* hbar[kMaxLvl];                // [rows_l][f] fp32 weighted activation sums, or
                                        // [rows_l][2f] bf16 (hi half, lo half) when
                                        // hbar_hilo[l]

@@ -250,6 +250,28 @@ def test_tree_generic_levels():
         assert err_ratio(gpu_forward(p), _oracle(p)) <= (TOL_F32 if dtype == "f32" else TOL_BF16)
 
 
+def test_general_token_kernels():
+    """k > 8 slots and a three-level correction tree take the general SwiGLU
+    and combine kernels (the fast ones cover k <= 8 with at most two
+    correction levels), here on bf16 shapes whose levels all keep f24 rows."""
+    require_gpu()
+    from lxsynth import Level
+    from lxsynth.gen import _make_factors
+    say("general token kernels: k=12 flat, three-level tree")
+    layer = make_layer_flat(32, 4, 64, 128, 64, "bf16", 21)
+    p = _tiny_problem(layer, 70, 12, 22, drop_frac=0.1)
+    assert err_ratio(gpu_forward(p), _oracle(p)) <= TOL_DESIGN
+    # depth-2 tree over 16 nodes, then 2 leaves (rank 64) under each of them
+    base = tiny_tree(E=16, d=64, f=64, n_roots=2, subs=2, r_sub=64, r_leaf=64, dtype="bf16", seed=23)
+    f3 = _make_factors(np.random.default_rng(24), 32, 64, 64, 64, "bf16", 0.3)
+    base.levels.append(Level(parent=(np.arange(32) // 2).astype(np.int32),
+                             factor_of=np.arange(32, dtype=np.int32), rank=64, **f3))
+    base.levels[2].factor_of[5] = -1
+    base.E = 32
+    p3 = _tiny_problem(base, 50, 6, 25)
+    assert err_ratio(gpu_forward(p3), _oracle(p3)) <= TOL_DESIGN
+
+
 def test_dense_comparator():
     """L = 0: the uncompressed MoE through lx_dense_moe_forward."""
     require_gpu()
