@@ -49,6 +49,9 @@ def parse():
                     help="independent device copies of the layer weights, used round-robin by the "
                          "timed steps so that the 256 MB last-level cache cannot hold one step's weights "
                          "for the next (1 = a single copy)")
+    ap.add_argument("--no-lo8", action="store_true",
+                    help="no fp8 copy of the anchor down weights: the anchor down projection multiplies "
+                         "both halves of its bf16 (hi, lo) input in bf16")
     ap.add_argument("--copy-calibration", action="store_true",
                     help="only run a plain 1 GiB device-to-device copy 5 times (scales the "
                          "FETCH_SIZE / WRITE_SIZE counters to bytes)")
@@ -134,8 +137,11 @@ def clone_layer(dl):
     import dataclasses
     names = ("a_gate", "b_gate", "a_up", "b_up", "a_down", "b_down")
     levels = [dataclasses.replace(lv, **{n: getattr(lv, n).clone() for n in names}) for lv in dl.levels]
+    f8 = {}
+    if dl.anchor_down_f8 is not None:
+        f8 = dict(anchor_down_f8=dl.anchor_down_f8.clone(), anchor_down_f8_scale=dl.anchor_down_f8_scale.clone())
     return dataclasses.replace(dl, anchor_gate=dl.anchor_gate.clone(), anchor_up=dl.anchor_up.clone(),
-                               anchor_down=dl.anchor_down.clone(), levels=levels)
+                               anchor_down=dl.anchor_down.clone(), levels=levels, **f8)
 
 
 def rotating(calls):
@@ -202,7 +208,7 @@ def main():
     cfg = p.cfg
     T, k = p.T, p.k
     layer = p.layer
-    dl = lx.to_device(layer)
+    dl = lx.to_device(layer, lo8=not a.no_lo8)
     if layer.dtype == "bf16":
         xd = torch.from_numpy(p.x.view(np.int16)).cuda().view(torch.bfloat16)
     else:
@@ -296,6 +302,8 @@ def main():
                             anchor_gate=wg.bfloat16().contiguous(), anchor_up=wu.bfloat16().contiguous(),
                             anchor_down=wd.bfloat16().contiguous(), levels=[])
         del wg, wu, wd
+        if not a.no_lo8:
+            dd = lx.attach_down_f8(dd)
         wsd = lx.alloc_workspace(dd, T, k, "dense")
         outd = torch.empty_like(out)
         dcopies = [dd] + [clone_layer(dd) for _ in range(max(a.rotate, 1) - 1)]
@@ -343,7 +351,8 @@ def main():
         "data": "synthetic (seeded; Gaussian or community routing; random-init weights)",
         "config": {"workload": workload, "T": T, "d": layer.d, "f": layer.f, "E": layer.E,
                    "k": k, "anchors": layer.n_anchors, "ranks": ranks[1:], "layer": kind,
-                   "seed": p.seed, "out_dtype": "f32"},
+                   "seed": p.seed, "out_dtype": "f32",
+                   "anchor_down_lo": "bf16" if a.no_lo8 else "fp8 (block-scaled)"},
         "roofline": roof,
         "layer_roofline": layer_perf,
         "kernels": kernels,

@@ -106,6 +106,11 @@ typedef struct lx_tree_layer {
   const void* anchor_down;   /* [n_anchors][d][f] */
   int32_t n_levels;          /* 0 .. LX_MAX_LEVELS */
   lx_level levels[LX_MAX_LEVELS];
+  /* Optional (NULL = not used): fp8 copy of anchor_down made by
+   * lx_quantize_f8. With it the anchor down projection multiplies the low
+   * half of its bf16 (hi, lo) input split in fp8 (see lx_quantize_f8). */
+  const void* anchor_down_f8;            /* [n_anchors][d][f] e4m3 */
+  const uint32_t* anchor_down_f8_scale;  /* [n_anchors][d][f / 64] */
 } lx_tree_layer;
 
 /* A flat LorExperts layer (Sec. 3 "Representation"): C clusters, one dominant
@@ -125,6 +130,8 @@ typedef struct lx_flat_layer {
   const void* b_up;          /* [M][r][d] */
   const void* a_down;        /* [M][d][r] */
   const void* b_down;        /* [M][r][f] */
+  const void* dom_down_f8;             /* optional fp8 copy of dom_down (lx_quantize_f8) */
+  const uint32_t* dom_down_f8_scale;   /* its scale words, [C][d][f / 64] */
 } lx_flat_layer;
 
 /* An uncompressed MoE layer (every expert stored in full): the comparator the
@@ -136,6 +143,8 @@ typedef struct lx_dense_layer {
   const void* w_gate;        /* [E][f][d] */
   const void* w_up;          /* [E][f][d] */
   const void* w_down;        /* [E][d][f] */
+  const void* w_down_f8;               /* optional fp8 copy of w_down (lx_quantize_f8) */
+  const uint32_t* w_down_f8_scale;     /* its scale words, [E][d][f / 64] */
 } lx_dense_layer;
 
 /* Human-readable name of a status code (static string). */
@@ -170,6 +179,28 @@ lx_status lx_dense_moe_forward(const lx_dense_layer* layer, int32_t T, int32_t k
                                const void* x, const int32_t* topk_ids,
                                const float* topk_weights, void* out, lx_dtype out_dtype,
                                void* workspace, size_t workspace_bytes, void* stream);
+
+/* fp8 copy of bf16 weights, for the anchor down projection.
+ *
+ * The precision policy keeps every fp32 intermediate that feeds a bf16 GEMM
+ * as a bf16 (hi, lo) pair, and the GEMM runs K twice: C = (hi + lo) W^T. The
+ * lo half is below 2^-8 of hi, so a few bits of it suffice: given an fp8 copy
+ * of the anchor down weights (layer field anchor_down_f8 / dom_down_f8 /
+ * w_down_f8 and its scale words), the anchor activation sums are stored as
+ * bf16 hi plus a block-scaled fp8 lo, and lo W^T runs on the gfx950
+ * block-scaled fp8 MFMA at twice the bf16 rate with half the bytes. Used for
+ * batches large enough for the large-tile kernel; decode-sized batches keep
+ * the bf16 pair.
+ *
+ * w [n][rows][cols] bf16 -> w_f8 [n][rows][cols] OCP e4m3 bytes (round to
+ * nearest even) and scales [n][rows][cols / 64] uint32: bytes 0 and 1 are the
+ * E8M0 exponents (value 2^(byte - 127)) of the two 32-column blocks of each
+ * 64-column slab, chosen so that each block's largest magnitude maps into
+ * [128, 256); bytes 2 and 3 are zero. cols must be a multiple of 64
+ * (LX_ERR_UNSUPPORTED otherwise); w_f8 16-byte and scales 4-byte aligned.
+ * Asynchronous on `stream`. */
+lx_status lx_quantize_f8(const void* w, int32_t n, int32_t rows, int32_t cols, void* w_f8,
+                         uint32_t* scales, void* stream);
 
 /* Routing bucketing alone (the first step of every forward), exposing the
  * arrays of one tree level `level` (0 = anchors, n_levels = experts):

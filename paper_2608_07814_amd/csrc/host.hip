@@ -107,6 +107,10 @@ struct Plan {
   // independent products of a phase share a launch).
   bool fast[kMaxLvl] = {}, skinny[kMaxLvl] = {};
   bool batch = false;
+  // lo8: the anchor activation sums are bf16 hi + block-scaled fp8 lo and the
+  // anchor down GEMM runs the lo half on the fp8 MFMA (needs the layer's fp8
+  // copy of the anchor down weights and the large-tile kernel)
+  bool lo8 = false;
 };
 
 int level_nodes(const lx_tree_layer& t, int l) { return l == 0 ? t.n_anchors : t.levels[l - 1].n_nodes; }
@@ -149,6 +153,7 @@ Plan make_plan(const lx_tree_layer& t, int T, int k) {
       const bool work = l == 0 || t.levels[l - 1].n_factors > 0;
       if (work && !p.skinny[l]) p.batch = false;
     }
+    p.lo8 = t.anchor_down_f8 && t.anchor_down_f8_scale && p.fast[0] && !p.skinny[0] && p.f % 64 == 0;
   }
   p.flags = take(16);  // first: lx_read_device_status reads offset 0
   p.anc = take((size_t)(p.L + 1) * p.E * 4);
@@ -205,6 +210,13 @@ lx_status check_layer(const lx_tree_layer* t) {
   const void* aw[3] = {t->anchor_gate, t->anchor_up, t->anchor_down};
   for (const void* q : aw)
     if (!q || !aligned(q, 16)) return fail(LX_ERR_INVALID_ARGUMENT, "anchor weights null or not 16-byte aligned");
+  if (t->anchor_down_f8 || t->anchor_down_f8_scale) {
+    if (!t->anchor_down_f8 || !t->anchor_down_f8_scale || !aligned(t->anchor_down_f8, 16) ||
+        !aligned(t->anchor_down_f8_scale, 4))
+      return fail(LX_ERR_INVALID_ARGUMENT, "fp8 down copy and its scales: both or neither, 16/4-byte aligned");
+    if (t->dtype != LX_BF16 || t->f % 64)
+      return fail(LX_ERR_UNSUPPORTED, "an fp8 down copy needs a bf16 layer with f a multiple of 64");
+  }
   for (int l = 0; l < t->n_levels; ++l) {
     const lx_level& v = t->levels[l];
     if (v.n_nodes < 1 || v.n_nodes > LX_MAX_NODES) return fail(LX_ERR_INVALID_ARGUMENT, "level node count out of range");
@@ -241,6 +253,8 @@ lx_tree_layer flat_to_tree(const lx_flat_layer& F) {
   t.anchor_gate = F.dom_gate;
   t.anchor_up = F.dom_up;
   t.anchor_down = F.dom_down;
+  t.anchor_down_f8 = F.dom_down_f8;
+  t.anchor_down_f8_scale = F.dom_down_f8_scale;
   t.n_levels = 1;
   lx_level& v = t.levels[0];
   v.n_nodes = F.E;
@@ -267,6 +281,8 @@ lx_tree_layer dense_to_tree(const lx_dense_layer& D) {
   t.anchor_gate = D.w_gate;
   t.anchor_up = D.w_up;
   t.anchor_down = D.w_down;
+  t.anchor_down_f8 = D.w_down_f8;
+  t.anchor_down_f8_scale = D.w_down_f8_scale;
   t.n_levels = 0;
   return t;
 }
@@ -624,7 +640,7 @@ lx_status run(const lx_tree_layer& t, int T, int k, const void* x, const int32_t
     ta.slot_flags[l] = ba.lv[l].slot_flags;
     ta.dgu[l] = (const float*)(W + q.gu);
     ta.hbar[l] = (float*)(W + q.hbar);
-    ta.hbar_hilo[l] = fast[l] ? 1 : 0;
+    ta.hbar_mode[l] = l == 0 && P.lo8 ? HBAR_LO8 : fast[l] ? HBAR_HILO : HBAR_F32;
     ta.f24[l] = fast[l] ? 1 : 0;
     ta.y[l] = (const float*)(W + q.y);
   }
@@ -644,7 +660,22 @@ lx_status run(const lx_tree_layer& t, int T, int k, const void* x, const int32_t
     g.ncols[0] = d;
     g.C = (float*)(W + q.y);
     g.ldc = d;
-    if (fast[0]) {
+    if (P.lo8) {
+      // row = [bf16 hi (f) | fp8 lo (f bytes) | scale words (f / 64)] in 4f bytes
+      g.lda = 2 * (int64_t)f;
+      g.K = 2 * f;
+      g.Kb = f;
+      g.b8 = (const uint8_t*)t.anchor_down_f8;
+      g.bsc = t.anchor_down_f8_scale;
+      g.a_lo8_off = 2 * f;
+      g.a_sc_off = 3 * f;
+      g.B[1] = g.B[0];
+      g.tiles = ba.lv[0].tiles[kTabBig];
+      g.n_tiles = ba.lv[0].n_tiles[kTabBig];
+      if (!gemm_lo8_ok(g, q.rows_max))
+        return fail(LX_ERR_UNSUPPORTED, "anchor_down: shape not supported by the fp8-lo GEMM");
+      LX_LAUNCH("anchor_down", launch_gemm_lo8(g, OUT_F24, (int)q.tiles_max[kTabBig], lstream));
+    } else if (fast[0]) {
       g.lda = 2 * (int64_t)f;
       g.K = 2 * f;
       g.Kb = f;
@@ -822,6 +853,20 @@ lx_status lx_bucket(const lx_tree_layer* layer, int32_t T, int32_t k, const int3
     e = hipMemcpyAsync(node_offsets, W + q.offsets, (size_t)(q.N + 1) * 4, hipMemcpyDeviceToDevice, s);
   if (e == hipSuccess && slot_row)
     e = hipMemcpyAsync(slot_row, W + q.slot_row, (size_t)T * k * 4, hipMemcpyDeviceToDevice, s);
+  if (e != hipSuccess) return fail(LX_ERR_HIP, hipGetErrorString(e));
+  return LX_OK;
+}
+
+lx_status lx_quantize_f8(const void* w, int32_t n, int32_t rows, int32_t cols, void* w_f8, uint32_t* scales,
+                         void* stream) {
+  g_err.clear();
+  if (n < 0 || rows < 0 || cols < 0) return fail(LX_ERR_INVALID_ARGUMENT, "negative size");
+  if (cols % 64) return fail(LX_ERR_UNSUPPORTED, "cols must be a multiple of 64");
+  const int64_t n_rows = (int64_t)n * rows;
+  if (n_rows == 0 || cols == 0) return LX_OK;
+  if (!w || !w_f8 || !scales || !aligned(w, 16) || !aligned(w_f8, 16) || !aligned(scales, 4))
+    return fail(LX_ERR_INVALID_ARGUMENT, "null or misaligned pointer");
+  const hipError_t e = launch_quantize_f8(w, n_rows, cols, (uint8_t*)w_f8, scales, (hipStream_t)stream);
   if (e != hipSuccess) return fail(LX_ERR_HIP, hipGetErrorString(e));
   return LX_OK;
 }

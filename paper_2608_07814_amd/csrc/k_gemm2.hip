@@ -74,6 +74,35 @@ __device__ __forceinline__ void load_lds16(const void* gptr, const void* lds_dst
                : "memory");
 }
 
+// One 4-byte direct HBM -> LDS load per lane (lane i writes LDS bytes
+// [lds_base + 4 i, lds_base + 4 i + 4)); same conventions as load_lds16.
+__device__ __forceinline__ void load_lds4(const void* gptr, const void* lds_dst) {
+  const uint32_t lds = (uint32_t)(uintptr_t)(lds_void_t*)lds_dst;
+  asm volatile("s_mov_b32 m0, %1\n\ts_nop 0\n\tglobal_load_lds_dword %0, off"
+               :
+               : "v"(gptr), "s"(__builtin_amdgcn_readfirstlane(lds))
+               : "memory");
+}
+
+// The same loads addressed as a wave-uniform 64-bit base (SGPR pair) plus a
+// 32-bit per-lane byte offset: one VGPR per address instead of two.
+__device__ __forceinline__ void load_lds16_sb(const void* base, uint32_t off, const void* lds_dst) {
+  const uint32_t lds = (uint32_t)(uintptr_t)(lds_void_t*)lds_dst;
+  asm volatile("s_mov_b32 m0, %2\n\ts_nop 0\n\tglobal_load_lds_dwordx4 %0, %1"
+               :
+               : "v"(off), "s"(base), "s"(__builtin_amdgcn_readfirstlane(lds))
+               : "memory");
+}
+__device__ __forceinline__ void load_lds4_sb(const void* base, uint32_t off, const void* lds_dst) {
+  const uint32_t lds = (uint32_t)(uintptr_t)(lds_void_t*)lds_dst;
+  asm volatile("s_mov_b32 m0, %2\n\ts_nop 0\n\tglobal_load_lds_dword %0, %1"
+               :
+               : "v"(off), "s"(base), "s"(__builtin_amdgcn_readfirstlane(lds))
+               : "memory");
+}
+
+typedef int v8i __attribute__((ext_vector_type(8)));
+
 // s_waitcnt with only the vector-memory counter constrained to <= N.
 template <int N>
 __device__ __forceinline__ void wait_vmcnt() {
@@ -118,10 +147,11 @@ struct BigCfg {
   static constexpr int WPE = NW / 4;  // wavefronts per SIMD
 };
 
-template <int BM, int BN, int OUT>
+template <int BM, int BN, int OUT, bool LO8 = false>
 __global__ __launch_bounds__((BigCfg<BM, BN>::NTHR), 1)
 __attribute__((amdgpu_waves_per_eu(BigCfg<BM, BN>::WPE, BigCfg<BM, BN>::WPE)))
 void k_gemm_big(GemmArgs p, int ntn) {
+  static_assert(!LO8 || (BM == 256 && BN == 256), "fp8 lo: 256 x 256 tiles");
   constexpr int NTHR = BigCfg<BM, BN>::NTHR, WGN = BigCfg<BM, BN>::WGN;
   constexpr int MI = BM / 64;              // 32-row MFMA blocks per wavefront
   constexpr int NI = BN / (32 * WGN);      // 32-column MFMA blocks per wavefront
@@ -282,6 +312,124 @@ void k_gemm_big(GemmArgs p, int ntn) {
         }
       }
       bar();
+    } else if constexpr (LO8) {
+      // K = 2 Kb: slab kt = 2 q + per is the hi (per 0) or lo (per 1) half of
+      // weight slab q. Hi slabs always sit in stage 0 ([A | B] bf16, 64 KB),
+      // lo slabs in stage 1: [A lo8 16 KB | B lo8 16 KB | A scale words 1 KB |
+      // B scale words 1 KB]. A lo slab is 5 direct loads per lane (2 + 2
+      // 16-byte rounds, one 4-byte scale load), a hi slab ROUNDS.
+      constexpr int RLO = 5;
+      uint8_t* const L1 = (uint8_t*)sA1;
+      const uint8_t* const Abytes = (const uint8_t*)p.A;
+      const uint32_t apitch = 2 * (uint32_t)p.lda;
+      const uint8_t* const B8 = p.b8 + (int64_t)te.widx * p.b_stride[0];
+      const uint32_t* const BS = p.bsc + (int64_t)te.widx * (p.b_stride[0] / 64);
+      const u16* const Bhi = Bw0;
+      // byte offsets (32 bit: the host routes operands of 2^31 or more
+      // elements elsewhere) of this thread's hi-slab chunks of B and of its lo
+      // and scale loads, slab 0
+      uint32_t bhoff[B_ROUNDS];
+#pragma unroll
+      for (int j = 0; j < B_ROUNDS; ++j) bhoff[j] = (uint32_t)((bptr[j] - Bhi) * 2);
+      uint32_t aloff[2], bloff[2];
+#pragma unroll
+      for (int j = 0; j < 2; ++j) {
+        const int Ps = j * NTHR + tid;
+        const int row = Ps >> 2;
+        const int c = (Ps & 3) ^ ((row >> 2) & 3);
+        const int r = row < te.nrows ? row : te.nrows - 1;
+        aloff[j] = (uint32_t)(te.row0 + r) * apitch + (uint32_t)p.a_lo8_off + c * 16;
+        const int n = n0 + row < ncol ? n0 + row : ncol - 1;
+        bloff[j] = (uint32_t)n * (uint32_t)Kb + c * 16;
+      }
+      uint32_t scoff;
+      {
+        const int row = (wave & 3) * 64 + lane;
+        if (wave < 4) {
+          const int r = row < te.nrows ? row : te.nrows - 1;
+          scoff = (uint32_t)(te.row0 + r) * apitch + (uint32_t)p.a_sc_off;
+        } else {
+          const int n = n0 + row < ncol ? n0 + row : ncol - 1;
+          scoff = (uint32_t)n * (uint32_t)(Kb / BK2) * 4;
+        }
+      }
+      auto issue_hi = [&](int kt) {
+        const int kb = (kt >> 1) * BK2;
+#pragma unroll
+        for (int j = 0; j < A_ROUNDS; ++j)
+          load_lds16(Ab + (aoff[j] + (uint32_t)kb), &sA0[(j * NTHR + wave * 64) * 8]);
+#pragma unroll
+        for (int j = 0; j < B_ROUNDS; ++j)
+          load_lds16_sb(Bhi, bhoff[j] + (uint32_t)kb * 2, &sB0[(j * NTHR + wave * 64) * 8]);
+      };
+      auto issue_lo = [&](int kt) {
+        const int q = kt >> 1, kb = q * BK2;
+#pragma unroll
+        for (int j = 0; j < 2; ++j) {
+          load_lds16_sb(Abytes, aloff[j] + kb, L1 + (j * NTHR + wave * 64) * 16);
+          load_lds16_sb(B8, bloff[j] + kb, L1 + 16384 + (j * NTHR + wave * 64) * 16);
+        }
+        if (wave < 4)
+          load_lds4_sb(Abytes, scoff + q * 4, L1 + 32768 + wave * 256);
+        else
+          load_lds4_sb(BS, scoff + q * 4, L1 + 33792 + (wave - 4) * 256);
+      };
+      // lo fragments: lane (row, half h) holds K [16h, 16h + 16) of the slab in
+      // bytes 0-15 and K [32 + 16h, 48 + 16h) in bytes 16-31 (scale block h);
+      // rows are 64 bytes, 16-byte chunks XOR-swizzled by (row / 4) % 4
+      auto compute_lo = [&]() {
+        const int h = lane >> 5;
+        v8i fb8[NI], fa8[2];
+        int sb[NI], sa[2];
+        auto lda8 = [&](int mi, int slot) {
+          const int row = wm * WM + mi * 32 + (lane & 31);
+          const int sw = (row >> 2) & 3;
+          const uint4 x0 = *(const uint4*)(L1 + row * 64 + ((h ^ sw) << 4));
+          const uint4 x1 = *(const uint4*)(L1 + row * 64 + (((2 + h) ^ sw) << 4));
+          fa8[slot] = v8i{(int)x0.x, (int)x0.y, (int)x0.z, (int)x0.w, (int)x1.x, (int)x1.y, (int)x1.z, (int)x1.w};
+          sa[slot] = (int)((*(const uint32_t*)(L1 + 32768 + row * 4) >> (8 * h)) & 0xFFu);
+        };
+#pragma unroll
+        for (int ni = 0; ni < NI; ++ni) {
+          const int col = wn * WN + ni * 32 + (lane & 31);
+          const int sw = (col >> 2) & 3;
+          const uint4 x0 = *(const uint4*)(L1 + 16384 + col * 64 + ((h ^ sw) << 4));
+          const uint4 x1 = *(const uint4*)(L1 + 16384 + col * 64 + (((2 + h) ^ sw) << 4));
+          fb8[ni] = v8i{(int)x0.x, (int)x0.y, (int)x0.z, (int)x0.w, (int)x1.x, (int)x1.y, (int)x1.z, (int)x1.w};
+          sb[ni] = (int)((*(const uint32_t*)(L1 + 33792 + col * 4) >> (8 * h)) & 0xFFu);
+        }
+        lda8(0, 0);
+        // A fragments double-buffered: block mi + 1 is read while mi multiplies
+#pragma unroll
+        for (int mi = 0; mi < MI; ++mi) {
+          __builtin_amdgcn_sched_barrier(0);
+          if (mi + 1 < MI) lda8(mi + 1, (mi + 1) & 1);
+          __builtin_amdgcn_sched_barrier(0);
+#pragma unroll
+          for (int ni = 0; ni < NI; ++ni)
+            acc[mi][ni] = __builtin_amdgcn_mfma_scale_f32_32x32x64_f8f6f4(fa8[mi & 1], fb8[ni], acc[mi][ni], 0, 0,
+                                                                          0, sa[mi & 1], 0, sb[ni]);
+        }
+        __builtin_amdgcn_sched_barrier(0);
+      };
+      issue_hi(0);
+      issue_lo(1);
+      for (int kt = 0; kt < nk; kt += 2) {
+        wait_vmcnt<RLO>();
+        bar();
+        LX_COMPUTE(sA0, sB0);
+        bar();
+        const bool more = kt + 2 < nk;
+        if (more) issue_hi(kt + 2);
+        if (more)
+          wait_vmcnt<ROUNDS>();
+        else
+          wait_vmcnt<0>();
+        bar();
+        compute_lo();
+        bar();
+        if (more) issue_lo(kt + 3);
+      }
     } else {
     LX_ISSUE(sA0, sB0, 0);
     if (nk > 1) LX_ISSUE(sA1, sB1, 1);
@@ -545,7 +693,54 @@ hipError_t launch_bn(const GemmArgs& g, int ofmt, int grid, int ntn, hipStream_t
   return hipGetLastError();
 }
 
+// fp8 copy of bf16 weights: one thread per (row, 64-column slab); each
+// 32-column block gets its own E8M0 scale (block max in [128, 256)).
+__global__ __launch_bounds__(256) void k_quantize_f8(const u16* __restrict__ w, int64_t n_rows, int cols,
+                                                     uint8_t* __restrict__ w8, uint32_t* __restrict__ sc) {
+  const int nsl = cols / BK2;
+  const int64_t i = (int64_t)blockIdx.x * blockDim.x + threadIdx.x;
+  if (i >= n_rows * nsl) return;
+  const int64_t row = i / nsl;
+  const int sl = (int)(i - row * nsl);
+  const u16* src = w + row * cols + sl * BK2;
+  uint8_t* dst = w8 + row * cols + sl * BK2;
+  uint32_t word = 0;
+  for (int b = 0; b < 2; ++b) {
+    float v[32];
+    float amax = 0.f;
+    for (int e = 0; e < 32; ++e) {
+      v[e] = __uint_as_float((uint32_t)src[b * 32 + e] << 16);
+      amax = fmaxf(amax, fabsf(v[e]));
+    }
+    const uint32_t be = e8m0_for(amax);
+    word |= be << (8 * b);
+    for (int e = 0; e < 32; e += 4) {
+      const uint32_t q = f32_to_e4m3(e8m0_unscale(v[e], be)) | (f32_to_e4m3(e8m0_unscale(v[e + 1], be)) << 8) |
+                         (f32_to_e4m3(e8m0_unscale(v[e + 2], be)) << 16) |
+                         (f32_to_e4m3(e8m0_unscale(v[e + 3], be)) << 24);
+      *(uint32_t*)(dst + b * 32 + e) = q;
+    }
+  }
+  sc[row * nsl + sl] = word;
+}
+
 }  // namespace
+
+bool gemm_lo8_ok(const GemmArgs& g, int64_t a_rows_total) {
+  if (!g.b8 || !g.bsc || g.a_rows || g.ncols[1] != 0 || g.Kb <= 0 || g.K != 2 * g.Kb || g.Kb % BK2) return false;
+  if (((uintptr_t)g.b8 & 15) || ((uintptr_t)g.bsc & 3) || (g.a_lo8_off & 15) || (g.a_sc_off & 3)) return false;
+  if (g.a_lo8_off < 2 * g.Kb || g.a_sc_off < g.a_lo8_off + g.Kb || g.a_sc_off + g.Kb / 16 > 2 * g.lda) return false;
+  if ((2 * g.lda) % 16) return false;
+  return gemm_big_ok(g, 256, a_rows_total);
+}
+
+hipError_t launch_quantize_f8(const void* w, int64_t n_rows, int cols, uint8_t* w8, uint32_t* sc, hipStream_t s) {
+  const int64_t n = n_rows * (cols / BK2);
+  if (n <= 0) return hipSuccess;
+  hipLaunchKernelGGL(k_quantize_f8, dim3((unsigned)((n + 255) / 256)), dim3(256), 0, s, (const u16*)w, n_rows,
+                     cols, w8, sc);
+  return hipGetLastError();
+}
 
 bool gemm_big_ok(const GemmArgs& g, int bn, int64_t a_rows_total) {
   const int Kb = g.Kb > 0 ? g.Kb : g.K;
@@ -590,6 +785,19 @@ hipError_t launch_gemm_big(const GemmArgs& g, int bm, int bn, int ofmt, int grid
   if (bn == 256) return launch_bn<128, 256>(g, ofmt, grid, ntn, s);
   if (bn == 128) return launch_bn<128, 128>(g, ofmt, grid, ntn, s);
   return launch_bn<128, 64>(g, ofmt, grid, ntn, s);
+}
+
+hipError_t launch_gemm_lo8(const GemmArgs& g, int ofmt, int grid_tiles, hipStream_t s) {
+  const int ntn = (g.ncols[0] + 255) / 256;
+  int grid = grid_tiles * ntn;
+  if (grid <= 0) return hipSuccess;
+  const int cap = grid_cap();
+  if (grid > cap) grid = cap;
+  if (ofmt == OUT_F24)
+    hipLaunchKernelGGL((k_gemm_big<256, 256, OUT_F24, true>), dim3(grid), dim3(512), 0, s, g, ntn);
+  else
+    hipLaunchKernelGGL((k_gemm_big<256, 256, OUT_F32, true>), dim3(grid), dim3(512), 0, s, g, ntn);
+  return hipGetLastError();
 }
 
 hipError_t launch_gemm_skinny_batch(const GemmArgs* g, const int* ofmt, const int* grid_tiles, int n,

@@ -61,25 +61,45 @@ __device__ __forceinline__ void add4(float4& a, const float4& b) {
 }
 __device__ __forceinline__ float silu_mul(float g, float u) { return g / (1.f + expf(-g)) * u; }
 
-// hbar row segment (4 neurons at column c): fp32, or a bf16 (hi, lo) pair in
-// a row of 2f (hi half, lo half).
-__device__ __forceinline__ void hbar_store(void* base, bool hilo, int row, int c, int f, float4 v) {
-  if (hilo) {
-    __bf16* hb = (__bf16*)base + (int64_t)row * 2 * f;
-    bf16x4 hi, lo;
-    hi[0] = (__bf16)v.x;
-    hi[1] = (__bf16)v.y;
-    hi[2] = (__bf16)v.z;
-    hi[3] = (__bf16)v.w;
-    lo[0] = (__bf16)(v.x - (float)hi[0]);
-    lo[1] = (__bf16)(v.y - (float)hi[1]);
-    lo[2] = (__bf16)(v.z - (float)hi[2]);
-    lo[3] = (__bf16)(v.w - (float)hi[3]);
-    *(bf16x4*)(hb + c) = hi;
-    *(bf16x4*)(hb + f + c) = lo;
-  } else {
+// hbar row segment (4 neurons at column c), rows of 4f bytes: fp32; or a
+// bf16 (hi, lo) pair (hi half, lo half); or bf16 hi, fp8 lo and one E8M0
+// scale per 32 neurons (HBAR_LO8). HBAR_LO8 reduces the block maximum over
+// the 8 lanes that hold a 32-neuron block, so those lanes must execute the
+// call together (columns 4 per lane, blocks aligned to 32 columns).
+__device__ __forceinline__ void hbar_store(void* base, int mode, int row, int c, int f, float4 v) {
+  if (mode == HBAR_F32) {
     *(float4*)((float*)base + (int64_t)row * f + c) = v;
+    return;
   }
+  __bf16* hb = (__bf16*)base + (int64_t)row * 2 * f;
+  bf16x4 hi;
+  hi[0] = (__bf16)v.x;
+  hi[1] = (__bf16)v.y;
+  hi[2] = (__bf16)v.z;
+  hi[3] = (__bf16)v.w;
+  *(bf16x4*)(hb + c) = hi;
+  const float l0 = v.x - (float)hi[0], l1 = v.y - (float)hi[1], l2 = v.z - (float)hi[2], l3 = v.w - (float)hi[3];
+  if (mode == HBAR_HILO) {
+    bf16x4 lo;
+    lo[0] = (__bf16)l0;
+    lo[1] = (__bf16)l1;
+    lo[2] = (__bf16)l2;
+    lo[3] = (__bf16)l3;
+    *(bf16x4*)(hb + f + c) = lo;
+    return;
+  }
+  float amax = fmaxf(fmaxf(fabsf(l0), fabsf(l1)), fmaxf(fabsf(l2), fabsf(l3)));
+  amax = fmaxf(amax, __shfl_xor(amax, 1, 64));
+  amax = fmaxf(amax, __shfl_xor(amax, 2, 64));
+  amax = fmaxf(amax, __shfl_xor(amax, 4, 64));
+  const uint32_t be = e8m0_for(amax);
+  uint8_t* const rb = (uint8_t*)base + (int64_t)row * 4 * f;
+  *(uint32_t*)(rb + 2 * f + c) = f32_to_e4m3(e8m0_unscale(l0, be)) | (f32_to_e4m3(e8m0_unscale(l1, be)) << 8) |
+                                 (f32_to_e4m3(e8m0_unscale(l2, be)) << 16) |
+                                 (f32_to_e4m3(e8m0_unscale(l3, be)) << 24);
+  // the first lane of each 64-neuron slab writes the slab's scale word
+  const uint32_t be_next = __shfl_down(be, 8, 64);
+  if ((c & 63) == 0) *(uint32_t*)(rb + 3 * f + (c >> 6) * 4) = be | (be_next << 8);
 }
 constexpr int kTokThr = 64, kTokCols = 4 * kTokThr;
 constexpr int kSlotGroups = 16;  // SwiGLU: up to 16 slots processed side by side
@@ -125,7 +145,7 @@ __global__ __launch_bounds__(kTokThr * kSlotGroups) void k_swiglu_reduce(TokenAr
       float4 hs = make_float4(0.f, 0.f, 0.f, 0.f);
       for (int j = j0; j < k; ++j)
         if (m.row[l][j] == r && (m.fl[L][j] & 1)) add4(hs, s_h[j * kTokThr + lane]);
-      hbar_store(a.hbar[l], a.hbar_hilo[l], r, c, f, hs);
+      hbar_store(a.hbar[l], a.hbar_mode[l], r, c, f, hs);
     }
   }
 }
@@ -306,7 +326,7 @@ __global__ __launch_bounds__(kFastThr) void k_swiglu_fast(TokenArgs a) {
 #pragma unroll
       for (int j = j0; j < kFastK; ++j)
         if (row[l][j] == row[l][j0] && (fl[NL][j] & 1)) add4(hs, h[j]);
-      hbar_store(a.hbar[l], a.hbar_hilo[l], row[l][j0], c, f, hs);
+      hbar_store(a.hbar[l], a.hbar_mode[l], row[l][j0], c, f, hs);
     }
 }
 

@@ -37,6 +37,49 @@ __device__ __forceinline__ float4 f24_unpack(F24x4 w) {
 
 // Output format of a GEMM: fp32, a bf16 (hi, lo) pair, or f24.
 enum OutFmt { OUT_F32 = 0, OUT_HILO = 1, OUT_F24 = 2 };
+// Format of the weighted activation sums (the down GEMMs' input).
+enum HbarMode { HBAR_F32 = 0, HBAR_HILO = 1, HBAR_LO8 = 2 };
+
+// ---------------------------------------------------------------- fp8 lo
+// The low half of a bf16 (hi, lo) split only needs a few bits: where the
+// anchor down weights come with an fp8 copy, the anchor activation sums are
+// stored as bf16 hi plus an fp8 (OCP e4m3) lo with one power-of-two scale per
+// 32 consecutive values (E8M0 exponent byte, value 2^(byte - 127)), and the
+// anchor down GEMM multiplies the lo half with the block-scaled fp8 MFMA.
+// Scale words: one uint32 per 64 values, bytes 0 and 1 the exponents of its
+// two 32-value blocks, bytes 2 and 3 zero.
+
+// E8M0 exponent byte for a block whose largest magnitude is amax: the block
+// max lands in [128, 256), inside e4m3's normal range (max 448).
+__device__ __forceinline__ uint32_t e8m0_for(float amax) {
+  const int e = (int)((__float_as_uint(amax) >> 23) & 0xFF) - 127;  // floor(log2) for normal amax
+  int b = e - 7 + 127;
+  b = b < 1 ? 1 : b > 254 ? 254 : b;
+  return (uint32_t)b;
+}
+
+// x * 2^(127 - b): the inverse of the block scale, exact.
+__device__ __forceinline__ float e8m0_unscale(float x, uint32_t b) {
+  return x * __uint_as_float((254u - b) << 23);
+}
+
+// fp32 -> OCP e4m3 byte, round to nearest even, for |x| <= 448 (the callers'
+// block scaling guarantees it); values below 2^-6 become e4m3 subnormals.
+__device__ __forceinline__ uint32_t f32_to_e4m3(float x) {
+  const uint32_t u = __float_as_uint(x);
+  const uint32_t sign = (u >> 24) & 0x80u;
+  const float a = fabsf(x);
+  uint32_t code;
+  if (a < 0.015625f) {  // subnormal: multiples of 2^-9 (rounding up to 8 gives 2^-6, code 0x08)
+    code = (uint32_t)__float2int_rn(a * 512.f);
+  } else {
+    const uint32_t v = __float_as_uint(a);
+    const uint32_t r = v + 0x7FFFFu + ((v >> 20) & 1u);  // keep 3 mantissa bits, ties to even
+    code = ((((r >> 23) & 0xFF) - 120u) << 3) | ((r >> 20) & 7u);
+    code = code > 0x7Eu ? 0x7Eu : code;
+  }
+  return sign | code;
+}
 
 constexpr int kTokTile = 64;          // tokens per bucketing tile (one wavefront)
 constexpr int kMaxLvl = LX_MAX_LEVELS + 1;  // anchor level + correction levels
@@ -123,6 +166,13 @@ struct GemmArgs {
   float* C;
   int64_t ldc;
   int32_t c_coloff[2];
+  // fp8 lo half (anchor down projection, K = 2 Kb, A rows without a gather
+  // map): A row = [bf16 hi (Kb) | fp8 lo (Kb bytes) at byte a_lo8_off |
+  // scale words (Kb / 64) at byte a_sc_off], row pitch 2 lda bytes; the
+  // weights' fp8 copy and scale words:
+  const uint8_t* b8;         // [widx][n][Kb]
+  const uint32_t* bsc;       // [widx][n][Kb / 64]
+  int32_t a_lo8_off, a_sc_off;
 };
 
 enum AMode { A_BF16 = 0, A_F32_HILO = 1 };
@@ -142,6 +192,13 @@ hipError_t launch_gemm(const GemmArgs& g, lx_dtype dt, AMode am, int grid_x, hip
 // bf16 elements).
 constexpr int kBigBM = 256;
 bool gemm_big_ok(const GemmArgs& g, int bn, int64_t a_rows_total);
+// The fp8-lo variant (256 x 256 tiles) of the large-tile kernel: hi slabs as
+// above, lo slabs from the fp8 copies with the block-scaled fp8 MFMA.
+bool gemm_lo8_ok(const GemmArgs& g, int64_t a_rows_total);
+hipError_t launch_gemm_lo8(const GemmArgs& g, int ofmt, int grid_tiles, hipStream_t s);
+// Weights [n][rows][cols] bf16 -> fp8 copy [n][rows][cols] and scale words
+// [n][rows][cols / 64] (cols a multiple of 64).
+hipError_t launch_quantize_f8(const void* w, int64_t n_rows, int cols, uint8_t* w8, uint32_t* sc, hipStream_t s);
 hipError_t launch_gemm_big(const GemmArgs& g, int bm, int bn, int ofmt, int grid_tiles,
                            hipStream_t s);
 
@@ -174,10 +231,11 @@ struct TokenArgs {
   const float* dgu[kMaxLvl];           // [rows_l][2f] correction gate|up (l >= 1)
   int32_t f24[kMaxLvl];                // level l's gate|up and down rows are f24
                                        // (else fp32)
-  float* hbar[kMaxLvl];                // [rows_l][f] fp32 weighted activation sums, or
-                                       // [rows_l][2f] bf16 (hi half, lo half) when
-                                       // hbar_hilo[l]
-  int32_t hbar_hilo[kMaxLvl];
+  float* hbar[kMaxLvl];                // weighted activation sums, rows of 4f bytes:
+                                       // HBAR_F32 fp32 [f]; HBAR_HILO bf16 hi [f] then
+                                       // lo [f]; HBAR_LO8 bf16 hi [f], fp8 lo [f bytes],
+                                       // scale words [f / 64]
+  int32_t hbar_mode[kMaxLvl];
   const float* y[kMaxLvl];             // [rows_l][d] down outputs per level
   void* out;
   lx_dtype out_dtype;

@@ -40,7 +40,8 @@ class LxTreeLayer(ctypes.Structure):
     _fields_ = [("E", _c_i32), ("d", _c_i32), ("f", _c_i32), ("dtype", _c_i32),
                 ("n_anchors", _c_i32), ("anchor_gate", _c_void), ("anchor_up", _c_void),
                 ("anchor_down", _c_void), ("n_levels", _c_i32),
-                ("levels", LxLevel * LX_MAX_LEVELS)]
+                ("levels", LxLevel * LX_MAX_LEVELS),
+                ("anchor_down_f8", _c_void), ("anchor_down_f8_scale", _c_void)]
 
 
 class LxFlatLayer(ctypes.Structure):
@@ -48,12 +49,14 @@ class LxFlatLayer(ctypes.Structure):
                 ("M", _c_i32), ("dtype", _c_i32), ("cluster_of", _c_void), ("factor_of", _c_void),
                 ("dom_gate", _c_void), ("dom_up", _c_void), ("dom_down", _c_void),
                 ("a_gate", _c_void), ("b_gate", _c_void), ("a_up", _c_void), ("b_up", _c_void),
-                ("a_down", _c_void), ("b_down", _c_void)]
+                ("a_down", _c_void), ("b_down", _c_void),
+                ("dom_down_f8", _c_void), ("dom_down_f8_scale", _c_void)]
 
 
 class LxDenseLayer(ctypes.Structure):
     _fields_ = [("E", _c_i32), ("d", _c_i32), ("f", _c_i32), ("dtype", _c_i32),
-                ("w_gate", _c_void), ("w_up", _c_void), ("w_down", _c_void)]
+                ("w_gate", _c_void), ("w_up", _c_void), ("w_down", _c_void),
+                ("w_down_f8", _c_void), ("w_down_f8_scale", _c_void)]
 
 
 EXPORTS = {
@@ -72,6 +75,7 @@ EXPORTS = {
     "lx_bucket": (_c_i32, [ctypes.POINTER(LxTreeLayer), _c_i32, _c_i32, _c_void, _c_i32, _c_void,
                            _c_void, _c_void, _c_void, ctypes.c_size_t, _c_void]),
     "lx_read_device_status": (_c_i32, [_c_void, _c_void, ctypes.POINTER(ctypes.c_uint32)]),
+    "lx_quantize_f8": (_c_i32, [_c_void, _c_i32, _c_i32, _c_i32, _c_void, _c_void, _c_void]),
     "lx_profile_enable": (_c_i32, [_c_i32]),
     "lx_profile_collect": (_c_i32, []),
     "lx_profile_count": (_c_i32, []),
@@ -167,6 +171,10 @@ class DeviceLayer:
     anchor_up: torch.Tensor
     anchor_down: torch.Tensor
     levels: list = field(default_factory=list)
+    # optional fp8 copy of anchor_down (lx_quantize_f8): uint8 [n][d][f] and
+    # int32 scale words [n][d][f // 64]
+    anchor_down_f8: Optional[torch.Tensor] = None
+    anchor_down_f8_scale: Optional[torch.Tensor] = None
 
     @property
     def lx_dtype(self) -> int:
@@ -182,6 +190,7 @@ class DeviceLayer:
         s.n_anchors = self.n_anchors
         s.anchor_gate, s.anchor_up, s.anchor_down = (_ptr(self.anchor_gate), _ptr(self.anchor_up),
                                                      _ptr(self.anchor_down))
+        s.anchor_down_f8, s.anchor_down_f8_scale = _ptr(self.anchor_down_f8), _ptr(self.anchor_down_f8_scale)
         s.n_levels = len(self.levels)
         for i, lv in enumerate(self.levels):
             c = s.levels[i]
@@ -202,6 +211,7 @@ class DeviceLayer:
         s.cluster_of, s.factor_of = _ptr(lv.parent), _ptr(lv.factor_of)
         s.dom_gate, s.dom_up, s.dom_down = (_ptr(self.anchor_gate), _ptr(self.anchor_up),
                                             _ptr(self.anchor_down))
+        s.dom_down_f8, s.dom_down_f8_scale = _ptr(self.anchor_down_f8), _ptr(self.anchor_down_f8_scale)
         s.a_gate, s.b_gate, s.a_up, s.b_up, s.a_down, s.b_down = (
             _ptr(lv.a_gate), _ptr(lv.b_gate), _ptr(lv.a_up), _ptr(lv.b_up), _ptr(lv.a_down),
             _ptr(lv.b_down))
@@ -213,11 +223,35 @@ class DeviceLayer:
         s = LxDenseLayer()
         s.E, s.d, s.f, s.dtype = self.E, self.d, self.f, self.lx_dtype
         s.w_gate, s.w_up, s.w_down = _ptr(self.anchor_gate), _ptr(self.anchor_up), _ptr(self.anchor_down)
+        s.w_down_f8, s.w_down_f8_scale = _ptr(self.anchor_down_f8), _ptr(self.anchor_down_f8_scale)
         return s
 
 
-def to_device(layer, device="cuda") -> DeviceLayer:
-    """Copy a host layer (fields as in ``lxsynth.Layer``) to device tensors."""
+def quantize_f8(w: torch.Tensor, stream=None):
+    """fp8 copy of bf16 weights [n][rows][cols] (lx_quantize_f8): returns
+    (uint8 [n][rows][cols], int32 scale words [n][rows][cols // 64])."""
+    if w.dtype != torch.bfloat16 or not w.is_contiguous() or w.dim() != 3:
+        raise ValueError("w must be a contiguous bf16 [n][rows][cols] tensor")
+    n, rows, cols = (int(v) for v in w.shape)
+    w8 = torch.empty(n, rows, cols, dtype=torch.uint8, device=w.device)
+    sc = torch.empty(n, rows, max(cols // 64, 1), dtype=torch.int32, device=w.device)
+    _check(lib().lx_quantize_f8(_ptr(w), n, rows, cols, _ptr(w8), _ptr(sc), _stream(stream)))
+    return w8, sc
+
+
+def attach_down_f8(layer: "DeviceLayer") -> "DeviceLayer":
+    """Give a bf16 layer the fp8 copy of its anchor down weights (used by the
+    anchor down projection where applicable); a no-op for other layers."""
+    if layer.dtype == "bf16" and layer.f % 64 == 0:
+        layer.anchor_down_f8, layer.anchor_down_f8_scale = quantize_f8(layer.anchor_down)
+    return layer
+
+
+def to_device(layer, device="cuda", lo8: bool = True) -> DeviceLayer:
+    """Copy a host layer (fields as in ``lxsynth.Layer``) to device tensors.
+    ``lo8``: also prepare the fp8 copy of the anchor down weights (bf16 layers
+    with f a multiple of 64), so the anchor down projection takes its fp8-lo
+    path."""
     dt = layer.dtype
     levels = []
     for lv in layer.levels:
@@ -227,10 +261,11 @@ def to_device(layer, device="cuda") -> DeviceLayer:
             rank=int(lv.rank),
             **{n: _dev_array(getattr(lv, n), dt, device)
                for n in ("a_gate", "b_gate", "a_up", "b_up", "a_down", "b_down")}))
-    return DeviceLayer(E=int(layer.E), d=int(layer.d), f=int(layer.f), dtype=dt,
-                       anchor_gate=_dev_array(layer.anchor_gate, dt, device),
-                       anchor_up=_dev_array(layer.anchor_up, dt, device),
-                       anchor_down=_dev_array(layer.anchor_down, dt, device), levels=levels)
+    dl = DeviceLayer(E=int(layer.E), d=int(layer.d), f=int(layer.f), dtype=dt,
+                     anchor_gate=_dev_array(layer.anchor_gate, dt, device),
+                     anchor_up=_dev_array(layer.anchor_up, dt, device),
+                     anchor_down=_dev_array(layer.anchor_down, dt, device), levels=levels)
+    return attach_down_f8(dl) if lo8 else dl
 
 
 # ----------------------------------------------------------------- calls

@@ -23,12 +23,12 @@ def L(root):
 def _declared(root):
     src = open(os.path.join(root, "include", "lorex.h")).read()
     src = re.sub(r"/\*.*?\*/", "", src, flags=re.S)
-    return sorted(set(re.findall(r"\b(lx_[a-z_]+)\s*\(", src)))
+    return sorted(set(re.findall(r"\b(lx_[a-z0-9_]+)\s*\(", src)))
 
 
 def test_every_declared_symbol_is_exported(L, root):
     names = _declared(root)
-    assert len(names) == len(lx.EXPORTS) == 16
+    assert len(names) == len(lx.EXPORTS) == 17
     for n in names:
         assert hasattr(L, n), n
         assert n in lx.EXPORTS, n
@@ -82,6 +82,14 @@ def test_workspace_bytes_valid_and_monotone(L):
     (lambda s: setattr(s.levels[0], "a_down", None), lx.LX_ERR_INVALID_ARGUMENT),  # null factor
     (lambda s: setattr(s, "n_levels", 5), lx.LX_ERR_INVALID_ARGUMENT),
     (lambda s: setattr(s, "E", 9000), lx.LX_ERR_UNSUPPORTED),
+    # fp8 down copy: both pointers or neither, aligned, bf16 with f % 64 == 0
+    (lambda s: setattr(s, "anchor_down_f8", FAKE), lx.LX_ERR_INVALID_ARGUMENT),
+    (lambda s: (setattr(s, "anchor_down_f8", FAKE + 8), setattr(s, "anchor_down_f8_scale", FAKE)),
+     lx.LX_ERR_INVALID_ARGUMENT),
+    (lambda s: (setattr(s, "anchor_down_f8", FAKE), setattr(s, "anchor_down_f8_scale", FAKE),
+                setattr(s, "f", 776)), lx.LX_ERR_UNSUPPORTED),
+    (lambda s: (setattr(s, "anchor_down_f8", FAKE), setattr(s, "anchor_down_f8_scale", FAKE),
+                setattr(s, "dtype", lx.LX_F32)), lx.LX_ERR_UNSUPPORTED),
 ])
 def test_descriptor_validation(L, mut, code):
     s = _tree()
@@ -110,6 +118,19 @@ def test_call_validation(L):
     assert L.lx_bucket(ctypes.byref(s), 64, 8, FAKE, 2, None, None, None, FAKE, need, None) \
         == lx.LX_ERR_INVALID_ARGUMENT
     assert L.lx_read_device_status(None, None, None) == lx.LX_ERR_INVALID_ARGUMENT
+
+
+def test_fp8_copy_planned_like_bf16_and_quantize_validation(L):
+    s = _tree()
+    plain = L.lx_moe_tree_workspace_bytes(ctypes.byref(s), 4096, 8)
+    s.anchor_down_f8, s.anchor_down_f8_scale = FAKE, FAKE
+    assert L.lx_moe_tree_workspace_bytes(ctypes.byref(s), 4096, 8) == plain
+    q = L.lx_quantize_f8
+    assert q(FAKE, 2, 8, 96, FAKE, FAKE, None) == lx.LX_ERR_UNSUPPORTED        # cols % 64
+    assert q(FAKE, -1, 8, 64, FAKE, FAKE, None) == lx.LX_ERR_INVALID_ARGUMENT
+    assert q(None, 2, 8, 64, FAKE, FAKE, None) == lx.LX_ERR_INVALID_ARGUMENT
+    assert q(FAKE, 2, 8, 64, FAKE + 4, FAKE, None) == lx.LX_ERR_INVALID_ARGUMENT
+    assert q(None, 0, 8, 64, None, None, None) == lx.LX_OK                      # empty: no launch
 
 
 def test_profile_entries_empty(L):

@@ -1,0 +1,97 @@
+"""The fp8 lo half of the anchor down projection.
+
+lx_quantize_f8 is checked byte for byte against an encoder written here from
+the format definitions (OCP e4m3: sign, 4 exponent bits with bias 7, 3
+mantissa bits, subnormals below 2^-6, 0x7E = 448 the largest finite value;
+E8M0: value 2^(byte - 127)), and the forward with the fp8 copy against the
+oracle and against the bf16 (hi, lo) path.
+"""
+import numpy as np
+import pytest
+import torch
+
+from lxsynth import make_problem
+from oracle import moe as O
+from paper_2608_07814_amd import lorex as lx
+from gpu_util import TOL_BF16, TOL_DESIGN, require_gpu, say, gpu_forward, err_ratio, sample_tokens
+
+pytestmark = pytest.mark.gpu
+
+
+def _e4m3_table():
+    codes = np.arange(0x7F)  # 0x00 .. 0x7E (0x7F is NaN)
+    e, m = codes >> 3, codes & 7
+    return np.where(e == 0, m / 8.0 * 2.0 ** -6, (1 + m / 8.0) * 2.0 ** (e - 7.0))
+
+
+def _encode_e4m3(x):
+    """Nearest e4m3 code (ties to the even code) of |x| <= 448, with x's sign."""
+    tab = _e4m3_table()
+    a = np.abs(x).ravel()
+    hi = np.searchsorted(tab, a, side="left").clip(1, len(tab) - 1)
+    lo = hi - 1
+    dlo, dhi = a - tab[lo], tab[hi] - a
+    pick = np.where(dlo < dhi, lo, np.where(dhi < dlo, hi, np.where(lo % 2 == 0, lo, hi)))
+    pick = np.where(a >= tab[-1], len(tab) - 1, pick)
+    return (pick | np.where(np.signbit(x.ravel()), 0x80, 0)).reshape(x.shape).astype(np.uint8)
+
+
+def _reference_quantize(w):
+    """w float64 [rows][cols] (bf16 values) -> codes [rows][cols], words [rows][cols // 64]."""
+    rows, cols = w.shape
+    blocks = w.reshape(rows, cols // 32, 32)
+    amax = np.abs(blocks).max(axis=2)
+    e = np.where(amax > 0, np.floor(np.log2(np.where(amax > 0, amax, 1.0))), -127)
+    b = np.clip(e - 7 + 127, 1, 254).astype(np.int64)
+    scaled = blocks * 2.0 ** (127 - b)[:, :, None]
+    codes = _encode_e4m3(scaled).reshape(rows, cols)
+    words = (b[:, 0::2] | (b[:, 1::2] << 8)).astype(np.int64)
+    return codes, words
+
+
+def test_quantize_f8_bytes():
+    require_gpu()
+    rng = np.random.default_rng(31)
+    w = (rng.standard_normal((2, 8, 192)) * 0.02).astype(np.float32)
+    w[0, 1, :32] = 0.0                    # an all-zero block
+    w[0, 2, 5] = 3.0                      # one large value in a block of small ones
+    w[1, 3, 64:96] *= 1e-4                # tiny block
+    w[1, 4, 7] = -w[1, 4, 7]
+    wt = torch.from_numpy(w).cuda().to(torch.bfloat16)
+    w8, sc = lx.quantize_f8(wt)
+    torch.cuda.synchronize()
+    wv = wt.float().cpu().numpy().astype(np.float64)
+    for n in range(2):
+        codes, words = _reference_quantize(wv[n])
+        assert np.array_equal(w8[n].cpu().numpy(), codes), n
+        assert np.array_equal(sc[n].cpu().numpy().astype(np.int64) & 0xFFFFFFFF, words), n
+
+
+@pytest.mark.parametrize("cfg,T", [(1, 384), (4, 96)])
+def test_lo8_forward_vs_oracle_and_bf16_pair(cfg, T):
+    """Both anchor-down paths meet the bar; the fp8 lo half stays within the
+    design bound (a lost lo half would give ~1e-2)."""
+    require_gpu()
+    p = make_problem(cfg, T=T)
+    ref = O.moe_forward(p.layer, p.x, p.routing.topk_ids, p.routing.topk_weights)
+    e8 = err_ratio(gpu_forward(p, dev_layer=lx.to_device(p.layer, lo8=True)), ref)
+    e16 = err_ratio(gpu_forward(p, dev_layer=lx.to_device(p.layer, lo8=False)), ref)
+    say(f"cfg{cfg} T={T}: fp8-lo err/RMS {e8:.3e}, bf16-pair err/RMS {e16:.3e}")
+    assert e16 <= TOL_DESIGN
+    assert e8 <= TOL_DESIGN
+
+
+def test_lo8_dense_comparator():
+    require_gpu()
+    from lxsynth import make_layer_flat
+    from helpers import random_routing
+    from lxsynth import Problem, Routing, f32_to_bf16_bits
+    layer = make_layer_flat(16, 16, 256, 128, 8, "bf16", 14)
+    layer.levels = []
+    rng = np.random.default_rng(15)
+    x = f32_to_bf16_bits(rng.standard_normal((300, 256)).astype(np.float32))
+    ids, w = random_routing(300, 4, 16, 16)
+    p = Problem(cfg={}, seed=15, layer=layer, x=x, routing=Routing(ids, w))
+    got = gpu_forward(p, kind="dense", dev_layer=lx.to_device(layer, lo8=True))
+    ref = O.moe_forward(layer, x, ids, w)
+    assert err_ratio(got, ref) <= TOL_DESIGN
