@@ -344,14 +344,20 @@ __device__ inline int wave_exscan(int v, int& total) {
   return incl - v;
 }
 
+// NL = the number of correction levels, a compile-time constant so that every
+// per-level loop unrolls and the level descriptors are read at fixed offsets
+// (their loads are issued together instead of one dependent load per use).
+template <int NL>
 __global__ __launch_bounds__(1024) void k_bucket_small(PrepareArgs pa, BucketArgs a) {
   extern __shared__ __attribute__((aligned(16))) unsigned char s_raw[];
   SmallLds& S = *(SmallLds*)s_raw;
   const int tid = threadIdx.x, nth = blockDim.x;
-  const int T = a.T, k = a.k, TK = T * k, E = a.E, L = a.L;
+  const int T = a.T, k = a.k, TK = T * k, E = a.E;
+  constexpr int L = NL;
   if (tid == 0) {
     S.bad = 0;
     int o = 0;
+#pragma unroll
     for (int l = 1; l <= L; ++l) {
       S.base[l] = o;
       o += pa.n_nodes[l];
@@ -365,6 +371,7 @@ __global__ __launch_bounds__(1024) void k_bucket_small(PrepareArgs pa, BucketArg
     S.w[s] = a.w ? a.w[s] : 0.f;
     if (e < -1 || e >= E) bad |= LX_DEVFLAG_BAD_ID;
   }
+#pragma unroll
   for (int l = 1; l <= L; ++l)
     for (int n = tid; n < pa.n_nodes[l]; n += nth) {
       S.par[S.base[l] + n] = pa.parent[l][n];
@@ -373,6 +380,7 @@ __global__ __launch_bounds__(1024) void k_bucket_small(PrepareArgs pa, BucketArg
   for (int n = tid; n < a.lv[0].n_nodes; n += nth) S.mask[0][n] = 0ull;
   lds_barrier();
 
+#pragma unroll
   for (int l = 0; l <= L; ++l) {
     const BucketLevel& lv = a.lv[l];
     const int N = lv.n_nodes;
@@ -508,7 +516,13 @@ bool bucket_small_ok(const BucketArgs& a) {
 }
 
 hipError_t launch_bucket_small(const PrepareArgs& pa, const BucketArgs& a, hipStream_t s) {
-  hipLaunchKernelGGL(k_bucket_small, dim3(1), dim3(1024), sizeof(SmallLds), s, pa, a);
+  switch (a.L) {
+    case 0: hipLaunchKernelGGL(k_bucket_small<0>, dim3(1), dim3(1024), sizeof(SmallLds), s, pa, a); break;
+    case 1: hipLaunchKernelGGL(k_bucket_small<1>, dim3(1), dim3(1024), sizeof(SmallLds), s, pa, a); break;
+    case 2: hipLaunchKernelGGL(k_bucket_small<2>, dim3(1), dim3(1024), sizeof(SmallLds), s, pa, a); break;
+    case 3: hipLaunchKernelGGL(k_bucket_small<3>, dim3(1), dim3(1024), sizeof(SmallLds), s, pa, a); break;
+    default: hipLaunchKernelGGL(k_bucket_small<4>, dim3(1), dim3(1024), sizeof(SmallLds), s, pa, a); break;
+  }
   return hipGetLastError();
 }
 

@@ -362,8 +362,11 @@ __global__ __launch_bounds__(kFastThr) void k_combine_fast(TokenArgs a) {
   }
 }
 
-// Threads per workgroup for n 4-column groups: whole wavefronts, at most kFastThr.
-int fast_threads(int cols) {
+// Threads per workgroup for n 4-column groups: whole wavefronts, at most
+// kFastThr; one wavefront for small batches, whose token count alone would
+// give fewer workgroups than the chip has compute units.
+int fast_threads(int cols, int T) {
+  if (T < 512) return 64;
   const int g = (cols / 4 + 63) / 64 * 64;
   return g < 64 ? 64 : g > kFastThr ? kFastThr : g;
 }
@@ -381,7 +384,7 @@ hipError_t launch_swiglu_reduce(const TokenArgs& a, hipStream_t s) {
   if (a.T == 0) return hipSuccess;
   const int fmt = uniform_fmt(a);
   if (a.k <= kFastK && a.L >= 1 && a.L <= kFastL && fmt >= 0) {
-    const int thr = fast_threads(a.f);
+    const int thr = fast_threads(a.f, a.T);
     const dim3 grid(a.T, (a.f / 4 + thr - 1) / thr);
     if (a.L == 1 && fmt)
       hipLaunchKernelGGL((k_swiglu_fast<1, true>), grid, dim3(thr), 0, s, a);
@@ -403,7 +406,7 @@ hipError_t launch_combine(const TokenArgs& a, hipStream_t s) {
   if (a.T == 0) return hipSuccess;
   const int fmt = uniform_fmt(a);
   if (a.k <= kFastK && a.L <= kFastL && fmt >= 0) {
-    const int thr = fast_threads(a.d);
+    const int thr = fast_threads(a.d, a.T);
     const dim3 grid(a.T, (a.d / 4 + thr - 1) / thr);
     switch (a.L * 2 + fmt) {
       case 0: hipLaunchKernelGGL((k_combine_fast<0, false>), grid, dim3(thr), 0, s, a); break;
