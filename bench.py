@@ -41,6 +41,7 @@ def parse():
     ap.add_argument("--warmup", type=int, default=20)
     ap.add_argument("--config", type=int, default=1)
     ap.add_argument("--seed", type=int, default=None)
+    ap.add_argument("--tokens", type=int, default=None, help="override the workload's token count")
     ap.add_argument("--no-dense", action="store_true", help="skip the dense comparator")
     ap.add_argument("--no-cpu", action="store_true", help="skip the CPU oracle baseline")
     ap.add_argument("--cpu-tokens", type=int, default=4096)
@@ -204,7 +205,7 @@ def main():
     if a.copy_calibration:
         copy_calibration(torch)
         return
-    p = make_problem(a.config, seed=a.seed)
+    p = make_problem(a.config, seed=a.seed, T=a.tokens)
     cfg = p.cfg
     T, k = p.T, p.k
     layer = p.layer
@@ -263,7 +264,7 @@ def main():
     dom = max(prof.items(), key=lambda kv: kv[1][1])[0]
     fl, by = kernel_work(dom, P, rows, touched)
     dom_avg_s = prof[dom][1] / prof[dom][0] * 1e-3
-    workload = cfg["name"]
+    workload = cfg["name"] if a.tokens is None else f"{cfg['name']} at T={T}"
     if fl and fl / max(by, 1) >= RIDGE:
         roof = dict(bound="mfma", achieved=round(fl / dom_avg_s / 1e12, 2), peak=PEAK_BF16_FLOPS / 1e12,
                     unit="TFLOP/s", frac=round(fl / dom_avg_s / PEAK_BF16_FLOPS, 4))
@@ -309,9 +310,22 @@ def main():
         dcopies = [dd] + [clone_layer(dd) for _ in range(max(a.rotate, 1) - 1)]
         dcall = rotating([lx.PreparedCall(c, xd, ids, w, outd, wsd, "dense") for c in dcopies])
         dms, _ = time_steps(dcall, a.steps, a.warmup, torch)
+        # algorithmic work of the dense layer: every touched expert's three
+        # matrices once, 6df FLOPs per routed slot
+        ids_np = p.routing.topk_ids
+        valid = ids_np[(ids_np >= 0) & (ids_np < layer.E)]
+        e_touched = int(np.unique(valid).size)
+        d_flops = 6 * layer.d * layer.f * int(valid.size)
+        d_bytes = 3 * layer.d * layer.f * 2 * e_touched + T * layer.d * (2 + 4) + T * k * 8
         dense = dict(tokens_per_s=round(T / (dms * 1e-3), 1), ms_per_step=round(dms, 4),
                      speedup_of_compressed=round(dms / ms, 3),
-                     alg_gflop=round(6 * layer.d * layer.f * T * k / 1e9, 2))
+                     alg_gflop=round(d_flops / 1e9, 2), alg_mbytes=round(d_bytes / 1e6, 1),
+                     experts_touched=e_touched,
+                     alg_flops_ratio=round(d_flops / work["flops"], 4),
+                     alg_bytes_ratio=round(d_bytes / work["bytes"], 4))
+        if cfg.get("routing") == "coselect":
+            # per-token cost ratio of Sec. 5 (k experts sharing one dominant)
+            dense["analytic_speedup"] = round(acc.closed_form_speedup(k, layer.f, layer.d, ranks[1]), 4)
         del dd, dcopies, dcall, wsd, outd
 
     cpu = None
@@ -348,7 +362,7 @@ def main():
         "scaling": "weak",
         "vs_baseline": None,
         "dtype": "bf16",
-        "data": "synthetic (seeded; Gaussian or community routing; random-init weights)",
+        "data": "synthetic (seeded; Gaussian, community or co-selected routing; random-init weights)",
         "config": {"workload": workload, "T": T, "d": layer.d, "f": layer.f, "E": layer.E,
                    "k": k, "anchors": layer.n_anchors, "ranks": ranks[1:], "layer": kind,
                    "seed": p.seed, "out_dtype": "f32",

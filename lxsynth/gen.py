@@ -43,6 +43,11 @@ CONFIGS = {
     4: dict(name="tree-d4096-f1024-E256-roots4-subs32-r128-r64-T8192", kind="tree",
             dtype="bf16", E=256, d=4096, f=1024, k=8, T=8192, n_roots=4,
             subs_per_root=8, r_sub=128, r_leaf=64, routing="gaussian"),
+    # the per-token cost example of Sec. 5 (Fig. flops): Mixtral-8x7B expert
+    # shape, all 8 experts in one cluster, each token's two experts co-selected
+    # among the corrected members (both pay a rank-64 correction)
+    5: dict(name="cosel-d4096-f14336-E8-C1-r64-k2-T1", kind="flat", dtype="bf16",
+            E=8, C=1, k=2, d=4096, f=14336, r=64, T=1, routing="coselect"),
 }
 
 
@@ -298,6 +303,28 @@ def route_community(T: int, members: list, k: int, p_home: float, seed: int) -> 
     return Routing(topk_ids=ids, topk_weights=w.astype(np.float32))
 
 
+def route_coselect(T: int, corrected: list, k: int, seed: int) -> Routing:
+    """Every token's k experts come from one cluster and all carry a correction.
+
+    ``corrected[c]`` lists cluster c's members that carry a correction (all
+    but the dominant). Per token a cluster is drawn uniformly among those with
+    at least k such members; its k experts are drawn uniformly without
+    replacement among them, in draw order. Weights are the softmax of k iid
+    N(0, 1) logits, in slot order.
+    """
+    rng = np.random.default_rng(_children(seed)[_S_ROUTE_EXTRA])
+    pools = [m for m in corrected if len(m) >= k]
+    if not pools:
+        raise ValueError("no cluster has k corrected members")
+    which = rng.integers(0, len(pools), size=T)
+    ids = np.empty((T, k), dtype=np.int32)
+    for t in range(T):
+        pool = pools[int(which[t])]
+        ids[t] = np.asarray(pool)[rng.permutation(len(pool))[:k]]
+    w = _softmax_rows(rng.standard_normal((T, k)))
+    return Routing(topk_ids=ids, topk_weights=w.astype(np.float32))
+
+
 def _cluster_members(layer: Layer) -> list:
     lv = layer.levels[-1]
     members = [[] for _ in range(layer.n_anchors)]
@@ -335,6 +362,10 @@ def make_problem(cfg, seed: Optional[int] = None, T: Optional[int] = None,
     elif cfg["routing"] == "community":
         routing = route_community(cfg["T"], _cluster_members(layer), cfg["k"],
                                   cfg["p_home"], seed)
+    elif cfg["routing"] == "coselect":
+        fo = layer.levels[-1].factor_of
+        corrected = [[e for e in m if fo[e] >= 0] for m in _cluster_members(layer)]
+        routing = route_coselect(cfg["T"], corrected, cfg["k"], seed)
     else:
         raise ValueError(cfg["routing"])
     return Problem(cfg=cfg, seed=seed, layer=layer, x=x, routing=routing)

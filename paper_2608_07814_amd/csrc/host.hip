@@ -94,6 +94,8 @@ struct LevelPlan {
   size_t hist, offsets, row_token, slot_row, slot_flags, fac;
   size_t tiles[kNumTab], n_tiles[kNumTab];
   size_t gu, z, hbar, v, y;
+  size_t part, cnt;   // split-K partial tiles and counters (skinny levels)
+  int64_t n_cnt;
 };
 
 struct Plan {
@@ -186,6 +188,11 @@ Plan make_plan(const lx_tree_layer& t, int T, int k) {
     q.hbar = take(work ? R * p.f * 4 : 0);
     q.v = take(l > 0 && work ? R * q.rank * 4 : 0);
     q.y = take(work ? R * p.d * 4 : 0);
+    // one counter per work item of the level's widest skinny product
+    const int widest = std::max(std::max(2 * p.f, p.d), 2 * q.rank);
+    q.n_cnt = p.skinny[l] && work && T > 0 ? q.tiles_max[kTabSkinny] * ((widest + kSkinnyBN - 1) / kSkinnyBN) : 0;
+    q.part = take(q.n_cnt ? (size_t)kSplitCap * kSkinnyBM * kSkinnyBN * 4 : 0);
+    q.cnt = take((size_t)q.n_cnt * 4);
   }
   p.total = off;
   return p;
@@ -443,6 +450,8 @@ lx_status run(const lx_tree_layer& t, int T, int k, const void* x, const int32_t
       b.tiles[i] = (TileEntry*)(W + q.tiles[i]);
       b.n_tiles[i] = (int32_t*)(W + q.n_tiles[i]);
     }
+    b.split_cnt = (uint32_t*)(W + q.cnt);
+    b.n_split_cnt = (int32_t)q.n_cnt;
   }
   if (bucket_small_ok(ba)) {
     LX_LAUNCH("bucket_small", launch_bucket_small(pa, ba, lstream));
@@ -491,6 +500,11 @@ lx_status run(const lx_tree_layer& t, int T, int k, const void* x, const int32_t
         return fail(LX_ERR_UNSUPPORTED, std::string(name) + ": shape not supported by the skinny GEMM");
       g.tiles = ba.lv[l].tiles[kTabSkinny];
       g.n_tiles = ba.lv[l].n_tiles[kTabSkinny];
+      if (q.n_cnt >= (int64_t)q.tiles_max[kTabSkinny] * ((g.ncols[0] + g.ncols[1] + kSkinnyBN - 1) / kSkinnyBN)) {
+        g.part = (float*)(W + q.part);
+        g.cnt = (uint32_t*)(W + q.cnt);
+        g.split_cap = kSplitCap;
+      }
       if (batch_mode) {
         if (npend == kSkinnyMaxProblems) {
           const lx_status st = flush();

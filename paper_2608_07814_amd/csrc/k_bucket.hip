@@ -202,6 +202,7 @@ __global__ __launch_bounds__(1024) void k_bucket_scan(BucketArgs a) {
   const int N = lv.n_nodes, NT = a.n_tok_tiles;
   const int64_t total = (int64_t)N * NT;
   const int nth = blockDim.x, tid = threadIdx.x;
+  for (int i = tid; i < lv.n_split_cnt; i += nth) lv.split_cnt[i] = 0u;
 
   // exclusive scan of hist in (node, tile) order, in place; entry (n, 0)
   // is node n's offset (kept in LDS for the tile tables)
@@ -378,6 +379,9 @@ __global__ __launch_bounds__(1024) void k_bucket_small(PrepareArgs pa, BucketArg
       S.fo[S.base[l] + n] = pa.factor_of[l][n];
     }
   for (int n = tid; n < a.lv[0].n_nodes; n += nth) S.mask[0][n] = 0ull;
+#pragma unroll
+  for (int l = 0; l <= L; ++l)
+    for (int i = tid; i < a.lv[l].n_split_cnt; i += nth) a.lv[l].split_cnt[i] = 0u;
   lds_barrier();
 
 #pragma unroll

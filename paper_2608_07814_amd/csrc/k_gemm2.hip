@@ -521,12 +521,29 @@ void k_gemm_big(GemmArgs p, int ntn) {
 }
 
 // ---------------------------------------------------------------- skinny
+// Device-scope coherent 32-bit store and load (relaxed agent-scope atomics):
+// another XCD's workgroup that reads the location after this access has
+// completed sees its value.
+__device__ __forceinline__ void store_dev(float* p, float v) {
+  __hip_atomic_store(p, v, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+}
+__device__ __forceinline__ float load_dev(const float* p) {
+  return __hip_atomic_load(const_cast<float*>(p), __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+}
+
 // 32 x 64 output tile per 128-thread workgroup (two wavefronts, one 32x32
-// MFMA block each), K-slabs of 64 through an LDS ring of SK_NST stages: 4
-// (48 KB, three workgroups per compute unit, three slabs in flight while one
-// is consumed), or 2 for products whose K is at most two slabs (24 KB, six
-// workgroups per compute unit). With few rows per tile the kernel streams
-// weights and is bound by HBM, not by the MFMAs.
+// MFMA block each). The K loop runs over steps through an LDS ring of SK_NST
+// stages; a step is one 64-wide slab of A's K with its weight slab, or, for
+// a bf16 (hi, lo) input against one weight row (K = 2 Kb) longer than two
+// weight slabs, one weight slab with both halves of A, so every weight slab
+// is fetched once. Rings: 4
+// stages of 12 KB or 3 of 16 KB (three workgroups per compute unit, two or
+// three steps in flight while one is consumed), 2 stages for products of at
+// most two steps. With few rows per tile the kernel streams weights and is
+// bound by HBM, not by the MFMAs. A product with few output tiles and a long
+// K (e.g. a down projection at batch 1) is split along K so that enough
+// workgroups stream weight slabs at once; the partial tiles meet in the
+// workspace and the last workgroup of a tile adds them.
 constexpr int SK_THR = 128;
 
 
@@ -534,12 +551,12 @@ constexpr int SK_THR = 128;
 // products that read the same input rows): problem i owns workgroups
 // [base[i], base[i+1]); every base is a multiple of 8, so the XCD of a
 // workgroup is its index within the problem modulo 8.
-template <int SK_NST>
+template <int SK_NST, int PER>
 __global__ __launch_bounds__(SK_THR) void k_gemm_skinny(SkinnyBatch b) {
   constexpr int BM = kSkinnyBM, BN = kSkinnyBN;
   constexpr int A_ROUNDS = BM * 8 / SK_THR, B_ROUNDS = BN * 8 / SK_THR;
-  constexpr int R = A_ROUNDS + B_ROUNDS;
-  constexpr int SA = BM * BK2, STAGE = (BM + BN) * BK2;
+  constexpr int R = PER * A_ROUNDS + B_ROUNDS;
+  constexpr int SA = BM * BK2, STAGE = (PER * BM + BN) * BK2;
   __shared__ __attribute__((aligned(1024))) u16 smem[SK_NST * STAGE];
 
   int pi = 0;
@@ -549,22 +566,48 @@ __global__ __launch_bounds__(SK_THR) void k_gemm_skinny(SkinnyBatch b) {
   const int ofmt = b.ofmt[pi];
   const int wg = (int)blockIdx.x - b.base[pi];
 
-  // one work item per workgroup, XCD-contiguous order (workgroups >= items)
-  const int real = *p.n_tiles * ntn;
+  const int K = p.K;
+  const int Kb = p.Kb > 0 ? p.Kb : K;
+  const int nk = K / BK2;
+  // slab kt: period kt % nper of weight slab kt / nper (as in k_gemm_big)
+  const int nper = K / Kb, nkw = nk / nper;
+  // A step of the K loop: PER == 1, one 64-wide slab of A's K (any nper);
+  // PER == 2 (nper == 2), one weight slab, multiplied by both periods of A
+  // (the weight slab is loaded once for the hi and the lo half)
+  const int spw = PER == 1 ? nper : 1;
+
+  // Split-K when the launch's work items are few: each product's items get
+  // S splits of cw weight slabs (the last possibly shorter, none empty),
+  // with S * (items of the whole launch) <= split_cap.
+  const int items = *p.n_tiles * ntn;
+  int S = 1, cw = nkw;
+  if (p.part && items > 0) {
+    int all = 0;
+    for (int i = 0; i < b.n; ++i) all += *b.g[i].n_tiles * b.ntn[i];
+    int s = p.split_cap / all;
+    s = s < nkw / kSplitMinSlabs ? s : nkw / kSplitMinSlabs;
+    if (s > 1) {
+      cw = (nkw + s - 1) / s;
+      S = (nkw + cw - 1) / cw;
+    }
+  }
+  // one work unit (item, split) per workgroup, XCD-contiguous order
+  // (workgroups >= units)
+  const int real = items * S;
   const int q = real / NXCD, rmd = real % NXCD;
   const int x = wg % NXCD;
   const int Lg = x * q + (x < rmd ? x : rmd) + wg / NXCD;
   if (Lg >= x * q + (x < rmd ? x : rmd) + q + (x < rmd ? 1 : 0)) return;
-  const int ti = Lg / ntn, nt = Lg % ntn;
+  const int item = Lg / S, sp = Lg - item * S;
+  const int ti = item / ntn, nt = item % ntn;
+  const int kt0 = sp * cw * spw;
+  const int nkl = ((sp + 1) * cw < nkw ? (sp + 1) * cw : nkw) * spw - kt0;
 
   const int tid = threadIdx.x;
   const int wave = tid >> 6, lane = tid & 63;
   const TileEntry te = p.tiles[ti];
   const int n0 = nt * BN;
   const int ncol = p.ncols[0] + p.ncols[1];
-  const int K = p.K;
-  const int Kb = p.Kb > 0 ? p.Kb : K;
-  const int nk = K / BK2;
   const int tpart = n0 < p.ncols[0] ? 0 : 1;
   const int akoff = p.a_koff[tpart];
   const u16* __restrict__ Ab = (const u16*)p.A;
@@ -592,16 +635,27 @@ __global__ __launch_bounds__(SK_THR) void k_gemm_skinny(SkinnyBatch b) {
     const int n = n0 + row < ncol ? n0 + row : ncol - 1;
     bptr[j] = (n < p.ncols[0] ? Bw0 + (int64_t)n * Kb : Bw1 + (int64_t)(n - p.ncols[0]) * Kb) + c * 8;
   }
-  // slab kt: period kt % nper of weight slab kt / nper (as in k_gemm_big)
-  const int nper = K / Kb;
+  // stage = [A period 0 | (A period 1) | B], one 64-wide K slab each
   auto issue = [&](int st, int kt) {
     u16* const sA = smem + st * STAGE;
-    const int q = kt / nper, per = kt - q * nper;
-    const int kb = q * BK2, ka = per * Kb + kb;
+    int kb;
+    if (PER == 1) {
+      const int qq = kt / nper, per = kt - qq * nper;
+      kb = qq * BK2;
+      const int ka = per * Kb + kb;
 #pragma unroll
-    for (int j = 0; j < A_ROUNDS; ++j) load_lds16(Ab + (aoff[j] + (uint32_t)ka), sA + (j * SK_THR + wave * 64) * 8);
+      for (int j = 0; j < A_ROUNDS; ++j)
+        load_lds16(Ab + (aoff[j] + (uint32_t)ka), sA + (j * SK_THR + wave * 64) * 8);
+    } else {
+      kb = kt * BK2;
 #pragma unroll
-    for (int j = 0; j < B_ROUNDS; ++j) load_lds16(bptr[j] + kb, sA + SA + (j * SK_THR + wave * 64) * 8);
+      for (int per = 0; per < PER; ++per)
+#pragma unroll
+        for (int j = 0; j < A_ROUNDS; ++j)
+          load_lds16(Ab + (aoff[j] + (uint32_t)(per * Kb + kb)), sA + per * SA + (j * SK_THR + wave * 64) * 8);
+    }
+#pragma unroll
+    for (int j = 0; j < B_ROUNDS; ++j) load_lds16(bptr[j] + kb, sA + PER * SA + (j * SK_THR + wave * 64) * 8);
   };
 
   f32x16 acc;
@@ -609,36 +663,40 @@ __global__ __launch_bounds__(SK_THR) void k_gemm_skinny(SkinnyBatch b) {
   for (int i = 0; i < 16; ++i) acc[i] = 0.f;
   auto compute = [&](int st) {
     const u16* const sA = smem + st * STAGE;
-    const u16* const sB = sA + SA;
+    const u16* const sB = sA + PER * SA;
     const int ra = lane & 31, rb = wave * 32 + (lane & 31);
-    bf16x8 fa[4], fb[4];
+    bf16x8 fa[PER][4], fb[4];
 #pragma unroll
     for (int ks = 0; ks < 4; ++ks) {
       const int kc = ks * 2 + (lane >> 5);
-      fa[ks] = *(const bf16x8*)&sA[lds_off2(ra, kc)];
+#pragma unroll
+      for (int per = 0; per < PER; ++per) fa[per][ks] = *(const bf16x8*)&sA[per * SA + lds_off2(ra, kc)];
       fb[ks] = *(const bf16x8*)&sB[lds_off2(rb, kc)];
     }
 #pragma unroll
-    for (int ks = 0; ks < 4; ++ks) acc = __builtin_amdgcn_mfma_f32_32x32x16_bf16(fa[ks], fb[ks], acc, 0, 0, 0);
+    for (int ks = 0; ks < 4; ++ks)
+#pragma unroll
+      for (int per = 0; per < PER; ++per)
+        acc = __builtin_amdgcn_mfma_f32_32x32x16_bf16(fa[per][ks], fb[ks], acc, 0, 0, 0);
   };
 
-  // Slab kt lives in stage kt % SK_NST. Slabs 0 .. SK_NST-1 are issued up
-  // front; after the barrier that follows slab kt's compute, stage
-  // kt % SK_NST is free and slab kt + SK_NST goes there.
-  static_assert((SK_NST & (SK_NST - 1)) == 0, "power-of-two ring");
-  const int npre = nk < SK_NST ? nk : SK_NST;
-  for (int i = 0; i < npre; ++i) issue(i, i);
+  // Local step i (global kt0 + i) lives in stage i % SK_NST. Steps
+  // 0 .. SK_NST-1 are issued up front; after the barrier that follows step
+  // i's compute, stage i % SK_NST is free and step i + SK_NST goes there.
+  static_assert(SK_NST >= 2 && SK_NST <= 4, "ring depth");
+  const int npre = nkl < SK_NST ? nkl : SK_NST;
+  for (int i = 0; i < npre; ++i) issue(i, kt0 + i);
   wait_slabs<R>(npre - 1);
   bar();
-  for (int kt = 0; kt < nk; ++kt) {
-    compute(kt & (SK_NST - 1));
-    if (kt + 1 < nk) {
-      // slabs issued so far: 0 .. min(kt + SK_NST - 1, nk - 1); wait for kt + 1
-      const int last = kt + SK_NST - 1 < nk - 1 ? kt + SK_NST - 1 : nk - 1;
-      wait_slabs<R>(last - (kt + 1));
+  for (int i = 0; i < nkl; ++i) {
+    compute(i % SK_NST);
+    if (i + 1 < nkl) {
+      // steps issued so far: 0 .. min(i + SK_NST - 1, nkl - 1); wait for i + 1
+      const int last = i + SK_NST - 1 < nkl - 1 ? i + SK_NST - 1 : nkl - 1;
+      wait_slabs<R>(last - (i + 1));
       wait_lgkm0();
       bar();
-      if (kt + SK_NST < nk) issue(kt & (SK_NST - 1), kt + SK_NST);
+      if (i + SK_NST < nkl) issue(i % SK_NST, kt0 + i + SK_NST);
     }
   }
   wait_lgkm0();
@@ -652,6 +710,36 @@ __global__ __launch_bounds__(SK_THR) void k_gemm_skinny(SkinnyBatch b) {
   for (int i = 0; i < 16; ++i) ep[(8 * (i >> 2) + 4 * (lane >> 5) + (i & 3)) * PITCH + (lane & 31)] = acc[i];
   const int c4 = (lane % LPR) * 4;
   const int col = n0 + wave * 32 + c4;
+  if (S > 1) {
+    // Partial tile -> slot Lg; the last workgroup of the item to arrive adds
+    // the item's S slots in split order (same sum whatever the arrival
+    // order). The slots and the counter are only accessed with device-scope
+    // coherent operations (they bypass the per-XCD L2 copies), so completing
+    // the slot stores before the counter increment is all the ordering the
+    // hand-off needs; no cache-wide write-back or invalidation is involved.
+    // Slot layout [wavefront][row][32 columns]: each 4-byte access
+    // instruction covers two rows, 256 contiguous bytes.
+    __shared__ int s_last;
+    const int nr = te.nrows;
+    const int rr = lane >> 5, cc = lane & 31;
+    float* const slot = p.part + (int64_t)Lg * (BM * BN) + wave * (32 * 32);
+    for (int r = rr; r < nr; r += 2) store_dev(slot + r * 32 + cc, ep[r * PITCH + cc]);
+    wait_vmcnt<0>();
+    __syncthreads();
+    if (tid == 0)
+      s_last = __hip_atomic_fetch_add(p.cnt + item, 1u, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT) ==
+               (unsigned)(S - 1);
+    __syncthreads();
+    if (!s_last) return;
+    if (tid == 0)  // ready for the next product of this level
+      __hip_atomic_store(p.cnt + item, 0u, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+    const float* const first = p.part + (int64_t)item * S * (BM * BN) + wave * (32 * 32);
+    for (int r = rr; r < nr; r += 2) {
+      float v = load_dev(first + r * 32 + cc);
+      for (int t = 1; t < S; ++t) v += load_dev(first + (int64_t)t * (BM * BN) + r * 32 + cc);
+      ep[r * PITCH + cc] = v;
+    }
+  }
 #pragma unroll
   for (int ps = 0; ps < 32 / RPP; ++ps) {
     const int r = ps * RPP + lane / LPR;
@@ -810,19 +898,36 @@ hipError_t launch_gemm_skinny_batch(const GemmArgs* g, const int* ofmt, const in
     b.ntn[i] = (g[i].ncols[0] + g[i].ncols[1] + kSkinnyBN - 1) / kSkinnyBN;
     b.ofmt[i] = ofmt[i];
     b.base[i] = wg;
-    const int items = grid_tiles[i] * b.ntn[i];  // >= work items of problem i
-    wg += (items + NXCD - 1) / NXCD * NXCD;
+    wg += skinny_grid(g[i], (int64_t)grid_tiles[i] * b.ntn[i]);  // a multiple of 8
   }
   b.base[n] = wg;
   b.n = n;
   if (wg <= 0) return hipSuccess;
-  int max_nk = 0;
-  for (int i = 0; i < n; ++i) max_nk = std::max(max_nk, g[i].K / BK2);
-  if (max_nk <= 2)
-    hipLaunchKernelGGL(k_gemm_skinny<2>, dim3(wg), dim3(SK_THR), 0, s, b);
-  else
-    hipLaunchKernelGGL(k_gemm_skinny<4>, dim3(wg), dim3(SK_THR), 0, s, b);
+  // every product a bf16 (hi, lo) pair against one weight row, some longer
+  // than two weight slabs: one weight slab per step for both halves
+  // (3-stage ring of 16 KB stages)
+  bool pair = true;
+  int max_steps = 0;
+  for (int i = 0; i < n; ++i) {
+    const int Kb = g[i].Kb > 0 ? g[i].Kb : g[i].K;
+    pair = pair && g[i].K == 2 * Kb;
+    max_steps = std::max(max_steps, g[i].K / BK2);
+  }
+  if (pair && max_steps > 4) {
+    hipLaunchKernelGGL((k_gemm_skinny<3, 2>), dim3(wg), dim3(SK_THR), 0, s, b);
+  } else if (max_steps <= 2) {
+    hipLaunchKernelGGL((k_gemm_skinny<2, 1>), dim3(wg), dim3(SK_THR), 0, s, b);
+  } else {
+    hipLaunchKernelGGL((k_gemm_skinny<4, 1>), dim3(wg), dim3(SK_THR), 0, s, b);
+  }
   return hipGetLastError();
+}
+
+int skinny_grid(const GemmArgs& g, int64_t items_max) {
+  const int Kb = g.Kb > 0 ? g.Kb : g.K;
+  int64_t n = items_max;
+  if (g.part && Kb / BK2 >= 2 * kSplitMinSlabs) n = std::max<int64_t>(n, g.split_cap);
+  return (int)((n + NXCD - 1) / NXCD * NXCD);
 }
 
 hipError_t launch_gemm_skinny(const GemmArgs& g, int ofmt, int grid_tiles, hipStream_t s) {

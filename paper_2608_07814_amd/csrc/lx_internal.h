@@ -112,6 +112,8 @@ struct BucketLevel {
                            // node does work at this level (always at level 0)
   TileEntry* tiles[kNumTab];  // [tiles_max of the table]
   int32_t* n_tiles[kNumTab];  // [1] each
+  uint32_t* split_cnt;        // [n_split_cnt] split-K arrival counters, zeroed
+  int32_t n_split_cnt;        // here for the level's skinny GEMMs
 };
 
 struct BucketArgs {
@@ -173,6 +175,15 @@ struct GemmArgs {
   const uint8_t* b8;         // [widx][n][Kb]
   const uint32_t* bsc;       // [widx][n][Kb / 64]
   int32_t a_lo8_off, a_sc_off;
+  // split-K (skinny kernel only): when the routed tiles give fewer work
+  // items than split_cap, each item's weight slabs are divided over up to
+  // split_cap / items workgroups. Each writes its fp32 partial tile to its
+  // slot of part ([split_cap][kSkinnyBM][kSkinnyBN]); the last of an item's
+  // workgroups to arrive (per-item counters cnt, zero on entry and left zero)
+  // adds the partials in split order and writes C. Null part: no split.
+  float* part;
+  uint32_t* cnt;
+  int32_t split_cap;
 };
 
 enum AMode { A_BF16 = 0, A_F32_HILO = 1 };
@@ -208,6 +219,13 @@ hipError_t launch_gemm_big(const GemmArgs& g, int bm, int bn, int ofmt, int grid
 // HBM rather than by MFMA work on padding rows. Same operand conventions and
 // applicability as the large-tile kernel (with bn = kSkinnyBN).
 constexpr int kSkinnyBM = 32, kSkinnyBN = 64;
+// Split-K: partial-tile slots per level (three 48 KB-LDS workgroups per
+// compute unit on 256 compute units) and the fewest weight slabs (64 K
+// values) a split covers.
+constexpr int kSplitCap = 768, kSplitMinSlabs = 4;
+// Workgroups the skinny kernel launches for a product with at most
+// items_max work items (all splits of all items fit when splitting).
+int skinny_grid(const GemmArgs& g, int64_t items_max);
 hipError_t launch_gemm_skinny(const GemmArgs& g, int ofmt, int grid_tiles, hipStream_t s);
 // Up to kSkinnyMaxProblems independent skinny GEMMs in one launch.
 constexpr int kSkinnyMaxProblems = 1 + LX_MAX_LEVELS;

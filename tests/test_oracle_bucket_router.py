@@ -129,6 +129,25 @@ def test_community_routing_structure():
     assert np.all(np.abs(p.routing.topk_weights.sum(1) - 1) < 1e-6)
 
 
+def test_coselect_routing_structure():
+    """Configuration 5's routing, at a small layer: both experts of a token are
+    distinct corrected members of one cluster, uniformly spread over them."""
+    p = make_problem(config(5, d=64, f=128, r=8, T=3000))
+    ids = p.routing.topk_ids
+    fo = p.layer.levels[0].factor_of
+    assert ids.shape == (3000, 2)
+    assert np.all(ids[:, 0] != ids[:, 1])
+    assert np.all(fo[ids] >= 0)                       # never the dominant (expert 0)
+    counts = np.bincount(ids.ravel(), minlength=8)
+    assert counts[0] == 0 and np.all(np.abs(counts[1:] / 6000 - 1 / 7) < 0.02)
+    assert np.all(np.abs(p.routing.topk_weights.sum(1) - 1) < 1e-6)
+    # two clusters of 4: a token never mixes them
+    q = make_problem(config(5, E=8, C=2, d=64, f=128, r=8, T=500))
+    cl = q.layer.levels[0].parent
+    assert np.all(cl[q.routing.topk_ids[:, 0]] == cl[q.routing.topk_ids[:, 1]])
+    assert np.all(q.layer.levels[0].factor_of[q.routing.topk_ids] >= 0)
+
+
 def test_bf16_rounding_is_rne():
     vals = np.array([1.0, 1.0 + 2**-8, 1.0 + 3 * 2**-9, -2.5, 3.0e-3], dtype=np.float32)
     bits = f32_to_bf16_bits(vals)
