@@ -170,7 +170,9 @@ Plan make_plan(const lx_tree_layer& t, int T, int k) {
     q.bm[kTabBig] = kBigBM;
     q.bm[kTabSkinny] = kSkinnyBM;
     q.rows_max = (int64_t)T * std::min(k, q.N);
-    for (int b = 0; b < kNumTab; ++b) q.tiles_max[b] = q.rows_max / q.bm[b] + q.N + 1;
+    // tiles = sum over touched nodes of ceil(rows / bm) <= floor(rows / bm) +
+    // touched nodes, and at most min(N, rows) nodes are touched
+    for (int b = 0; b < kNumTab; ++b) q.tiles_max[b] = q.rows_max / q.bm[b] + std::min<int64_t>(q.N, q.rows_max);
     q.hist = take((size_t)q.N * p.NT * 4);
     q.offsets = take((size_t)(q.N + 1) * 4);
     q.row_token = take((size_t)q.rows_max * 4);

@@ -45,6 +45,27 @@ def test_bucket_definition_equals_bruteforce(kind, seed):
     _eq(a, b)
 
 
+@pytest.mark.parametrize("T,k,hot", [(1, 2, False), (7, 3, False), (64, 8, False), (300, 8, True),
+                                      (1000, 4, False)])
+def test_tile_count_bound(T, k, hot):
+    """The workspace's tile tables hold floor(R / bm) + min(N, R) entries per
+    level (R = T * min(k, N) rows at most): the tiles the bucketing makes,
+    sum over nodes of ceil(rows / bm), never exceed that."""
+    layer = tiny_tree(E=32, n_roots=2, subs=4)
+    parents, n_nodes = _structure(layer)
+    ids, _ = random_routing(T, k, layer.E, 500 + T, allow_dupes=True, drop_frac=0.1)
+    if hot:
+        ids[:, :2] = [3, 4]
+    lv, _ = B.bucket(parents, n_nodes, layer.E, ids)
+    for li, arrs in enumerate(lv):
+        cnt = np.diff(arrs["offsets"])
+        R = T * min(k, n_nodes[li])
+        assert cnt.sum() <= R
+        for bm in (32, 128, 256):
+            tiles = int(np.sum((cnt + bm - 1) // bm))
+            assert tiles <= R // bm + min(n_nodes[li], R)
+
+
 def test_bucket_invariants_cfg1_shape():
     p = make_problem(1, T=512)
     parents, n_nodes = _structure(p.layer)
