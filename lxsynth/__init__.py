@@ -44,5 +44,7 @@ from .gen import (  # noqa: F401
     make_x,
     route_gaussian,
     route_community,
+    route_coselect,
+    make_router,
     config,
 )

@@ -258,6 +258,15 @@ def _softmax_rows(logits: np.ndarray) -> np.ndarray:
     return e / e.sum(axis=1, keepdims=True)
 
 
+def make_router(d: int, E: int, dtype: str, seed: int) -> np.ndarray:
+    """Router weights [E, d] in the storage dtype: the same N(0, 1/d) draw that
+    ``route_gaussian`` uses (child stream of ``seed``), transposed to the
+    nn.Linear layout and stored (bf16: round to nearest even from fp32)."""
+    rng = np.random.default_rng(_children(seed)[_S_ROUTER])
+    w_r = rng.standard_normal((d, E)) / math.sqrt(d)
+    return _store(np.ascontiguousarray(w_r.T).astype(np.float32), dtype)
+
+
 def route_gaussian(x: np.ndarray, dtype: str, E: int, k: int, seed: int) -> Routing:
     """Unchanged top-k router on x @ W_r (fp64), softmax over the chosen logits."""
     T, d = x.shape

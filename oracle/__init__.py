@@ -14,9 +14,11 @@ Contents:
 * ``moe.moe_forward_bruteforce`` scalar Python loops for tiny shapes;
 * ``bucket.bucket``              the routing-bucketing arrays, from their
                                   definition (sort + unique), bit-exact target;
-* ``bucket.bucket_bruteforce``   the same arrays from explicit loops.
+* ``bucket.bucket_bruteforce``   the same arrays from explicit loops;
+* ``router.route_topk``          the unchanged top-k router (logits, top-k in
+                                  descending order, renormalised softmax), fp64.
 
 Every function is pinned by ``tests/test_oracle_*.py`` against brute force,
 closed forms, library routines and invariants of the method.
 """
-from . import bucket, moe  # noqa: F401
+from . import bucket, moe, router  # noqa: F401

@@ -221,3 +221,93 @@ def test_algorithmic_counts_from_buckets():
     assert rows[1].rows == S_nd
     assert c["flops"] == 6 * 2048 * 768 * U + 6 * 64 * (2048 + 768) * S_nd
     assert c["gate_up_flops"] == 4 * 2048 * 768 * U
+
+
+# ------------------------------------------------------------ router oracle
+def _router_bruteforce(x64, w64, k):
+    """Scalar loops: logits, selection by repeated maximum (lower index wins a
+    tie), weights exp(l_j) / sum over chosen exp(l_i)."""
+    T, d = x64.shape
+    E = w64.shape[0]
+    ids = np.zeros((T, k), np.int64)
+    ws = np.zeros((T, k))
+    for t in range(T):
+        lg = [math.fsum(float(x64[t, i]) * float(w64[e, i]) for i in range(d)) for e in range(E)]
+        left = list(range(E))
+        for j in range(k):
+            best = left[0]
+            for e in left[1:]:
+                if lg[e] > lg[best]:
+                    best = e
+            ids[t, j] = best
+            left.remove(best)
+        m = lg[ids[t, 0]]
+        ex = [math.exp(lg[e] - m) for e in ids[t]]
+        s = math.fsum(ex)
+        ws[t] = [v / s for v in ex]
+    return ids, ws
+
+
+@pytest.mark.parametrize("dtype", ["bf16", "f32"])
+def test_router_oracle_bruteforce(dtype):
+    from oracle import router as R
+    from lxsynth import make_router
+    from oracle.moe import to_f64
+    x = make_x(9, 24, dtype, 41)
+    w = make_router(24, 11, dtype, 41)
+    for k in (1, 3, 11):
+        ids, ws, lg = R.route_topk(x, w, dtype, k)
+        bi, bw = _router_bruteforce(to_f64(x, dtype), to_f64(w, dtype), k)
+        assert np.array_equal(ids, bi)
+        assert np.max(np.abs(ws - bw)) < 1e-14
+        assert np.all(np.abs(ws.sum(1) - 1) < 1e-14)
+        assert np.all(np.diff(np.take_along_axis(lg, ids.astype(np.int64), 1), axis=1) <= 0)
+    # k = E: every expert once; the weights are the full softmax
+    ids, ws, lg = R.route_topk(x, w, dtype, 11)
+    assert np.array_equal(np.sort(ids, 1), np.tile(np.arange(11), (9, 1)))
+    full = np.exp(lg - lg.max(1, keepdims=True))
+    full /= full.sum(1, keepdims=True)
+    assert np.max(np.abs(np.take_along_axis(full, ids.astype(np.int64), 1) - ws)) < 1e-14
+
+
+def test_router_oracle_ties_and_matrix():
+    """Identical router rows tie exactly: the lower expert index comes first.
+    The generated router matrix is the harness router's draw (same stream)."""
+    from oracle import router as R
+    from lxsynth import make_router
+    w = make_router(32, 6, "f32", 5)
+    w[4] = w[1]                      # experts 1 and 4 always tie
+    x = make_x(50, 32, "f32", 6)
+    ids, ws, lg = R.route_topk(x, w, "f32", 6)
+    pos = np.argsort(ids, axis=1)
+    assert np.all(pos[:, 1] < pos[:, 4])
+    both = ids[:, :2]
+    sel = np.all(np.isin(both, [1, 4]), axis=1)
+    assert np.allclose(ws[sel, 0], ws[sel, 1])
+    # same draw as the Gaussian harness router: its fp64 top-k agrees with the
+    # oracle on the fp32-stored matrix except at near-ties
+    p = make_problem(config(1, d=64, f=64, E=16, C=4, k=4, T=400))
+    wr = make_router(64, 16, "bf16", p.seed)
+    lg2 = R.router_logits(p.x, wr, "bf16")
+    ids2, _, _ = R.route_topk(p.x, wr, "bf16", 4)
+    gap = np.sort(lg2, 1)[:, ::-1]
+    # bf16 rounding of the matrix moves a logit by ~2^-9 of its scale (~0.002)
+    clear = np.min(np.abs(np.diff(gap[:, :5], axis=1)), axis=1) > 0.01
+    assert clear.mean() > 0.7
+    assert np.array_equal(ids2[clear], p.routing.topk_ids[clear])
+
+
+def test_fp32_sum_bound_covers_fp32_sums():
+    from oracle import router as R
+    from lxsynth import make_router
+    from oracle.moe import to_f64
+    x = make_x(20, 2048, "bf16", 7)
+    w = make_router(2048, 8, "bf16", 7)
+    exact = R.router_logits(x, w, "bf16")
+    b = R.fp32_sum_bound(x, w, "bf16")
+    xs, ws = to_f64(x, "bf16").astype(np.float32), to_f64(w, "bf16").astype(np.float32)
+    for order in (np.arange(2048), np.random.default_rng(0).permutation(2048)):
+        acc = np.zeros((20, 8), np.float32)
+        for i in order:               # sequential fp32 accumulation
+            acc += xs[:, i:i + 1] * ws[:, i][None, :]
+        assert np.all(np.abs(acc.astype(np.float64) - exact) <= b)
