@@ -53,6 +53,7 @@ def parse():
     ap.add_argument("--no-lo8", action="store_true",
                     help="no fp8 copy of the anchor down weights: the anchor down projection multiplies "
                          "both halves of its bf16 (hi, lo) input in bf16")
+    ap.add_argument("--no-route", action="store_true", help="skip timing the GPU top-k router")
     ap.add_argument("--copy-calibration", action="store_true",
                     help="only run a plain 1 GiB device-to-device copy 5 times (scales the "
                          "FETCH_SIZE / WRITE_SIZE counters to bytes)")
@@ -328,6 +329,30 @@ def main():
             dense["analytic_speedup"] = round(acc.closed_form_speedup(k, layer.f, layer.d, ranks[1]), 4)
         del dd, dcopies, dcall, wsd, outd
 
+    routed = None
+    if not a.no_route and layer.dtype == "bf16" and layer.d % 128 == 0 and layer.E <= 512:
+        # the unchanged top-k router on the GPU (lx_route_topk), alone and
+        # chained with the forward on one stream (ids and weights stay in HBM)
+        from lxsynth import make_router
+        wr = torch.from_numpy(make_router(layer.d, layer.E, "bf16", p.seed).view(np.int16)).cuda() \
+            .view(torch.bfloat16)
+        rids = torch.empty(T, k, dtype=torch.int32, device="cuda")
+        rw = torch.empty(T, k, dtype=torch.float32, device="cuda")
+        rws = lx.route_workspace(T, layer.d, layer.E)
+        lx.route_topk(xd, wr, k, ids=rids, weights=rw, workspace=rws)  # argument checks once
+        rargs = (xd.data_ptr(), wr.data_ptr(), lx.LX_BF16, T, layer.d, layer.E, k, rids.data_ptr(),
+                 rw.data_ptr(), rws.data_ptr(), rws.numel(), None)
+        rfn = lx.lib().lx_route_topk
+        route = lambda: rfn(*rargs)
+        rms, _ = time_steps(route, a.steps, a.warmup, torch)
+        fwd = [lx.PreparedCall(c, xd, rids, rw, out, ws, kind) for c in copies]
+        chain = rotating([(lambda f=f: (route(), f())) for f in fwd])
+        cms, _ = time_steps(chain, a.steps, a.warmup, torch)
+        routed = dict(router_us=round(rms * 1e3, 3),
+                      router_gflop=round(2 * T * layer.d * layer.E / 1e9, 3),
+                      router_and_forward_ms=round(cms, 4),
+                      router_and_forward_tokens_per_s=round(T / (cms * 1e-3), 1))
+
     cpu = None
     if not a.no_cpu:
         from threadpoolctl import threadpool_info
@@ -371,6 +396,7 @@ def main():
         "layer_roofline": layer_perf,
         "kernels": kernels,
         "dense_comparator": dense,
+        "gpu_router": routed,
         "cpu_baseline": cpu,
     }
     print(json.dumps(res), flush=True)

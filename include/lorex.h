@@ -202,6 +202,32 @@ lx_status lx_dense_moe_forward(const lx_dense_layer* layer, int32_t T, int32_t k
 lx_status lx_quantize_f8(const void* w, int32_t n, int32_t rows, int32_t cols, void* w_f8,
                          uint32_t* scales, void* stream);
 
+/* The model's unchanged top-k router on the GPU (Sec. 3 "Stage 1" and Fig.
+ * overview: compression leaves the router as it is and every expert
+ * addressable), producing the routing inputs of lx_moe_forward /
+ * lx_moe_forward_tree / lx_dense_moe_forward on the same stream, with no
+ * host round trip.
+ *
+ * logits[t][e] = sum_i w_r[e][i] * x[t][i] (fp32 accumulation of the exact
+ * bf16 products); topk_ids[t][0..k) = the k largest logits in descending
+ * order, equal logits ordered by ascending expert index (NaN below every
+ * number); topk_weights[t][j] = exp(l_j - l_0) / sum_i exp(l_i - l_0) over the
+ * chosen logits (the softmax over all E restricted to the chosen experts and
+ * renormalised to sum 1).
+ *
+ * x [T][d] and w_r [E][d] bf16 (dtype must be LX_BF16, else
+ * LX_ERR_UNSUPPORTED), 16-byte aligned; topk_ids [T][k] int32 and
+ * topk_weights [T][k] fp32, 4-byte aligned, caller-owned, fully overwritten;
+ * workspace 256-byte aligned, at least lx_route_workspace_bytes(T, d, E)
+ * bytes (LX_ERR_WORKSPACE_TOO_SMALL), contents irrelevant on entry. d a
+ * positive multiple of 64, E a multiple of 4 in 4 .. 512, T * d < 2^31
+ * (LX_ERR_UNSUPPORTED); 1 <= k <= min(E, LX_MAX_K) (LX_ERR_INVALID_ARGUMENT).
+ * T = 0 is a no-op. Deterministic run to run. Asynchronous on `stream`. */
+size_t lx_route_workspace_bytes(int32_t T, int32_t d, int32_t E);
+lx_status lx_route_topk(const void* x, const void* w_r, lx_dtype dtype, int32_t T, int32_t d, int32_t E,
+                        int32_t k, int32_t* topk_ids, float* topk_weights, void* workspace,
+                        size_t workspace_bytes, void* stream);
+
 /* Routing bucketing alone (the first step of every forward), exposing the
  * arrays of one tree level `level` (0 = anchors, n_levels = experts):
  *   row_token   [T * min(k, N_level)] (only the first node_offsets[N] entries

@@ -887,6 +887,77 @@ lx_status lx_quantize_f8(const void* w, int32_t n, int32_t rows, int32_t cols, v
   return LX_OK;
 }
 
+namespace {
+// Router plan: logits [T][E] fp32, then (split) the partial tiles.
+struct RoutePlan {
+  int items, s, S;  // work items, requested and made splits
+  size_t logits, part, total;
+};
+RoutePlan route_plan(int T, int d, int E) {
+  RoutePlan r{};
+  r.items = (T + kSkinnyBM - 1) / kSkinnyBM * ((E + kSkinnyBN - 1) / kSkinnyBN);
+  const int nkw = d / 64;
+  r.s = std::min(kSplitCap / std::max(r.items, 1), nkw / kSplitMinSlabs);
+  r.S = skinny_splits(nkw, r.s);
+  r.logits = 0;
+  r.part = align_up((size_t)T * E * 4);
+  r.total = r.part + (r.S > 1 ? align_up((size_t)r.items * r.S * kSkinnyBM * kSkinnyBN * 4) : 0);
+  return r;
+}
+
+lx_status check_route(lx_dtype dtype, int32_t T, int32_t d, int32_t E, int32_t k) {
+  if (T < 0 || d < 0 || E < 0) return fail(LX_ERR_INVALID_ARGUMENT, "negative size");
+  if (dtype != LX_BF16) return fail(LX_ERR_UNSUPPORTED, "the router takes bf16 activations and weights");
+  if (d == 0 || d % 64) return fail(LX_ERR_UNSUPPORTED, "d must be a positive multiple of 64");
+  if (E < 1 || E > kRouteMaxE || E % 4) return fail(LX_ERR_UNSUPPORTED, "E must be a multiple of 4 in 4 .. 512");
+  if (k < 1 || k > E || k > LX_MAX_K) return fail(LX_ERR_INVALID_ARGUMENT, "k must be in 1 .. min(E, LX_MAX_K)");
+  if ((int64_t)T * d >= ((int64_t)1 << 31)) return fail(LX_ERR_UNSUPPORTED, "T * d must be below 2^31");
+  return LX_OK;
+}
+}  // namespace
+
+size_t lx_route_workspace_bytes(int32_t T, int32_t d, int32_t E) {
+  if (check_route(LX_BF16, T, d, E, 1) != LX_OK) return 0;
+  return route_plan(T, d, E).total;
+}
+
+lx_status lx_route_topk(const void* x, const void* w_r, lx_dtype dtype, int32_t T, int32_t d, int32_t E,
+                        int32_t k, int32_t* topk_ids, float* topk_weights, void* workspace,
+                        size_t workspace_bytes, void* stream) {
+  g_err.clear();
+  const lx_status st = check_route(dtype, T, d, E, k);
+  if (st != LX_OK) return st;
+  if (T == 0) return LX_OK;
+  if (!x || !w_r || !topk_ids || !topk_weights || !workspace || !aligned(x, 16) || !aligned(w_r, 16) ||
+      !aligned(topk_ids, 4) || !aligned(topk_weights, 4) || !aligned(workspace, 256))
+    return fail(LX_ERR_INVALID_ARGUMENT, "null or misaligned pointer");
+  const RoutePlan P = route_plan(T, d, E);
+  if (workspace_bytes < P.total) return fail(LX_ERR_WORKSPACE_TOO_SMALL, "workspace too small");
+  hipStream_t s = (hipStream_t)stream;
+  uint8_t* const W = (uint8_t*)workspace;
+  // logits = x W_r^T on the skinny kernel over implicit 32-row tiles
+  GemmArgs g{};
+  g.A = x;
+  g.lda = d;
+  g.B[0] = g.B[1] = w_r;
+  g.ncols[0] = E;
+  g.K = d;
+  g.C = (float*)(W + P.logits);
+  g.ldc = E;
+  g.dense_rows = T;
+  if (P.S > 1) {
+    g.part = (float*)(W + P.part);
+    g.split_force = P.s;
+    g.defer = 1;
+  }
+  if (!gemm_big_ok(g, kSkinnyBN, T)) return fail(LX_ERR_UNSUPPORTED, "router shape not supported");
+  hipStream_t lstream = s;
+  LX_LAUNCH("router_logits", launch_gemm_skinny(g, OUT_F32, (T + kSkinnyBM - 1) / kSkinnyBM, lstream));
+  LX_LAUNCH("router_topk", launch_topk((const float*)(W + P.logits), (const float*)(W + P.part), P.S, T, E, k,
+                                       topk_ids, topk_weights, lstream));
+  return LX_OK;
+}
+
 lx_status lx_read_device_status(const void* workspace, void* stream, uint32_t* flags) {
   g_err.clear();
   if (!workspace || !flags) return fail(LX_ERR_INVALID_ARGUMENT, "null argument");

@@ -521,6 +521,11 @@ void k_gemm_big(GemmArgs p, int ntn) {
 }
 
 // ---------------------------------------------------------------- skinny
+// Tiles of a product: the bucketing's tile table, or implicit dense tiles.
+__device__ __forceinline__ int skinny_tiles(const GemmArgs& g) {
+  return g.tiles ? *g.n_tiles : (g.dense_rows + kSkinnyBM - 1) / kSkinnyBM;
+}
+
 // Device-scope coherent 32-bit store and load (relaxed agent-scope atomics):
 // another XCD's workgroup that reads the location after this access has
 // completed sees its value.
@@ -579,16 +584,19 @@ __global__ __launch_bounds__(SK_THR) void k_gemm_skinny(SkinnyBatch b) {
   // Split-K when the launch's work items are few: each product's items get
   // S splits of cw weight slabs (the last possibly shorter, none empty),
   // with S * (items of the whole launch) <= split_cap.
-  const int items = *p.n_tiles * ntn;
+  const int items = skinny_tiles(p) * ntn;
   int S = 1, cw = nkw;
-  if (p.part && items > 0) {
+  if (p.split_force > 1) {
+    S = skinny_splits(nkw, p.split_force);
+    cw = (nkw + p.split_force - 1) / p.split_force;
+  } else if (p.part && items > 0) {
     int all = 0;
-    for (int i = 0; i < b.n; ++i) all += *b.g[i].n_tiles * b.ntn[i];
+    for (int i = 0; i < b.n; ++i) all += skinny_tiles(b.g[i]) * b.ntn[i];
     int s = p.split_cap / all;
     s = s < nkw / kSplitMinSlabs ? s : nkw / kSplitMinSlabs;
     if (s > 1) {
       cw = (nkw + s - 1) / s;
-      S = (nkw + cw - 1) / cw;
+      S = skinny_splits(nkw, s);
     }
   }
   // one work unit (item, split) per workgroup, XCD-contiguous order
@@ -605,7 +613,15 @@ __global__ __launch_bounds__(SK_THR) void k_gemm_skinny(SkinnyBatch b) {
 
   const int tid = threadIdx.x;
   const int wave = tid >> 6, lane = tid & 63;
-  const TileEntry te = p.tiles[ti];
+  TileEntry te;
+  if (p.tiles) {
+    te = p.tiles[ti];
+  } else {
+    te.widx = 0;
+    te.row0 = ti * BM;
+    te.nrows = p.dense_rows - te.row0 < BM ? p.dense_rows - te.row0 : BM;
+    te.node = 0;
+  }
   const int n0 = nt * BN;
   const int ncol = p.ncols[0] + p.ncols[1];
   const int tpart = n0 < p.ncols[0] ? 0 : 1;
@@ -724,6 +740,7 @@ __global__ __launch_bounds__(SK_THR) void k_gemm_skinny(SkinnyBatch b) {
     const int rr = lane >> 5, cc = lane & 31;
     float* const slot = p.part + (int64_t)Lg * (BM * BN) + wave * (32 * 32);
     for (int r = rr; r < nr; r += 2) store_dev(slot + r * 32 + cc, ep[r * PITCH + cc]);
+    if (p.defer) return;  // the consumer adds the slots
     wait_vmcnt<0>();
     __syncthreads();
     if (tid == 0)
@@ -926,7 +943,10 @@ hipError_t launch_gemm_skinny_batch(const GemmArgs* g, const int* ofmt, const in
 int skinny_grid(const GemmArgs& g, int64_t items_max) {
   const int Kb = g.Kb > 0 ? g.Kb : g.K;
   int64_t n = items_max;
-  if (g.part && Kb / BK2 >= 2 * kSplitMinSlabs) n = std::max<int64_t>(n, g.split_cap);
+  if (g.split_force > 1)
+    n = items_max * skinny_splits(Kb / BK2, g.split_force);  // Kb / 64 weight slabs
+  else if (g.part && Kb / BK2 >= 2 * kSplitMinSlabs)
+    n = std::max<int64_t>(n, g.split_cap);
   return (int)((n + NXCD - 1) / NXCD * NXCD);
 }
 

@@ -184,6 +184,16 @@ struct GemmArgs {
   float* part;
   uint32_t* cnt;
   int32_t split_cap;
+  // split_force > 1: split into that many pieces before normalisation (the
+  // caller's count, at most the weight slabs / kSplitMinSlabs; the splits
+  // actually made are skinny_splits(weight slabs, split_force)); with defer
+  // set, every split only writes its partial tile to its slot of part and
+  // the consumer of C adds the slots (no counters).
+  int32_t split_force;
+  int32_t defer;
+  // tiles == null: implicit tiles of kSkinnyBM consecutive rows over
+  // dense_rows rows of A (identity row map, weight index 0)
+  int32_t dense_rows;
 };
 
 enum AMode { A_BF16 = 0, A_F32_HILO = 1 };
@@ -223,6 +233,13 @@ constexpr int kSkinnyBM = 32, kSkinnyBN = 64;
 // compute unit on 256 compute units) and the fewest weight slabs (64 K
 // values) a split covers.
 constexpr int kSplitCap = 768, kSplitMinSlabs = 4;
+// Splits made of nkw weight slabs asked to split s ways: pieces of
+// ceil(nkw / s) slabs, none empty.
+__host__ __device__ inline int skinny_splits(int nkw, int s) {
+  if (s <= 1) return 1;
+  const int cw = (nkw + s - 1) / s;
+  return (nkw + cw - 1) / cw;
+}
 // Workgroups the skinny kernel launches for a product with at most
 // items_max work items (all splits of all items fit when splitting).
 int skinny_grid(const GemmArgs& g, int64_t items_max);
@@ -258,6 +275,15 @@ struct TokenArgs {
   void* out;
   lx_dtype out_dtype;
 };
+
+// ---------------------------------------------------------------- router
+// Top-k over router logits: logits [T][E] fp32 (S == 1), or the S partial
+// tiles per (32-row tile, 64-column tile) item that a deferred split-K
+// skinny GEMM left in part (slot (item * S + split), layout [wavefront][row]
+// [32 columns]). 1 <= k <= min(E, LX_MAX_K), E <= kRouteMaxE.
+constexpr int kRouteMaxE = 512;
+hipError_t launch_topk(const float* logits, const float* part, int S, int T, int E, int k, int32_t* ids,
+                       float* weights, hipStream_t s);
 
 hipError_t launch_swiglu_reduce(const TokenArgs& a, hipStream_t s);
 hipError_t launch_combine(const TokenArgs& a, hipStream_t s);

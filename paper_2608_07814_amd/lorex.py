@@ -76,6 +76,9 @@ EXPORTS = {
                            _c_void, _c_void, _c_void, ctypes.c_size_t, _c_void]),
     "lx_read_device_status": (_c_i32, [_c_void, _c_void, ctypes.POINTER(ctypes.c_uint32)]),
     "lx_quantize_f8": (_c_i32, [_c_void, _c_i32, _c_i32, _c_i32, _c_void, _c_void, _c_void]),
+    "lx_route_workspace_bytes": (ctypes.c_size_t, [_c_i32, _c_i32, _c_i32]),
+    "lx_route_topk": (_c_i32, [_c_void, _c_void, _c_i32, _c_i32, _c_i32, _c_i32, _c_i32, _c_void, _c_void,
+                               _c_void, ctypes.c_size_t, _c_void]),
     "lx_profile_enable": (_c_i32, [_c_i32]),
     "lx_profile_collect": (_c_i32, []),
     "lx_profile_count": (_c_i32, []),
@@ -237,6 +240,37 @@ def quantize_f8(w: torch.Tensor, stream=None):
     sc = torch.empty(n, rows, max(cols // 64, 1), dtype=torch.int32, device=w.device)
     _check(lib().lx_quantize_f8(_ptr(w), n, rows, cols, _ptr(w8), _ptr(sc), _stream(stream)))
     return w8, sc
+
+
+def route_workspace(T: int, d: int, E: int, device="cuda") -> torch.Tensor:
+    n = int(lib().lx_route_workspace_bytes(T, d, E))
+    if n == 0:
+        raise LorexError(f"unsupported router shape T={T} d={d} E={E}")
+    return torch.empty(n, dtype=torch.uint8, device=device)
+
+
+def route_topk(x: torch.Tensor, w_r: torch.Tensor, k: int, ids: Optional[torch.Tensor] = None,
+               weights: Optional[torch.Tensor] = None, workspace: Optional[torch.Tensor] = None, stream=None):
+    """The top-k router on the GPU (lx_route_topk): bf16 x [T][d] and router
+    weights [E][d] -> (int32 ids [T][k], fp32 weights [T][k]), ready for
+    ``forward`` on the same stream."""
+    if x.dtype != torch.bfloat16 or w_r.dtype != torch.bfloat16:
+        raise ValueError("x and w_r must be bf16")
+    if not (x.is_contiguous() and w_r.is_contiguous()) or x.dim() != 2 or w_r.dim() != 2:
+        raise ValueError("x [T][d] and w_r [E][d] must be contiguous 2-d tensors")
+    T, d = (int(v) for v in x.shape)
+    E = int(w_r.shape[0])
+    if int(w_r.shape[1]) != d:
+        raise ValueError("w_r must be [E][d]")
+    if ids is None:
+        ids = torch.empty(T, k, dtype=torch.int32, device=x.device)
+    if weights is None:
+        weights = torch.empty(T, k, dtype=torch.float32, device=x.device)
+    if workspace is None:
+        workspace = route_workspace(T, d, E, x.device)
+    _check(lib().lx_route_topk(_ptr(x), _ptr(w_r), LX_BF16, T, d, E, k, _ptr(ids), _ptr(weights),
+                               _ptr(workspace), workspace.numel(), _stream(stream)))
+    return ids, weights
 
 
 def attach_down_f8(layer: "DeviceLayer") -> "DeviceLayer":

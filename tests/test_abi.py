@@ -28,7 +28,7 @@ def _declared(root):
 
 def test_every_declared_symbol_is_exported(L, root):
     names = _declared(root)
-    assert len(names) == len(lx.EXPORTS) == 17
+    assert len(names) == len(lx.EXPORTS) == 19
     for n in names:
         assert hasattr(L, n), n
         assert n in lx.EXPORTS, n
@@ -137,3 +137,33 @@ def test_profile_entries_empty(L):
     assert L.lx_profile_reset() == lx.LX_OK
     assert L.lx_profile_count() == 0
     assert L.lx_profile_entry(0, None, None, None) == lx.LX_ERR_INVALID_ARGUMENT
+
+
+def test_route_validation(L):
+    r = L.lx_route_topk
+    need = L.lx_route_workspace_bytes(64, 2048, 128)
+    # logits, then the partial tiles of the split logits GEMM: 4 items (two
+    # 32-row tiles x two 64-expert tiles) x 8 splits (32 weight slabs / 4)
+    assert need == 64 * 128 * 4 + 4 * 8 * 32 * 64 * 4
+    # enough items to fill the machine: no split, logits only
+    assert L.lx_route_workspace_bytes(32768, 2048, 128) == 32768 * 128 * 4
+    assert L.lx_route_workspace_bytes(64, 2000, 128) == 0
+    ok = dict(x=FAKE, w=FAKE, dt=lx.LX_BF16, T=64, d=2048, E=128, k=8, ids=FAKE, wt=FAKE, ws=FAKE, n=need)
+
+    def call(**kw):
+        a = dict(ok, **kw)
+        return r(a["x"], a["w"], a["dt"], a["T"], a["d"], a["E"], a["k"], a["ids"], a["wt"], a["ws"], a["n"], None)
+    assert call(dt=lx.LX_F32) == lx.LX_ERR_UNSUPPORTED
+    assert call(d=2000) == lx.LX_ERR_UNSUPPORTED           # d % 64
+    assert call(E=513) == lx.LX_ERR_UNSUPPORTED
+    assert call(E=42) == lx.LX_ERR_UNSUPPORTED             # E % 4
+    assert call(n=need - 1) == lx.LX_ERR_WORKSPACE_TOO_SMALL
+    assert call(ws=None) == lx.LX_ERR_INVALID_ARGUMENT
+    assert call(k=0) == lx.LX_ERR_INVALID_ARGUMENT
+    assert call(k=33) == lx.LX_ERR_INVALID_ARGUMENT
+    assert call(E=4, k=5) == lx.LX_ERR_INVALID_ARGUMENT
+    assert call(T=-1) == lx.LX_ERR_INVALID_ARGUMENT
+    assert call(x=None) == lx.LX_ERR_INVALID_ARGUMENT
+    assert call(w=FAKE + 8) == lx.LX_ERR_INVALID_ARGUMENT
+    assert call(ids=FAKE + 2) == lx.LX_ERR_INVALID_ARGUMENT
+    assert call(T=0, x=None, ids=None, ws=None) == lx.LX_OK  # empty: no launch
