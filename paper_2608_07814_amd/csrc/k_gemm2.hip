@@ -556,35 +556,36 @@ constexpr int SK_THR = 128;
 // products that read the same input rows): problem i owns workgroups
 // [base[i], base[i+1]); every base is a multiple of 8, so the XCD of a
 // workgroup is its index within the problem modulo 8.
-template <int SK_NST, int PER>
-__global__ __launch_bounds__(SK_THR) void k_gemm_skinny(SkinnyBatch b) {
-  constexpr int BM = kSkinnyBM, BN = kSkinnyBN;
-  constexpr int A_ROUNDS = BM * 8 / SK_THR, B_ROUNDS = BN * 8 / SK_THR;
-  constexpr int R = PER * A_ROUNDS + B_ROUNDS;
-  constexpr int SA = BM * BK2, STAGE = (PER * BM + BN) * BK2;
-  __shared__ __attribute__((aligned(1024))) u16 smem[SK_NST * STAGE];
+// One work unit of a skinny launch: problem, (item, split), tile, K range.
+struct SkUnit {
+  const GemmArgs* p;
+  int ntn, ofmt, S, Lg, item, kt0, nkl, Kb, nper, n0, ncol, akoff;
+  TileEntry te;
+};
 
+// Decode this workgroup's unit; false if it has none. spw = K-loop steps per
+// weight slab (nper for the slab-per-step LDS kernel in PER == 1 mode, 1
+// when a step covers every period of a weight slab).
+__device__ __forceinline__ bool sk_unit(const SkinnyBatch& b, bool step_per_weight_slab, SkUnit& u) {
   int pi = 0;
   while (pi + 1 < b.n && (int)blockIdx.x >= b.base[pi + 1]) ++pi;
   const GemmArgs& p = b.g[pi];
-  const int ntn = b.ntn[pi];
-  const int ofmt = b.ofmt[pi];
+  u.p = &p;
+  u.ntn = b.ntn[pi];
+  u.ofmt = b.ofmt[pi];
   const int wg = (int)blockIdx.x - b.base[pi];
-
   const int K = p.K;
-  const int Kb = p.Kb > 0 ? p.Kb : K;
+  u.Kb = p.Kb > 0 ? p.Kb : K;
   const int nk = K / BK2;
   // slab kt: period kt % nper of weight slab kt / nper (as in k_gemm_big)
-  const int nper = K / Kb, nkw = nk / nper;
-  // A step of the K loop: PER == 1, one 64-wide slab of A's K (any nper);
-  // PER == 2 (nper == 2), one weight slab, multiplied by both periods of A
-  // (the weight slab is loaded once for the hi and the lo half)
-  const int spw = PER == 1 ? nper : 1;
+  u.nper = K / u.Kb;
+  const int nkw = nk / u.nper;
+  const int spw = step_per_weight_slab ? 1 : u.nper;
 
   // Split-K when the launch's work items are few: each product's items get
   // S splits of cw weight slabs (the last possibly shorter, none empty),
   // with S * (items of the whole launch) <= split_cap.
-  const int items = skinny_tiles(p) * ntn;
+  const int items = skinny_tiles(p) * u.ntn;
   int S = 1, cw = nkw;
   if (p.split_force > 1) {
     S = skinny_splits(nkw, p.split_force);
@@ -599,33 +600,127 @@ __global__ __launch_bounds__(SK_THR) void k_gemm_skinny(SkinnyBatch b) {
       S = skinny_splits(nkw, s);
     }
   }
+  u.S = S;
   // one work unit (item, split) per workgroup, XCD-contiguous order
   // (workgroups >= units)
   const int real = items * S;
   const int q = real / NXCD, rmd = real % NXCD;
   const int x = wg % NXCD;
   const int Lg = x * q + (x < rmd ? x : rmd) + wg / NXCD;
-  if (Lg >= x * q + (x < rmd ? x : rmd) + q + (x < rmd ? 1 : 0)) return;
-  const int item = Lg / S, sp = Lg - item * S;
-  const int ti = item / ntn, nt = item % ntn;
-  const int kt0 = sp * cw * spw;
-  const int nkl = ((sp + 1) * cw < nkw ? (sp + 1) * cw : nkw) * spw - kt0;
+  if (Lg >= x * q + (x < rmd ? x : rmd) + q + (x < rmd ? 1 : 0)) return false;
+  u.Lg = Lg;
+  u.item = Lg / S;
+  const int sp = Lg - u.item * S;
+  const int ti = u.item / u.ntn, nt = u.item % u.ntn;
+  u.kt0 = sp * cw * spw;
+  u.nkl = ((sp + 1) * cw < nkw ? (sp + 1) * cw : nkw) * spw - u.kt0;
+  if (p.tiles) {
+    u.te = p.tiles[ti];
+  } else {
+    u.te.widx = 0;
+    u.te.row0 = ti * kSkinnyBM;
+    u.te.nrows = p.dense_rows - u.te.row0 < kSkinnyBM ? p.dense_rows - u.te.row0 : kSkinnyBM;
+    u.te.node = 0;
+  }
+  u.n0 = nt * kSkinnyBN;
+  u.ncol = p.ncols[0] + p.ncols[1];
+  u.akoff = p.a_koff[u.n0 < p.ncols[0] ? 0 : 1];
+  return true;
+}
+
+// Epilogue of a unit: 32 x 32 block per wavefront through its LDS region ep
+// (pitch 36 floats), then 4 consecutive columns per lane; with a split, the
+// partial-tile hand-off first. Every wavefront of the workgroup calls it.
+__device__ __forceinline__ void sk_epilogue(const SkUnit& u, const f32x16& acc, float* ep) {
+  constexpr int BM = kSkinnyBM, BN = kSkinnyBN, PITCH = 36, LPR = 8, RPP = 8;
+  const GemmArgs& p = *u.p;
+  const int tid = threadIdx.x, wave = tid >> 6, lane = tid & 63;
+  const TileEntry& te = u.te;
+#pragma unroll
+  for (int i = 0; i < 16; ++i) ep[(8 * (i >> 2) + 4 * (lane >> 5) + (i & 3)) * PITCH + (lane & 31)] = acc[i];
+  const int c4 = (lane % LPR) * 4;
+  const int col = u.n0 + wave * 32 + c4;
+  if (u.S > 1) {
+    // Partial tile -> slot Lg; the last workgroup of the item to arrive adds
+    // the item's S slots in split order (same sum whatever the arrival
+    // order). The slots and the counter are only accessed with device-scope
+    // coherent operations (they bypass the per-XCD L2 copies), so completing
+    // the slot stores before the counter increment is all the ordering the
+    // hand-off needs; no cache-wide write-back or invalidation is involved.
+    // Slot layout [wavefront][row][32 columns]: each 4-byte access
+    // instruction covers two rows, 256 contiguous bytes.
+    __shared__ int s_last;
+    const int nr = te.nrows;
+    const int rr = lane >> 5, cc = lane & 31;
+    float* const slot = p.part + (int64_t)u.Lg * (BM * BN) + wave * (32 * 32);
+    for (int r = rr; r < nr; r += 2) store_dev(slot + r * 32 + cc, ep[r * PITCH + cc]);
+    if (p.defer) return;  // the consumer adds the slots
+    wait_vmcnt<0>();
+    __syncthreads();
+    if (tid == 0)
+      s_last = __hip_atomic_fetch_add(p.cnt + u.item, 1u, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT) ==
+               (unsigned)(u.S - 1);
+    __syncthreads();
+    if (!s_last) return;
+    if (tid == 0)  // ready for the next product of this level
+      __hip_atomic_store(p.cnt + u.item, 0u, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+    const float* const first = p.part + (int64_t)u.item * u.S * (BM * BN) + wave * (32 * 32);
+    for (int r = rr; r < nr; r += 2) {
+      float v = load_dev(first + r * 32 + cc);
+      for (int t = 1; t < u.S; ++t) v += load_dev(first + (int64_t)t * (BM * BN) + r * 32 + cc);
+      ep[r * PITCH + cc] = v;
+    }
+  }
+#pragma unroll
+  for (int ps = 0; ps < 32 / RPP; ++ps) {
+    const int r = ps * RPP + lane / LPR;
+    const float4 v = *(const float4*)&ep[r * PITCH + c4];
+    if (r >= te.nrows || col >= u.ncol) continue;
+    if (u.ofmt == OUT_HILO) {
+      const int pp = col < p.ncols[0] ? 0 : 1;
+      const int c = pp ? col - p.ncols[0] : col;
+      const int hi_col = (pp ? 2 * p.ncols[0] : 0) + c;
+      const int lo_col = hi_col + p.ncols[pp];
+      bf16x4 h, l;
+      h[0] = (__bf16)v.x;
+      h[1] = (__bf16)v.y;
+      h[2] = (__bf16)v.z;
+      h[3] = (__bf16)v.w;
+      l[0] = (__bf16)(v.x - (float)h[0]);
+      l[1] = (__bf16)(v.y - (float)h[1]);
+      l[2] = (__bf16)(v.z - (float)h[2]);
+      l[3] = (__bf16)(v.w - (float)h[3]);
+      __bf16* const rowp = (__bf16*)p.C + (int64_t)(te.row0 + r) * p.ldc;
+      *(bf16x4*)(rowp + hi_col) = h;
+      *(bf16x4*)(rowp + lo_col) = l;
+    } else if (u.ofmt == OUT_F24) {
+      *(F24x4*)((uint8_t*)p.C + ((int64_t)(te.row0 + r) * p.ldc + col) * 3) = f24_pack(v);
+    } else {
+      *(float4*)(p.C + (int64_t)(te.row0 + r) * p.ldc + col) = v;
+    }
+  }
+}
+
+template <int SK_NST, int PER>
+__global__ __launch_bounds__(SK_THR) void k_gemm_skinny(SkinnyBatch b) {
+  constexpr int BM = kSkinnyBM, BN = kSkinnyBN;
+  constexpr int A_ROUNDS = BM * 8 / SK_THR, B_ROUNDS = BN * 8 / SK_THR;
+  constexpr int R = PER * A_ROUNDS + B_ROUNDS;
+  constexpr int SA = BM * BK2, STAGE = (PER * BM + BN) * BK2;
+  __shared__ __attribute__((aligned(1024))) u16 smem[SK_NST * STAGE];
+
+  // A step of the K loop: PER == 1, one 64-wide slab of A's K (any nper);
+  // PER == 2 (nper == 2), one weight slab, multiplied by both periods of A
+  // (the weight slab is loaded once for the hi and the lo half)
+  SkUnit u;
+  if (!sk_unit(b, PER == 2, u)) return;
+  const GemmArgs& p = *u.p;
+  const int Kb = u.Kb, nper = u.nper, kt0 = u.kt0, nkl = u.nkl;
+  const TileEntry& te = u.te;
 
   const int tid = threadIdx.x;
   const int wave = tid >> 6, lane = tid & 63;
-  TileEntry te;
-  if (p.tiles) {
-    te = p.tiles[ti];
-  } else {
-    te.widx = 0;
-    te.row0 = ti * BM;
-    te.nrows = p.dense_rows - te.row0 < BM ? p.dense_rows - te.row0 : BM;
-    te.node = 0;
-  }
-  const int n0 = nt * BN;
-  const int ncol = p.ncols[0] + p.ncols[1];
-  const int tpart = n0 < p.ncols[0] ? 0 : 1;
-  const int akoff = p.a_koff[tpart];
+  const int ncol = u.ncol;
   const u16* __restrict__ Ab = (const u16*)p.A;
   const u16* __restrict__ Bw0 = (const u16*)p.B[0] + (int64_t)te.widx * p.b_stride[0];
   const u16* __restrict__ Bw1 = (const u16*)p.B[1] + (int64_t)te.widx * p.b_stride[1];
@@ -640,7 +735,7 @@ __global__ __launch_bounds__(SK_THR) void k_gemm_skinny(SkinnyBatch b) {
     const int c = (Ps & 7) ^ swz2(row);
     const int r = row < te.nrows ? row : te.nrows - 1;
     const int src = p.a_rows ? p.a_rows[te.row0 + r] : te.row0 + r;
-    aoff[j] = (uint32_t)src * (uint32_t)p.lda + (uint32_t)(akoff + c * 8);
+    aoff[j] = (uint32_t)src * (uint32_t)p.lda + (uint32_t)(u.akoff + c * 8);
   }
   const u16* bptr[B_ROUNDS];
 #pragma unroll
@@ -648,7 +743,7 @@ __global__ __launch_bounds__(SK_THR) void k_gemm_skinny(SkinnyBatch b) {
     const int Ps = j * SK_THR + tid;
     const int row = Ps >> 3;
     const int c = (Ps & 7) ^ swz2(row);
-    const int n = n0 + row < ncol ? n0 + row : ncol - 1;
+    const int n = u.n0 + row < ncol ? u.n0 + row : ncol - 1;
     bptr[j] = (n < p.ncols[0] ? Bw0 + (int64_t)n * Kb : Bw1 + (int64_t)(n - p.ncols[0]) * Kb) + c * 8;
   }
   // stage = [A period 0 | (A period 1) | B], one 64-wide K slab each
@@ -717,75 +812,9 @@ __global__ __launch_bounds__(SK_THR) void k_gemm_skinny(SkinnyBatch b) {
   }
   wait_lgkm0();
   bar();  // every wavefront is done with the stages: the epilogue reuses them
-
-  // Epilogue: 32 x 32 block per wavefront through LDS (pitch 36 floats), then
-  // 4 consecutive columns per lane.
-  constexpr int PITCH = 36, LPR = 8, RPP = 8;
-  float* const ep = (float*)smem + wave * (32 * PITCH);
-#pragma unroll
-  for (int i = 0; i < 16; ++i) ep[(8 * (i >> 2) + 4 * (lane >> 5) + (i & 3)) * PITCH + (lane & 31)] = acc[i];
-  const int c4 = (lane % LPR) * 4;
-  const int col = n0 + wave * 32 + c4;
-  if (S > 1) {
-    // Partial tile -> slot Lg; the last workgroup of the item to arrive adds
-    // the item's S slots in split order (same sum whatever the arrival
-    // order). The slots and the counter are only accessed with device-scope
-    // coherent operations (they bypass the per-XCD L2 copies), so completing
-    // the slot stores before the counter increment is all the ordering the
-    // hand-off needs; no cache-wide write-back or invalidation is involved.
-    // Slot layout [wavefront][row][32 columns]: each 4-byte access
-    // instruction covers two rows, 256 contiguous bytes.
-    __shared__ int s_last;
-    const int nr = te.nrows;
-    const int rr = lane >> 5, cc = lane & 31;
-    float* const slot = p.part + (int64_t)Lg * (BM * BN) + wave * (32 * 32);
-    for (int r = rr; r < nr; r += 2) store_dev(slot + r * 32 + cc, ep[r * PITCH + cc]);
-    if (p.defer) return;  // the consumer adds the slots
-    wait_vmcnt<0>();
-    __syncthreads();
-    if (tid == 0)
-      s_last = __hip_atomic_fetch_add(p.cnt + item, 1u, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT) ==
-               (unsigned)(S - 1);
-    __syncthreads();
-    if (!s_last) return;
-    if (tid == 0)  // ready for the next product of this level
-      __hip_atomic_store(p.cnt + item, 0u, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
-    const float* const first = p.part + (int64_t)item * S * (BM * BN) + wave * (32 * 32);
-    for (int r = rr; r < nr; r += 2) {
-      float v = load_dev(first + r * 32 + cc);
-      for (int t = 1; t < S; ++t) v += load_dev(first + (int64_t)t * (BM * BN) + r * 32 + cc);
-      ep[r * PITCH + cc] = v;
-    }
-  }
-#pragma unroll
-  for (int ps = 0; ps < 32 / RPP; ++ps) {
-    const int r = ps * RPP + lane / LPR;
-    const float4 v = *(const float4*)&ep[r * PITCH + c4];
-    if (r >= te.nrows || col >= ncol) continue;
-    if (ofmt == OUT_HILO) {
-      const int pp = col < p.ncols[0] ? 0 : 1;
-      const int c = pp ? col - p.ncols[0] : col;
-      const int hi_col = (pp ? 2 * p.ncols[0] : 0) + c;
-      const int lo_col = hi_col + p.ncols[pp];
-      bf16x4 h, l;
-      h[0] = (__bf16)v.x;
-      h[1] = (__bf16)v.y;
-      h[2] = (__bf16)v.z;
-      h[3] = (__bf16)v.w;
-      l[0] = (__bf16)(v.x - (float)h[0]);
-      l[1] = (__bf16)(v.y - (float)h[1]);
-      l[2] = (__bf16)(v.z - (float)h[2]);
-      l[3] = (__bf16)(v.w - (float)h[3]);
-      __bf16* const rowp = (__bf16*)p.C + (int64_t)(te.row0 + r) * p.ldc;
-      *(bf16x4*)(rowp + hi_col) = h;
-      *(bf16x4*)(rowp + lo_col) = l;
-    } else if (ofmt == OUT_F24) {
-      *(F24x4*)((uint8_t*)p.C + ((int64_t)(te.row0 + r) * p.ldc + col) * 3) = f24_pack(v);
-    } else {
-      *(float4*)(p.C + (int64_t)(te.row0 + r) * p.ldc + col) = v;
-    }
-  }
+  sk_epilogue(u, acc, (float*)smem + wave * (32 * 36));
 }
+
 
 template <int BM, int BN>
 hipError_t launch_bn(const GemmArgs& g, int ofmt, int grid, int ntn, hipStream_t s) {
