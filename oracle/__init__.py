@@ -16,9 +16,12 @@ Contents:
                                   definition (sort + unique), bit-exact target;
 * ``bucket.bucket_bruteforce``   the same arrays from explicit loops;
 * ``router.route_topk``          the unchanged top-k router (logits, top-k in
-                                  descending order, renormalised softmax), fp64.
+                                  descending order, renormalised softmax), fp64;
+* ``cluster``                     firing / co-activation counts, the NPMI
+                                  distance and frequency-seeded k-medoids with
+                                  the dominant choice (Stages 1-2), fp64.
 
 Every function is pinned by ``tests/test_oracle_*.py`` against brute force,
 closed forms, library routines and invariants of the method.
 """
-from . import bucket, moe, router  # noqa: F401
+from . import bucket, cluster, moe, router  # noqa: F401
