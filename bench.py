@@ -54,6 +54,9 @@ def parse():
                     help="no fp8 copy of the anchor down weights: the anchor down projection multiplies "
                          "both halves of its bf16 (hi, lo) input in bf16")
     ap.add_argument("--no-route", action="store_true", help="skip timing the GPU top-k router")
+    ap.add_argument("--cluster", action="store_true",
+                    help="also time router profiling + NPMI distance + k-medoids (Stages 1-2) on a calibration "
+                         "routing of 64 x 2048 tokens, against the oracle on the host")
     ap.add_argument("--copy-calibration", action="store_true",
                     help="only run a plain 1 GiB device-to-device copy 5 times (scales the "
                          "FETCH_SIZE / WRITE_SIZE counters to bytes)")
@@ -184,6 +187,45 @@ def time_steps(fn, steps, warmup, torch):
     torch.cuda.synchronize()
     wall = time.perf_counter() - w0
     return e0.elapsed_time(e1) / steps, wall
+
+
+def bench_clustering(torch, np, lx, a):
+    """Stages 1-2 on the GPU: firing / co-activation counts and the NPMI
+    distance over a calibration routing (64 sequences x 2048 tokens, 128
+    experts, top-8, community-structured: 16 groups of 8, 70% of slots in the
+    token's home group), then k-medoids to 64 clusters (k = E / 2). Timed with
+    events around the two calls; the oracle runs the same steps on the host."""
+    from lxsynth import route_community
+    from oracle import cluster as K
+    E, k, N, C = 128, 8, 64 * 2048, 64
+    members = [list(range(g * 8, g * 8 + 8)) for g in range(16)]
+    ids = route_community(N, members, k, 0.7, 5).topk_ids
+    ids_d = torch.from_numpy(np.ascontiguousarray(ids, np.int32)).cuda()
+    fire, pair, dist = lx.coact_distance(ids_d, E)
+    lx.kmedoids(dist, fire, C)
+    torch.cuda.synchronize()
+    reps = 20
+    e0, e1, e2 = (torch.cuda.Event(enable_timing=True) for _ in range(3))
+    e0.record()
+    for _ in range(reps):
+        lx.coact_distance(ids_d, E)
+    e1.record()
+    outs = None
+    for _ in range(reps):
+        outs = lx.kmedoids(dist, fire, C)
+    e2.record()
+    torch.cuda.synchronize()
+    it = int(outs[3].cpu()[0])
+    t0 = time.perf_counter()
+    f0, p0 = K.coact_counts(ids, E)
+    d0 = K.npmi_distance(f0, p0, N)
+    K.kmedoids(d0, f0, C)
+    cpu_s = time.perf_counter() - t0
+    same = bool(np.array_equal(outs[0].cpu().numpy(), K.kmedoids(dist.cpu().numpy(),
+                                                                 fire.cpu().numpy().view(np.uint32), C)[0]))
+    return dict(tokens=N, E=E, k=k, C=C, coact_distance_us=round(e0.elapsed_time(e1) / reps * 1e3, 2),
+                kmedoids_us=round(e1.elapsed_time(e2) / reps * 1e3, 2), kmedoids_update_rounds=it,
+                ids_bytes=N * k * 4, cpu_oracle_s=round(cpu_s, 2), clusters_match_oracle=same)
 
 
 def main():
@@ -353,6 +395,10 @@ def main():
                       router_and_forward_ms=round(cms, 4),
                       router_and_forward_tokens_per_s=round(T / (cms * 1e-3), 1))
 
+    clustering = None
+    if a.cluster:
+        clustering = bench_clustering(torch, np, lx, a)
+
     cpu = None
     if not a.no_cpu:
         from threadpoolctl import threadpool_info
@@ -397,6 +443,7 @@ def main():
         "kernels": kernels,
         "dense_comparator": dense,
         "gpu_router": routed,
+        "clustering": clustering,
         "cpu_baseline": cpu,
     }
     print(json.dumps(res), flush=True)

@@ -228,6 +228,48 @@ lx_status lx_route_topk(const void* x, const void* w_r, lx_dtype dtype, int32_t 
                         int32_t k, int32_t* topk_ids, float* topk_weights, void* workspace,
                         size_t workspace_bytes, void* stream);
 
+/* Router profiling and the Coact-NPMI clustering distance (Sec. 3,
+ * "Compression pipeline", Stage 1, and "Variants"), from the routing ids of N
+ * calibration tokens (topk_ids [N][k] int32, device; ids outside [0, E) and
+ * repeated ids within a row are ignored).
+ *
+ * fire [E] uint32: tokens on which expert e fires; pair [E][E] uint32
+ * (symmetric, zero diagonal): tokens on which both fire; dist [E][E] fp64:
+ * D = 1 - NPMI with p_i = fire[i] / N, p_ij = pair[i][j] / N, NPMI = log(p_ij /
+ * (p_i p_j)) / (-log p_ij), NPMI = -1 for pairs that never co-fire and 1 for
+ * pairs that co-fire on every token, zero diagonal. All outputs caller-owned
+ * device memory (4-, 4- and 8-byte aligned), fully overwritten. E in 1 ..
+ * 1024 (LX_ERR_UNSUPPORTED), 1 <= k <= LX_MAX_K and N >= 0
+ * (LX_ERR_INVALID_ARGUMENT). Exact integer counts; asynchronous on `stream`. */
+lx_status lx_coact_distance(const int32_t* topk_ids, int32_t N, int32_t k, int32_t E, uint32_t* fire,
+                            uint32_t* pair, double* dist, void* stream);
+
+/* Frequency-seeded k-medoids and the dominant choice (Sec. 3, Stage 2):
+ * clusters C experts' worth of medoids over the distance dist [E][E] fp64
+ * (device; any symmetric matrix with zero diagonal, e.g. lx_coact_distance's)
+ * and firing counts fire [E] uint32 (device).
+ *
+ * The experts listed in protected_ids (HOST array, n_protected distinct ids)
+ * become singleton clusters C - n_protected .. C - 1 in ascending id order.
+ * The others: seeds = the C - n_protected highest-firing ones (ties: lower
+ * id), cluster c seeded by the c-th; then assign (nearest medoid, ties to the
+ * lower cluster; a medoid stays in its own cluster) and update (the member
+ * with the smallest sum of distances to its cluster, summed in ascending
+ * member order; ties: lower id) until no medoid changes, at most max_iter
+ * updates. Dominant of a cluster: highest firing count, then the largest sum
+ * of (1 - dist) to the other members, then the lower id.
+ *
+ * Outputs (device, caller-owned): cluster_of [E] and factor_of [E] int32 in
+ * the layout lx_flat_layer takes (factor_of = -1 for a dominant, 0, 1, ...
+ * for the other experts in ascending id order), dominant [C] int32,
+ * iterations [1] int32 (update rounds run). E in 1 .. 1024
+ * (LX_ERR_UNSUPPORTED); 1 <= C - n_protected <= E - n_protected, ids in range
+ * and distinct, max_iter >= 0 (LX_ERR_INVALID_ARGUMENT). Decisions are exact
+ * fp64 comparisons: deterministic. Asynchronous on `stream`. */
+lx_status lx_kmedoids(const double* dist, const uint32_t* fire, int32_t E, int32_t C, const int32_t* protected_ids,
+                      int32_t n_protected, int32_t max_iter, int32_t* cluster_of, int32_t* factor_of,
+                      int32_t* dominant, int32_t* iterations, void* stream);
+
 /* Routing bucketing alone (the first step of every forward), exposing the
  * arrays of one tree level `level` (0 = anchors, n_levels = experts):
  *   row_token   [T * min(k, N_level)] (only the first node_offsets[N] entries

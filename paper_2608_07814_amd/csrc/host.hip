@@ -958,6 +958,45 @@ lx_status lx_route_topk(const void* x, const void* w_r, lx_dtype dtype, int32_t 
   return LX_OK;
 }
 
+lx_status lx_coact_distance(const int32_t* topk_ids, int32_t N, int32_t k, int32_t E, uint32_t* fire,
+                            uint32_t* pair, double* dist, void* stream) {
+  g_err.clear();
+  if (N < 0 || k < 1 || k > LX_MAX_K) return fail(LX_ERR_INVALID_ARGUMENT, "need N >= 0 and 1 <= k <= LX_MAX_K");
+  if (E < 1 || E > kClusterMaxE) return fail(LX_ERR_UNSUPPORTED, "E must be in 1 .. 1024");
+  if ((N > 0 && (!topk_ids || !aligned(topk_ids, 4))) || !fire || !pair || !dist || !aligned(fire, 4) ||
+      !aligned(pair, 4) || !aligned(dist, 8))
+    return fail(LX_ERR_INVALID_ARGUMENT, "null or misaligned pointer");
+  hipStream_t lstream = (hipStream_t)stream;
+  LX_LAUNCH("coact_distance", launch_coact(topk_ids, N, k, E, fire, pair, dist, lstream));
+  return LX_OK;
+}
+
+lx_status lx_kmedoids(const double* dist, const uint32_t* fire, int32_t E, int32_t C, const int32_t* protected_ids,
+                      int32_t n_protected, int32_t max_iter, int32_t* cluster_of, int32_t* factor_of,
+                      int32_t* dominant, int32_t* iterations, void* stream) {
+  g_err.clear();
+  if (E < 1 || E > kClusterMaxE) return fail(LX_ERR_UNSUPPORTED, "E must be in 1 .. 1024");
+  if (n_protected < 0 || n_protected > E || (n_protected > 0 && !protected_ids) || max_iter < 0)
+    return fail(LX_ERR_INVALID_ARGUMENT, "bad protection list or max_iter");
+  if (C - n_protected < 1 || C - n_protected > E - n_protected)
+    return fail(LX_ERR_INVALID_ARGUMENT, "need 1 <= C - n_protected <= E - n_protected");
+  ProtMask pm{};
+  for (int i = 0; i < n_protected; ++i) {
+    const int p = protected_ids[i];
+    if (p < 0 || p >= E) return fail(LX_ERR_INVALID_ARGUMENT, "protected expert id out of range");
+    if ((pm.bits[p >> 5] >> (p & 31)) & 1u) return fail(LX_ERR_INVALID_ARGUMENT, "repeated protected expert id");
+    pm.bits[p >> 5] |= 1u << (p & 31);
+  }
+  if (!dist || !fire || !cluster_of || !factor_of || !dominant || !iterations || !aligned(dist, 8) ||
+      !aligned(fire, 4) || !aligned(cluster_of, 4) || !aligned(factor_of, 4) || !aligned(dominant, 4) ||
+      !aligned(iterations, 4))
+    return fail(LX_ERR_INVALID_ARGUMENT, "null or misaligned pointer");
+  hipStream_t lstream = (hipStream_t)stream;
+  LX_LAUNCH("kmedoids", launch_kmedoids(dist, fire, E, C, pm, n_protected, max_iter, cluster_of, factor_of, dominant,
+                                        iterations, lstream));
+  return LX_OK;
+}
+
 lx_status lx_read_device_status(const void* workspace, void* stream, uint32_t* flags) {
   g_err.clear();
   if (!workspace || !flags) return fail(LX_ERR_INVALID_ARGUMENT, "null argument");

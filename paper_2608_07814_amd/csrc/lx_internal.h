@@ -285,6 +285,20 @@ constexpr int kRouteMaxE = 512;
 hipError_t launch_topk(const float* logits, const float* part, int S, int T, int E, int k, int32_t* ids,
                        float* weights, hipStream_t s);
 
+// ---------------------------------------------------------------- clustering
+// Router profiling counts and the NPMI distance (fire [E], pair [E][E]
+// symmetric, dist [E][E] fp64), and frequency-seeded k-medoids (E <=
+// kClusterMaxE, protected experts as a bit mask).
+constexpr int kClusterMaxE = 1024;
+struct ProtMask {
+  uint32_t bits[kClusterMaxE / 32];
+};
+hipError_t launch_coact(const int32_t* ids, int N, int k, int E, uint32_t* fire, uint32_t* pair, double* dist,
+                        hipStream_t s);
+hipError_t launch_kmedoids(const double* dist, const uint32_t* fire, int E, int C, const ProtMask& pm, int P,
+                           int max_iter, int32_t* cluster_of, int32_t* factor_of, int32_t* dominant,
+                           int32_t* iterations, hipStream_t s);
+
 hipError_t launch_swiglu_reduce(const TokenArgs& a, hipStream_t s);
 hipError_t launch_combine(const TokenArgs& a, hipStream_t s);
 

@@ -77,6 +77,9 @@ EXPORTS = {
     "lx_read_device_status": (_c_i32, [_c_void, _c_void, ctypes.POINTER(ctypes.c_uint32)]),
     "lx_quantize_f8": (_c_i32, [_c_void, _c_i32, _c_i32, _c_i32, _c_void, _c_void, _c_void]),
     "lx_route_workspace_bytes": (ctypes.c_size_t, [_c_i32, _c_i32, _c_i32]),
+    "lx_coact_distance": (_c_i32, [_c_void, _c_i32, _c_i32, _c_i32, _c_void, _c_void, _c_void, _c_void]),
+    "lx_kmedoids": (_c_i32, [_c_void, _c_void, _c_i32, _c_i32, ctypes.POINTER(ctypes.c_int32), _c_i32, _c_i32,
+                             _c_void, _c_void, _c_void, _c_void, _c_void]),
     "lx_route_topk": (_c_i32, [_c_void, _c_void, _c_i32, _c_i32, _c_i32, _c_i32, _c_i32, _c_void, _c_void,
                                _c_void, ctypes.c_size_t, _c_void]),
     "lx_profile_enable": (_c_i32, [_c_i32]),
@@ -271,6 +274,38 @@ def route_topk(x: torch.Tensor, w_r: torch.Tensor, k: int, ids: Optional[torch.T
     _check(lib().lx_route_topk(_ptr(x), _ptr(w_r), LX_BF16, T, d, E, k, _ptr(ids), _ptr(weights),
                                _ptr(workspace), workspace.numel(), _stream(stream)))
     return ids, weights
+
+
+def coact_distance(topk_ids: torch.Tensor, E: int, stream=None):
+    """Router profiling counts and the Coact-NPMI distance (lx_coact_distance):
+    int32 ids [N][k] on the device -> (fire uint32-as-int32 [E], pair [E][E],
+    dist fp64 [E][E])."""
+    if topk_ids.dtype != torch.int32 or topk_ids.dim() != 2 or not topk_ids.is_contiguous():
+        raise ValueError("topk_ids must be a contiguous int32 [N][k] tensor")
+    N, k = (int(v) for v in topk_ids.shape)
+    dev = topk_ids.device
+    fire = torch.empty(E, dtype=torch.int32, device=dev)
+    pair = torch.empty(E, E, dtype=torch.int32, device=dev)
+    dist = torch.empty(E, E, dtype=torch.float64, device=dev)
+    _check(lib().lx_coact_distance(_ptr(topk_ids), N, k, E, _ptr(fire), _ptr(pair), _ptr(dist), _stream(stream)))
+    return fire, pair, dist
+
+
+def kmedoids(dist: torch.Tensor, fire: torch.Tensor, C: int, protected=(), max_iter: int = 100, stream=None):
+    """Frequency-seeded k-medoids and dominants (lx_kmedoids) -> (cluster_of,
+    factor_of, dominant, iterations) int32 device tensors."""
+    if dist.dtype != torch.float64 or not dist.is_contiguous() or dist.dim() != 2:
+        raise ValueError("dist must be a contiguous fp64 [E][E] tensor")
+    E = int(dist.shape[0])
+    dev = dist.device
+    cl = torch.empty(E, dtype=torch.int32, device=dev)
+    fo = torch.empty(E, dtype=torch.int32, device=dev)
+    dom = torch.empty(max(C, 1), dtype=torch.int32, device=dev)
+    it = torch.empty(1, dtype=torch.int32, device=dev)
+    prot = (ctypes.c_int32 * max(len(protected), 1))(*[int(p) for p in protected])
+    _check(lib().lx_kmedoids(_ptr(dist), _ptr(fire), E, C, prot, len(protected), max_iter, _ptr(cl), _ptr(fo),
+                             _ptr(dom), _ptr(it), _stream(stream)))
+    return cl, fo, dom, it
 
 
 def attach_down_f8(layer: "DeviceLayer") -> "DeviceLayer":

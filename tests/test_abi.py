@@ -28,7 +28,7 @@ def _declared(root):
 
 def test_every_declared_symbol_is_exported(L, root):
     names = _declared(root)
-    assert len(names) == len(lx.EXPORTS) == 19
+    assert len(names) == len(lx.EXPORTS) == 21
     for n in names:
         assert hasattr(L, n), n
         assert n in lx.EXPORTS, n
@@ -167,3 +167,26 @@ def test_route_validation(L):
     assert call(w=FAKE + 8) == lx.LX_ERR_INVALID_ARGUMENT
     assert call(ids=FAKE + 2) == lx.LX_ERR_INVALID_ARGUMENT
     assert call(T=0, x=None, ids=None, ws=None) == lx.LX_OK  # empty: no launch
+
+
+def test_cluster_validation(L):
+    import ctypes as C
+    co = L.lx_coact_distance
+    assert co(FAKE, 10, 0, 8, FAKE, FAKE, FAKE, None) == lx.LX_ERR_INVALID_ARGUMENT   # k
+    assert co(FAKE, 10, 2, 1025, FAKE, FAKE, FAKE, None) == lx.LX_ERR_UNSUPPORTED      # E
+    assert co(FAKE, -1, 2, 8, FAKE, FAKE, FAKE, None) == lx.LX_ERR_INVALID_ARGUMENT
+    assert co(FAKE, 10, 2, 8, FAKE, FAKE, FAKE + 4, None) == lx.LX_ERR_INVALID_ARGUMENT  # dist 8-aligned
+    km = L.lx_kmedoids
+    none = (C.c_int32 * 1)(0)
+
+    def call(E=8, Cn=3, prot=(), it=10):
+        arr = (C.c_int32 * max(len(prot), 1))(*prot)
+        return km(FAKE, FAKE, E, Cn, arr, len(prot), it, FAKE, FAKE, FAKE, FAKE, None)
+    assert call(E=0) == lx.LX_ERR_UNSUPPORTED
+    assert call(Cn=0) == lx.LX_ERR_INVALID_ARGUMENT
+    assert call(Cn=9) == lx.LX_ERR_INVALID_ARGUMENT
+    assert call(Cn=2, prot=(1, 2)) == lx.LX_ERR_INVALID_ARGUMENT          # no seeded cluster left
+    assert call(prot=(1, 1)) == lx.LX_ERR_INVALID_ARGUMENT                # repeated
+    assert call(prot=(8,)) == lx.LX_ERR_INVALID_ARGUMENT                  # out of range
+    assert call(it=-1) == lx.LX_ERR_INVALID_ARGUMENT
+    assert km(FAKE, FAKE, 8, 3, none, 0, 10, None, FAKE, FAKE, FAKE, None) == lx.LX_ERR_INVALID_ARGUMENT
