@@ -19,9 +19,12 @@ Contents:
                                   descending order, renormalised softmax), fp64;
 * ``cluster``                     firing / co-activation counts, the NPMI
                                   distance and frequency-seeded k-medoids with
-                                  the dominant choice (Stages 1-2), fp64.
+                                  the dominant choice (Stages 1-2), fp64;
+* ``stage3``                      neuron-alignment cost, exact assignment,
+                                  aligned residual and randomized truncated
+                                  SVD with the symmetric split (Stage 3), fp64.
 
 Every function is pinned by ``tests/test_oracle_*.py`` against brute force,
 closed forms, library routines and invariants of the method.
 """
-from . import bucket, cluster, moe, router  # noqa: F401
+from . import bucket, cluster, moe, router, stage3  # noqa: F401
