@@ -270,6 +270,52 @@ lx_status lx_kmedoids(const double* dist, const uint32_t* fire, int32_t E, int32
                       int32_t n_protected, int32_t max_iter, int32_t* cluster_of, int32_t* factor_of,
                       int32_t* dominant, int32_t* iterations, void* stream);
 
+/* Stage 3, neuron alignment (Sec. 3, "Alignment and low-rank decomposition"
+ * (i), eqs. cost and assign). Neuron i of an expert is the concatenation of
+ * gate row i, up row i and down column i (3d values); the cost of matching
+ * the dominant's neuron i with the member's neuron j is
+ * cost[i][j] = ||a_i||^2 + ||b_j||^2 - 2 a_i . b_j, computed in fp64 from the
+ * stored weights (gate, up [f][d], down [d][f], LX_BF16 or LX_F32, device,
+ * element-aligned). cost [f][f] fp64 device (8-byte aligned); workspace
+ * 256-byte aligned, lx_align_workspace_bytes(f, d) bytes
+ * (LX_ERR_WORKSPACE_TOO_SMALL). f * 3d < 2^31 (LX_ERR_UNSUPPORTED).
+ * Asynchronous on `stream`. */
+size_t lx_align_workspace_bytes(int32_t f, int32_t d);
+lx_status lx_align_cost(const void* dom_gate, const void* dom_up, const void* dom_down, const void* mem_gate,
+                        const void* mem_up, const void* mem_down, lx_dtype dtype, int32_t f, int32_t d, double* cost,
+                        void* workspace, size_t workspace_bytes, void* stream);
+
+/* The exact minimum-cost perfect matching of an n x n cost matrix (eq.
+ * assign), on the HOST: cost [n][n] fp64 host memory; perm [n] int32 host
+ * memory receives, for each row i, the column matched to it; total (may be
+ * NULL) its summed cost. Shortest augmenting paths with dual potentials (the
+ * augmentation phase of Jonker-Volgenant), O(n^3). Synchronous; no GPU. */
+lx_status lx_assign(const double* cost, int32_t n, int32_t* perm, double* total);
+
+/* Stage 3, low-rank factors (eqs. svd and factors): the rank-r truncated SVD
+ * of the aligned residual R = W_m^P - W_dom (rows x cols; the member's rows,
+ * perm_axis 0, or columns, perm_axis 1, taken in the order perm [device
+ * int32, or NULL for none]) from a randomized solver, split symmetrically:
+ * A = U_r Sigma_r^(1/2) [rows][r] and B = Sigma_r^(1/2) V_r^T [r][cols] fp32
+ * (output-side and input-side factors of W ~ W_dom + A B), sigma [r] fp64.
+ * Solver: subspace iteration with the Gaussian test matrix omega
+ * [cols][r + p] fp64 (device, caller-drawn), q power iterations, every
+ * product orthonormalised (CholeskyQR2), then the eigendecomposition of the
+ * small Gram matrix of Q^T R (cyclic Jacobi). All in fp64. A sketch
+ * direction the residual does not have (exactly low-rank R) yields a zero
+ * basis column and carries no weight.
+ *
+ * w_dom, w_mem [rows][cols] LX_BF16 or LX_F32 (device); r >= 1, p >= 0,
+ * 0 <= q <= 16 (LX_ERR_INVALID_ARGUMENT); r + p <= min(128, rows, cols),
+ * rows * cols < 2^31 (LX_ERR_UNSUPPORTED); workspace 256-byte aligned,
+ * lx_lowrank_workspace_bytes(rows, cols, r, p) bytes. Asynchronous on
+ * `stream`; deterministic. */
+size_t lx_lowrank_workspace_bytes(int32_t rows, int32_t cols, int32_t r, int32_t p);
+lx_status lx_lowrank_factors(const void* w_dom, const void* w_mem, lx_dtype dtype, int32_t rows, int32_t cols,
+                             const int32_t* perm, int32_t perm_axis, int32_t r, int32_t p, int32_t q,
+                             const double* omega, float* A, float* B, double* sigma, void* workspace,
+                             size_t workspace_bytes, void* stream);
+
 /* Routing bucketing alone (the first step of every forward), exposing the
  * arrays of one tree level `level` (0 = anchors, n_levels = experts):
  *   row_token   [T * min(k, N_level)] (only the first node_offsets[N] entries

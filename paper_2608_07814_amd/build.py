@@ -17,7 +17,7 @@ CSRC = os.path.join(PKG, "csrc")
 INCLUDE = os.path.join(ROOT, "include")
 OBJDIR = os.path.join(ROOT, "_build")
 LIB = os.path.join(PKG, "liblorex.so")
-SOURCES = ["host.hip", "k_bucket.hip", "k_cluster.hip", "k_gemm.hip", "k_gemm2.hip", "k_route.hip", "k_token.hip"]
+SOURCES = ["host.hip", "k_bucket.hip", "k_cluster.hip", "k_gemm.hip", "k_gemm2.hip", "k_route.hip", "k_stage3.hip", "k_token.hip"]
 
 HIPCC = os.environ.get("HIPCC", "/opt/rocm/bin/hipcc")
 # packed fp32 ops are disabled for all device code.

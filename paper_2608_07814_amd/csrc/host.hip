@@ -17,6 +17,7 @@
 #include <algorithm>
 #include <deque>
 #include <map>
+#include <limits>
 #include <mutex>
 #include <string>
 #include <vector>
@@ -994,6 +995,119 @@ lx_status lx_kmedoids(const double* dist, const uint32_t* fire, int32_t E, int32
   hipStream_t lstream = (hipStream_t)stream;
   LX_LAUNCH("kmedoids", launch_kmedoids(dist, fire, E, C, pm, n_protected, max_iter, cluster_of, factor_of, dominant,
                                         iterations, lstream));
+  return LX_OK;
+}
+
+size_t lx_align_workspace_bytes(int32_t f, int32_t d) {
+  if (f < 1 || d < 1) return 0;
+  return (size_t)2 * f * (3 * (size_t)d + 1) * sizeof(double);
+}
+
+lx_status lx_align_cost(const void* dom_gate, const void* dom_up, const void* dom_down, const void* mem_gate,
+                        const void* mem_up, const void* mem_down, lx_dtype dtype, int32_t f, int32_t d, double* cost,
+                        void* workspace, size_t workspace_bytes, void* stream) {
+  g_err.clear();
+  if (dtype != LX_BF16 && dtype != LX_F32) return fail(LX_ERR_INVALID_ARGUMENT, "bad dtype");
+  if (f < 1 || d < 1) return fail(LX_ERR_INVALID_ARGUMENT, "f and d must be positive");
+  if ((int64_t)f * 3 * d >= ((int64_t)1 << 31)) return fail(LX_ERR_UNSUPPORTED, "f * 3d must be below 2^31");
+  const size_t es = dtype == LX_BF16 ? 2 : 4;
+  const void* w[6] = {dom_gate, dom_up, dom_down, mem_gate, mem_up, mem_down};
+  for (const void* q : w)
+    if (!q || !aligned(q, es)) return fail(LX_ERR_INVALID_ARGUMENT, "null or misaligned weight pointer");
+  if (!cost || !aligned(cost, 8) || !workspace || !aligned(workspace, 256))
+    return fail(LX_ERR_INVALID_ARGUMENT, "null or misaligned cost or workspace");
+  if (workspace_bytes < lx_align_workspace_bytes(f, d)) return fail(LX_ERR_WORKSPACE_TOO_SMALL, "workspace too small");
+  hipStream_t lstream = (hipStream_t)stream;
+  LX_LAUNCH("align_cost", launch_align_cost(dom_gate, dom_up, dom_down, mem_gate, mem_up, mem_down,
+                                            dtype == LX_BF16, f, d, cost, (double*)workspace, lstream));
+  return LX_OK;
+}
+
+lx_status lx_assign(const double* cost, int32_t n, int32_t* perm, double* total) {
+  g_err.clear();
+  if (n < 0 || (n > 0 && (!cost || !perm))) return fail(LX_ERR_INVALID_ARGUMENT, "bad arguments");
+  // Shortest augmenting paths with dual potentials (the augmentation phase of
+  // Jonker-Volgenant): rows are added one at a time; each is matched along a
+  // shortest alternating path in reduced costs, found Dijkstra-style over the
+  // columns, after which the potentials keep every reduced cost >= 0.
+  const double inf = std::numeric_limits<double>::infinity();
+  std::vector<double> u(n + 1, 0.0), v(n + 1, 0.0), minv(n + 1);
+  std::vector<int> match(n + 1, 0), way(n + 1, 0);  // match[j]: row of column j (1-based, 0 = free)
+  std::vector<char> used(n + 1);
+  for (int i = 1; i <= n; ++i) {
+    match[0] = i;
+    int j0 = 0;
+    std::fill(minv.begin(), minv.end(), inf);
+    std::fill(used.begin(), used.end(), 0);
+    do {
+      used[j0] = 1;
+      const int i0 = match[j0];
+      double delta = inf;
+      int j1 = 0;
+      const double* const crow = cost + (size_t)(i0 - 1) * n;
+      for (int j = 1; j <= n; ++j) {
+        if (used[j]) continue;
+        const double cur = crow[j - 1] - u[i0] - v[j];
+        if (cur < minv[j]) {
+          minv[j] = cur;
+          way[j] = j0;
+        }
+        if (minv[j] < delta) {
+          delta = minv[j];
+          j1 = j;
+        }
+      }
+      if (j1 == 0) return fail(LX_ERR_INVALID_ARGUMENT, "cost matrix has non-finite entries");
+      for (int j = 0; j <= n; ++j) {
+        if (used[j]) {
+          u[match[j]] += delta;
+          v[j] -= delta;
+        } else {
+          minv[j] -= delta;
+        }
+      }
+      j0 = j1;
+    } while (match[j0] != 0);
+    do {  // flip the path
+      const int j1 = way[j0];
+      match[j0] = match[j1];
+      j0 = j1;
+    } while (j0 != 0);
+  }
+  double t = 0.0;
+  for (int j = 1; j <= n; ++j) perm[match[j] - 1] = j - 1;
+  for (int i = 0; i < n; ++i) t += cost[(size_t)i * n + perm[i]];
+  if (total) *total = t;
+  return LX_OK;
+}
+
+size_t lx_lowrank_workspace_bytes(int32_t rows, int32_t cols, int32_t r, int32_t p) {
+  const int l = r + p;
+  if (rows < 1 || cols < 1 || r < 1 || p < 0 || l > 128 || l > rows || l > cols) return 0;
+  return lowrank_ws_doubles(rows, cols, l) * sizeof(double);
+}
+
+lx_status lx_lowrank_factors(const void* w_dom, const void* w_mem, lx_dtype dtype, int32_t rows, int32_t cols,
+                             const int32_t* perm, int32_t perm_axis, int32_t r, int32_t p, int32_t q,
+                             const double* omega, float* A, float* B, double* sigma, void* workspace,
+                             size_t workspace_bytes, void* stream) {
+  g_err.clear();
+  if (dtype != LX_BF16 && dtype != LX_F32) return fail(LX_ERR_INVALID_ARGUMENT, "bad dtype");
+  if (rows < 1 || cols < 1 || r < 1 || p < 0 || q < 0 || q > 16 || (perm_axis != 0 && perm_axis != 1))
+    return fail(LX_ERR_INVALID_ARGUMENT, "bad sizes, q or perm_axis");
+  const int l = r + p;
+  if (l > 128 || l > rows || l > cols) return fail(LX_ERR_UNSUPPORTED, "r + p must be at most 128, rows and cols");
+  if ((int64_t)rows * cols >= ((int64_t)1 << 31)) return fail(LX_ERR_UNSUPPORTED, "rows * cols must be below 2^31");
+  const size_t es = dtype == LX_BF16 ? 2 : 4;
+  if (!w_dom || !w_mem || !aligned(w_dom, es) || !aligned(w_mem, es) || !omega || !aligned(omega, 8) || !A ||
+      !aligned(A, 4) || !B || !aligned(B, 4) || !sigma || !aligned(sigma, 8) || (perm && !aligned(perm, 4)) ||
+      !workspace || !aligned(workspace, 256))
+    return fail(LX_ERR_INVALID_ARGUMENT, "null or misaligned pointer");
+  if (workspace_bytes < lx_lowrank_workspace_bytes(rows, cols, r, p))
+    return fail(LX_ERR_WORKSPACE_TOO_SMALL, "workspace too small");
+  hipStream_t lstream = (hipStream_t)stream;
+  LX_LAUNCH("lowrank_factors", launch_lowrank(w_dom, w_mem, dtype == LX_BF16, rows, cols, perm, perm_axis, r, l, q,
+                                              omega, A, B, sigma, (double*)workspace, lstream));
   return LX_OK;
 }
 

@@ -299,6 +299,17 @@ hipError_t launch_kmedoids(const double* dist, const uint32_t* fire, int E, int 
                            int max_iter, int32_t* cluster_of, int32_t* factor_of, int32_t* dominant,
                            int32_t* iterations, hipStream_t s);
 
+// ---------------------------------------------------------------- stage 3
+// Alignment cost [f][f] fp64 of two experts (workspace 2 f (3d + 1)
+// doubles); rank-r factors of the aligned residual by a randomized SVD with
+// sketch width l = r + p <= 128 (workspace lowrank_ws_doubles).
+hipError_t launch_align_cost(const void* dg, const void* du, const void* dd, const void* mg, const void* mu,
+                             const void* md, int bf16, int f, int d, double* cost, double* ws, hipStream_t s);
+size_t lowrank_ws_doubles(int rows, int cols, int l);
+hipError_t launch_lowrank(const void* wd, const void* wm, int bf16, int rows, int cols, const int32_t* perm, int axis,
+                          int r, int l, int q, const double* omega, float* A, float* B, double* sigma, double* ws,
+                          hipStream_t s);
+
 hipError_t launch_swiglu_reduce(const TokenArgs& a, hipStream_t s);
 hipError_t launch_combine(const TokenArgs& a, hipStream_t s);
 

@@ -80,6 +80,12 @@ EXPORTS = {
     "lx_coact_distance": (_c_i32, [_c_void, _c_i32, _c_i32, _c_i32, _c_void, _c_void, _c_void, _c_void]),
     "lx_kmedoids": (_c_i32, [_c_void, _c_void, _c_i32, _c_i32, ctypes.POINTER(ctypes.c_int32), _c_i32, _c_i32,
                              _c_void, _c_void, _c_void, _c_void, _c_void]),
+    "lx_align_workspace_bytes": (ctypes.c_size_t, [_c_i32, _c_i32]),
+    "lx_align_cost": (_c_i32, [_c_void] * 6 + [_c_i32, _c_i32, _c_i32, _c_void, _c_void, ctypes.c_size_t, _c_void]),
+    "lx_assign": (_c_i32, [_c_void, _c_i32, _c_void, _c_void]),
+    "lx_lowrank_workspace_bytes": (ctypes.c_size_t, [_c_i32, _c_i32, _c_i32, _c_i32]),
+    "lx_lowrank_factors": (_c_i32, [_c_void, _c_void, _c_i32, _c_i32, _c_i32, _c_void, _c_i32, _c_i32, _c_i32,
+                                    _c_i32, _c_void, _c_void, _c_void, _c_void, _c_void, ctypes.c_size_t, _c_void]),
     "lx_route_topk": (_c_i32, [_c_void, _c_void, _c_i32, _c_i32, _c_i32, _c_i32, _c_i32, _c_void, _c_void,
                                _c_void, ctypes.c_size_t, _c_void]),
     "lx_profile_enable": (_c_i32, [_c_i32]),
@@ -306,6 +312,58 @@ def kmedoids(dist: torch.Tensor, fire: torch.Tensor, C: int, protected=(), max_i
     _check(lib().lx_kmedoids(_ptr(dist), _ptr(fire), E, C, prot, len(protected), max_iter, _ptr(cl), _ptr(fo),
                              _ptr(dom), _ptr(it), _stream(stream)))
     return cl, fo, dom, it
+
+
+def align_cost(dom, mem, stream=None) -> torch.Tensor:
+    """Neuron-alignment cost (lx_align_cost): dom and mem are (gate, up, down)
+    device tensors of one dtype -> fp64 [f][f]."""
+    g = dom[0]
+    f, d = (int(v) for v in g.shape)
+    dt = LX_BF16 if g.dtype == torch.bfloat16 else LX_F32
+    for t in (*dom, *mem):
+        if not t.is_contiguous() or t.dtype != g.dtype:
+            raise ValueError("expert tensors must be contiguous and of one dtype")
+    cost = torch.empty(f, f, dtype=torch.float64, device=g.device)
+    n = int(lib().lx_align_workspace_bytes(f, d))
+    ws = torch.empty(n, dtype=torch.uint8, device=g.device)
+    _check(lib().lx_align_cost(*[_ptr(t) for t in (*dom, *mem)], dt, f, d, _ptr(cost), _ptr(ws), n,
+                               _stream(stream)))
+    return cost
+
+
+def assign(cost) -> tuple:
+    """Exact assignment on the host (lx_assign): fp64 numpy [n][n] ->
+    (int32 perm [n], total cost)."""
+    import numpy as np
+    c = np.ascontiguousarray(cost, dtype=np.float64)
+    n = int(c.shape[0])
+    perm = np.empty(n, np.int32)
+    total = ctypes.c_double(0.0)
+    _check(lib().lx_assign(c.ctypes.data, n, perm.ctypes.data, ctypes.addressof(total)))
+    return perm, total.value
+
+
+def lowrank_factors(w_dom: torch.Tensor, w_mem: torch.Tensor, r: int, omega: torch.Tensor, q: int = 2,
+                    perm: Optional[torch.Tensor] = None, perm_axis: int = 0, stream=None):
+    """Rank-r factors of the aligned residual (lx_lowrank_factors) ->
+    (A fp32 [rows][r], B fp32 [r][cols], sigma fp64 [r])."""
+    rows, cols = (int(v) for v in w_dom.shape)
+    p = int(omega.shape[1]) - r
+    dt = LX_BF16 if w_dom.dtype == torch.bfloat16 else LX_F32
+    if omega.dtype != torch.float64 or not omega.is_contiguous() or int(omega.shape[0]) != cols:
+        raise ValueError("omega must be a contiguous fp64 [cols][r + p] tensor")
+    dev = w_dom.device
+    A = torch.empty(rows, r, dtype=torch.float32, device=dev)
+    B = torch.empty(r, cols, dtype=torch.float32, device=dev)
+    sig = torch.empty(r, dtype=torch.float64, device=dev)
+    n = int(lib().lx_lowrank_workspace_bytes(rows, cols, r, p))
+    if n == 0:
+        raise LorexError("unsupported shape for lx_lowrank_factors")
+    ws = torch.empty(n, dtype=torch.uint8, device=dev)
+    _check(lib().lx_lowrank_factors(_ptr(w_dom), _ptr(w_mem), dt, rows, cols, _ptr(perm) if perm is not None else None,
+                                    perm_axis, r, p, q, _ptr(omega), _ptr(A), _ptr(B), _ptr(sig), _ptr(ws), n,
+                                    _stream(stream)))
+    return A, B, sig
 
 
 def attach_down_f8(layer: "DeviceLayer") -> "DeviceLayer":

@@ -28,7 +28,7 @@ def _declared(root):
 
 def test_every_declared_symbol_is_exported(L, root):
     names = _declared(root)
-    assert len(names) == len(lx.EXPORTS) == 21
+    assert len(names) == len(lx.EXPORTS) == 26
     for n in names:
         assert hasattr(L, n), n
         assert n in lx.EXPORTS, n
@@ -190,3 +190,45 @@ def test_cluster_validation(L):
     assert call(prot=(8,)) == lx.LX_ERR_INVALID_ARGUMENT                  # out of range
     assert call(it=-1) == lx.LX_ERR_INVALID_ARGUMENT
     assert km(FAKE, FAKE, 8, 3, none, 0, 10, None, FAKE, FAKE, FAKE, None) == lx.LX_ERR_INVALID_ARGUMENT
+
+
+def test_assign_on_host_matches_brute_force():
+    """lx_assign is host code: checked here against every permutation."""
+    import itertools
+    import numpy as np
+    rng = np.random.default_rng(7)
+    for n in (1, 3, 6, 8):
+        C = rng.random((n, n))
+        if n == 6:
+            C = np.round(C * 4) / 4              # many ties among optima
+        perm, total = lx.assign(C)
+        best = min(sum(C[i, p[i]] for i in range(n)) for p in itertools.permutations(range(n)))
+        assert sorted(perm.tolist()) == list(range(n))
+        assert abs(total - best) < 1e-12 and abs(total - C[np.arange(n), perm].sum()) < 1e-12
+    perm, total = lx.assign(np.zeros((0, 0)))
+    assert perm.size == 0 and total == 0.0
+
+
+def test_stage3_validation(L):
+    need = L.lx_align_workspace_bytes(768, 2048)
+    assert need == 2 * 768 * (3 * 2048 + 1) * 8
+    args = [FAKE] * 6
+    assert L.lx_align_cost(*args, lx.LX_BF16, 768, 2048, FAKE, FAKE, need - 1, None) == lx.LX_ERR_WORKSPACE_TOO_SMALL
+    assert L.lx_align_cost(*args, 7, 768, 2048, FAKE, FAKE, need, None) == lx.LX_ERR_INVALID_ARGUMENT
+    assert L.lx_align_cost(FAKE + 1, *args[1:], lx.LX_BF16, 768, 2048, FAKE, FAKE, need, None) \
+        == lx.LX_ERR_INVALID_ARGUMENT
+    assert L.lx_lowrank_workspace_bytes(768, 2048, 120, 10) == 0          # r + p > 128
+    n = L.lx_lowrank_workspace_bytes(768, 2048, 64, 10)
+    lr = L.lx_lowrank_factors
+    base = dict(t=lx.LX_BF16, rows=768, cols=2048, perm=None, ax=0, r=64, p=10, q=2, n=n)
+
+    def call(**kw):
+        a = dict(base, **kw)
+        return lr(FAKE, FAKE, a["t"], a["rows"], a["cols"], a["perm"], a["ax"], a["r"], a["p"], a["q"], FAKE, FAKE,
+                  FAKE, FAKE, FAKE, a["n"], None)
+    assert call(r=120) == lx.LX_ERR_UNSUPPORTED
+    assert call(rows=50) == lx.LX_ERR_UNSUPPORTED                          # r + p > rows
+    assert call(q=-1) == lx.LX_ERR_INVALID_ARGUMENT
+    assert call(ax=2) == lx.LX_ERR_INVALID_ARGUMENT
+    assert call(n=n - 1) == lx.LX_ERR_WORKSPACE_TOO_SMALL
+    assert call(perm=FAKE + 2) == lx.LX_ERR_INVALID_ARGUMENT
