@@ -54,6 +54,10 @@ def parse():
                     help="no fp8 copy of the anchor down weights: the anchor down projection multiplies "
                          "both halves of its bf16 (hi, lo) input in bf16")
     ap.add_argument("--no-route", action="store_true", help="skip timing the GPU top-k router")
+    ap.add_argument("--stage3", action="store_true",
+                    help="also time Stage-3 factor production for one member at the workload's expert shape "
+                         "(alignment cost, host assignment, randomized SVD factors of the three projections), "
+                         "against the oracle on the host")
     ap.add_argument("--cluster", action="store_true",
                     help="also time router profiling + NPMI distance + k-medoids (Stages 1-2) on a calibration "
                          "routing of 64 x 2048 tokens, against the oracle on the host")
@@ -228,6 +232,62 @@ def bench_clustering(torch, np, lx, a):
                 ids_bytes=N * k * 4, cpu_oracle_s=round(cpu_s, 2), clusters_match_oracle=same)
 
 
+def bench_stage3(torch, np, lx, layer):
+    """Stage 3 for one member at the layer's expert shape (d, f, rank r,
+    oversampling 10, 2 power iterations): a dominant and a member that is the
+    dominant plus rank-r corrections with its neurons shuffled, both bf16.
+    GPU: alignment cost, host assignment, factors of gate, up and down; the
+    oracle runs the same steps on the host."""
+    from lxsynth import f32_to_bf16_bits
+    from oracle import stage3 as S
+    d, f, r, p = layer.d, layer.f, layer.levels[0].rank, 10
+    rng = np.random.default_rng(3)
+    s = np.sqrt(0.3 / np.sqrt(r * d))
+    dom64 = [rng.standard_normal(sh) / np.sqrt(d) for sh in ((f, d), (f, d), (d, f))]
+    cor = [(rng.standard_normal((a, r)) * s) @ (rng.standard_normal((r, b)) * s) for a, b in ((f, d), (f, d), (d, f))]
+    inv = np.argsort(rng.permutation(f))
+    bf = lambda x: f32_to_bf16_bits(np.asarray(x, np.float32))
+    dom = [bf(x) for x in dom64]
+    mem = [bf((dom64[0] + cor[0])[inv]), bf((dom64[1] + cor[1])[inv]), bf((dom64[2] + cor[2])[:, inv])]
+    dev = lambda b: torch.from_numpy(b.view(np.int16)).cuda().view(torch.bfloat16)
+    ddom, dmem = [dev(x) for x in dom], [dev(x) for x in mem]
+    oms = [rng.standard_normal((w.shape[1], r + p)) for w in dom]
+    doms = [torch.from_numpy(o).cuda() for o in oms]
+
+    def factors(pd):
+        for i in range(3):
+            lx.lowrank_factors(ddom[i], dmem[i], r, doms[i], q=2, perm=pd, perm_axis=1 if i == 2 else 0)
+
+    factors(torch.from_numpy(lx.assign(lx.align_cost(tuple(ddom), tuple(dmem)).cpu().numpy())[0]).cuda())  # warm-up
+    torch.cuda.synchronize()
+    ev = [torch.cuda.Event(enable_timing=True) for _ in range(4)]
+    ev[0].record()
+    cost = lx.align_cost(tuple(ddom), tuple(dmem))
+    ev[1].record()
+    torch.cuda.synchronize()
+    t0 = time.perf_counter()
+    perm, _ = lx.assign(cost.cpu().numpy())
+    t_assign = time.perf_counter() - t0
+    pd = torch.from_numpy(perm).cuda()
+    torch.cuda.synchronize()
+    ev[2].record()
+    factors(pd)
+    ev[3].record()
+    torch.cuda.synchronize()
+    t1 = time.perf_counter()
+    perm0, _ = S.assign(S.align_cost(dom, mem, "bf16"))
+    for i in range(3):
+        S.factors(S.aligned_residual(dom[i], mem[i], perm0, 1 if i == 2 else 0, "bf16"), oms[i], r, q=2)
+    cpu_s = time.perf_counter() - t1
+    return dict(d=d, f=f, r=r, oversampling=p, power_iterations=2,
+                align_cost_us=round(ev[0].elapsed_time(ev[1]) * 1e3, 1),
+                align_cost_gflop=round(2 * f * f * 3 * d / 1e9, 2),
+                assign_host_ms=round(t_assign * 1e3, 2),
+                factors_3_projections_us=round(ev[2].elapsed_time(ev[3]) * 1e3, 1),
+                permutation_matches_oracle=bool(np.array_equal(perm, perm0)),
+                cpu_oracle_s=round(cpu_s, 2))
+
+
 def main():
     a = parse()
     if a.gpus != 1:
@@ -398,6 +458,9 @@ def main():
     clustering = None
     if a.cluster:
         clustering = bench_clustering(torch, np, lx, a)
+    stage3 = None
+    if a.stage3 and kind == "flat" and layer.dtype == "bf16":
+        stage3 = bench_stage3(torch, np, lx, layer)
 
     cpu = None
     if not a.no_cpu:
@@ -444,6 +507,7 @@ def main():
         "dense_comparator": dense,
         "gpu_router": routed,
         "clustering": clustering,
+        "stage3": stage3,
         "cpu_baseline": cpu,
     }
     print(json.dumps(res), flush=True)

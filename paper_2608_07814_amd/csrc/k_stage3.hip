@@ -23,24 +23,29 @@ namespace {
 
 constexpr int DG_T = 64, DG_K = 16;
 
+// Split-K: blockIdx.z takes K range [z kc, (z + 1) kc) and writes its
+// partial tile to C + z * M * N (ldc = N); k_dsum adds the partials in z
+// order.
 __global__ __launch_bounds__(256) void k_dgemm(int M, int N, int K, double alpha, const double* __restrict__ A,
                                                int64_t lda, int ta, const double* __restrict__ B, int64_t ldb, int tb,
-                                               double* __restrict__ C, int64_t ldc, int accumulate) {
+                                               double* __restrict__ C, int64_t ldc, int kc) {
   __shared__ double sA[DG_K][DG_T + 1];
   __shared__ double sB[DG_K][DG_T + 1];
   const int tx = threadIdx.x & 15, ty = threadIdx.x >> 4;
   const int m0 = blockIdx.y * DG_T, n0 = blockIdx.x * DG_T;
+  const int kbeg = blockIdx.z * kc, kend = kbeg + kc < K ? kbeg + kc : K;
+  C += (int64_t)blockIdx.z * M * N;
   double acc[4][4] = {};
-  for (int k0 = 0; k0 < K; k0 += DG_K) {
+  for (int k0 = kbeg; k0 < kend; k0 += DG_K) {
     for (int q = threadIdx.x; q < DG_K * DG_T; q += 256) {
       const int kk = q / DG_T, mm = q % DG_T;
       const int gm = m0 + mm, gk = k0 + kk;
       double va = 0.0;
-      if (gm < M && gk < K) va = ta ? A[(int64_t)gk * lda + gm] : A[(int64_t)gm * lda + gk];
+      if (gm < M && gk < kend) va = ta ? A[(int64_t)gk * lda + gm] : A[(int64_t)gm * lda + gk];
       sA[kk][mm] = va;
       const int gn = n0 + mm;
       double vb = 0.0;
-      if (gn < N && gk < K) vb = tb ? B[(int64_t)gn * ldb + gk] : B[(int64_t)gk * ldb + gn];
+      if (gn < N && gk < kend) vb = tb ? B[(int64_t)gn * ldb + gk] : B[(int64_t)gk * ldb + gn];
       sB[kk][mm] = vb;
     }
     __syncthreads();
@@ -63,11 +68,17 @@ __global__ __launch_bounds__(256) void k_dgemm(int M, int N, int K, double alpha
 #pragma unroll
     for (int j = 0; j < 4; ++j) {
       const int gm = m0 + ty * 4 + i, gn = n0 + tx * 4 + j;
-      if (gm < M && gn < N) {
-        double* const c = C + (int64_t)gm * ldc + gn;
-        *c = accumulate ? *c + alpha * acc[i][j] : alpha * acc[i][j];
-      }
+      if (gm < M && gn < N) C[(int64_t)gm * ldc + gn] = alpha * acc[i][j];
     }
+}
+
+__global__ __launch_bounds__(256) void k_dsum(const double* __restrict__ part, int S, int M, int N,
+                                              double* __restrict__ C, int64_t ldc) {
+  const int64_t q = (int64_t)blockIdx.x * blockDim.x + threadIdx.x;
+  if (q >= (int64_t)M * N) return;
+  double v = part[q];
+  for (int z = 1; z < S; ++z) v += part[(int64_t)z * M * N + q];
+  C[(q / N) * ldc + q % N] = v;
 }
 
 // Neuron vectors of an expert, fp64 [f][3d]: row i = (gate[i, :], up[i, :],
@@ -176,28 +187,45 @@ __global__ __launch_bounds__(1024) void k_chol(const double* __restrict__ G, int
 }
 
 // Y[i, :] <- Y[i, :] U^-1 for the upper-triangular l x l U: x U = y, solved
-// left to right, one thread per row.
-__global__ __launch_bounds__(256) void k_trsm_rows(double* __restrict__ Y, int rows, int l,
-                                                   const double* __restrict__ U) {
-  const int i = blockIdx.x * blockDim.x + threadIdx.x;
-  if (i >= rows) return;
-  double* const y = Y + (int64_t)i * l;
-  for (int j = 0; j < l; ++j) {
-    double s = y[j];
-    for (int k = 0; k < j; ++k) s -= y[k] * U[k * l + j];
-    const double ujj = U[j * l + j];
-    y[j] = ujj != 0.0 ? s / ujj : 0.0;
+// left to right, one thread per row; U and the workgroup's rw rows (pitch
+// l + 1) staged in LDS.
+__global__ __launch_bounds__(64) void k_trsm_rows(double* __restrict__ Y, int rows, int l, int rw,
+                                                  const double* __restrict__ U) {
+  extern __shared__ double s_t[];
+  double* const su = s_t;
+  double* const sy = s_t + l * l;
+  const int r0 = blockIdx.x * rw, tid = threadIdx.x;
+  const int nr = rows - r0 < rw ? rows - r0 : rw;
+  for (int q = tid; q < l * l; q += 64) su[q] = U[q];
+  for (int q = tid; q < nr * l; q += 64) sy[(q / l) * (l + 1) + q % l] = Y[(int64_t)(r0 + q / l) * l + q % l];
+  __syncthreads();
+  if (tid < nr) {
+    double* const y = sy + tid * (l + 1);
+    for (int j = 0; j < l; ++j) {
+      double acc = y[j];
+      for (int k = 0; k < j; ++k) acc -= y[k] * su[k * l + j];
+      const double ujj = su[j * l + j];
+      y[j] = ujj != 0.0 ? acc / ujj : 0.0;
+    }
   }
+  __syncthreads();
+  for (int q = tid; q < nr * l; q += 64) Y[(int64_t)(r0 + q / l) * l + q % l] = sy[(q / l) * (l + 1) + q % l];
 }
+
+inline int trsm_rows_per_wg(int l) { return l <= 96 ? 64 : 16; }
+inline size_t trsm_lds(int l) { return ((size_t)l * l + (size_t)trsm_rows_per_wg(l) * (l + 1)) * sizeof(double); }
 
 // Eigendecomposition of the symmetric l x l M (l even after padding with a
 // zero row/column when odd): cyclic Jacobi, round-robin pair order; V
-// (global, l x l row-major) accumulates the rotations. Output: eigenvalues
+// (lp x lp row-major, in LDS when both fit, else global) accumulates the
+// rotations. Output: eigenvalues
 // descending in w[0..l), eigenvectors as columns of Vs (sorted).
+template <bool VLDS>
 __global__ __launch_bounds__(1024) void k_jacobi(const double* __restrict__ Min, int l, int lp,
-                                                 double* __restrict__ V, double* __restrict__ w,
+                                                 double* __restrict__ Vg, double* __restrict__ w,
                                                  double* __restrict__ Vs, int max_sweeps) {
-  extern __shared__ double s_m[];  // [lp][lp]
+  extern __shared__ double s_m[];  // [lp][lp], then V [lp][lp] when VLDS
+  double* const V = VLDS ? s_m + lp * lp : Vg;
   __shared__ int s_p[64], s_q[64];
   __shared__ double s_c[64], s_s[64];
   __shared__ int s_order[128];
@@ -318,11 +346,32 @@ __global__ __launch_bounds__(256) void k_to_f32(const double* __restrict__ x, in
 
 inline unsigned blocks(int64_t n, int t = 256) { return (unsigned)((n + t - 1) / t); }
 
+// Partial tiles for the split products: at most kDgParts doubles.
+constexpr int64_t kDgParts = 384 * DG_T * DG_T;
+
+// C = alpha op(A) op(B). With few output tiles and a long K the K range is
+// split (at least 4 slabs of 16 per split, about 256 workgroups in all) over
+// the partial buffer part (kDgParts doubles, may be null: no split).
 hipError_t dgemm(int M, int N, int K, double alpha, const double* A, int64_t lda, int ta, const double* B, int64_t ldb,
-                 int tb, double* C, int64_t ldc, hipStream_t s) {
+                 int tb, double* C, int64_t ldc, hipStream_t s, double* part) {
   if (M <= 0 || N <= 0) return hipSuccess;
-  hipLaunchKernelGGL(k_dgemm, dim3((N + DG_T - 1) / DG_T, (M + DG_T - 1) / DG_T), dim3(256), 0, s, M, N, K, alpha, A,
-                     lda, ta, B, ldb, tb, C, ldc, 0);
+  const int tiles = ((M + DG_T - 1) / DG_T) * ((N + DG_T - 1) / DG_T);
+  int S = 1;
+  if (part && tiles < 128) {
+    S = (256 + tiles - 1) / tiles;
+    const int smax = K / (4 * DG_K);
+    S = S < smax ? S : smax;
+    while (S > 1 && (int64_t)S * M * N > kDgParts) --S;
+    if (S < 1) S = 1;
+  }
+  const dim3 grid((N + DG_T - 1) / DG_T, (M + DG_T - 1) / DG_T, S);
+  if (S == 1) {
+    hipLaunchKernelGGL(k_dgemm, grid, dim3(256), 0, s, M, N, K, alpha, A, lda, ta, B, ldb, tb, C, ldc, K);
+    return hipGetLastError();
+  }
+  const int kc = ((K + S - 1) / S + DG_K - 1) / DG_K * DG_K;
+  hipLaunchKernelGGL(k_dgemm, grid, dim3(256), 0, s, M, N, K, alpha, A, lda, ta, B, ldb, tb, part, (int64_t)N, kc);
+  hipLaunchKernelGGL(k_dsum, dim3(blocks((int64_t)M * N)), dim3(256), 0, s, part, S, M, N, C, ldc);
   return hipGetLastError();
 }
 
@@ -330,20 +379,23 @@ hipError_t dgemm(int M, int N, int K, double alpha, const double* A, int64_t lda
 // Kernels with up to 128 KB of dynamic LDS: allow it once per process.
 hipError_t allow_lds() {
   static hipError_t e = [] {
-    hipError_t r = hipFuncSetAttribute((const void*)k_chol, hipFuncAttributeMaxDynamicSharedMemorySize, 128 * 1024);
-    if (r == hipSuccess)
-      r = hipFuncSetAttribute((const void*)k_jacobi, hipFuncAttributeMaxDynamicSharedMemorySize, 128 * 1024);
+    const hipFuncAttribute a = hipFuncAttributeMaxDynamicSharedMemorySize;
+    hipError_t r = hipFuncSetAttribute((const void*)k_chol, a, 128 * 1024);
+    if (r == hipSuccess) r = hipFuncSetAttribute((const void*)k_jacobi<false>, a, 128 * 1024);
+    if (r == hipSuccess) r = hipFuncSetAttribute((const void*)k_jacobi<true>, a, 2 * 96 * 96 * 8);
+    if (r == hipSuccess) r = hipFuncSetAttribute((const void*)k_trsm_rows, a, 148 * 1024);
     return r;
   }();
   return e;
 }
 
-hipError_t cholqr2(double* Y, int rows, int l, double* G, double* U, hipStream_t s) {
+hipError_t cholqr2(double* Y, int rows, int l, double* G, double* U, hipStream_t s, double* part) {
   for (int pass = 0; pass < 2; ++pass) {
-    hipError_t e = dgemm(l, l, rows, 1.0, Y, l, 1, Y, l, 0, G, l, s);
+    hipError_t e = dgemm(l, l, rows, 1.0, Y, l, 1, Y, l, 0, G, l, s, part);
     if (e != hipSuccess) return e;
     hipLaunchKernelGGL(k_chol, dim3(1), dim3(1024), (size_t)l * l * sizeof(double), s, G, l, U);
-    hipLaunchKernelGGL(k_trsm_rows, dim3(blocks(rows)), dim3(256), 0, s, Y, rows, l, U);
+    const int rw = trsm_rows_per_wg(l);
+    hipLaunchKernelGGL(k_trsm_rows, dim3((rows + rw - 1) / rw), dim3(64), trsm_lds(l), s, Y, rows, l, rw, U);
     if ((e = hipGetLastError()) != hipSuccess) return e;
   }
   return hipSuccess;
@@ -354,7 +406,7 @@ hipError_t cholqr2(double* Y, int rows, int l, double* G, double* U, hipStream_t
 size_t lowrank_ws_doubles(int rows, int cols, int l) {
   const int lp = l + (l & 1);
   return (size_t)rows * cols + (size_t)rows * l + (size_t)cols * l + (size_t)l * cols + 4 * (size_t)lp * lp + 2 * lp +
-         (size_t)rows * l;
+         (size_t)rows * l + (size_t)kDgParts;
 }
 
 hipError_t launch_align_cost(const void* dg, const void* du, const void* dd, const void* mg, const void* mu,
@@ -365,7 +417,7 @@ hipError_t launch_align_cost(const void* dg, const void* du, const void* dd, con
   double* const nb = na + f;
   hipLaunchKernelGGL(k_neurons, dim3(f), dim3(256), 0, s, dg, du, dd, bf16, f, d, a, na);
   hipLaunchKernelGGL(k_neurons, dim3(f), dim3(256), 0, s, mg, mu, md, bf16, f, d, b, nb);
-  hipError_t e = dgemm(f, f, 3 * d, 1.0, a, 3 * d, 0, b, 3 * d, 1, cost, f, s);
+  hipError_t e = dgemm(f, f, 3 * d, 1.0, a, 3 * d, 0, b, 3 * d, 1, cost, f, s, nullptr);
   if (e != hipSuccess) return e;
   hipLaunchKernelGGL(k_cost_finish, dim3(blocks((int64_t)f * f)), dim3(256), 0, s, na, nb, f, cost);
   return hipGetLastError();
@@ -387,30 +439,36 @@ hipError_t launch_lowrank(const void* wd, const void* wm, int bf16, int rows, in
   double* const lam = Ve + (size_t)lp * lp;          // lp
   double* const sig = lam + lp;                      // lp
   double* const Ad = sig + lp;                       // rows x l (A before truncation)
+  double* const part = Ad + (size_t)rows * l;        // kDgParts (split-K partial tiles)
   hipLaunchKernelGGL(k_residual, dim3(blocks((int64_t)rows * cols)), dim3(256), 0, s, wd, wm, bf16, rows, cols, perm,
                      axis, R);
   hipError_t e;
   // Y = R Omega, orthonormalised; q rounds of Z = R^T Y, Y = R Z, each
   // orthonormalised
-  if ((e = dgemm(rows, l, cols, 1.0, R, cols, 0, omega, l, 0, Y, l, s)) != hipSuccess) return e;
-  if ((e = cholqr2(Y, rows, l, G, U, s)) != hipSuccess) return e;
+  if ((e = dgemm(rows, l, cols, 1.0, R, cols, 0, omega, l, 0, Y, l, s, part)) != hipSuccess) return e;
+  if ((e = cholqr2(Y, rows, l, G, U, s, part)) != hipSuccess) return e;
   for (int it = 0; it < q; ++it) {
-    if ((e = dgemm(cols, l, rows, 1.0, R, cols, 1, Y, l, 0, Z, l, s)) != hipSuccess) return e;
-    if ((e = cholqr2(Z, cols, l, G, U, s)) != hipSuccess) return e;
-    if ((e = dgemm(rows, l, cols, 1.0, R, cols, 0, Z, l, 0, Y, l, s)) != hipSuccess) return e;
-    if ((e = cholqr2(Y, rows, l, G, U, s)) != hipSuccess) return e;
+    if ((e = dgemm(cols, l, rows, 1.0, R, cols, 1, Y, l, 0, Z, l, s, part)) != hipSuccess) return e;
+    if ((e = cholqr2(Z, cols, l, G, U, s, part)) != hipSuccess) return e;
+    if ((e = dgemm(rows, l, cols, 1.0, R, cols, 0, Z, l, 0, Y, l, s, part)) != hipSuccess) return e;
+    if ((e = cholqr2(Y, rows, l, G, U, s, part)) != hipSuccess) return e;
   }
   // Bs = Y^T R (l x cols); M = Bs Bs^T (l x l) = Ut diag(lambda) Ut^T
-  if ((e = dgemm(l, cols, rows, 1.0, Y, l, 1, R, cols, 0, Bs, cols, s)) != hipSuccess) return e;
-  if ((e = dgemm(l, l, cols, 1.0, Bs, cols, 0, Bs, cols, 1, G, l, s)) != hipSuccess) return e;
-  hipLaunchKernelGGL(k_jacobi, dim3(1), dim3(1024), (size_t)lp * lp * sizeof(double), s, G, l, lp, V, lam, Ve, 40);
+  if ((e = dgemm(l, cols, rows, 1.0, Y, l, 1, R, cols, 0, Bs, cols, s, part)) != hipSuccess) return e;
+  if ((e = dgemm(l, l, cols, 1.0, Bs, cols, 0, Bs, cols, 1, G, l, s, part)) != hipSuccess) return e;
+  if (lp <= 96)
+    hipLaunchKernelGGL(k_jacobi<true>, dim3(1), dim3(1024), 2 * (size_t)lp * lp * sizeof(double), s, G, l, lp, V, lam,
+                       Ve, 40);
+  else
+    hipLaunchKernelGGL(k_jacobi<false>, dim3(1), dim3(1024), (size_t)lp * lp * sizeof(double), s, G, l, lp, V, lam,
+                       Ve, 40);
   hipLaunchKernelGGL(k_sqrt_vec, dim3(1), dim3(256), 0, s, lam, r, sig);
   // A = Y Ut[:, :r] sigma^(1/2); B = sigma^(-1/2) Ut[:, :r]^T Bs
-  if ((e = dgemm(rows, r, l, 1.0, Y, l, 0, Ve, l, 0, Ad, r, s)) != hipSuccess) return e;
+  if ((e = dgemm(rows, r, l, 1.0, Y, l, 0, Ve, l, 0, Ad, r, s, part)) != hipSuccess) return e;
   hipLaunchKernelGGL(k_scale, dim3(blocks((int64_t)rows * r)), dim3(256), 0, s, Ad, rows, r, sig, 1, 0);
   hipLaunchKernelGGL(k_to_f32, dim3(blocks((int64_t)rows * r)), dim3(256), 0, s, Ad, (int64_t)rows * r, A);
   double* const Bd = Z;  // r x cols (Z is cols x l, l >= r)
-  if ((e = dgemm(r, cols, l, 1.0, Ve, l, 1, Bs, cols, 0, Bd, cols, s)) != hipSuccess) return e;
+  if ((e = dgemm(r, cols, l, 1.0, Ve, l, 1, Bs, cols, 0, Bd, cols, s, part)) != hipSuccess) return e;
   hipLaunchKernelGGL(k_scale, dim3(blocks((int64_t)r * cols)), dim3(256), 0, s, Bd, r, cols, sig, 0, 1);
   hipLaunchKernelGGL(k_to_f32, dim3(blocks((int64_t)r * cols)), dim3(256), 0, s, Bd, (int64_t)r * cols, B);
   hipLaunchKernelGGL(k_copy_f64, dim3(1), dim3(256), 0, s, sig, r, sigma);
