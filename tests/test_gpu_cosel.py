@@ -80,3 +80,16 @@ def test_paper_shape_cosel():
         e = err_ratio(got, ref[:n])
         say(f"  err/RMS = {e:.3e}")
         assert e <= TOL_BF16 and e <= TOL_DESIGN
+
+
+@pytest.mark.parametrize("T", [1, 8, 64])
+def test_tree_decode_sizes(T):
+    """The BTExperts tree (d = 4096, f = 1024, 256 leaves) at decode sizes:
+    every level on the skinny kernel, long-K products split."""
+    require_gpu()
+    say(f"tree decode T={T}")
+    p = make_problem(4, T=T)
+    got = gpu_forward(p)
+    e = err_ratio(got, _oracle(p))
+    say(f"  err/RMS = {e:.3e}")
+    assert e <= TOL_BF16 and e <= TOL_DESIGN
