@@ -476,10 +476,25 @@ def main():
             if dt >= a.cpu_seconds or reps >= 64:
                 break
         threads = max([i.get("num_threads", 1) for i in threadpool_info()] or [1])
+        # one core: a shorter sample (a quarter of the tokens, one pass)
+        from threadpoolctl import threadpool_limits
+        n1 = max(1, n // 4)
+        with threadpool_limits(limits=1):
+            t1 = time.perf_counter()
+            O.moe_forward(layer, p.x, p.routing.topk_ids, p.routing.topk_weights, tokens=np.arange(n1))
+            dt1 = time.perf_counter() - t1
+        model = None
+        try:
+            with open("/proc/cpuinfo") as fh:
+                model = next((ln.split(":", 1)[1].strip() for ln in fh if ln.startswith("model name")), None)
+        except OSError:
+            pass
         cpu = dict(value=round(n * reps / dt, 2), unit="tokens/s", cores=int(threads), kind="oracle",
                    sample=f"first {n} of {T} tokens of the same workload, {reps} passes, fp64 numpy "
                           f"oracle (dense reconstruction of every routed expert + per-slot SwiGLU), "
-                          f"{dt:.1f} s wall", nproc=os.cpu_count())
+                          f"{dt:.1f} s wall", nproc=os.cpu_count(), cpu_model=model,
+                   single_core_value=round(n1 / dt1, 2),
+                   single_core_sample=f"first {n1} tokens, one pass, {dt1:.1f} s wall")
 
     res = {
         "metric": "MoE-layer tokens/s (LorExperts forward, bucketing included)",
