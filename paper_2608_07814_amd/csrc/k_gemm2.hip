@@ -816,6 +816,122 @@ __global__ __launch_bounds__(SK_THR) void k_gemm_skinny(SkinnyBatch b) {
 }
 
 
+// Wide variant for products whose K is one weight slab (K = 64, or a bf16
+// (hi, lo) pair against a 64-column weight row): a workgroup takes NB
+// consecutive 64-column tiles of one row tile, loads the A slab(s) once and
+// every weight slab at once (no K loop, nothing to pipeline), so the fixed
+// per-workgroup latency (tile entry, row map, one load round trip, epilogue)
+// is paid once per NB tiles. Wavefront w computes columns w * 32 .. w * 32 + 31
+// of each of its tiles.
+template <int NB, int PER>
+__global__ __launch_bounds__(SK_THR) void k_gemm_skinny_wide(SkinnyBatch b) {
+  constexpr int BM = kSkinnyBM, BN = kSkinnyBN;
+  constexpr int A_ROUNDS = BM * 8 / SK_THR, B_ROUNDS = BN * 8 / SK_THR;
+  constexpr int SA = BM * BK2, SBt = BN * BK2;
+  __shared__ __attribute__((aligned(1024))) u16 smem[PER * SA + NB * SBt];
+
+  int pi = 0;
+  while (pi + 1 < b.n && (int)blockIdx.x >= b.base[pi + 1]) ++pi;
+  const GemmArgs& p = b.g[pi];
+  const int ntn = b.ntn[pi], ofmt = b.ofmt[pi];
+  const int ngr = (ntn + NB - 1) / NB;  // column groups
+  const int wg = (int)blockIdx.x - b.base[pi];
+  const int real = skinny_tiles(p) * ngr;
+  const int q = real / NXCD, rmd = real % NXCD;
+  const int x = wg % NXCD;
+  const int Lg = x * q + (x < rmd ? x : rmd) + wg / NXCD;
+  if (Lg >= x * q + (x < rmd ? x : rmd) + q + (x < rmd ? 1 : 0)) return;
+  const int ti = Lg / ngr, gr = Lg % ngr;
+  SkUnit u;
+  u.p = &p;
+  u.ntn = ntn;
+  u.ofmt = ofmt;
+  u.S = 1;
+  u.Lg = Lg;
+  u.item = 0;
+  u.kt0 = 0;
+  u.nkl = 1;
+  u.Kb = p.Kb > 0 ? p.Kb : p.K;
+  u.nper = p.K / u.Kb;
+  if (p.tiles) {
+    u.te = p.tiles[ti];
+  } else {
+    u.te.widx = 0;
+    u.te.row0 = ti * BM;
+    u.te.nrows = p.dense_rows - u.te.row0 < BM ? p.dense_rows - u.te.row0 : BM;
+    u.te.node = 0;
+  }
+  u.ncol = p.ncols[0] + p.ncols[1];
+  const TileEntry& te = u.te;
+  const int tid = threadIdx.x, wave = tid >> 6, lane = tid & 63;
+  const int Kb = u.Kb;
+  const u16* __restrict__ Ab = (const u16*)p.A;
+  const u16* __restrict__ Bw0 = (const u16*)p.B[0] + (int64_t)te.widx * p.b_stride[0];
+  const u16* __restrict__ Bw1 = (const u16*)p.B[1] + (int64_t)te.widx * p.b_stride[1];
+  const int n0g = gr * NB * BN;
+  // the group's A column offset: its tiles lie in one part (the host checks
+  // that the part boundary is a multiple of NB * 64 when the parts differ)
+  const int akoff = p.a_koff[n0g < p.ncols[0] ? 0 : 1];
+
+#pragma unroll
+  for (int per = 0; per < PER; ++per)
+#pragma unroll
+    for (int j = 0; j < A_ROUNDS; ++j) {
+      const int Ps = j * SK_THR + tid;
+      const int row = Ps >> 3;
+      const int c = (Ps & 7) ^ swz2(row);
+      const int r = row < te.nrows ? row : te.nrows - 1;
+      const int src = p.a_rows ? p.a_rows[te.row0 + r] : te.row0 + r;
+      load_lds16(Ab + ((uint32_t)src * (uint32_t)p.lda + (uint32_t)(akoff + per * Kb + c * 8)),
+                 smem + per * SA + (j * SK_THR + wave * 64) * 8);
+    }
+#pragma unroll
+  for (int t = 0; t < NB; ++t)
+#pragma unroll
+    for (int j = 0; j < B_ROUNDS; ++j) {
+      const int Ps = j * SK_THR + tid;
+      const int row = Ps >> 3;
+      const int c = (Ps & 7) ^ swz2(row);
+      int n = n0g + t * BN + row;
+      n = n < u.ncol ? n : u.ncol - 1;
+      const u16* bp = (n < p.ncols[0] ? Bw0 + (int64_t)n * Kb : Bw1 + (int64_t)(n - p.ncols[0]) * Kb) + c * 8;
+      load_lds16(bp, smem + PER * SA + t * SBt + (j * SK_THR + wave * 64) * 8);
+    }
+  wait_vmcnt<0>();
+  bar();
+  f32x16 acc[NB];
+#pragma unroll
+  for (int t = 0; t < NB; ++t)
+#pragma unroll
+    for (int i = 0; i < 16; ++i) acc[t][i] = 0.f;
+  const int ra = lane & 31, rb = wave * 32 + (lane & 31);
+#pragma unroll
+  for (int ks = 0; ks < 4; ++ks) {
+    const int kc = ks * 2 + (lane >> 5);
+    bf16x8 fa[PER];
+#pragma unroll
+    for (int per = 0; per < PER; ++per) fa[per] = *(const bf16x8*)&smem[per * SA + lds_off2(ra, kc)];
+#pragma unroll
+    for (int t = 0; t < NB; ++t) {
+      const bf16x8 fb = *(const bf16x8*)&smem[PER * SA + t * SBt + lds_off2(rb, kc)];
+#pragma unroll
+      for (int per = 0; per < PER; ++per)
+        acc[t] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(fa[per], fb, acc[t], 0, 0, 0);
+    }
+  }
+  wait_lgkm0();
+  bar();  // the epilogue reuses the LDS
+  float* const ep = (float*)smem + wave * (32 * 36);
+#pragma unroll
+  for (int t = 0; t < NB; ++t) {
+    u.n0 = n0g + t * BN;
+    if (u.n0 >= u.ncol) break;  // uniform
+    u.akoff = akoff;
+    sk_epilogue(u, acc[t], ep);
+    bar();  // ep is rewritten by the next tile
+  }
+}
+
 template <int BM, int BN>
 hipError_t launch_bn(const GemmArgs& g, int ofmt, int grid, int ntn, hipStream_t s) {
   if (ofmt == OUT_HILO)
@@ -958,6 +1074,36 @@ hipError_t launch_gemm_skinny_batch(const GemmArgs* g, const int* ofmt, const in
     const int Kb = g[i].Kb > 0 ? g[i].Kb : g[i].K;
     pair = pair && g[i].K == 2 * Kb;
     max_steps = std::max(max_steps, g[i].K / BK2);
+  }
+  // every product one weight slab of 64 (K = 64, or a hi/lo pair of them),
+  // no split, part boundaries that no 4-tile group straddles, and enough row
+  // tiles that 4-tile groups still give at least 512 workgroups: wide
+  // (with few row tiles, e.g. one token, the narrow kernel keeps more
+  // workgroups, hence more loads, in flight)
+  bool wide = true;
+  int64_t groups = 0;
+  for (int i = 0; i < n; ++i) groups += (int64_t)grid_tiles[i] * ((b.ntn[i] + 3) / 4);
+  wide = groups >= 512;
+  for (int i = 0; i < n; ++i) {
+    const int Kb = g[i].Kb > 0 ? g[i].Kb : g[i].K;
+    wide = wide && Kb == BK2 && (g[i].K == BK2 || g[i].K == 2 * BK2) && g[i].K == g[0].K && g[i].split_force <= 1 &&
+           (g[i].ncols[1] == 0 || g[i].a_koff[0] == g[i].a_koff[1] || g[i].ncols[0] % (4 * kSkinnyBN) == 0);
+  }
+  if (wide) {
+    SkinnyBatch bw = b;
+    int wgw = 0;
+    for (int i = 0; i < n; ++i) {
+      bw.base[i] = wgw;
+      const int ngr = (b.ntn[i] + 3) / 4;
+      wgw += (grid_tiles[i] * ngr + NXCD - 1) / NXCD * NXCD;
+    }
+    bw.base[n] = wgw;
+    if (wgw <= 0) return hipSuccess;
+    if (g[0].K == 2 * BK2)
+      hipLaunchKernelGGL((k_gemm_skinny_wide<4, 2>), dim3(wgw), dim3(SK_THR), 0, s, bw);
+    else
+      hipLaunchKernelGGL((k_gemm_skinny_wide<4, 1>), dim3(wgw), dim3(SK_THR), 0, s, bw);
+    return hipGetLastError();
   }
   if (pair && max_steps > 4) {
     hipLaunchKernelGGL((k_gemm_skinny<3, 2>), dim3(wg), dim3(SK_THR), 0, s, b);
