@@ -22,6 +22,21 @@ notation: weights [out][in], A output-side, B input-side, W ~ W_dom + A B):
   Algorithm 4.4, with a Gaussian test matrix Omega [cols][r + p] passed in,
   p = 10 oversampling columns and q = 2 power iterations, each product
   re-orthonormalised (QR), then the SVD of the small matrix Q^T R.
+* (iii) the activation-weighted fit (Sec. 3 "Output-matching refinement",
+  its closed form in Sec. 6 "Calibration cost" and Sec. 7 "Hessian-weighted
+  fitting"): the rank-r (A, B) that minimise the error of the emitted
+  output on calibration activations X [n][cols] (rows = tokens),
+  ||(R - A B) X^T||_F^2 + damp ||R - A B||_F^2 (damp >= 0: the damping the
+  paper leaves unspecified, read as a ridge term). With G = X^T X + damp I =
+  L L^T, the objective is ||(R - A B) L||_F^2, so the optimum is the rank-r
+  truncation of R L: R L = U S V^T, A = U_r S_r^(1/2), B = S_r^(1/2) V_r^T
+  L^(-1) (weighted_factors_exact). The library's route to the same optimum
+  (weighted_factors): M = R X'^T with X' = [X; sqrt(damp) I] has M M^T =
+  R G R^T, so M and R L share left singular vectors and values; the
+  randomized solver above runs on M with a test matrix Omega [n (+ cols)]
+  [r + p], and B = S_r^(-1/2) U_r^T R (equal to the formula above, since
+  U_r^T R L = S_r V_r^T); rows of B (and columns of A) whose singular value
+  is 0 are 0.
 """
 from __future__ import annotations
 
@@ -81,3 +96,47 @@ def factors(R, omega, r: int, q: int = 2):
     U, s, Vt = randomized_svd(R, omega, r, q)
     h = np.sqrt(s)
     return U * h[None, :], h[:, None] * Vt, s
+
+
+def whitened_moment(X, damp: float = 0.0):
+    """G = X^T X + damp I for activations X [n][cols] (fp64)."""
+    X = np.asarray(X, np.float64)
+    return X.T @ X + damp * np.eye(X.shape[1])
+
+
+def weighted_factors_exact(R, X, r: int, damp: float = 0.0):
+    """(A [rows, r], B [r, cols], sigma [r]) minimising ||(R - A B) X^T||_F^2 +
+    damp ||R - A B||_F^2: whitening by G = L L^T, exact SVD of R L."""
+    L = np.linalg.cholesky(whitened_moment(X, damp))
+    U, s, Vt = np.linalg.svd(np.asarray(R, np.float64) @ L, full_matrices=False)
+    h = np.sqrt(s[:r])
+    A = U[:, :r] * h[None, :]
+    # B = S^(1/2) V_r^T L^(-1): solve L^T B^T = (S^(1/2) V_r^T)^T
+    B = np.linalg.solve(L.T, (h[:, None] * Vt[:r]).T).T
+    return A, B, s[:r]
+
+
+def weighted_objective(R, X, A, B, damp: float = 0.0) -> float:
+    """sqrt(||(R - A B) X^T||_F^2 + damp ||R - A B||_F^2)."""
+    E = np.asarray(R, np.float64) - np.asarray(A, np.float64) @ np.asarray(B, np.float64)
+    X = np.asarray(X, np.float64)
+    return float(np.sqrt(np.linalg.norm(E @ X.T) ** 2 + damp * np.linalg.norm(E) ** 2))
+
+
+def weighted_operator(R, X, damp: float = 0.0):
+    """M = R X'^T, X' = [X; sqrt(damp) I] ([rows][n (+ cols)])."""
+    X = np.asarray(X, np.float64)
+    if damp > 0:
+        X = np.vstack([X, np.sqrt(damp) * np.eye(X.shape[1])])
+    return np.asarray(R, np.float64) @ X.T
+
+
+def weighted_factors(R, X, omega, r: int, q: int = 2, damp: float = 0.0):
+    """The randomized route: subspace iteration on M = R X'^T with the
+    caller's test matrix omega [n (+ cols)][r + p]; A = U_r S^(1/2),
+    B = S^(-1/2) U_r^T R (zero where S is 0)."""
+    R = np.asarray(R, np.float64)
+    U, s, _ = randomized_svd(weighted_operator(R, X, damp), omega, r, q)
+    h = np.sqrt(s)
+    inv = np.where(h > 0, 1.0 / np.where(h > 0, h, 1.0), 0.0)
+    return U * h[None, :], inv[:, None] * (U.T @ R), s

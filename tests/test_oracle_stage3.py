@@ -75,3 +75,74 @@ def test_randomized_svd_exact_on_low_rank_and_close_to_truncated_svd():
     # symmetric split: A^T A = B B^T = diag(sigma)
     assert np.allclose(A2.T @ A2, np.diag(s2), atol=1e-10)
     assert np.allclose(B2 @ B2.T, np.diag(s2), atol=1e-10)
+
+
+def _decaying(rng, rows, cols, rate=0.7):
+    U0, _ = np.linalg.qr(rng.standard_normal((rows, min(rows, cols))))
+    V0, _ = np.linalg.qr(rng.standard_normal((cols, min(rows, cols))))
+    return (U0 * rate ** np.arange(min(rows, cols))) @ V0.T
+
+
+@pytest.mark.parametrize("damp", [0.0, 0.5])
+def test_weighted_fit_reaches_the_closed_form_optimum(damp):
+    """The fit's emitted error equals the Eckart-Young bound of R L (the tail
+    of its singular values), and no perturbation of (A, B) lowers it."""
+    rng = np.random.default_rng(5)
+    rows, cols, n, r = 30, 20, 60, 4
+    R = rng.standard_normal((rows, cols))
+    X = rng.standard_normal((n, cols)) * np.linspace(0.2, 3.0, cols)[None, :]
+    A, B, s = S.weighted_factors_exact(R, X, r, damp)
+    L = np.linalg.cholesky(X.T @ X + damp * np.eye(cols))
+    sv = np.linalg.svd(R @ L, compute_uv=False)
+    best = S.weighted_objective(R, X, A, B, damp)
+    assert best == pytest.approx(np.sqrt((sv[r:] ** 2).sum()), rel=1e-10)
+    assert np.allclose(s, sv[:r], rtol=1e-12)
+    for _ in range(20):
+        dA, dB = rng.standard_normal(A.shape) * 1e-3, rng.standard_normal(B.shape) * 1e-3
+        assert S.weighted_objective(R, X, A + dA, B + dB, damp) >= best * (1 - 1e-12)
+    # the plain (unweighted) truncation is worse in the weighted norm
+    U, sp, Vt = np.linalg.svd(R, full_matrices=False)
+    assert S.weighted_objective(R, X, U[:, :r] * sp[:r], Vt[:r], damp) > best * 1.001
+
+
+def test_weighted_fit_with_identity_activations_is_the_plain_truncation():
+    rng = np.random.default_rng(6)
+    R = rng.standard_normal((25, 18))
+    A, B, s = S.weighted_factors_exact(R, np.eye(18), 5)
+    U, sp, Vt = np.linalg.svd(R, full_matrices=False)
+    assert np.allclose(A @ B, (U[:, :5] * sp[:5]) @ Vt[:5], atol=1e-12)
+    assert np.allclose(s, sp[:5], rtol=1e-12)
+    # symmetric split: A^T A = diag(s) = B G B^T
+    assert np.allclose(A.T @ A, np.diag(s), atol=1e-10)
+    assert np.allclose(B @ B.T, np.diag(s), atol=1e-10)
+
+
+def test_weighted_fit_exact_on_low_rank_and_scale_invariant():
+    """A residual of rank r is fitted exactly; scaling X by c scales the
+    singular values by c and leaves A B unchanged."""
+    rng = np.random.default_rng(7)
+    rows, cols, n, r = 24, 16, 40, 3
+    R = rng.standard_normal((rows, r)) @ rng.standard_normal((r, cols))
+    X = rng.standard_normal((n, cols))
+    A, B, s = S.weighted_factors_exact(R, X, r)
+    assert np.linalg.norm(A @ B - R) <= 1e-10 * np.linalg.norm(R)
+    A2, B2, s2 = S.weighted_factors_exact(R, 3.0 * X, r)
+    assert np.allclose(s2, 3.0 * s, rtol=1e-10)
+    assert np.allclose(A2 @ B2, A @ B, atol=1e-10 * np.abs(R).max())
+
+
+@pytest.mark.parametrize("damp", [0.0, 2.0])
+def test_weighted_randomized_route_matches_whitening(damp):
+    """The operator route (randomized SVD of R X'^T, B = S^(-1/2) U^T R)
+    reaches the whitened SVD's factors on a fast-decaying weighted spectrum;
+    with damping the operator carries the extra sqrt(damp) I block."""
+    rng = np.random.default_rng(8)
+    rows, cols, n, r, p = 40, 30, 80, 6, 10
+    R = _decaying(rng, rows, cols, 0.5)
+    X = rng.standard_normal((n, cols))
+    A0, B0, s0 = S.weighted_factors_exact(R, X, r, damp)
+    om = rng.standard_normal((n + (cols if damp > 0 else 0), r + p))
+    A1, B1, s1 = S.weighted_factors(R, X, om, r, q=2, damp=damp)
+    assert np.allclose(s1, s0, rtol=1e-8)
+    assert np.linalg.norm(A1 @ B1 - A0 @ B0) <= 1e-8 * np.linalg.norm(A0 @ B0)
+    assert S.weighted_operator(R, X, damp).shape == (rows, om.shape[0])
