@@ -236,8 +236,9 @@ def bench_stage3(torch, np, lx, layer):
     """Stage 3 for one member at the layer's expert shape (d, f, rank r,
     oversampling 10, 2 power iterations): a dominant and a member that is the
     dominant plus rank-r corrections with its neurons shuffled, both bf16.
-    GPU: alignment cost, host assignment, factors of gate, up and down; the
-    oracle runs the same steps on the host."""
+    GPU: alignment cost, host assignment, factors of gate, up and down, and
+    the activation-weighted factors on calibration activations; the oracle
+    runs the same steps on the host."""
     from lxsynth import f32_to_bf16_bits
     from oracle import stage3 as S
     d, f, r, p = layer.d, layer.f, layer.levels[0].rank, 10
@@ -279,7 +280,34 @@ def bench_stage3(torch, np, lx, layer):
     for i in range(3):
         S.factors(S.aligned_residual(dom[i], mem[i], perm0, 1 if i == 2 else 0, "bf16"), oms[i], r, q=2)
     cpu_s = time.perf_counter() - t1
+    # activation-weighted fit of the same three projections on 4096
+    # calibration rows (bf16 Gaussian activations of each projection's input)
+    n_cal = 4096
+    xs = [bf(rng.standard_normal((n_cal, w.shape[1]))) for w in dom]
+    dxs = [dev(x) for x in xs]
+    woms = [rng.standard_normal((n_cal, r + p)) for _ in dom]
+    dwoms = [torch.from_numpy(o).cuda() for o in woms]
+
+    def weighted(pd_):
+        for i in range(3):
+            lx.weighted_factors(ddom[i], dmem[i], r, dxs[i], dwoms[i], q=2, perm=pd_, perm_axis=1 if i == 2 else 0)
+
+    weighted(pd)  # warm-up
+    torch.cuda.synchronize()
+    evw = [torch.cuda.Event(enable_timing=True) for _ in range(2)]
+    evw[0].record()
+    weighted(pd)
+    evw[1].record()
+    torch.cuda.synchronize()
+    t2 = time.perf_counter()
+    for i in range(3):
+        S.weighted_factors(S.aligned_residual(dom[i], mem[i], perm0, 1 if i == 2 else 0, "bf16"),
+                           S.to_f64(xs[i], "bf16"), woms[i], r, q=2)
+    cpu_w = time.perf_counter() - t2
     return dict(d=d, f=f, r=r, oversampling=p, power_iterations=2,
+                weighted_fit_calibration_rows=n_cal,
+                weighted_factors_3_projections_us=round(evw[0].elapsed_time(evw[1]) * 1e3, 1),
+                weighted_cpu_oracle_s=round(cpu_w, 2),
                 align_cost_us=round(ev[0].elapsed_time(ev[1]) * 1e3, 1),
                 align_cost_gflop=round(2 * f * f * 3 * d / 1e9, 2),
                 assign_host_ms=round(t_assign * 1e3, 2),

@@ -316,6 +316,37 @@ lx_status lx_lowrank_factors(const void* w_dom, const void* w_mem, lx_dtype dtyp
                              const double* omega, float* A, float* B, double* sigma, void* workspace,
                              size_t workspace_bytes, void* stream);
 
+/* Stage 3, activation-weighted factors (Sec. 3 "Output-matching
+ * refinement"; its closed form, whitening by the activation second moment
+ * and one SVD, in Secs. 6 "Calibration cost" and 7 "Hessian-weighted
+ * fitting"): the rank-r (A, B) minimising the error the member emits on
+ * calibration activations x [n][cols] (one token per row),
+ *   ||(R - A B) x^T||_F^2 + damp ||R - A B||_F^2,
+ * for the aligned residual R as in lx_lowrank_factors. With G = x^T x +
+ * damp I = L L^T the optimum is the rank-r truncation of R L = U S V^T:
+ * A = U_r S_r^(1/2) [rows][r], B = S_r^(1/2) V_r^T L^(-1) = S_r^(-1/2)
+ * U_r^T R [r][cols] fp32, sigma = S_r [r] fp64 (rows of B and columns of A
+ * with sigma = 0 are 0). damp >= 0 is a ridge term for experts that saw few
+ * tokens (with damp = 0 and x not of full column rank the optimum is not
+ * unique; this returns the one with B in the row space of U_r^T R).
+ * Solver: lx_lowrank_factors' randomized subspace iteration applied to the
+ * operator M = R x'^T, x' = [x; sqrt(damp) I] (M M^T = R G R^T: the left
+ * singular vectors and values of R L), with the caller's Gaussian test
+ * matrix omega [n'][r + p] fp64 (device), n' = n + (damp > 0 ? cols : 0).
+ *
+ * w_dom, w_mem [rows][cols] LX_BF16 or LX_F32 (device); x [n][cols] LX_BF16
+ * or LX_F32 (device, may be NULL when n = 0); r >= 1, p >= 0, n >= 0,
+ * 0 <= q <= 16, damp finite and >= 0 (LX_ERR_INVALID_ARGUMENT); r + p <=
+ * min(128, rows, cols, n'), rows * cols and n' * cols < 2^31
+ * (LX_ERR_UNSUPPORTED); workspace 256-byte aligned,
+ * lx_weighted_workspace_bytes(rows, cols, n, damp > 0, r, p) bytes (0 for
+ * an unsupported shape). Asynchronous on `stream`; deterministic. */
+size_t lx_weighted_workspace_bytes(int32_t rows, int32_t cols, int32_t n, int32_t damped, int32_t r, int32_t p);
+lx_status lx_weighted_factors(const void* w_dom, const void* w_mem, lx_dtype dtype, int32_t rows, int32_t cols,
+                              const int32_t* perm, int32_t perm_axis, const void* x, lx_dtype x_dtype, int32_t n,
+                              double damp, int32_t r, int32_t p, int32_t q, const double* omega, float* A, float* B,
+                              double* sigma, void* workspace, size_t workspace_bytes, void* stream);
+
 /* Routing bucketing alone (the first step of every forward), exposing the
  * arrays of one tree level `level` (0 = anchors, n_levels = experts):
  *   row_token   [T * min(k, N_level)] (only the first node_offsets[N] entries

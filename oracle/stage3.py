@@ -106,7 +106,8 @@ def whitened_moment(X, damp: float = 0.0):
 
 def weighted_factors_exact(R, X, r: int, damp: float = 0.0):
     """(A [rows, r], B [r, cols], sigma [r]) minimising ||(R - A B) X^T||_F^2 +
-    damp ||R - A B||_F^2: whitening by G = L L^T, exact SVD of R L."""
+    damp ||R - A B||_F^2: whitening by G = L L^T, exact SVD of R L. G must be
+    positive definite (damp > 0, or X of full column rank)."""
     L = np.linalg.cholesky(whitened_moment(X, damp))
     U, s, Vt = np.linalg.svd(np.asarray(R, np.float64) @ L, full_matrices=False)
     h = np.sqrt(s[:r])

@@ -15,6 +15,7 @@
 //   per level l >= 1       v = hbar_l * B_down^T, y_l = v * A_down^T
 //   combine                out[t] = sum of the token's rows over all levels
 #include <algorithm>
+#include <cmath>
 #include <deque>
 #include <map>
 #include <limits>
@@ -1108,6 +1109,44 @@ lx_status lx_lowrank_factors(const void* w_dom, const void* w_mem, lx_dtype dtyp
   hipStream_t lstream = (hipStream_t)stream;
   LX_LAUNCH("lowrank_factors", launch_lowrank(w_dom, w_mem, dtype == LX_BF16, rows, cols, perm, perm_axis, r, l, q,
                                               omega, A, B, sigma, (double*)workspace, lstream));
+  return LX_OK;
+}
+
+size_t lx_weighted_workspace_bytes(int32_t rows, int32_t cols, int32_t n, int32_t damped, int32_t r, int32_t p) {
+  const int l = r + p;
+  const int64_t np = (int64_t)n + (damped ? cols : 0);
+  if (rows < 1 || cols < 1 || n < 0 || r < 1 || p < 0 || l > 128 || l > rows || l > cols || np < l) return 0;
+  if ((int64_t)rows * cols >= ((int64_t)1 << 31) || np * cols >= ((int64_t)1 << 31)) return 0;
+  return weighted_ws_doubles(rows, cols, (int)np, l) * sizeof(double);
+}
+
+lx_status lx_weighted_factors(const void* w_dom, const void* w_mem, lx_dtype dtype, int32_t rows, int32_t cols,
+                              const int32_t* perm, int32_t perm_axis, const void* x, lx_dtype x_dtype, int32_t n,
+                              double damp, int32_t r, int32_t p, int32_t q, const double* omega, float* A, float* B,
+                              double* sigma, void* workspace, size_t workspace_bytes, void* stream) {
+  g_err.clear();
+  if ((dtype != LX_BF16 && dtype != LX_F32) || (x_dtype != LX_BF16 && x_dtype != LX_F32))
+    return fail(LX_ERR_INVALID_ARGUMENT, "bad dtype");
+  if (rows < 1 || cols < 1 || n < 0 || r < 1 || p < 0 || q < 0 || q > 16 || (perm_axis != 0 && perm_axis != 1) ||
+      !(damp >= 0.0) || !std::isfinite(damp))
+    return fail(LX_ERR_INVALID_ARGUMENT, "bad sizes, damp, q or perm_axis");
+  const int l = r + p;
+  const int64_t np = (int64_t)n + (damp > 0.0 ? cols : 0);
+  if (l > 128 || l > rows || l > cols || np < l)
+    return fail(LX_ERR_UNSUPPORTED, "r + p must be at most 128, rows, cols and the activation rows");
+  if ((int64_t)rows * cols >= ((int64_t)1 << 31) || np * cols >= ((int64_t)1 << 31))
+    return fail(LX_ERR_UNSUPPORTED, "rows * cols and activation rows * cols must be below 2^31");
+  const size_t es = dtype == LX_BF16 ? 2 : 4, xs = x_dtype == LX_BF16 ? 2 : 4;
+  if (!w_dom || !w_mem || !aligned(w_dom, es) || !aligned(w_mem, es) || (n > 0 && (!x || !aligned(x, xs))) ||
+      !omega || !aligned(omega, 8) || !A || !aligned(A, 4) || !B || !aligned(B, 4) || !sigma || !aligned(sigma, 8) ||
+      (perm && !aligned(perm, 4)) || !workspace || !aligned(workspace, 256))
+    return fail(LX_ERR_INVALID_ARGUMENT, "null or misaligned pointer");
+  if (workspace_bytes < lx_weighted_workspace_bytes(rows, cols, n, damp > 0.0 ? 1 : 0, r, p))
+    return fail(LX_ERR_WORKSPACE_TOO_SMALL, "workspace too small");
+  hipStream_t lstream = (hipStream_t)stream;
+  LX_LAUNCH("weighted_factors", launch_weighted(w_dom, w_mem, dtype == LX_BF16, rows, cols, perm, perm_axis, x,
+                                                x_dtype == LX_BF16, n, damp, r, l, q, omega, A, B, sigma,
+                                                (double*)workspace, lstream));
   return LX_OK;
 }
 

@@ -2,7 +2,14 @@
 // low-rank decomposition"), in fp64: the neuron-alignment cost matrix
 // (eq. cost), the aligned residual and its rank-r factors from a randomized
 // truncated SVD with the symmetric split (eqs. svd and factors). The exact
-// assignment between the two (eq. assign) runs on the host.
+// assignment between the two (eq. assign) runs on the host. Also the
+// activation-weighted fit of the factors (Sec. 3 "Output-matching
+// refinement", closed form in Secs. 6-7): minimising ||(R - A B) X^T||^2 +
+// damp ||R - A B||^2 over calibration activations X is the rank-r
+// truncation of R L (G = X^T X + damp I = L L^T); the same randomized solver
+// runs on the operator M = R Xp^T, Xp = [X; sqrt(damp) I], which has the
+// left singular vectors and values of R L (M M^T = R G R^T), and B =
+// sigma^(-1/2) U_r^T R, so no Cholesky factor of G or its inverse is formed.
 //
 //   * k_dgemm: C = alpha op(A) op(B) (+ C when accumulate), fp64, 64 x 64
 //     output tiles, 16-deep K slabs through LDS, 4 x 4 outputs per thread;
@@ -339,6 +346,19 @@ __global__ __launch_bounds__(256) void k_copy_f64(const double* __restrict__ x, 
   for (int i = threadIdx.x; i < n; i += blockDim.x) y[i] = x[i];
 }
 
+// Xp = [X; sqrt(damp) I]: rows i < n the activations X [n][cols] (bf16 or
+// fp32) in fp64, rows n .. np - 1 the scaled identity (np = n or n + cols).
+__global__ __launch_bounds__(256) void k_fill_act(const void* __restrict__ x, int bf16, int n, int cols, double sd,
+                                                  int np, double* __restrict__ Xp) {
+  const int64_t q = (int64_t)blockIdx.x * blockDim.x + threadIdx.x;
+  if (q >= (int64_t)np * cols) return;
+  const int i = (int)(q / cols), j = (int)(q % cols);
+  if (i < n)
+    Xp[q] = bf16 ? (double)__uint_as_float((uint32_t)((const uint16_t*)x)[q] << 16) : (double)((const float*)x)[q];
+  else
+    Xp[q] = j == i - n ? sd : 0.0;
+}
+
 __global__ __launch_bounds__(256) void k_to_f32(const double* __restrict__ x, int64_t n, float* __restrict__ y) {
   const int64_t q = (int64_t)blockIdx.x * blockDim.x + threadIdx.x;
   if (q < n) y[q] = (float)x[q];
@@ -401,12 +421,45 @@ hipError_t cholqr2(double* Y, int rows, int l, double* G, double* U, hipStream_t
   return hipSuccess;
 }
 
+// From an orthonormal sketch Y (rows x l) of the range of an operator M, T =
+// Y^T R (l x cols) and Gm = (Y^T M)(Y^T M)^T (l x l): the eigenpairs of Gm
+// (descending), sigma = the square roots of the r largest, A = Y Ut[:, :r]
+// sigma^(1/2) and B = sigma^(-1/2) Ut[:, :r]^T T (rows of B with sigma = 0
+// are 0); Bd (r x cols doubles) is scratch.
+hipError_t factors_from_sketch(int rows, int cols, int r, int l, const double* Y, const double* T, const double* Gm,
+                               double* V, double* lam, double* Ve, double* sig, double* Ad, double* Bd, float* A,
+                               float* B, double* sigma, hipStream_t s, double* part) {
+  const int lp = l + (l & 1);
+  if (lp <= 96)
+    hipLaunchKernelGGL(k_jacobi<true>, dim3(1), dim3(1024), 2 * (size_t)lp * lp * sizeof(double), s, Gm, l, lp, V, lam,
+                       Ve, 40);
+  else
+    hipLaunchKernelGGL(k_jacobi<false>, dim3(1), dim3(1024), (size_t)lp * lp * sizeof(double), s, Gm, l, lp, V, lam,
+                       Ve, 40);
+  hipLaunchKernelGGL(k_sqrt_vec, dim3(1), dim3(256), 0, s, lam, r, sig);
+  hipError_t e;
+  if ((e = dgemm(rows, r, l, 1.0, Y, l, 0, Ve, l, 0, Ad, r, s, part)) != hipSuccess) return e;
+  hipLaunchKernelGGL(k_scale, dim3(blocks((int64_t)rows * r)), dim3(256), 0, s, Ad, rows, r, sig, 1, 0);
+  hipLaunchKernelGGL(k_to_f32, dim3(blocks((int64_t)rows * r)), dim3(256), 0, s, Ad, (int64_t)rows * r, A);
+  if ((e = dgemm(r, cols, l, 1.0, Ve, l, 1, T, cols, 0, Bd, cols, s, part)) != hipSuccess) return e;
+  hipLaunchKernelGGL(k_scale, dim3(blocks((int64_t)r * cols)), dim3(256), 0, s, Bd, r, cols, sig, 0, 1);
+  hipLaunchKernelGGL(k_to_f32, dim3(blocks((int64_t)r * cols)), dim3(256), 0, s, Bd, (int64_t)r * cols, B);
+  hipLaunchKernelGGL(k_copy_f64, dim3(1), dim3(256), 0, s, sig, r, sigma);
+  return hipGetLastError();
+}
+
 }  // namespace
 
 size_t lowrank_ws_doubles(int rows, int cols, int l) {
   const int lp = l + (l & 1);
   return (size_t)rows * cols + (size_t)rows * l + (size_t)cols * l + (size_t)l * cols + 4 * (size_t)lp * lp + 2 * lp +
          (size_t)rows * l + (size_t)kDgParts;
+}
+
+size_t weighted_ws_doubles(int rows, int cols, int np, int l) {
+  const int lp = l + (l & 1);
+  return (size_t)rows * cols + (size_t)np * cols + (size_t)cols * l + (size_t)rows * l + (size_t)np * l +
+         (size_t)l * cols + (size_t)l * np + 4 * (size_t)lp * lp + 2 * lp + (size_t)rows * l + (size_t)kDgParts;
 }
 
 hipError_t launch_align_cost(const void* dg, const void* du, const void* dd, const void* mg, const void* mu,
@@ -453,26 +506,58 @@ hipError_t launch_lowrank(const void* wd, const void* wm, int bf16, int rows, in
     if ((e = dgemm(rows, l, cols, 1.0, R, cols, 0, Z, l, 0, Y, l, s, part)) != hipSuccess) return e;
     if ((e = cholqr2(Y, rows, l, G, U, s, part)) != hipSuccess) return e;
   }
-  // Bs = Y^T R (l x cols); M = Bs Bs^T (l x l) = Ut diag(lambda) Ut^T
+  // Bs = Y^T R (l x cols); Bs Bs^T (l x l) = Ut diag(lambda) Ut^T
   if ((e = dgemm(l, cols, rows, 1.0, Y, l, 1, R, cols, 0, Bs, cols, s, part)) != hipSuccess) return e;
   if ((e = dgemm(l, l, cols, 1.0, Bs, cols, 0, Bs, cols, 1, G, l, s, part)) != hipSuccess) return e;
-  if (lp <= 96)
-    hipLaunchKernelGGL(k_jacobi<true>, dim3(1), dim3(1024), 2 * (size_t)lp * lp * sizeof(double), s, G, l, lp, V, lam,
-                       Ve, 40);
-  else
-    hipLaunchKernelGGL(k_jacobi<false>, dim3(1), dim3(1024), (size_t)lp * lp * sizeof(double), s, G, l, lp, V, lam,
-                       Ve, 40);
-  hipLaunchKernelGGL(k_sqrt_vec, dim3(1), dim3(256), 0, s, lam, r, sig);
-  // A = Y Ut[:, :r] sigma^(1/2); B = sigma^(-1/2) Ut[:, :r]^T Bs
-  if ((e = dgemm(rows, r, l, 1.0, Y, l, 0, Ve, l, 0, Ad, r, s, part)) != hipSuccess) return e;
-  hipLaunchKernelGGL(k_scale, dim3(blocks((int64_t)rows * r)), dim3(256), 0, s, Ad, rows, r, sig, 1, 0);
-  hipLaunchKernelGGL(k_to_f32, dim3(blocks((int64_t)rows * r)), dim3(256), 0, s, Ad, (int64_t)rows * r, A);
-  double* const Bd = Z;  // r x cols (Z is cols x l, l >= r)
-  if ((e = dgemm(r, cols, l, 1.0, Ve, l, 1, Bs, cols, 0, Bd, cols, s, part)) != hipSuccess) return e;
-  hipLaunchKernelGGL(k_scale, dim3(blocks((int64_t)r * cols)), dim3(256), 0, s, Bd, r, cols, sig, 0, 1);
-  hipLaunchKernelGGL(k_to_f32, dim3(blocks((int64_t)r * cols)), dim3(256), 0, s, Bd, (int64_t)r * cols, B);
-  hipLaunchKernelGGL(k_copy_f64, dim3(1), dim3(256), 0, s, sig, r, sigma);
-  return hipGetLastError();
+  return factors_from_sketch(rows, cols, r, l, Y, Bs, G, V, lam, Ve, sig, Ad, Z, A, B, sigma, s, part);
+}
+
+hipError_t launch_weighted(const void* wd, const void* wm, int bf16, int rows, int cols, const int32_t* perm, int axis,
+                           const void* x, int x_bf16, int n, double damp, int r, int l, int q, const double* omega,
+                           float* A, float* B, double* sigma, double* ws, hipStream_t s) {
+  const int lp = l + (l & 1);
+  const int np = n + (damp > 0.0 ? cols : 0);
+  if (const hipError_t e0 = allow_lds(); e0 != hipSuccess) return e0;
+  double* const R = ws;                              // rows x cols
+  double* const Xp = R + (size_t)rows * cols;        // np x cols: [X; sqrt(damp) I]
+  double* const P = Xp + (size_t)np * cols;          // cols x l
+  double* const Y = P + (size_t)cols * l;            // rows x l
+  double* const Z = Y + (size_t)rows * l;            // np x l
+  double* const T = Z + (size_t)np * l;              // l x cols
+  double* const Wt = T + (size_t)l * cols;           // l x np
+  double* const G = Wt + (size_t)l * np;             // lp x lp (four of them)
+  double* const U = G + (size_t)lp * lp;
+  double* const V = U + (size_t)lp * lp;
+  double* const Ve = V + (size_t)lp * lp;
+  double* const lam = Ve + (size_t)lp * lp;          // lp
+  double* const sig = lam + lp;                      // lp
+  double* const Ad = sig + lp;                       // rows x l
+  double* const part = Ad + (size_t)rows * l;        // kDgParts
+  hipLaunchKernelGGL(k_residual, dim3(blocks((int64_t)rows * cols)), dim3(256), 0, s, wd, wm, bf16, rows, cols, perm,
+                     axis, R);
+  hipLaunchKernelGGL(k_fill_act, dim3(blocks((int64_t)np * cols)), dim3(256), 0, s, x, x_bf16, n, cols, sqrt(damp),
+                     np, Xp);
+  hipError_t e;
+  // The operator M = R Xp^T (rows x np), applied as two thin products:
+  // Y = R (Xp^T Omega), orthonormalised; q rounds of Z = Xp (R^T Y) and
+  // Y = R (Xp^T Z), each orthonormalised
+  if ((e = dgemm(cols, l, np, 1.0, Xp, cols, 1, omega, l, 0, P, l, s, part)) != hipSuccess) return e;
+  if ((e = dgemm(rows, l, cols, 1.0, R, cols, 0, P, l, 0, Y, l, s, part)) != hipSuccess) return e;
+  if ((e = cholqr2(Y, rows, l, G, U, s, part)) != hipSuccess) return e;
+  for (int it = 0; it < q; ++it) {
+    if ((e = dgemm(cols, l, rows, 1.0, R, cols, 1, Y, l, 0, P, l, s, part)) != hipSuccess) return e;
+    if ((e = dgemm(np, l, cols, 1.0, Xp, cols, 0, P, l, 0, Z, l, s, part)) != hipSuccess) return e;
+    if ((e = cholqr2(Z, np, l, G, U, s, part)) != hipSuccess) return e;
+    if ((e = dgemm(cols, l, np, 1.0, Xp, cols, 1, Z, l, 0, P, l, s, part)) != hipSuccess) return e;
+    if ((e = dgemm(rows, l, cols, 1.0, R, cols, 0, P, l, 0, Y, l, s, part)) != hipSuccess) return e;
+    if ((e = cholqr2(Y, rows, l, G, U, s, part)) != hipSuccess) return e;
+  }
+  // T = Y^T R (l x cols); Wt = Y^T M = T Xp^T (l x np); Wt Wt^T = Ut diag(lambda) Ut^T.
+  // B = sigma^(-1/2) Ut^T T is sigma^(-1/2) U_r^T R with U_r = Y Ut[:, :r].
+  if ((e = dgemm(l, cols, rows, 1.0, Y, l, 1, R, cols, 0, T, cols, s, part)) != hipSuccess) return e;
+  if ((e = dgemm(l, np, cols, 1.0, T, cols, 0, Xp, cols, 1, Wt, np, s, part)) != hipSuccess) return e;
+  if ((e = dgemm(l, l, np, 1.0, Wt, np, 0, Wt, np, 1, G, l, s, part)) != hipSuccess) return e;
+  return factors_from_sketch(rows, cols, r, l, Y, T, G, V, lam, Ve, sig, Ad, P, A, B, sigma, s, part);
 }
 
 }  // namespace lx

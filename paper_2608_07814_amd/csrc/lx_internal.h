@@ -306,6 +306,12 @@ hipError_t launch_kmedoids(const double* dist, const uint32_t* fire, int E, int 
 hipError_t launch_align_cost(const void* dg, const void* du, const void* dd, const void* mg, const void* mu,
                              const void* md, int bf16, int f, int d, double* cost, double* ws, hipStream_t s);
 size_t lowrank_ws_doubles(int rows, int cols, int l);
+// activation-weighted fit: the same randomized solver on M = R Xp^T, Xp =
+// [X; sqrt(damp) I] with np = n (+ cols when damp > 0) rows
+size_t weighted_ws_doubles(int rows, int cols, int np, int l);
+hipError_t launch_weighted(const void* wd, const void* wm, int bf16, int rows, int cols, const int32_t* perm, int axis,
+                           const void* x, int x_bf16, int n, double damp, int r, int l, int q, const double* omega,
+                           float* A, float* B, double* sigma, double* ws, hipStream_t s);
 hipError_t launch_lowrank(const void* wd, const void* wm, int bf16, int rows, int cols, const int32_t* perm, int axis,
                           int r, int l, int q, const double* omega, float* A, float* B, double* sigma, double* ws,
                           hipStream_t s);

@@ -86,6 +86,10 @@ EXPORTS = {
     "lx_lowrank_workspace_bytes": (ctypes.c_size_t, [_c_i32, _c_i32, _c_i32, _c_i32]),
     "lx_lowrank_factors": (_c_i32, [_c_void, _c_void, _c_i32, _c_i32, _c_i32, _c_void, _c_i32, _c_i32, _c_i32,
                                     _c_i32, _c_void, _c_void, _c_void, _c_void, _c_void, ctypes.c_size_t, _c_void]),
+    "lx_weighted_workspace_bytes": (ctypes.c_size_t, [_c_i32] * 6),
+    "lx_weighted_factors": (_c_i32, [_c_void, _c_void, _c_i32, _c_i32, _c_i32, _c_void, _c_i32, _c_void, _c_i32,
+                                     _c_i32, ctypes.c_double, _c_i32, _c_i32, _c_i32, _c_void, _c_void, _c_void,
+                                     _c_void, _c_void, ctypes.c_size_t, _c_void]),
     "lx_route_topk": (_c_i32, [_c_void, _c_void, _c_i32, _c_i32, _c_i32, _c_i32, _c_i32, _c_void, _c_void,
                                _c_void, ctypes.c_size_t, _c_void]),
     "lx_profile_enable": (_c_i32, [_c_i32]),
@@ -363,6 +367,39 @@ def lowrank_factors(w_dom: torch.Tensor, w_mem: torch.Tensor, r: int, omega: tor
     _check(lib().lx_lowrank_factors(_ptr(w_dom), _ptr(w_mem), dt, rows, cols, _ptr(perm) if perm is not None else None,
                                     perm_axis, r, p, q, _ptr(omega), _ptr(A), _ptr(B), _ptr(sig), _ptr(ws), n,
                                     _stream(stream)))
+    return A, B, sig
+
+
+def weighted_factors(w_dom: torch.Tensor, w_mem: torch.Tensor, r: int, x: torch.Tensor, omega: torch.Tensor,
+                     q: int = 2, damp: float = 0.0, perm: Optional[torch.Tensor] = None, perm_axis: int = 0,
+                     stream=None):
+    """Activation-weighted rank-r factors of the aligned residual on
+    calibration activations x [n][cols] (lx_weighted_factors) ->
+    (A fp32 [rows][r], B fp32 [r][cols], sigma fp64 [r]); omega fp64
+    [n (+ cols when damp > 0)][r + p]."""
+    rows, cols = (int(v) for v in w_dom.shape)
+    n = int(x.shape[0])
+    if x.dim() != 2 or int(x.shape[1]) != cols or not x.is_contiguous() or x.dtype not in (torch.bfloat16,
+                                                                                           torch.float32):
+        raise ValueError("x must be a contiguous bf16 or fp32 [n][cols] tensor")
+    np_rows = n + (cols if damp > 0 else 0)
+    p = int(omega.shape[1]) - r
+    if omega.dtype != torch.float64 or not omega.is_contiguous() or int(omega.shape[0]) != np_rows:
+        raise ValueError("omega must be a contiguous fp64 [n (+ cols when damp > 0)][r + p] tensor")
+    dt = LX_BF16 if w_dom.dtype == torch.bfloat16 else LX_F32
+    xdt = LX_BF16 if x.dtype == torch.bfloat16 else LX_F32
+    dev = w_dom.device
+    A = torch.empty(rows, r, dtype=torch.float32, device=dev)
+    B = torch.empty(r, cols, dtype=torch.float32, device=dev)
+    sig = torch.empty(r, dtype=torch.float64, device=dev)
+    nb = int(lib().lx_weighted_workspace_bytes(rows, cols, n, 1 if damp > 0 else 0, r, p))
+    if nb == 0:
+        raise LorexError("unsupported shape for lx_weighted_factors")
+    ws = torch.empty(nb, dtype=torch.uint8, device=dev)
+    _check(lib().lx_weighted_factors(_ptr(w_dom), _ptr(w_mem), dt, rows, cols,
+                                     _ptr(perm) if perm is not None else None, perm_axis, _ptr(x), xdt, n,
+                                     float(damp), r, p, q, _ptr(omega), _ptr(A), _ptr(B), _ptr(sig), _ptr(ws), nb,
+                                     _stream(stream)))
     return A, B, sig
 
 

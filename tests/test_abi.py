@@ -28,7 +28,7 @@ def _declared(root):
 
 def test_every_declared_symbol_is_exported(L, root):
     names = _declared(root)
-    assert len(names) == len(lx.EXPORTS) == 26
+    assert len(names) == len(lx.EXPORTS) == 28
     for n in names:
         assert hasattr(L, n), n
         assert n in lx.EXPORTS, n
@@ -232,3 +232,33 @@ def test_stage3_validation(L):
     assert call(ax=2) == lx.LX_ERR_INVALID_ARGUMENT
     assert call(n=n - 1) == lx.LX_ERR_WORKSPACE_TOO_SMALL
     assert call(perm=FAKE + 2) == lx.LX_ERR_INVALID_ARGUMENT
+
+
+def test_weighted_fit_validation(L):
+    """Host-side checks of lx_weighted_factors (no kernel is launched)."""
+    ws = L.lx_weighted_workspace_bytes
+    assert ws(768, 2048, 512, 0, 120, 10) == 0                  # r + p > 128
+    assert ws(768, 2048, 40, 0, 64, 10) == 0                    # r + p > activation rows
+    assert ws(768, 2048, 40, 1, 64, 10) > 0                     # damping adds cols rows
+    assert ws(768, 2048, 4096, 1, 64, 10) > ws(768, 2048, 4096, 0, 64, 10)
+    n = ws(768, 2048, 512, 0, 64, 10)
+    base = dict(t=lx.LX_BF16, xt=lx.LX_BF16, rows=768, cols=2048, n_act=512, damp=0.0, r=64, p=10, q=2, n=n,
+                x=FAKE, ax=0)
+
+    def call(**kw):
+        a = dict(base, **kw)
+        return L.lx_weighted_factors(FAKE, FAKE, a["t"], a["rows"], a["cols"], None, a["ax"], a["x"], a["xt"],
+                                     a["n_act"], a["damp"], a["r"], a["p"], a["q"], FAKE, FAKE, FAKE, FAKE, FAKE,
+                                     a["n"], None)
+    assert call(damp=-1.0) == lx.LX_ERR_INVALID_ARGUMENT
+    assert call(damp=float("nan")) == lx.LX_ERR_INVALID_ARGUMENT
+    assert call(damp=float("inf")) == lx.LX_ERR_INVALID_ARGUMENT
+    assert call(xt=7) == lx.LX_ERR_INVALID_ARGUMENT
+    assert call(n_act=-1) == lx.LX_ERR_INVALID_ARGUMENT
+    assert call(n_act=40) == lx.LX_ERR_UNSUPPORTED                 # r + p > n'
+    assert call(x=None) == lx.LX_ERR_INVALID_ARGUMENT
+    assert call(x=FAKE + 1) == lx.LX_ERR_INVALID_ARGUMENT          # misaligned bf16
+    assert call(ax=3) == lx.LX_ERR_INVALID_ARGUMENT
+    assert call(n=n - 1) == lx.LX_ERR_WORKSPACE_TOO_SMALL
+    # damping: the same call needs the larger workspace
+    assert call(damp=0.1) == lx.LX_ERR_WORKSPACE_TOO_SMALL

@@ -105,3 +105,65 @@ def test_factors_full_rank_residual_and_no_permutation():
     A, B, sig = lx.lowrank_factors(torch.from_numpy(wd).cuda(), torch.from_numpy(wd).cuda(), r,
                                    torch.from_numpy(om).cuda(), q=0)
     assert float(sig.abs().max()) == 0.0 and float(A.abs().max()) == 0.0 and float(B.abs().max()) == 0.0
+
+
+def _weighted_case(rng, rows, cols, n, r, noise=0.02):
+    """A residual of rank r plus noise (dominant and member as bf16) and
+    calibration activations with unequal column scales."""
+    wd = rng.standard_normal((rows, cols)) / np.sqrt(cols)
+    corr = (rng.standard_normal((rows, r)) @ rng.standard_normal((r, cols))) * (0.3 / np.sqrt(r * cols))
+    wm = wd + corr + rng.standard_normal((rows, cols)) * (noise / np.sqrt(cols))
+    x = rng.standard_normal((n, cols)) * np.exp(rng.standard_normal(cols) * 0.5)[None, :]
+    return _bf(wd), _bf(wm), x.astype(np.float32)
+
+
+@pytest.mark.parametrize("rows,cols,n,damp,xdt", [(768, 2048, 1024, 0.0, "bf16"), (768, 2048, 1024, 4.0, "f32"),
+                                                  (200, 130, 300, 0.0, "f32")])
+def test_weighted_factors_vs_oracle(rows, cols, n, damp, xdt):
+    """Same caller-drawn test matrix on both sides: the GPU's factors equal
+    the oracle's randomized route, and their emitted error is within 1% of
+    the whitened SVD's optimum."""
+    require_gpu()
+    say(f"weighted fit rows={rows} cols={cols} n={n} damp={damp} x={xdt}")
+    rng = np.random.default_rng(rows + n)
+    r, p = 32, 10
+    wd, wm, x = _weighted_case(rng, rows, cols, n, r)
+    xb = _bf(x) if xdt == "bf16" else x
+    xd = _dev(xb) if xdt == "bf16" else torch.from_numpy(x).cuda()
+    xo = to_f64(xb, "bf16") if xdt == "bf16" else x.astype(np.float64)
+    om = rng.standard_normal((n + (cols if damp > 0 else 0), r + p))
+    A, B, sig = lx.weighted_factors(_dev(wd), _dev(wm), r, xd, torch.from_numpy(om).cuda(), q=2, damp=damp)
+    A, B, sig = A.cpu().numpy().astype(np.float64), B.cpu().numpy().astype(np.float64), sig.cpu().numpy()
+    R = to_f64(wm, "bf16") - to_f64(wd, "bf16")
+    A0, B0, s0 = S.weighted_factors(R, xo, om, r, q=2, damp=damp)
+    e_ab, e_s = _rel(A @ B, A0 @ B0), float(np.max(np.abs(sig - s0) / s0))
+    # the optimum: the Eckart-Young tail of the operator (R L when G is
+    # positive definite; also defined for n < cols without damping)
+    sv = np.linalg.svd(S.weighted_operator(R, xo, damp), compute_uv=False)
+    opt = float(np.sqrt((sv[r:] ** 2).sum()))
+    got = S.weighted_objective(R, xo, A, B, damp)
+    U, sp, Vt = np.linalg.svd(R, full_matrices=False)
+    plain = S.weighted_objective(R, xo, U[:, :r] * sp[:r], Vt[:r], damp)
+    say(f"  |AB - AB_oracle| / |AB_oracle| = {e_ab:.2e}, sigma rel {e_s:.2e}; emitted error {got:.4e} "
+        f"(optimum {opt:.4e}, plain SVD {plain:.4e})")
+    assert e_ab <= 1e-5 and e_s <= 1e-9
+    assert got <= 1.01 * opt
+
+
+def test_weighted_factors_pure_damping_is_the_plain_fit():
+    """No activations and damp > 0: G = damp I, so the weighted fit is the
+    plain one with sigma scaled by sqrt(damp) and the same product A B
+    (same test matrix for both entry points); also with a permutation."""
+    require_gpu()
+    say("weighted fit, damping only")
+    rng = np.random.default_rng(17)
+    rows, cols, r, p, damp = 300, 256, 24, 8, 2.25
+    wd, wm, _ = _weighted_case(rng, rows, cols, 1, r)
+    perm = torch.from_numpy(rng.permutation(rows).astype(np.int32)).cuda()
+    om = torch.from_numpy(rng.standard_normal((cols, r + p))).cuda()
+    x0 = torch.empty(0, cols, dtype=torch.float32, device="cuda")
+    Aw, Bw, sw = lx.weighted_factors(_dev(wd), _dev(wm), r, x0, om, q=2, damp=damp, perm=perm, perm_axis=0)
+    Ap, Bp, sp = lx.lowrank_factors(_dev(wd), _dev(wm), r, om, q=2, perm=perm, perm_axis=0)
+    Aw, Bw, Ap, Bp = (t.cpu().numpy().astype(np.float64) for t in (Aw, Bw, Ap, Bp))
+    assert np.allclose(sw.cpu().numpy(), np.sqrt(damp) * sp.cpu().numpy(), rtol=1e-10)
+    assert _rel(Aw @ Bw, Ap @ Bp) <= 1e-5
