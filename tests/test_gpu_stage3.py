@@ -132,9 +132,13 @@ def test_weighted_factors_vs_oracle(rows, cols, n, damp, xdt):
     xd = _dev(xb) if xdt == "bf16" else torch.from_numpy(x).cuda()
     xo = to_f64(xb, "bf16") if xdt == "bf16" else x.astype(np.float64)
     om = rng.standard_normal((n + (cols if damp > 0 else 0), r + p))
-    A, B, sig = lx.weighted_factors(_dev(wd), _dev(wm), r, xd, torch.from_numpy(om).cuda(), q=2, damp=damp)
+    # the small shape also aligns the member's columns by a permutation
+    perm = rng.permutation(cols).astype(np.int32) if cols < 1000 else None
+    A, B, sig = lx.weighted_factors(_dev(wd), _dev(wm), r, xd, torch.from_numpy(om).cuda(), q=2, damp=damp,
+                                    perm=torch.from_numpy(perm).cuda() if perm is not None else None, perm_axis=1)
     A, B, sig = A.cpu().numpy().astype(np.float64), B.cpu().numpy().astype(np.float64), sig.cpu().numpy()
-    R = to_f64(wm, "bf16") - to_f64(wd, "bf16")
+    R = (S.aligned_residual(wd, wm, perm, 1, "bf16") if perm is not None
+         else to_f64(wm, "bf16") - to_f64(wd, "bf16"))
     A0, B0, s0 = S.weighted_factors(R, xo, om, r, q=2, damp=damp)
     e_ab, e_s = _rel(A @ B, A0 @ B0), float(np.max(np.abs(sig - s0) / s0))
     # the optimum: the Eckart-Young tail of the operator (R L when G is
