@@ -142,9 +142,10 @@ Plan make_plan(const lx_tree_layer& t, int T, int k) {
     for (int l = 1; l <= p.L; ++l) {
       const int r = t.levels[l - 1].rank;
       const int64_t R = (int64_t)T * std::min(k, t.levels[l - 1].n_nodes);
-      // rank multiple of 64: every 64-wide K-slab of a (hi | lo) operand lies
-      // inside one half, so its weight columns stay inside the weight row
-      p.fast[l] = p.fast[0] && r % 64 == 0 && R * 2 * p.f < two31 && R * 4 * r < two31;
+      // rank multiple of 32: the (hi | lo) operands of K = 2r are whole 64-wide
+      // K-slabs (a slab may cross from the hi to the lo half; the large-tile
+      // kernel then takes its weight columns modulo r)
+      p.fast[l] = p.fast[0] && r % 32 == 0 && R * 2 * p.f < two31 && R * 4 * r < two31;
     }
     // Fast levels with few rows per node (decode-sized batches) stream their
     // weights through the skinny kernel; the large tiles would spend their
@@ -153,7 +154,9 @@ Plan make_plan(const lx_tree_layer& t, int T, int k) {
     for (int l = 0; l <= p.L; ++l) {
       const int N = level_nodes(t, l);
       const int64_t R = (int64_t)T * std::min(k, N);
-      p.skinny[l] = p.fast[l] && R / std::max(N, 1) <= 64;
+      // (the skinny kernel's hi and lo halves share whole weight slabs: rank
+      // a multiple of 64)
+      p.skinny[l] = p.fast[l] && R / std::max(N, 1) <= 64 && (l == 0 || t.levels[l - 1].rank % 64 == 0);
       const bool work = l == 0 || t.levels[l - 1].n_factors > 0;
       if (work && !p.skinny[l]) p.batch = false;
     }
@@ -500,7 +503,7 @@ lx_status run(const lx_tree_layer& t, int T, int k, const void* x, const int32_t
     const LevelPlan& q = P.lv[l];
     if (!g.B[1]) g.B[1] = g.B[0];
     if (skinny[l]) {
-      if (!gemm_big_ok(g, kSkinnyBN, a_rows_total))
+      if (!gemm_big_ok(g, kSkinnyBN, a_rows_total) || (g.Kb > 0 ? g.Kb : g.K) % 64)
         return fail(LX_ERR_UNSUPPORTED, std::string(name) + ": shape not supported by the skinny GEMM");
       g.tiles = ba.lv[l].tiles[kTabSkinny];
       g.n_tiles = ba.lv[l].n_tiles[kTabSkinny];

@@ -236,14 +236,32 @@ void k_gemm_big(GemmArgs p, int ntn) {
     // per of weight slab q, so the periods that reuse one weight slab (hi and
     // lo halves) run back to back and the second read hits in cache.
     const int nper = K / Kb;
+    // A period Kb that is a multiple of 8 but not of 64 (ranks 32 and 96 on
+    // their (hi | lo) operands): slabs in plain K order (A columns
+    // [64 kt, 64 kt + 64)), each 8-column chunk of a slab taking its weight
+    // columns modulo Kb, so a slab that crosses from the hi to the lo half
+    // reads the end and then the start of the weight row.
+    const bool wrap = (Kb % BK2) != 0;
 #define LX_ISSUE(SA_, SB_, KT)                                                      \
   do {                                                                              \
-    const int q_ = (KT) / nper, per_ = (KT) - q_ * nper;                            \
-    const int kb_ = q_ * BK2, ka_ = per_ * Kb + kb_;                                \
-    _Pragma("unroll") for (int j = 0; j < A_ROUNDS; ++j)                            \
-        load_lds16(Ab + (aoff[j] + (uint32_t)ka_), &(SA_)[(j * NTHR + wave * 64) * 8]);  \
-    _Pragma("unroll") for (int j = 0; j < B_ROUNDS; ++j)                            \
-        load_lds16(bptr[j] + kb_, &(SB_)[(j * NTHR + wave * 64) * 8]);              \
+    if (!wrap) {                                                                    \
+      const int q_ = (KT) / nper, per_ = (KT) - q_ * nper;                          \
+      const int kb_ = q_ * BK2, ka_ = per_ * Kb + kb_;                              \
+      _Pragma("unroll") for (int j = 0; j < A_ROUNDS; ++j)                          \
+          load_lds16(Ab + (aoff[j] + (uint32_t)ka_), &(SA_)[(j * NTHR + wave * 64) * 8]);  \
+      _Pragma("unroll") for (int j = 0; j < B_ROUNDS; ++j)                          \
+          load_lds16(bptr[j] + kb_, &(SB_)[(j * NTHR + wave * 64) * 8]);            \
+    } else {                                                                        \
+      const int ka_ = (KT) * BK2, k0_ = ka_ % Kb;                                   \
+      _Pragma("unroll") for (int j = 0; j < A_ROUNDS; ++j)                          \
+          load_lds16(Ab + (aoff[j] + (uint32_t)ka_), &(SA_)[(j * NTHR + wave * 64) * 8]);  \
+      _Pragma("unroll") for (int j = 0; j < B_ROUNDS; ++j) {                        \
+        const int ps_ = j * NTHR + tid, row_ = ps_ >> 3;                            \
+        const int c8_ = (((ps_ & 7) ^ swzb(row_)) << 3);                            \
+        const int w_ = k0_ + c8_ >= Kb ? k0_ - Kb : k0_;                            \
+        load_lds16(bptr[j] + w_, &(SB_)[(j * NTHR + wave * 64) * 8]);               \
+      }                                                                             \
+    }                                                                               \
   } while (0)
 
     f32x16 acc[MI][NI];
@@ -994,8 +1012,9 @@ hipError_t launch_quantize_f8(const void* w, int64_t n_rows, int cols, uint8_t* 
 
 bool gemm_big_ok(const GemmArgs& g, int bn, int64_t a_rows_total) {
   const int Kb = g.Kb > 0 ? g.Kb : g.K;
-  // every 64-wide K-slab must map to 64 consecutive weight columns of a row
-  if (g.K <= 0 || g.K % BK2 || Kb % BK2 || g.K % Kb) return false;
+  // 64-wide K-slabs; a period Kb < K that is not a multiple of 64 is taken
+  // chunk by chunk (large-tile kernel only, 8-column chunks)
+  if (g.K <= 0 || g.K % BK2 || Kb % 8 || g.K % Kb || (Kb % BK2 && Kb == g.K)) return false;
   if (g.a_koff[0] + g.K > g.lda || (g.ncols[1] > 0 && g.a_koff[1] + g.K > g.lda)) return false;
   if (g.ncols[1] > 0 && g.a_koff[0] != g.a_koff[1] && g.ncols[0] % bn) return false;
   // the epilogue stores 4 consecutive columns per lane

@@ -9,7 +9,7 @@ import numpy as np
 import pytest
 import torch
 
-from lxsynth import make_problem, make_layer_flat
+from lxsynth import config, make_problem, make_layer_flat
 from oracle import moe as O
 from paper_2608_07814_amd import lorex as lx
 from gpu_util import (TOL_BF16, TOL_F32, TOL_DESIGN, require_gpu, say, gpu_forward, err_ratio, sample_tokens,
@@ -105,6 +105,22 @@ def test_cfg3_full_size_sampled():
     say(f"  err/RMS = {e:.3e}")
     assert e <= TOL_BF16
     assert e <= TOL_DESIGN
+
+
+@pytest.mark.parametrize("cfg,over,T", [(3, {"d": 512, "f": 256}, 40), (1, {"r": 32}, 600),
+                                          (1, {"r": 96, "d": 512, "f": 320}, 900),
+                                          (3, {"r": 160, "d": 512, "f": 256}, 200)])
+def test_rank_not_multiple_of_64(cfg, over, T):
+    """Ranks 32, 96 and 160 on the bf16 (hi, lo) path: the low-rank output
+    products' 64-wide K-slabs cross from the hi to the lo half of their
+    operand (weight columns taken modulo r); small batches of such levels
+    stay on the large-tile kernel."""
+    require_gpu()
+    say(f"rank {over.get('r', 96)} cfg{cfg} {over} T={T}")
+    p = make_problem(config(cfg, **over), seed=5 + T)
+    e = err_ratio(gpu_forward(p), _oracle(p))
+    say(f"  err/RMS = {e:.3e}")
+    assert e <= TOL_BF16 and e <= TOL_DESIGN
 
 
 def test_cfg4_tree_small():
