@@ -417,23 +417,25 @@ def main():
                       rows_per_level=rows, nodes_touched=touched)
 
     dense = None
-    if not a.no_dense and kind == "flat":
-        # uncompressed comparator: every expert dom + A B rounded to bf16 (setup, untimed)
-        lv = dl.levels[0]
-        cl = lv.parent.long()
-        fo = lv.factor_of.long()
-        wg = dl.anchor_gate[cl].float()
-        wu = dl.anchor_up[cl].float()
-        wd = dl.anchor_down[cl].float()
-        m = fo >= 0
-        fi = fo[m]
-        wg[m] += torch.bmm(lv.a_gate[fi].float(), lv.b_gate[fi].float())
-        wu[m] += torch.bmm(lv.a_up[fi].float(), lv.b_up[fi].float())
-        wd[m] += torch.bmm(lv.a_down[fi].float(), lv.b_down[fi].float())
+    if not a.no_dense and kind in ("flat", "tree"):
+        # uncompressed comparator: every expert = its anchor + the A B of every
+        # factor-carrying node on its path, rounded to bf16 (setup, untimed)
+        def reconstruct(anchor, an, bn):
+            wt = anchor.float()
+            for lv in dl.levels:
+                wt = wt[lv.parent.long()]
+                fo = lv.factor_of.long()
+                m = fo >= 0
+                if bool(m.any()):
+                    fi = fo[m]
+                    wt[m] += torch.bmm(getattr(lv, an)[fi].float(), getattr(lv, bn)[fi].float())
+            return wt.bfloat16().contiguous()
+
         dd = lx.DeviceLayer(E=layer.E, d=layer.d, f=layer.f, dtype="bf16",
-                            anchor_gate=wg.bfloat16().contiguous(), anchor_up=wu.bfloat16().contiguous(),
-                            anchor_down=wd.bfloat16().contiguous(), levels=[])
-        del wg, wu, wd
+                            anchor_gate=reconstruct(dl.anchor_gate, "a_gate", "b_gate"),
+                            anchor_up=reconstruct(dl.anchor_up, "a_up", "b_up"),
+                            anchor_down=reconstruct(dl.anchor_down, "a_down", "b_down"), levels=[])
+        torch.cuda.empty_cache()
         if not a.no_lo8:
             dd = lx.attach_down_f8(dd)
         wsd = lx.alloc_workspace(dd, T, k, "dense")
