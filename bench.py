@@ -319,7 +319,7 @@ def bench_stage3(torch, np, lx, layer):
 def main():
     a = parse()
     if a.gpus != 1:
-        print(f"bench.py runs on one GPU only (asked for --gpus {a.gpus}); this build has no "
+        print(f"bench.py runs on one GPU only (asked for --gpus {a.gpus}); this implementation has no "
               "multi-GPU path.", file=sys.stderr)
         sys.exit(2)
     import numpy as np

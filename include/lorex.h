@@ -316,11 +316,11 @@ lx_status lx_lowrank_factors(const void* w_dom, const void* w_mem, lx_dtype dtyp
                              const double* omega, float* A, float* B, double* sigma, void* workspace,
                              size_t workspace_bytes, void* stream);
 
-/* Stage 3, activation-weighted factors (Sec. 3 "Output-matching
- * refinement"; its closed form, whitening by the activation second moment
- * and one SVD, in Secs. 6 "Calibration cost" and 7 "Hessian-weighted
- * fitting"): the rank-r (A, B) minimising the error the member emits on
- * calibration activations x [n][cols] (one token per row),
+/* Stage 3, activation-weighted factors (the output-matching objective of
+ * Sec. 4, reconstruction fine-tuning; its closed form, whitening by the
+ * activation second moment and one SVD, in Secs. 6 "Calibration cost" and
+ * 7 "Hessian-weighted fitting"): the rank-r (A, B) minimising the error the
+ * member emits on calibration activations x [n][cols] (one token per row),
  *   ||(R - A B) x^T||_F^2 + damp ||R - A B||_F^2,
  * for the aligned residual R as in lx_lowrank_factors. With G = x^T x +
  * damp I = L L^T the optimum is the rank-r truncation of R L = U S V^T:

@@ -1,6 +1,6 @@
 """fp64 reference forward of one compressed MoE layer (test infrastructure).
 
-Definitions followed, stated in the build's notation (output-side factor A,
+Definitions followed, stated in this library's notation (output-side factor A,
 input-side factor B, weights in [out][in] layout):
 
 * Sec. 3 "Representation" (unnumbered equation): a cluster member's weights are

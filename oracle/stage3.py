@@ -3,7 +3,7 @@
 THIS MODULE IS TEST INFRASTRUCTURE, like the rest of the package: only the
 test suite, the smoke check and the benchmark's CPU-baseline leg use it.
 
-What it follows (Sec. 3 "Compression pipeline", Stage 3, in the build's
+What it follows (Sec. 3 "Compression pipeline", Stage 3, in this library's
 notation: weights [out][in], A output-side, B input-side, W ~ W_dom + A B):
 
 * (i) neuron alignment: neuron i of an expert is the concatenation of gate
@@ -22,7 +22,7 @@ notation: weights [out][in], A output-side, B input-side, W ~ W_dom + A B):
   Algorithm 4.4, with a Gaussian test matrix Omega [cols][r + p] passed in,
   p = 10 oversampling columns and q = 2 power iterations, each product
   re-orthonormalised (QR), then the SVD of the small matrix Q^T R.
-* (iii) the activation-weighted fit (Sec. 3 "Output-matching refinement",
+* (iii) the activation-weighted fit (Sec. 4, reconstruction fine-tuning;
   its closed form in Sec. 6 "Calibration cost" and Sec. 7 "Hessian-weighted
   fitting"): the rank-r (A, B) that minimise the error of the emitted
   output on calibration activations X [n][cols] (rows = tokens),

@@ -3,8 +3,8 @@
 // (eq. cost), the aligned residual and its rank-r factors from a randomized
 // truncated SVD with the symmetric split (eqs. svd and factors). The exact
 // assignment between the two (eq. assign) runs on the host. Also the
-// activation-weighted fit of the factors (Sec. 3 "Output-matching
-// refinement", closed form in Secs. 6-7): minimising ||(R - A B) X^T||^2 +
+// activation-weighted fit of the factors (Sec. 4, reconstruction fine-
+// tuning; its closed form in Secs. 6-7): minimising ||(R - A B) X^T||^2 +
 // damp ||R - A B||^2 over calibration activations X is the rank-r
 // truncation of R L (G = X^T X + damp I = L L^T); the same randomized solver
 // runs on the operator M = R Xp^T, Xp = [X; sqrt(damp) I], which has the
