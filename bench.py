@@ -1,21 +1,27 @@
 #!/usr/bin/env python3
 """MoE-layer forward benchmark of the LorExperts / BTExperts hot path on one GPU.
 
-Default workload: the flat LorExperts layer at 30B-A3B-class shape (d=2048,
-f=768, E=128 in 16 clusters of 8, top-8, rank 64, bf16, T=4096 tokens, seeded
-synthetic inputs, Gaussian router). One step = one call of lx_moe_forward
+Headline workload: the BTExperts tree layer (d=4096, f=1024, E=256 under 4
+roots x 8 sub-dominants with rank-128 corrections, leaves with rank-64
+corrections, top-8, bf16, T=8192 tokens, Gaussian router), the largest
+configuration; the flat 30B-A3B-class prefill (d=2048, f=768, E=128 in 16
+clusters of 8, rank 64, T=4096) and its decode-sized batch (T=64) follow as
+extra objects, each with its own roofline (MFMA-bound prefill, HBM-bound
+decode). Seeded synthetic inputs. One step = one call of the layer forward
 (bucketing included, router excluded: ids and weights are inputs), with all
 inputs resident in HBM; consecutive steps use independent copies of the
 layer weights (round-robin over --rotate copies), so no step finds the
 previous step's weights in the last-level cache.
 
 Prints ONE JSON line: tokens/s of the whole layer, the roofline of the
-dominant kernel (per-kernel durations from HIP events recorded around each
-launch on the launch stream, over K further steps), the uncompressed
-dense-expert comparator on the same shapes, and the CPU oracle timed on a
-bounded token sample.
+dominant kernel (the longest per-step kernel; durations from HIP events
+recorded around each launch on its launch stream, over K further steps) with
+every kernel's own fraction beside it, the uncompressed dense-expert
+comparator on the same shapes, and the CPU oracle timed on a bounded token
+sample.
 
-  python bench.py [--gpus 1] [--steps K] [--warmup W] [--config I]
+  python bench.py [--gpus 1] [--steps K] [--warmup W] [--workloads 4,1,2]
+  python bench.py --summarize-profile DIR --workloads I   (rocprofv3 CSVs -> profiles/)
 """
 from __future__ import annotations
 
@@ -37,14 +43,19 @@ RIDGE = PEAK_BF16_FLOPS / PEAK_HBM_BYTES
 def parse():
     ap = argparse.ArgumentParser()
     ap.add_argument("--gpus", type=int, default=1)
-    ap.add_argument("--steps", type=int, default=200)
+    ap.add_argument("--steps", type=int, default=100)
     ap.add_argument("--warmup", type=int, default=20)
-    ap.add_argument("--config", type=int, default=1)
+    ap.add_argument("--workloads", default="4,1,2",
+                    help="configurations to run, headline first (4 = BTExperts tree, 1 = flat prefill, "
+                         "2 = flat decode, 3 = community-routed prefill, 5 = the paper's co-selected "
+                         "cost example)")
+    ap.add_argument("--config", type=int, default=None, help="run this one configuration only")
     ap.add_argument("--seed", type=int, default=None)
-    ap.add_argument("--tokens", type=int, default=None, help="override the workload's token count")
+    ap.add_argument("--tokens", type=int, default=None, help="override the headline workload's token count")
     ap.add_argument("--no-dense", action="store_true", help="skip the dense comparator")
     ap.add_argument("--no-cpu", action="store_true", help="skip the CPU oracle baseline")
-    ap.add_argument("--cpu-tokens", type=int, default=4096)
+    ap.add_argument("--cpu-tokens", type=int, default=None,
+                    help="tokens of the CPU oracle sample (default: 2048 for the tree, 4096 otherwise)")
     ap.add_argument("--cpu-seconds", type=float, default=10.0)
     ap.add_argument("--rotate", type=int, default=5,
                     help="independent device copies of the layer weights, used round-robin by the "
@@ -55,16 +66,23 @@ def parse():
                          "both halves of its bf16 (hi, lo) input in bf16")
     ap.add_argument("--no-route", action="store_true", help="skip timing the GPU top-k router")
     ap.add_argument("--stage3", action="store_true",
-                    help="also time Stage-3 factor production for one member at the workload's expert shape "
-                         "(alignment cost, host assignment, randomized SVD factors of the three projections), "
-                         "against the oracle on the host")
+                    help="also time Stage-3 factor production for one member at the flat workload's expert "
+                         "shape (alignment cost, host assignment, randomized SVD factors of the three "
+                         "projections), against the oracle on the host")
     ap.add_argument("--cluster", action="store_true",
                     help="also time router profiling + NPMI distance + k-medoids (Stages 1-2) on a calibration "
                          "routing of 64 x 2048 tokens, against the oracle on the host")
     ap.add_argument("--copy-calibration", action="store_true",
                     help="only run a plain 1 GiB device-to-device copy 5 times (scales the "
                          "FETCH_SIZE / WRITE_SIZE counters to bytes)")
-    return ap.parse_args()
+    ap.add_argument("--summarize-profile", default=None, metavar="DIR",
+                    help="no GPU work: summarise the rocprofv3 runs under DIR (see profile_commands) into "
+                         "profiles/ for the one workload given by --workloads")
+    a = ap.parse_args()
+    if a.config is not None:
+        a.workloads = str(a.config)
+    a.workload_list = [int(v) for v in a.workloads.split(",") if v.strip()]
+    return a
 
 
 def copy_calibration(torch):
@@ -316,27 +334,27 @@ def bench_stage3(torch, np, lx, layer):
                 cpu_oracle_s=round(cpu_s, 2))
 
 
-def main():
-    a = parse()
-    if a.gpus != 1:
-        print(f"bench.py runs on one GPU only (asked for --gpus {a.gpus}); this implementation has no "
-              "multi-GPU path.", file=sys.stderr)
-        sys.exit(2)
-    import numpy as np
-    import torch
+def roofline_of(name, P, rows, touched, avg_s):
+    """Roofline of one kernel launch: bound by its own arithmetic intensity
+    (algorithmic FLOPs / algorithmic bytes against the ridge point)."""
+    fl, by = kernel_work(name, P, rows, touched)
+    if not fl and not by:
+        return None
+    if fl and fl / max(by, 1) >= RIDGE:
+        return dict(bound="mfma", achieved=round(fl / avg_s / 1e12, 2), peak=PEAK_BF16_FLOPS / 1e12,
+                    unit="TFLOP/s", frac=round(fl / avg_s / PEAK_BF16_FLOPS, 4),
+                    alg_flops_per_launch=fl, alg_bytes_per_launch=by)
+    return dict(bound="hbm", achieved=round(by / avg_s / 1e9, 1), peak=PEAK_HBM_BYTES / 1e9,
+                unit="GB/s", frac=round(by / avg_s / PEAK_HBM_BYTES, 4),
+                alg_flops_per_launch=fl, alg_bytes_per_launch=by)
 
+
+def run_workload(cfg_index, a, torch, np, lx, headline):
+    """Time one configuration; returns (result dict, problem, prepared state)."""
     from lxsynth import make_problem
     from paper_2608_07814_amd import accounting as acc
-    from paper_2608_07814_amd import lorex as lx
 
-    if not torch.cuda.is_available():
-        print("bench.py needs a GPU", file=sys.stderr)
-        sys.exit(3)
-    torch.cuda.set_device(0)
-    if a.copy_calibration:
-        copy_calibration(torch)
-        return
-    p = make_problem(a.config, seed=a.seed, T=a.tokens)
+    p = make_problem(cfg_index, seed=a.seed, T=a.tokens if headline else None)
     cfg = p.cfg
     T, k = p.T, p.k
     layer = p.layer
@@ -350,23 +368,9 @@ def main():
     kind = "flat" if layer.n_levels == 1 else "tree"
     ws = lx.alloc_workspace(dl, T, k, kind)
     out = torch.empty(T, layer.d, dtype=torch.float32, device="cuda")
-    copies = [dl] + [clone_layer(dl) for _ in range(max(a.rotate, 1) - 1)]
-    call = rotating([lx.PreparedCall(c, xd, ids, w, out, ws, kind) for c in copies])
+    workload = cfg["name"] if not (headline and a.tokens) else f"{cfg['name']} at T={T}"
 
-    ms, wall = time_steps(call, a.steps, a.warmup, torch)
-    tokens_per_s = T / (ms * 1e-3)
-    pct = step_percentiles(call, min(a.steps, 100), torch)
-
-    # per-kernel durations: HIP events around every launch, same stream
-    lx.profile_reset()
-    lx.profile_enable(True)
-    for _ in range(a.steps):
-        call()
-    torch.cuda.synchronize()
-    prof = lx.profile_read()
-    lx.profile_enable(False)
-
-    # bucket counts (outside the timed regions) for the algorithmic counts
+    # bucket counts for the algorithmic counts (before any timed region)
     n_lv = layer.n_levels
     rows, touched = [], []
     for l in range(n_lv + 1):
@@ -382,31 +386,39 @@ def main():
     work = acc.algorithmic_counts(layer.d, layer.f, lvrows, T, k)
     P = dict(d=layer.d, f=layer.f, T=T, ranks=ranks)
 
+    copies = [dl] + [clone_layer(dl) for _ in range(max(a.rotate, 1) - 1)]
+    call = rotating([lx.PreparedCall(c, xd, ids, w, out, ws, kind) for c in copies])
+
+    ms, wall = time_steps(call, a.steps, a.warmup, torch)
+    tokens_per_s = T / (ms * 1e-3)
+    pct = step_percentiles(call, min(a.steps, 100), torch)
+
+    # per-kernel durations: HIP events around every launch, on its stream
+    lx.profile_reset()
+    lx.profile_enable(True)
+    for _ in range(a.steps):
+        call()
+    torch.cuda.synchronize()
+    prof = lx.profile_read()  # launch order of one forward
+    lx.profile_enable(False)
+
     kernels = {}
-    for name, (n, tot) in prof.items():
-        fl, by = kernel_work(name, P, rows, touched)
-        avg_ms = tot / max(n, 1)
-        kernels[name] = dict(launches=n, avg_us=round(avg_ms * 1e3, 3),
-                             share=None, alg_tflops=round(fl / (avg_ms * 1e-3) / 1e12, 2) if fl else None,
-                             alg_gbps=round(by / (avg_ms * 1e-3) / 1e9, 1) if by else None)
     tot_all = sum(v[1] for v in prof.values())
     for name, (n, tot) in prof.items():
-        kernels[name]["share"] = round(tot / tot_all, 4)
+        avg_s = tot / max(n, 1) * 1e-3
+        rf = roofline_of(name, P, rows, touched, avg_s)
+        kernels[name] = dict(launches=n, avg_us=round(avg_s * 1e6, 3), share=round(tot / tot_all, 4),
+                             bound=rf["bound"] if rf else None, frac=rf["frac"] if rf else None,
+                             achieved=rf["achieved"] if rf else None, unit=rf["unit"] if rf else None)
+    # the dominant kernel: the longest per step
     dom = max(prof.items(), key=lambda kv: kv[1][1])[0]
-    fl, by = kernel_work(dom, P, rows, touched)
     dom_avg_s = prof[dom][1] / prof[dom][0] * 1e-3
-    workload = cfg["name"] if a.tokens is None else f"{cfg['name']} at T={T}"
-    if fl and fl / max(by, 1) >= RIDGE:
-        roof = dict(bound="mfma", achieved=round(fl / dom_avg_s / 1e12, 2), peak=PEAK_BF16_FLOPS / 1e12,
-                    unit="TFLOP/s", frac=round(fl / dom_avg_s / PEAK_BF16_FLOPS, 4))
-    else:
-        roof = dict(bound="hbm", achieved=round(by / dom_avg_s / 1e9, 1), peak=PEAK_HBM_BYTES / 1e9,
-                    unit="GB/s", frac=round(by / dom_avg_s / PEAK_HBM_BYTES, 4))
+    roof = roofline_of(dom, P, rows, touched, dom_avg_s) or dict(bound="alu", achieved=None, peak=None, unit=None,
+                                                                 frac=None)
     roof["kernel"] = dom
-    roof["alg_flops_per_launch"] = fl
-    roof["alg_bytes_per_launch"] = by
     roof["avg_launch_us"] = round(dom_avg_s * 1e6, 3)
     roof["traffic"] = load_traffic(dom, workload)
+    roof["launches_per_step"] = len(prof)
 
     step_s = ms * 1e-3
     layer_perf = dict(alg_gflop=round(work["flops"] / 1e9, 2), alg_mbytes=round(work["bytes"] / 1e6, 1),
@@ -414,7 +426,8 @@ def main():
                       frac_bf16_peak=round(work["flops"] / step_s / PEAK_BF16_FLOPS, 4),
                       alg_gbps=round(work["bytes"] / step_s / 1e9, 1),
                       frac_hbm_peak=round(work["bytes"] / step_s / PEAK_HBM_BYTES, 4),
-                      rows_per_level=rows, nodes_touched=touched)
+                      rows_per_level=rows, nodes_touched=touched,
+                      serial_kernel_us=round(tot_all / a.steps * 1e3, 2))
 
     dense = None
     if not a.no_dense and kind in ("flat", "tree"):
@@ -460,6 +473,7 @@ def main():
             # per-token cost ratio of Sec. 5 (k experts sharing one dominant)
             dense["analytic_speedup"] = round(acc.closed_form_speedup(k, layer.f, layer.d, ranks[1]), 4)
         del dd, dcopies, dcall, wsd, outd
+        torch.cuda.empty_cache()
 
     routed = None
     if not a.no_route and layer.dtype == "bf16" and layer.d % 128 == 0 and layer.E <= 512:
@@ -485,77 +499,272 @@ def main():
                       router_and_forward_ms=round(cms, 4),
                       router_and_forward_tokens_per_s=round(T / (cms * 1e-3), 1))
 
+    res = dict(workload=workload, tokens_per_s=round(tokens_per_s, 1), ms_per_step=round(ms, 4), step_ms=pct,
+               wall_s_timed=round(wall, 3), weight_copies=len(copies),
+               config={"workload": workload, "T": T, "d": layer.d, "f": layer.f, "E": layer.E, "k": k,
+                       "anchors": layer.n_anchors, "ranks": ranks[1:], "layer": kind, "seed": p.seed,
+                       "out_dtype": "f32", "anchor_down_lo": "bf16" if a.no_lo8 else "fp8 (block-scaled)"},
+               roofline=roof, layer_roofline=layer_perf, kernels=kernels, dense_comparator=dense,
+               gpu_router=routed)
+    del copies, call
+    return res, p
+
+
+def cpu_baseline(p, a, np):
+    """The fp64 oracle on a bounded sample of the workload (host cores)."""
+    from threadpoolctl import threadpool_info, threadpool_limits
+    from oracle import moe as O
+    layer = p.layer
+    T = p.T
+    # a bounded sample: the first n tokens, repeated until ~cpu_seconds of CPU work
+    n = min(a.cpu_tokens or (2048 if layer.n_levels > 1 else 4096), T)
+    reps, t0 = 0, time.perf_counter()
+    while True:
+        O.moe_forward(layer, p.x, p.routing.topk_ids, p.routing.topk_weights, tokens=np.arange(n))
+        reps += 1
+        dt = time.perf_counter() - t0
+        if dt >= a.cpu_seconds or reps >= 64:
+            break
+    threads = max([i.get("num_threads", 1) for i in threadpool_info()] or [1])
+    # one core: a short sample (few tokens, one pass; the oracle reconstructs
+    # every expert the sample touches, which dominates at small samples)
+    n1 = max(1, min(n // 4, 16 if layer.n_levels > 1 else 1024))
+    with threadpool_limits(limits=1):
+        t1 = time.perf_counter()
+        O.moe_forward(layer, p.x, p.routing.topk_ids, p.routing.topk_weights, tokens=np.arange(n1))
+        dt1 = time.perf_counter() - t1
+    model = None
+    try:
+        with open("/proc/cpuinfo") as fh:
+            model = next((ln.split(":", 1)[1].strip() for ln in fh if ln.startswith("model name")), None)
+    except OSError:
+        pass
+    return dict(value=round(n * reps / dt, 2), unit="tokens/s", cores=int(threads), kind="oracle",
+                sample=f"first {n} of {T} tokens of the same workload, {reps} passes, fp64 numpy "
+                       f"oracle (dense reconstruction of every routed expert + per-slot SwiGLU), "
+                       f"{dt:.1f} s wall", nproc=os.cpu_count(), cpu_model=model,
+                single_core_value=round(n1 / dt1, 2),
+                single_core_sample=f"first {n1} tokens, one pass, {dt1:.1f} s wall")
+
+
+def main():
+    a = parse()
+    if a.summarize_profile:
+        summarize_profile(a)
+        return
+    if a.gpus != 1:
+        print(f"bench.py runs on one GPU only (asked for --gpus {a.gpus}); this implementation has no "
+              "multi-GPU path.", file=sys.stderr)
+        sys.exit(2)
+    import numpy as np
+    import torch
+
+    from paper_2608_07814_amd import lorex as lx
+
+    if not torch.cuda.is_available():
+        print("bench.py needs a GPU", file=sys.stderr)
+        sys.exit(3)
+    torch.cuda.set_device(0)
+    if a.copy_calibration:
+        copy_calibration(torch)
+        return
+    results, head_p = [], None
+    for i, c in enumerate(a.workload_list):
+        print(f"[bench] workload {c}", file=sys.stderr, flush=True)
+        r, p = run_workload(c, a, torch, np, lx, headline=(i == 0))
+        results.append(r)
+        if i == 0:
+            head_p = p
+        else:
+            del p
+        torch.cuda.empty_cache()
+    head = results[0]
+
     clustering = None
     if a.cluster:
         clustering = bench_clustering(torch, np, lx, a)
     stage3 = None
-    if a.stage3 and kind == "flat" and layer.dtype == "bf16":
-        stage3 = bench_stage3(torch, np, lx, layer)
+    if a.stage3:
+        from lxsynth import make_problem
+        stage3 = bench_stage3(torch, np, lx, make_problem(1, T=16).layer)
 
     cpu = None
     if not a.no_cpu:
-        from threadpoolctl import threadpool_info
-        from oracle import moe as O
-        # a bounded sample: the first n tokens, repeated until ~10 s of CPU work
-        n = min(a.cpu_tokens, T)
-        reps, t0 = 0, time.perf_counter()
-        while True:
-            O.moe_forward(layer, p.x, p.routing.topk_ids, p.routing.topk_weights, tokens=np.arange(n))
-            reps += 1
-            dt = time.perf_counter() - t0
-            if dt >= a.cpu_seconds or reps >= 64:
-                break
-        threads = max([i.get("num_threads", 1) for i in threadpool_info()] or [1])
-        # one core: a shorter sample (a quarter of the tokens, one pass)
-        from threadpoolctl import threadpool_limits
-        n1 = max(1, n // 4)
-        with threadpool_limits(limits=1):
-            t1 = time.perf_counter()
-            O.moe_forward(layer, p.x, p.routing.topk_ids, p.routing.topk_weights, tokens=np.arange(n1))
-            dt1 = time.perf_counter() - t1
-        model = None
-        try:
-            with open("/proc/cpuinfo") as fh:
-                model = next((ln.split(":", 1)[1].strip() for ln in fh if ln.startswith("model name")), None)
-        except OSError:
-            pass
-        cpu = dict(value=round(n * reps / dt, 2), unit="tokens/s", cores=int(threads), kind="oracle",
-                   sample=f"first {n} of {T} tokens of the same workload, {reps} passes, fp64 numpy "
-                          f"oracle (dense reconstruction of every routed expert + per-slot SwiGLU), "
-                          f"{dt:.1f} s wall", nproc=os.cpu_count(), cpu_model=model,
-                   single_core_value=round(n1 / dt1, 2),
-                   single_core_sample=f"first {n1} tokens, one pass, {dt1:.1f} s wall")
+        print("[bench] cpu baseline", file=sys.stderr, flush=True)
+        cpu = cpu_baseline(head_p, a, np)
 
     res = {
-        "metric": "MoE-layer tokens/s (LorExperts forward, bucketing included)",
-        "value": round(tokens_per_s, 1),
+        "metric": "MoE-layer tokens/s (LorExperts / BTExperts forward, bucketing included)",
+        "value": head["tokens_per_s"],
         "unit": "tokens/s",
         "n_gpus": 1,
         "steps": a.steps,
         "warmup": a.warmup,
-        "ms_per_step": round(ms, 4),
-        "step_ms": pct,
-        "weight_copies": len(copies),
-        "wall_s_timed": round(wall, 3),
+        "ms_per_step": head["ms_per_step"],
+        "step_ms": head["step_ms"],
+        "weight_copies": head["weight_copies"],
+        "wall_s_timed": head["wall_s_timed"],
         "higher_is_better": True,
         "scaling": "weak",
         "vs_baseline": None,
         "dtype": "bf16",
         "data": "synthetic (seeded; Gaussian, community or co-selected routing; random-init weights)",
-        "config": {"workload": workload, "T": T, "d": layer.d, "f": layer.f, "E": layer.E,
-                   "k": k, "anchors": layer.n_anchors, "ranks": ranks[1:], "layer": kind,
-                   "seed": p.seed, "out_dtype": "f32",
-                   "anchor_down_lo": "bf16" if a.no_lo8 else "fp8 (block-scaled)"},
-        "roofline": roof,
-        "layer_roofline": layer_perf,
-        "kernels": kernels,
-        "dense_comparator": dense,
-        "gpu_router": routed,
+        "config": head["config"],
+        "roofline": head["roofline"],
+        "layer_roofline": head["layer_roofline"],
+        "kernels": head["kernels"],
+        "dense_comparator": head["dense_comparator"],
+        "gpu_router": head["gpu_router"],
+        "workloads": {r["workload"]: {k: r[k] for k in ("tokens_per_s", "ms_per_step", "step_ms", "roofline",
+                                                         "layer_roofline", "kernels", "dense_comparator",
+                                                         "gpu_router", "config")}
+                      for r in results[1:]},
         "clustering": clustering,
         "stage3": stage3,
         "cpu_baseline": cpu,
     }
     print(json.dumps(res), flush=True)
+
+
+# ------------------------------------------------------------------ profiles
+def profile_commands(c):
+    """The rocprofv3 runs a profile summary is made from (run from the
+    repository root on one MI355X after `cd /tmp && export TMPDIR=/tmp`;
+    OUT is any output directory)."""
+    b = f"python3 bench.py --workloads {c} --no-cpu --no-dense --no-route"
+    return [
+        ("trace", f"rocprofv3 --kernel-trace --stats -f csv -d OUT/trace_c{c} -o t -- {b} --steps 20 --warmup 5"),
+        ("FETCH_SIZE", f"rocprofv3 --pmc FETCH_SIZE -f csv -d OUT/FETCH_SIZE_c{c} -o p -- {b} --steps 2 --warmup 1 "
+                       f"--rotate 1"),
+        ("WRITE_SIZE", f"rocprofv3 --pmc WRITE_SIZE -f csv -d OUT/WRITE_SIZE_c{c} -o p -- {b} --steps 2 --warmup 1 "
+                       f"--rotate 1"),
+        ("copy FETCH_SIZE", "rocprofv3 --pmc FETCH_SIZE -f csv -d OUT/FETCH_SIZE_copy -o p -- python3 bench.py "
+                            "--copy-calibration"),
+        ("copy WRITE_SIZE", "rocprofv3 --pmc WRITE_SIZE -f csv -d OUT/WRITE_SIZE_copy -o p -- python3 bench.py "
+                            "--copy-calibration"),
+    ]
+
+
+def _csv(path):
+    import csv
+    with open(path) as fh:
+        return list(csv.DictReader(fh))
+
+
+def _find(d, sub, name):
+    for root, _, files in os.walk(os.path.join(d, sub)):
+        for f in files:
+            if f.endswith(name):
+                return os.path.join(root, f)
+    raise FileNotFoundError(f"{sub}/*{name} under {d}")
+
+
+def _counter_per_dispatch(path):
+    by = {}
+    for r in _csv(path):
+        i = int(r["Dispatch_Id"])
+        ent = by.setdefault(i, [r["Kernel_Name"], 0.0])
+        ent[1] += float(r["Counter_Value"])
+    return [(by[i][0], by[i][1]) for i in sorted(by)]
+
+
+def summarize_profile(a):
+    """rocprofv3 output (profile_commands) -> profiles/<workload>.md and the
+    workload's entries of profiles/traffic.json. The library's kernels are the
+    dispatches whose names carry its namespace; the last K x n of them are the
+    benchmark's serialised per-kernel timing pass (K steps of n launches, in
+    the launch order the benchmark's own JSON line lists)."""
+    import statistics
+    from lxsynth import config as _cfg
+    c = a.workload_list[0]
+    d = a.summarize_profile
+    wl = _cfg(c)["name"]
+    # the benchmark's JSON line of the trace run names the launches in order
+    line = None
+    with open(os.path.join(d, f"trace_c{c}.log")) as fh:
+        for ln in fh:
+            if ln.startswith("{"):
+                line = json.loads(ln)
+    if line is None:
+        raise RuntimeError("no JSON line in the trace run's log")
+    roles = list(line["kernels"].keys())
+    n = len(roles)
+    steps = int(line["steps"])
+    tr = sorted(_csv(_find(d, f"trace_c{c}", "kernel_trace.csv")), key=lambda r: int(r["Dispatch_Id"]))
+    lxr = [r for r in tr if "lx::" in r["Kernel_Name"]]
+    ser = lxr[-steps * n:]
+    dur = {r: [] for r in roles}
+    for i, row in enumerate(ser):
+        dur[roles[i % n]].append((int(row["End_Timestamp"]) - int(row["Start_Timestamp"])) / 1e3)
+    # whole forwards of the timed loops before the serialised pass (first to
+    # last dispatch of each group of n)
+    warm = int(line["warmup"])
+    n_timed = warm + steps + min(steps, 100)
+    timed = lxr[max(0, len(lxr) - steps * n - n_timed * n): len(lxr) - steps * n]
+    fwd = []
+    for g in range(len(timed) // n):
+        grp = timed[g * n:(g + 1) * n]
+        fwd.append((max(int(x["End_Timestamp"]) for x in grp) - min(int(x["Start_Timestamp"]) for x in grp)) / 1e3)
+
+    def scale(ctr):
+        vals = [v for nm, v in _counter_per_dispatch(_find(d, f"{ctr}_copy", "counter_collection.csv"))
+                if "copy" in nm.lower() or "elementwise" in nm.lower()]
+        return (1 << 30) / (statistics.median(vals) * 1024.0)
+
+    sc = {ctr: scale(ctr) for ctr in ("FETCH_SIZE", "WRITE_SIZE")}
+    cnt = {}
+    for ctr in ("FETCH_SIZE", "WRITE_SIZE"):
+        rows = [(nm, v) for nm, v in _counter_per_dispatch(_find(d, f"{ctr}_c{c}", "counter_collection.csv"))
+                if "lx::" in nm]
+        per = {r: [] for r in roles}
+        # the counter runs end, like the trace run, with the serialised pass
+        # of K forwards (same launch sequence)
+        k_ctr = 2
+        tail = rows[len(rows) - k_ctr * n:]
+        for i, (_, v) in enumerate(tail):
+            per[roles[i % n]].append(v * 1024.0 * sc[ctr])
+        cnt[ctr] = {r: statistics.mean(v) if v else None for r, v in per.items()}
+    sha = source_sha()
+    lines = [f"# rocprofv3 kernel summary: {wl}", "",
+             f"Kernel sources sha256[:16] = `{sha}`.", "",
+             "Commands (from the repository root on one MI355X, after `cd /tmp && export TMPDIR=/tmp`; "
+             "OUT is the output directory), then "
+             f"`python3 bench.py --summarize-profile OUT --workloads {c}`:", ""]
+    lines += [f"- {what}: `{cmd}`" for what, cmd in profile_commands(c)]
+    lines += ["", f"FETCH_SIZE scale = {sc['FETCH_SIZE']:.4f} bytes per counted byte, WRITE_SIZE scale = "
+                  f"{sc['WRITE_SIZE']:.4f} (a plain 1 GiB device copy reads and writes exactly 1 GiB).", "",
+              f"Per-kernel rows: the last {steps} forwards of the trace (the benchmark's serialised per-kernel "
+              f"timing pass, {n} launches each). Whole forward (first dispatch start to last dispatch end) over "
+              f"the {len(fwd)} forwards of the timed loops: median {statistics.median(fwd):.1f} us, min "
+              f"{min(fwd):.1f} us." if fwd else "", "",
+              "| kernel (role) | dispatches | avg us | min us | max us | roofline of the benchmark run "
+              "| HBM read MB/launch | HBM write MB/launch |",
+              "|---|---:|---:|---:|---:|---|---:|---:|"]
+    db_path = os.path.join(ROOT, "profiles", "traffic.json")
+    db = json.load(open(db_path)) if os.path.exists(db_path) else {}
+    db = {k: v for k, v in db.items() if not k.endswith("@" + wl)}
+    tot = 0.0
+    for r in roles:
+        v = dur[r]
+        kr = line["kernels"][r]
+        rf = f"{kr['frac']:.3f} of {kr['bound']} ({kr['achieved']} {kr['unit']})" if kr.get("frac") else "-"
+        fb, wb = cnt["FETCH_SIZE"][r], cnt["WRITE_SIZE"][r]
+        tot += statistics.mean(v)
+        lines.append(f"| {r} | {len(v)} | {statistics.mean(v):.2f} | {min(v):.2f} | {max(v):.2f} | {rf} | "
+                     f"{fb / 1e6:.1f} | {wb / 1e6:.1f} |")
+        db[f"{r}@{wl}"] = dict(avg_us=round(statistics.mean(v), 3), fetch_bytes_per_launch=int(fb),
+                               write_bytes_per_launch=int(wb), source_sha=sha)
+    dom = line["roofline"]["kernel"]
+    lines += ["", f"Sum of per-role averages (serialised): {tot:.1f} us. Longest kernel in this trace: "
+                  f"{max(roles, key=lambda r: statistics.mean(dur[r]))} "
+                  f"({max(statistics.mean(dur[r]) for r in roles):.2f} us); the benchmark's dominant kernel: {dom}.",
+              ""]
+    out = os.path.join(ROOT, "profiles", f"forward_{wl}.md")
+    with open(out, "w") as fh:
+        fh.write("\n".join(lines))
+    with open(db_path, "w") as fh:
+        json.dump(dict(sorted(db.items())), fh, indent=1)
+    print(out)
 
 
 if __name__ == "__main__":

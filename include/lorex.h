@@ -21,7 +21,9 @@
  * Conventions for every entry point:
  *   - All array arguments are DEVICE pointers to caller-owned memory (the
  *     layer descriptor structs themselves live on the host and are read during
- *     the call only). The library never allocates, frees or retains memory.
+ *     the call only). The library never allocates or frees device memory and
+ *     keeps no pointer past the call. The only resources it creates itself are
+ *     described under "Auxiliary stream" below.
  *   - Weights use nn.Linear layout [out][in], input dimension contiguous.
  *     Every array is dense row-major; pointers must be 16-byte aligned.
  *   - x and all weights share one dtype (LX_BF16 or LX_F32). bf16 inputs are
@@ -38,11 +40,27 @@
  *     *_workspace_bytes function returns; its contents need no initialization.
  *   - `stream` is a hipStream_t (NULL = the default stream). Every call is
  *     asynchronous on that stream; inputs must stay valid until the stream's
- *     work completes. The library keeps no mutable global state apart from the
- *     optional kernel-timing records, so calls with distinct workspaces may
- *     run concurrently.
+ *     work completes. Calls with distinct workspaces may be issued from
+ *     several host threads at once (see the serialisation noted below).
  *   - T = 0 is a valid no-op. Host-side argument errors are returned before
  *     anything is enqueued; the message is available from lx_last_error().
+ *
+ * Auxiliary stream (forward entry points only). When a batch is large enough
+ * for the anchor GEMMs to run on the persistent large-tile kernel and the
+ * layer has corrections, the correction GEMM chains are forked onto a second
+ * stream of the same device (default priority, non-blocking) between two
+ * events recorded on the caller's stream, so they overlap the anchor GEMMs;
+ * the caller's stream is ordered after all of the call's work when the call
+ * returns. That stream and its two events are created on the first such call
+ * on each device and kept until the process ends (per device, shared by all
+ * callers). A per-device mutex is held while a forward enqueues its work
+ * (host side only), so concurrent forwards on one device enqueue one after
+ * another, and their correction chains run one after another on the shared
+ * stream. lx_set_aux_stream(0) turns this off: every launch then goes to the
+ * caller's stream, nothing is created and no lock is taken. Decode-sized
+ * batches and per-kernel timing (lx_profile_enable) never use it. Mutable
+ * global state besides this: the switch itself, the per-thread error message
+ * and the optional kernel-timing records.
  */
 #ifndef LOREX_H
 #define LOREX_H
@@ -348,7 +366,11 @@ lx_status lx_weighted_factors(const void* w_dom, const void* w_mem, lx_dtype dty
                               double* sigma, void* workspace, size_t workspace_bytes, void* stream);
 
 /* Routing bucketing alone (the first step of every forward), exposing the
- * arrays of one tree level `level` (0 = anchors, n_levels = experts):
+ * arrays of one tree level `level` (0 = anchors, n_levels = experts). It
+ * organises the sharing of Sec. 5.1 ("Amortized forward pass"): the terms an
+ * anchor or a tree node contributes are computed once per token that selects
+ * any expert below it, so each level gets one row per distinct (token, node)
+ * pair, and each slot the row it reads:
  *   row_token   [T * min(k, N_level)] (only the first node_offsets[N] entries
  *               are written): tokens of the unique (token, node) pairs, sorted
  *               by (node, token);
@@ -361,6 +383,13 @@ lx_status lx_bucket(const lx_tree_layer* layer, int32_t T, int32_t k,
                     const int32_t* topk_ids, int32_t level, int32_t* row_token,
                     int32_t* node_offsets, int32_t* slot_row, void* workspace,
                     size_t workspace_bytes, void* stream);
+
+/* Switch for the auxiliary stream of the forward entry points (see
+ * "Auxiliary stream" above): enable = 1 (the default) lets prefill-sized
+ * forwards fork their correction chains onto it, 0 keeps every launch on the
+ * caller's stream. Process-wide; returns the previous setting. Results are
+ * bitwise the same either way. No device call is made. */
+int32_t lx_set_aux_stream(int32_t enable);
 
 /* Device status bits (LX_DEVFLAG_*) of the last call that used `workspace`.
  * Synchronizes `stream`. */

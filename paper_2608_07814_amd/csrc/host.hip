@@ -15,6 +15,7 @@
 //   per level l >= 1       v = hbar_l * B_down^T, y_l = v * A_down^T
 //   combine                out[t] = sum of the token's rows over all levels
 #include <algorithm>
+#include <atomic>
 #include <cmath>
 #include <deque>
 #include <map>
@@ -325,6 +326,10 @@ struct Aux {
   bool ok = false;
 };
 
+// lx_set_aux_stream: whether prefill-sized forwards may use the auxiliary
+// stream at all (process-wide).
+std::atomic<int> g_aux_enabled{1};
+
 Aux* aux_for_current_device() {
   static std::mutex mu;
   static Aux aux[64];
@@ -558,7 +563,8 @@ lx_status run(const lx_tree_layer& t, int T, int k, const void* x, const int32_t
   // kernel's duration is its own.
   bool any_fac = false;
   for (int l = 1; l <= L; ++l) any_fac |= t.levels[l - 1].n_factors > 0;
-  Aux* const aux = any_fac && !skinny[0] && !g_prof ? aux_for_current_device() : nullptr;
+  Aux* const aux =
+      any_fac && !skinny[0] && !g_prof && g_aux_enabled.load(std::memory_order_relaxed) ? aux_for_current_device() : nullptr;
   std::unique_lock<std::mutex> aux_lock;
   if (aux) aux_lock = std::unique_lock<std::mutex>(aux->mu);
   ForkJoin fj_up(aux, stream), fj_down(aux, stream);
@@ -799,6 +805,8 @@ const char* lx_status_string(lx_status s) {
 const char* lx_last_error(void) { return g_err.c_str(); }
 
 int32_t lx_version(void) { return 100; }
+
+int32_t lx_set_aux_stream(int32_t enable) { return g_aux_enabled.exchange(enable ? 1 : 0); }
 
 size_t lx_moe_tree_workspace_bytes(const lx_tree_layer* layer, int32_t T, int32_t k) {
   if (check_call(layer, T, k) != LX_OK) return 0;

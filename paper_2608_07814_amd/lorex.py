@@ -63,6 +63,7 @@ EXPORTS = {
     "lx_status_string": (ctypes.c_char_p, [_c_i32]),
     "lx_last_error": (ctypes.c_char_p, []),
     "lx_version": (_c_i32, []),
+    "lx_set_aux_stream": (_c_i32, [_c_i32]),
     "lx_moe_workspace_bytes": (ctypes.c_size_t, [ctypes.POINTER(LxFlatLayer), _c_i32, _c_i32]),
     "lx_moe_tree_workspace_bytes": (ctypes.c_size_t, [ctypes.POINTER(LxTreeLayer), _c_i32, _c_i32]),
     "lx_dense_moe_workspace_bytes": (ctypes.c_size_t, [ctypes.POINTER(LxDenseLayer), _c_i32, _c_i32]),
@@ -258,7 +259,7 @@ def quantize_f8(w: torch.Tensor, stream=None):
 def route_workspace(T: int, d: int, E: int, device="cuda") -> torch.Tensor:
     n = int(lib().lx_route_workspace_bytes(T, d, E))
     if n == 0:
-        raise LorexError(f"unsupported router shape T={T} d={d} E={E}")
+        raise LorexError(LX_ERR_UNSUPPORTED, f"unsupported router shape T={T} d={d} E={E}")
     return torch.empty(n, dtype=torch.uint8, device=device)
 
 
@@ -362,7 +363,7 @@ def lowrank_factors(w_dom: torch.Tensor, w_mem: torch.Tensor, r: int, omega: tor
     sig = torch.empty(r, dtype=torch.float64, device=dev)
     n = int(lib().lx_lowrank_workspace_bytes(rows, cols, r, p))
     if n == 0:
-        raise LorexError("unsupported shape for lx_lowrank_factors")
+        raise LorexError(LX_ERR_UNSUPPORTED, f"unsupported shape for lx_lowrank_factors: rows={rows} cols={cols} r={r} p={p}")
     ws = torch.empty(n, dtype=torch.uint8, device=dev)
     _check(lib().lx_lowrank_factors(_ptr(w_dom), _ptr(w_mem), dt, rows, cols, _ptr(perm) if perm is not None else None,
                                     perm_axis, r, p, q, _ptr(omega), _ptr(A), _ptr(B), _ptr(sig), _ptr(ws), n,
@@ -394,7 +395,7 @@ def weighted_factors(w_dom: torch.Tensor, w_mem: torch.Tensor, r: int, x: torch.
     sig = torch.empty(r, dtype=torch.float64, device=dev)
     nb = int(lib().lx_weighted_workspace_bytes(rows, cols, n, 1 if damp > 0 else 0, r, p))
     if nb == 0:
-        raise LorexError("unsupported shape for lx_weighted_factors")
+        raise LorexError(LX_ERR_UNSUPPORTED, f"unsupported shape for lx_weighted_factors: rows={rows} cols={cols} n={n} r={r} p={p}")
     ws = torch.empty(nb, dtype=torch.uint8, device=dev)
     _check(lib().lx_weighted_factors(_ptr(w_dom), _ptr(w_mem), dt, rows, cols,
                                      _ptr(perm) if perm is not None else None, perm_axis, _ptr(x), xdt, n,
@@ -501,6 +502,12 @@ def bucket(layer: DeviceLayer, topk_ids: torch.Tensor, level: int,
     torch.cuda.current_stream().synchronize() if stream is None else stream.synchronize()
     n = int(offsets[-1].item())
     return row_token[:n], offsets, slot_row[:T * k]
+
+
+def set_aux_stream(enable: bool) -> bool:
+    """Allow (True, the default) or forbid the forward's auxiliary stream
+    (lx_set_aux_stream); returns the previous setting."""
+    return bool(lib().lx_set_aux_stream(1 if enable else 0))
 
 
 def read_device_status(workspace: torch.Tensor, stream=None) -> int:

@@ -28,7 +28,7 @@ def _declared(root):
 
 def test_every_declared_symbol_is_exported(L, root):
     names = _declared(root)
-    assert len(names) == len(lx.EXPORTS) == 28
+    assert len(names) == len(lx.EXPORTS) == 29
     for n in names:
         assert hasattr(L, n), n
         assert n in lx.EXPORTS, n
@@ -262,3 +262,36 @@ def test_weighted_fit_validation(L):
     assert call(n=n - 1) == lx.LX_ERR_WORKSPACE_TOO_SMALL
     # damping: the same call needs the larger workspace
     assert call(damp=0.1) == lx.LX_ERR_WORKSPACE_TOO_SMALL
+
+
+def test_binding_error_paths_raise_lorex_error(L):
+    """The binding's own shape checks raise LorexError with a status (no kernel
+    is launched: every shape below is refused by a workspace-size query)."""
+    import torch
+    with pytest.raises(lx.LorexError) as e:
+        lx.route_workspace(16, 100, 128, device="cpu")              # d not a multiple of 64
+    assert e.value.status == lx.LX_ERR_UNSUPPORTED and "router shape" in str(e.value)
+    with pytest.raises(lx.LorexError) as e:
+        lx.route_workspace(16, 2048, 6, device="cpu")               # E not a multiple of 4
+    assert e.value.status == lx.LX_ERR_UNSUPPORTED
+    w = torch.zeros(200, 200, dtype=torch.float32)
+    with pytest.raises(lx.LorexError) as e:                        # r + p > 128
+        lx.lowrank_factors(w, w, 120, torch.zeros(200, 130, dtype=torch.float64))
+    assert e.value.status == lx.LX_ERR_UNSUPPORTED and "lx_lowrank_factors" in str(e.value)
+    x = torch.zeros(300, 200, dtype=torch.float32)
+    with pytest.raises(lx.LorexError) as e:                        # r + p > 128
+        lx.weighted_factors(w, w, 120, x, torch.zeros(300, 130, dtype=torch.float64))
+    assert e.value.status == lx.LX_ERR_UNSUPPORTED and "lx_weighted_factors" in str(e.value)
+    with pytest.raises(lx.LorexError) as e:                        # r + p > activation rows
+        lx.weighted_factors(w, w, 60, x[:50], torch.zeros(50, 70, dtype=torch.float64))
+    assert e.value.status == lx.LX_ERR_UNSUPPORTED
+
+
+def test_aux_stream_switch(L):
+    """lx_set_aux_stream is a plain process-wide switch that returns the
+    previous setting (on by default) and touches no device."""
+    assert lx.set_aux_stream(False) is True
+    assert lx.set_aux_stream(False) is False
+    assert L.lx_set_aux_stream(7) == 0          # any non-zero value enables
+    assert lx.set_aux_stream(True) is True
+    assert lx.set_aux_stream(True) is True

@@ -33,8 +33,10 @@ def _check(layer, ids, expect_flag=0):
     assert lx.read_device_status(ws) & lx.LX_DEVFLAG_BAD_ID == expect_flag
 
 
-@pytest.mark.parametrize("cfg,T", [(0, 16), (1, 4096), (2, 64), (3, 2000), (4, 1000)])
+@pytest.mark.parametrize("cfg,T", [(0, 16), (1, 4096), (2, 64), (3, 2000), (3, 16384), (4, 1000), (4, 8192)])
 def test_bucket_configs(cfg, T):
+    """Full sizes included: cfg3 at T=16384 (256 token tiles x 32 nodes, the
+    scan's reload branch) and the cfg4 tree at T=8192."""
     say(f"bucket cfg{cfg} T={T}")
     p = make_problem(cfg, T=T)
     _check(p.layer, p.routing.topk_ids)

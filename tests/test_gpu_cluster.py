@@ -101,3 +101,58 @@ def test_clusters_drive_the_forward():
     e = err_ratio(gpu_forward(p), O.moe_forward(layer, x, rids, rw))
     say(f"  err/RMS = {e:.3e}")
     assert e <= TOL_BF16 and e <= TOL_DESIGN
+
+
+def _final_margins(D, Dg, cl, C):
+    """Smallest gap between the best and the second-best choice among the
+    final decisions of a k-medoids result: a member's nearest medoid, and a
+    cluster's medoid (smallest in-cluster distance sum). An exact tie that
+    both matrices hold exactly (e.g. D = 2 for pairs that never co-fire, no
+    rounding involved) is decided by the index on both sides and is skipped."""
+    med = []
+    gap = np.inf
+    for c in range(C):
+        mem = np.nonzero(cl == c)[0]
+        s = np.array([sum(D[m, j] for j in mem) for m in mem])
+        sg = np.array([sum(Dg[m, j] for j in mem) for m in mem])
+        med.append(int(mem[np.argmin(s)]))
+        if len(mem) > 1:
+            o = np.argsort(s, kind="stable")
+            g = s[o[1]] - s[o[0]]
+            if not (g == 0 and sg[o[1]] == sg[o[0]]):
+                gap = min(gap, g)
+    med = np.array(med)
+    for e in range(D.shape[0]):
+        if e in med:
+            continue
+        o = np.argsort(D[e, med], kind="stable")
+        g = D[e, med[o[1]]] - D[e, med[o[0]]]
+        if g == 0 and Dg[e, med[o[1]]] == Dg[e, med[o[0]]]:
+            continue
+        gap = min(gap, g)
+    return gap
+
+
+@pytest.mark.parametrize("E,C,N", [(128, 32, 4096), (64, 16, 2000)])
+def test_cluster_chain_against_oracle_only_chain(E, C, N):
+    """ids -> counts -> distance -> k-medoids on the GPU against the same chain
+    run by the oracle alone (oracle counts, oracle distance, oracle k-medoids).
+    The two distance matrices agree to 1e-13; a decision may legitimately
+    differ only where two candidates are closer than that bound, so the test
+    first shows that every final decision of the oracle's run has a margin far
+    above it, and then requires identical clusterings."""
+    require_gpu()
+    say(f"cluster chain E={E} C={C} N={N}")
+    ids = _calib(E, min(E // 4, 32), N, 8, 70 + E)
+    fire, _, dist, dist_d = _gpu_counts(ids, E)
+    cl, fo, dom, it = (t.cpu().numpy() for t in
+                       lx.kmedoids(dist_d, torch.from_numpy(fire.astype(np.int32)).cuda(), C))
+    f0, p0 = K.coact_counts(ids, E)
+    d0 = K.npmi_distance(f0, p0, N)
+    c0, fo0, dom0, it0 = K.kmedoids(d0, f0, C)
+    bound = float(np.max(np.abs(dist - d0)))
+    margin = _final_margins(d0, dist, c0, C)
+    say(f"  distance bound {bound:.2e}, smallest final decision margin {margin:.2e}, rounds {int(it[0])}/{it0}")
+    assert bound <= 1e-13
+    assert margin > 1e3 * E * max(bound, 1e-16)
+    assert np.array_equal(cl, c0) and np.array_equal(fo, fo0) and np.array_equal(dom, dom0) and it[0] == it0
