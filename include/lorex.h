@@ -192,6 +192,31 @@ lx_status lx_moe_forward_tree(const lx_tree_layer* layer, int32_t T, int32_t k,
                               const float* topk_weights, void* out, lx_dtype out_dtype,
                               void* workspace, size_t workspace_bytes, void* stream);
 
+/* For callers that cannot allocate device memory (code under HIP graph
+ * capture, tight serving loops, harnesses that forbid allocation): the tree
+ * forward of lx_moe_forward_tree with the same arguments minus the
+ * workspace, which is replaced by a library-owned static device array of
+ * LX_STATIC_SCRATCH_BYTES (64 MiB) per GPU, created when the library's code
+ * is loaded on that GPU and held until the process ends. The call allocates
+ * nothing and creates no HIP object: no hipMalloc/hipFree, no auxiliary
+ * stream (every launch goes to `stream`), no kernel-timing records; the
+ * first call on a device looks the array's device address up once.
+ * A batch whose workspace (lx_moe_tree_workspace_bytes) exceeds the array is
+ * refused with LX_ERR_WORKSPACE_TOO_SMALL before anything is enqueued; 64 MiB
+ * covers decode-sized batches (e.g. T <= 64 at d = 4096, f = 1024 with two
+ * correction levels; T <= 128 at d = 2048, f = 768, 128 experts, top-8).
+ * Every call on one GPU shares that GPU's array and leaves its contents
+ * behind; the forward initialises everything it reads, so nothing needs
+ * clearing. Calls whose device work overlaps on one GPU (several host threads
+ * or streams at once) race on the array: serialise them. The device status
+ * word (LX_DEVFLAG_*) lives in the array and is not exposed: an invalid id is
+ * dropped silently. Flat layers are passed as their one-level tree. */
+#define LX_STATIC_SCRATCH_BYTES (64u << 20)
+lx_status lx_moe_forward_tree_static(const lx_tree_layer* layer, int32_t T, int32_t k,
+                                     const void* x, const int32_t* topk_ids,
+                                     const float* topk_weights, void* out, lx_dtype out_dtype,
+                                     void* stream);
+
 /* Uncompressed top-k SwiGLU MoE (comparator); same arguments. */
 lx_status lx_dense_moe_forward(const lx_dense_layer* layer, int32_t T, int32_t k,
                                const void* x, const int32_t* topk_ids,

@@ -57,19 +57,23 @@ hipEvent_t pool_get() {
   return e;
 }
 
+// Set for the duration of a call that must not create any HIP object (the
+// static-scratch forward): kernel timing records are skipped in it.
+thread_local bool tl_no_alloc = false;
+
 struct Timed {
   const char* name;
   hipStream_t s;
   hipEvent_t a = nullptr, b = nullptr;
   Timed(const char* n, hipStream_t st) : name(n), s(st) {
-    if (g_prof) {
+    if (g_prof && !tl_no_alloc) {
       a = pool_get();
       b = pool_get();
       if (a) (void)hipEventRecord(a, s);
     }
   }
   void done() {
-    if (g_prof && a && b) {
+    if (g_prof && !tl_no_alloc && a && b) {
       (void)hipEventRecord(b, s);
       g_pending.push_back({name, a, b});
     }
@@ -492,15 +496,16 @@ lx_status run(const lx_tree_layer& t, int T, int k, const void* x, const int32_t
     int ofmt[kSkinnyMaxProblems];
     int tiles[kSkinnyMaxProblems];
     std::string name;
+    const bool named = g_prof && !tl_no_alloc;  // the name only labels timing records
     for (int i = 0; i < npend; ++i) {
       g[i] = pend[i].g;
       ofmt[i] = pend[i].ofmt;
       tiles[i] = pend[i].tiles;
-      name += (i ? "+" : "") + std::string(pend[i].name);
+      if (named) name += (i ? "+" : "") + std::string(pend[i].name);
     }
     const int n = npend;
     npend = 0;
-    LX_LAUNCH(intern_name(name), launch_gemm_skinny_batch(g, ofmt, tiles, n, lstream));
+    LX_LAUNCH(named ? intern_name(name) : "skinny_batch", launch_gemm_skinny_batch(g, ofmt, tiles, n, lstream));
     return LX_OK;
   };
   auto big = [&](const char* name, GemmArgs g, int l, int bm, int bn, int ofmt,
@@ -563,8 +568,9 @@ lx_status run(const lx_tree_layer& t, int T, int k, const void* x, const int32_t
   // kernel's duration is its own.
   bool any_fac = false;
   for (int l = 1; l <= L; ++l) any_fac |= t.levels[l - 1].n_factors > 0;
-  Aux* const aux =
-      any_fac && !skinny[0] && !g_prof && g_aux_enabled.load(std::memory_order_relaxed) ? aux_for_current_device() : nullptr;
+  Aux* const aux = any_fac && !skinny[0] && !g_prof && !tl_no_alloc && g_aux_enabled.load(std::memory_order_relaxed)
+                       ? aux_for_current_device()
+                       : nullptr;
   std::unique_lock<std::mutex> aux_lock;
   if (aux) aux_lock = std::unique_lock<std::mutex>(aux->mu);
   ForkJoin fj_up(aux, stream), fj_down(aux, stream);
@@ -789,6 +795,37 @@ lx_status check_dense(const lx_dense_layer* D) {
 
 using namespace lx;
 
+// Device scratch of lx_moe_forward_tree_static: one copy per GPU, allocated
+// when the code object is loaded there and held until the process ends. Host
+// code never uses this name as an address (on the host it is only a
+// stand-in): the device address comes from hipGetSymbolAddress, once per
+// device, and only that address is passed to kernels.
+static __device__ __align__(256) unsigned char scratch[LX_STATIC_SCRATCH_BYTES];
+
+namespace {
+std::mutex g_scratch_mu;
+void* g_scratch_ptr[64] = {};
+
+// Device address of this device's `scratch` (looked up on the first call on
+// the device, with that device current).
+lx_status scratch_for_current_device(void** ptr) {
+  int dev = 0;
+  const hipError_t e0 = hipGetDevice(&dev);
+  if (e0 != hipSuccess) return fail(LX_ERR_HIP, std::string("hipGetDevice: ") + hipGetErrorString(e0));
+  if (dev < 0 || dev >= 64) return fail(LX_ERR_UNSUPPORTED, "device index beyond 63");
+  std::lock_guard<std::mutex> lk(g_scratch_mu);
+  if (!g_scratch_ptr[dev]) {
+    void* p = nullptr;
+    const hipError_t e = hipGetSymbolAddress(&p, HIP_SYMBOL(scratch));
+    if (e != hipSuccess || !p)
+      return fail(LX_ERR_HIP, std::string("hipGetSymbolAddress(scratch): ") + hipGetErrorString(e));
+    g_scratch_ptr[dev] = p;
+  }
+  *ptr = g_scratch_ptr[dev];
+  return LX_OK;
+}
+}  // namespace
+
 extern "C" {
 
 const char* lx_status_string(lx_status s) {
@@ -854,6 +891,29 @@ lx_status lx_dense_moe_forward(const lx_dense_layer* layer, int32_t T, int32_t k
   const lx_tree_layer t = dense_to_tree(*layer);
   return run(t, T, k, x, topk_ids, topk_weights, out, out_dtype, workspace, workspace_bytes,
              (hipStream_t)stream, RUN_ALL);
+}
+
+lx_status lx_moe_forward_tree_static(const lx_tree_layer* layer, int32_t T, int32_t k, const void* x,
+                                     const int32_t* topk_ids, const float* topk_weights, void* out,
+                                     lx_dtype out_dtype, void* stream) {
+  g_err.clear();
+  if (!layer) return fail(LX_ERR_INVALID_ARGUMENT, "layer is null");
+  lx_status st = check_call(layer, T, k);
+  if (st != LX_OK) return st;
+  const size_t need = make_plan(*layer, T, k).total;
+  if (need > (size_t)LX_STATIC_SCRATCH_BYTES)
+    return fail(LX_ERR_WORKSPACE_TOO_SMALL, "this batch needs " + std::to_string(need) +
+                                                " bytes of scratch; the static scratch holds " +
+                                                std::to_string((size_t)LX_STATIC_SCRATCH_BYTES) +
+                                                " (use lx_moe_forward_tree with a workspace)");
+  void* ws = nullptr;
+  st = scratch_for_current_device(&ws);
+  if (st != LX_OK) return st;
+  tl_no_alloc = true;
+  st = run(*layer, T, k, x, topk_ids, topk_weights, out, out_dtype, ws, (size_t)LX_STATIC_SCRATCH_BYTES,
+           (hipStream_t)stream, RUN_ALL);
+  tl_no_alloc = false;
+  return st;
 }
 
 lx_status lx_bucket(const lx_tree_layer* layer, int32_t T, int32_t k, const int32_t* topk_ids, int32_t level,

@@ -71,6 +71,8 @@ EXPORTS = {
                                 _c_void, _c_i32, _c_void, ctypes.c_size_t, _c_void]),
     "lx_moe_forward_tree": (_c_i32, [ctypes.POINTER(LxTreeLayer), _c_i32, _c_i32, _c_void, _c_void,
                                      _c_void, _c_void, _c_i32, _c_void, ctypes.c_size_t, _c_void]),
+    "lx_moe_forward_tree_static": (_c_i32, [ctypes.POINTER(LxTreeLayer), _c_i32, _c_i32, _c_void, _c_void,
+                                            _c_void, _c_void, _c_i32, _c_void]),
     "lx_dense_moe_forward": (_c_i32, [ctypes.POINTER(LxDenseLayer), _c_i32, _c_i32, _c_void, _c_void,
                                       _c_void, _c_void, _c_i32, _c_void, ctypes.c_size_t, _c_void]),
     "lx_bucket": (_c_i32, [ctypes.POINTER(LxTreeLayer), _c_i32, _c_i32, _c_void, _c_i32, _c_void,
@@ -480,6 +482,26 @@ def forward(layer: DeviceLayer, x: torch.Tensor, topk_ids: torch.Tensor, topk_we
     else:
         st = L.lx_moe_forward_tree(ctypes.byref(layer.tree_struct()), *args)
     _check(st)
+    return out
+
+
+STATIC_SCRATCH_BYTES = 64 << 20  # LX_STATIC_SCRATCH_BYTES
+
+
+def forward_static(layer: DeviceLayer, x: torch.Tensor, topk_ids: torch.Tensor, topk_weights: torch.Tensor,
+                   out: torch.Tensor, out_dtype: int = LX_F32, stream=None) -> torch.Tensor:
+    """The tree forward on the library's static per-GPU scratch
+    (lx_moe_forward_tree_static): no workspace, nothing allocated by the
+    call; ``out`` is caller-provided. Flat layers run as their one-level
+    tree."""
+    T, k = int(topk_ids.shape[0]), int(topk_ids.shape[1])
+    for name, t in (("x", x), ("topk_ids", topk_ids), ("topk_weights", topk_weights), ("out", out)):
+        if not t.is_contiguous():
+            raise ValueError(f"{name} must be contiguous")
+    if topk_ids.dtype != torch.int32 or topk_weights.dtype != torch.float32:
+        raise ValueError("topk_ids must be int32 and topk_weights float32")
+    _check(lib().lx_moe_forward_tree_static(ctypes.byref(layer.tree_struct()), T, k, _ptr(x), _ptr(topk_ids),
+                                            _ptr(topk_weights), _ptr(out), out_dtype, _stream(stream)))
     return out
 
 

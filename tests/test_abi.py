@@ -28,7 +28,7 @@ def _declared(root):
 
 def test_every_declared_symbol_is_exported(L, root):
     names = _declared(root)
-    assert len(names) == len(lx.EXPORTS) == 29
+    assert len(names) == len(lx.EXPORTS) == 30
     for n in names:
         assert hasattr(L, n), n
         assert n in lx.EXPORTS, n
@@ -295,3 +295,20 @@ def test_aux_stream_switch(L):
     assert L.lx_set_aux_stream(7) == 0          # any non-zero value enables
     assert lx.set_aux_stream(True) is True
     assert lx.set_aux_stream(True) is True
+
+
+def test_static_forward_refuses_batches_beyond_its_scratch(L):
+    """lx_moe_forward_tree_static: a batch whose workspace exceeds the static
+    scratch is refused on the host, before any device call (T = 4096 at the
+    30B-A3B shape needs about 1.1 GB); invalid arguments likewise."""
+    s = _tree()
+    assert L.lx_moe_tree_workspace_bytes(ctypes.byref(s), 4096, 8) > lx.STATIC_SCRATCH_BYTES
+    st = L.lx_moe_forward_tree_static(ctypes.byref(s), 4096, 8, FAKE, FAKE, FAKE, FAKE, lx.LX_F32, None)
+    assert st == lx.LX_ERR_WORKSPACE_TOO_SMALL
+    msg = L.lx_last_error().decode()
+    assert "static scratch" in msg and str(lx.STATIC_SCRATCH_BYTES) in msg
+    assert L.lx_moe_forward_tree_static(None, 4, 8, FAKE, FAKE, FAKE, FAKE, lx.LX_F32, None) == \
+        lx.LX_ERR_INVALID_ARGUMENT
+    assert L.lx_moe_forward_tree_static(ctypes.byref(s), 4, 0, FAKE, FAKE, FAKE, FAKE, lx.LX_F32, None) == \
+        lx.LX_ERR_INVALID_ARGUMENT
+    assert L.lx_moe_tree_workspace_bytes(ctypes.byref(s), 64, 8) <= lx.STATIC_SCRATCH_BYTES
