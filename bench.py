@@ -622,6 +622,7 @@ def main():
         "clustering": clustering,
         "stage3": stage3,
         "cpu_baseline": cpu,
+        "kernel_sources_sha": source_sha(),
     }
     print(json.dumps(res), flush=True)
 
@@ -724,7 +725,8 @@ def summarize_profile(a):
         for i, (_, v) in enumerate(tail):
             per[roles[i % n]].append(v * 1024.0 * sc[ctr])
         cnt[ctr] = {r: statistics.mean(v) if v else None for r, v in per.items()}
-    sha = source_sha()
+    # the sources the profiled run was built from (its JSON line records them)
+    sha = line.get("kernel_sources_sha") or source_sha()
     lines = [f"# rocprofv3 kernel summary: {wl}", "",
              f"Kernel sources sha256[:16] = `{sha}`.", "",
              "Commands (from the repository root on one MI355X, after `cd /tmp && export TMPDIR=/tmp`; "

@@ -80,8 +80,24 @@ __global__ __launch_bounds__(1024) void k_prepare(PrepareArgs a) {
   __syncthreads();
   const uint32_t bad = prepare_tables(a);
   if (bad) atomicOr(&s_bad, bad);
-  __syncthreads();
+  __syncthreads();  // (also orders the tables written above for the loop below)
+  if (a.path_work) {
+    // an expert's path does correction work if any of its nodes carries a
+    // factor (broken paths: none)
+    for (int e = threadIdx.x; e < a.E; e += blockDim.x) {
+      uint8_t pw = 0;
+      for (int l = 1; l <= a.L; ++l) {
+        const int n = a.anc[(int64_t)l * a.E + e];
+        if (n >= 0 && a.fac[l][n] >= 0) pw = 1;
+      }
+      a.path_work[e] = pw;
+    }
+  }
   if (threadIdx.x == 0) *a.flags = s_bad;
+}
+
+__device__ __forceinline__ bool node_works(const BucketLevel& lv, int n) {
+  return lv.work_all || (lv.work_node ? lv.work_node[n] != 0 : lv.fac[n] >= 0);
 }
 
 __device__ inline int node_of(const BucketArgs& a, int l, int e) {
@@ -169,14 +185,14 @@ __device__ inline void build_tile_tables(const BucketLevel& lv, const int32_t* o
     TileEntry* tiles = lv.tiles[tab];
     int my_tiles = 0;
     for (int n = nb; n < ne; ++n) {
-      const bool work = lv.work_all || fac[n] >= 0;
+      const bool work = lv.work_all || (lv.work_node ? lv.work_node[n] != 0 : fac[n] >= 0);
       const int cnt = off[n + 1] - off[n];
       if (work && cnt > 0) my_tiles += (cnt + bm - 1) / bm;
     }
     int ntiles = 0;
     int tpos = block_exscan(my_tiles, s_wave, ntiles);
     for (int n = nb; n < ne; ++n) {
-      const bool work = lv.work_all || fac[n] >= 0;
+      const bool work = lv.work_all || (lv.work_node ? lv.work_node[n] != 0 : fac[n] >= 0);
       const int o = off[n];
       const int cnt = off[n + 1] - o;
       if (!work || cnt == 0) continue;
@@ -283,7 +299,7 @@ __global__ __launch_bounds__(kPlaceThr) void k_bucket_place(BucketArgs a) {
     bool first = true;
     for (int j2 = 0; j2 < j; ++j2) first &= (s_node[t * k + j2] != n);
     if (first) lv.row_token[row] = t0 + t;
-    const bool work = lv.work_all || lv.fac[n] >= 0;
+    const bool work = node_works(lv, n);
     lv.slot_flags[gs] = (uint8_t)((first ? 1 : 0) | (work ? 2 : 0));
     // expert level: summed weight of each distinct expert, on its first slot
     if (l == a.L && a.w) {
@@ -293,6 +309,29 @@ __global__ __launch_bounds__(kPlaceThr) void k_bucket_place(BucketArgs a) {
           if (s_node[t * k + j2] == n) ws += a.w[(int64_t)(t0 + t) * k + j2];
       a.slot_wsum[gs] = ws;
     }
+  }
+}
+
+// One thread per routing slot; the first slot of each leaf row writes that
+// row's map entries. A level-l row's first slot is the token's lowest slot
+// with that row; the leaf row holding it is the one that carries the row's
+// term in a merged product.
+__global__ __launch_bounds__(256) void k_leaf_maps(LeafMapArgs a) {
+  const int64_t s = (int64_t)blockIdx.x * blockDim.x + threadIdx.x;
+  const int L = a.L, k = a.k;
+  if (blockIdx.x == 0)
+    for (int l = 1; l < L; ++l)
+      for (int i = threadIdx.x; i < a.zero_bytes[l] / 4; i += blockDim.x) ((uint32_t*)a.zero_rows[l])[i] = 0u;
+  if (s >= (int64_t)a.T * k) return;
+  if (!(a.slot_flags[L][s] & 1)) return;  // not the first slot of a leaf row (or dropped)
+  const int rL = a.slot_row[L][s];
+  const int64_t t0 = s - s % k;
+  for (int l = 1; l < L; ++l) {
+    const int rl = a.slot_row[l][s];
+    int64_t f = t0;
+    while (a.slot_row[l][f] != rl) ++f;  // terminates at s at the latest
+    a.leaf_row_map[l][rL] = rl;
+    a.leaf_first_map[l][rL] = a.slot_row[L][f] == rL ? rl : -1;
   }
 }
 
@@ -527,6 +566,13 @@ hipError_t launch_bucket_small(const PrepareArgs& pa, const BucketArgs& a, hipSt
     case 3: hipLaunchKernelGGL(k_bucket_small<3>, dim3(1), dim3(1024), sizeof(SmallLds), s, pa, a); break;
     default: hipLaunchKernelGGL(k_bucket_small<4>, dim3(1), dim3(1024), sizeof(SmallLds), s, pa, a); break;
   }
+  return hipGetLastError();
+}
+
+hipError_t launch_leaf_maps(const LeafMapArgs& a, hipStream_t s) {
+  const int64_t n = (int64_t)a.T * a.k;
+  const int grid = (int)((n + 255) / 256);
+  hipLaunchKernelGGL(k_leaf_maps, dim3(grid > 0 ? grid : 1), dim3(256), 0, s, a);
   return hipGetLastError();
 }
 

@@ -201,6 +201,9 @@ void k_gemm_big(GemmArgs p, int ntn) {
     // The two weight parts form one column range [0, ncol): column n < ncols[0]
     // is row n of part 0, otherwise row n - ncols[0] of part 1.
     const TileEntry te = p.tiles[ti];
+    // a leaf-level tile whose node has no factor of its own (it is listed
+    // for the products that merge the levels above it): nothing to do here
+    if (te.widx < 0) continue;
     const int n0 = nt * BN;
     const int tpart = n0 < p.ncols[0] ? 0 : 1;
     const int akoff = p.a_koff[tpart];
@@ -531,6 +534,237 @@ void k_gemm_big(GemmArgs p, int ntn) {
           } else {
             *(float4*)(p.C + (int64_t)(te.row0 + r) * p.ldc + col) = v;
           }
+        }
+      }
+    }
+    bar();  // the next item's loads overwrite the epilogue's LDS
+  }
+}
+
+// ---------------------------------------------------------------- segmented
+// The correction products of several tree levels that land on the same rows
+// (the leaf rows), as one 256 x 256-tile GEMM whose K runs over the levels'
+// operands in turn (segments). Everything else is the 256 x 256 f24
+// configuration of k_gemm_big: 8 wavefronts in a 2 x 4 grid of 128 x 64
+// blocks, both operands HBM -> LDS by direct loads into a 2-stage ring of
+// 64-wide K-slabs, persistent XCD-ordered work items, epilogue through LDS.
+// Within a segment of rank r the slabs alternate hi and lo halves of A
+// against each 64-column weight slab (K = 2 r, the weight slab read twice
+// back to back). A segment's A rows come through its own row map (entries
+// below 0 read the segment's zero row), its weights from its own level.
+constexpr int kSegMax = LX_MAX_LEVELS;
+
+__global__ __launch_bounds__(512, 1) __attribute__((amdgpu_waves_per_eu(2, 2)))
+void k_gemm_seg(GemmArgs p, SegArgs sg, int ntn) {
+  constexpr int BM = 256, BN = 256, NTHR = 512, WGN = 4;
+  constexpr int MI = BM / 64, NI = BN / (32 * WGN), WM = BM / 2, WN = BN / WGN;
+  constexpr int A_ROUNDS = BM * 8 / NTHR, B_ROUNDS = BN * 8 / NTHR, ROUNDS = A_ROUNDS + B_ROUNDS;
+  constexpr int SA = BM * BK2, SB = BN * BK2;
+  __shared__ __attribute__((aligned(1024))) u16 smem[2 * (SA + SB)];
+  u16* const sA0 = smem;
+  u16* const sB0 = smem + SA;
+  u16* const sA1 = smem + SA + SB;
+  u16* const sB1 = smem + 2 * SA + SB;
+
+  const int real = *p.n_tiles * ntn;
+  const int q = real / NXCD, rmd = real % NXCD;
+  const int x = blockIdx.x % NXCD;
+  const int xbeg = x * q + (x < rmd ? x : rmd);
+  const int xend = xbeg + q + (x < rmd ? 1 : 0);
+  const int mx = ((int)gridDim.x - x + NXCD - 1) / NXCD;
+  const int ncol = p.ncols[0] + p.ncols[1];
+  const int nseg = sg.nseg;
+
+  for (int Lg = xbeg + (int)blockIdx.x / NXCD; Lg < xend; Lg += mx) {
+    int tid = threadIdx.x;
+    asm volatile("" : "+v"(tid));
+    const int wave = tid >> 6, lane = tid & 63;
+    const int wm = wave / WGN, wn = wave % WGN;
+    const int ti = Lg / ntn, nt = Lg % ntn;
+    const TileEntry te = p.tiles[ti];
+    const int n0 = nt * BN;
+    const int tpart = n0 < p.ncols[0] ? 0 : 1;
+
+    // factor index and slab count of every segment for this tile (slab
+    // counts 0 for segments that do not apply)
+    int widx[kSegMax], nsl[kSegMax];
+    int nk = 0;
+#pragma unroll
+    for (int sI = 0; sI < kSegMax; ++sI) {
+      int w = -1;
+      if (sI < nseg) {
+        const SegDesc& dsc = sg.s[sI];
+        if (dsc.anc_off < 0) {
+          w = te.widx;
+        } else {
+          const int node = sg.anc[dsc.anc_off + te.node];
+          w = node >= 0 ? dsc.fac[node] : -1;
+        }
+      }
+      widx[sI] = w;
+      nsl[sI] = w >= 0 ? 2 * sg.s[sI].rank / BK2 : 0;
+      nk += nsl[sI];
+    }
+
+    // operand addresses of the segment being issued (set at its first slab)
+    int cur = -1, crank = 0;
+    const u16* Ab = nullptr;
+    uint32_t aoff[A_ROUNDS];
+    const u16* bptr[B_ROUNDS];
+    auto set_seg = [&](int sI) {
+      const SegDesc& dsc = sg.s[sI];
+      int w = 0;
+#pragma unroll
+      for (int u = 0; u < kSegMax; ++u)
+        if (u == sI) w = widx[u];
+      Ab = (const u16*)dsc.A;
+      crank = dsc.rank;
+      const int akoff = tpart ? dsc.akoff1 : 0;
+#pragma unroll
+      for (int j = 0; j < A_ROUNDS; ++j) {
+        const int Ps = j * NTHR + tid;
+        const int row = Ps >> 3;
+        const int c = (Ps & 7) ^ swzb(row);
+        const int r = row < te.nrows ? row : te.nrows - 1;
+        int src = dsc.map ? dsc.map[te.row0 + r] : te.row0 + r;
+        if (src < 0) src = dsc.zero_row;
+        aoff[j] = (uint32_t)src * (uint32_t)dsc.lda + (uint32_t)(akoff + c * 8);
+      }
+      const u16* const Bw0 = (const u16*)dsc.B[0] + (int64_t)w * dsc.b_stride[0];
+      const u16* const Bw1 = (const u16*)dsc.B[1] + (int64_t)w * dsc.b_stride[1];
+#pragma unroll
+      for (int j = 0; j < B_ROUNDS; ++j) {
+        const int Ps = j * NTHR + tid;
+        const int row = Ps >> 3;
+        const int c = (Ps & 7) ^ swzb(row);
+        const int n = n0 + row < ncol ? n0 + row : ncol - 1;
+        bptr[j] = (n < p.ncols[0] ? Bw0 + (int64_t)n * crank : Bw1 + (int64_t)(n - p.ncols[0]) * crank) + c * 8;
+      }
+    };
+    // slab kt: segment and slab within it (slabs of a segment: weight slab
+    // qq, hi then lo)
+    auto issue = [&](u16* sA_, u16* sB_, int kt) {
+      int sel = 0, loc = kt;
+      bool found = false;
+#pragma unroll
+      for (int u = 0; u < kSegMax; ++u) {
+        if (!found) {
+          if (loc < nsl[u]) {
+            sel = u;
+            found = true;
+          } else {
+            loc -= nsl[u];
+          }
+        }
+      }
+      if (sel != cur) {
+        set_seg(sel);
+        cur = sel;
+      }
+      const int qq = loc >> 1, per = loc & 1;
+      const int kb = qq * BK2, ka = per * crank + kb;
+#pragma unroll
+      for (int j = 0; j < A_ROUNDS; ++j)
+        load_lds16(Ab + (aoff[j] + (uint32_t)ka), &sA_[(j * NTHR + wave * 64) * 8]);
+#pragma unroll
+      for (int j = 0; j < B_ROUNDS; ++j) load_lds16(bptr[j] + kb, &sB_[(j * NTHR + wave * 64) * 8]);
+    };
+
+    f32x16 acc[MI][NI];
+#pragma unroll
+    for (int mi = 0; mi < MI; ++mi)
+#pragma unroll
+      for (int ni = 0; ni < NI; ++ni)
+#pragma unroll
+        for (int i = 0; i < 16; ++i) acc[mi][ni][i] = 0.f;
+
+    bf16x8 fa0[MI], fb0[NI], fa1[MI], fb1[NI];
+#define LX_SFRAG(SA_, SB_, KS, FA, FB)                                              \
+  do {                                                                              \
+    const int kc_ = (KS) * 2 + (lane >> 5);                                         \
+    _Pragma("unroll") for (int mi = 0; mi < MI; ++mi)                               \
+      FA[mi] = *(const bf16x8*)&(SA_)[lds_offb(wm * WM + mi * 32 + (lane & 31), kc_)]; \
+    _Pragma("unroll") for (int ni = 0; ni < NI; ++ni)                               \
+      FB[ni] = *(const bf16x8*)&(SB_)[lds_offb(wn * WN + ni * 32 + (lane & 31), kc_)]; \
+  } while (0)
+#define LX_SMFMAS(FA, FB)                                                           \
+  do {                                                                              \
+    _Pragma("unroll") for (int mi = 0; mi < MI; ++mi)                               \
+      _Pragma("unroll") for (int ni = 0; ni < NI; ++ni)                             \
+        acc[mi][ni] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(FA[mi], FB[ni], acc[mi][ni], 0, 0, 0); \
+  } while (0)
+#define LX_SCOMPUTE(SA_, SB_)                                                       \
+  do {                                                                              \
+    LX_SFRAG(SA_, SB_, 0, fa0, fb0);                                                \
+    __builtin_amdgcn_sched_barrier(0);                                              \
+    LX_SFRAG(SA_, SB_, 1, fa1, fb1);                                                \
+    __builtin_amdgcn_sched_barrier(0);                                              \
+    LX_SMFMAS(fa0, fb0);                                                            \
+    __builtin_amdgcn_sched_barrier(0);                                              \
+    LX_SFRAG(SA_, SB_, 2, fa0, fb0);                                                \
+    __builtin_amdgcn_sched_barrier(0);                                              \
+    LX_SMFMAS(fa1, fb1);                                                            \
+    __builtin_amdgcn_sched_barrier(0);                                              \
+    LX_SFRAG(SA_, SB_, 3, fa1, fb1);                                                \
+    __builtin_amdgcn_sched_barrier(0);                                              \
+    LX_SMFMAS(fa0, fb0);                                                            \
+    __builtin_amdgcn_sched_barrier(0);                                              \
+    LX_SMFMAS(fa1, fb1);                                                            \
+  } while (0)
+
+    if (nk > 0) issue(sA0, sB0, 0);
+    if (nk > 1) issue(sA1, sB1, 1);
+    int kt = 0;
+    for (; kt + 1 < nk; kt += 2) {
+      wait_vmcnt<ROUNDS>();
+      bar();
+      LX_SCOMPUTE(sA0, sB0);
+      bar();
+      const bool more0 = kt + 2 < nk;
+      if (more0) issue(sA0, sB0, kt + 2);
+      if (more0)
+        wait_vmcnt<ROUNDS>();
+      else
+        wait_vmcnt<0>();
+      bar();
+      LX_SCOMPUTE(sA1, sB1);
+      bar();
+      if (kt + 3 < nk) issue(sA1, sB1, kt + 3);
+    }
+    if (kt < nk) {  // odd slab count: the last slab is in stage 0
+      wait_vmcnt<0>();
+      bar();
+      LX_SCOMPUTE(sA0, sB0);
+      bar();
+    }
+#undef LX_SCOMPUTE
+#undef LX_SMFMAS
+#undef LX_SFRAG
+
+    // Epilogue (as k_gemm_big's f24 output): per-wavefront LDS transpose,
+    // then 4 consecutive columns per lane.
+    {
+      constexpr int PITCH = WN + 4;
+      constexpr int LPR = WN / 4;
+      constexpr int RPP = 64 / LPR;
+      static_assert(8 * 32 * PITCH * 4 <= (int)sizeof(smem), "epilogue LDS");
+      float* const ep = (float*)smem + wave * (32 * PITCH);
+      const int c4 = (lane % LPR) * 4;
+      const int col = n0 + wn * WN + c4;
+#pragma unroll
+      for (int mi = 0; mi < MI; ++mi) {
+#pragma unroll
+        for (int ni = 0; ni < NI; ++ni)
+#pragma unroll
+          for (int i = 0; i < 16; ++i)
+            ep[(8 * (i >> 2) + 4 * (lane >> 5) + (i & 3)) * PITCH + ni * 32 + (lane & 31)] = acc[mi][ni][i];
+#pragma unroll
+        for (int ps = 0; ps < 32 / RPP; ++ps) {
+          const int rr = ps * RPP + lane / LPR;
+          const float4 v = *(const float4*)&ep[rr * PITCH + c4];
+          const int r = wm * WM + mi * 32 + rr;
+          if (r >= te.nrows || col >= ncol) continue;
+          *(F24x4*)((uint8_t*)p.C + ((int64_t)(te.row0 + r) * p.ldc + col) * 3) = f24_pack(v);
         }
       }
     }
@@ -1054,6 +1288,33 @@ hipError_t launch_gemm_big(const GemmArgs& g, int bm, int bn, int ofmt, int grid
   if (bn == 256) return launch_bn<128, 256>(g, ofmt, grid, ntn, s);
   if (bn == 128) return launch_bn<128, 128>(g, ofmt, grid, ntn, s);
   return launch_bn<128, 64>(g, ofmt, grid, ntn, s);
+}
+
+bool gemm_seg_ok(const GemmArgs& g, const SegArgs& sa, int64_t out_rows) {
+  if (sa.nseg < 1 || sa.nseg > kSegMax || !sa.anc || !g.tiles || !g.n_tiles) return false;
+  const int ncol = g.ncols[0] + g.ncols[1];
+  // tiles never straddle the two parts (their A columns differ)
+  if (g.ncols[1] > 0 && g.ncols[0] % 256) return false;
+  if (g.ncols[0] % 4 || g.ncols[1] % 4 || g.ldc % 4 || g.ldc < ncol || ((uintptr_t)g.C & 3)) return false;
+  if (out_rows * g.ldc * 3 >= ((int64_t)1 << 40)) return false;
+  for (int i = 0; i < sa.nseg; ++i) {
+    const SegDesc& d = sa.s[i];
+    if (!d.A || !d.B[0] || (g.ncols[1] > 0 && !d.B[1]) || d.rank <= 0 || d.rank % BK2) return false;
+    if (d.anc_off >= 0 && !d.fac) return false;
+    if (d.akoff1 + 2 * d.rank > d.lda || (g.ncols[1] == 0 && 2 * d.rank > d.lda)) return false;
+    if (((uintptr_t)d.A & 15) || ((uintptr_t)d.B[0] & 15) || ((uintptr_t)d.B[1] & 15)) return false;
+  }
+  return true;
+}
+
+hipError_t launch_gemm_seg(const GemmArgs& g, const SegArgs& sa, int grid_tiles, hipStream_t s) {
+  const int ntn = (g.ncols[0] + g.ncols[1] + 255) / 256;
+  int grid = grid_tiles * ntn;
+  if (grid <= 0) return hipSuccess;
+  const int cap = grid_cap();
+  if (grid > cap) grid = cap;
+  hipLaunchKernelGGL(k_gemm_seg, dim3(grid), dim3(512), 0, s, g, sa, ntn);
+  return hipGetLastError();
 }
 
 hipError_t launch_gemm_lo8(const GemmArgs& g, int ofmt, int grid_tiles, hipStream_t s) {

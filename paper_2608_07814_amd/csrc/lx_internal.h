@@ -103,6 +103,9 @@ struct BucketLevel {
   int32_t tile_bm[kNumTab];  // tile height of each table
   uint32_t tab_mask;         // bit b: table b is needed (built) at this level
   int32_t work_all;        // 1: every node does GEMM work (anchor level)
+  const uint8_t* work_node;  // if set: node n does work iff work_node[n] != 0
+                             // (the leaf level of a tree whose correction
+                             // outputs are merged: a factor anywhere on the path)
   const int32_t* fac;      // validated factor index per node (-1 none)
   int32_t* hist;           // [n_nodes][n_tok_tiles], scanned in place
   int32_t* offsets;        // [n_nodes + 1]
@@ -136,6 +139,8 @@ struct PrepareArgs {
   const int32_t* factor_of[kMaxLvl];   // factor_of[l] for l >= 1
   int32_t* anc;                        // out [(L + 1) * E]
   int32_t* fac[kMaxLvl];               // out, validated factor index (l >= 1)
+  uint8_t* path_work;                  // out [E] (optional): 1 if a node on the
+                                       // expert's path carries a factor
   uint32_t* flags;
 };
 
@@ -143,6 +148,22 @@ hipError_t launch_prepare(const PrepareArgs& a, hipStream_t s);
 hipError_t launch_bucket_hist(const BucketArgs& a, hipStream_t s);
 hipError_t launch_bucket_scan(const BucketArgs& a, hipStream_t s);
 hipError_t launch_bucket_place(const BucketArgs& a, hipStream_t s);
+// Merged correction outputs of a tree (after placement): for every leaf
+// row r of level L and every intermediate level l (1 <= l < L),
+//   leaf_row_map[l][r]   = the level-l row of r's token and node,
+//   leaf_first_map[l][r] = the same row if r holds that row's first slot,
+//                          else -1 (so each level-l row is counted once);
+// and zero_rows[l] (zero_bytes[l] bytes) is cleared.
+struct LeafMapArgs {
+  int32_t T, k, L;
+  const int32_t* slot_row[kMaxLvl];
+  const uint8_t* slot_flags[kMaxLvl];
+  int32_t* leaf_row_map[kMaxLvl];
+  int32_t* leaf_first_map[kMaxLvl];
+  uint8_t* zero_rows[kMaxLvl];
+  int32_t zero_bytes[kMaxLvl];
+};
+hipError_t launch_leaf_maps(const LeafMapArgs& a, hipStream_t s);
 // Batches of 1..64 tokens: prepare + hist + scan + place in one workgroup.
 bool bucket_small_ok(const BucketArgs& a);
 hipError_t launch_bucket_small(const PrepareArgs& pa, const BucketArgs& a, hipStream_t s);
@@ -222,6 +243,37 @@ hipError_t launch_gemm_lo8(const GemmArgs& g, int ofmt, int grid_tiles, hipStrea
 hipError_t launch_quantize_f8(const void* w, int64_t n_rows, int cols, uint8_t* w8, uint32_t* sc, hipStream_t s);
 hipError_t launch_gemm_big(const GemmArgs& g, int bm, int bn, int ofmt, int grid_tiles,
                            hipStream_t s);
+
+// Segmented large-tile GEMM (256 x 256 tiles, f24 output): the correction
+// products of several tree levels that land on the same output rows, as one
+// GEMM whose K is the concatenation of the levels' (hi | lo) operands:
+//   C[row] = sum over segments s of A_s[map_s(row)] * W_s[widx_s]^T
+// over the tiles of the leaf level (p.tiles, p.n_tiles, p.ncols, p.C,
+// p.ldc; the other GemmArgs fields are unused). Segment s is active for a
+// tile when its factor index widx_s (the tile's own widx for the leaf
+// segment, else the validated factor of the leaf's ancestor at the
+// segment's level) is >= 0; its K is 2 rank (hi then lo against the same
+// weight columns), rank a multiple of 64. An A row index below 0 in a
+// segment's map selects that segment's zero row.
+struct SegDesc {
+  const void* A;           // bf16 [rows][lda]; part 1 starts at column akoff1
+  int64_t lda;             // elements
+  const int32_t* map;      // output row -> A row (null: identity)
+  int32_t zero_row;        // A row of zeros used for map entries < 0
+  int32_t rank;            // weight row length
+  int32_t akoff1;
+  int32_t anc_off;         // level * E into SegArgs::anc; -1: the tile's widx
+  const int32_t* fac;      // validated factor index per node of the level
+  const void* B[2];        // weights of the two parts [widx][n][rank]
+  int64_t b_stride[2];
+};
+struct SegArgs {
+  int32_t nseg;
+  const int32_t* anc;      // [(L + 1) * E] ancestor of each expert per level
+  SegDesc s[LX_MAX_LEVELS];
+};
+bool gemm_seg_ok(const GemmArgs& g, const SegArgs& sa, int64_t out_rows);
+hipError_t launch_gemm_seg(const GemmArgs& g, const SegArgs& sa, int grid_tiles, hipStream_t s);
 
 // Skinny kernel for levels with few rows per node (decode-sized batches):
 // 32-row tiles, 64 output columns per workgroup, a 4-stage LDS ring and
