@@ -115,6 +115,11 @@ def kernel_work(name, P, rows, touched):
         parts = [kernel_work(n, P, rows, touched) for n in name.split("+")]
         return sum(p[0] for p in parts), sum(p[1] for p in parts)
     d, f, T = P["d"], P["f"], P["T"]
+    if name in ("lowrank_gate_up_out_merged", "lowrank_down_out_merged"):
+        # one launch doing every correction level's output product
+        tag = "lowrank_gate_up_out_l" if "gate_up" in name else "lowrank_down_out_l"
+        parts = [kernel_work(f"{tag}{l}", P, rows, touched) for l in range(1, len(P["ranks"]))]
+        return sum(p[0] for p in parts), sum(p[1] for p in parts)
     if name == "anchor_gate_up":
         return 4 * d * f * rows[0], 2 * f * d * 2 * touched[0] + T * d * 2
     if name == "anchor_down":

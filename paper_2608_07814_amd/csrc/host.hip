@@ -109,6 +109,15 @@ struct Plan {
   int T, k, E, L, d, f, NT;
   LevelPlan lv[kMaxLvl];
   size_t flags, anc, slot_wsum, total;
+  // merged: a tree (L >= 2) whose correction levels all run on the
+  // large-tile kernel with ranks that are multiples of 64 computes the gate|up
+  // and down corrections of every level as one product over the leaf rows
+  // (K concatenated over the levels), so the intermediate levels' full-width
+  // outputs are never written; path_work marks the experts whose path has a
+  // factor, leaf_row / leaf_first map leaf rows to intermediate-level rows
+  bool merged = false;
+  size_t path_work = 0;
+  size_t leaf_row[kMaxLvl] = {}, leaf_first[kMaxLvl] = {};
   // kernel choice per level (shapes only): "fast" levels keep every
   // GEMM-feeding intermediate as a bf16 (hi, lo) pair and run on the
   // large-tile or skinny kernel; "skinny" ones (few rows per node) on the
@@ -166,11 +175,24 @@ Plan make_plan(const lx_tree_layer& t, int T, int k) {
       if (work && !p.skinny[l]) p.batch = false;
     }
     p.lo8 = t.anchor_down_f8 && t.anchor_down_f8_scale && p.fast[0] && !p.skinny[0] && p.f % 64 == 0;
+    // (batches of at most 64 tokens always run their fast levels on the
+    // skinny kernel, so merged trees take the four-pass bucketing)
+    p.merged = p.L >= 2 && T > kTokTile && p.f % 256 == 0 && p.d % 256 == 0;
+    for (int l = 1; l <= p.L && p.merged; ++l)
+      p.merged = p.fast[l] && !p.skinny[l] && t.levels[l - 1].rank % 64 == 0;
   }
   p.flags = take(16);  // first: lx_read_device_status reads offset 0
   p.anc = take((size_t)(p.L + 1) * p.E * 4);
   const size_t tk = (size_t)T * k;
   p.slot_wsum = take(tk * 4);
+  if (p.merged) {
+    p.path_work = take((size_t)p.E);
+    const size_t rl = (size_t)T * std::min(k, t.E);  // leaf rows, at most
+    for (int l = 1; l < p.L; ++l) {
+      p.leaf_row[l] = take(rl * 4);
+      p.leaf_first[l] = take(rl * 4);
+    }
+  }
   for (int l = 0; l <= p.L; ++l) {
     LevelPlan& q = p.lv[l];
     q.N = level_nodes(t, l);
@@ -195,11 +217,17 @@ Plan make_plan(const lx_tree_layer& t, int T, int k) {
     q.fac = take((size_t)q.N * 4);
     const size_t R = (size_t)q.rows_max;
     const bool work = l == 0 || q.nfac > 0;
-    q.gu = take(work ? R * 2 * p.f * 4 : 0);
+    // merged trees: the intermediate levels' gate|up and down outputs are
+    // folded into the leaf level's (which then exist even without leaf factors)
+    const bool inter = p.merged && l > 0 && l < p.L;
+    const bool leafm = p.merged && l == p.L;
+    q.gu = take((work && !inter) || leafm ? R * 2 * p.f * 4 : 0);
     q.z = take(l > 0 && work ? R * 2 * q.rank * 4 : 0);
-    q.hbar = take(work ? R * p.f * 4 : 0);
-    q.v = take(l > 0 && work ? R * q.rank * 4 : 0);
-    q.y = take(work ? R * p.d * 4 : 0);
+    q.hbar = take(work || leafm ? R * p.f * 4 : 0);
+    // (+1 row: the zero row a merged down product reads for rows that do not
+    // carry this level's term)
+    q.v = take(l > 0 && work ? (R + (inter ? 1 : 0)) * q.rank * 4 : 0);
+    q.y = take((work && !inter) || leafm ? R * p.d * 4 : 0);
     // one counter per work item of the level's widest skinny product
     const int widest = std::max(std::max(2 * p.f, p.d), 2 * q.rank);
     q.n_cnt = p.skinny[l] && work && T > 0 ? q.tiles_max[kTabSkinny] * ((widest + kSkinnyBN - 1) / kSkinnyBN) : 0;
@@ -418,6 +446,7 @@ lx_status run(const lx_tree_layer& t, int T, int k, const void* x, const int32_t
   pa.L = L;
   pa.anc = (int32_t*)(W + P.anc);
   pa.flags = (uint32_t*)(W + P.flags);
+  pa.path_work = P.merged ? (uint8_t*)(W + P.path_work) : nullptr;
   for (int l = 0; l <= L; ++l) {
     pa.n_nodes[l] = P.lv[l].N;
     if (l > 0) {
@@ -456,6 +485,7 @@ lx_status run(const lx_tree_layer& t, int T, int k, const void* x, const int32_t
     // (also 128-row large-tile) and 256-row tables
     b.tab_mask = skinny[l] ? 1u << kTabSkinny : (1u << kTabSmall) | (1u << kTabBig);
     b.work_all = l == 0;
+    b.work_node = P.merged && l == L ? pa.path_work : nullptr;
     b.fac = l > 0 ? (const int32_t*)(W + q.fac) : nullptr;
     b.hist = (int32_t*)(W + q.hist);
     b.offsets = (int32_t*)(W + q.offsets);
@@ -469,7 +499,7 @@ lx_status run(const lx_tree_layer& t, int T, int k, const void* x, const int32_t
     b.split_cnt = (uint32_t*)(W + q.cnt);
     b.n_split_cnt = (int32_t)q.n_cnt;
   }
-  if (bucket_small_ok(ba)) {
+  if (bucket_small_ok(ba) && !P.merged) {
     LX_LAUNCH("bucket_small", launch_bucket_small(pa, ba, lstream));
   } else {
     LX_LAUNCH("bucket_prepare", launch_prepare(pa, lstream));
@@ -478,6 +508,24 @@ lx_status run(const lx_tree_layer& t, int T, int k, const void* x, const int32_t
     LX_LAUNCH("bucket_place", launch_bucket_place(ba, lstream));
   }
   if (stop == RUN_BUCKET) return LX_OK;
+  if (P.merged) {
+    LeafMapArgs lm{};
+    lm.T = T;
+    lm.k = k;
+    lm.L = L;
+    for (int l = 0; l <= L; ++l) {
+      lm.slot_row[l] = ba.lv[l].slot_row;
+      lm.slot_flags[l] = ba.lv[l].slot_flags;
+      if (l >= 1 && l < L) {
+        lm.leaf_row_map[l] = (int32_t*)(W + P.leaf_row[l]);
+        lm.leaf_first_map[l] = (int32_t*)(W + P.leaf_first[l]);
+        // the zero row of the level's v buffer (row rows_max, 4 r bytes)
+        lm.zero_rows[l] = (uint8_t*)(W + P.lv[l].v) + (size_t)P.lv[l].rows_max * P.lv[l].rank * 4;
+        lm.zero_bytes[l] = t.levels[l - 1].n_factors > 0 ? P.lv[l].rank * 4 : 0;
+      }
+    }
+    LX_LAUNCH("leaf_maps", launch_leaf_maps(lm, lstream));
+  }
 
   // Decode-sized batches (every level with GEMM work on the skinny kernel):
   // the independent products of one phase share a launch.
@@ -625,9 +673,59 @@ lx_status run(const lx_tree_layer& t, int T, int k, const void* x, const int32_t
       LX_TRY(small("anchor_gate_up", g, 0, A_BF16));
   }
   LX_TRY(flush());
-  // correction gate|up per level, part 2: dgu = A z
+  // correction gate|up per level, part 2: dgu = A z (merged trees: one
+  // product over the leaf rows, dgu_L = sum over levels of A_l z_l)
   lstream = side;
-  for (int l = 1; l <= L; ++l) {
+  auto seg_args = [&](bool down) {
+    SegArgs sa{};
+    sa.anc = pa.anc;
+    for (int l = 1; l <= L; ++l) {
+      const lx_level& v = t.levels[l - 1];
+      if (v.n_factors == 0) continue;
+      const LevelPlan& q = P.lv[l];
+      const int r = v.rank;
+      SegDesc& sd = sa.s[sa.nseg++];
+      sd.rank = r;
+      sd.anc_off = l == L ? -1 : l * E;
+      sd.fac = l == L ? nullptr : (const int32_t*)(W + q.fac);
+      if (!down) {
+        sd.A = W + q.z;
+        sd.lda = 4 * (int64_t)r;  // [gate hi | gate lo | up hi | up lo]
+        sd.akoff1 = 2 * r;
+        sd.map = l == L ? nullptr : (const int32_t*)(W + P.leaf_row[l]);
+        sd.zero_row = 0;
+        sd.B[0] = v.a_gate;
+        sd.B[1] = v.a_up;
+        sd.b_stride[0] = sd.b_stride[1] = (int64_t)f * r;
+      } else {
+        sd.A = W + q.v;
+        sd.lda = 2 * (int64_t)r;  // [hi | lo]
+        sd.akoff1 = 0;
+        sd.map = l == L ? nullptr : (const int32_t*)(W + P.leaf_first[l]);
+        sd.zero_row = (int32_t)q.rows_max;
+        sd.B[0] = sd.B[1] = v.a_down;
+        sd.b_stride[0] = sd.b_stride[1] = (int64_t)d * r;
+      }
+    }
+    return sa;
+  };
+  auto seg = [&](const char* name, bool down) -> lx_status {
+    const LevelPlan& q = P.lv[L];
+    const SegArgs sa = seg_args(down);
+    GemmArgs g{};
+    g.tiles = ba.lv[L].tiles[kTabBig];
+    g.n_tiles = ba.lv[L].n_tiles[kTabBig];
+    g.ncols[0] = down ? d : f;
+    g.ncols[1] = down ? 0 : f;
+    g.C = (float*)(W + (down ? q.y : q.gu));
+    g.ldc = down ? d : 2 * (int64_t)f;
+    if (!gemm_seg_ok(g, sa, q.rows_max))
+      return fail(LX_ERR_UNSUPPORTED, std::string(name) + ": shape not supported by the merged GEMM");
+    LX_LAUNCH(name, launch_gemm_seg(g, sa, (int)q.tiles_max[kTabBig], lstream));
+    return LX_OK;
+  };
+  if (P.merged) LX_TRY(seg("lowrank_gate_up_out_merged", false));
+  for (int l = 1; l <= L && !P.merged; ++l) {
     const LevelPlan& q = P.lv[l];
     const lx_level& v = t.levels[l - 1];
     if (v.n_factors == 0) continue;
@@ -679,6 +777,7 @@ lx_status run(const lx_tree_layer& t, int T, int k, const void* x, const int32_t
   }
   ta.out = out;
   ta.out_dtype = out_dtype;
+  ta.merged = P.merged ? 1 : 0;
   LX_HIP(fj_up.join());
   LX_LAUNCH("swiglu_reduce", launch_swiglu_reduce(ta, lstream));
   LX_HIP(fj_down.fork());
@@ -746,8 +845,11 @@ lx_status run(const lx_tree_layer& t, int T, int k, const void* x, const int32_t
     }
   }
   LX_TRY(flush());
-  // correction down per level, part 2: y = A_down v
-  for (int l = 1; l <= L; ++l) {
+  // correction down per level, part 2: y = A_down v (merged trees: one
+  // product over the leaf rows; a level-l row's term rides on the leaf row of
+  // its first slot)
+  if (P.merged) LX_TRY(seg("lowrank_down_out_merged", true));
+  for (int l = 1; l <= L && !P.merged; ++l) {
     const LevelPlan& q = P.lv[l];
     const lx_level& v = t.levels[l - 1];
     if (v.n_factors == 0) continue;

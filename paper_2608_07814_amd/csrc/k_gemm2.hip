@@ -606,11 +606,12 @@ void k_gemm_seg(GemmArgs p, SegArgs sg, int ntn) {
       nk += nsl[sI];
     }
 
-    // operand addresses of the segment being issued (set at its first slab)
+    // operand addresses of the segment being issued (set at its first slab):
+    // wave-uniform bases and 32-bit per-lane byte offsets
     int cur = -1, crank = 0;
     const u16* Ab = nullptr;
-    uint32_t aoff[A_ROUNDS];
-    const u16* bptr[B_ROUNDS];
+    const u16* Bb = nullptr;
+    uint32_t aoff[A_ROUNDS], boff[B_ROUNDS];
     auto set_seg = [&](int sI) {
       const SegDesc& dsc = sg.s[sI];
       int w = 0;
@@ -628,17 +629,19 @@ void k_gemm_seg(GemmArgs p, SegArgs sg, int ntn) {
         const int r = row < te.nrows ? row : te.nrows - 1;
         int src = dsc.map ? dsc.map[te.row0 + r] : te.row0 + r;
         if (src < 0) src = dsc.zero_row;
-        aoff[j] = (uint32_t)src * (uint32_t)dsc.lda + (uint32_t)(akoff + c * 8);
+        aoff[j] = ((uint32_t)src * (uint32_t)dsc.lda + (uint32_t)(akoff + c * 8)) * 2u;
       }
-      const u16* const Bw0 = (const u16*)dsc.B[0] + (int64_t)w * dsc.b_stride[0];
-      const u16* const Bw1 = (const u16*)dsc.B[1] + (int64_t)w * dsc.b_stride[1];
+      // the tile lies inside one part: one weight matrix for all its rows
+      Bb = (const u16*)dsc.B[tpart] + (int64_t)w * dsc.b_stride[tpart];
+      const int nbase = tpart ? p.ncols[0] : 0;
+      const int nlast = tpart ? ncol - 1 : p.ncols[0] - 1;
 #pragma unroll
       for (int j = 0; j < B_ROUNDS; ++j) {
         const int Ps = j * NTHR + tid;
         const int row = Ps >> 3;
         const int c = (Ps & 7) ^ swzb(row);
-        const int n = n0 + row < ncol ? n0 + row : ncol - 1;
-        bptr[j] = (n < p.ncols[0] ? Bw0 + (int64_t)n * crank : Bw1 + (int64_t)(n - p.ncols[0]) * crank) + c * 8;
+        const int n = n0 + row < nlast ? n0 + row : nlast;
+        boff[j] = ((uint32_t)(n - nbase) * (uint32_t)crank + (uint32_t)(c * 8)) * 2u;
       }
     };
     // slab kt: segment and slab within it (slabs of a segment: weight slab
@@ -665,9 +668,10 @@ void k_gemm_seg(GemmArgs p, SegArgs sg, int ntn) {
       const int kb = qq * BK2, ka = per * crank + kb;
 #pragma unroll
       for (int j = 0; j < A_ROUNDS; ++j)
-        load_lds16(Ab + (aoff[j] + (uint32_t)ka), &sA_[(j * NTHR + wave * 64) * 8]);
+        load_lds16_sb(Ab, aoff[j] + (uint32_t)ka * 2u, &sA_[(j * NTHR + wave * 64) * 8]);
 #pragma unroll
-      for (int j = 0; j < B_ROUNDS; ++j) load_lds16(bptr[j] + kb, &sB_[(j * NTHR + wave * 64) * 8]);
+      for (int j = 0; j < B_ROUNDS; ++j)
+        load_lds16_sb(Bb, boff[j] + (uint32_t)kb * 2u, &sB_[(j * NTHR + wave * 64) * 8]);
     };
 
     f32x16 acc[MI][NI];
@@ -712,30 +716,20 @@ void k_gemm_seg(GemmArgs p, SegArgs sg, int ntn) {
     LX_SMFMAS(fa1, fb1);                                                            \
   } while (0)
 
-    if (nk > 0) issue(sA0, sB0, 0);
-    if (nk > 1) issue(sA1, sB1, 1);
-    int kt = 0;
-    for (; kt + 1 < nk; kt += 2) {
-      wait_vmcnt<ROUNDS>();
-      bar();
-      LX_SCOMPUTE(sA0, sB0);
-      bar();
-      const bool more0 = kt + 2 < nk;
-      if (more0) issue(sA0, sB0, kt + 2);
-      if (more0)
+    // 2-stage ring: slab kt lives in stage kt & 1; one issue site and one
+    // compute site (the segment switch inside issue() is then inlined once)
+    for (int i = 0; i < 2 && i < nk; ++i) issue(i ? sA1 : sA0, i ? sB1 : sB0, i);
+    for (int kt = 0; kt < nk; ++kt) {
+      u16* const cA = (kt & 1) ? sA1 : sA0;
+      u16* const cB = (kt & 1) ? sB1 : sB0;
+      if (kt + 1 < nk)
         wait_vmcnt<ROUNDS>();
       else
         wait_vmcnt<0>();
       bar();
-      LX_SCOMPUTE(sA1, sB1);
+      LX_SCOMPUTE(cA, cB);
       bar();
-      if (kt + 3 < nk) issue(sA1, sB1, kt + 3);
-    }
-    if (kt < nk) {  // odd slab count: the last slab is in stage 0
-      wait_vmcnt<0>();
-      bar();
-      LX_SCOMPUTE(sA0, sB0);
-      bar();
+      if (kt + 2 < nk) issue(cA, cB, kt + 2);
     }
 #undef LX_SCOMPUTE
 #undef LX_SMFMAS
@@ -1303,6 +1297,8 @@ bool gemm_seg_ok(const GemmArgs& g, const SegArgs& sa, int64_t out_rows) {
     if (d.anc_off >= 0 && !d.fac) return false;
     if (d.akoff1 + 2 * d.rank > d.lda || (g.ncols[1] == 0 && 2 * d.rank > d.lda)) return false;
     if (((uintptr_t)d.A & 15) || ((uintptr_t)d.B[0] & 15) || ((uintptr_t)d.B[1] & 15)) return false;
+    // 32-bit byte offsets: the weight rows of one factor
+    if ((int64_t)ncol * d.rank * 2 >= ((int64_t)1 << 31)) return false;
   }
   return true;
 }

@@ -126,7 +126,7 @@ __global__ __launch_bounds__(kTokThr * kSlotGroups) void k_swiglu_reduce(TokenAr
     const bool f0 = a.f24[0] != 0;
     float4 g = ldrow4(a.gu0, f0, m.row[0][j], ld, c), u = ldrow4(a.gu0, f0, m.row[0][j], ld, f + c);
     for (int l = 1; l <= L; ++l) {
-      if (!(m.fl[l][j] & 2)) continue;
+      if (!(m.fl[l][j] & 2) || (a.merged && l < L)) continue;
       const bool fl = a.f24[l] != 0;
       add4(g, ldrow4(a.dgu[l], fl, m.row[l][j], ld, c));
       add4(u, ldrow4(a.dgu[l], fl, m.row[l][j], ld, f + c));
@@ -175,7 +175,7 @@ __global__ __launch_bounds__(kCombMaxThr) void k_combine(TokenArgs a) {
         const int l = q / k, j = q - l * k;
         const int64_t sl = (int64_t)t * k + j;
         const int row = a.slot_row[l][sl];  // loaded alongside the flags
-        if ((a.slot_flags[l][sl] & 3) == 3) {
+        if ((a.slot_flags[l][sl] & 3) == 3 && !(a.merged && l > 0 && l < L)) {
           take = true;
           f24 = a.f24[l] != 0;
           ptr = (const uint8_t*)a.y[l] + (int64_t)row * d * (f24 ? 3 : 4);
@@ -287,6 +287,7 @@ __global__ __launch_bounds__(kFastThr) void k_swiglu_fast(TokenArgs a) {
   int row[NL + 1][kFastK], fl[NL + 1][kFastK];
   float w[kFastK];
   token_meta_fast<NL>(a, t, row, fl, w);
+  const bool merged = a.merged != 0;
   // loads of every distinct expert's gate|up rows, then h = w silu(g) u
   Raw4<F24> gv[kFastK][NL + 1], uv[kFastK][NL + 1];
 #pragma unroll
@@ -296,7 +297,7 @@ __global__ __launch_bounds__(kFastThr) void k_swiglu_fast(TokenArgs a) {
     uv[j][0] = ldraw<F24>(a.gu0, row[0][j], ld, f + c);
 #pragma unroll
     for (int l = 1; l <= NL; ++l) {
-      if (!(fl[l][j] & 2)) continue;
+      if (!(fl[l][j] & 2) || (merged && l < NL)) continue;
       gv[j][l] = ldraw<F24>(a.dgu[l], row[l][j], ld, c);
       uv[j][l] = ldraw<F24>(a.dgu[l], row[l][j], ld, f + c);
     }
@@ -309,7 +310,7 @@ __global__ __launch_bounds__(kFastThr) void k_swiglu_fast(TokenArgs a) {
     float4 g = cvt<F24>(gv[j][0]), u = cvt<F24>(uv[j][0]);
 #pragma unroll
     for (int l = 1; l <= NL; ++l) {
-      if (!(fl[l][j] & 2)) continue;
+      if (!(fl[l][j] & 2) || (merged && l < NL)) continue;
       add4(g, cvt<F24>(gv[j][l]));
       add4(u, cvt<F24>(uv[j][l]));
     }
@@ -338,18 +339,20 @@ __global__ __launch_bounds__(kFastThr) void k_combine_fast(TokenArgs a) {
   int row[NL + 1][kFastK], fl[NL + 1][kFastK];
   float w[kFastK];
   token_meta_fast<NL>(a, t, row, fl, w);
+  // merged trees: the intermediate levels' terms are in the leaf rows
+  const bool merged = a.merged != 0;
   Raw4<F24> v[NL + 1][kFastK];
 #pragma unroll
   for (int l = 0; l <= NL; ++l)
 #pragma unroll
     for (int j = 0; j < kFastK; ++j)
-      if ((fl[l][j] & 3) == 3) v[l][j] = ldraw<F24>(a.y[l], row[l][j], d, c);
+      if ((fl[l][j] & 3) == 3 && !(merged && l > 0 && l < NL)) v[l][j] = ldraw<F24>(a.y[l], row[l][j], d, c);
   float4 acc = make_float4(0.f, 0.f, 0.f, 0.f);
 #pragma unroll
   for (int l = 0; l <= NL; ++l)
 #pragma unroll
     for (int j = 0; j < kFastK; ++j)
-      if ((fl[l][j] & 3) == 3) add4(acc, cvt<F24>(v[l][j]));
+      if ((fl[l][j] & 3) == 3 && !(merged && l > 0 && l < NL)) add4(acc, cvt<F24>(v[l][j]));
   if (a.out_dtype == LX_F32) {
     *(float4*)((float*)a.out + (int64_t)t * d + c) = acc;
   } else {

@@ -324,6 +324,9 @@ struct TokenArgs {
                                        // scale words [f / 64]
   int32_t hbar_mode[kMaxLvl];
   const float* y[kMaxLvl];             // [rows_l][d] down outputs per level
+  int32_t merged;                      // 1: the gate|up and down corrections of
+                                       // levels 1 .. L-1 are folded into level
+                                       // L's rows (their dgu / y are not read)
   void* out;
   lx_dtype out_dtype;
 };

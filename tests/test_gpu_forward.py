@@ -309,3 +309,50 @@ def test_aux_stream_switch_bitwise():
         finally:
             lx.set_aux_stream(prev)
         assert np.array_equal(a, b), f"cfg{cfg}"
+
+
+def _merged_layer(case):
+    from lxsynth import Level, make_layer_tree
+    from lxsynth.gen import _make_factors
+    if case == "three_levels":
+        base = tiny_tree(E=16, d=512, f=256, n_roots=2, subs=2, r_sub=128, r_leaf=64, dtype="bf16", seed=31)
+        f3 = _make_factors(np.random.default_rng(32), 32, 512, 256, 64, "bf16", 0.3)
+        base.levels.append(Level(parent=(np.arange(32) // 2).astype(np.int32),
+                                 factor_of=np.arange(32, dtype=np.int32), rank=64, **f3))
+        base.levels[1].factor_of[5] = -1
+        base.levels[2].factor_of[[0, 9, 17]] = -1
+        base.E = 32
+        return base, 1024
+    layer = make_layer_tree(64, 512, 256, 2, 4, 128, 64, "bf16", 33)
+    if case == "holes":
+        layer.levels[0].factor_of[1] = -1          # a sub-dominant without a correction
+        layer.levels[1].factor_of[3:11] = -1       # leaves without one (some under that sub)
+    return layer, 2048
+
+
+@pytest.mark.parametrize("case", ["all_factors", "holes", "three_levels"])
+def test_merged_tree_products(case):
+    """Trees whose correction levels all run on the large-tile kernel compute
+    every level's gate|up and down corrections as one product over the leaf
+    rows (K concatenated over the levels; an intermediate level's down term
+    rides on the leaf row of its first slot). Leaves and sub-dominants without
+    factors, dropped and duplicate slots; three levels take the general token
+    kernels. The merged launches must be the ones that ran."""
+    require_gpu()
+    say(f"merged tree products: {case}")
+    layer, T = _merged_layer(case)
+    p = _tiny_problem(layer, T, 4, 34, allow_dupes=(case == "holes"), drop_frac=0.1 if case == "holes" else 0.0)
+    lx.profile_reset()
+    lx.profile_enable(True)
+    try:
+        got = gpu_forward(p)
+        names = set(lx.profile_read())
+    finally:
+        lx.profile_enable(False)
+    assert "lowrank_gate_up_out_merged" in names and "lowrank_down_out_merged" in names, names
+    assert not any(n.startswith("lowrank_down_out_l") for n in names)
+    e = err_ratio(got, _oracle(p))
+    say(f"  err/RMS = {e:.3e}")
+    assert e <= TOL_BF16 and e <= TOL_DESIGN
+    # the same forward with the correction chains on the auxiliary stream
+    assert np.array_equal(got, gpu_forward(p))
