@@ -499,10 +499,30 @@ def run_workload(cfg_index, a, torch, np, lx, headline):
         fwd = [lx.PreparedCall(c, xd, rids, rw, out, ws, kind) for c in copies]
         chain = rotating([(lambda f=f: (route(), f())) for f in fwd])
         cms, _ = time_steps(chain, a.steps, a.warmup, torch)
+        # the router's top-k fused into the bucketing (lx_route_moe_forward_tree)
+        import ctypes
+        L = lx.lib()
+        fused = []
+        for c in copies:
+            desc = c.tree_struct()
+            nws = int(L.lx_route_moe_tree_workspace_bytes(ctypes.byref(desc), T, k))
+            fws = torch.empty(nws, dtype=torch.uint8, device="cuda")
+            args = (ctypes.byref(desc), T, k, xd.data_ptr(), wr.data_ptr(), rids.data_ptr(), rw.data_ptr(),
+                    out.data_ptr(), lx.LX_F32, fws.data_ptr(), nws, None)
+            fused.append((desc, fws, args))
+        ffn = L.lx_route_moe_forward_tree
+        fcall = rotating([(lambda a_=f[2]: ffn(*a_)) for f in fused])
+        fcall()
+        torch.cuda.synchronize()
+        fms, _ = time_steps(fcall, a.steps, a.warmup, torch)
         routed = dict(router_us=round(rms * 1e3, 3),
                       router_gflop=round(2 * T * layer.d * layer.E / 1e9, 3),
                       router_and_forward_ms=round(cms, 4),
-                      router_and_forward_tokens_per_s=round(T / (cms * 1e-3), 1))
+                      router_and_forward_tokens_per_s=round(T / (cms * 1e-3), 1),
+                      fused_router_forward_ms=round(fms, 4),
+                      fused_router_forward_tokens_per_s=round(T / (fms * 1e-3), 1),
+                      fused_saving_us=round((cms - fms) * 1e3, 2))
+        del fused, fcall
 
     res = dict(workload=workload, tokens_per_s=round(tokens_per_s, 1), ms_per_step=round(ms, 4), step_ms=pct,
                wall_s_timed=round(wall, 3), weight_copies=len(copies),

@@ -271,6 +271,32 @@ lx_status lx_route_topk(const void* x, const void* w_r, lx_dtype dtype, int32_t 
                         int32_t k, int32_t* topk_ids, float* topk_weights, void* workspace,
                         size_t workspace_bytes, void* stream);
 
+/* The unchanged router fused into the tree forward (Sec. 3 "Stage 1" and
+ * Fig. overview: the router is left as it is and selects among all experts;
+ * Sec. 5.1: the forward shares work among the experts it selects). The
+ * router's logits x W_r^T run first (as in lx_route_topk); their top-k and
+ * renormalised softmax are computed inside the first bucketing kernel, which
+ * writes topk_ids and topk_weights (outputs here, same values and layout as
+ * lx_route_topk's, bit for bit) and organises them into the rows the forward
+ * shares, so routing and bucketing take one launch fewer than
+ * lx_route_topk followed by lx_moe_forward_tree. Batches of at most 64
+ * tokens, whose bucketing is a single workgroup, keep the router's own top-k
+ * launch (one workgroup would take every token's top-k on one compute
+ * unit). Then the forward as lx_moe_forward_tree on those ids and weights:
+ * out is bitwise the same.
+ *
+ * layer: as for lx_moe_forward_tree, bf16 (LX_ERR_UNSUPPORTED otherwise);
+ * w_r [E][d] bf16, 16-byte aligned; E a multiple of 4 in 4 .. 512, k <=
+ * min(E, LX_MAX_K) (as lx_route_topk); topk_ids [T][k] int32 and
+ * topk_weights [T][k] fp32, caller-owned device memory, fully overwritten;
+ * workspace 256-byte aligned, lx_route_moe_tree_workspace_bytes(layer, T, k)
+ * bytes (0 for an invalid or unsupported call). Asynchronous on `stream`;
+ * the auxiliary-stream conventions of the forward apply. */
+size_t lx_route_moe_tree_workspace_bytes(const lx_tree_layer* layer, int32_t T, int32_t k);
+lx_status lx_route_moe_forward_tree(const lx_tree_layer* layer, int32_t T, int32_t k, const void* x,
+                                    const void* w_r, int32_t* topk_ids, float* topk_weights, void* out,
+                                    lx_dtype out_dtype, void* workspace, size_t workspace_bytes, void* stream);
+
 /* Router profiling and the Coact-NPMI clustering distance (Sec. 3,
  * "Compression pipeline", Stage 1, and "Variants"), from the routing ids of N
  * calibration tokens (topk_ids [N][k] int32, device; ids outside [0, E) and

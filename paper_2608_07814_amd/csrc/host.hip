@@ -418,9 +418,11 @@ const char* intern_name(const std::string& n) {
 enum Stop { RUN_ALL, RUN_BUCKET };
 
 // The whole forward (or just the bucketing) of a validated tree.
+// route: the router's logits, when its top-k is fused into the bucketing
+// (ids and w are then outputs, written by the first bucketing kernel).
 lx_status run(const lx_tree_layer& t, int T, int k, const void* x, const int32_t* ids, const float* w,
               void* out, lx_dtype out_dtype, void* ws, size_t ws_bytes, hipStream_t stream, Stop stop,
-              Plan* plan_out = nullptr) {
+              Plan* plan_out = nullptr, const RouteIn* route = nullptr) {
   lx_status st = check_call(&t, T, k);
   if (st != LX_OK) return st;
   if (stop == RUN_ALL && out_dtype != LX_F32 && out_dtype != LX_BF16)
@@ -476,6 +478,7 @@ lx_status run(const lx_tree_layer& t, int T, int k, const void* x, const int32_t
   ba.slot_wsum = (float*)(W + P.slot_wsum);
   ba.anc = pa.anc;
   ba.flags = pa.flags;
+  if (route) ba.route = *route;
   for (int l = 0; l <= L; ++l) {
     const LevelPlan& q = P.lv[l];
     BucketLevel& b = ba.lv[l];
@@ -500,10 +503,21 @@ lx_status run(const lx_tree_layer& t, int T, int k, const void* x, const int32_t
     b.n_split_cnt = (int32_t)q.n_cnt;
   }
   if (bucket_small_ok(ba) && !P.merged) {
+    if (route) {
+      // batches of at most 64 tokens: the single-workgroup bucketing would
+      // run every token's top-k on one compute unit, slower than the
+      // router's own kernel with one wavefront per token
+      LX_LAUNCH("router_topk", launch_topk(route->logits, route->part, route->S, T, E, k,
+                                           const_cast<int32_t*>(ids), const_cast<float*>(w), lstream));
+      ba.route = RouteIn{};
+    }
     LX_LAUNCH("bucket_small", launch_bucket_small(pa, ba, lstream));
   } else {
     LX_LAUNCH("bucket_prepare", launch_prepare(pa, lstream));
-    LX_LAUNCH("bucket_hist", launch_bucket_hist(ba, lstream));
+    if (route)
+      LX_LAUNCH("router_topk+bucket_hist", launch_bucket_hist_route(ba, lstream));
+    else
+      LX_LAUNCH("bucket_hist", launch_bucket_hist(ba, lstream));
     LX_LAUNCH("bucket_scan", launch_bucket_scan(ba, lstream));
     LX_LAUNCH("bucket_place", launch_bucket_place(ba, lstream));
   }
@@ -1131,6 +1145,57 @@ lx_status lx_route_topk(const void* x, const void* w_r, lx_dtype dtype, int32_t 
   LX_LAUNCH("router_topk", launch_topk((const float*)(W + P.logits), (const float*)(W + P.part), P.S, T, E, k,
                                        topk_ids, topk_weights, lstream));
   return LX_OK;
+}
+
+size_t lx_route_moe_tree_workspace_bytes(const lx_tree_layer* layer, int32_t T, int32_t k) {
+  if (check_call(layer, T, k) != LX_OK) return 0;
+  if (check_route(layer->dtype, T, layer->d, layer->E, k) != LX_OK) return 0;
+  return align_up(make_plan(*layer, T, k).total) + route_plan(T, layer->d, layer->E).total;
+}
+
+lx_status lx_route_moe_forward_tree(const lx_tree_layer* layer, int32_t T, int32_t k, const void* x, const void* w_r,
+                                    int32_t* topk_ids, float* topk_weights, void* out, lx_dtype out_dtype,
+                                    void* workspace, size_t workspace_bytes, void* stream) {
+  g_err.clear();
+  if (!layer) return fail(LX_ERR_INVALID_ARGUMENT, "layer is null");
+  lx_status st = check_call(layer, T, k);
+  if (st != LX_OK) return st;
+  st = check_route(layer->dtype, T, layer->d, layer->E, k);
+  if (st != LX_OK) return st;
+  if (T == 0) return run(*layer, 0, k, x, topk_ids, topk_weights, out, out_dtype, workspace, workspace_bytes,
+                         (hipStream_t)stream, RUN_ALL);
+  if (!x || !w_r || !topk_ids || !topk_weights || !workspace || !aligned(x, 16) || !aligned(w_r, 16) ||
+      !aligned(topk_ids, 4) || !aligned(topk_weights, 4) || !aligned(workspace, 256))
+    return fail(LX_ERR_INVALID_ARGUMENT, "null or misaligned pointer");
+  const size_t fwd = align_up(make_plan(*layer, T, k).total);
+  const RoutePlan R = route_plan(T, layer->d, layer->E);
+  if (workspace_bytes < fwd + R.total) return fail(LX_ERR_WORKSPACE_TOO_SMALL, "workspace too small");
+  uint8_t* const W = (uint8_t*)workspace + fwd;
+  // logits = x W_r^T on the skinny kernel over implicit 32-row tiles, as in
+  // lx_route_topk; their top-k runs inside the first bucketing kernel
+  GemmArgs g{};
+  g.A = x;
+  g.lda = layer->d;
+  g.B[0] = g.B[1] = w_r;
+  g.ncols[0] = layer->E;
+  g.K = layer->d;
+  g.C = (float*)(W + R.logits);
+  g.ldc = layer->E;
+  g.dense_rows = T;
+  RouteIn ri{};
+  ri.logits = g.C;
+  ri.S = R.S;
+  if (R.S > 1) {
+    g.part = (float*)(W + R.part);
+    g.split_force = R.s;
+    g.defer = 1;
+    ri.part = g.part;
+  }
+  if (!gemm_big_ok(g, kSkinnyBN, T)) return fail(LX_ERR_UNSUPPORTED, "router shape not supported");
+  hipStream_t lstream = (hipStream_t)stream;
+  LX_LAUNCH("router_logits", launch_gemm_skinny(g, OUT_F32, (T + kSkinnyBM - 1) / kSkinnyBM, lstream));
+  return run(*layer, T, k, x, topk_ids, topk_weights, out, out_dtype, workspace, fwd, lstream, RUN_ALL, nullptr,
+             &ri);
 }
 
 lx_status lx_coact_distance(const int32_t* topk_ids, int32_t N, int32_t k, int32_t E, uint32_t* fire,

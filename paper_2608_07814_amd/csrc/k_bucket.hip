@@ -16,6 +16,7 @@
 //   place : the masks are rebuilt; a token's row inside its (node, tile)
 //           segment is the popcount of the mask bits below its lane.
 #include "lx_internal.h"
+#include "lx_topk.h"
 
 namespace lx {
 namespace {
@@ -137,6 +138,52 @@ __global__ __launch_bounds__(64) void k_bucket_hist(BucketArgs a) {
         bad |= (e < -1 || e >= a.E);
       }
     if (bad) atomicOr(a.flags, (uint32_t)LX_DEVFLAG_BAD_ID);
+  }
+}
+
+// Router top-k fused with the histogram pass: one workgroup per 64-token
+// tile; each wavefront picks the experts of 16 of the tile's tokens (ids and
+// weights to memory, for the later passes and the forward, and ids to LDS),
+// then every level's masks are built from LDS in turn.
+constexpr int kRouteHistThr = 1024, kRouteTok = kTokTile / (kRouteHistThr / 64);
+__global__ __launch_bounds__(kRouteHistThr) void k_bucket_hist_route(BucketArgs a) {
+  extern __shared__ unsigned long long s_mask[];
+  __shared__ int s_ids[kTokTile * LX_MAX_K];
+  const int tt = blockIdx.x, tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
+  const int k = a.k;
+  const int t0 = tt * kTokTile;
+  const int nt = a.T - t0 < kTokTile ? a.T - t0 : kTokTile;
+  int32_t* const ids_out = const_cast<int32_t*>(a.ids);
+  {
+    // wavefront w: tokens w, w + 16, w + 32, w + 48 of the tile together
+    int tok[kRouteTok], id[kRouteTok];
+    float wt[kRouteTok];
+#pragma unroll
+    for (int u = 0; u < kRouteTok; ++u) {
+      const int r = wave + u * (kRouteHistThr / 64);
+      tok[u] = r < nt ? t0 + r : -1;
+    }
+    topk_tokens<kRouteTok>(a.route.logits, a.route.part, a.route.S, a.E, k, tok, id, wt);
+#pragma unroll
+    for (int u = 0; u < kRouteTok; ++u)
+      if (tok[u] >= 0 && lane < k) {
+        ids_out[(int64_t)tok[u] * k + lane] = id[u];
+        const_cast<float*>(a.w)[(int64_t)tok[u] * k + lane] = wt[u];
+        s_ids[(tok[u] - t0) * k + lane] = id[u];
+      }
+  }
+  for (int l = 0; l <= a.L; ++l) {
+    const int N = a.lv[l].n_nodes;
+    for (int n = tid; n < N; n += kRouteHistThr) s_mask[n] = 0ull;
+    __syncthreads();  // (the first round also orders the ids written above)
+    for (int s = tid; s < nt * k; s += kRouteHistThr) {
+      const int n = node_of(a, l, s_ids[s]);
+      if (n >= 0) atomicOr(&s_mask[n], 1ull << (s / k));
+    }
+    __syncthreads();
+    int32_t* hist = a.lv[l].hist;
+    for (int n = tid; n < N; n += kRouteHistThr) hist[(int64_t)n * a.n_tok_tiles + tt] = __popcll(s_mask[n]);
+    __syncthreads();  // before the next level clears the masks
   }
 }
 
@@ -573,6 +620,12 @@ hipError_t launch_leaf_maps(const LeafMapArgs& a, hipStream_t s) {
   const int64_t n = (int64_t)a.T * a.k;
   const int grid = (int)((n + 255) / 256);
   hipLaunchKernelGGL(k_leaf_maps, dim3(grid > 0 ? grid : 1), dim3(256), 0, s, a);
+  return hipGetLastError();
+}
+
+hipError_t launch_bucket_hist_route(const BucketArgs& a, hipStream_t s) {
+  if (a.n_tok_tiles == 0) return hipSuccess;
+  hipLaunchKernelGGL(k_bucket_hist_route, dim3(a.n_tok_tiles), dim3(kRouteHistThr), mask_lds_bytes(a), s, a);
   return hipGetLastError();
 }
 

@@ -119,6 +119,16 @@ struct BucketLevel {
   int32_t n_split_cnt;        // here for the level's skinny GEMMs
 };
 
+// Router top-k fused into the first bucketing kernel: the logits of the
+// router GEMM (final [T][E], or S split-K partial tiles, as for launch_topk)
+// are turned into the ids and weights that the rest of the bucketing and
+// the forward read (written to BucketArgs::ids / w, which are then outputs).
+struct RouteIn {
+  const float* logits;     // null: no fused router (ids and w are inputs)
+  const float* part;
+  int32_t S;
+};
+
 struct BucketArgs {
   int32_t T, k, E, L;      // L = number of correction levels
   int32_t n_tok_tiles;
@@ -128,6 +138,7 @@ struct BucketArgs {
                            // slot holds the sum of its slots' weights, others 0
   const int32_t* anc;      // [(L + 1) * E] ancestor per level, -1 = invalid expert
   uint32_t* flags;
+  RouteIn route;
   BucketLevel lv[kMaxLvl];
 };
 
@@ -146,6 +157,9 @@ struct PrepareArgs {
 
 hipError_t launch_prepare(const PrepareArgs& a, hipStream_t s);
 hipError_t launch_bucket_hist(const BucketArgs& a, hipStream_t s);
+// With a.route set: top-k of every token (ids and weights written to a.ids
+// and a.w) and the histogram of every level, one workgroup per token tile.
+hipError_t launch_bucket_hist_route(const BucketArgs& a, hipStream_t s);
 hipError_t launch_bucket_scan(const BucketArgs& a, hipStream_t s);
 hipError_t launch_bucket_place(const BucketArgs& a, hipStream_t s);
 // Merged correction outputs of a tree (after placement): for every leaf

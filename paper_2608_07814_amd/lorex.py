@@ -71,6 +71,9 @@ EXPORTS = {
                                 _c_void, _c_i32, _c_void, ctypes.c_size_t, _c_void]),
     "lx_moe_forward_tree": (_c_i32, [ctypes.POINTER(LxTreeLayer), _c_i32, _c_i32, _c_void, _c_void,
                                      _c_void, _c_void, _c_i32, _c_void, ctypes.c_size_t, _c_void]),
+    "lx_route_moe_tree_workspace_bytes": (ctypes.c_size_t, [ctypes.POINTER(LxTreeLayer), _c_i32, _c_i32]),
+    "lx_route_moe_forward_tree": (_c_i32, [ctypes.POINTER(LxTreeLayer), _c_i32, _c_i32, _c_void, _c_void, _c_void,
+                                           _c_void, _c_void, _c_i32, _c_void, ctypes.c_size_t, _c_void]),
     "lx_moe_forward_tree_static": (_c_i32, [ctypes.POINTER(LxTreeLayer), _c_i32, _c_i32, _c_void, _c_void,
                                             _c_void, _c_void, _c_i32, _c_void]),
     "lx_dense_moe_forward": (_c_i32, [ctypes.POINTER(LxDenseLayer), _c_i32, _c_i32, _c_void, _c_void,
@@ -483,6 +486,37 @@ def forward(layer: DeviceLayer, x: torch.Tensor, topk_ids: torch.Tensor, topk_we
         st = L.lx_moe_forward_tree(ctypes.byref(layer.tree_struct()), *args)
     _check(st)
     return out
+
+
+def route_forward(layer: DeviceLayer, x: torch.Tensor, w_r: torch.Tensor, k: int,
+                  out: Optional[torch.Tensor] = None, ids: Optional[torch.Tensor] = None,
+                  weights: Optional[torch.Tensor] = None, workspace: Optional[torch.Tensor] = None,
+                  out_dtype: int = LX_F32, stream=None):
+    """The router fused into the tree forward (lx_route_moe_forward_tree):
+    bf16 x [T][d] and router weights [E][d] -> (out, int32 ids [T][k], fp32
+    weights [T][k]). Flat layers run as their one-level tree."""
+    if x.dtype != torch.bfloat16 or w_r.dtype != torch.bfloat16:
+        raise ValueError("x and w_r must be bf16")
+    if not (x.is_contiguous() and w_r.is_contiguous()):
+        raise ValueError("x and w_r must be contiguous")
+    T = int(x.shape[0])
+    desc = layer.tree_struct()
+    L = lib()
+    if ids is None:
+        ids = torch.empty(T, k, dtype=torch.int32, device=x.device)
+    if weights is None:
+        weights = torch.empty(T, k, dtype=torch.float32, device=x.device)
+    if out is None:
+        out = torch.empty(T, layer.d, device=x.device,
+                          dtype=torch.float32 if out_dtype == LX_F32 else torch.bfloat16)
+    if workspace is None:
+        n = int(L.lx_route_moe_tree_workspace_bytes(ctypes.byref(desc), T, k))
+        if n == 0:
+            raise LorexError(LX_ERR_INVALID_ARGUMENT, L.lx_last_error().decode())
+        workspace = torch.empty(n, dtype=torch.uint8, device=x.device)
+    _check(L.lx_route_moe_forward_tree(ctypes.byref(desc), T, k, _ptr(x), _ptr(w_r), _ptr(ids), _ptr(weights),
+                                       _ptr(out), out_dtype, _ptr(workspace), workspace.numel(), _stream(stream)))
+    return out, ids, weights
 
 
 STATIC_SCRATCH_BYTES = 64 << 20  # LX_STATIC_SCRATCH_BYTES

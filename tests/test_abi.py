@@ -28,7 +28,7 @@ def _declared(root):
 
 def test_every_declared_symbol_is_exported(L, root):
     names = _declared(root)
-    assert len(names) == len(lx.EXPORTS) == 30
+    assert len(names) == len(lx.EXPORTS) == 32
     for n in names:
         assert hasattr(L, n), n
         assert n in lx.EXPORTS, n

@@ -124,3 +124,56 @@ def test_route_then_forward_on_one_stream():
     e = err_ratio(out.cpu().numpy().astype(np.float64), ref)
     say(f"  err/RMS = {e:.3e}")
     assert e <= TOL_BF16 and e <= TOL_DESIGN
+
+
+@pytest.mark.parametrize("cfg,T", [(2, 64), (1, 300), (4, 100), (4, 2500)])
+def test_route_fused_into_bucketing(cfg, T):
+    """lx_route_moe_forward_tree: the router's top-k runs inside the first
+    bucketing kernel, the histogram pass (batches of at most 64 tokens keep
+    the router's own top-k launch ahead of the single-workgroup bucketing;
+    split-K router logits at these sizes). Its ids and weights are
+    bitwise those of lx_route_topk, tie-aware against the fp64 router oracle;
+    the bucketing of those ids is byte-equal to the bucketing oracle's; the
+    output is bitwise that of lx_moe_forward_tree on the same ids and meets
+    the oracle bar; no separate top-k launch runs."""
+    require_gpu()
+    from oracle import bucket as B
+    say(f"route fused into bucketing cfg{cfg} T={T}")
+    p = make_problem(cfg, T=T)
+    w = make_router(p.layer.d, p.layer.E, "bf16", p.seed)
+    dl = lx.to_device(p.layer)
+    xd, wd = _bf16_dev(p.x), _bf16_dev(w)
+    lx.profile_reset()
+    lx.profile_enable(True)
+    try:
+        out, ids, wts = lx.route_forward(dl, xd, wd, p.k)
+        names = list(lx.profile_read())
+    finally:
+        lx.profile_enable(False)
+    assert "router_logits" in names
+    if T <= 64:  # the single-workgroup bucketing keeps the router's own top-k launch
+        assert "router_topk" in names and "bucket_small" in names, names
+    else:
+        assert "router_topk" not in names and "router_topk+bucket_hist" in names, names
+    ids_r, wts_r = lx.route_topk(xd, wd, p.k)
+    torch.cuda.synchronize()
+    assert torch.equal(ids, ids_r) and torch.equal(wts, wts_r)
+    ids_h, w_h = ids.cpu().numpy(), wts.cpu().numpy()
+    _check(p.x, w, p.k, ids_h, w_h.astype(np.float64))
+    # the bucketing of the GPU's own ids against the bucketing oracle
+    parents = [lv.parent for lv in p.layer.levels]
+    n_nodes = [p.layer.n_anchors] + [lv.n_nodes for lv in p.layer.levels]
+    ref, _ = B.bucket(parents, n_nodes, p.layer.E, ids_h)
+    ws = lx.alloc_workspace(dl, T, p.k, "tree")
+    for li in range(p.layer.n_levels + 1):
+        rt, off, sr = (t.cpu().numpy() for t in lx.bucket(dl, ids, li, workspace=ws))
+        assert np.array_equal(off, ref[li]["offsets"]) and np.array_equal(rt, ref[li]["row_token"])
+        assert np.array_equal(sr, ref[li]["slot_row"])
+    # the forward on those ids: bitwise the unfused call, and the oracle bar
+    plain = lx.forward(dl, xd, ids, wts, kind="tree")
+    torch.cuda.synchronize()
+    got = out.cpu().numpy()
+    assert np.array_equal(got, plain.cpu().numpy())
+    e = err_ratio(got.astype(np.float64), O.moe_forward(p.layer, p.x, ids_h, w_h))
+    say(f"  err/RMS = {e:.3e}")
+    assert e <= TOL_BF16 and e <= TOL_DESIGN
