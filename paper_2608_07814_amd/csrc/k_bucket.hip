@@ -269,18 +269,33 @@ __global__ __launch_bounds__(1024) void k_bucket_scan(BucketArgs a) {
 
   // exclusive scan of hist in (node, tile) order, in place; entry (n, 0)
   // is node n's offset (kept in LDS for the tile tables)
-  // Each thread's chunk is read CH entries at a time with all loads in
-  // flight (a dependent load per entry would serialise on memory latency);
-  // chunks of at most CH entries stay in registers between the two passes.
-  constexpr int CH = 16;
-  const int64_t chunk = (total + nth - 1) / nth;
+  // Each thread owns a chunk of consecutive entries (a multiple of 4, so it
+  // is read and written as 16-byte vectors): up to CH entries stay in
+  // registers between the two passes, all loaded at once; longer chunks are
+  // read CH at a time in both passes.
+  constexpr int CH = 32;
+  const int64_t chunk = ((total + nth - 1) / nth + 3) & ~(int64_t)3;
   const int64_t b = (int64_t)tid * chunk;
   const int64_t e = b + chunk < total ? b + chunk : total;
   int v[CH];
+  auto load = [&](int64_t c0) {
+#pragma unroll
+    for (int u = 0; u < CH; u += 4) {
+      if (c0 + u + 4 <= e) {
+        const int4 q = *(const int4*)(lv.hist + c0 + u);
+        v[u] = q.x;
+        v[u + 1] = q.y;
+        v[u + 2] = q.z;
+        v[u + 3] = q.w;
+      } else {
+#pragma unroll
+        for (int w = 0; w < 4; ++w) v[u + w] = c0 + u + w < e ? lv.hist[c0 + u + w] : 0;
+      }
+    }
+  };
   int local = 0;
   for (int64_t c0 = b; c0 < e; c0 += CH) {
-#pragma unroll
-    for (int u = 0; u < CH; ++u) v[u] = c0 + u < e ? lv.hist[c0 + u] : 0;
+    load(c0);
 #pragma unroll
     for (int u = 0; u < CH; ++u) local += v[u];
   }
@@ -289,21 +304,29 @@ __global__ __launch_bounds__(1024) void k_bucket_scan(BucketArgs a) {
   // (node, tile) of entry b, advanced incrementally (no division per entry)
   int node = (int)(b / NT), tile = (int)(b - (int64_t)node * NT);
   for (int64_t c0 = b; c0 < e; c0 += CH) {
-    if (e - b > CH) {  // chunk larger than the register cache: reload
-#pragma unroll
-      for (int u = 0; u < CH; ++u) v[u] = c0 + u < e ? lv.hist[c0 + u] : 0;
-    }
+    if (e - b > CH) load(c0);  // chunk larger than the register cache: reload
 #pragma unroll
     for (int u = 0; u < CH; ++u) {
       const int64_t i = c0 + u;
+      const int cnt = v[u];
       if (i < e) {
-        lv.hist[i] = run;
+        v[u] = run;
         if (tile == 0) s_off[node] = run;
-        run += v[u];
+        run += cnt;
         if (++tile == NT) {
           tile = 0;
           ++node;
         }
+      }
+    }
+#pragma unroll
+    for (int u = 0; u < CH; u += 4) {
+      if (c0 + u + 4 <= e) {
+        *(int4*)(lv.hist + c0 + u) = make_int4(v[u], v[u + 1], v[u + 2], v[u + 3]);
+      } else {
+#pragma unroll
+        for (int w = 0; w < 4; ++w)
+          if (c0 + u + w < e) lv.hist[c0 + u + w] = v[u + w];
       }
     }
   }
