@@ -114,10 +114,10 @@ struct Plan {
   // and down corrections of every level as one product over the leaf rows
   // (K concatenated over the levels), so the intermediate levels' full-width
   // outputs are never written; path_work marks the experts whose path has a
-  // factor, leaf_row / leaf_first map leaf rows to intermediate-level rows
+  // factor, leaf_row maps leaf rows to intermediate-level rows
   bool merged = false;
   size_t path_work = 0;
-  size_t leaf_row[kMaxLvl] = {}, leaf_first[kMaxLvl] = {};
+  size_t leaf_row[kMaxLvl] = {};
   // kernel choice per level (shapes only): "fast" levels keep every
   // GEMM-feeding intermediate as a bf16 (hi, lo) pair and run on the
   // large-tile or skinny kernel; "skinny" ones (few rows per node) on the
@@ -188,10 +188,7 @@ Plan make_plan(const lx_tree_layer& t, int T, int k) {
   if (p.merged) {
     p.path_work = take((size_t)p.E);
     const size_t rl = (size_t)T * std::min(k, t.E);  // leaf rows, at most
-    for (int l = 1; l < p.L; ++l) {
-      p.leaf_row[l] = take(rl * 4);
-      p.leaf_first[l] = take(rl * 4);
-    }
+    for (int l = 1; l < p.L; ++l) p.leaf_row[l] = take(rl * 4);
   }
   for (int l = 0; l <= p.L; ++l) {
     LevelPlan& q = p.lv[l];
@@ -223,10 +220,12 @@ Plan make_plan(const lx_tree_layer& t, int T, int k) {
     const bool leafm = p.merged && l == p.L;
     q.gu = take((work && !inter) || leafm ? R * 2 * p.f * 4 : 0);
     q.z = take(l > 0 && work ? R * 2 * q.rank * 4 : 0);
-    q.hbar = take(work || leafm ? R * p.f * 4 : 0);
-    // (+1 row: the zero row a merged down product reads for rows that do not
-    // carry this level's term)
-    q.v = take(l > 0 && work ? (R + (inter ? 1 : 0)) * q.rank * 4 : 0);
+    q.hbar = take((work && !inter) || leafm ? R * p.f * 4 : 0);
+    // merged trees: an intermediate level's down-in product runs on the leaf
+    // rows (by linearity, the sum over a row's leaf rows of B_down h_leaf is
+    // B_down of the row's sum), so its v has one row per leaf row
+    const size_t Rv = inter ? (size_t)T * std::min(k, t.E) : R;
+    q.v = take(l > 0 && work ? Rv * q.rank * 4 : 0);
     q.y = take((work && !inter) || leafm ? R * p.d * 4 : 0);
     // one counter per work item of the level's widest skinny product
     const int widest = std::max(std::max(2 * p.f, p.d), 2 * q.rank);
@@ -530,13 +529,7 @@ lx_status run(const lx_tree_layer& t, int T, int k, const void* x, const int32_t
     for (int l = 0; l <= L; ++l) {
       lm.slot_row[l] = ba.lv[l].slot_row;
       lm.slot_flags[l] = ba.lv[l].slot_flags;
-      if (l >= 1 && l < L) {
-        lm.leaf_row_map[l] = (int32_t*)(W + P.leaf_row[l]);
-        lm.leaf_first_map[l] = (int32_t*)(W + P.leaf_first[l]);
-        // the zero row of the level's v buffer (row rows_max, 4 r bytes)
-        lm.zero_rows[l] = (uint8_t*)(W + P.lv[l].v) + (size_t)P.lv[l].rows_max * P.lv[l].rank * 4;
-        lm.zero_bytes[l] = t.levels[l - 1].n_factors > 0 ? P.lv[l].rank * 4 : 0;
-      }
+      if (l >= 1 && l < L) lm.leaf_row_map[l] = (int32_t*)(W + P.leaf_row[l]);
     }
     LX_LAUNCH("leaf_maps", launch_leaf_maps(lm, lstream));
   }
@@ -712,11 +705,11 @@ lx_status run(const lx_tree_layer& t, int T, int k, const void* x, const int32_t
         sd.B[1] = v.a_up;
         sd.b_stride[0] = sd.b_stride[1] = (int64_t)f * r;
       } else {
-        sd.A = W + q.v;
+        sd.A = W + q.v;  // one row per leaf row at every level
         sd.lda = 2 * (int64_t)r;  // [hi | lo]
         sd.akoff1 = 0;
-        sd.map = l == L ? nullptr : (const int32_t*)(W + P.leaf_first[l]);
-        sd.zero_row = (int32_t)q.rows_max;
+        sd.map = nullptr;
+        sd.zero_row = 0;
         sd.B[0] = sd.B[1] = v.a_down;
         sd.b_stride[0] = sd.b_stride[1] = (int64_t)d * r;
       }
@@ -832,7 +825,8 @@ lx_status run(const lx_tree_layer& t, int T, int k, const void* x, const int32_t
       LX_TRY(small("anchor_down", g, 0, A_F32_HILO));
     }
   }
-  // correction down per level, part 1: v = B_down hbar
+  // correction down per level, part 1: v = B_down hbar (merged trees: over
+  // the leaf rows at every level, each with its ancestor's weights)
   lstream = side;
   for (int l = 1; l <= L; ++l) {
     const LevelPlan& q = P.lv[l];
@@ -845,6 +839,20 @@ lx_status run(const lx_tree_layer& t, int T, int k, const void* x, const int32_t
     g.b_stride[0] = (int64_t)r * f;
     g.ncols[0] = r;
     g.C = (float*)(W + q.v);
+    if (P.merged) {
+      const LevelPlan& qL = P.lv[L];
+      g.A = W + qL.hbar;
+      if (l < L) {
+        g.widx_anc = pa.anc + (size_t)l * E;
+        g.widx_fac = (const int32_t*)(W + q.fac);
+      }
+      g.lda = 2 * (int64_t)f;
+      g.K = 2 * f;
+      g.Kb = f;
+      g.ldc = 2 * (int64_t)r;
+      LX_TRY(big(kDownIn[l], g, L, kBigBM, r <= 64 ? 64 : 128, OUT_HILO, qL.rows_max));
+      continue;
+    }
     if (fast[l]) {
       g.lda = 2 * (int64_t)f;
       g.K = 2 * f;

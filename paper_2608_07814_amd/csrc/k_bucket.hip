@@ -383,26 +383,13 @@ __global__ __launch_bounds__(kPlaceThr) void k_bucket_place(BucketArgs a) {
 }
 
 // One thread per routing slot; the first slot of each leaf row writes that
-// row's map entries. A level-l row's first slot is the token's lowest slot
-// with that row; the leaf row holding it is the one that carries the row's
-// term in a merged product.
+// row's map entries.
 __global__ __launch_bounds__(256) void k_leaf_maps(LeafMapArgs a) {
   const int64_t s = (int64_t)blockIdx.x * blockDim.x + threadIdx.x;
-  const int L = a.L, k = a.k;
-  if (blockIdx.x == 0)
-    for (int l = 1; l < L; ++l)
-      for (int i = threadIdx.x; i < a.zero_bytes[l] / 4; i += blockDim.x) ((uint32_t*)a.zero_rows[l])[i] = 0u;
-  if (s >= (int64_t)a.T * k) return;
-  if (!(a.slot_flags[L][s] & 1)) return;  // not the first slot of a leaf row (or dropped)
-  const int rL = a.slot_row[L][s];
-  const int64_t t0 = s - s % k;
-  for (int l = 1; l < L; ++l) {
-    const int rl = a.slot_row[l][s];
-    int64_t f = t0;
-    while (a.slot_row[l][f] != rl) ++f;  // terminates at s at the latest
-    a.leaf_row_map[l][rL] = rl;
-    a.leaf_first_map[l][rL] = a.slot_row[L][f] == rL ? rl : -1;
-  }
+  if (s >= (int64_t)a.T * a.k) return;
+  if (!(a.slot_flags[a.L][s] & 1)) return;  // not the first slot of a leaf row (or dropped)
+  const int rL = a.slot_row[a.L][s];
+  for (int l = 1; l < a.L; ++l) a.leaf_row_map[l][rL] = a.slot_row[l][s];
 }
 
 // Whole bucketing of a batch of at most 64 tokens in one workgroup. All

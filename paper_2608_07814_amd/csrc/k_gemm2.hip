@@ -201,14 +201,21 @@ void k_gemm_big(GemmArgs p, int ntn) {
     // The two weight parts form one column range [0, ncol): column n < ncols[0]
     // is row n of part 0, otherwise row n - ncols[0] of part 1.
     const TileEntry te = p.tiles[ti];
-    // a leaf-level tile whose node has no factor of its own (it is listed
+    // weight index: the tile's, or that of the tile node's ancestor at
+    // another level (a leaf-row product with an upper level's weights)
+    int widx = te.widx;
+    if (p.widx_anc) {
+      const int an = p.widx_anc[te.node];
+      widx = an >= 0 ? p.widx_fac[an] : -1;
+    }
+    // a leaf-level tile whose node (or ancestor) has no factor (it is listed
     // for the products that merge the levels above it): nothing to do here
-    if (te.widx < 0) continue;
+    if (widx < 0) continue;
     const int n0 = nt * BN;
     const int tpart = n0 < p.ncols[0] ? 0 : 1;
     const int akoff = p.a_koff[tpart];
-    const u16* __restrict__ Bw0 = (const u16*)p.B[0] + (int64_t)te.widx * p.b_stride[0];
-    const u16* __restrict__ Bw1 = (const u16*)p.B[1] + (int64_t)te.widx * p.b_stride[1];
+    const u16* __restrict__ Bw0 = (const u16*)p.B[0] + (int64_t)widx * p.b_stride[0];
+    const u16* __restrict__ Bw1 = (const u16*)p.B[1] + (int64_t)widx * p.b_stride[1];
 
     // Per-thread source offsets (elements, chunk offset folded in) for each
     // 16-byte chunk it loads. LDS slot P = round*256 + tid holds row P>>3,
@@ -343,8 +350,8 @@ void k_gemm_big(GemmArgs p, int ntn) {
       uint8_t* const L1 = (uint8_t*)sA1;
       const uint8_t* const Abytes = (const uint8_t*)p.A;
       const uint32_t apitch = 2 * (uint32_t)p.lda;
-      const uint8_t* const B8 = p.b8 + (int64_t)te.widx * p.b_stride[0];
-      const uint32_t* const BS = p.bsc + (int64_t)te.widx * (p.b_stride[0] / 64);
+      const uint8_t* const B8 = p.b8 + (int64_t)widx * p.b_stride[0];
+      const uint32_t* const BS = p.bsc + (int64_t)widx * (p.b_stride[0] / 64);
       const u16* const Bhi = Bw0;
       // byte offsets (32 bit: the host routes operands of 2^31 or more
       // elements elsewhere) of this thread's hi-slab chunks of B and of its lo

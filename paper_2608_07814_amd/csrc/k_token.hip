@@ -141,6 +141,7 @@ __global__ __launch_bounds__(kTokThr * kSlotGroups) void k_swiglu_reduce(TokenAr
     for (int l = 0; l <= L; ++l) {
       const unsigned char fl0 = m.fl[l][j0];
       if ((fl0 & 3) != 3) continue;  // j0 starts a level-l row that does work
+      if (a.merged && l > 0 && l < L) continue;  // folded into the leaf rows
       const int r = m.row[l][j0];
       float4 hs = make_float4(0.f, 0.f, 0.f, 0.f);
       for (int j = j0; j < k; ++j)
@@ -318,11 +319,13 @@ __global__ __launch_bounds__(kFastThr) void k_swiglu_fast(TokenArgs a) {
                        w[j] * silu_mul(g.w, u.w));
   }
   // each level-l row that does work: the sum of its experts' h in slot order
+  // (merged trees: the intermediate levels' down products run on the leaf
+  // rows' sums, so only the anchor and leaf levels are stored)
 #pragma unroll
   for (int l = 0; l <= NL; ++l)
 #pragma unroll
     for (int j0 = 0; j0 < kFastK; ++j0) {
-      if ((fl[l][j0] & 3) != 3) continue;
+      if ((fl[l][j0] & 3) != 3 || (merged && l > 0 && l < NL)) continue;
       float4 hs = make_float4(0.f, 0.f, 0.f, 0.f);
 #pragma unroll
       for (int j = j0; j < kFastK; ++j)

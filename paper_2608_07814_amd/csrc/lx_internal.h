@@ -164,18 +164,12 @@ hipError_t launch_bucket_scan(const BucketArgs& a, hipStream_t s);
 hipError_t launch_bucket_place(const BucketArgs& a, hipStream_t s);
 // Merged correction outputs of a tree (after placement): for every leaf
 // row r of level L and every intermediate level l (1 <= l < L),
-//   leaf_row_map[l][r]   = the level-l row of r's token and node,
-//   leaf_first_map[l][r] = the same row if r holds that row's first slot,
-//                          else -1 (so each level-l row is counted once);
-// and zero_rows[l] (zero_bytes[l] bytes) is cleared.
+// leaf_row_map[l][r] = the level-l row of r's token and node.
 struct LeafMapArgs {
   int32_t T, k, L;
   const int32_t* slot_row[kMaxLvl];
   const uint8_t* slot_flags[kMaxLvl];
   int32_t* leaf_row_map[kMaxLvl];
-  int32_t* leaf_first_map[kMaxLvl];
-  uint8_t* zero_rows[kMaxLvl];
-  int32_t zero_bytes[kMaxLvl];
 };
 hipError_t launch_leaf_maps(const LeafMapArgs& a, hipStream_t s);
 // Batches of 1..64 tokens: prepare + hist + scan + place in one workgroup.
@@ -229,6 +223,11 @@ struct GemmArgs {
   // tiles == null: implicit tiles of kSkinnyBM consecutive rows over
   // dense_rows rows of A (identity row map, weight index 0)
   int32_t dense_rows;
+  // large-tile kernel: when widx_anc is set, a tile's weight index is
+  // widx_fac[widx_anc[tile node]] (the factor of the tile node's ancestor at
+  // another level; below 0: the tile is skipped) instead of its own
+  const int32_t* widx_anc;
+  const int32_t* widx_fac;
 };
 
 enum AMode { A_BF16 = 0, A_F32_HILO = 1 };
