@@ -64,6 +64,9 @@ def parse():
     ap.add_argument("--no-lo8", action="store_true",
                     help="no fp8 copy of the anchor down weights: the anchor down projection multiplies "
                          "both halves of its bf16 (hi, lo) input in bf16")
+    ap.add_argument("--no-f16", action="store_true",
+                    help="no fp16 copy of the anchor down weights: the anchor down projection keeps the fp8-lo "
+                         "(or bf16 pair) path on every batch")
     ap.add_argument("--no-route", action="store_true", help="skip timing the GPU top-k router")
     ap.add_argument("--stage3", action="store_true",
                     help="also time Stage-3 factor production for one member at the flat workload's expert "
@@ -363,7 +366,7 @@ def run_workload(cfg_index, a, torch, np, lx, headline):
     cfg = p.cfg
     T, k = p.T, p.k
     layer = p.layer
-    dl = lx.to_device(layer, lo8=not a.no_lo8)
+    dl = lx.to_device(layer, lo8=not a.no_lo8, f16=not a.no_f16)
     if layer.dtype == "bf16":
         xd = torch.from_numpy(p.x.view(np.int16)).cuda().view(torch.bfloat16)
     else:
@@ -456,6 +459,8 @@ def run_workload(cfg_index, a, torch, np, lx, headline):
         torch.cuda.empty_cache()
         if not a.no_lo8:
             dd = lx.attach_down_f8(dd)
+        if not a.no_f16:
+            dd = lx.attach_down_f16(dd)
         wsd = lx.alloc_workspace(dd, T, k, "dense")
         outd = torch.empty_like(out)
         dcopies = [dd] + [clone_layer(dd) for _ in range(max(a.rotate, 1) - 1)]
@@ -528,7 +533,9 @@ def run_workload(cfg_index, a, torch, np, lx, headline):
                wall_s_timed=round(wall, 3), weight_copies=len(copies),
                config={"workload": workload, "T": T, "d": layer.d, "f": layer.f, "E": layer.E, "k": k,
                        "anchors": layer.n_anchors, "ranks": ranks[1:], "layer": kind, "seed": p.seed,
-                       "out_dtype": "f32", "anchor_down_lo": "bf16" if a.no_lo8 else "fp8 (block-scaled)"},
+                       "out_dtype": "f32",
+                       "anchor_down_copies": [c for c, off in (("fp8 lo (block-scaled)", a.no_lo8),
+                                                               ("fp16 (row-scaled sums)", a.no_f16)) if not off]},
                roofline=roof, layer_roofline=layer_perf, kernels=kernels, dense_comparator=dense,
                gpu_router=routed)
     del copies, call

@@ -129,6 +129,12 @@ typedef struct lx_tree_layer {
    * half of its bf16 (hi, lo) input split in fp8 (see lx_quantize_f8). */
   const void* anchor_down_f8;            /* [n_anchors][d][f] e4m3 */
   const uint32_t* anchor_down_f8_scale;  /* [n_anchors][d][f / 64] */
+  /* Optional (NULL = not used): fp16 copy of anchor_down made by
+   * lx_convert_f16. With it, batches whose activation sums fit the fp16 path
+   * (see lx_convert_f16) run the anchor down projection as one fp16 product
+   * instead of the bf16 (hi, lo) pair; it takes precedence over the fp8 copy. */
+  const void* anchor_down_f16;           /* [n_anchors][d][f] fp16, scaled */
+  const int32_t* anchor_down_f16_exp;    /* [n_anchors] scale exponents */
 } lx_tree_layer;
 
 /* A flat LorExperts layer (Sec. 3 "Representation"): C clusters, one dominant
@@ -150,6 +156,8 @@ typedef struct lx_flat_layer {
   const void* b_down;        /* [M][r][f] */
   const void* dom_down_f8;             /* optional fp8 copy of dom_down (lx_quantize_f8) */
   const uint32_t* dom_down_f8_scale;   /* its scale words, [C][d][f / 64] */
+  const void* dom_down_f16;            /* optional fp16 copy of dom_down (lx_convert_f16) */
+  const int32_t* dom_down_f16_exp;     /* its scale exponents, [C] */
 } lx_flat_layer;
 
 /* An uncompressed MoE layer (every expert stored in full): the comparator the
@@ -163,6 +171,8 @@ typedef struct lx_dense_layer {
   const void* w_down;        /* [E][d][f] */
   const void* w_down_f8;               /* optional fp8 copy of w_down (lx_quantize_f8) */
   const uint32_t* w_down_f8_scale;     /* its scale words, [E][d][f / 64] */
+  const void* w_down_f16;              /* optional fp16 copy of w_down (lx_convert_f16) */
+  const int32_t* w_down_f16_exp;       /* its scale exponents, [E] */
 } lx_dense_layer;
 
 /* Human-readable name of a status code (static string). */
@@ -244,6 +254,29 @@ lx_status lx_dense_moe_forward(const lx_dense_layer* layer, int32_t T, int32_t k
  * Asynchronous on `stream`. */
 lx_status lx_quantize_f8(const void* w, int32_t n, int32_t rows, int32_t cols, void* w_f8,
                          uint32_t* scales, void* stream);
+
+/* fp16 copy of bf16 weights, for the anchor down projection.
+ *
+ * The anchor down projection multiplies the anchor activation sums hbar
+ * (Sec. 5.1: the routing-weighted sum of the SwiGLU activations of a token's
+ * experts under one anchor) by the anchor's down weights. Rounded to bf16,
+ * hbar costs about 1e-2 x RMS of the output (the acceptance bar), hence the
+ * (hi, lo) pair; fp16 keeps 3 more bits (about 1.3e-3 x RMS) at the bf16 MFMA
+ * rate in a single product. With this copy in the layer, the forward stores
+ * hbar as fp16 with one power-of-two scale per row (its largest magnitude in
+ * [2^14, 2^15)) and multiplies it with the copy, undoing both scales exactly
+ * in the output. Used for batches of at least 512 tokens with f a multiple
+ * of 256 and at most 1024, k <= 8 and at most two correction levels, on the
+ * large-tile kernel; other batches take the fp8 copy (if any) or the pair.
+ *
+ * w [n][rows][cols] bf16 -> w_f16 [n][rows][cols] fp16 equal to w * 2^e_i
+ * for matrix i, rounded to nearest even, with exps[i] = e_i chosen so that
+ * the matrix's largest magnitude lands in [2^14, 2^15) (0 for an all-zero
+ * matrix); exact for every bf16 value down to 2^-28 of that maximum. Device
+ * pointers: w_f16 16-byte aligned, exps 4-byte aligned; n, rows, cols >= 1
+ * (LX_ERR_INVALID_ARGUMENT). Asynchronous on `stream`. */
+lx_status lx_convert_f16(const void* w, int32_t n, int32_t rows, int32_t cols, void* w_f16, int32_t* exps,
+                         void* stream);
 
 /* The model's unchanged top-k router on the GPU (Sec. 3 "Stage 1" and Fig.
  * overview: compression leaves the router as it is and every expert

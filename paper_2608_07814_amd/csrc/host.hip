@@ -129,6 +129,12 @@ struct Plan {
   // anchor down GEMM runs the lo half on the fp8 MFMA (needs the layer's fp8
   // copy of the anchor down weights and the large-tile kernel)
   bool lo8 = false;
+  // f16: the anchor activation sums are fp16 rows with a power-of-two scale
+  // per row and the anchor down GEMM runs once, in fp16, against the
+  // layer's fp16 copy (needs the large-tile kernel and whole rows per
+  // SwiGLU workgroup); preferred over lo8
+  bool f16 = false;
+  size_t hbar_exp = 0;
 };
 
 int level_nodes(const lx_tree_layer& t, int l) { return l == 0 ? t.n_anchors : t.levels[l - 1].n_nodes; }
@@ -175,6 +181,15 @@ Plan make_plan(const lx_tree_layer& t, int T, int k) {
       if (work && !p.skinny[l]) p.batch = false;
     }
     p.lo8 = t.anchor_down_f8 && t.anchor_down_f8_scale && p.fast[0] && !p.skinny[0] && p.f % 64 == 0;
+    {
+      bool all_fast = true;
+      for (int l = 0; l <= p.L; ++l) all_fast &= p.fast[l];
+      // (the fast SwiGLU kernel: k <= 8, at most two correction levels,
+      // 512+ tokens give f / 4 threads per token, one workgroup per row)
+      p.f16 = t.anchor_down_f16 && t.anchor_down_f16_exp && p.fast[0] && !p.skinny[0] && all_fast && k <= 8 &&
+              p.L <= 2 && T >= 512 && p.f % 256 == 0 && p.f <= 1024;
+      if (p.f16) p.lo8 = false;
+    }
     // (batches of at most 64 tokens always run their fast levels on the
     // skinny kernel, so merged trees take the four-pass bucketing)
     p.merged = p.L >= 2 && T > kTokTile && p.f % 256 == 0 && p.d % 256 == 0;
@@ -185,6 +200,7 @@ Plan make_plan(const lx_tree_layer& t, int T, int k) {
   p.anc = take((size_t)(p.L + 1) * p.E * 4);
   const size_t tk = (size_t)T * k;
   p.slot_wsum = take(tk * 4);
+  if (p.f16) p.hbar_exp = take((size_t)T * std::min(k, t.n_anchors) * 4);
   if (p.merged) {
     p.path_work = take((size_t)p.E);
     const size_t rl = (size_t)T * std::min(k, t.E);  // leaf rows, at most
@@ -263,6 +279,12 @@ lx_status check_layer(const lx_tree_layer* t) {
     if (t->dtype != LX_BF16 || t->f % 64)
       return fail(LX_ERR_UNSUPPORTED, "an fp8 down copy needs a bf16 layer with f a multiple of 64");
   }
+  if (t->anchor_down_f16 || t->anchor_down_f16_exp) {
+    if (!t->anchor_down_f16 || !t->anchor_down_f16_exp || !aligned(t->anchor_down_f16, 16) ||
+        !aligned(t->anchor_down_f16_exp, 4))
+      return fail(LX_ERR_INVALID_ARGUMENT, "fp16 down copy and its exponents: both or neither, 16/4-byte aligned");
+    if (t->dtype != LX_BF16) return fail(LX_ERR_UNSUPPORTED, "an fp16 down copy needs a bf16 layer");
+  }
   for (int l = 0; l < t->n_levels; ++l) {
     const lx_level& v = t->levels[l];
     if (v.n_nodes < 1 || v.n_nodes > LX_MAX_NODES) return fail(LX_ERR_INVALID_ARGUMENT, "level node count out of range");
@@ -301,6 +323,8 @@ lx_tree_layer flat_to_tree(const lx_flat_layer& F) {
   t.anchor_down = F.dom_down;
   t.anchor_down_f8 = F.dom_down_f8;
   t.anchor_down_f8_scale = F.dom_down_f8_scale;
+  t.anchor_down_f16 = F.dom_down_f16;
+  t.anchor_down_f16_exp = F.dom_down_f16_exp;
   t.n_levels = 1;
   lx_level& v = t.levels[0];
   v.n_nodes = F.E;
@@ -329,6 +353,8 @@ lx_tree_layer dense_to_tree(const lx_dense_layer& D) {
   t.anchor_down = D.w_down;
   t.anchor_down_f8 = D.w_down_f8;
   t.anchor_down_f8_scale = D.w_down_f8_scale;
+  t.anchor_down_f16 = D.w_down_f16;
+  t.anchor_down_f16_exp = D.w_down_f16_exp;
   t.n_levels = 0;
   return t;
 }
@@ -778,7 +804,8 @@ lx_status run(const lx_tree_layer& t, int T, int k, const void* x, const int32_t
     ta.slot_flags[l] = ba.lv[l].slot_flags;
     ta.dgu[l] = (const float*)(W + q.gu);
     ta.hbar[l] = (float*)(W + q.hbar);
-    ta.hbar_mode[l] = l == 0 && P.lo8 ? HBAR_LO8 : fast[l] ? HBAR_HILO : HBAR_F32;
+    ta.hbar_mode[l] = l == 0 && P.f16 ? HBAR_F16 : l == 0 && P.lo8 ? HBAR_LO8 : fast[l] ? HBAR_HILO : HBAR_F32;
+    ta.hbar_exp[l] = l == 0 && P.f16 ? (int32_t*)(W + P.hbar_exp) : nullptr;
     ta.f24[l] = fast[l] ? 1 : 0;
     ta.y[l] = (const float*)(W + q.y);
   }
@@ -799,7 +826,20 @@ lx_status run(const lx_tree_layer& t, int T, int k, const void* x, const int32_t
     g.ncols[0] = d;
     g.C = (float*)(W + q.y);
     g.ldc = d;
-    if (P.lo8) {
+    if (P.f16) {
+      // row = fp16 [f] scaled by 2^hbar_exp[row]
+      g.lda = f;
+      g.K = f;
+      g.Kb = f;
+      g.B[0] = g.B[1] = t.anchor_down_f16;
+      g.a_row_exp = (const int32_t*)(W + P.hbar_exp);
+      g.b_exp = t.anchor_down_f16_exp;
+      g.tiles = ba.lv[0].tiles[kTabBig];
+      g.n_tiles = ba.lv[0].n_tiles[kTabBig];
+      if (!gemm_f16_ok(g, q.rows_max))
+        return fail(LX_ERR_UNSUPPORTED, "anchor_down: shape not supported by the fp16 GEMM");
+      LX_LAUNCH("anchor_down", launch_gemm_f16(g, OUT_F24, (int)q.tiles_max[kTabBig], lstream));
+    } else if (P.lo8) {
       // row = [bf16 hi (f) | fp8 lo (f bytes) | scale words (f / 64)] in 4f bytes
       g.lda = 2 * (int64_t)f;
       g.K = 2 * f;
@@ -1067,6 +1107,17 @@ lx_status lx_bucket(const lx_tree_layer* layer, int32_t T, int32_t k, const int3
   if (e == hipSuccess && slot_row)
     e = hipMemcpyAsync(slot_row, W + q.slot_row, (size_t)T * k * 4, hipMemcpyDeviceToDevice, s);
   if (e != hipSuccess) return fail(LX_ERR_HIP, hipGetErrorString(e));
+  return LX_OK;
+}
+
+lx_status lx_convert_f16(const void* w, int32_t n, int32_t rows, int32_t cols, void* w_f16, int32_t* exps,
+                         void* stream) {
+  g_err.clear();
+  if (n < 1 || rows < 1 || cols < 1) return fail(LX_ERR_INVALID_ARGUMENT, "n, rows and cols must be positive");
+  if (!w || !w_f16 || !exps || !aligned(w, 2) || !aligned(w_f16, 16) || !aligned(exps, 4))
+    return fail(LX_ERR_INVALID_ARGUMENT, "null or misaligned pointer");
+  const hipError_t e = launch_convert_f16(w, n, (int64_t)rows * cols, w_f16, exps, (hipStream_t)stream);
+  if (e != hipSuccess) return fail(LX_ERR_HIP, std::string("lx_convert_f16: ") + hipGetErrorString(e));
   return LX_OK;
 }
 

@@ -39,6 +39,7 @@
 
 namespace lx {
 namespace {
+int grid_cap();  // defined below
 
 typedef __bf16 bf16x8 __attribute__((ext_vector_type(8)));
 typedef __bf16 bf16x4 __attribute__((ext_vector_type(4)));
@@ -147,11 +148,28 @@ struct BigCfg {
   static constexpr int WPE = NW / 4;  // wavefronts per SIMD
 };
 
-template <int BM, int BN, int OUT, bool LO8 = false>
+typedef _Float16 f16x8 __attribute__((ext_vector_type(8)));
+
+// One 32x32x16 MFMA on 16-bit operands: bf16, or fp16 (the same bits
+// reinterpreted) for the fp16 anchor down projection.
+template <bool F16>
+__device__ __forceinline__ f32x16 mfma16(bf16x8 a, bf16x8 b, f32x16 c) {
+  if constexpr (F16)
+    return __builtin_amdgcn_mfma_f32_32x32x16_f16(__builtin_bit_cast(f16x8, a), __builtin_bit_cast(f16x8, b), c, 0,
+                                                  0, 0);
+  else
+    return __builtin_amdgcn_mfma_f32_32x32x16_bf16(a, b, c, 0, 0, 0);
+}
+
+// F16: A and W are fp16, both scaled by powers of two (A row r by
+// 2^a_row_exp[r], weight matrix i by 2^b_exp[i]); the epilogue multiplies
+// each output row by 2^-(a_row_exp[row] + b_exp[widx]), an exact rescale.
+template <int BM, int BN, int OUT, bool LO8 = false, bool F16 = false>
 __global__ __launch_bounds__((BigCfg<BM, BN>::NTHR), 1)
 __attribute__((amdgpu_waves_per_eu(BigCfg<BM, BN>::WPE, BigCfg<BM, BN>::WPE)))
 void k_gemm_big(GemmArgs p, int ntn) {
   static_assert(!LO8 || (BM == 256 && BN == 256), "fp8 lo: 256 x 256 tiles");
+  static_assert(!(LO8 && F16), "one precision mode at a time");
   constexpr int NTHR = BigCfg<BM, BN>::NTHR, WGN = BigCfg<BM, BN>::WGN;
   constexpr int MI = BM / 64;              // 32-row MFMA blocks per wavefront
   constexpr int NI = BN / (32 * WGN);      // 32-column MFMA blocks per wavefront
@@ -298,7 +316,7 @@ void k_gemm_big(GemmArgs p, int ntn) {
   do {                                                                              \
     _Pragma("unroll") for (int mi = 0; mi < MI; ++mi)                               \
       _Pragma("unroll") for (int ni = 0; ni < NI; ++ni)                             \
-        acc[mi][ni] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(FA[mi], FB[ni], acc[mi][ni], 0, 0, 0); \
+        acc[mi][ni] = mfma16<F16>(FA[mi], FB[ni], acc[mi][ni]);                   \
   } while (0)
 #define LX_COMPUTE(SA_, SB_)                                                        \
   do {                                                                              \
@@ -505,6 +523,7 @@ void k_gemm_big(GemmArgs p, int ntn) {
       float* const ep = (float*)smem + wave * (32 * PITCH);
       const int c4 = (lane % LPR) * 4;
       const int col = n0 + wn * WN + c4;
+      const int bexp = F16 ? p.b_exp[widx] : 0;
 #pragma unroll
       for (int mi = 0; mi < MI; ++mi) {
 #pragma unroll
@@ -515,9 +534,13 @@ void k_gemm_big(GemmArgs p, int ntn) {
 #pragma unroll
         for (int ps = 0; ps < 32 / RPP; ++ps) {
           const int rr = ps * RPP + lane / LPR;
-          const float4 v = *(const float4*)&ep[rr * PITCH + c4];
+          float4 v = *(const float4*)&ep[rr * PITCH + c4];
           const int r = wm * WM + mi * 32 + rr;
           if (r >= te.nrows || col >= ncol) continue;
+          if constexpr (F16) {
+            const int e = -(p.a_row_exp[te.row0 + r] + bexp);
+            v = make_float4(ldexpf(v.x, e), ldexpf(v.y, e), ldexpf(v.z, e), ldexpf(v.w, e));
+          }
           if (OUT == OUT_HILO) {
             // part p, local column c -> hi at base_p + c, lo at base_p + ncols[p] + c
             const int pp = col < p.ncols[0] ? 0 : 1;
@@ -1227,7 +1250,79 @@ __global__ __launch_bounds__(256) void k_quantize_f8(const u16* __restrict__ w, 
   sc[row * nsl + sl] = word;
 }
 
+// fp16 copy of bf16 weights, scaled per matrix by a power of two so that its
+// largest magnitude lands in [2^14, 2^15): max |w| per matrix (float bits
+// compare as integers for non-negative values), then the exponents, then the
+// conversion (round to nearest even; exact for every bf16 value down to
+// 2^-28 of the matrix maximum).
+__global__ __launch_bounds__(256) void k_absmax_bits(const u16* __restrict__ w, int64_t per, int n,
+                                                     uint32_t* __restrict__ mx) {
+  const int i = blockIdx.y;
+  uint32_t m = 0;
+  for (int64_t j = (int64_t)blockIdx.x * blockDim.x + threadIdx.x; j < per; j += (int64_t)gridDim.x * blockDim.x)
+    m = max(m, (uint32_t)(w[(int64_t)i * per + j] & 0x7FFFu) << 16);
+  for (int off = 32; off >= 1; off >>= 1) m = max(m, (uint32_t)__shfl_xor((int)m, off, 64));
+  if ((threadIdx.x & 63) == 0) atomicMax(mx + i, m);
+}
+
+__device__ __forceinline__ int f16_exp_for(uint32_t maxbits) {
+  if (maxbits == 0) return 0;
+  const int e = (int)(maxbits >> 23) - 127;  // floor(log2(max)); subnormal maxima count as 2^-127
+  const int s = 14 - e;
+  return s < -100 ? -100 : s > 100 ? 100 : s;
+}
+
+__global__ __launch_bounds__(256) void k_to_f16(const u16* __restrict__ w, int64_t per, int n,
+                                                const uint32_t* __restrict__ mx, _Float16* __restrict__ w16) {
+  const int i = blockIdx.y;
+  const int s = f16_exp_for(mx[i]);
+  for (int64_t j = (int64_t)blockIdx.x * blockDim.x + threadIdx.x; j < per; j += (int64_t)gridDim.x * blockDim.x) {
+    const float v = __uint_as_float((uint32_t)w[(int64_t)i * per + j] << 16);
+    w16[(int64_t)i * per + j] = (_Float16)ldexpf(v, s);
+  }
+}
+
+__global__ void k_f16_exps(uint32_t* __restrict__ mx, int n) {
+  const int i = blockIdx.x * blockDim.x + threadIdx.x;
+  if (i < n) mx[i] = (uint32_t)f16_exp_for(mx[i]);
+}
+
+__global__ void k_zero_u32(uint32_t* __restrict__ p, int n) {
+  const int i = blockIdx.x * blockDim.x + threadIdx.x;
+  if (i < n) p[i] = 0u;
+}
+
 }  // namespace
+
+hipError_t launch_convert_f16(const void* w, int n, int64_t per, void* w16, int32_t* exps, hipStream_t s) {
+  if (n <= 0 || per <= 0) return hipSuccess;
+  uint32_t* const mx = (uint32_t*)exps;
+  const int g1 = (n + 255) / 256;
+  hipLaunchKernelGGL(k_zero_u32, dim3(g1), dim3(256), 0, s, mx, n);
+  const int gx = (int)std::min<int64_t>((per + 255) / 256, 1024);
+  hipLaunchKernelGGL(k_absmax_bits, dim3(gx, n), dim3(256), 0, s, (const u16*)w, per, n, mx);
+  hipLaunchKernelGGL(k_to_f16, dim3(gx, n), dim3(256), 0, s, (const u16*)w, per, n, mx, (_Float16*)w16);
+  hipLaunchKernelGGL(k_f16_exps, dim3(g1), dim3(256), 0, s, mx, n);
+  return hipGetLastError();
+}
+
+bool gemm_f16_ok(const GemmArgs& g, int64_t a_rows_total) {
+  if (!g.a_row_exp || !g.b_exp || g.ncols[1] != 0 || g.K <= 0 || g.K % BK2 || (g.Kb > 0 && g.Kb != g.K)) return false;
+  return gemm_big_ok(g, 256, a_rows_total);
+}
+
+hipError_t launch_gemm_f16(const GemmArgs& g, int ofmt, int grid_tiles, hipStream_t s) {
+  const int ntn = (g.ncols[0] + 255) / 256;
+  int grid = grid_tiles * ntn;
+  if (grid <= 0) return hipSuccess;
+  const int cap = grid_cap();
+  if (grid > cap) grid = cap;
+  if (ofmt == OUT_F24)
+    hipLaunchKernelGGL((k_gemm_big<256, 256, OUT_F24, false, true>), dim3(grid), dim3(512), 0, s, g, ntn);
+  else
+    hipLaunchKernelGGL((k_gemm_big<256, 256, OUT_F32, false, true>), dim3(grid), dim3(512), 0, s, g, ntn);
+  return hipGetLastError();
+}
 
 bool gemm_lo8_ok(const GemmArgs& g, int64_t a_rows_total) {
   if (!g.b8 || !g.bsc || g.a_rows || g.ncols[1] != 0 || g.Kb <= 0 || g.K != 2 * g.Kb || g.Kb % BK2) return false;

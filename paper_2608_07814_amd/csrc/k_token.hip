@@ -101,6 +101,35 @@ __device__ __forceinline__ void hbar_store(void* base, int mode, int row, int c,
   const uint32_t be_next = __shfl_down(be, 8, 64);
   if ((c & 63) == 0) *(uint32_t*)(rb + 3 * f + (c >> 6) * 4) = be | (be_next << 8);
 }
+// HBAR_F16: the largest magnitude over a whole row (every thread of the
+// workgroup holds 4 of its values and must call this), then the row stored
+// as fp16 scaled by 2^s with the maximum in [2^14, 2^15) (s to exps[row]).
+constexpr int kMaxWaves = 16;
+__device__ __forceinline__ void hbar_store_f16(void* base, int32_t* exps, int row, int c, int f, float4 v) {
+  __shared__ float s_red[kMaxWaves];
+  float m = fmaxf(fmaxf(fabsf(v.x), fabsf(v.y)), fmaxf(fabsf(v.z), fabsf(v.w)));
+#pragma unroll
+  for (int off = 32; off >= 1; off >>= 1) m = fmaxf(m, __shfl_xor(m, off, 64));
+  if ((threadIdx.x & 63) == 0) s_red[threadIdx.x >> 6] = m;
+  __syncthreads();
+  float rm = 0.f;
+  for (int i = 0; i < (int)(blockDim.x >> 6); ++i) rm = fmaxf(rm, s_red[i]);
+  __syncthreads();  // s_red is reused by the next row
+  int sh = 0;
+  if (rm > 0.f) {
+    sh = 14 - ((int)((__float_as_uint(rm) >> 23) & 0xFF) - 127);
+    sh = sh < -100 ? -100 : sh > 100 ? 100 : sh;
+  }
+  typedef _Float16 h4 __attribute__((ext_vector_type(4)));
+  h4 q;
+  q[0] = (_Float16)ldexpf(v.x, sh);
+  q[1] = (_Float16)ldexpf(v.y, sh);
+  q[2] = (_Float16)ldexpf(v.z, sh);
+  q[3] = (_Float16)ldexpf(v.w, sh);
+  *(h4*)((_Float16*)base + (int64_t)row * f + c) = q;
+  if (threadIdx.x == 0) exps[row] = sh;
+}
+
 constexpr int kTokThr = 64, kTokCols = 4 * kTokThr;
 constexpr int kSlotGroups = 16;  // SwiGLU: up to 16 slots processed side by side
 
@@ -330,7 +359,10 @@ __global__ __launch_bounds__(kFastThr) void k_swiglu_fast(TokenArgs a) {
 #pragma unroll
       for (int j = j0; j < kFastK; ++j)
         if (row[l][j] == row[l][j0] && (fl[NL][j] & 1)) add4(hs, h[j]);
-      hbar_store(a.hbar[l], a.hbar_mode[l], row[l][j0], c, f, hs);
+      if (a.hbar_mode[l] == HBAR_F16)  // (whole rows per workgroup: see the launch)
+        hbar_store_f16(a.hbar[l], a.hbar_exp[l], row[l][j0], c, f, hs);
+      else
+        hbar_store(a.hbar[l], a.hbar_mode[l], row[l][j0], c, f, hs);
     }
 }
 
@@ -389,10 +421,18 @@ static int uniform_fmt(const TokenArgs& a) {
 hipError_t launch_swiglu_reduce(const TokenArgs& a, hipStream_t s) {
   if (a.T == 0) return hipSuccess;
   const int fmt = uniform_fmt(a);
-  if (a.k <= kFastK && a.L >= 1 && a.L <= kFastL && fmt >= 0) {
+  bool f16 = false;
+  for (int l = 0; l <= a.L; ++l) f16 |= a.hbar_mode[l] == HBAR_F16;
+  if (a.k <= kFastK && a.L <= kFastL && fmt >= 0) {
     const int thr = fast_threads(a.f, a.T);
     const dim3 grid(a.T, (a.f / 4 + thr - 1) / thr);
-    if (a.L == 1 && fmt)
+    // fp16 rows need every row's values in one workgroup, all threads live
+    if (f16 && (grid.y != 1 || thr * 4 != a.f)) return hipErrorInvalidValue;
+    if (a.L == 0 && fmt)
+      hipLaunchKernelGGL((k_swiglu_fast<0, true>), grid, dim3(thr), 0, s, a);
+    else if (a.L == 0)
+      hipLaunchKernelGGL((k_swiglu_fast<0, false>), grid, dim3(thr), 0, s, a);
+    else if (a.L == 1 && fmt)
       hipLaunchKernelGGL((k_swiglu_fast<1, true>), grid, dim3(thr), 0, s, a);
     else if (a.L == 1)
       hipLaunchKernelGGL((k_swiglu_fast<1, false>), grid, dim3(thr), 0, s, a);
@@ -402,6 +442,7 @@ hipError_t launch_swiglu_reduce(const TokenArgs& a, hipStream_t s) {
       hipLaunchKernelGGL((k_swiglu_fast<2, false>), grid, dim3(thr), 0, s, a);
     return hipGetLastError();
   }
+  if (f16) return hipErrorInvalidValue;  // the general kernel splits rows
   const int groups = a.k < kSlotGroups ? a.k : kSlotGroups;
   hipLaunchKernelGGL(k_swiglu_reduce, dim3(a.T, (a.f + kTokCols - 1) / kTokCols), dim3(kTokThr * groups),
                      (size_t)a.k * kTokThr * sizeof(float4), s, a);

@@ -37,8 +37,10 @@ __device__ __forceinline__ float4 f24_unpack(F24x4 w) {
 
 // Output format of a GEMM: fp32, a bf16 (hi, lo) pair, or f24.
 enum OutFmt { OUT_F32 = 0, OUT_HILO = 1, OUT_F24 = 2 };
-// Format of the weighted activation sums (the down GEMMs' input).
-enum HbarMode { HBAR_F32 = 0, HBAR_HILO = 1, HBAR_LO8 = 2 };
+// Format of the weighted activation sums (the down GEMMs' input); HBAR_F16:
+// fp16 rows of f values scaled by 2^exp (exp per row, in a separate array,
+// chosen so that the row's largest magnitude lands in [2^14, 2^15)).
+enum HbarMode { HBAR_F32 = 0, HBAR_HILO = 1, HBAR_LO8 = 2, HBAR_F16 = 3 };
 
 // ---------------------------------------------------------------- fp8 lo
 // The low half of a bf16 (hi, lo) split only needs a few bits: where the
@@ -228,6 +230,10 @@ struct GemmArgs {
   // another level; below 0: the tile is skipped) instead of its own
   const int32_t* widx_anc;
   const int32_t* widx_fac;
+  // fp16 anchor down projection (launch_gemm_f16): A row r is scaled by
+  // 2^a_row_exp[r], weight matrix i by 2^b_exp[i]
+  const int32_t* a_row_exp;
+  const int32_t* b_exp;
 };
 
 enum AMode { A_BF16 = 0, A_F32_HILO = 1 };
@@ -251,6 +257,15 @@ bool gemm_big_ok(const GemmArgs& g, int bn, int64_t a_rows_total);
 // above, lo slabs from the fp8 copies with the block-scaled fp8 MFMA.
 bool gemm_lo8_ok(const GemmArgs& g, int64_t a_rows_total);
 hipError_t launch_gemm_lo8(const GemmArgs& g, int ofmt, int grid_tiles, hipStream_t s);
+// The fp16 variant (256 x 256 tiles, one part, K = Kb): A and W fp16 with
+// their power-of-two scales (GemmArgs::a_row_exp, b_exp), undone exactly in
+// the epilogue.
+bool gemm_f16_ok(const GemmArgs& g, int64_t a_rows_total);
+hipError_t launch_gemm_f16(const GemmArgs& g, int ofmt, int grid_tiles, hipStream_t s);
+// Weights [n][per] bf16 -> fp16 [n][per] scaled per matrix i by 2^exps[i]
+// (exps[i] puts the matrix's largest magnitude in [2^14, 2^15); 0 for an
+// all-zero matrix).
+hipError_t launch_convert_f16(const void* w, int n, int64_t per, void* w16, int32_t* exps, hipStream_t s);
 // Weights [n][rows][cols] bf16 -> fp8 copy [n][rows][cols] and scale words
 // [n][rows][cols / 64] (cols a multiple of 64).
 hipError_t launch_quantize_f8(const void* w, int64_t n_rows, int cols, uint8_t* w8, uint32_t* sc, hipStream_t s);
@@ -336,6 +351,7 @@ struct TokenArgs {
                                        // lo [f]; HBAR_LO8 bf16 hi [f], fp8 lo [f bytes],
                                        // scale words [f / 64]
   int32_t hbar_mode[kMaxLvl];
+  int32_t* hbar_exp[kMaxLvl];          // HBAR_F16: per-row scale exponents
   const float* y[kMaxLvl];             // [rows_l][d] down outputs per level
   int32_t merged;                      // 1: the gate|up and down corrections of
                                        // levels 1 .. L-1 are folded into level

@@ -41,7 +41,8 @@ class LxTreeLayer(ctypes.Structure):
                 ("n_anchors", _c_i32), ("anchor_gate", _c_void), ("anchor_up", _c_void),
                 ("anchor_down", _c_void), ("n_levels", _c_i32),
                 ("levels", LxLevel * LX_MAX_LEVELS),
-                ("anchor_down_f8", _c_void), ("anchor_down_f8_scale", _c_void)]
+                ("anchor_down_f8", _c_void), ("anchor_down_f8_scale", _c_void),
+                ("anchor_down_f16", _c_void), ("anchor_down_f16_exp", _c_void)]
 
 
 class LxFlatLayer(ctypes.Structure):
@@ -50,13 +51,15 @@ class LxFlatLayer(ctypes.Structure):
                 ("dom_gate", _c_void), ("dom_up", _c_void), ("dom_down", _c_void),
                 ("a_gate", _c_void), ("b_gate", _c_void), ("a_up", _c_void), ("b_up", _c_void),
                 ("a_down", _c_void), ("b_down", _c_void),
-                ("dom_down_f8", _c_void), ("dom_down_f8_scale", _c_void)]
+                ("dom_down_f8", _c_void), ("dom_down_f8_scale", _c_void),
+                ("dom_down_f16", _c_void), ("dom_down_f16_exp", _c_void)]
 
 
 class LxDenseLayer(ctypes.Structure):
     _fields_ = [("E", _c_i32), ("d", _c_i32), ("f", _c_i32), ("dtype", _c_i32),
                 ("w_gate", _c_void), ("w_up", _c_void), ("w_down", _c_void),
-                ("w_down_f8", _c_void), ("w_down_f8_scale", _c_void)]
+                ("w_down_f8", _c_void), ("w_down_f8_scale", _c_void),
+                ("w_down_f16", _c_void), ("w_down_f16_exp", _c_void)]
 
 
 EXPORTS = {
@@ -81,6 +84,7 @@ EXPORTS = {
     "lx_bucket": (_c_i32, [ctypes.POINTER(LxTreeLayer), _c_i32, _c_i32, _c_void, _c_i32, _c_void,
                            _c_void, _c_void, _c_void, ctypes.c_size_t, _c_void]),
     "lx_read_device_status": (_c_i32, [_c_void, _c_void, ctypes.POINTER(ctypes.c_uint32)]),
+    "lx_convert_f16": (_c_i32, [_c_void, _c_i32, _c_i32, _c_i32, _c_void, _c_void, _c_void]),
     "lx_quantize_f8": (_c_i32, [_c_void, _c_i32, _c_i32, _c_i32, _c_void, _c_void, _c_void]),
     "lx_route_workspace_bytes": (ctypes.c_size_t, [_c_i32, _c_i32, _c_i32]),
     "lx_coact_distance": (_c_i32, [_c_void, _c_i32, _c_i32, _c_i32, _c_void, _c_void, _c_void, _c_void]),
@@ -197,6 +201,10 @@ class DeviceLayer:
     # int32 scale words [n][d][f // 64]
     anchor_down_f8: Optional[torch.Tensor] = None
     anchor_down_f8_scale: Optional[torch.Tensor] = None
+    # optional fp16 copy of anchor_down (lx_convert_f16): fp16 [n][d][f] and
+    # int32 scale exponents [n]
+    anchor_down_f16: Optional[torch.Tensor] = None
+    anchor_down_f16_exp: Optional[torch.Tensor] = None
 
     @property
     def lx_dtype(self) -> int:
@@ -213,6 +221,7 @@ class DeviceLayer:
         s.anchor_gate, s.anchor_up, s.anchor_down = (_ptr(self.anchor_gate), _ptr(self.anchor_up),
                                                      _ptr(self.anchor_down))
         s.anchor_down_f8, s.anchor_down_f8_scale = _ptr(self.anchor_down_f8), _ptr(self.anchor_down_f8_scale)
+        s.anchor_down_f16, s.anchor_down_f16_exp = _ptr(self.anchor_down_f16), _ptr(self.anchor_down_f16_exp)
         s.n_levels = len(self.levels)
         for i, lv in enumerate(self.levels):
             c = s.levels[i]
@@ -234,6 +243,7 @@ class DeviceLayer:
         s.dom_gate, s.dom_up, s.dom_down = (_ptr(self.anchor_gate), _ptr(self.anchor_up),
                                             _ptr(self.anchor_down))
         s.dom_down_f8, s.dom_down_f8_scale = _ptr(self.anchor_down_f8), _ptr(self.anchor_down_f8_scale)
+        s.dom_down_f16, s.dom_down_f16_exp = _ptr(self.anchor_down_f16), _ptr(self.anchor_down_f16_exp)
         s.a_gate, s.b_gate, s.a_up, s.b_up, s.a_down, s.b_down = (
             _ptr(lv.a_gate), _ptr(lv.b_gate), _ptr(lv.a_up), _ptr(lv.b_up), _ptr(lv.a_down),
             _ptr(lv.b_down))
@@ -246,6 +256,7 @@ class DeviceLayer:
         s.E, s.d, s.f, s.dtype = self.E, self.d, self.f, self.lx_dtype
         s.w_gate, s.w_up, s.w_down = _ptr(self.anchor_gate), _ptr(self.anchor_up), _ptr(self.anchor_down)
         s.w_down_f8, s.w_down_f8_scale = _ptr(self.anchor_down_f8), _ptr(self.anchor_down_f8_scale)
+        s.w_down_f16, s.w_down_f16_exp = _ptr(self.anchor_down_f16), _ptr(self.anchor_down_f16_exp)
         return s
 
 
@@ -409,6 +420,26 @@ def weighted_factors(w_dom: torch.Tensor, w_mem: torch.Tensor, r: int, x: torch.
     return A, B, sig
 
 
+def convert_f16(w: torch.Tensor, stream=None):
+    """fp16 copy of bf16 weights [n][rows][cols] (lx_convert_f16): returns
+    (fp16 [n][rows][cols] = w * 2^exps[i] per matrix, int32 exps [n])."""
+    if w.dtype != torch.bfloat16 or not w.is_contiguous() or w.dim() != 3:
+        raise ValueError("w must be a contiguous bf16 [n][rows][cols] tensor")
+    n, rows, cols = (int(v) for v in w.shape)
+    w16 = torch.empty(n, rows, cols, dtype=torch.float16, device=w.device)
+    ex = torch.empty(n, dtype=torch.int32, device=w.device)
+    _check(lib().lx_convert_f16(_ptr(w), n, rows, cols, _ptr(w16), _ptr(ex), _stream(stream)))
+    return w16, ex
+
+
+def attach_down_f16(layer: "DeviceLayer") -> "DeviceLayer":
+    """Give a bf16 layer the fp16 copy of its anchor down weights; a no-op
+    for fp32 layers."""
+    if layer.dtype == "bf16":
+        layer.anchor_down_f16, layer.anchor_down_f16_exp = convert_f16(layer.anchor_down)
+    return layer
+
+
 def attach_down_f8(layer: "DeviceLayer") -> "DeviceLayer":
     """Give a bf16 layer the fp8 copy of its anchor down weights (used by the
     anchor down projection where applicable); a no-op for other layers."""
@@ -417,11 +448,12 @@ def attach_down_f8(layer: "DeviceLayer") -> "DeviceLayer":
     return layer
 
 
-def to_device(layer, device="cuda", lo8: bool = True) -> DeviceLayer:
+def to_device(layer, device="cuda", lo8: bool = True, f16: bool = True) -> DeviceLayer:
     """Copy a host layer (fields as in ``lxsynth.Layer``) to device tensors.
     ``lo8``: also prepare the fp8 copy of the anchor down weights (bf16 layers
-    with f a multiple of 64), so the anchor down projection takes its fp8-lo
-    path."""
+    with f a multiple of 64), so the anchor down projection can take its
+    fp8-lo path; ``f16``: also prepare their fp16 copy (bf16 layers), for the
+    fp16 path (preferred where it applies)."""
     dt = layer.dtype
     levels = []
     for lv in layer.levels:
@@ -435,7 +467,11 @@ def to_device(layer, device="cuda", lo8: bool = True) -> DeviceLayer:
                      anchor_gate=_dev_array(layer.anchor_gate, dt, device),
                      anchor_up=_dev_array(layer.anchor_up, dt, device),
                      anchor_down=_dev_array(layer.anchor_down, dt, device), levels=levels)
-    return attach_down_f8(dl) if lo8 else dl
+    if lo8:
+        dl = attach_down_f8(dl)
+    if f16:
+        dl = attach_down_f16(dl)
+    return dl
 
 
 # ----------------------------------------------------------------- calls

@@ -14,11 +14,14 @@ TOL_BF16 = 1e-2
 # fp32 end to end: a tighter self-check that catches logic slips
 TOL_F32 = 1e-4
 # The library's precision policy (bf16 hi+lo pairs for every fp32
-# intermediate that feeds a GEMM) lands near 2e-5 * RMS, or near 5e-4 * RMS
-# where the anchor down projection carries the lo half in block-scaled fp8;
-# this looser design bound catches a lost lo half (~1e-2) or a mis-indexed
-# K-slab well before the acceptance bar would.
-TOL_DESIGN = 1e-3
+# intermediate that feeds a GEMM) lands near 2e-5 * RMS, near 5e-4 * RMS
+# where the anchor down projection carries the lo half in block-scaled fp8,
+# and near 1.3e-3 * RMS where it multiplies fp16 activation sums (fp16
+# rounding of the sums alone, emulated in fp64 on the 30B-A3B and tree
+# shapes: 1.0-1.3e-3); this looser design bound catches a lost lo half or a
+# bf16-rounded sum (~1e-2) or a mis-indexed K-slab well before the
+# acceptance bar would.
+TOL_DESIGN = 3e-3
 
 
 def require_gpu():

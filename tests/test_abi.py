@@ -28,7 +28,7 @@ def _declared(root):
 
 def test_every_declared_symbol_is_exported(L, root):
     names = _declared(root)
-    assert len(names) == len(lx.EXPORTS) == 32
+    assert len(names) == len(lx.EXPORTS) == 33
     for n in names:
         assert hasattr(L, n), n
         assert n in lx.EXPORTS, n
@@ -312,3 +312,15 @@ def test_static_forward_refuses_batches_beyond_its_scratch(L):
     assert L.lx_moe_forward_tree_static(ctypes.byref(s), 4, 0, FAKE, FAKE, FAKE, FAKE, lx.LX_F32, None) == \
         lx.LX_ERR_INVALID_ARGUMENT
     assert L.lx_moe_tree_workspace_bytes(ctypes.byref(s), 64, 8) <= lx.STATIC_SCRATCH_BYTES
+
+
+def test_convert_f16_validation(L):
+    assert L.lx_convert_f16(FAKE, 0, 4, 4, FAKE, FAKE, None) == lx.LX_ERR_INVALID_ARGUMENT
+    assert L.lx_convert_f16(FAKE, 1, 4, 4, FAKE + 8, FAKE, None) == lx.LX_ERR_INVALID_ARGUMENT  # w_f16 % 16
+    assert L.lx_convert_f16(None, 1, 4, 4, FAKE, FAKE, None) == lx.LX_ERR_INVALID_ARGUMENT
+    # a layer whose fp16 down copy lacks its exponents is refused
+    s = _tree()
+    s.anchor_down_f16 = FAKE
+    assert L.lx_moe_tree_workspace_bytes(ctypes.byref(s), 64, 8) == 0
+    s.anchor_down_f16_exp = FAKE
+    assert L.lx_moe_tree_workspace_bytes(ctypes.byref(s), 64, 8) > 0

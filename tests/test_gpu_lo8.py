@@ -1,4 +1,4 @@
-"""The fp8 lo half of the anchor down projection.
+"""The anchor down projection's precision modes: the fp8 lo half and fp16.
 
 lx_quantize_f8 is checked byte for byte against an encoder written here from
 the format definitions (OCP e4m3: sign, 4 exponent bits with bias 7, 3
@@ -74,8 +74,8 @@ def test_lo8_forward_vs_oracle_and_bf16_pair(cfg, T):
     require_gpu()
     p = make_problem(cfg, T=T)
     ref = O.moe_forward(p.layer, p.x, p.routing.topk_ids, p.routing.topk_weights)
-    e8 = err_ratio(gpu_forward(p, dev_layer=lx.to_device(p.layer, lo8=True)), ref)
-    e16 = err_ratio(gpu_forward(p, dev_layer=lx.to_device(p.layer, lo8=False)), ref)
+    e8 = err_ratio(gpu_forward(p, dev_layer=lx.to_device(p.layer, lo8=True, f16=False)), ref)
+    e16 = err_ratio(gpu_forward(p, dev_layer=lx.to_device(p.layer, lo8=False, f16=False)), ref)
     say(f"cfg{cfg} T={T}: fp8-lo err/RMS {e8:.3e}, bf16-pair err/RMS {e16:.3e}")
     assert e16 <= TOL_DESIGN
     assert e8 <= TOL_DESIGN
@@ -92,6 +92,57 @@ def test_lo8_dense_comparator():
     x = f32_to_bf16_bits(rng.standard_normal((300, 256)).astype(np.float32))
     ids, w = random_routing(300, 4, 16, 16)
     p = Problem(cfg={}, seed=15, layer=layer, x=x, routing=Routing(ids, w))
-    got = gpu_forward(p, kind="dense", dev_layer=lx.to_device(layer, lo8=True))
+    got = gpu_forward(p, kind="dense", dev_layer=lx.to_device(layer, lo8=True, f16=False))
     ref = O.moe_forward(layer, x, ids, w)
     assert err_ratio(got, ref) <= TOL_DESIGN
+
+
+def test_convert_f16_exact():
+    """lx_convert_f16: per matrix the exponent puts the largest magnitude in
+    [2^14, 2^15), and every value is the bf16 value times 2^exp exactly (all
+    of these are within fp16's normal range after scaling); an all-zero
+    matrix gets exponent 0."""
+    require_gpu()
+    rng = np.random.default_rng(41)
+    w = (rng.standard_normal((4, 16, 320)) * 0.02).astype(np.float32)
+    w[1] *= 3000.0           # large weights
+    w[2] = 0.0               # all zero
+    w[3] *= 1e-6             # tiny weights
+    w[3, 0, 0] = 2.0 ** -20  # an exact power of two as the maximum
+    wt = torch.from_numpy(w).cuda().to(torch.bfloat16)
+    w16, ex = lx.convert_f16(wt)
+    torch.cuda.synchronize()
+    wv = wt.float().cpu().numpy().astype(np.float64)
+    ex = ex.cpu().numpy()
+    for i in range(4):
+        m = np.abs(wv[i]).max()
+        want = 0 if m == 0 else 14 - int(np.floor(np.log2(m)))
+        assert ex[i] == want, (i, ex[i], want)
+        got = w16[i].float().cpu().numpy().astype(np.float64) * 2.0 ** -int(ex[i])
+        assert np.array_equal(got, wv[i]), i
+
+
+@pytest.mark.parametrize("cfg,T,kind", [(1, 1024, None), (4, 600, None), ("dense", 600, "dense")])
+def test_f16_forward(cfg, T, kind):
+    """With the fp16 copy the anchor down projection multiplies fp16 sums
+    (a different result from the fp8-lo path: the path ran) within the
+    design bound, and the output meets the bar, flat, tree and uncompressed."""
+    require_gpu()
+    if cfg == "dense":
+        from lxsynth import make_layer_flat, Problem, Routing, f32_to_bf16_bits
+        from helpers import random_routing
+        layer = make_layer_flat(16, 16, 256, 256, 8, "bf16", 44)
+        layer.levels = []
+        rng = np.random.default_rng(45)
+        x = f32_to_bf16_bits(rng.standard_normal((T, 256)).astype(np.float32))
+        ids, w = random_routing(T, 4, 16, 46)
+        p = Problem(cfg={}, seed=45, layer=layer, x=x, routing=Routing(ids, w))
+    else:
+        p = make_problem(cfg, T=T)
+    ref = O.moe_forward(p.layer, p.x, p.routing.topk_ids, p.routing.topk_weights)
+    g16 = gpu_forward(p, kind=kind, dev_layer=lx.to_device(p.layer, lo8=True, f16=True))
+    g8 = gpu_forward(p, kind=kind, dev_layer=lx.to_device(p.layer, lo8=True, f16=False))
+    e16, e8 = err_ratio(g16, ref), err_ratio(g8, ref)
+    say(f"{cfg} T={T}: fp16 err/RMS {e16:.3e}, fp8-lo err/RMS {e8:.3e}")
+    assert not np.array_equal(g16, g8)
+    assert e16 <= TOL_DESIGN and e16 <= TOL_BF16
