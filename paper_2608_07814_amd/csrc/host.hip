@@ -701,7 +701,7 @@ lx_status run(const lx_tree_layer& t, int T, int k, const void* x, const int32_t
     g.ldc = 2 * (int64_t)f;
     g.c_coloff[1] = f;
     if (fast[0])
-      LX_TRY(big("anchor_gate_up", g, 0, kBigBM, 256, OUT_F24, T));
+      LX_TRY(big("anchor_gate_up", g, 0, kBigBM, 256, OUT_X16, T));
     else
       LX_TRY(small("anchor_gate_up", g, 0, A_BF16));
   }
@@ -778,7 +778,7 @@ lx_status run(const lx_tree_layer& t, int T, int k, const void* x, const int32_t
       h.K = 2 * r;
       h.Kb = r;
       // gate and up read different z columns: tiles must not straddle them
-      LX_TRY(big(kLowOut[l], h, l, kBigBM, f % 256 == 0 ? 256 : f % 128 == 0 ? 128 : 64, OUT_F24, q.rows_max));
+      LX_TRY(big(kLowOut[l], h, l, kBigBM, f % 256 == 0 ? 256 : f % 128 == 0 ? 128 : 64, OUT_X16, q.rows_max));
     } else {
       h.lda = 2 * (int64_t)r;
       h.a_koff[1] = r;
@@ -806,7 +806,7 @@ lx_status run(const lx_tree_layer& t, int T, int k, const void* x, const int32_t
     ta.hbar[l] = (float*)(W + q.hbar);
     ta.hbar_mode[l] = l == 0 && P.f16 ? HBAR_F16 : l == 0 && P.lo8 ? HBAR_LO8 : fast[l] ? HBAR_HILO : HBAR_F32;
     ta.hbar_exp[l] = l == 0 && P.f16 ? (int32_t*)(W + P.hbar_exp) : nullptr;
-    ta.f24[l] = fast[l] ? 1 : 0;
+    ta.x16[l] = fast[l] ? 1 : 0;
     ta.y[l] = (const float*)(W + q.y);
   }
   ta.out = out;
@@ -838,7 +838,7 @@ lx_status run(const lx_tree_layer& t, int T, int k, const void* x, const int32_t
       g.n_tiles = ba.lv[0].n_tiles[kTabBig];
       if (!gemm_f16_ok(g, q.rows_max))
         return fail(LX_ERR_UNSUPPORTED, "anchor_down: shape not supported by the fp16 GEMM");
-      LX_LAUNCH("anchor_down", launch_gemm_f16(g, OUT_F24, (int)q.tiles_max[kTabBig], lstream));
+      LX_LAUNCH("anchor_down", launch_gemm_f16(g, OUT_X16, (int)q.tiles_max[kTabBig], lstream));
     } else if (P.lo8) {
       // row = [bf16 hi (f) | fp8 lo (f bytes) | scale words (f / 64)] in 4f bytes
       g.lda = 2 * (int64_t)f;
@@ -853,12 +853,12 @@ lx_status run(const lx_tree_layer& t, int T, int k, const void* x, const int32_t
       g.n_tiles = ba.lv[0].n_tiles[kTabBig];
       if (!gemm_lo8_ok(g, q.rows_max))
         return fail(LX_ERR_UNSUPPORTED, "anchor_down: shape not supported by the fp8-lo GEMM");
-      LX_LAUNCH("anchor_down", launch_gemm_lo8(g, OUT_F24, (int)q.tiles_max[kTabBig], lstream));
+      LX_LAUNCH("anchor_down", launch_gemm_lo8(g, OUT_X16, (int)q.tiles_max[kTabBig], lstream));
     } else if (fast[0]) {
       g.lda = 2 * (int64_t)f;
       g.K = 2 * f;
       g.Kb = f;
-      LX_TRY(big("anchor_down", g, 0, kBigBM, 256, OUT_F24, q.rows_max));
+      LX_TRY(big("anchor_down", g, 0, kBigBM, 256, OUT_X16, q.rows_max));
     } else {
       g.lda = f;
       g.K = f;
@@ -927,7 +927,7 @@ lx_status run(const lx_tree_layer& t, int T, int k, const void* x, const int32_t
       h.lda = 2 * (int64_t)r;
       h.K = 2 * r;
       h.Kb = r;
-      LX_TRY(big(kDownOut[l], h, l, kBigBM, 256, OUT_F24, q.rows_max));
+      LX_TRY(big(kDownOut[l], h, l, kBigBM, 256, OUT_X16, q.rows_max));
     } else {
       h.lda = r;
       h.K = r;

@@ -21,7 +21,7 @@
 //     against the same W, i.e. C = (A_hi + A_lo) W^T, which keeps ~16 bits of
 //     an fp32 intermediate at bf16 MFMA rate;
 //   * output fp32, a bf16 (hi, lo) pair ready to feed the next GEMM as its
-//     two K-halves, or f24 (rows read back only by the elementwise kernels);
+//     two K-halves, or x16 (rows read back only by the elementwise kernels);
 //   * persistent: the grid is at most one workgroup per compute unit and each
 //     workgroup loops over (tile, n-tile) work items, so the epilogue of one
 //     item and the prologue loads of the next are not separated by a
@@ -559,8 +559,8 @@ void k_gemm_big(GemmArgs p, int ntn) {
             __bf16* const rowp = (__bf16*)p.C + (int64_t)(te.row0 + r) * p.ldc;
             *(bf16x4*)(rowp + hi_col) = h;
             *(bf16x4*)(rowp + lo_col) = l;
-          } else if (OUT == OUT_F24) {
-            *(F24x4*)((uint8_t*)p.C + ((int64_t)(te.row0 + r) * p.ldc + col) * 3) = f24_pack(v);
+          } else if (OUT == OUT_X16) {
+            x16_store(p.C, te.row0 + r, p.ldc, col, v);
           } else {
             *(float4*)(p.C + (int64_t)(te.row0 + r) * p.ldc + col) = v;
           }
@@ -574,7 +574,7 @@ void k_gemm_big(GemmArgs p, int ntn) {
 // ---------------------------------------------------------------- segmented
 // The correction products of several tree levels that land on the same rows
 // (the leaf rows), as one 256 x 256-tile GEMM whose K runs over the levels'
-// operands in turn (segments). Everything else is the 256 x 256 f24
+// operands in turn (segments). Everything else is the 256 x 256 x16
 // configuration of k_gemm_big: 8 wavefronts in a 2 x 4 grid of 128 x 64
 // blocks, both operands HBM -> LDS by direct loads into a 2-stage ring of
 // 64-wide K-slabs, persistent XCD-ordered work items, epilogue through LDS.
@@ -765,7 +765,7 @@ void k_gemm_seg(GemmArgs p, SegArgs sg, int ntn) {
 #undef LX_SMFMAS
 #undef LX_SFRAG
 
-    // Epilogue (as k_gemm_big's f24 output): per-wavefront LDS transpose,
+    // Epilogue (as k_gemm_big's x16 output): per-wavefront LDS transpose,
     // then 4 consecutive columns per lane.
     {
       constexpr int PITCH = WN + 4;
@@ -788,7 +788,7 @@ void k_gemm_seg(GemmArgs p, SegArgs sg, int ntn) {
           const float4 v = *(const float4*)&ep[rr * PITCH + c4];
           const int r = wm * WM + mi * 32 + rr;
           if (r >= te.nrows || col >= ncol) continue;
-          *(F24x4*)((uint8_t*)p.C + ((int64_t)(te.row0 + r) * p.ldc + col) * 3) = f24_pack(v);
+          x16_store(p.C, te.row0 + r, p.ldc, col, v);
         }
       }
     }
@@ -969,8 +969,8 @@ __device__ __forceinline__ void sk_epilogue(const SkUnit& u, const f32x16& acc, 
       __bf16* const rowp = (__bf16*)p.C + (int64_t)(te.row0 + r) * p.ldc;
       *(bf16x4*)(rowp + hi_col) = h;
       *(bf16x4*)(rowp + lo_col) = l;
-    } else if (u.ofmt == OUT_F24) {
-      *(F24x4*)((uint8_t*)p.C + ((int64_t)(te.row0 + r) * p.ldc + col) * 3) = f24_pack(v);
+    } else if (u.ofmt == OUT_X16) {
+      x16_store(p.C, te.row0 + r, p.ldc, col, v);
     } else {
       *(float4*)(p.C + (int64_t)(te.row0 + r) * p.ldc + col) = v;
     }
@@ -1212,8 +1212,8 @@ template <int BM, int BN>
 hipError_t launch_bn(const GemmArgs& g, int ofmt, int grid, int ntn, hipStream_t s) {
   if (ofmt == OUT_HILO)
     hipLaunchKernelGGL((k_gemm_big<BM, BN, OUT_HILO>), dim3(grid), dim3(BigCfg<BM, BN>::NTHR), 0, s, g, ntn);
-  else if (ofmt == OUT_F24)
-    hipLaunchKernelGGL((k_gemm_big<BM, BN, OUT_F24>), dim3(grid), dim3(BigCfg<BM, BN>::NTHR), 0, s, g, ntn);
+  else if (ofmt == OUT_X16)
+    hipLaunchKernelGGL((k_gemm_big<BM, BN, OUT_X16>), dim3(grid), dim3(BigCfg<BM, BN>::NTHR), 0, s, g, ntn);
   else
     hipLaunchKernelGGL((k_gemm_big<BM, BN, OUT_F32>), dim3(grid), dim3(BigCfg<BM, BN>::NTHR), 0, s, g, ntn);
   return hipGetLastError();
@@ -1311,14 +1311,18 @@ bool gemm_f16_ok(const GemmArgs& g, int64_t a_rows_total) {
   return gemm_big_ok(g, 256, a_rows_total);
 }
 
+// x16 rows need a row length that keeps every 8-byte mantissa word aligned.
+static bool x16_shape_ok(const GemmArgs& g, int ofmt) { return ofmt != OUT_X16 || g.ldc % 32 == 0; }
+
 hipError_t launch_gemm_f16(const GemmArgs& g, int ofmt, int grid_tiles, hipStream_t s) {
+  if (!x16_shape_ok(g, ofmt)) return hipErrorInvalidValue;
   const int ntn = (g.ncols[0] + 255) / 256;
   int grid = grid_tiles * ntn;
   if (grid <= 0) return hipSuccess;
   const int cap = grid_cap();
   if (grid > cap) grid = cap;
-  if (ofmt == OUT_F24)
-    hipLaunchKernelGGL((k_gemm_big<256, 256, OUT_F24, false, true>), dim3(grid), dim3(512), 0, s, g, ntn);
+  if (ofmt == OUT_X16)
+    hipLaunchKernelGGL((k_gemm_big<256, 256, OUT_X16, false, true>), dim3(grid), dim3(512), 0, s, g, ntn);
   else
     hipLaunchKernelGGL((k_gemm_big<256, 256, OUT_F32, false, true>), dim3(grid), dim3(512), 0, s, g, ntn);
   return hipGetLastError();
@@ -1371,6 +1375,7 @@ int grid_cap() {
 }  // namespace
 
 hipError_t launch_gemm_big(const GemmArgs& g, int bm, int bn, int ofmt, int grid_tiles, hipStream_t s) {
+  if (!x16_shape_ok(g, ofmt)) return hipErrorInvalidValue;
   const int ntn = (g.ncols[0] + g.ncols[1] + bn - 1) / bn;
   int grid = grid_tiles * ntn;  // upper bound on work items
   if (grid <= 0) return hipSuccess;
@@ -1391,7 +1396,7 @@ bool gemm_seg_ok(const GemmArgs& g, const SegArgs& sa, int64_t out_rows) {
   const int ncol = g.ncols[0] + g.ncols[1];
   // tiles never straddle the two parts (their A columns differ)
   if (g.ncols[1] > 0 && g.ncols[0] % 256) return false;
-  if (g.ncols[0] % 4 || g.ncols[1] % 4 || g.ldc % 4 || g.ldc < ncol || ((uintptr_t)g.C & 3)) return false;
+  if (g.ncols[0] % 4 || g.ncols[1] % 4 || g.ldc % 32 || g.ldc < ncol || ((uintptr_t)g.C & 7)) return false;
   if (out_rows * g.ldc * 3 >= ((int64_t)1 << 40)) return false;
   for (int i = 0; i < sa.nseg; ++i) {
     const SegDesc& d = sa.s[i];
@@ -1416,13 +1421,14 @@ hipError_t launch_gemm_seg(const GemmArgs& g, const SegArgs& sa, int grid_tiles,
 }
 
 hipError_t launch_gemm_lo8(const GemmArgs& g, int ofmt, int grid_tiles, hipStream_t s) {
+  if (!x16_shape_ok(g, ofmt)) return hipErrorInvalidValue;
   const int ntn = (g.ncols[0] + 255) / 256;
   int grid = grid_tiles * ntn;
   if (grid <= 0) return hipSuccess;
   const int cap = grid_cap();
   if (grid > cap) grid = cap;
-  if (ofmt == OUT_F24)
-    hipLaunchKernelGGL((k_gemm_big<256, 256, OUT_F24, true>), dim3(grid), dim3(512), 0, s, g, ntn);
+  if (ofmt == OUT_X16)
+    hipLaunchKernelGGL((k_gemm_big<256, 256, OUT_X16, true>), dim3(grid), dim3(512), 0, s, g, ntn);
   else
     hipLaunchKernelGGL((k_gemm_big<256, 256, OUT_F32, true>), dim3(grid), dim3(512), 0, s, g, ntn);
   return hipGetLastError();
@@ -1431,6 +1437,8 @@ hipError_t launch_gemm_lo8(const GemmArgs& g, int ofmt, int grid_tiles, hipStrea
 hipError_t launch_gemm_skinny_batch(const GemmArgs* g, const int* ofmt, const int* grid_tiles, int n,
                                     hipStream_t s) {
   if (n < 1 || n > kSkinnyMaxProblems) return hipErrorInvalidValue;
+  for (int i = 0; i < n; ++i)
+    if (!x16_shape_ok(g[i], ofmt[i])) return hipErrorInvalidValue;
   SkinnyBatch b{};
   int wg = 0;
   for (int i = 0; i < n; ++i) {
@@ -1504,6 +1512,7 @@ int skinny_grid(const GemmArgs& g, int64_t items_max) {
 }
 
 hipError_t launch_gemm_skinny(const GemmArgs& g, int ofmt, int grid_tiles, hipStream_t s) {
+  if (!x16_shape_ok(g, ofmt)) return hipErrorInvalidValue;
   return launch_gemm_skinny_batch(&g, &ofmt, &grid_tiles, 1, s);
 }
 

@@ -2,8 +2,8 @@
 // deterministic combine. SwiGLU runs one workgroup per (token, 256-neuron
 // chunk), combine one per token; every thread owns 4 consecutive neurons
 // (SwiGLU) or output columns (combine), so every access is one vector: 16
-// bytes of fp32, or 12 bytes of f24 (the format of the gate|up and down rows
-// written by the bf16 GEMM kernels).
+// bytes of fp32, or an 8-byte word and an exponent byte of x16 (the format
+// of the gate|up and down rows written by the bf16 GEMM kernels).
 //
 // For a token t with selected experts e_j (j ascending), every tree level l
 // has one row per distinct level-l node among the e_j (from the bucketing,
@@ -48,9 +48,9 @@ __device__ inline void token_meta(const TokenArgs& a, int t, TokenMeta& m) {
 
 __device__ __forceinline__ float4 ld4(const float* p) { return *(const float4*)p; }
 // 4 consecutive values at column c of row `row` (row length ld values) of an
-// fp32 or f24 matrix.
-__device__ __forceinline__ float4 ldrow4(const float* base, bool f24, int64_t row, int64_t ld, int c) {
-  if (f24) return f24_unpack(*(const F24x4*)((const uint8_t*)base + (row * ld + c) * 3));
+// fp32 or x16 matrix.
+__device__ __forceinline__ float4 ldrow4(const float* base, bool x16, int64_t row, int64_t ld, int c) {
+  if (x16) return x16_unpack(x16_load_raw(base, row, ld, c));
   return *(const float4*)(base + row * ld + c);
 }
 __device__ __forceinline__ void add4(float4& a, const float4& b) {
@@ -152,11 +152,11 @@ __global__ __launch_bounds__(kTokThr * kSlotGroups) void k_swiglu_reduce(TokenAr
   const bool colok = c < f;
   for (int j = sg; j < k && colok; j += nsg) {
     if (!(m.fl[L][j] & 1)) continue;  // not the first slot of a valid expert
-    const bool f0 = a.f24[0] != 0;
+    const bool f0 = a.x16[0] != 0;
     float4 g = ldrow4(a.gu0, f0, m.row[0][j], ld, c), u = ldrow4(a.gu0, f0, m.row[0][j], ld, f + c);
     for (int l = 1; l <= L; ++l) {
       if (!(m.fl[l][j] & 2) || (a.merged && l < L)) continue;
-      const bool fl = a.f24[l] != 0;
+      const bool fl = a.x16[l] != 0;
       add4(g, ldrow4(a.dgu[l], fl, m.row[l][j], ld, c));
       add4(u, ldrow4(a.dgu[l], fl, m.row[l][j], ld, f + c));
     }
@@ -184,12 +184,12 @@ __global__ __launch_bounds__(kTokThr * kSlotGroups) void k_swiglu_reduce(TokenAr
 // token is read as one contiguous stretch): wavefront 0 lists the token's rows
 // to sum (first slot of a row that does work) in (level, slot) order with a
 // ballot compaction; then every thread sums its 4 columns over that list, 16
-// row loads in flight at a time, adding in list order. Rows are fp32 or f24
-// per level; s_rows holds each row's first byte and s_f24 its format.
+// row loads in flight at a time, adding in list order. Rows are fp32 or x16
+// per level; s_rows holds each row's first byte and s_x16 its format.
 constexpr int kCombMaxThr = 512;
 __global__ __launch_bounds__(kCombMaxThr) void k_combine(TokenArgs a) {
   __shared__ const uint8_t* s_rows[kMaxLvl * LX_MAX_K];
-  __shared__ uint8_t s_f24[kMaxLvl * LX_MAX_K];
+  __shared__ uint8_t s_x16[kMaxLvl * LX_MAX_K];
   __shared__ int s_n;
   const int t = blockIdx.x;
   const int k = a.k, L = a.L, d = a.d;
@@ -199,7 +199,7 @@ __global__ __launch_bounds__(kCombMaxThr) void k_combine(TokenArgs a) {
     int base = 0;
     for (int q0 = 0; q0 < nq; q0 += 64) {
       const int q = q0 + lane;
-      bool take = false, f24 = false;
+      bool take = false, x16 = false;
       const uint8_t* ptr = nullptr;
       if (q < nq) {
         const int l = q / k, j = q - l * k;
@@ -207,15 +207,15 @@ __global__ __launch_bounds__(kCombMaxThr) void k_combine(TokenArgs a) {
         const int row = a.slot_row[l][sl];  // loaded alongside the flags
         if ((a.slot_flags[l][sl] & 3) == 3 && !(a.merged && l > 0 && l < L)) {
           take = true;
-          f24 = a.f24[l] != 0;
-          ptr = (const uint8_t*)a.y[l] + (int64_t)row * d * (f24 ? 3 : 4);
+          x16 = a.x16[l] != 0;
+          ptr = (const uint8_t*)a.y[l] + (int64_t)row * (x16 ? x16_row_bytes(d) : (int64_t)d * 4);
         }
       }
       const uint64_t bal = __ballot(take);
       if (take) {
         const int at = base + __popcll(bal & ((1ull << lane) - 1));
         s_rows[at] = ptr;
-        s_f24[at] = f24 ? 1 : 0;
+        s_x16[at] = x16 ? 1 : 0;
       }
       base += __popcll(bal);
     }
@@ -230,7 +230,7 @@ __global__ __launch_bounds__(kCombMaxThr) void k_combine(TokenArgs a) {
 #pragma unroll
       for (int i = 0; i < 16; ++i)
         if (b + i < n)
-          v[i] = s_f24[b + i] ? f24_unpack(*(const F24x4*)(s_rows[b + i] + c * 3))
+          v[i] = s_x16[b + i] ? x16_unpack(x16_load_raw(s_rows[b + i], 0, d, c))
                               : *(const float4*)(s_rows[b + i] + c * 4);
 #pragma unroll
       for (int i = 0; i < 16; ++i)
@@ -286,29 +286,29 @@ __device__ __forceinline__ void token_meta_fast(const TokenArgs& a, int t, int (
 
 // Raw row segment (4 values at column c): loaded in one pass, converted in a
 // later one, so every load of a thread is in flight before the first use.
-template <bool F24>
+template <bool X16>
 struct Raw4 {
-  using T = typename std::conditional<F24, F24x4, float4>::type;
+  using T = typename std::conditional<X16, X16x4, float4>::type;
   T v;
 };
-template <bool F24>
-__device__ __forceinline__ Raw4<F24> ldraw(const float* base, int64_t row, int64_t ld, int c) {
-  Raw4<F24> r;
-  if constexpr (F24)
-    r.v = *(const F24x4*)((const uint8_t*)base + (row * ld + c) * 3);
+template <bool X16>
+__device__ __forceinline__ Raw4<X16> ldraw(const float* base, int64_t row, int64_t ld, int c) {
+  Raw4<X16> r;
+  if constexpr (X16)
+    r.v = x16_load_raw(base, row, ld, c);
   else
     r.v = *(const float4*)(base + row * ld + c);
   return r;
 }
-template <bool F24>
-__device__ __forceinline__ float4 cvt(const Raw4<F24>& r) {
-  if constexpr (F24)
-    return f24_unpack(r.v);
+template <bool X16>
+__device__ __forceinline__ float4 cvt(const Raw4<X16>& r) {
+  if constexpr (X16)
+    return x16_unpack(r.v);
   else
     return r.v;
 }
 
-template <int NL, bool F24>
+template <int NL, bool X16>
 __global__ __launch_bounds__(kFastThr) void k_swiglu_fast(TokenArgs a) {
   const int t = blockIdx.x, k = a.k, f = a.f;
   const int c = (blockIdx.y * blockDim.x + threadIdx.x) * 4;
@@ -319,17 +319,17 @@ __global__ __launch_bounds__(kFastThr) void k_swiglu_fast(TokenArgs a) {
   token_meta_fast<NL>(a, t, row, fl, w);
   const bool merged = a.merged != 0;
   // loads of every distinct expert's gate|up rows, then h = w silu(g) u
-  Raw4<F24> gv[kFastK][NL + 1], uv[kFastK][NL + 1];
+  Raw4<X16> gv[kFastK][NL + 1], uv[kFastK][NL + 1];
 #pragma unroll
   for (int j = 0; j < kFastK; ++j) {
     if (!(fl[NL][j] & 1)) continue;
-    gv[j][0] = ldraw<F24>(a.gu0, row[0][j], ld, c);
-    uv[j][0] = ldraw<F24>(a.gu0, row[0][j], ld, f + c);
+    gv[j][0] = ldraw<X16>(a.gu0, row[0][j], ld, c);
+    uv[j][0] = ldraw<X16>(a.gu0, row[0][j], ld, f + c);
 #pragma unroll
     for (int l = 1; l <= NL; ++l) {
       if (!(fl[l][j] & 2) || (merged && l < NL)) continue;
-      gv[j][l] = ldraw<F24>(a.dgu[l], row[l][j], ld, c);
-      uv[j][l] = ldraw<F24>(a.dgu[l], row[l][j], ld, f + c);
+      gv[j][l] = ldraw<X16>(a.dgu[l], row[l][j], ld, c);
+      uv[j][l] = ldraw<X16>(a.dgu[l], row[l][j], ld, f + c);
     }
   }
   float4 h[kFastK];
@@ -337,12 +337,12 @@ __global__ __launch_bounds__(kFastThr) void k_swiglu_fast(TokenArgs a) {
   for (int j = 0; j < kFastK; ++j) {
     h[j] = make_float4(0.f, 0.f, 0.f, 0.f);
     if (!(fl[NL][j] & 1)) continue;
-    float4 g = cvt<F24>(gv[j][0]), u = cvt<F24>(uv[j][0]);
+    float4 g = cvt<X16>(gv[j][0]), u = cvt<X16>(uv[j][0]);
 #pragma unroll
     for (int l = 1; l <= NL; ++l) {
       if (!(fl[l][j] & 2) || (merged && l < NL)) continue;
-      add4(g, cvt<F24>(gv[j][l]));
-      add4(u, cvt<F24>(uv[j][l]));
+      add4(g, cvt<X16>(gv[j][l]));
+      add4(u, cvt<X16>(uv[j][l]));
     }
     h[j] = make_float4(w[j] * silu_mul(g.x, u.x), w[j] * silu_mul(g.y, u.y), w[j] * silu_mul(g.z, u.z),
                        w[j] * silu_mul(g.w, u.w));
@@ -366,7 +366,7 @@ __global__ __launch_bounds__(kFastThr) void k_swiglu_fast(TokenArgs a) {
     }
 }
 
-template <int NL, bool F24>
+template <int NL, bool X16>
 __global__ __launch_bounds__(kFastThr) void k_combine_fast(TokenArgs a) {
   const int t = blockIdx.x, k = a.k, d = a.d;
   const int c = (blockIdx.y * blockDim.x + threadIdx.x) * 4;
@@ -376,18 +376,18 @@ __global__ __launch_bounds__(kFastThr) void k_combine_fast(TokenArgs a) {
   token_meta_fast<NL>(a, t, row, fl, w);
   // merged trees: the intermediate levels' terms are in the leaf rows
   const bool merged = a.merged != 0;
-  Raw4<F24> v[NL + 1][kFastK];
+  Raw4<X16> v[NL + 1][kFastK];
 #pragma unroll
   for (int l = 0; l <= NL; ++l)
 #pragma unroll
     for (int j = 0; j < kFastK; ++j)
-      if ((fl[l][j] & 3) == 3 && !(merged && l > 0 && l < NL)) v[l][j] = ldraw<F24>(a.y[l], row[l][j], d, c);
+      if ((fl[l][j] & 3) == 3 && !(merged && l > 0 && l < NL)) v[l][j] = ldraw<X16>(a.y[l], row[l][j], d, c);
   float4 acc = make_float4(0.f, 0.f, 0.f, 0.f);
 #pragma unroll
   for (int l = 0; l <= NL; ++l)
 #pragma unroll
     for (int j = 0; j < kFastK; ++j)
-      if ((fl[l][j] & 3) == 3 && !(merged && l > 0 && l < NL)) add4(acc, cvt<F24>(v[l][j]));
+      if ((fl[l][j] & 3) == 3 && !(merged && l > 0 && l < NL)) add4(acc, cvt<X16>(v[l][j]));
   if (a.out_dtype == LX_F32) {
     *(float4*)((float*)a.out + (int64_t)t * d + c) = acc;
   } else {
@@ -411,11 +411,11 @@ int fast_threads(int cols, int T) {
 
 }  // namespace
 
-// The fast paths need one row format on every level (all f24 or all fp32).
+// The fast paths need one row format on every level (all x16 or all fp32).
 static int uniform_fmt(const TokenArgs& a) {
   for (int l = 1; l <= a.L; ++l)
-    if (a.f24[l] != a.f24[0]) return -1;
-  return a.f24[0] ? 1 : 0;
+    if (a.x16[l] != a.x16[0]) return -1;
+  return a.x16[0] ? 1 : 0;
 }
 
 hipError_t launch_swiglu_reduce(const TokenArgs& a, hipStream_t s) {

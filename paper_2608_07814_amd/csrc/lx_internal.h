@@ -9,34 +9,62 @@
 
 namespace lx {
 
-// ---------------------------------------------------------------- f24 rows
+// ---------------------------------------------------------------- x16 rows
 // Intermediates that only the elementwise kernels read back (gate|up
-// outputs, down outputs) are stored as 24-bit floats: sign, exponent and the
-// top 15 mantissa bits of the fp32 value, rounded to nearest even (relative
-// error at most 2^-16, the precision of a bf16 hi + lo pair, in 3 bytes
-// instead of 4). Four consecutive values occupy 12 bytes; a row of n values
-// (n a multiple of 4) is 3n bytes.
-struct __attribute__((packed, aligned(4))) F24x4 {
-  uint32_t a, b, c;
+// outputs, down outputs) are stored as groups of 4 consecutive values that
+// share one exponent: the biased exponent byte E of the group's largest
+// magnitude, and each value as a 16-bit signed integer m = round(v * 2^(141
+// - E)), |m| <= 32767, i.e. v = m * 2^(E - 141). The error of a value is at
+// most 2^-15 of the group's largest magnitude. A row of n values (n a
+// multiple of 32) is 9n/4 bytes: the n mantissas (2n bytes), then the n/4
+// exponent bytes; a lane's 4 values are one 8-byte word and one byte.
+struct X16x4 {
+  uint2 m;    // mantissas 0, 1 | 2, 3 (low half first)
+  uint32_t e; // exponent byte (low 8 bits)
 };
 
-__device__ __forceinline__ uint32_t f24_round(float x) {
-  const uint32_t u = __float_as_uint(x);
-  return (u + 0x7Fu + ((u >> 8) & 1u)) >> 8;
+__host__ __device__ __forceinline__ int64_t x16_row_bytes(int64_t n) { return n * 9 / 4; }
+
+__device__ __forceinline__ X16x4 x16_pack(float4 v) {
+  const float mx = fmaxf(fmaxf(fabsf(v.x), fabsf(v.y)), fmaxf(fabsf(v.z), fabsf(v.w)));
+  const int eb = (int)((__float_as_uint(mx) >> 23) & 0xFFu);
+  const int sh = 141 - eb;
+  auto q = [&](float x) -> uint32_t {
+    float r = rintf(ldexpf(x, sh));
+    r = fminf(fmaxf(r, -32767.f), 32767.f);
+    return (uint32_t)(int32_t)r & 0xFFFFu;
+  };
+  X16x4 w;
+  w.m.x = q(v.x) | (q(v.y) << 16);
+  w.m.y = q(v.z) | (q(v.w) << 16);
+  w.e = (uint32_t)eb;
+  return w;
 }
 
-__device__ __forceinline__ F24x4 f24_pack(float4 v) {
-  const uint32_t p = f24_round(v.x), q = f24_round(v.y), r = f24_round(v.z), s = f24_round(v.w);
-  return F24x4{p | (q << 24), (q >> 8) | (r << 16), (r >> 16) | (s << 8)};
+__device__ __forceinline__ float4 x16_unpack(X16x4 w) {
+  const int sh = (int)(w.e & 0xFFu) - 141;
+  auto d = [&](uint32_t h) { return ldexpf((float)(int32_t)(int16_t)(uint16_t)h, sh); };
+  return make_float4(d(w.m.x & 0xFFFFu), d(w.m.x >> 16), d(w.m.y & 0xFFFFu), d(w.m.y >> 16));
 }
 
-__device__ __forceinline__ float4 f24_unpack(F24x4 w) {
-  return make_float4(__uint_as_float(w.a << 8), __uint_as_float(((w.a >> 24) | (w.b << 8)) << 8),
-                     __uint_as_float(((w.b >> 16) | (w.c << 16)) << 8), __uint_as_float(w.c & 0xFFFFFF00u));
+// Values [c, c + 4) of row `row` (n values per row) at base.
+__device__ __forceinline__ void x16_store(void* base, int64_t row, int64_t n, int64_t c, float4 v) {
+  uint8_t* const rp = (uint8_t*)base + row * x16_row_bytes(n);
+  const X16x4 w = x16_pack(v);
+  *(uint2*)(rp + 2 * c) = w.m;
+  rp[2 * n + (c >> 2)] = (uint8_t)w.e;
 }
 
-// Output format of a GEMM: fp32, a bf16 (hi, lo) pair, or f24.
-enum OutFmt { OUT_F32 = 0, OUT_HILO = 1, OUT_F24 = 2 };
+__device__ __forceinline__ X16x4 x16_load_raw(const void* base, int64_t row, int64_t n, int64_t c) {
+  const uint8_t* const rp = (const uint8_t*)base + row * x16_row_bytes(n);
+  X16x4 w;
+  w.m = *(const uint2*)(rp + 2 * c);
+  w.e = rp[2 * n + (c >> 2)];
+  return w;
+}
+
+// Output format of a GEMM: fp32, a bf16 (hi, lo) pair, or x16.
+enum OutFmt { OUT_F32 = 0, OUT_HILO = 1, OUT_X16 = 2 };
 // Format of the weighted activation sums (the down GEMMs' input); HBAR_F16:
 // fp16 rows of f values scaled by 2^exp (exp per row, in a separate array,
 // chosen so that the row's largest magnitude lands in [2^14, 2^15)).
@@ -246,8 +274,8 @@ hipError_t launch_gemm(const GemmArgs& g, lx_dtype dt, AMode am, int grid_x, hip
 // Large-tile kernel (BM x BN tiles, direct HBM->LDS loads). Applicable when A
 // is bf16, K and Kb are multiples of 64, the parts either share A columns or
 // the part boundary is a multiple of BN, and A's element count fits in 31
-// bits. fp32 and f24 output is written at columns [0, ncols[0] + ncols[1]) of
-// C (the parts adjacent; ldc in values, an f24 row is 3 ldc bytes); bf16
+// bits. fp32 and x16 output is written at columns [0, ncols[0] + ncols[1]) of
+// C (the parts adjacent; ldc in values, an x16 row is 9 ldc / 4 bytes); bf16
 // (hi, lo) output writes part p's hi values at columns base_p + c and lo
 // values at base_p + ncols[p] + c, base_0 = 0, base_1 = 2 ncols[0] (ldc in
 // bf16 elements).
@@ -272,7 +300,7 @@ hipError_t launch_quantize_f8(const void* w, int64_t n_rows, int cols, uint8_t* 
 hipError_t launch_gemm_big(const GemmArgs& g, int bm, int bn, int ofmt, int grid_tiles,
                            hipStream_t s);
 
-// Segmented large-tile GEMM (256 x 256 tiles, f24 output): the correction
+// Segmented large-tile GEMM (256 x 256 tiles, x16 output): the correction
 // products of several tree levels that land on the same output rows, as one
 // GEMM whose K is the concatenation of the levels' (hi | lo) operands:
 //   C[row] = sum over segments s of A_s[map_s(row)] * W_s[widx_s]^T
@@ -344,7 +372,7 @@ struct TokenArgs {
   const float* slot_wsum;
   const float* gu0;                    // [rows0][2f] anchor gate|up
   const float* dgu[kMaxLvl];           // [rows_l][2f] correction gate|up (l >= 1)
-  int32_t f24[kMaxLvl];                // level l's gate|up and down rows are f24
+  int32_t x16[kMaxLvl];                // level l's gate|up and down rows are x16
                                        // (else fp32)
   float* hbar[kMaxLvl];                // weighted activation sums, rows of 4f bytes:
                                        // HBAR_F32 fp32 [f]; HBAR_HILO bf16 hi [f] then
