@@ -36,6 +36,7 @@
 
 #include <algorithm>
 #include <mutex>
+#include <type_traits>
 
 namespace lx {
 namespace {
@@ -524,48 +525,61 @@ void k_gemm_big(GemmArgs p, int ntn) {
       const int c4 = (lane % LPR) * 4;
       const int col = n0 + wn * WN + c4;
       const int bexp = F16 ? p.b_exp[widx] : 0;
+      X16Rows xr(p.C, p.ldc, te.row0 + wm * WM + lane / LPR, RPP, col);
+      // full tiles store without per-row checks (a separate, branch-free copy)
+      auto emit = [&](auto check) {
 #pragma unroll
-      for (int mi = 0; mi < MI; ++mi) {
+        for (int mi = 0; mi < MI; ++mi) {
 #pragma unroll
-        for (int ni = 0; ni < NI; ++ni)
+          for (int ni = 0; ni < NI; ++ni)
 #pragma unroll
-          for (int i = 0; i < 16; ++i)
-            ep[(8 * (i >> 2) + 4 * (lane >> 5) + (i & 3)) * PITCH + ni * 32 + (lane & 31)] = acc[mi][ni][i];
+            for (int i = 0; i < 16; ++i)
+              ep[(8 * (i >> 2) + 4 * (lane >> 5) + (i & 3)) * PITCH + ni * 32 + (lane & 31)] = acc[mi][ni][i];
 #pragma unroll
-        for (int ps = 0; ps < 32 / RPP; ++ps) {
-          const int rr = ps * RPP + lane / LPR;
-          float4 v = *(const float4*)&ep[rr * PITCH + c4];
-          const int r = wm * WM + mi * 32 + rr;
-          if (r >= te.nrows || col >= ncol) continue;
-          if constexpr (F16) {
-            const int e = -(p.a_row_exp[te.row0 + r] + bexp);
-            v = make_float4(ldexpf(v.x, e), ldexpf(v.y, e), ldexpf(v.z, e), ldexpf(v.w, e));
-          }
-          if (OUT == OUT_HILO) {
-            // part p, local column c -> hi at base_p + c, lo at base_p + ncols[p] + c
-            const int pp = col < p.ncols[0] ? 0 : 1;
-            const int c = pp ? col - p.ncols[0] : col;
-            const int hi_col = (pp ? 2 * p.ncols[0] : 0) + c;
-            const int lo_col = hi_col + p.ncols[pp];
-            bf16x4 h, l;
-            h[0] = (__bf16)v.x;
-            h[1] = (__bf16)v.y;
-            h[2] = (__bf16)v.z;
-            h[3] = (__bf16)v.w;
-            l[0] = (__bf16)(v.x - (float)h[0]);
-            l[1] = (__bf16)(v.y - (float)h[1]);
-            l[2] = (__bf16)(v.z - (float)h[2]);
-            l[3] = (__bf16)(v.w - (float)h[3]);
-            __bf16* const rowp = (__bf16*)p.C + (int64_t)(te.row0 + r) * p.ldc;
-            *(bf16x4*)(rowp + hi_col) = h;
-            *(bf16x4*)(rowp + lo_col) = l;
-          } else if (OUT == OUT_X16) {
-            x16_store(p.C, te.row0 + r, p.ldc, col, v);
-          } else {
-            *(float4*)(p.C + (int64_t)(te.row0 + r) * p.ldc + col) = v;
+          for (int ps = 0; ps < 32 / RPP; ++ps) {
+            const int rr = ps * RPP + lane / LPR;
+            float4 v = *(const float4*)&ep[rr * PITCH + c4];
+            const int r = wm * WM + mi * 32 + rr;
+            const bool ok = !decltype(check)::value || (r < te.nrows && col < ncol);
+            if constexpr (F16) {
+              if (ok) {
+                const int e = -(p.a_row_exp[te.row0 + r] + bexp);
+                v = make_float4(ldexpf(v.x, e), ldexpf(v.y, e), ldexpf(v.z, e), ldexpf(v.w, e));
+              }
+            }
+            if constexpr (OUT == OUT_X16) {
+              if (ok) xr.store(v);
+              xr.next();
+            } else if constexpr (OUT == OUT_HILO) {
+              if (!ok) continue;
+              // part p, local column c -> hi at base_p + c, lo at base_p + ncols[p] + c
+              const int pp = col < p.ncols[0] ? 0 : 1;
+              const int c = pp ? col - p.ncols[0] : col;
+              const int hi_col = (pp ? 2 * p.ncols[0] : 0) + c;
+              const int lo_col = hi_col + p.ncols[pp];
+              bf16x4 h, l;
+              h[0] = (__bf16)v.x;
+              h[1] = (__bf16)v.y;
+              h[2] = (__bf16)v.z;
+              h[3] = (__bf16)v.w;
+              l[0] = (__bf16)(v.x - (float)h[0]);
+              l[1] = (__bf16)(v.y - (float)h[1]);
+              l[2] = (__bf16)(v.z - (float)h[2]);
+              l[3] = (__bf16)(v.w - (float)h[3]);
+              __bf16* const rowp = (__bf16*)p.C + (int64_t)(te.row0 + r) * p.ldc;
+              *(bf16x4*)(rowp + hi_col) = h;
+              *(bf16x4*)(rowp + lo_col) = l;
+            } else {
+              if (!ok) continue;
+              *(float4*)(p.C + (int64_t)(te.row0 + r) * p.ldc + col) = v;
+            }
           }
         }
-      }
+      };
+      if (te.nrows >= BM && n0 + BN <= ncol)
+        emit(std::false_type{});
+      else
+        emit(std::true_type{});
     }
     bar();  // the next item's loads overwrite the epilogue's LDS
   }
@@ -775,22 +789,29 @@ void k_gemm_seg(GemmArgs p, SegArgs sg, int ntn) {
       float* const ep = (float*)smem + wave * (32 * PITCH);
       const int c4 = (lane % LPR) * 4;
       const int col = n0 + wn * WN + c4;
+      X16Rows xr(p.C, p.ldc, te.row0 + wm * WM + lane / LPR, RPP, col);
+      // full tiles store without per-row checks (a separate, branch-free copy)
+      auto emit = [&](auto check) {
 #pragma unroll
-      for (int mi = 0; mi < MI; ++mi) {
+        for (int mi = 0; mi < MI; ++mi) {
 #pragma unroll
-        for (int ni = 0; ni < NI; ++ni)
+          for (int ni = 0; ni < NI; ++ni)
 #pragma unroll
-          for (int i = 0; i < 16; ++i)
-            ep[(8 * (i >> 2) + 4 * (lane >> 5) + (i & 3)) * PITCH + ni * 32 + (lane & 31)] = acc[mi][ni][i];
+            for (int i = 0; i < 16; ++i)
+              ep[(8 * (i >> 2) + 4 * (lane >> 5) + (i & 3)) * PITCH + ni * 32 + (lane & 31)] = acc[mi][ni][i];
 #pragma unroll
-        for (int ps = 0; ps < 32 / RPP; ++ps) {
-          const int rr = ps * RPP + lane / LPR;
-          const float4 v = *(const float4*)&ep[rr * PITCH + c4];
-          const int r = wm * WM + mi * 32 + rr;
-          if (r >= te.nrows || col >= ncol) continue;
-          x16_store(p.C, te.row0 + r, p.ldc, col, v);
+          for (int ps = 0; ps < 32 / RPP; ++ps) {
+            const int rr = ps * RPP + lane / LPR;
+            const float4 v = *(const float4*)&ep[rr * PITCH + c4];
+            if (!decltype(check)::value || (wm * WM + mi * 32 + rr < te.nrows && col < ncol)) xr.store(v);
+            xr.next();
+          }
         }
-      }
+      };
+      if (te.nrows >= BM && n0 + BN <= ncol)
+        emit(std::false_type{});
+      else
+        emit(std::true_type{});
     }
     bar();  // the next item's loads overwrite the epilogue's LDS
   }

@@ -13,11 +13,14 @@ namespace lx {
 // Intermediates that only the elementwise kernels read back (gate|up
 // outputs, down outputs) are stored as groups of 4 consecutive values that
 // share one exponent: the biased exponent byte E of the group's largest
-// magnitude, and each value as a 16-bit signed integer m = round(v * 2^(141
-// - E)), |m| <= 32767, i.e. v = m * 2^(E - 141). The error of a value is at
-// most 2^-15 of the group's largest magnitude. A row of n values (n a
-// multiple of 32) is 9n/4 bytes: the n mantissas (2n bytes), then the n/4
-// exponent bytes; a lane's 4 values are one 8-byte word and one byte.
+// magnitude (mx in [2^(E-127), 2^(E-126))), and each value v as the 16-bit
+// signed normalized integer m = round(32767 * v * 2^(126 - E)) (|v| 2^(126-E)
+// < 1, so |m| <= 32767), i.e. v = m / 32767 * 2^(E - 126). The error of a
+// value is at most 2^-15 of the group's largest magnitude. One conversion
+// instruction (v_cvt_pknorm_i16_f32: clamp to [-1, 1], scale by 32767, round
+// to nearest) encodes two values. A row of n values (n a multiple of 32) is
+// 9n/4 bytes: the n mantissas (2n bytes), then the n/4 exponent bytes; a
+// lane's 4 values are one 8-byte word and one byte.
 struct X16x4 {
   uint2 m;    // mantissas 0, 1 | 2, 3 (low half first)
   uint32_t e; // exponent byte (low 8 bits)
@@ -25,25 +28,25 @@ struct X16x4 {
 
 __host__ __device__ __forceinline__ int64_t x16_row_bytes(int64_t n) { return n * 9 / 4; }
 
+typedef short x16_short2 __attribute__((ext_vector_type(2)));
+
 __device__ __forceinline__ X16x4 x16_pack(float4 v) {
   const float mx = fmaxf(fmaxf(fabsf(v.x), fabsf(v.y)), fmaxf(fabsf(v.z), fabsf(v.w)));
   const int eb = (int)((__float_as_uint(mx) >> 23) & 0xFFu);
-  const int sh = 141 - eb;
-  auto q = [&](float x) -> uint32_t {
-    float r = rintf(ldexpf(x, sh));
-    r = fminf(fmaxf(r, -32767.f), 32767.f);
-    return (uint32_t)(int32_t)r & 0xFFFFu;
-  };
+  const int sh = 126 - eb;
+  const x16_short2 a = __builtin_amdgcn_cvt_pknorm_i16(ldexpf(v.x, sh), ldexpf(v.y, sh));
+  const x16_short2 b = __builtin_amdgcn_cvt_pknorm_i16(ldexpf(v.z, sh), ldexpf(v.w, sh));
   X16x4 w;
-  w.m.x = q(v.x) | (q(v.y) << 16);
-  w.m.y = q(v.z) | (q(v.w) << 16);
+  w.m.x = __builtin_bit_cast(uint32_t, a);
+  w.m.y = __builtin_bit_cast(uint32_t, b);
   w.e = (uint32_t)eb;
   return w;
 }
 
 __device__ __forceinline__ float4 x16_unpack(X16x4 w) {
-  const int sh = (int)(w.e & 0xFFu) - 141;
-  auto d = [&](uint32_t h) { return ldexpf((float)(int32_t)(int16_t)(uint16_t)h, sh); };
+  const int sh = (int)(w.e & 0xFFu) - 126;
+  constexpr float inv = 1.0f / 32767.0f;
+  auto d = [&](uint32_t h) { return ldexpf((float)(int32_t)(int16_t)(uint16_t)h * inv, sh); };
   return make_float4(d(w.m.x & 0xFFFFu), d(w.m.x >> 16), d(w.m.y & 0xFFFFu), d(w.m.y >> 16));
 }
 
@@ -54,6 +57,28 @@ __device__ __forceinline__ void x16_store(void* base, int64_t row, int64_t n, in
   *(uint2*)(rp + 2 * c) = w.m;
   rp[2 * n + (c >> 2)] = (uint8_t)w.e;
 }
+
+// A lane's x16 stores down a column group: rows row, row + step, row + 2 step,
+// ... of a row-major x16 matrix with n values per row, columns [c, c + 4);
+// the row address advances by a constant stride instead of being multiplied
+// out per row.
+struct X16Rows {
+  uint8_t* m;        // mantissa word of the current row
+  int64_t stride;    // bytes between consecutive rows of this lane
+  int32_t eoff;      // exponent byte, relative to m
+  __device__ __forceinline__ X16Rows(void* base, int64_t n, int64_t row, int step, int64_t c) {
+    const int64_t rb = x16_row_bytes(n);
+    m = (uint8_t*)base + row * rb + 2 * c;
+    stride = rb * step;
+    eoff = (int32_t)(2 * n + (c >> 2) - 2 * c);
+  }
+  __device__ __forceinline__ void store(float4 v) const {
+    const X16x4 w = x16_pack(v);
+    *(uint2*)m = w.m;
+    m[eoff] = (uint8_t)w.e;
+  }
+  __device__ __forceinline__ void next() { m += stride; }
+};
 
 __device__ __forceinline__ X16x4 x16_load_raw(const void* base, int64_t row, int64_t n, int64_t c) {
   const uint8_t* const rp = (const uint8_t*)base + row * x16_row_bytes(n);
