@@ -170,13 +170,14 @@ def load_traffic(kernel, workload):
 def clone_layer(dl):
     """Independent device copy of a DeviceLayer's weights (same routing structure)."""
     import dataclasses
-    names = ("a_gate", "b_gate", "a_up", "b_up", "a_down", "b_down")
-    levels = [dataclasses.replace(lv, **{n: getattr(lv, n).clone() for n in names}) for lv in dl.levels]
-    f8 = {}
-    if dl.anchor_down_f8 is not None:
-        f8 = dict(anchor_down_f8=dl.anchor_down_f8.clone(), anchor_down_f8_scale=dl.anchor_down_f8_scale.clone())
+    from paper_2608_07814_amd import lorex as lx
+    names = ("a_gate", "b_gate", "a_up", "b_up", "a_down", "b_down") + lx.FACTOR_F16
+    levels = [dataclasses.replace(lv, **{n: getattr(lv, n).clone() for n in names if getattr(lv, n) is not None})
+              for lv in dl.levels]
+    copies = {n: getattr(dl, n).clone() for n in ("anchor_down_f8", "anchor_down_f8_scale", "anchor_down_f16",
+                                                   "anchor_down_f16_exp") if getattr(dl, n) is not None}
     return dataclasses.replace(dl, anchor_gate=dl.anchor_gate.clone(), anchor_up=dl.anchor_up.clone(),
-                               anchor_down=dl.anchor_down.clone(), levels=levels, **f8)
+                               anchor_down=dl.anchor_down.clone(), levels=levels, **copies)
 
 
 def rotating(calls):

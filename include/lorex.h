@@ -110,6 +110,20 @@ typedef struct lx_level {
   const void* b_up;          /* [n_factors][rank][d] */
   const void* a_down;        /* [n_factors][d][rank] */
   const void* b_down;        /* [n_factors][rank][f] */
+  /* Optional (NULL = not used, all four or none): fp16 copies of the factors
+   * made by lx_convert_f16 (one power-of-two scale per factor matrix). With
+   * them, batches on the fp16 anchor path (see lx_convert_f16) run every
+   * correction product of the level as one fp16 product: the rank-`rank`
+   * intermediates and the level's activation sums are fp16 with power-of-two
+   * scales instead of bf16 (hi, lo) pairs. */
+  const void* a_gate_f16;            /* [n_factors][f][rank] */
+  const int32_t* a_gate_f16_exp;     /* [n_factors] */
+  const void* a_up_f16;              /* [n_factors][f][rank] */
+  const int32_t* a_up_f16_exp;       /* [n_factors] */
+  const void* a_down_f16;            /* [n_factors][d][rank] */
+  const int32_t* a_down_f16_exp;     /* [n_factors] */
+  const void* b_down_f16;            /* [n_factors][rank][f] */
+  const int32_t* b_down_f16_exp;     /* [n_factors] */
 } lx_level;
 
 /* A BTExperts tree (Sec. 5): dense anchors, then n_levels correction levels;
@@ -158,6 +172,16 @@ typedef struct lx_flat_layer {
   const uint32_t* dom_down_f8_scale;   /* its scale words, [C][d][f / 64] */
   const void* dom_down_f16;            /* optional fp16 copy of dom_down (lx_convert_f16) */
   const int32_t* dom_down_f16_exp;     /* its scale exponents, [C] */
+  /* optional fp16 copies of the factors (lx_convert_f16; all four or none),
+   * as the fp16 factor copies of lx_level */
+  const void* a_gate_f16;
+  const int32_t* a_gate_f16_exp;       /* [M] */
+  const void* a_up_f16;
+  const int32_t* a_up_f16_exp;
+  const void* a_down_f16;
+  const int32_t* a_down_f16_exp;
+  const void* b_down_f16;
+  const int32_t* b_down_f16_exp;
 } lx_flat_layer;
 
 /* An uncompressed MoE layer (every expert stored in full): the comparator the
@@ -255,7 +279,8 @@ lx_status lx_dense_moe_forward(const lx_dense_layer* layer, int32_t T, int32_t k
 lx_status lx_quantize_f8(const void* w, int32_t n, int32_t rows, int32_t cols, void* w_f8,
                          uint32_t* scales, void* stream);
 
-/* fp16 copy of bf16 weights, for the anchor down projection.
+/* fp16 copy of bf16 weights, for the anchor down projection and the
+ * correction products.
  *
  * The anchor down projection multiplies the anchor activation sums hbar
  * (Sec. 5.1: the routing-weighted sum of the SwiGLU activations of a token's
@@ -263,11 +288,16 @@ lx_status lx_quantize_f8(const void* w, int32_t n, int32_t rows, int32_t cols, v
  * hbar costs about 1e-2 x RMS of the output (the acceptance bar), hence the
  * (hi, lo) pair; fp16 keeps 3 more bits (about 1.3e-3 x RMS) at the bf16 MFMA
  * rate in a single product. With this copy in the layer, the forward stores
- * hbar as fp16 with one power-of-two scale per row (its largest magnitude in
- * [2^14, 2^15)) and multiplies it with the copy, undoing both scales exactly
- * in the output. Used for batches of at least 512 tokens with f a multiple
- * of 256 and at most 1024, k <= 8 and at most two correction levels, on the
- * large-tile kernel; other batches take the fp8 copy (if any) or the pair.
+ * hbar as fp16 with one power-of-two scale per token (the largest magnitude
+ * over the token's fp16 sums in [2^14, 2^15)) and multiplies it with the
+ * copy, undoing both scales exactly in the output. Used for batches of at
+ * least 512 tokens with f a multiple of 256 and at most 1024, k <= 8 and at
+ * most two correction levels, on the large-tile kernel; other batches take
+ * the fp8 copy (if any) or the pair. With fp16 copies of a level's factors
+ * too (lx_level), that level's correction products run the same way: its
+ * activation sums as above, its rank-r intermediates fp16 with one
+ * power-of-two scale per 256-row tile (rank a multiple of 64, at most 128;
+ * levels with at most 64 rows per node keep the pair).
  *
  * w [n][rows][cols] bf16 -> w_f16 [n][rows][cols] fp16 equal to w * 2^e_i
  * for matrix i, rounded to nearest even, with exps[i] = e_i chosen so that

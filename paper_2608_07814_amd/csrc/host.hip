@@ -101,6 +101,9 @@ struct LevelPlan {
   size_t hist, offsets, row_token, slot_row, slot_flags, fac;
   size_t tiles[kNumTab], n_tiles[kNumTab];
   size_t gu, z, hbar, v, y;
+  // fp16 correction products: row exponents of z, v and the level's
+  // activation sums (stored value = true value * 2^exp)
+  size_t z_exp = 0, v_exp = 0, hbar_exp = 0;
   size_t part, cnt;   // split-K partial tiles and counters (skinny levels)
   int64_t n_cnt;
 };
@@ -130,11 +133,16 @@ struct Plan {
   // copy of the anchor down weights and the large-tile kernel)
   bool lo8 = false;
   // f16: the anchor activation sums are fp16 rows with a power-of-two scale
-  // per row and the anchor down GEMM runs once, in fp16, against the
+  // per token and the anchor down GEMM runs once, in fp16, against the
   // layer's fp16 copy (needs the large-tile kernel and whole rows per
   // SwiGLU workgroup); preferred over lo8
   bool f16 = false;
   size_t hbar_exp = 0;
+  // cf16: on top of f16, every correction product runs once in fp16 against
+  // the levels' fp16 factor copies: z = B x and v = B_down hbar are fp16 with
+  // one power-of-two scale per 256-row tile (a tile spans whole rows: 2 rank
+  // <= 256), the correction levels' activation sums fp16 rows as the anchor's
+  bool cf16 = false;
 };
 
 int level_nodes(const lx_tree_layer& t, int l) { return l == 0 ? t.n_anchors : t.levels[l - 1].n_nodes; }
@@ -189,6 +197,13 @@ Plan make_plan(const lx_tree_layer& t, int T, int k) {
       p.f16 = t.anchor_down_f16 && t.anchor_down_f16_exp && p.fast[0] && !p.skinny[0] && all_fast && k <= 8 &&
               p.L <= 2 && T >= 512 && p.f % 256 == 0 && p.f <= 1024;
       if (p.f16) p.lo8 = false;
+      p.cf16 = p.f16;
+      for (int l = 1; l <= p.L && p.cf16; ++l) {
+        const lx_level& v = t.levels[l - 1];
+        if (v.n_factors == 0) continue;
+        p.cf16 = v.a_gate_f16 && v.a_up_f16 && v.a_down_f16 && v.b_down_f16 && v.rank % 64 == 0 &&
+                 2 * v.rank <= 256 && !p.skinny[l];
+      }
     }
     // (batches of at most 64 tokens always run their fast levels on the
     // skinny kernel, so merged trees take the four-pass bucketing)
@@ -243,6 +258,11 @@ Plan make_plan(const lx_tree_layer& t, int T, int k) {
     const size_t Rv = inter ? (size_t)T * std::min(k, t.E) : R;
     q.v = take(l > 0 && work ? Rv * q.rank * 4 : 0);
     q.y = take((work && !inter) || leafm ? R * p.d * 4 : 0);
+    if (p.cf16 && l > 0) {
+      q.z_exp = take(work ? R * 4 : 0);
+      q.v_exp = take(work ? Rv * 4 : 0);
+      q.hbar_exp = take((work && !inter) || leafm ? R * 4 : 0);
+    }
     // one counter per work item of the level's widest skinny product
     const int widest = std::max(std::max(2 * p.f, p.d), 2 * q.rank);
     q.n_cnt = p.skinny[l] && work && T > 0 ? q.tiles_max[kTabSkinny] * ((widest + kSkinnyBN - 1) / kSkinnyBN) : 0;
@@ -298,6 +318,17 @@ lx_status check_layer(const lx_tree_layer* t) {
       for (const void* q : fw)
         if (!q || !aligned(q, 16)) return fail(LX_ERR_INVALID_ARGUMENT, "factor arrays null or not 16-byte aligned");
     }
+    const void* cw[4] = {v.a_gate_f16, v.a_up_f16, v.a_down_f16, v.b_down_f16};
+    const int32_t* ce[4] = {v.a_gate_f16_exp, v.a_up_f16_exp, v.a_down_f16_exp, v.b_down_f16_exp};
+    int nset = 0;
+    for (int i = 0; i < 4; ++i) {
+      nset += (cw[i] != nullptr) + (ce[i] != nullptr);
+      if ((cw[i] && !aligned(cw[i], 16)) || (ce[i] && !aligned(ce[i], 4)))
+        return fail(LX_ERR_INVALID_ARGUMENT, "fp16 factor copies not 16-byte aligned or exponents not 4-byte aligned");
+    }
+    if (nset != 0 && nset != 8)
+      return fail(LX_ERR_INVALID_ARGUMENT, "fp16 factor copies and their exponents: all eight or none");
+    if (nset && t->dtype != LX_BF16) return fail(LX_ERR_UNSUPPORTED, "fp16 factor copies need a bf16 layer");
   }
   return LX_OK;
 }
@@ -338,6 +369,14 @@ lx_tree_layer flat_to_tree(const lx_flat_layer& F) {
   v.b_up = F.b_up;
   v.a_down = F.a_down;
   v.b_down = F.b_down;
+  v.a_gate_f16 = F.a_gate_f16;
+  v.a_gate_f16_exp = F.a_gate_f16_exp;
+  v.a_up_f16 = F.a_up_f16;
+  v.a_up_f16_exp = F.a_up_f16_exp;
+  v.a_down_f16 = F.a_down_f16;
+  v.a_down_f16_exp = F.a_down_f16_exp;
+  v.b_down_f16 = F.b_down_f16;
+  v.b_down_f16_exp = F.b_down_f16_exp;
   return t;
 }
 
@@ -623,6 +662,17 @@ lx_status run(const lx_tree_layer& t, int T, int k, const void* x, const int32_t
     LX_LAUNCH(name, launch_gemm_big(g, bm, bn, ofmt, (int)q.tiles_max[tab], lstream));
     return LX_OK;
   };
+  // fp16 operands (A rows and weight matrices with power-of-two scales) on
+  // the large-tile kernel, level l's 256-row tiles
+  auto f16big = [&](const char* name, GemmArgs g, int l, int bn, int ofmt, int64_t a_rows_total) -> lx_status {
+    if (!g.B[1]) g.B[1] = g.B[0];
+    if (!gemm_f16_ok(g, bn, ofmt, a_rows_total))
+      return fail(LX_ERR_UNSUPPORTED, std::string(name) + ": shape not supported by the fp16 GEMM");
+    g.tiles = ba.lv[l].tiles[kTabBig];
+    g.n_tiles = ba.lv[l].n_tiles[kTabBig];
+    LX_LAUNCH(name, launch_gemm_f16(g, bn, ofmt, (int)P.lv[l].tiles_max[kTabBig], lstream));
+    return LX_OK;
+  };
   auto small = [&](const char* name, GemmArgs g, int l, AMode am) -> lx_status {
     g.tiles = ba.lv[l].tiles[kTabSmall];
     g.n_tiles = ba.lv[l].n_tiles[kTabSmall];
@@ -675,7 +725,11 @@ lx_status run(const lx_tree_layer& t, int T, int k, const void* x, const int32_t
     g.ncols[0] = g.ncols[1] = r;
     g.K = d;
     g.C = (float*)(W + q.z);
-    if (fast[l]) {
+    if (fast[l] && P.cf16) {
+      g.ldc = 2 * (int64_t)r;  // [gate | up], fp16, one scale per tile
+      g.c_row_exp = (int32_t*)(W + q.z_exp);
+      LX_TRY(big(kLowIn[l], g, l, kBigBM, 2 * r <= 128 ? 128 : 256, OUT_F16T, T));
+    } else if (fast[l]) {
       g.ldc = 4 * (int64_t)r;  // [gate hi | gate lo | up hi | up lo], bf16
       LX_TRY(big(kLowIn[l], g, l, kBigBM, 2 * r <= 128 ? 128 : 256, OUT_HILO, T));
     } else {
@@ -712,6 +766,7 @@ lx_status run(const lx_tree_layer& t, int T, int k, const void* x, const int32_t
   auto seg_args = [&](bool down) {
     SegArgs sa{};
     sa.anc = pa.anc;
+    sa.f16 = P.cf16 ? 1 : 0;
     for (int l = 1; l <= L; ++l) {
       const lx_level& v = t.levels[l - 1];
       if (v.n_factors == 0) continue;
@@ -723,21 +778,26 @@ lx_status run(const lx_tree_layer& t, int T, int k, const void* x, const int32_t
       sd.fac = l == L ? nullptr : (const int32_t*)(W + q.fac);
       if (!down) {
         sd.A = W + q.z;
-        sd.lda = 4 * (int64_t)r;  // [gate hi | gate lo | up hi | up lo]
-        sd.akoff1 = 2 * r;
+        sd.lda = (P.cf16 ? 2 : 4) * (int64_t)r;  // [gate | up] fp16 or [gate hi | gate lo | up hi | up lo]
+        sd.akoff1 = (P.cf16 ? 1 : 2) * r;
         sd.map = l == L ? nullptr : (const int32_t*)(W + P.leaf_row[l]);
         sd.zero_row = 0;
-        sd.B[0] = v.a_gate;
-        sd.B[1] = v.a_up;
+        sd.B[0] = P.cf16 ? v.a_gate_f16 : v.a_gate;
+        sd.B[1] = P.cf16 ? v.a_up_f16 : v.a_up;
         sd.b_stride[0] = sd.b_stride[1] = (int64_t)f * r;
+        sd.a_exp = P.cf16 ? (const int32_t*)(W + q.z_exp) : nullptr;
+        sd.b_exp[0] = v.a_gate_f16_exp;
+        sd.b_exp[1] = v.a_up_f16_exp;
       } else {
         sd.A = W + q.v;  // one row per leaf row at every level
-        sd.lda = 2 * (int64_t)r;  // [hi | lo]
+        sd.lda = (P.cf16 ? 1 : 2) * (int64_t)r;  // fp16 or [hi | lo]
         sd.akoff1 = 0;
         sd.map = nullptr;
         sd.zero_row = 0;
-        sd.B[0] = sd.B[1] = v.a_down;
+        sd.B[0] = sd.B[1] = P.cf16 ? v.a_down_f16 : v.a_down;
         sd.b_stride[0] = sd.b_stride[1] = (int64_t)d * r;
+        sd.a_exp = P.cf16 ? (const int32_t*)(W + q.v_exp) : nullptr;
+        sd.b_exp[0] = sd.b_exp[1] = v.a_down_f16_exp;
       }
     }
     return sa;
@@ -772,7 +832,17 @@ lx_status run(const lx_tree_layer& t, int T, int k, const void* x, const int32_t
     h.C = (float*)(W + q.gu);
     h.ldc = 2 * (int64_t)f;
     h.c_coloff[1] = f;
-    if (fast[l]) {
+    if (fast[l] && P.cf16) {
+      h.B[0] = v.a_gate_f16;
+      h.B[1] = v.a_up_f16;
+      h.lda = 2 * (int64_t)r;  // [gate | up] fp16
+      h.a_koff[1] = r;
+      h.K = h.Kb = r;
+      h.a_row_exp = (const int32_t*)(W + q.z_exp);
+      h.b_exp = v.a_gate_f16_exp;
+      h.b_exp1 = v.a_up_f16_exp;
+      LX_TRY(f16big(kLowOut[l], h, l, 256, OUT_X16, q.rows_max));
+    } else if (fast[l]) {
       h.lda = 4 * (int64_t)r;
       h.a_koff[1] = 2 * r;
       h.K = 2 * r;
@@ -804,8 +874,9 @@ lx_status run(const lx_tree_layer& t, int T, int k, const void* x, const int32_t
     ta.slot_flags[l] = ba.lv[l].slot_flags;
     ta.dgu[l] = (const float*)(W + q.gu);
     ta.hbar[l] = (float*)(W + q.hbar);
-    ta.hbar_mode[l] = l == 0 && P.f16 ? HBAR_F16 : l == 0 && P.lo8 ? HBAR_LO8 : fast[l] ? HBAR_HILO : HBAR_F32;
-    ta.hbar_exp[l] = l == 0 && P.f16 ? (int32_t*)(W + P.hbar_exp) : nullptr;
+    const bool hf16 = l == 0 ? P.f16 : P.cf16;
+    ta.hbar_mode[l] = hf16 ? HBAR_F16 : l == 0 && P.lo8 ? HBAR_LO8 : fast[l] ? HBAR_HILO : HBAR_F32;
+    ta.hbar_exp[l] = !hf16 ? nullptr : l == 0 ? (int32_t*)(W + P.hbar_exp) : (int32_t*)(W + q.hbar_exp);
     ta.x16[l] = fast[l] ? 1 : 0;
     ta.y[l] = (const float*)(W + q.y);
   }
@@ -836,9 +907,9 @@ lx_status run(const lx_tree_layer& t, int T, int k, const void* x, const int32_t
       g.b_exp = t.anchor_down_f16_exp;
       g.tiles = ba.lv[0].tiles[kTabBig];
       g.n_tiles = ba.lv[0].n_tiles[kTabBig];
-      if (!gemm_f16_ok(g, q.rows_max))
+      if (!gemm_f16_ok(g, 256, OUT_X16, q.rows_max))
         return fail(LX_ERR_UNSUPPORTED, "anchor_down: shape not supported by the fp16 GEMM");
-      LX_LAUNCH("anchor_down", launch_gemm_f16(g, OUT_X16, (int)q.tiles_max[kTabBig], lstream));
+      LX_LAUNCH("anchor_down", launch_gemm_f16(g, 256, OUT_X16, (int)q.tiles_max[kTabBig], lstream));
     } else if (P.lo8) {
       // row = [bf16 hi (f) | fp8 lo (f bytes) | scale words (f / 64)] in 4f bytes
       g.lda = 2 * (int64_t)f;
@@ -879,6 +950,26 @@ lx_status run(const lx_tree_layer& t, int T, int k, const void* x, const int32_t
     g.b_stride[0] = (int64_t)r * f;
     g.ncols[0] = r;
     g.C = (float*)(W + q.v);
+    if (P.cf16) {
+      // fp16 activation sums (row scales) against the fp16 copy; v fp16 with
+      // one scale per tile (merged trees: over the leaf rows, as below)
+      const int lt = P.merged ? L : l;
+      const LevelPlan& qa = P.lv[lt];
+      g.A = W + qa.hbar;
+      if (P.merged && l < L) {
+        g.widx_anc = pa.anc + (size_t)l * E;
+        g.widx_fac = (const int32_t*)(W + q.fac);
+      }
+      g.B[0] = v.b_down_f16;
+      g.lda = f;
+      g.K = g.Kb = f;
+      g.ldc = r;
+      g.a_row_exp = (const int32_t*)(W + qa.hbar_exp);
+      g.b_exp = v.b_down_f16_exp;
+      g.c_row_exp = (int32_t*)(W + q.v_exp);
+      LX_TRY(f16big(kDownIn[l], g, lt, r <= 64 ? 64 : 128, OUT_F16T, qa.rows_max));
+      continue;
+    }
     if (P.merged) {
       const LevelPlan& qL = P.lv[L];
       g.A = W + qL.hbar;
@@ -923,7 +1014,14 @@ lx_status run(const lx_tree_layer& t, int T, int k, const void* x, const int32_t
     h.ncols[0] = d;
     h.C = (float*)(W + q.y);
     h.ldc = d;
-    if (fast[l]) {
+    if (fast[l] && P.cf16) {
+      h.B[0] = v.a_down_f16;
+      h.lda = r;
+      h.K = h.Kb = r;
+      h.a_row_exp = (const int32_t*)(W + q.v_exp);
+      h.b_exp = v.a_down_f16_exp;
+      LX_TRY(f16big(kDownOut[l], h, l, 256, OUT_X16, q.rows_max));
+    } else if (fast[l]) {
       h.lda = 2 * (int64_t)r;
       h.K = 2 * r;
       h.Kb = r;

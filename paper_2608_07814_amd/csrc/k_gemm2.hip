@@ -186,6 +186,9 @@ void k_gemm_big(GemmArgs p, int ntn) {
   constexpr int NST = NST_FIT > 4 ? 4 : NST_FIT;
   static_assert(NST >= 2, "two stages must fit");
   __shared__ __attribute__((aligned(1024))) u16 smem[NST * (SA + SB)];
+  // fp16 operands: the scale exponents of the tile's A rows (read by the
+  // epilogue; loaded when the item starts)
+  __shared__ int s_rexp[F16 ? BM : 1];
   u16* const sA0 = smem;
   u16* const sB0 = smem + SA;
   u16* const sA1 = smem + SA + SB;
@@ -233,6 +236,11 @@ void k_gemm_big(GemmArgs p, int ntn) {
     const int n0 = nt * BN;
     const int tpart = n0 < p.ncols[0] ? 0 : 1;
     const int akoff = p.a_koff[tpart];
+    if constexpr (F16) {
+      for (int row = tid; row < BM; row += NTHR) s_rexp[row] = p.a_row_exp[te.row0 + (row < te.nrows ? row : te.nrows - 1)];
+      asm volatile("" ::: "memory");
+      wait_lgkm0();
+    }
     const u16* __restrict__ Bw0 = (const u16*)p.B[0] + (int64_t)widx * p.b_stride[0];
     const u16* __restrict__ Bw1 = (const u16*)p.B[1] + (int64_t)widx * p.b_stride[1];
 
@@ -524,7 +532,33 @@ void k_gemm_big(GemmArgs p, int ntn) {
       float* const ep = (float*)smem + wave * (32 * PITCH);
       const int c4 = (lane % LPR) * 4;
       const int col = n0 + wn * WN + c4;
-      const int bexp = F16 ? p.b_exp[widx] : 0;
+      const int bexp = F16 ? ((tpart && p.b_exp1) ? p.b_exp1 : p.b_exp)[widx] : 0;
+      // OUT_F16T: one power-of-two scale 2^tsh for the whole tile (its rows
+      // are whole rows), from the largest magnitude over every wavefront's
+      // block; with fp16 operands the accumulators already carry 2^(a_row_exp
+      // + bexp), which the row exponents add
+      int tsh = 0;
+      if constexpr (OUT == OUT_F16T) {
+        __shared__ float s_tmax[BigCfg<BM, BN>::NW];
+        float m = 0.f;
+#pragma unroll
+        for (int mi = 0; mi < MI; ++mi)
+#pragma unroll
+          for (int ni = 0; ni < NI; ++ni)
+#pragma unroll
+            for (int i = 0; i < 16; ++i) m = fmaxf(m, fabsf(acc[mi][ni][i]));
+#pragma unroll
+        for (int off = 32; off >= 1; off >>= 1) m = fmaxf(m, __shfl_xor(m, off, 64));
+        if (lane == 0) s_tmax[wave] = m;
+        __syncthreads();
+        float tm = 0.f;
+#pragma unroll
+        for (int w = 0; w < BigCfg<BM, BN>::NW; ++w) tm = fmaxf(tm, s_tmax[w]);
+        if (tm > 0.f) {
+          tsh = 14 - ((int)((__float_as_uint(tm) >> 23) & 0xFF) - 127);
+          tsh = tsh < -100 ? -100 : tsh > 100 ? 100 : tsh;
+        }
+      }
       X16Rows xr(p.C, p.ldc, te.row0 + wm * WM + lane / LPR, RPP, col);
       // full tiles store without per-row checks (a separate, branch-free copy)
       auto emit = [&](auto check) {
@@ -541,15 +575,26 @@ void k_gemm_big(GemmArgs p, int ntn) {
             float4 v = *(const float4*)&ep[rr * PITCH + c4];
             const int r = wm * WM + mi * 32 + rr;
             const bool ok = !decltype(check)::value || (r < te.nrows && col < ncol);
-            if constexpr (F16) {
+            if constexpr (F16 && OUT != OUT_F16T) {
               if (ok) {
-                const int e = -(p.a_row_exp[te.row0 + r] + bexp);
+                const int e = -(s_rexp[r] + bexp);
                 v = make_float4(ldexpf(v.x, e), ldexpf(v.y, e), ldexpf(v.z, e), ldexpf(v.w, e));
               }
             }
             if constexpr (OUT == OUT_X16) {
               if (ok) xr.store(v);
               xr.next();
+            } else if constexpr (OUT == OUT_F16T) {
+              if (!ok) continue;
+              typedef _Float16 h4 __attribute__((ext_vector_type(4)));
+              h4 q;
+              q[0] = (_Float16)ldexpf(v.x, tsh);
+              q[1] = (_Float16)ldexpf(v.y, tsh);
+              q[2] = (_Float16)ldexpf(v.z, tsh);
+              q[3] = (_Float16)ldexpf(v.w, tsh);
+              *(h4*)((_Float16*)p.C + (int64_t)(te.row0 + r) * p.ldc + col) = q;
+              if (wn == 0 && lane % LPR == 0)
+                p.c_row_exp[te.row0 + r] = tsh + (F16 ? s_rexp[r] + bexp : 0);
             } else if constexpr (OUT == OUT_HILO) {
               if (!ok) continue;
               // part p, local column c -> hi at base_p + c, lo at base_p + ncols[p] + c
@@ -592,12 +637,19 @@ void k_gemm_big(GemmArgs p, int ntn) {
 // configuration of k_gemm_big: 8 wavefronts in a 2 x 4 grid of 128 x 64
 // blocks, both operands HBM -> LDS by direct loads into a 2-stage ring of
 // 64-wide K-slabs, persistent XCD-ordered work items, epilogue through LDS.
-// Within a segment of rank r the slabs alternate hi and lo halves of A
-// against each 64-column weight slab (K = 2 r, the weight slab read twice
-// back to back). A segment's A rows come through its own row map (entries
-// below 0 read the segment's zero row), its weights from its own level.
+// bf16 (F16 false): within a segment of rank r the slabs alternate hi and
+// lo halves of A against each 64-column weight slab (K = 2 r, the weight slab
+// read twice back to back). fp16 (F16 true): one slab per 64 columns of the
+// rank; A row a and weight matrix i of part p carry the scales 2^a_exp[a] and
+// 2^b_exp[p][i], so segment s adds its products at scale 2^E_s(row) with
+// E_s(row) = a_exp[map_s(row)] + b_exp[p][widx_s]; the accumulators are
+// multiplied row by row by 2^(E_next - E_prev) when the segment changes and by
+// 2^-E_last at the end (exact power-of-two steps). A segment's A rows come
+// through its own row map (entries below 0 read the segment's zero row), its
+// weights from its own level.
 constexpr int kSegMax = LX_MAX_LEVELS;
 
+template <bool F16>
 __global__ __launch_bounds__(512, 1) __attribute__((amdgpu_waves_per_eu(2, 2)))
 void k_gemm_seg(GemmArgs p, SegArgs sg, int ntn) {
   constexpr int BM = 256, BN = 256, NTHR = 512, WGN = 4;
@@ -609,6 +661,8 @@ void k_gemm_seg(GemmArgs p, SegArgs sg, int ntn) {
   u16* const sB0 = smem + SA;
   u16* const sA1 = smem + SA + SB;
   u16* const sB1 = smem + 2 * SA + SB;
+  // fp16 segments: scale exponent E_s of each tile row per segment
+  __shared__ __attribute__((aligned(16))) int s_e[F16 ? kSegMax : 1][BM];
 
   const int real = *p.n_tiles * ntn;
   const int q = real / NXCD, rmd = real % NXCD;
@@ -646,8 +700,24 @@ void k_gemm_seg(GemmArgs p, SegArgs sg, int ntn) {
         }
       }
       widx[sI] = w;
-      nsl[sI] = w >= 0 ? 2 * sg.s[sI].rank / BK2 : 0;
+      nsl[sI] = w >= 0 ? (F16 ? 1 : 2) * sg.s[sI].rank / BK2 : 0;
       nk += nsl[sI];
+    }
+    if constexpr (F16) {
+      // every row's exponent per active segment (visible to all wavefronts
+      // after the K loop's first barrier, before any use)
+#pragma unroll
+      for (int sI = 0; sI < kSegMax; ++sI) {
+        if (sI >= nseg || widx[sI] < 0) continue;
+        const SegDesc& dsc = sg.s[sI];
+        for (int row = tid; row < BM; row += NTHR) {
+          const int r = row < te.nrows ? row : te.nrows - 1;
+          const int src = dsc.map ? dsc.map[te.row0 + r] : te.row0 + r;
+          s_e[sI][row] = (src >= 0 ? dsc.a_exp[src] : 0) + dsc.b_exp[tpart][widx[sI]];
+        }
+      }
+      asm volatile("" ::: "memory");
+      wait_lgkm0();
     }
 
     // operand addresses of the segment being issued (set at its first slab):
@@ -708,7 +778,7 @@ void k_gemm_seg(GemmArgs p, SegArgs sg, int ntn) {
         set_seg(sel);
         cur = sel;
       }
-      const int qq = loc >> 1, per = loc & 1;
+      const int qq = F16 ? loc : loc >> 1, per = F16 ? 0 : loc & 1;
       const int kb = qq * BK2, ka = per * crank + kb;
 #pragma unroll
       for (int j = 0; j < A_ROUNDS; ++j)
@@ -739,7 +809,7 @@ void k_gemm_seg(GemmArgs p, SegArgs sg, int ntn) {
   do {                                                                              \
     _Pragma("unroll") for (int mi = 0; mi < MI; ++mi)                               \
       _Pragma("unroll") for (int ni = 0; ni < NI; ++ni)                             \
-        acc[mi][ni] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(FA[mi], FB[ni], acc[mi][ni], 0, 0, 0); \
+        acc[mi][ni] = mfma16<F16>(FA[mi], FB[ni], acc[mi][ni]);                   \
   } while (0)
 #define LX_SCOMPUTE(SA_, SB_)                                                       \
   do {                                                                              \
@@ -760,6 +830,27 @@ void k_gemm_seg(GemmArgs p, SegArgs sg, int ntn) {
     LX_SMFMAS(fa1, fb1);                                                            \
   } while (0)
 
+    // fp16: accumulators from scale 2^E_from to 2^E_to row by row (to < 0:
+    // the true scale). Lane rows of block mi: 8 q + 4 (lane / 32) + j for
+    // accumulator element 4 q + j.
+    auto rescale = [&](int from, int to) {
+#pragma unroll
+      for (int mi = 0; mi < MI; ++mi)
+#pragma unroll
+        for (int qd = 0; qd < 4; ++qd) {
+          const int rb = wm * WM + mi * 32 + 8 * qd + 4 * (lane >> 5);
+          const int4 ef = *(const int4*)&s_e[from][rb];
+          int4 et = make_int4(0, 0, 0, 0);
+          if (to >= 0) et = *(const int4*)&s_e[to][rb];
+          const int dd[4] = {et.x - ef.x, et.y - ef.y, et.z - ef.z, et.w - ef.w};
+#pragma unroll
+          for (int ni = 0; ni < NI; ++ni)
+#pragma unroll
+            for (int j = 0; j < 4; ++j) acc[mi][ni][4 * qd + j] = ldexpf(acc[mi][ni][4 * qd + j], dd[j]);
+        }
+    };
+    int aseg = -1;  // segment whose scale the accumulators carry
+
     // 2-stage ring: slab kt lives in stage kt & 1; one issue site and one
     // compute site (the segment switch inside issue() is then inlined once)
     for (int i = 0; i < 2 && i < nk; ++i) issue(i ? sA1 : sA0, i ? sB1 : sB0, i);
@@ -771,9 +862,31 @@ void k_gemm_seg(GemmArgs p, SegArgs sg, int ntn) {
       else
         wait_vmcnt<0>();
       bar();
+      if constexpr (F16) {
+        int sel = 0, loc = kt;
+        bool found = false;
+#pragma unroll
+        for (int u = 0; u < kSegMax; ++u) {
+          if (!found) {
+            if (loc < nsl[u]) {
+              sel = u;
+              found = true;
+            } else {
+              loc -= nsl[u];
+            }
+          }
+        }
+        if (sel != aseg) {
+          if (aseg >= 0) rescale(aseg, sel);
+          aseg = sel;
+        }
+      }
       LX_SCOMPUTE(cA, cB);
       bar();
       if (kt + 2 < nk) issue(cA, cB, kt + 2);
+    }
+    if constexpr (F16) {
+      if (aseg >= 0) rescale(aseg, -1);
     }
 #undef LX_SCOMPUTE
 #undef LX_SMFMAS
@@ -1231,6 +1344,13 @@ __global__ __launch_bounds__(SK_THR) void k_gemm_skinny_wide(SkinnyBatch b) {
 
 template <int BM, int BN>
 hipError_t launch_bn(const GemmArgs& g, int ofmt, int grid, int ntn, hipStream_t s) {
+  if constexpr (BM == 256 && BN >= 128) {
+    if (ofmt == OUT_F16T) {
+      hipLaunchKernelGGL((k_gemm_big<BM, BN, OUT_F16T>), dim3(grid), dim3(BigCfg<BM, BN>::NTHR), 0, s, g, ntn);
+      return hipGetLastError();
+    }
+  }
+  if (ofmt == OUT_F16T) return hipErrorInvalidValue;
   if (ofmt == OUT_HILO)
     hipLaunchKernelGGL((k_gemm_big<BM, BN, OUT_HILO>), dim3(grid), dim3(BigCfg<BM, BN>::NTHR), 0, s, g, ntn);
   else if (ofmt == OUT_X16)
@@ -1327,25 +1447,39 @@ hipError_t launch_convert_f16(const void* w, int n, int64_t per, void* w16, int3
   return hipGetLastError();
 }
 
-bool gemm_f16_ok(const GemmArgs& g, int64_t a_rows_total) {
-  if (!g.a_row_exp || !g.b_exp || g.ncols[1] != 0 || g.K <= 0 || g.K % BK2 || (g.Kb > 0 && g.Kb != g.K)) return false;
-  return gemm_big_ok(g, 256, a_rows_total);
+bool gemm_f16_ok(const GemmArgs& g, int bn, int ofmt, int64_t a_rows_total) {
+  if (!g.a_row_exp || !g.b_exp || g.a_rows || g.K <= 0 || g.K % BK2 || (g.Kb > 0 && g.Kb != g.K)) return false;
+  if (ofmt == OUT_F16T) {
+    if (bn != 64 && bn != 128) return false;
+    if (!g.c_row_exp || g.ncols[0] + g.ncols[1] > bn || ((uintptr_t)g.c_row_exp & 3)) return false;
+  } else if (bn != 256 || (ofmt != OUT_X16 && ofmt != OUT_F32)) {
+    return false;
+  }
+  return gemm_big_ok(g, bn, a_rows_total);
 }
 
 // x16 rows need a row length that keeps every 8-byte mantissa word aligned.
 static bool x16_shape_ok(const GemmArgs& g, int ofmt) { return ofmt != OUT_X16 || g.ldc % 32 == 0; }
 
-hipError_t launch_gemm_f16(const GemmArgs& g, int ofmt, int grid_tiles, hipStream_t s) {
+hipError_t launch_gemm_f16(const GemmArgs& g, int bn, int ofmt, int grid_tiles, hipStream_t s) {
   if (!x16_shape_ok(g, ofmt)) return hipErrorInvalidValue;
-  const int ntn = (g.ncols[0] + 255) / 256;
+  const int ntn = (g.ncols[0] + g.ncols[1] + bn - 1) / bn;
   int grid = grid_tiles * ntn;
   if (grid <= 0) return hipSuccess;
   const int cap = grid_cap();
   if (grid > cap) grid = cap;
-  if (ofmt == OUT_X16)
+  if (ofmt == OUT_F16T && bn == 64)
+    hipLaunchKernelGGL((k_gemm_big<256, 64, OUT_F16T, false, true>), dim3(grid), dim3(BigCfg<256, 64>::NTHR), 0, s,
+                       g, ntn);
+  else if (ofmt == OUT_F16T && bn == 128)
+    hipLaunchKernelGGL((k_gemm_big<256, 128, OUT_F16T, false, true>), dim3(grid), dim3(BigCfg<256, 128>::NTHR), 0,
+                       s, g, ntn);
+  else if (ofmt == OUT_X16 && bn == 256)
     hipLaunchKernelGGL((k_gemm_big<256, 256, OUT_X16, false, true>), dim3(grid), dim3(512), 0, s, g, ntn);
-  else
+  else if (ofmt == OUT_F32 && bn == 256)
     hipLaunchKernelGGL((k_gemm_big<256, 256, OUT_F32, false, true>), dim3(grid), dim3(512), 0, s, g, ntn);
+  else
+    return hipErrorInvalidValue;
   return hipGetLastError();
 }
 
@@ -1397,6 +1531,9 @@ int grid_cap() {
 
 hipError_t launch_gemm_big(const GemmArgs& g, int bm, int bn, int ofmt, int grid_tiles, hipStream_t s) {
   if (!x16_shape_ok(g, ofmt)) return hipErrorInvalidValue;
+  // fp16 output with one scale per tile: the tile spans whole rows
+  if (ofmt == OUT_F16T && (!g.c_row_exp || g.ncols[0] + g.ncols[1] > bn || bm != 256 || bn < 128))
+    return hipErrorInvalidValue;
   const int ntn = (g.ncols[0] + g.ncols[1] + bn - 1) / bn;
   int grid = grid_tiles * ntn;  // upper bound on work items
   if (grid <= 0) return hipSuccess;
@@ -1423,7 +1560,9 @@ bool gemm_seg_ok(const GemmArgs& g, const SegArgs& sa, int64_t out_rows) {
     const SegDesc& d = sa.s[i];
     if (!d.A || !d.B[0] || (g.ncols[1] > 0 && !d.B[1]) || d.rank <= 0 || d.rank % BK2) return false;
     if (d.anc_off >= 0 && !d.fac) return false;
-    if (d.akoff1 + 2 * d.rank > d.lda || (g.ncols[1] == 0 && 2 * d.rank > d.lda)) return false;
+    const int kw = sa.f16 ? d.rank : 2 * d.rank;  // A columns per part
+    if (d.akoff1 + kw > d.lda || (g.ncols[1] == 0 && kw > d.lda)) return false;
+    if (sa.f16 && (!d.a_exp || !d.b_exp[0] || (g.ncols[1] > 0 && !d.b_exp[1]))) return false;
     if (((uintptr_t)d.A & 15) || ((uintptr_t)d.B[0] & 15) || ((uintptr_t)d.B[1] & 15)) return false;
     // 32-bit byte offsets: the weight rows of one factor
     if ((int64_t)ncol * d.rank * 2 >= ((int64_t)1 << 31)) return false;
@@ -1437,7 +1576,10 @@ hipError_t launch_gemm_seg(const GemmArgs& g, const SegArgs& sa, int grid_tiles,
   if (grid <= 0) return hipSuccess;
   const int cap = grid_cap();
   if (grid > cap) grid = cap;
-  hipLaunchKernelGGL(k_gemm_seg, dim3(grid), dim3(512), 0, s, g, sa, ntn);
+  if (sa.f16)
+    hipLaunchKernelGGL(k_gemm_seg<true>, dim3(grid), dim3(512), 0, s, g, sa, ntn);
+  else
+    hipLaunchKernelGGL(k_gemm_seg<false>, dim3(grid), dim3(512), 0, s, g, sa, ntn);
   return hipGetLastError();
 }
 

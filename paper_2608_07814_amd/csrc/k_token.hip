@@ -101,25 +101,31 @@ __device__ __forceinline__ void hbar_store(void* base, int mode, int row, int c,
   const uint32_t be_next = __shfl_down(be, 8, 64);
   if ((c & 63) == 0) *(uint32_t*)(rb + 3 * f + (c >> 6) * 4) = be | (be_next << 8);
 }
-// HBAR_F16: the largest magnitude over a whole row (every thread of the
-// workgroup holds 4 of its values and must call this), then the row stored
-// as fp16 scaled by 2^s with the maximum in [2^14, 2^15) (s to exps[row]).
+// HBAR_F16: a token's fp16 rows share one power-of-two scale 2^sh, chosen
+// from the largest magnitude over all of the token's fp16 rows (the rows are
+// partial sums of the same activations, within a few binades of each other,
+// and fp16 keeps 11 bits of every value within 29 binades of the maximum).
+// Every thread of the workgroup holds 4 values of every row and calls this
+// with its own maximum; returns sh (largest magnitude in [2^14, 2^15)).
 constexpr int kMaxWaves = 16;
-__device__ __forceinline__ void hbar_store_f16(void* base, int32_t* exps, int row, int c, int f, float4 v) {
+__device__ __forceinline__ int f16_token_shift(float m) {
   __shared__ float s_red[kMaxWaves];
-  float m = fmaxf(fmaxf(fabsf(v.x), fabsf(v.y)), fmaxf(fabsf(v.z), fabsf(v.w)));
 #pragma unroll
   for (int off = 32; off >= 1; off >>= 1) m = fmaxf(m, __shfl_xor(m, off, 64));
   if ((threadIdx.x & 63) == 0) s_red[threadIdx.x >> 6] = m;
   __syncthreads();
   float rm = 0.f;
   for (int i = 0; i < (int)(blockDim.x >> 6); ++i) rm = fmaxf(rm, s_red[i]);
-  __syncthreads();  // s_red is reused by the next row
+  __syncthreads();  // s_red is reused by the next token
   int sh = 0;
   if (rm > 0.f) {
     sh = 14 - ((int)((__float_as_uint(rm) >> 23) & 0xFF) - 127);
     sh = sh < -100 ? -100 : sh > 100 ? 100 : sh;
   }
+  return sh;
+}
+// The row's 4 values at column c as fp16 scaled by 2^sh; thread 0 records sh.
+__device__ __forceinline__ void hbar_store_f16(void* base, int32_t* exps, int row, int c, int f, float4 v, int sh) {
   typedef _Float16 h4 __attribute__((ext_vector_type(4)));
   h4 q;
   q[0] = (_Float16)ldexpf(v.x, sh);
@@ -350,17 +356,40 @@ __global__ __launch_bounds__(kFastThr) void k_swiglu_fast(TokenArgs a) {
   // each level-l row that does work: the sum of its experts' h in slot order
   // (merged trees: the intermediate levels' down products run on the leaf
   // rows' sums, so only the anchor and leaf levels are stored)
+  auto row_sum = [&](int l, int j0) {
+    float4 hs = make_float4(0.f, 0.f, 0.f, 0.f);
+#pragma unroll
+    for (int j = j0; j < kFastK; ++j)
+      if (row[l][j] == row[l][j0] && (fl[NL][j] & 1)) add4(hs, h[j]);
+    return hs;
+  };
+  auto stored = [&](int l, int j0) { return (fl[l][j0] & 3) == 3 && !(merged && l > 0 && l < NL); };
+  // fp16 rows: one scale for the token (whole rows per workgroup: see the
+  // launch), from the largest magnitude over its fp16 rows
+  bool any16 = false;
+#pragma unroll
+  for (int l = 0; l <= NL; ++l) any16 |= a.hbar_mode[l] == HBAR_F16;
+  int sh = 0;
+  if (any16) {
+    float m = 0.f;
+#pragma unroll
+    for (int l = 0; l <= NL; ++l)
+#pragma unroll
+      for (int j0 = 0; j0 < kFastK; ++j0) {
+        if (!stored(l, j0) || a.hbar_mode[l] != HBAR_F16) continue;
+        const float4 hs = row_sum(l, j0);
+        m = fmaxf(m, fmaxf(fmaxf(fabsf(hs.x), fabsf(hs.y)), fmaxf(fabsf(hs.z), fabsf(hs.w))));
+      }
+    sh = f16_token_shift(m);
+  }
 #pragma unroll
   for (int l = 0; l <= NL; ++l)
 #pragma unroll
     for (int j0 = 0; j0 < kFastK; ++j0) {
-      if ((fl[l][j0] & 3) != 3 || (merged && l > 0 && l < NL)) continue;
-      float4 hs = make_float4(0.f, 0.f, 0.f, 0.f);
-#pragma unroll
-      for (int j = j0; j < kFastK; ++j)
-        if (row[l][j] == row[l][j0] && (fl[NL][j] & 1)) add4(hs, h[j]);
-      if (a.hbar_mode[l] == HBAR_F16)  // (whole rows per workgroup: see the launch)
-        hbar_store_f16(a.hbar[l], a.hbar_exp[l], row[l][j0], c, f, hs);
+      if (!stored(l, j0)) continue;
+      const float4 hs = row_sum(l, j0);
+      if (a.hbar_mode[l] == HBAR_F16)
+        hbar_store_f16(a.hbar[l], a.hbar_exp[l], row[l][j0], c, f, hs, sh);
       else
         hbar_store(a.hbar[l], a.hbar_mode[l], row[l][j0], c, f, hs);
     }

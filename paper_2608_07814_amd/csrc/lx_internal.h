@@ -88,11 +88,15 @@ __device__ __forceinline__ X16x4 x16_load_raw(const void* base, int64_t row, int
   return w;
 }
 
-// Output format of a GEMM: fp32, a bf16 (hi, lo) pair, or x16.
-enum OutFmt { OUT_F32 = 0, OUT_HILO = 1, OUT_X16 = 2 };
+// Output format of a GEMM: fp32, a bf16 (hi, lo) pair, x16, or OUT_F16T:
+// fp16 [rows][ldc] with one power-of-two scale per tile (the tile spans whole
+// rows), the scale's exponent s written per row to GemmArgs::c_row_exp
+// (stored value = true value * 2^s).
+enum OutFmt { OUT_F32 = 0, OUT_HILO = 1, OUT_X16 = 2, OUT_F16T = 3 };
 // Format of the weighted activation sums (the down GEMMs' input); HBAR_F16:
-// fp16 rows of f values scaled by 2^exp (exp per row, in a separate array,
-// chosen so that the row's largest magnitude lands in [2^14, 2^15)).
+// fp16 rows of f values scaled by 2^exp (exp per row, in a separate array;
+// one value for all of a token's fp16 rows, chosen so that their largest
+// magnitude lands in [2^14, 2^15)).
 enum HbarMode { HBAR_F32 = 0, HBAR_HILO = 1, HBAR_LO8 = 2, HBAR_F16 = 3 };
 
 // ---------------------------------------------------------------- fp8 lo
@@ -283,10 +287,14 @@ struct GemmArgs {
   // another level; below 0: the tile is skipped) instead of its own
   const int32_t* widx_anc;
   const int32_t* widx_fac;
-  // fp16 anchor down projection (launch_gemm_f16): A row r is scaled by
-  // 2^a_row_exp[r], weight matrix i by 2^b_exp[i]
+  // fp16 operands (launch_gemm_f16): A row r is scaled by 2^a_row_exp[r],
+  // weight matrix i of part 0 by 2^b_exp[i], of part 1 by 2^b_exp1[i] (null:
+  // b_exp)
   const int32_t* a_row_exp;
   const int32_t* b_exp;
+  const int32_t* b_exp1;
+  // OUT_F16T: per-row scale exponents of the output
+  int32_t* c_row_exp;
 };
 
 enum AMode { A_BF16 = 0, A_F32_HILO = 1 };
@@ -310,11 +318,12 @@ bool gemm_big_ok(const GemmArgs& g, int bn, int64_t a_rows_total);
 // above, lo slabs from the fp8 copies with the block-scaled fp8 MFMA.
 bool gemm_lo8_ok(const GemmArgs& g, int64_t a_rows_total);
 hipError_t launch_gemm_lo8(const GemmArgs& g, int ofmt, int grid_tiles, hipStream_t s);
-// The fp16 variant (256 x 256 tiles, one part, K = Kb): A and W fp16 with
-// their power-of-two scales (GemmArgs::a_row_exp, b_exp), undone exactly in
-// the epilogue.
-bool gemm_f16_ok(const GemmArgs& g, int64_t a_rows_total);
-hipError_t launch_gemm_f16(const GemmArgs& g, int ofmt, int grid_tiles, hipStream_t s);
+// The fp16 variant (256 x bn tiles, K = Kb): A and W fp16 with their
+// power-of-two scales (GemmArgs::a_row_exp, b_exp, b_exp1), undone exactly in
+// the epilogue (x16 or fp32 output) or carried into the output's row
+// exponents (OUT_F16T).
+bool gemm_f16_ok(const GemmArgs& g, int bn, int ofmt, int64_t a_rows_total);
+hipError_t launch_gemm_f16(const GemmArgs& g, int bn, int ofmt, int grid_tiles, hipStream_t s);
 // Weights [n][per] bf16 -> fp16 [n][per] scaled per matrix i by 2^exps[i]
 // (exps[i] puts the matrix's largest magnitude in [2^14, 2^15); 0 for an
 // all-zero matrix).
@@ -327,17 +336,20 @@ hipError_t launch_gemm_big(const GemmArgs& g, int bm, int bn, int ofmt, int grid
 
 // Segmented large-tile GEMM (256 x 256 tiles, x16 output): the correction
 // products of several tree levels that land on the same output rows, as one
-// GEMM whose K is the concatenation of the levels' (hi | lo) operands:
+// GEMM whose K is the concatenation of the levels' operands:
 //   C[row] = sum over segments s of A_s[map_s(row)] * W_s[widx_s]^T
 // over the tiles of the leaf level (p.tiles, p.n_tiles, p.ncols, p.C,
 // p.ldc; the other GemmArgs fields are unused). Segment s is active for a
 // tile when its factor index widx_s (the tile's own widx for the leaf
 // segment, else the validated factor of the leaf's ancestor at the
-// segment's level) is >= 0; its K is 2 rank (hi then lo against the same
-// weight columns), rank a multiple of 64. An A row index below 0 in a
-// segment's map selects that segment's zero row.
+// segment's level) is >= 0; rank a multiple of 64. bf16 segments: K is 2
+// rank (hi then lo against the same weight columns). fp16 segments (f16 set):
+// K is rank, A row a carries 2^a_exp[a] and weight matrix i of part p
+// 2^b_exp[p][i]; the accumulators are rescaled row by row when the segment
+// changes, so each level's products are added at the true scale. An A row
+// index below 0 in a segment's map selects that segment's zero row.
 struct SegDesc {
-  const void* A;           // bf16 [rows][lda]; part 1 starts at column akoff1
+  const void* A;           // bf16 or fp16 [rows][lda]; part 1 starts at column akoff1
   int64_t lda;             // elements
   const int32_t* map;      // output row -> A row (null: identity)
   int32_t zero_row;        // A row of zeros used for map entries < 0
@@ -347,9 +359,12 @@ struct SegDesc {
   const int32_t* fac;      // validated factor index per node of the level
   const void* B[2];        // weights of the two parts [widx][n][rank]
   int64_t b_stride[2];
+  const int32_t* a_exp;    // fp16 segments: row exponents of A
+  const int32_t* b_exp[2]; // fp16 segments: exponents of the weight matrices
 };
 struct SegArgs {
   int32_t nseg;
+  int32_t f16;             // fp16 segments
   const int32_t* anc;      // [(L + 1) * E] ancestor of each expert per level
   SegDesc s[LX_MAX_LEVELS];
 };

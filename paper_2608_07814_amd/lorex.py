@@ -33,7 +33,14 @@ class LxLevel(ctypes.Structure):
     _fields_ = [("n_nodes", _c_i32), ("rank", _c_i32), ("n_factors", _c_i32),
                 ("parent", _c_void), ("factor_of", _c_void),
                 ("a_gate", _c_void), ("b_gate", _c_void), ("a_up", _c_void), ("b_up", _c_void),
-                ("a_down", _c_void), ("b_down", _c_void)]
+                ("a_down", _c_void), ("b_down", _c_void),
+                ("a_gate_f16", _c_void), ("a_gate_f16_exp", _c_void), ("a_up_f16", _c_void),
+                ("a_up_f16_exp", _c_void), ("a_down_f16", _c_void), ("a_down_f16_exp", _c_void),
+                ("b_down_f16", _c_void), ("b_down_f16_exp", _c_void)]
+
+# the optional fp16 factor copies of a level (lx_convert_f16), with exponents
+FACTOR_F16 = ("a_gate_f16", "a_gate_f16_exp", "a_up_f16", "a_up_f16_exp", "a_down_f16", "a_down_f16_exp",
+              "b_down_f16", "b_down_f16_exp")
 
 
 class LxTreeLayer(ctypes.Structure):
@@ -52,7 +59,10 @@ class LxFlatLayer(ctypes.Structure):
                 ("a_gate", _c_void), ("b_gate", _c_void), ("a_up", _c_void), ("b_up", _c_void),
                 ("a_down", _c_void), ("b_down", _c_void),
                 ("dom_down_f8", _c_void), ("dom_down_f8_scale", _c_void),
-                ("dom_down_f16", _c_void), ("dom_down_f16_exp", _c_void)]
+                ("dom_down_f16", _c_void), ("dom_down_f16_exp", _c_void),
+                ("a_gate_f16", _c_void), ("a_gate_f16_exp", _c_void), ("a_up_f16", _c_void),
+                ("a_up_f16_exp", _c_void), ("a_down_f16", _c_void), ("a_down_f16_exp", _c_void),
+                ("b_down_f16", _c_void), ("b_down_f16_exp", _c_void)]
 
 
 class LxDenseLayer(ctypes.Structure):
@@ -176,6 +186,16 @@ class DeviceLevel:
     b_up: torch.Tensor
     a_down: torch.Tensor
     b_down: torch.Tensor
+    # optional fp16 copies of the factors (lx_convert_f16): fp16 tensors of
+    # the same shapes and int32 exponents [n_factors]
+    a_gate_f16: Optional[torch.Tensor] = None
+    a_gate_f16_exp: Optional[torch.Tensor] = None
+    a_up_f16: Optional[torch.Tensor] = None
+    a_up_f16_exp: Optional[torch.Tensor] = None
+    a_down_f16: Optional[torch.Tensor] = None
+    a_down_f16_exp: Optional[torch.Tensor] = None
+    b_down_f16: Optional[torch.Tensor] = None
+    b_down_f16_exp: Optional[torch.Tensor] = None
 
     @property
     def n_nodes(self) -> int:
@@ -230,6 +250,8 @@ class DeviceLayer:
             c.a_gate, c.b_gate, c.a_up, c.b_up, c.a_down, c.b_down = (
                 _ptr(lv.a_gate), _ptr(lv.b_gate), _ptr(lv.a_up), _ptr(lv.b_up),
                 _ptr(lv.a_down), _ptr(lv.b_down))
+            for n in FACTOR_F16:
+                setattr(c, n, _ptr(getattr(lv, n)))
         return s
 
     def flat_struct(self) -> LxFlatLayer:
@@ -247,6 +269,8 @@ class DeviceLayer:
         s.a_gate, s.b_gate, s.a_up, s.b_up, s.a_down, s.b_down = (
             _ptr(lv.a_gate), _ptr(lv.b_gate), _ptr(lv.a_up), _ptr(lv.b_up), _ptr(lv.a_down),
             _ptr(lv.b_down))
+        for n in FACTOR_F16:
+            setattr(s, n, _ptr(getattr(lv, n)))
         return s
 
     def dense_struct(self) -> LxDenseLayer:
@@ -440,6 +464,21 @@ def attach_down_f16(layer: "DeviceLayer") -> "DeviceLayer":
     return layer
 
 
+def attach_factors_f16(layer: "DeviceLayer") -> "DeviceLayer":
+    """Give every level of a bf16 layer the fp16 copies of its factors (used,
+    with the anchor down fp16 copy, by the fp16 path of the correction
+    products); a no-op for fp32 layers and levels without factors."""
+    if layer.dtype == "bf16":
+        for lv in layer.levels:
+            if lv.n_factors == 0:
+                continue
+            for n in ("a_gate", "a_up", "a_down", "b_down"):
+                w16, ex = convert_f16(getattr(lv, n))
+                setattr(lv, n + "_f16", w16)
+                setattr(lv, n + "_f16_exp", ex)
+    return layer
+
+
 def attach_down_f8(layer: "DeviceLayer") -> "DeviceLayer":
     """Give a bf16 layer the fp8 copy of its anchor down weights (used by the
     anchor down projection where applicable); a no-op for other layers."""
@@ -452,8 +491,9 @@ def to_device(layer, device="cuda", lo8: bool = True, f16: bool = True) -> Devic
     """Copy a host layer (fields as in ``lxsynth.Layer``) to device tensors.
     ``lo8``: also prepare the fp8 copy of the anchor down weights (bf16 layers
     with f a multiple of 64), so the anchor down projection can take its
-    fp8-lo path; ``f16``: also prepare their fp16 copy (bf16 layers), for the
-    fp16 path (preferred where it applies)."""
+    fp8-lo path; ``f16``: also prepare their fp16 copy and the fp16 copies of
+    every level's factors (bf16 layers), for the fp16 path (preferred where it
+    applies)."""
     dt = layer.dtype
     levels = []
     for lv in layer.levels:
@@ -470,7 +510,7 @@ def to_device(layer, device="cuda", lo8: bool = True, f16: bool = True) -> Devic
     if lo8:
         dl = attach_down_f8(dl)
     if f16:
-        dl = attach_down_f16(dl)
+        dl = attach_factors_f16(attach_down_f16(dl))
     return dl
 
 

@@ -324,3 +324,33 @@ def test_convert_f16_validation(L):
     assert L.lx_moe_tree_workspace_bytes(ctypes.byref(s), 64, 8) == 0
     s.anchor_down_f16_exp = FAKE
     assert L.lx_moe_tree_workspace_bytes(ctypes.byref(s), 64, 8) > 0
+
+
+def test_factor_f16_copies_validation(L):
+    """The fp16 factor copies of a level come as all eight arrays or none,
+    aligned, and only in bf16 layers (checked on the host, no device access);
+    the flat layer carries them the same way."""
+    s = _tree()
+    lv = s.levels[0]
+    names = lx.FACTOR_F16
+    lv.a_gate_f16 = FAKE
+    assert L.lx_moe_tree_workspace_bytes(ctypes.byref(s), 64, 8) == 0
+    assert "fp16 factor copies" in L.lx_last_error().decode()
+    for n in names:
+        setattr(lv, n, FAKE)
+    assert L.lx_moe_tree_workspace_bytes(ctypes.byref(s), 64, 8) > 0
+    lv.b_down_f16 = FAKE + 8  # not 16-byte aligned
+    assert L.lx_moe_tree_workspace_bytes(ctypes.byref(s), 64, 8) == 0
+    lv.b_down_f16 = FAKE
+    s.dtype = lx.LX_F32
+    assert L.lx_moe_tree_workspace_bytes(ctypes.byref(s), 64, 8) == 0
+    f = lx.LxFlatLayer()
+    f.E, f.C, f.d, f.f, f.r, f.M, f.dtype = 128, 16, 2048, 768, 64, 112, lx.LX_BF16
+    for n in ("cluster_of", "factor_of", "dom_gate", "dom_up", "dom_down", "a_gate", "b_gate",
+              "a_up", "b_up", "a_down", "b_down"):
+        setattr(f, n, FAKE)
+    f.a_down_f16 = FAKE
+    assert L.lx_moe_workspace_bytes(ctypes.byref(f), 64, 8) == 0
+    for n in names:
+        setattr(f, n, FAKE)
+    assert L.lx_moe_workspace_bytes(ctypes.byref(f), 64, 8) > 0

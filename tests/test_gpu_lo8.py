@@ -146,3 +146,29 @@ def test_f16_forward(cfg, T, kind):
     say(f"{cfg} T={T}: fp16 err/RMS {e16:.3e}, fp8-lo err/RMS {e8:.3e}")
     assert not np.array_equal(g16, g8)
     assert e16 <= TOL_DESIGN and e16 <= TOL_BF16
+
+
+@pytest.mark.parametrize("cfg,T,used", [(1, 2048, True), (4, 2304, True), (3, 2048, False)])
+def test_f16_correction_products(cfg, T, used):
+    """With the fp16 copies of the factors every correction product runs once
+    in fp16 (tile-scaled fp16 intermediates, token-scaled fp16 activation
+    sums): a different result from the same layer without those copies (the
+    path ran), and both meet the design bound against the oracle. Rank 96
+    (not a multiple of 64) keeps the bf16 pair products: identical results.
+    (Sizes with more than 64 rows per expert at every level: smaller batches
+    take the skinny kernel, which keeps the pairs.)"""
+    require_gpu()
+    p = make_problem(cfg, T=T)
+    ref = O.moe_forward(p.layer, p.x, p.routing.topk_ids, p.routing.topk_weights)
+    full = lx.to_device(p.layer, lo8=True, f16=True)
+    assert all(lv.b_down_f16 is not None for lv in full.levels if lv.n_factors > 0)
+    anchor_only = lx.to_device(p.layer, lo8=True, f16=True)
+    for lv in anchor_only.levels:
+        for n in lx.FACTOR_F16:
+            setattr(lv, n, None)
+    g_full = gpu_forward(p, dev_layer=full)
+    g_anchor = gpu_forward(p, dev_layer=anchor_only)
+    e_full, e_anchor = err_ratio(g_full, ref), err_ratio(g_anchor, ref)
+    say(f"cfg{cfg} T={T}: fp16 corrections err/RMS {e_full:.3e}, bf16-pair corrections {e_anchor:.3e}")
+    assert np.array_equal(g_full, g_anchor) != used
+    assert e_full <= TOL_DESIGN and e_anchor <= TOL_DESIGN
