@@ -395,6 +395,119 @@ __global__ __launch_bounds__(kFastThr) void k_swiglu_fast(TokenArgs a) {
     }
 }
 
+// x16 gate|up rows and fp16 activation sums on every stored level, 8
+// columns per thread: one 16-byte mantissa load and one 2-byte exponent load
+// per row half (half the load instructions of k_swiglu_fast); whole rows per
+// workgroup (threads past f / 8 only join the token's scale reduction).
+// Same sums, in the same order, as k_swiglu_fast.
+template <int NL, bool MERGED>
+__global__ __launch_bounds__(kFastThr) void k_swiglu_x16w(TokenArgs a) {
+  const int t = blockIdx.x, f = a.f;
+  const int c = threadIdx.x * 8;
+  const bool act = c < f;
+  const int64_t rb = x16_row_bytes(2 * (int64_t)f);
+  int row[NL + 1][kFastK], fl[NL + 1][kFastK];
+  float w[kFastK];
+  token_meta_fast<NL>(a, t, row, fl, w);
+  constexpr bool merged = MERGED;  // (a.merged, as a template argument)
+  struct Raw8 {
+    uint4 m;
+    uint32_t e;
+  };
+  auto ld8 = [&](const float* base, int r, int col) {
+    const uint8_t* rp = (const uint8_t*)base + (int64_t)r * rb;
+    Raw8 v;
+    v.m = *(const uint4*)(rp + 2 * col);
+    v.e = *(const uint16_t*)(rp + 4 * f + (col >> 2));
+    return v;
+  };
+  auto add8 = [&](float4 (&acc)[2], const Raw8& v) {
+    X16x4 q0, q1;
+    q0.m = make_uint2(v.m.x, v.m.y);
+    q0.e = v.e & 0xFFu;
+    q1.m = make_uint2(v.m.z, v.m.w);
+    q1.e = v.e >> 8;
+    add4(acc[0], x16_unpack(q0));
+    add4(acc[1], x16_unpack(q1));
+  };
+  auto live = [&](int l, int j) { return (fl[l][j] & 2) && !(merged && l < NL); };
+  Raw8 gv[kFastK][NL + 1], uv[kFastK][NL + 1];
+#pragma unroll
+  for (int j = 0; j < kFastK; ++j) {
+    if (!act || !(fl[NL][j] & 1)) continue;
+    gv[j][0] = ld8(a.gu0, row[0][j], c);
+    uv[j][0] = ld8(a.gu0, row[0][j], f + c);
+#pragma unroll
+    for (int l = 1; l <= NL; ++l) {
+      if (!live(l, j)) continue;
+      gv[j][l] = ld8(a.dgu[l], row[l][j], c);
+      uv[j][l] = ld8(a.dgu[l], row[l][j], f + c);
+    }
+  }
+  float4 h[kFastK][2];
+#pragma unroll
+  for (int j = 0; j < kFastK; ++j) {
+    h[j][0] = h[j][1] = make_float4(0.f, 0.f, 0.f, 0.f);
+    if (!act || !(fl[NL][j] & 1)) continue;
+    float4 g[2] = {make_float4(0.f, 0.f, 0.f, 0.f), make_float4(0.f, 0.f, 0.f, 0.f)};
+    float4 u[2] = {g[0], g[0]};
+    add8(g, gv[j][0]);
+    add8(u, uv[j][0]);
+#pragma unroll
+    for (int l = 1; l <= NL; ++l) {
+      if (!live(l, j)) continue;
+      add8(g, gv[j][l]);
+      add8(u, uv[j][l]);
+    }
+#pragma unroll
+    for (int q = 0; q < 2; ++q)
+      h[j][q] = make_float4(w[j] * silu_mul(g[q].x, u[q].x), w[j] * silu_mul(g[q].y, u[q].y),
+                            w[j] * silu_mul(g[q].z, u[q].z), w[j] * silu_mul(g[q].w, u[q].w));
+  }
+  auto stored = [&](int l, int j0) { return (fl[l][j0] & 3) == 3 && !(merged && l > 0 && l < NL); };
+  auto row_sum = [&](int l, int j0, int q) {
+    float4 hs = make_float4(0.f, 0.f, 0.f, 0.f);
+#pragma unroll
+    for (int j = j0; j < kFastK; ++j)
+      if (row[l][j] == row[l][j0] && (fl[NL][j] & 1)) add4(hs, h[j][q]);
+    return hs;
+  };
+  float m = 0.f;
+#pragma unroll
+  for (int l = 0; l <= NL; ++l)
+#pragma unroll
+    for (int j0 = 0; j0 < kFastK; ++j0) {
+      if (!stored(l, j0)) continue;
+#pragma unroll
+      for (int q = 0; q < 2; ++q) {
+        const float4 hs = row_sum(l, j0, q);
+        m = fmaxf(m, fmaxf(fmaxf(fabsf(hs.x), fabsf(hs.y)), fmaxf(fabsf(hs.z), fabsf(hs.w))));
+      }
+    }
+  const int sh = f16_token_shift(m);
+  typedef _Float16 h8 __attribute__((ext_vector_type(8)));
+#pragma unroll
+  for (int l = 0; l <= NL; ++l)
+#pragma unroll
+    for (int j0 = 0; j0 < kFastK; ++j0) {
+      if (!stored(l, j0)) continue;
+      if (act) {
+        const float4 s0 = row_sum(l, j0, 0), s1 = row_sum(l, j0, 1);
+        h8 o;
+        o[0] = (_Float16)ldexpf(s0.x, sh);
+        o[1] = (_Float16)ldexpf(s0.y, sh);
+        o[2] = (_Float16)ldexpf(s0.z, sh);
+        o[3] = (_Float16)ldexpf(s0.w, sh);
+        o[4] = (_Float16)ldexpf(s1.x, sh);
+        o[5] = (_Float16)ldexpf(s1.y, sh);
+        o[6] = (_Float16)ldexpf(s1.z, sh);
+        o[7] = (_Float16)ldexpf(s1.w, sh);
+        *(h8*)((_Float16*)a.hbar[l] + (int64_t)row[l][j0] * f + c) = o;
+      }
+      if (threadIdx.x == 0) a.hbar_exp[l][row[l][j0]] = sh;
+    }
+}
+
 template <int NL, bool X16>
 __global__ __launch_bounds__(kFastThr) void k_combine_fast(TokenArgs a) {
   const int t = blockIdx.x, k = a.k, d = a.d;
@@ -429,6 +542,69 @@ __global__ __launch_bounds__(kFastThr) void k_combine_fast(TokenArgs a) {
   }
 }
 
+// x16 rows, CPT (8 or 16) columns per thread: 16-byte mantissa loads and
+// one 2- or 4-byte exponent load per row (a fraction of the load
+// instructions of 4 columns per thread); otherwise as k_combine_fast.
+template <int NL, int CPT>
+__global__ __launch_bounds__(kFastThr) void k_combine_x16w(TokenArgs a) {
+  constexpr int NG = CPT / 4;  // 4-value groups per thread
+  const int t = blockIdx.x, k = a.k, d = a.d;
+  const int c = (blockIdx.y * blockDim.x + threadIdx.x) * CPT;
+  if (c >= d) return;
+  int row[NL + 1][kFastK], fl[NL + 1][kFastK];
+  float w[kFastK];
+  token_meta_fast<NL>(a, t, row, fl, w);
+  const bool merged = a.merged != 0;
+  const int64_t rb = x16_row_bytes(d);
+  uint4 mv[NL + 1][kFastK][NG / 2];
+  uint32_t ev[NL + 1][kFastK];
+#pragma unroll
+  for (int l = 0; l <= NL; ++l)
+#pragma unroll
+    for (int j = 0; j < kFastK; ++j)
+      if ((fl[l][j] & 3) == 3 && !(merged && l > 0 && l < NL)) {
+        const uint8_t* rp = (const uint8_t*)a.y[l] + (int64_t)row[l][j] * rb;
+#pragma unroll
+        for (int h = 0; h < NG / 2; ++h) mv[l][j][h] = *(const uint4*)(rp + 2 * c + 16 * h);
+        if constexpr (NG == 2)
+          ev[l][j] = *(const uint16_t*)(rp + 2 * d + (c >> 2));
+        else
+          ev[l][j] = *(const uint32_t*)(rp + 2 * d + (c >> 2));
+      }
+  float4 acc[NG];
+#pragma unroll
+  for (int g = 0; g < NG; ++g) acc[g] = make_float4(0.f, 0.f, 0.f, 0.f);
+#pragma unroll
+  for (int l = 0; l <= NL; ++l)
+#pragma unroll
+    for (int j = 0; j < kFastK; ++j)
+      if ((fl[l][j] & 3) == 3 && !(merged && l > 0 && l < NL)) {
+#pragma unroll
+        for (int g = 0; g < NG; ++g) {
+          const uint4 m = mv[l][j][g >> 1];
+          X16x4 q;
+          q.m = (g & 1) ? make_uint2(m.z, m.w) : make_uint2(m.x, m.y);
+          q.e = (ev[l][j] >> (8 * g)) & 0xFFu;
+          add4(acc[g], x16_unpack(q));
+        }
+      }
+  if (a.out_dtype == LX_F32) {
+    float4* o = (float4*)((float*)a.out + (int64_t)t * d + c);
+#pragma unroll
+    for (int g = 0; g < NG; ++g) o[g] = acc[g];
+  } else {
+#pragma unroll
+    for (int g = 0; g < NG; ++g) {
+      bf16x4 o;
+      o[0] = (__bf16)acc[g].x;
+      o[1] = (__bf16)acc[g].y;
+      o[2] = (__bf16)acc[g].z;
+      o[3] = (__bf16)acc[g].w;
+      *(bf16x4*)((uint16_t*)a.out + (int64_t)t * d + c + 4 * g) = o;
+    }
+  }
+}
+
 // Threads per workgroup for n 4-column groups: whole wavefronts, at most
 // kFastThr; one wavefront for small batches, whose token count alone would
 // give fewer workgroups than the chip has compute units.
@@ -452,6 +628,23 @@ hipError_t launch_swiglu_reduce(const TokenArgs& a, hipStream_t s) {
   const int fmt = uniform_fmt(a);
   bool f16 = false;
   for (int l = 0; l <= a.L; ++l) f16 |= a.hbar_mode[l] == HBAR_F16;
+  // x16 rows and fp16 sums on every stored level: the wide kernel, where
+  // f / 8 threads fill whole wavefronts (f = 768 measured faster on the
+  // 4-column kernel)
+  bool all16 = true;
+  for (int l = 0; l <= a.L; ++l) all16 &= a.hbar_mode[l] == HBAR_F16 || (a.merged && l > 0 && l < a.L);
+  if (a.k <= kFastK && a.L <= kFastL && fmt == 1 && all16 && a.f % 512 == 0 && a.f <= 8 * kFastThr) {
+    const int thr = (a.f / 8 + 63) / 64 * 64;
+    if (a.L == 0)
+      hipLaunchKernelGGL((k_swiglu_x16w<0, false>), dim3(a.T), dim3(thr), 0, s, a);
+    else if (a.L == 1)
+      hipLaunchKernelGGL((k_swiglu_x16w<1, false>), dim3(a.T), dim3(thr), 0, s, a);
+    else if (a.merged)
+      hipLaunchKernelGGL((k_swiglu_x16w<2, true>), dim3(a.T), dim3(thr), 0, s, a);
+    else
+      hipLaunchKernelGGL((k_swiglu_x16w<2, false>), dim3(a.T), dim3(thr), 0, s, a);
+    return hipGetLastError();
+  }
   if (a.k <= kFastK && a.L <= kFastL && fmt >= 0) {
     const int thr = fast_threads(a.f, a.T);
     const dim3 grid(a.T, (a.f / 4 + thr - 1) / thr);
@@ -481,6 +674,18 @@ hipError_t launch_swiglu_reduce(const TokenArgs& a, hipStream_t s) {
 hipError_t launch_combine(const TokenArgs& a, hipStream_t s) {
   if (a.T == 0) return hipSuccess;
   const int fmt = uniform_fmt(a);
+  if (a.k <= kFastK && a.L <= kFastL && fmt == 1 && a.d % 64 == 0) {  // 16-byte aligned rows
+    constexpr int CPT = 8;  // (16 measured no faster)
+    const int thr = fast_threads(a.d * 4 / CPT, a.T);
+    const dim3 grid(a.T, (a.d / CPT + thr - 1) / thr);
+    if (a.L == 0)
+      hipLaunchKernelGGL((k_combine_x16w<0, CPT>), grid, dim3(thr), 0, s, a);
+    else if (a.L == 1)
+      hipLaunchKernelGGL((k_combine_x16w<1, CPT>), grid, dim3(thr), 0, s, a);
+    else
+      hipLaunchKernelGGL((k_combine_x16w<2, CPT>), grid, dim3(thr), 0, s, a);
+    return hipGetLastError();
+  }
   if (a.k <= kFastK && a.L <= kFastL && fmt >= 0) {
     const int thr = fast_threads(a.d, a.T);
     const dim3 grid(a.T, (a.d / 4 + thr - 1) / thr);
