@@ -656,13 +656,20 @@ void k_gemm_seg(GemmArgs p, SegArgs sg, int ntn) {
   constexpr int MI = BM / 64, NI = BN / (32 * WGN), WM = BM / 2, WN = BN / WGN;
   constexpr int A_ROUNDS = BM * 8 / NTHR, B_ROUNDS = BN * 8 / NTHR, ROUNDS = A_ROUNDS + B_ROUNDS;
   constexpr int SA = BM * BK2, SB = BN * BK2;
+  constexpr int PITCH = WN + 4, LPR = WN / 4, RPP = 64 / LPR;  // epilogue
   __shared__ __attribute__((aligned(1024))) u16 smem[2 * (SA + SB)];
   u16* const sA0 = smem;
   u16* const sB0 = smem + SA;
   u16* const sA1 = smem + SA + SB;
   u16* const sB1 = smem + 2 * SA + SB;
-  // fp16 segments: scale exponent E_s of each tile row per segment
-  __shared__ __attribute__((aligned(16))) int s_e[F16 ? kSegMax : 1][BM];
+  // epilogue transposes, 8 rows at a time per wavefront, apart from the
+  // stages: the next item's first two slabs load while this item's outputs
+  // are stored
+  __shared__ __attribute__((aligned(16))) float s_ep[8][8 * PITCH];
+  // fp16 segments: scale exponent E_s of each tile row per segment, one
+  // buffer per item parity (the next item's table is written while this
+  // item's may still be read)
+  __shared__ __attribute__((aligned(16))) int s_e[F16 ? 2 : 1][F16 ? kSegMax : 1][BM];
 
   const int real = *p.n_tiles * ntn;
   const int q = real / NXCD, rmd = real % NXCD;
@@ -672,21 +679,32 @@ void k_gemm_seg(GemmArgs p, SegArgs sg, int ntn) {
   const int mx = ((int)gridDim.x - x + NXCD - 1) / NXCD;
   const int ncol = p.ncols[0] + p.ncols[1];
   const int nseg = sg.nseg;
+  int Lg = xbeg + (int)blockIdx.x / NXCD;
+  if (Lg >= xend) return;
 
-  for (int Lg = xbeg + (int)blockIdx.x / NXCD; Lg < xend; Lg += mx) {
-    int tid = threadIdx.x;
-    asm volatile("" : "+v"(tid));
-    const int wave = tid >> 6, lane = tid & 63;
-    const int wm = wave / WGN, wn = wave % WGN;
-    const int ti = Lg / ntn, nt = Lg % ntn;
-    const TileEntry te = p.tiles[ti];
-    const int n0 = nt * BN;
-    const int tpart = n0 < p.ncols[0] ? 0 : 1;
+  // the lane index is made opaque once per item (below), so per-lane address
+  // arithmetic is recomputed per item instead of being kept live throughout
+  int tid = threadIdx.x;
 
-    // factor index and slab count of every segment for this tile (slab
-    // counts 0 for segments that do not apply)
-    int widx[kSegMax], nsl[kSegMax];
-    int nk = 0;
+  // the item being loaded: its tile, n-tile, part, factor index and slab
+  // count of every segment (0 for segments that do not apply)
+  TileEntry te;
+  int n0 = 0, tpart = 0, nk = 0, eb = 0;
+  int widx[kSegMax], nsl[kSegMax];
+  // operand addresses of the segment being issued (set at its first slab):
+  // wave-uniform bases and 32-bit per-lane byte offsets
+  int cur = -1, crank = 0;
+  const u16* Ab = nullptr;
+  const u16* Bb = nullptr;
+  uint32_t aoff[A_ROUNDS], boff[B_ROUNDS];
+
+  auto setup = [&](int L_) {
+    const int ti = L_ / ntn, nt = L_ % ntn;
+    te = p.tiles[ti];
+    n0 = nt * BN;
+    tpart = n0 < p.ncols[0] ? 0 : 1;
+    nk = 0;
+    cur = -1;
 #pragma unroll
     for (int sI = 0; sI < kSegMax; ++sI) {
       int w = -1;
@@ -713,90 +731,84 @@ void k_gemm_seg(GemmArgs p, SegArgs sg, int ntn) {
         for (int row = tid; row < BM; row += NTHR) {
           const int r = row < te.nrows ? row : te.nrows - 1;
           const int src = dsc.map ? dsc.map[te.row0 + r] : te.row0 + r;
-          s_e[sI][row] = (src >= 0 ? dsc.a_exp[src] : 0) + dsc.b_exp[tpart][widx[sI]];
+          s_e[eb][sI][row] = (src >= 0 ? dsc.a_exp[src] : 0) + dsc.b_exp[tpart][widx[sI]];
         }
       }
       asm volatile("" ::: "memory");
       wait_lgkm0();
     }
-
-    // operand addresses of the segment being issued (set at its first slab):
-    // wave-uniform bases and 32-bit per-lane byte offsets
-    int cur = -1, crank = 0;
-    const u16* Ab = nullptr;
-    const u16* Bb = nullptr;
-    uint32_t aoff[A_ROUNDS], boff[B_ROUNDS];
-    auto set_seg = [&](int sI) {
-      const SegDesc& dsc = sg.s[sI];
-      int w = 0;
+  };
+  auto set_seg = [&](int sI) {
+    const SegDesc& dsc = sg.s[sI];
+    int w = 0;
 #pragma unroll
-      for (int u = 0; u < kSegMax; ++u)
-        if (u == sI) w = widx[u];
-      Ab = (const u16*)dsc.A;
-      crank = dsc.rank;
-      const int akoff = tpart ? dsc.akoff1 : 0;
+    for (int u = 0; u < kSegMax; ++u)
+      if (u == sI) w = widx[u];
+    Ab = (const u16*)dsc.A;
+    crank = dsc.rank;
+    const int akoff = tpart ? dsc.akoff1 : 0;
 #pragma unroll
-      for (int j = 0; j < A_ROUNDS; ++j) {
-        const int Ps = j * NTHR + tid;
-        const int row = Ps >> 3;
-        const int c = (Ps & 7) ^ swzb(row);
-        const int r = row < te.nrows ? row : te.nrows - 1;
-        int src = dsc.map ? dsc.map[te.row0 + r] : te.row0 + r;
-        if (src < 0) src = dsc.zero_row;
-        aoff[j] = ((uint32_t)src * (uint32_t)dsc.lda + (uint32_t)(akoff + c * 8)) * 2u;
-      }
-      // the tile lies inside one part: one weight matrix for all its rows
-      Bb = (const u16*)dsc.B[tpart] + (int64_t)w * dsc.b_stride[tpart];
-      const int nbase = tpart ? p.ncols[0] : 0;
-      const int nlast = tpart ? ncol - 1 : p.ncols[0] - 1;
+    for (int j = 0; j < A_ROUNDS; ++j) {
+      const int Ps = j * NTHR + tid;
+      const int row = Ps >> 3;
+      const int c = (Ps & 7) ^ swzb(row);
+      const int r = row < te.nrows ? row : te.nrows - 1;
+      int src = dsc.map ? dsc.map[te.row0 + r] : te.row0 + r;
+      if (src < 0) src = dsc.zero_row;
+      aoff[j] = ((uint32_t)src * (uint32_t)dsc.lda + (uint32_t)(akoff + c * 8)) * 2u;
+    }
+    // the tile lies inside one part: one weight matrix for all its rows
+    Bb = (const u16*)dsc.B[tpart] + (int64_t)w * dsc.b_stride[tpart];
+    const int nbase = tpart ? p.ncols[0] : 0;
+    const int nlast = tpart ? ncol - 1 : p.ncols[0] - 1;
 #pragma unroll
-      for (int j = 0; j < B_ROUNDS; ++j) {
-        const int Ps = j * NTHR + tid;
-        const int row = Ps >> 3;
-        const int c = (Ps & 7) ^ swzb(row);
-        const int n = n0 + row < nlast ? n0 + row : nlast;
-        boff[j] = ((uint32_t)(n - nbase) * (uint32_t)crank + (uint32_t)(c * 8)) * 2u;
-      }
-    };
-    // slab kt: segment and slab within it (slabs of a segment: weight slab
-    // qq, hi then lo)
-    auto issue = [&](u16* sA_, u16* sB_, int kt) {
-      int sel = 0, loc = kt;
-      bool found = false;
+    for (int j = 0; j < B_ROUNDS; ++j) {
+      const int Ps = j * NTHR + tid;
+      const int row = Ps >> 3;
+      const int c = (Ps & 7) ^ swzb(row);
+      const int n = n0 + row < nlast ? n0 + row : nlast;
+      boff[j] = ((uint32_t)(n - nbase) * (uint32_t)crank + (uint32_t)(c * 8)) * 2u;
+    }
+  };
+  // segment of slab kt and the slab's index within it
+  auto seg_of = [&](int kt, int& loc) {
+    int sel = 0;
+    loc = kt;
+    bool found = false;
 #pragma unroll
-      for (int u = 0; u < kSegMax; ++u) {
-        if (!found) {
-          if (loc < nsl[u]) {
-            sel = u;
-            found = true;
-          } else {
-            loc -= nsl[u];
-          }
+    for (int u = 0; u < kSegMax; ++u) {
+      if (!found) {
+        if (loc < nsl[u]) {
+          sel = u;
+          found = true;
+        } else {
+          loc -= nsl[u];
         }
       }
-      if (sel != cur) {
-        set_seg(sel);
-        cur = sel;
-      }
-      const int qq = F16 ? loc : loc >> 1, per = F16 ? 0 : loc & 1;
-      const int kb = qq * BK2, ka = per * crank + kb;
+    }
+    return sel;
+  };
+  // slab kt of the loaded item (slabs of a bf16 segment: weight slab qq, hi
+  // then lo)
+  auto issue = [&](u16* sA_, u16* sB_, int kt) {
+    int loc;
+    const int sel = seg_of(kt, loc);
+    if (sel != cur) {
+      set_seg(sel);
+      cur = sel;
+    }
+    const int qq = F16 ? loc : loc >> 1, per = F16 ? 0 : loc & 1;
+    const int kb = qq * BK2, ka = per * crank + kb;
 #pragma unroll
-      for (int j = 0; j < A_ROUNDS; ++j)
-        load_lds16_sb(Ab, aoff[j] + (uint32_t)ka * 2u, &sA_[(j * NTHR + wave * 64) * 8]);
+    for (int j = 0; j < A_ROUNDS; ++j)
+      load_lds16_sb(Ab, aoff[j] + (uint32_t)ka * 2u, &sA_[(j * NTHR + (tid >> 6) * 64) * 8]);
 #pragma unroll
-      for (int j = 0; j < B_ROUNDS; ++j)
-        load_lds16_sb(Bb, boff[j] + (uint32_t)kb * 2u, &sB_[(j * NTHR + wave * 64) * 8]);
-    };
+    for (int j = 0; j < B_ROUNDS; ++j)
+      load_lds16_sb(Bb, boff[j] + (uint32_t)kb * 2u, &sB_[(j * NTHR + (tid >> 6) * 64) * 8]);
+  };
 
-    f32x16 acc[MI][NI];
-#pragma unroll
-    for (int mi = 0; mi < MI; ++mi)
-#pragma unroll
-      for (int ni = 0; ni < NI; ++ni)
-#pragma unroll
-        for (int i = 0; i < 16; ++i) acc[mi][ni][i] = 0.f;
-
-    bf16x8 fa0[MI], fb0[NI], fa1[MI], fb1[NI];
+  f32x16 acc[MI][NI];
+  bf16x8 fa0[MI], fb0[NI], fa1[MI], fb1[NI];
 #define LX_SFRAG(SA_, SB_, KS, FA, FB)                                              \
   do {                                                                              \
     const int kc_ = (KS) * 2 + (lane >> 5);                                         \
@@ -830,30 +842,43 @@ void k_gemm_seg(GemmArgs p, SegArgs sg, int ntn) {
     LX_SMFMAS(fa1, fb1);                                                            \
   } while (0)
 
-    // fp16: accumulators from scale 2^E_from to 2^E_to row by row (to < 0:
-    // the true scale). Lane rows of block mi: 8 q + 4 (lane / 32) + j for
-    // accumulator element 4 q + j.
-    auto rescale = [&](int from, int to) {
+  // fp16: accumulators from scale 2^E_from to 2^E_to row by row (to < 0:
+  // the true scale), table buffer tb. Lane rows of block mi: 8 q + 4 (lane /
+  // 32) + j for accumulator element 4 q + j.
+  auto rescale = [&](int tb, int from, int to) {
 #pragma unroll
-      for (int mi = 0; mi < MI; ++mi)
+    for (int mi = 0; mi < MI; ++mi)
 #pragma unroll
-        for (int qd = 0; qd < 4; ++qd) {
-          const int rb = wm * WM + mi * 32 + 8 * qd + 4 * (lane >> 5);
-          const int4 ef = *(const int4*)&s_e[from][rb];
-          int4 et = make_int4(0, 0, 0, 0);
-          if (to >= 0) et = *(const int4*)&s_e[to][rb];
-          const int dd[4] = {et.x - ef.x, et.y - ef.y, et.z - ef.z, et.w - ef.w};
+      for (int qd = 0; qd < 4; ++qd) {
+        const int rb = ((tid >> 6) / WGN) * WM + mi * 32 + 8 * qd + 4 * ((tid & 63) >> 5);
+        const int4 ef = *(const int4*)&s_e[tb][from][rb];
+        int4 et = make_int4(0, 0, 0, 0);
+        if (to >= 0) et = *(const int4*)&s_e[tb][to][rb];
+        const int dd[4] = {et.x - ef.x, et.y - ef.y, et.z - ef.z, et.w - ef.w};
 #pragma unroll
-          for (int ni = 0; ni < NI; ++ni)
+        for (int ni = 0; ni < NI; ++ni)
 #pragma unroll
-            for (int j = 0; j < 4; ++j) acc[mi][ni][4 * qd + j] = ldexpf(acc[mi][ni][4 * qd + j], dd[j]);
-        }
-    };
-    int aseg = -1;  // segment whose scale the accumulators carry
+          for (int j = 0; j < 4; ++j) acc[mi][ni][4 * qd + j] = ldexpf(acc[mi][ni][4 * qd + j], dd[j]);
+      }
+  };
 
-    // 2-stage ring: slab kt lives in stage kt & 1; one issue site and one
-    // compute site (the segment switch inside issue() is then inlined once)
-    for (int i = 0; i < 2 && i < nk; ++i) issue(i ? sA1 : sA0, i ? sB1 : sB0, i);
+  // 2-stage ring: slab kt lives in stage kt & 1; one issue site and one
+  // compute site per item (the segment switch inside issue() is then inlined
+  // once). Slabs 0 and 1 of an item are issued before the previous item's
+  // epilogue.
+  setup(Lg);
+  for (int i = 0; i < 2 && i < nk; ++i) issue(i ? sA1 : sA0, i ? sB1 : sB0, i);
+  while (true) {
+    asm volatile("" : "+v"(tid));
+    const int wave = tid >> 6, lane = tid & 63;
+    const int wm = wave / WGN, wn = wave % WGN;
+#pragma unroll
+    for (int mi = 0; mi < MI; ++mi)
+#pragma unroll
+      for (int ni = 0; ni < NI; ++ni)
+#pragma unroll
+        for (int i = 0; i < 16; ++i) acc[mi][ni][i] = 0.f;
+    int aseg = -1;  // segment whose scale the accumulators carry
     for (int kt = 0; kt < nk; ++kt) {
       u16* const cA = (kt & 1) ? sA1 : sA0;
       u16* const cB = (kt & 1) ? sB1 : sB0;
@@ -863,21 +888,10 @@ void k_gemm_seg(GemmArgs p, SegArgs sg, int ntn) {
         wait_vmcnt<0>();
       bar();
       if constexpr (F16) {
-        int sel = 0, loc = kt;
-        bool found = false;
-#pragma unroll
-        for (int u = 0; u < kSegMax; ++u) {
-          if (!found) {
-            if (loc < nsl[u]) {
-              sel = u;
-              found = true;
-            } else {
-              loc -= nsl[u];
-            }
-          }
-        }
+        int loc;
+        const int sel = seg_of(kt, loc);
         if (sel != aseg) {
-          if (aseg >= 0) rescale(aseg, sel);
+          if (aseg >= 0) rescale(eb, aseg, sel);
           aseg = sel;
         }
       }
@@ -886,48 +900,60 @@ void k_gemm_seg(GemmArgs p, SegArgs sg, int ntn) {
       if (kt + 2 < nk) issue(cA, cB, kt + 2);
     }
     if constexpr (F16) {
-      if (aseg >= 0) rescale(aseg, -1);
+      if (aseg >= 0) rescale(eb, aseg, -1);
     }
-#undef LX_SCOMPUTE
-#undef LX_SMFMAS
-#undef LX_SFRAG
 
-    // Epilogue (as k_gemm_big's x16 output): per-wavefront LDS transpose,
-    // then 4 consecutive columns per lane.
+    // every wavefront is done with both stages: load the next item's first
+    // slabs, then store this item's outputs
+    const int row0 = te.row0, nrows = te.nrows, en0 = n0;
+    const int nLg = Lg + mx;
+    const bool more = nLg < xend;
+    if (more) {
+      if constexpr (F16) eb ^= 1;
+      setup(nLg);
+      for (int i = 0; i < 2 && i < nk; ++i) issue(i ? sA1 : sA0, i ? sB1 : sB0, i);
+    }
+
+    // Epilogue (as k_gemm_big's x16 output): per-wavefront LDS transpose of
+    // 8 rows at a time, then 4 consecutive columns per lane.
     {
-      constexpr int PITCH = WN + 4;
-      constexpr int LPR = WN / 4;
-      constexpr int RPP = 64 / LPR;
-      static_assert(8 * 32 * PITCH * 4 <= (int)sizeof(smem), "epilogue LDS");
-      float* const ep = (float*)smem + wave * (32 * PITCH);
+      float* const ep = s_ep[wave];
       const int c4 = (lane % LPR) * 4;
-      const int col = n0 + wn * WN + c4;
-      X16Rows xr(p.C, p.ldc, te.row0 + wm * WM + lane / LPR, RPP, col);
+      const int col = en0 + wn * WN + c4;
+      X16Rows xr(p.C, p.ldc, row0 + wm * WM + lane / LPR, RPP, col);
       // full tiles store without per-row checks (a separate, branch-free copy)
       auto emit = [&](auto check) {
 #pragma unroll
-        for (int mi = 0; mi < MI; ++mi) {
+        for (int mi = 0; mi < MI; ++mi)
 #pragma unroll
-          for (int ni = 0; ni < NI; ++ni)
+          for (int qd = 0; qd < 4; ++qd) {
+            // rows 8 qd .. 8 qd + 7 of block mi: elements 4 qd + j (row 4 (lane / 32) + j)
 #pragma unroll
-            for (int i = 0; i < 16; ++i)
-              ep[(8 * (i >> 2) + 4 * (lane >> 5) + (i & 3)) * PITCH + ni * 32 + (lane & 31)] = acc[mi][ni][i];
+            for (int ni = 0; ni < NI; ++ni)
 #pragma unroll
-          for (int ps = 0; ps < 32 / RPP; ++ps) {
-            const int rr = ps * RPP + lane / LPR;
-            const float4 v = *(const float4*)&ep[rr * PITCH + c4];
-            if (!decltype(check)::value || (wm * WM + mi * 32 + rr < te.nrows && col < ncol)) xr.store(v);
-            xr.next();
+              for (int j = 0; j < 4; ++j)
+                ep[(4 * (lane >> 5) + j) * PITCH + ni * 32 + (lane & 31)] = acc[mi][ni][4 * qd + j];
+#pragma unroll
+            for (int ps = 0; ps < 8 / RPP; ++ps) {
+              const int rr = ps * RPP + lane / LPR;
+              const float4 v = *(const float4*)&ep[rr * PITCH + c4];
+              if (!decltype(check)::value || (wm * WM + mi * 32 + 8 * qd + rr < nrows && col < ncol)) xr.store(v);
+              xr.next();
+            }
           }
-        }
       };
-      if (te.nrows >= BM && n0 + BN <= ncol)
+      if (nrows >= BM && en0 + BN <= ncol)
         emit(std::false_type{});
       else
         emit(std::true_type{});
     }
-    bar();  // the next item's loads overwrite the epilogue's LDS
+    if (!more) break;
+    Lg = nLg;
+    cur = -1;  // the next issue recomputes the operand offsets (not kept live across the epilogue)
   }
+#undef LX_SCOMPUTE
+#undef LX_SMFMAS
+#undef LX_SFRAG
 }
 
 // ---------------------------------------------------------------- skinny
