@@ -45,9 +45,13 @@
  *   - T = 0 is a valid no-op. Host-side argument errors are returned before
  *     anything is enqueued; the message is available from lx_last_error().
  *
- * Auxiliary stream (forward entry points only). When a batch is large enough
- * for the anchor GEMMs to run on the persistent large-tile kernel and the
- * layer has corrections, the correction GEMM chains are forked onto a second
+ * Auxiliary stream (forward entry points only; off unless enabled with
+ * lx_set_aux_stream(1): every large GEMM is a persistent kernel holding one
+ * workgroup per compute unit, so two chains mostly take turns, and the
+ * measured forwards run slightly faster on one stream). When enabled, a
+ * batch is large enough for the anchor GEMMs to run on the persistent
+ * large-tile kernel and the layer has corrections, the correction GEMM
+ * chains are forked onto a second
  * stream of the same device (default priority, non-blocking) between two
  * events recorded on the caller's stream, so they overlap the anchor GEMMs;
  * the caller's stream is ordered after all of the call's work when the call
@@ -56,8 +60,8 @@
  * callers). A per-device mutex is held while a forward enqueues its work
  * (host side only), so concurrent forwards on one device enqueue one after
  * another, and their correction chains run one after another on the shared
- * stream. lx_set_aux_stream(0) turns this off: every launch then goes to the
- * caller's stream, nothing is created and no lock is taken. Decode-sized
+ * stream. With it off (the default) every launch goes to the caller's
+ * stream, nothing is created and no lock is taken. Decode-sized
  * batches and per-kernel timing (lx_profile_enable) never use it. Mutable
  * global state besides this: the switch itself, the per-thread error message
  * and the optional kernel-timing records.
@@ -499,8 +503,8 @@ lx_status lx_bucket(const lx_tree_layer* layer, int32_t T, int32_t k,
                     size_t workspace_bytes, void* stream);
 
 /* Switch for the auxiliary stream of the forward entry points (see
- * "Auxiliary stream" above): enable = 1 (the default) lets prefill-sized
- * forwards fork their correction chains onto it, 0 keeps every launch on the
+ * "Auxiliary stream" above): enable = 1 lets prefill-sized forwards fork
+ * their correction chains onto it, 0 (the default) keeps every launch on the
  * caller's stream. Process-wide; returns the previous setting. Results are
  * bitwise the same either way. No device call is made. */
 int32_t lx_set_aux_stream(int32_t enable);

@@ -423,8 +423,9 @@ struct Aux {
 };
 
 // lx_set_aux_stream: whether prefill-sized forwards may use the auxiliary
-// stream at all (process-wide).
-std::atomic<int> g_aux_enabled{1};
+// stream at all (process-wide; off by default: the persistent GEMMs of the
+// two chains contend for the compute units rather than overlap).
+std::atomic<int> g_aux_enabled{0};
 
 Aux* aux_for_current_device() {
   static std::mutex mu;

@@ -637,8 +637,8 @@ def bucket(layer: DeviceLayer, topk_ids: torch.Tensor, level: int,
 
 
 def set_aux_stream(enable: bool) -> bool:
-    """Allow (True, the default) or forbid the forward's auxiliary stream
-    (lx_set_aux_stream); returns the previous setting."""
+    """Allow (True) or forbid (False, the default) the forward's auxiliary
+    stream (lx_set_aux_stream); returns the previous setting."""
     return bool(lib().lx_set_aux_stream(1 if enable else 0))
 
 

@@ -289,12 +289,12 @@ def test_binding_error_paths_raise_lorex_error(L):
 
 def test_aux_stream_switch(L):
     """lx_set_aux_stream is a plain process-wide switch that returns the
-    previous setting (on by default) and touches no device."""
-    assert lx.set_aux_stream(False) is True
+    previous setting (off by default) and touches no device."""
     assert lx.set_aux_stream(False) is False
     assert L.lx_set_aux_stream(7) == 0          # any non-zero value enables
     assert lx.set_aux_stream(True) is True
-    assert lx.set_aux_stream(True) is True
+    assert lx.set_aux_stream(False) is True
+    assert lx.set_aux_stream(False) is False
 
 
 def test_static_forward_refuses_batches_beyond_its_scratch(L):

@@ -294,21 +294,21 @@ def test_dense_comparator():
 
 
 def test_aux_stream_switch_bitwise():
-    """With the auxiliary stream turned off (lx_set_aux_stream(0)) every
-    launch runs on the caller's stream; the results are bitwise those of the
-    default forked run, flat and tree."""
+    """With the auxiliary stream turned on (lx_set_aux_stream(1)) the
+    correction chains fork onto it; the results are bitwise those of the
+    default single-stream run, flat and tree."""
     require_gpu()
     say("aux stream on/off")
-    for cfg, T in ((1, 700), (4, 300)):
+    for cfg, T in ((1, 700), (4, 300), (4, 2304)):
         p = make_problem(cfg, T=T)
         dl = lx.to_device(p.layer)
         a = gpu_forward(p, dev_layer=dl)
-        prev = lx.set_aux_stream(False)
+        prev = lx.set_aux_stream(True)
         try:
             b = gpu_forward(p, dev_layer=dl)
         finally:
             lx.set_aux_stream(prev)
-        assert np.array_equal(a, b), f"cfg{cfg}"
+        assert np.array_equal(a, b), f"cfg{cfg} T={T}"
 
 
 def _merged_layer(case):
