@@ -204,6 +204,28 @@ def step_percentiles(fn, steps, torch):
                 p90=round(float(np.percentile(t, 90)), 4))
 
 
+def graph_timing(make_call, copies, a, torch):
+    """The same forward captured once per weight copy into a HIP graph (torch's
+    CUDAGraph API) and replayed in rotation: what a serving loop that cannot
+    afford per-kernel launch latency runs. Returns ms per step."""
+    graphs = []
+    for c in copies:
+        call = make_call(c)
+        call()  # the first call on a stream outside capture (plans, device queries)
+        torch.cuda.synchronize()
+        g = torch.cuda.CUDAGraph()
+        with torch.cuda.graph(g):
+            make_call(c)()
+        graphs.append(g)
+    it = [0]
+
+    def step():
+        graphs[it[0] % len(graphs)].replay()
+        it[0] += 1
+    ms, _ = time_steps(step, a.steps, a.warmup, torch)
+    return dict(ms_per_step=round(ms, 4), note="HIP graph replay of the same forward (launch latency removed)")
+
+
 def time_steps(fn, steps, warmup, torch):
     for _ in range(warmup):
         fn()
@@ -401,6 +423,7 @@ def run_workload(cfg_index, a, torch, np, lx, headline):
     ms, wall = time_steps(call, a.steps, a.warmup, torch)
     tokens_per_s = T / (ms * 1e-3)
     pct = step_percentiles(call, min(a.steps, 100), torch)
+    graph = graph_timing(lambda c: lx.PreparedCall(c, xd, ids, w, out, ws, kind), copies, a, torch)
 
     # per-kernel durations: HIP events around every launch, on its stream
     lx.profile_reset()
@@ -530,13 +553,16 @@ def run_workload(cfg_index, a, torch, np, lx, headline):
                       fused_saving_us=round((cms - fms) * 1e3, 2))
         del fused, fcall
 
+    graph["tokens_per_s"] = round(T / (graph["ms_per_step"] * 1e-3), 1)
     res = dict(workload=workload, tokens_per_s=round(tokens_per_s, 1), ms_per_step=round(ms, 4), step_ms=pct,
+               graph=graph,
                wall_s_timed=round(wall, 3), weight_copies=len(copies),
                config={"workload": workload, "T": T, "d": layer.d, "f": layer.f, "E": layer.E, "k": k,
                        "anchors": layer.n_anchors, "ranks": ranks[1:], "layer": kind, "seed": p.seed,
                        "out_dtype": "f32",
                        "anchor_down_copies": [c for c, off in (("fp8 lo (block-scaled)", a.no_lo8),
-                                                               ("fp16 (row-scaled sums)", a.no_f16)) if not off]},
+                                                               ("fp16 (token-scaled sums)", a.no_f16)) if not off],
+                       "factor_copies": [] if a.no_f16 else ["fp16 (tile-scaled low-rank intermediates)"]},
                roofline=roof, layer_roofline=layer_perf, kernels=kernels, dense_comparator=dense,
                gpu_router=routed)
     del copies, call
@@ -635,6 +661,7 @@ def main():
         "warmup": a.warmup,
         "ms_per_step": head["ms_per_step"],
         "step_ms": head["step_ms"],
+        "graph": head["graph"],
         "weight_copies": head["weight_copies"],
         "wall_s_timed": head["wall_s_timed"],
         "higher_is_better": True,
@@ -648,7 +675,7 @@ def main():
         "kernels": head["kernels"],
         "dense_comparator": head["dense_comparator"],
         "gpu_router": head["gpu_router"],
-        "workloads": {r["workload"]: {k: r[k] for k in ("tokens_per_s", "ms_per_step", "step_ms", "roofline",
+        "workloads": {r["workload"]: {k: r[k] for k in ("tokens_per_s", "ms_per_step", "step_ms", "graph", "roofline",
                                                          "layer_roofline", "kernels", "dense_comparator",
                                                          "gpu_router", "config")}
                       for r in results[1:]},

@@ -12,7 +12,7 @@ import torch
 from lxsynth import config, make_problem, make_layer_flat
 from oracle import moe as O
 from paper_2608_07814_amd import lorex as lx
-from gpu_util import TOL_BF16, TOL_F32, TOL_DESIGN, require_gpu, say, gpu_forward, err_ratio
+from gpu_util import TOL_BF16, TOL_F32, TOL_DESIGN, require_gpu, say, gpu_forward, err_ratio, dev_inputs
 from helpers import tiny_flat, tiny_tree, random_routing, zero_level
 
 pytestmark = pytest.mark.gpu
@@ -356,3 +356,38 @@ def test_merged_tree_products(case):
     assert e <= TOL_BF16 and e <= TOL_DESIGN
     # the same forward with the correction chains on the auxiliary stream
     assert np.array_equal(got, gpu_forward(p))
+
+
+@pytest.mark.parametrize("cfg,T", [(2, 64), (1, 700), (4, 2304)])
+def test_hip_graph_capture_replays(cfg, T):
+    """The forward captured into a HIP graph (torch's CUDAGraph API; every
+    launch on the caller's stream, no allocation, memset or host sync inside
+    the call) replays to the eager result bitwise, several times, with eager
+    forwards on other routing run between the replays."""
+    require_gpu()
+    import torch
+    say(f"graph capture cfg{cfg} T={T}")
+    p = make_problem(cfg, T=T)
+    dl = lx.to_device(p.layer)
+    xt, ids_d, w_d = dev_inputs(p)
+    kind = {1: "flat"}.get(len(dl.levels), "tree")
+    ws = lx.alloc_workspace(dl, p.T, p.k, kind)
+    out = torch.empty(p.T, p.layer.d, dtype=torch.float32, device="cuda")
+    eager = gpu_forward(p, dev_layer=dl)
+    call = lx.PreparedCall(dl, xt, ids_d, w_d, out, ws, kind)
+    call()
+    torch.cuda.synchronize()
+    g = torch.cuda.CUDAGraph()
+    with torch.cuda.graph(g):
+        lx.PreparedCall(dl, xt, ids_d, w_d, out, ws, kind)()
+    rng = np.random.default_rng(7)
+    out2 = torch.empty_like(out)
+    for rep in range(3):
+        out.zero_()
+        g.replay()
+        torch.cuda.synchronize()
+        assert np.array_equal(out.cpu().numpy().astype(np.float64), eager), f"replay {rep}"
+        # eager work on another routing between replays, in the same workspace
+        perm = torch.from_numpy(rng.permutation(p.T)).cuda()
+        lx.PreparedCall(dl, xt, ids_d[perm].contiguous(), w_d[perm].contiguous(), out2, ws, kind)()
+        torch.cuda.synchronize()
