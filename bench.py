@@ -118,9 +118,10 @@ def kernel_work(name, P, rows, touched):
         parts = [kernel_work(n, P, rows, touched) for n in name.split("+")]
         return sum(p[0] for p in parts), sum(p[1] for p in parts)
     d, f, T = P["d"], P["f"], P["T"]
-    if name in ("lowrank_gate_up_out_merged", "lowrank_down_out_merged"):
-        # one launch doing every correction level's output product
-        tag = "lowrank_gate_up_out_l" if "gate_up" in name else "lowrank_down_out_l"
+    if name in ("lowrank_gate_up_out_merged", "lowrank_down_out_merged", "lowrank_down_in_merged"):
+        # one launch doing every correction level's product of that kind
+        tag = {"lowrank_gate_up_out_merged": "lowrank_gate_up_out_l", "lowrank_down_out_merged": "lowrank_down_out_l",
+               "lowrank_down_in_merged": "lowrank_down_in_l"}[name]
         parts = [kernel_work(f"{tag}{l}", P, rows, touched) for l in range(1, len(P["ranks"]))]
         return sum(p[0] for p in parts), sum(p[1] for p in parts)
     if name == "anchor_gate_up":

@@ -143,6 +143,10 @@ struct Plan {
   // one power-of-two scale per 256-row tile (a tile spans whole rows: 2 rank
   // <= 256), the correction levels' activation sums fp16 rows as the anchor's
   bool cf16 = false;
+  // dmerge: a merged two-level tree on the fp16 path runs both levels'
+  // down-in products as one GEMM over the leaf rows, output [v1 | v2] per
+  // leaf row (level 1's v buffer, one row exponent for both)
+  bool dmerge = false;
 };
 
 int level_nodes(const lx_tree_layer& t, int l) { return l == 0 ? t.n_anchors : t.levels[l - 1].n_nodes; }
@@ -210,6 +214,8 @@ Plan make_plan(const lx_tree_layer& t, int T, int k) {
     p.merged = p.L >= 2 && T > kTokTile && p.f % 256 == 0 && p.d % 256 == 0;
     for (int l = 1; l <= p.L && p.merged; ++l)
       p.merged = p.fast[l] && !p.skinny[l] && t.levels[l - 1].rank % 64 == 0;
+    p.dmerge = p.cf16 && p.merged && p.L == 2 && t.levels[0].n_factors > 0 && t.levels[1].n_factors > 0 &&
+               t.levels[0].rank + t.levels[1].rank <= 256;
   }
   p.flags = take(16);  // first: lx_read_device_status reads offset 0
   p.anc = take((size_t)(p.L + 1) * p.E * 4);
@@ -256,7 +262,9 @@ Plan make_plan(const lx_tree_layer& t, int T, int k) {
     // rows (by linearity, the sum over a row's leaf rows of B_down h_leaf is
     // B_down of the row's sum), so its v has one row per leaf row
     const size_t Rv = inter ? (size_t)T * std::min(k, t.E) : R;
-    q.v = take(l > 0 && work ? Rv * q.rank * 4 : 0);
+    const size_t vrow = p.dmerge && l == 1 ? std::max<size_t>(q.rank * 4, (size_t)(q.rank + t.levels[1].rank) * 2)
+                                           : (size_t)q.rank * 4;
+    q.v = take(l > 0 && work ? Rv * vrow : 0);
     q.y = take((work && !inter) || leafm ? R * p.d * 4 : 0);
     if (p.cf16 && l > 0) {
       q.z_exp = take(work ? R * 4 : 0);
@@ -799,6 +807,13 @@ lx_status run(const lx_tree_layer& t, int T, int k, const void* x, const int32_t
         sd.b_stride[0] = sd.b_stride[1] = (int64_t)d * r;
         sd.a_exp = P.cf16 ? (const int32_t*)(W + q.v_exp) : nullptr;
         sd.b_exp[0] = sd.b_exp[1] = v.a_down_f16_exp;
+        if (P.dmerge) {  // [v1 | v2] rows of level 1's buffer, one exponent per row
+          const LevelPlan& q1 = P.lv[1];
+          sd.A = W + q1.v;
+          sd.lda = t.levels[0].rank + t.levels[1].rank;
+          sd.a_col0 = l == 1 ? 0 : t.levels[0].rank;
+          sd.a_exp = (const int32_t*)(W + q1.v_exp);
+        }
       }
     }
     return sa;
@@ -940,7 +955,34 @@ lx_status run(const lx_tree_layer& t, int T, int k, const void* x, const int32_t
   // correction down per level, part 1: v = B_down hbar (merged trees: over
   // the leaf rows at every level, each with its ancestor's weights)
   lstream = side;
-  for (int l = 1; l <= L; ++l) {
+  if (P.dmerge) {
+    // both levels at once: part 0 the leaf's level-1 ancestor's B_down, part 1
+    // the leaf's own
+    const lx_level& v1 = t.levels[0];
+    const lx_level& v2 = t.levels[1];
+    const LevelPlan& qL = P.lv[L];
+    GemmArgs g{};
+    g.A = W + qL.hbar;
+    g.lda = f;
+    g.K = g.Kb = f;
+    g.B[0] = v1.b_down_f16;
+    g.B[1] = v2.b_down_f16;
+    g.b_stride[0] = (int64_t)v1.rank * f;
+    g.b_stride[1] = (int64_t)v2.rank * f;
+    g.ncols[0] = v1.rank;
+    g.ncols[1] = v2.rank;
+    g.widx_anc = pa.anc + (size_t)1 * E;
+    g.widx_fac = (const int32_t*)(W + P.lv[1].fac);
+    g.widx_own1 = 1;
+    g.a_row_exp = (const int32_t*)(W + qL.hbar_exp);
+    g.b_exp = v1.b_down_f16_exp;
+    g.b_exp1 = v2.b_down_f16_exp;
+    g.C = (float*)(W + P.lv[1].v);
+    g.ldc = v1.rank + v2.rank;
+    g.c_row_exp = (int32_t*)(W + P.lv[1].v_exp);
+    LX_TRY(f16big("lowrank_down_in_merged", g, L, 256, OUT_F16T, qL.rows_max));
+  }
+  for (int l = 1; l <= L && !P.dmerge; ++l) {
     const LevelPlan& q = P.lv[l];
     const lx_level& v = t.levels[l - 1];
     if (v.n_factors == 0) continue;

@@ -225,14 +225,20 @@ void k_gemm_big(GemmArgs p, int ntn) {
     const TileEntry te = p.tiles[ti];
     // weight index: the tile's, or that of the tile node's ancestor at
     // another level (a leaf-row product with an upper level's weights)
+    // (widx_own1: that lookup is part 0's only, part 1 takes the tile's own)
     int widx = te.widx;
     if (p.widx_anc) {
       const int an = p.widx_anc[te.node];
       widx = an >= 0 ? p.widx_fac[an] : -1;
     }
+    int widx1 = p.widx_own1 ? te.widx : widx;
     // a leaf-level tile whose node (or ancestor) has no factor (it is listed
-    // for the products that merge the levels above it): nothing to do here
-    if (widx < 0) continue;
+    // for the products that merge the levels above it): nothing to do here;
+    // with two weight sources a missing one reads matrix 0 (its outputs are
+    // never used)
+    if (widx < 0 && widx1 < 0) continue;
+    if (widx < 0) widx = 0;
+    if (widx1 < 0) widx1 = 0;
     const int n0 = nt * BN;
     const int tpart = n0 < p.ncols[0] ? 0 : 1;
     const int akoff = p.a_koff[tpart];
@@ -242,7 +248,7 @@ void k_gemm_big(GemmArgs p, int ntn) {
       wait_lgkm0();
     }
     const u16* __restrict__ Bw0 = (const u16*)p.B[0] + (int64_t)widx * p.b_stride[0];
-    const u16* __restrict__ Bw1 = (const u16*)p.B[1] + (int64_t)widx * p.b_stride[1];
+    const u16* __restrict__ Bw1 = (const u16*)p.B[1] + (int64_t)widx1 * p.b_stride[1];
 
     // Per-thread source offsets (elements, chunk offset folded in) for each
     // 16-byte chunk it loads. LDS slot P = round*256 + tid holds row P>>3,
@@ -532,7 +538,7 @@ void k_gemm_big(GemmArgs p, int ntn) {
       float* const ep = (float*)smem + wave * (32 * PITCH);
       const int c4 = (lane % LPR) * 4;
       const int col = n0 + wn * WN + c4;
-      const int bexp = F16 ? ((tpart && p.b_exp1) ? p.b_exp1 : p.b_exp)[widx] : 0;
+      const int bexp = F16 ? (tpart ? (p.b_exp1 ? p.b_exp1 : p.b_exp)[widx1] : p.b_exp[widx]) : 0;
       // OUT_F16T: one power-of-two scale 2^tsh for the whole tile (its rows
       // are whole rows), from the largest magnitude over every wavefront's
       // block; with fp16 operands the accumulators already carry 2^(a_row_exp
@@ -540,6 +546,23 @@ void k_gemm_big(GemmArgs p, int ntn) {
       int tsh = 0;
       if constexpr (OUT == OUT_F16T) {
         __shared__ float s_tmax[BigCfg<BM, BN>::NW];
+        // fp16 operands, a tile over both parts: part 1's columns carry its
+        // own weight scale; bring them to part 0's (exact) so that one row
+        // exponent holds for the whole row
+        if constexpr (F16) {
+          if (tpart == 0 && n0 + BN > p.ncols[0] && p.ncols[1] > 0) {
+            const int d1 = bexp - (p.b_exp1 ? p.b_exp1 : p.b_exp)[widx1];
+#pragma unroll
+            for (int ni = 0; ni < NI; ++ni) {
+              const bool in1 = n0 + wn * WN + ni * 32 + (lane & 31) >= p.ncols[0];
+#pragma unroll
+              for (int mi = 0; mi < MI; ++mi)
+#pragma unroll
+                for (int i = 0; i < 16; ++i)
+                  if (in1) acc[mi][ni][i] = ldexpf(acc[mi][ni][i], d1);
+            }
+          }
+        }
         float m = 0.f;
 #pragma unroll
         for (int mi = 0; mi < MI; ++mi)
@@ -755,7 +778,7 @@ void k_gemm_seg(GemmArgs p, SegArgs sg, int ntn) {
       const int r = row < te.nrows ? row : te.nrows - 1;
       int src = dsc.map ? dsc.map[te.row0 + r] : te.row0 + r;
       if (src < 0) src = dsc.zero_row;
-      aoff[j] = ((uint32_t)src * (uint32_t)dsc.lda + (uint32_t)(akoff + c * 8)) * 2u;
+      aoff[j] = ((uint32_t)src * (uint32_t)dsc.lda + (uint32_t)(dsc.a_col0 + akoff + c * 8)) * 2u;
     }
     // the tile lies inside one part: one weight matrix for all its rows
     Bb = (const u16*)dsc.B[tpart] + (int64_t)w * dsc.b_stride[tpart];
@@ -1476,7 +1499,7 @@ hipError_t launch_convert_f16(const void* w, int n, int64_t per, void* w16, int3
 bool gemm_f16_ok(const GemmArgs& g, int bn, int ofmt, int64_t a_rows_total) {
   if (!g.a_row_exp || !g.b_exp || g.a_rows || g.K <= 0 || g.K % BK2 || (g.Kb > 0 && g.Kb != g.K)) return false;
   if (ofmt == OUT_F16T) {
-    if (bn != 64 && bn != 128) return false;
+    if (bn != 64 && bn != 128 && bn != 256) return false;
     if (!g.c_row_exp || g.ncols[0] + g.ncols[1] > bn || ((uintptr_t)g.c_row_exp & 3)) return false;
   } else if (bn != 256 || (ofmt != OUT_X16 && ofmt != OUT_F32)) {
     return false;
@@ -1500,6 +1523,8 @@ hipError_t launch_gemm_f16(const GemmArgs& g, int bn, int ofmt, int grid_tiles, 
   else if (ofmt == OUT_F16T && bn == 128)
     hipLaunchKernelGGL((k_gemm_big<256, 128, OUT_F16T, false, true>), dim3(grid), dim3(BigCfg<256, 128>::NTHR), 0,
                        s, g, ntn);
+  else if (ofmt == OUT_F16T && bn == 256)
+    hipLaunchKernelGGL((k_gemm_big<256, 256, OUT_F16T, false, true>), dim3(grid), dim3(512), 0, s, g, ntn);
   else if (ofmt == OUT_X16 && bn == 256)
     hipLaunchKernelGGL((k_gemm_big<256, 256, OUT_X16, false, true>), dim3(grid), dim3(512), 0, s, g, ntn);
   else if (ofmt == OUT_F32 && bn == 256)
@@ -1587,7 +1612,8 @@ bool gemm_seg_ok(const GemmArgs& g, const SegArgs& sa, int64_t out_rows) {
     if (!d.A || !d.B[0] || (g.ncols[1] > 0 && !d.B[1]) || d.rank <= 0 || d.rank % BK2) return false;
     if (d.anc_off >= 0 && !d.fac) return false;
     const int kw = sa.f16 ? d.rank : 2 * d.rank;  // A columns per part
-    if (d.akoff1 + kw > d.lda || (g.ncols[1] == 0 && kw > d.lda)) return false;
+    if (d.a_col0 < 0 || d.a_col0 % 8 || d.a_col0 + d.akoff1 + kw > d.lda || (g.ncols[1] == 0 && d.a_col0 + kw > d.lda))
+      return false;
     if (sa.f16 && (!d.a_exp || !d.b_exp[0] || (g.ncols[1] > 0 && !d.b_exp[1]))) return false;
     if (((uintptr_t)d.A & 15) || ((uintptr_t)d.B[0] & 15) || ((uintptr_t)d.B[1] & 15)) return false;
     // 32-bit byte offsets: the weight rows of one factor

@@ -287,6 +287,7 @@ struct GemmArgs {
   // another level; below 0: the tile is skipped) instead of its own
   const int32_t* widx_anc;
   const int32_t* widx_fac;
+  int32_t widx_own1;         // with widx_anc: part 1 uses the tile's own widx
   // fp16 operands (launch_gemm_f16): A row r is scaled by 2^a_row_exp[r],
   // weight matrix i of part 0 by 2^b_exp[i], of part 1 by 2^b_exp1[i] (null:
   // b_exp)
@@ -361,6 +362,7 @@ struct SegDesc {
   int64_t b_stride[2];
   const int32_t* a_exp;    // fp16 segments: row exponents of A
   const int32_t* b_exp[2]; // fp16 segments: exponents of the weight matrices
+  int32_t a_col0;          // first A column of this segment's operand
 };
 struct SegArgs {
   int32_t nseg;
