@@ -903,7 +903,11 @@ lx_status run(const lx_tree_layer& t, int T, int k, const void* x, const int32_t
   LX_LAUNCH("swiglu_reduce", launch_swiglu_reduce(ta, lstream));
   LX_HIP(fj_down.fork());
 
-  // anchor down, once per (token, anchor), on the weighted activation sums
+  // anchor down, once per (token, anchor), on the weighted activation sums.
+  // With the merged down-in of a two-level tree on the same stream, both fp16
+  // products share one persistent launch (below).
+  const bool pair_down = P.f16 && P.dmerge && side == stream;
+  GemmArgs g_anchor_down{};
   {
     const LevelPlan& q = P.lv[0];
     GemmArgs g{};
@@ -925,7 +929,10 @@ lx_status run(const lx_tree_layer& t, int T, int k, const void* x, const int32_t
       g.n_tiles = ba.lv[0].n_tiles[kTabBig];
       if (!gemm_f16_ok(g, 256, OUT_X16, q.rows_max))
         return fail(LX_ERR_UNSUPPORTED, "anchor_down: shape not supported by the fp16 GEMM");
-      LX_LAUNCH("anchor_down", launch_gemm_f16(g, 256, OUT_X16, (int)q.tiles_max[kTabBig], lstream));
+      if (pair_down)
+        g_anchor_down = g;
+      else
+        LX_LAUNCH("anchor_down", launch_gemm_f16(g, 256, OUT_X16, (int)q.tiles_max[kTabBig], lstream));
     } else if (P.lo8) {
       // row = [bf16 hi (f) | fp8 lo (f bytes) | scale words (f / 64)] in 4f bytes
       g.lda = 2 * (int64_t)f;
@@ -980,7 +987,17 @@ lx_status run(const lx_tree_layer& t, int T, int k, const void* x, const int32_t
     g.C = (float*)(W + P.lv[1].v);
     g.ldc = v1.rank + v2.rank;
     g.c_row_exp = (int32_t*)(W + P.lv[1].v_exp);
-    LX_TRY(f16big("lowrank_down_in_merged", g, L, 256, OUT_F16T, qL.rows_max));
+    if (pair_down) {
+      g.tiles = ba.lv[L].tiles[kTabBig];
+      g.n_tiles = ba.lv[L].n_tiles[kTabBig];
+      if (!gemm_f16_ok(g, 256, OUT_F16T, qL.rows_max))
+        return fail(LX_ERR_UNSUPPORTED, "lowrank_down_in_merged: shape not supported by the fp16 GEMM");
+      LX_LAUNCH("anchor_down+lowrank_down_in_merged",
+                launch_gemm_f16_pair(g_anchor_down, (int)P.lv[0].tiles_max[kTabBig], g, OUT_F16T,
+                                     (int)qL.tiles_max[kTabBig], lstream));
+    } else {
+      LX_TRY(f16big("lowrank_down_in_merged", g, L, 256, OUT_F16T, qL.rows_max));
+    }
   }
   for (int l = 1; l <= L && !P.dmerge; ++l) {
     const LevelPlan& q = P.lv[l];

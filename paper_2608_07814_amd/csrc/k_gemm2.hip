@@ -165,10 +165,17 @@ __device__ __forceinline__ f32x16 mfma16(bf16x8 a, bf16x8 b, f32x16 c) {
 // F16: A and W are fp16, both scaled by powers of two (A row r by
 // 2^a_row_exp[r], weight matrix i by 2^b_exp[i]); the epilogue multiplies
 // each output row by 2^-(a_row_exp[row] + b_exp[widx]), an exact rescale.
-template <int BM, int BN, int OUT, bool LO8 = false, bool F16 = false>
-__global__ __launch_bounds__((BigCfg<BM, BN>::NTHR), 1)
-__attribute__((amdgpu_waves_per_eu(BigCfg<BM, BN>::WPE, BigCfg<BM, BN>::WPE)))
-void k_gemm_big(GemmArgs p, int ntn) {
+// OUT2 >= 0: a second, independent product p2 in the same launch (same tile
+// shape and operand precision; its own operands, tile table, columns and
+// output format OUT2). Its work items follow p's in one persistent schedule,
+// so the two products share one tail instead of ending in two.
+template <int OUT>
+struct OutC {
+  static constexpr int value = OUT;
+};
+
+template <int BM, int BN, int OUT, bool LO8, bool F16, int OUT2>
+__device__ __forceinline__ void gemm_big_body(const GemmArgs& p, int ntn, const GemmArgs& p2, int ntn2) {
   static_assert(!LO8 || (BM == 256 && BN == 256), "fp8 lo: 256 x 256 tiles");
   static_assert(!(LO8 && F16), "one precision mode at a time");
   constexpr int NTHR = BigCfg<BM, BN>::NTHR, WGN = BigCfg<BM, BN>::WGN;
@@ -189,6 +196,8 @@ void k_gemm_big(GemmArgs p, int ntn) {
   // fp16 operands: the scale exponents of the tile's A rows (read by the
   // epilogue; loaded when the item starts)
   __shared__ int s_rexp[F16 ? BM : 1];
+  // OUT_F16T: every wavefront's largest magnitude in the tile
+  __shared__ float s_tmax[BigCfg<BM, BN>::NW];
   u16* const sA0 = smem;
   u16* const sB0 = smem + SA;
   u16* const sA1 = smem + SA + SB;
@@ -198,19 +207,19 @@ void k_gemm_big(GemmArgs p, int ntn) {
   // [xbeg, xend); its mx workgroups take every mx-th item of it. The host
   // launches either one workgroup per item or a multiple of 8 workgroups, so
   // every XCD with items has at least one workgroup.
-  const int real = *p.n_tiles * ntn;
+  const int real1 = *p.n_tiles * ntn;
+  const int real = OUT2 >= 0 ? real1 + *p2.n_tiles * ntn2 : real1;
   const int q = real / NXCD, rmd = real % NXCD;
   const int x = blockIdx.x % NXCD;
   const int xbeg = x * q + (x < rmd ? x : rmd);
   const int xend = xbeg + q + (x < rmd ? 1 : 0);
   const int mx = ((int)gridDim.x - x + NXCD - 1) / NXCD;
-  const int ncol = p.ncols[0] + p.ncols[1];
-  const int K = p.K;
-  const int Kb = p.Kb > 0 ? p.Kb : K;
-  const int nk = K / BK2;
-  const u16* __restrict__ Ab = (const u16*)p.A;
 
-  for (int Lg = xbeg + (int)blockIdx.x / NXCD; Lg < xend; Lg += mx) {
+  // One work item of product g (item Li of its own list, ntn_i column tiles
+  // per row tile, output format decltype(oc)::value), inlined once per product
+  // so that each copy reads its own arguments directly.
+  auto item = [&](const GemmArgs& g, const int Li, const int ntn_i, auto oc) __attribute__((always_inline)) {
+    constexpr int O = decltype(oc)::value;
     // The empty asm makes the lane index opaque per item, so the per-lane
     // address arithmetic below is recomputed each item instead of being
     // hoisted out of the item loop (where it would not fit in registers).
@@ -218,37 +227,42 @@ void k_gemm_big(GemmArgs p, int ntn) {
     asm volatile("" : "+v"(tid));
     const int wave = tid >> 6, lane = tid & 63;
     const int wm = wave / WGN, wn = wave % WGN;
-    const int ti = Lg / ntn, nt = Lg % ntn;
+    const int ti = Li / ntn_i, nt = Li % ntn_i;
+    const int ncol = g.ncols[0] + g.ncols[1];
+    const int K = g.K;
+    const int Kb = g.Kb > 0 ? g.Kb : K;
+    const int nk = K / BK2;
+    const u16* __restrict__ Ab = (const u16*)g.A;
 
     // The two weight parts form one column range [0, ncol): column n < ncols[0]
     // is row n of part 0, otherwise row n - ncols[0] of part 1.
-    const TileEntry te = p.tiles[ti];
+    const TileEntry te = g.tiles[ti];
     // weight index: the tile's, or that of the tile node's ancestor at
     // another level (a leaf-row product with an upper level's weights)
     // (widx_own1: that lookup is part 0's only, part 1 takes the tile's own)
     int widx = te.widx;
-    if (p.widx_anc) {
-      const int an = p.widx_anc[te.node];
-      widx = an >= 0 ? p.widx_fac[an] : -1;
+    if (g.widx_anc) {
+      const int an = g.widx_anc[te.node];
+      widx = an >= 0 ? g.widx_fac[an] : -1;
     }
-    int widx1 = p.widx_own1 ? te.widx : widx;
+    int widx1 = g.widx_own1 ? te.widx : widx;
     // a leaf-level tile whose node (or ancestor) has no factor (it is listed
     // for the products that merge the levels above it): nothing to do here;
     // with two weight sources a missing one reads matrix 0 (its outputs are
     // never used)
-    if (widx < 0 && widx1 < 0) continue;
+    if (widx < 0 && widx1 < 0) return;
     if (widx < 0) widx = 0;
     if (widx1 < 0) widx1 = 0;
     const int n0 = nt * BN;
-    const int tpart = n0 < p.ncols[0] ? 0 : 1;
-    const int akoff = p.a_koff[tpart];
+    const int tpart = n0 < g.ncols[0] ? 0 : 1;
+    const int akoff = g.a_koff[tpart];
     if constexpr (F16) {
-      for (int row = tid; row < BM; row += NTHR) s_rexp[row] = p.a_row_exp[te.row0 + (row < te.nrows ? row : te.nrows - 1)];
+      for (int row = tid; row < BM; row += NTHR) s_rexp[row] = g.a_row_exp[te.row0 + (row < te.nrows ? row : te.nrows - 1)];
       asm volatile("" ::: "memory");
       wait_lgkm0();
     }
-    const u16* __restrict__ Bw0 = (const u16*)p.B[0] + (int64_t)widx * p.b_stride[0];
-    const u16* __restrict__ Bw1 = (const u16*)p.B[1] + (int64_t)widx1 * p.b_stride[1];
+    const u16* __restrict__ Bw0 = (const u16*)g.B[0] + (int64_t)widx * g.b_stride[0];
+    const u16* __restrict__ Bw1 = (const u16*)g.B[1] + (int64_t)widx1 * g.b_stride[1];
 
     // Per-thread source offsets (elements, chunk offset folded in) for each
     // 16-byte chunk it loads. LDS slot P = round*256 + tid holds row P>>3,
@@ -261,8 +275,8 @@ void k_gemm_big(GemmArgs p, int ntn) {
       const int row = Ps >> 3;
       const int c = (Ps & 7) ^ swzb(row);
       const int r = row < te.nrows ? row : te.nrows - 1;
-      const int src = p.a_rows ? p.a_rows[te.row0 + r] : te.row0 + r;
-      aoff[j] = (uint32_t)src * (uint32_t)p.lda + (uint32_t)(akoff + c * 8);
+      const int src = g.a_rows ? g.a_rows[te.row0 + r] : te.row0 + r;
+      aoff[j] = (uint32_t)src * (uint32_t)g.lda + (uint32_t)(akoff + c * 8);
     }
     const u16* bptr[B_ROUNDS];
 #pragma unroll
@@ -271,7 +285,7 @@ void k_gemm_big(GemmArgs p, int ntn) {
       const int row = Ps >> 3;
       const int c = (Ps & 7) ^ swzb(row);
       const int n = n0 + row < ncol ? n0 + row : ncol - 1;
-      bptr[j] = (n < p.ncols[0] ? Bw0 + (int64_t)n * Kb : Bw1 + (int64_t)(n - p.ncols[0]) * Kb) + c * 8;
+      bptr[j] = (n < g.ncols[0] ? Bw0 + (int64_t)n * Kb : Bw1 + (int64_t)(n - g.ncols[0]) * Kb) + c * 8;
     }
 
     // Slab kt covers A columns [ka, ka + 64) and weight columns [kb, kb + 64)
@@ -381,10 +395,10 @@ void k_gemm_big(GemmArgs p, int ntn) {
       // 16-byte rounds, one 4-byte scale load), a hi slab ROUNDS.
       constexpr int RLO = 5;
       uint8_t* const L1 = (uint8_t*)sA1;
-      const uint8_t* const Abytes = (const uint8_t*)p.A;
-      const uint32_t apitch = 2 * (uint32_t)p.lda;
-      const uint8_t* const B8 = p.b8 + (int64_t)widx * p.b_stride[0];
-      const uint32_t* const BS = p.bsc + (int64_t)widx * (p.b_stride[0] / 64);
+      const uint8_t* const Abytes = (const uint8_t*)g.A;
+      const uint32_t apitch = 2 * (uint32_t)g.lda;
+      const uint8_t* const B8 = g.b8 + (int64_t)widx * g.b_stride[0];
+      const uint32_t* const BS = g.bsc + (int64_t)widx * (g.b_stride[0] / 64);
       const u16* const Bhi = Bw0;
       // byte offsets (32 bit: the host routes operands of 2^31 or more
       // elements elsewhere) of this thread's hi-slab chunks of B and of its lo
@@ -399,7 +413,7 @@ void k_gemm_big(GemmArgs p, int ntn) {
         const int row = Ps >> 2;
         const int c = (Ps & 3) ^ ((row >> 2) & 3);
         const int r = row < te.nrows ? row : te.nrows - 1;
-        aloff[j] = (uint32_t)(te.row0 + r) * apitch + (uint32_t)p.a_lo8_off + c * 16;
+        aloff[j] = (uint32_t)(te.row0 + r) * apitch + (uint32_t)g.a_lo8_off + c * 16;
         const int n = n0 + row < ncol ? n0 + row : ncol - 1;
         bloff[j] = (uint32_t)n * (uint32_t)Kb + c * 16;
       }
@@ -408,7 +422,7 @@ void k_gemm_big(GemmArgs p, int ntn) {
         const int row = (wave & 3) * 64 + lane;
         if (wave < 4) {
           const int r = row < te.nrows ? row : te.nrows - 1;
-          scoff = (uint32_t)(te.row0 + r) * apitch + (uint32_t)p.a_sc_off;
+          scoff = (uint32_t)(te.row0 + r) * apitch + (uint32_t)g.a_sc_off;
         } else {
           const int n = n0 + row < ncol ? n0 + row : ncol - 1;
           scoff = (uint32_t)n * (uint32_t)(Kb / BK2) * 4;
@@ -525,7 +539,7 @@ void k_gemm_big(GemmArgs p, int ntn) {
 #undef LX_FRAG
 #undef LX_MFMAS
 
-    // Epilogue. 32x32 accumulator layout: lane holds column (lane & 31) and
+    // Epilogue (output format O). 32x32 accumulator layout: lane holds column (lane & 31) and
     // rows 8*(i/4) + 4*(lane/32) + (i%4) for i = 0..15. Each wavefront writes
     // its 32 x WN block of one mi into its own LDS region (row pitch WN + 4
     // floats), then reads it back as 4 consecutive columns per lane. All
@@ -538,23 +552,22 @@ void k_gemm_big(GemmArgs p, int ntn) {
       float* const ep = (float*)smem + wave * (32 * PITCH);
       const int c4 = (lane % LPR) * 4;
       const int col = n0 + wn * WN + c4;
-      const int bexp = F16 ? (tpart ? (p.b_exp1 ? p.b_exp1 : p.b_exp)[widx1] : p.b_exp[widx]) : 0;
+      const int bexp = F16 ? (tpart ? (g.b_exp1 ? g.b_exp1 : g.b_exp)[widx1] : g.b_exp[widx]) : 0;
       // OUT_F16T: one power-of-two scale 2^tsh for the whole tile (its rows
       // are whole rows), from the largest magnitude over every wavefront's
       // block; with fp16 operands the accumulators already carry 2^(a_row_exp
       // + bexp), which the row exponents add
       int tsh = 0;
-      if constexpr (OUT == OUT_F16T) {
-        __shared__ float s_tmax[BigCfg<BM, BN>::NW];
+      if constexpr (O == OUT_F16T) {
         // fp16 operands, a tile over both parts: part 1's columns carry its
         // own weight scale; bring them to part 0's (exact) so that one row
         // exponent holds for the whole row
         if constexpr (F16) {
-          if (tpart == 0 && n0 + BN > p.ncols[0] && p.ncols[1] > 0) {
-            const int d1 = bexp - (p.b_exp1 ? p.b_exp1 : p.b_exp)[widx1];
+          if (tpart == 0 && n0 + BN > g.ncols[0] && g.ncols[1] > 0) {
+            const int d1 = bexp - (g.b_exp1 ? g.b_exp1 : g.b_exp)[widx1];
 #pragma unroll
             for (int ni = 0; ni < NI; ++ni) {
-              const bool in1 = n0 + wn * WN + ni * 32 + (lane & 31) >= p.ncols[0];
+              const bool in1 = n0 + wn * WN + ni * 32 + (lane & 31) >= g.ncols[0];
 #pragma unroll
               for (int mi = 0; mi < MI; ++mi)
 #pragma unroll
@@ -582,7 +595,7 @@ void k_gemm_big(GemmArgs p, int ntn) {
           tsh = tsh < -100 ? -100 : tsh > 100 ? 100 : tsh;
         }
       }
-      X16Rows xr(p.C, p.ldc, te.row0 + wm * WM + lane / LPR, RPP, col);
+      X16Rows xr(g.C, g.ldc, te.row0 + wm * WM + lane / LPR, RPP, col);
       // full tiles store without per-row checks (a separate, branch-free copy)
       auto emit = [&](auto check) {
 #pragma unroll
@@ -598,16 +611,16 @@ void k_gemm_big(GemmArgs p, int ntn) {
             float4 v = *(const float4*)&ep[rr * PITCH + c4];
             const int r = wm * WM + mi * 32 + rr;
             const bool ok = !decltype(check)::value || (r < te.nrows && col < ncol);
-            if constexpr (F16 && OUT != OUT_F16T) {
+            if constexpr (F16 && O != OUT_F16T) {
               if (ok) {
                 const int e = -(s_rexp[r] + bexp);
                 v = make_float4(ldexpf(v.x, e), ldexpf(v.y, e), ldexpf(v.z, e), ldexpf(v.w, e));
               }
             }
-            if constexpr (OUT == OUT_X16) {
+            if constexpr (O == OUT_X16) {
               if (ok) xr.store(v);
               xr.next();
-            } else if constexpr (OUT == OUT_F16T) {
+            } else if constexpr (O == OUT_F16T) {
               if (!ok) continue;
               typedef _Float16 h4 __attribute__((ext_vector_type(4)));
               h4 q;
@@ -615,16 +628,16 @@ void k_gemm_big(GemmArgs p, int ntn) {
               q[1] = (_Float16)ldexpf(v.y, tsh);
               q[2] = (_Float16)ldexpf(v.z, tsh);
               q[3] = (_Float16)ldexpf(v.w, tsh);
-              *(h4*)((_Float16*)p.C + (int64_t)(te.row0 + r) * p.ldc + col) = q;
+              *(h4*)((_Float16*)g.C + (int64_t)(te.row0 + r) * g.ldc + col) = q;
               if (wn == 0 && lane % LPR == 0)
-                p.c_row_exp[te.row0 + r] = tsh + (F16 ? s_rexp[r] + bexp : 0);
-            } else if constexpr (OUT == OUT_HILO) {
+                g.c_row_exp[te.row0 + r] = tsh + (F16 ? s_rexp[r] + bexp : 0);
+            } else if constexpr (O == OUT_HILO) {
               if (!ok) continue;
               // part p, local column c -> hi at base_p + c, lo at base_p + ncols[p] + c
-              const int pp = col < p.ncols[0] ? 0 : 1;
-              const int c = pp ? col - p.ncols[0] : col;
-              const int hi_col = (pp ? 2 * p.ncols[0] : 0) + c;
-              const int lo_col = hi_col + p.ncols[pp];
+              const int pp = col < g.ncols[0] ? 0 : 1;
+              const int c = pp ? col - g.ncols[0] : col;
+              const int hi_col = (pp ? 2 * g.ncols[0] : 0) + c;
+              const int lo_col = hi_col + g.ncols[pp];
               bf16x4 h, l;
               h[0] = (__bf16)v.x;
               h[1] = (__bf16)v.y;
@@ -634,12 +647,12 @@ void k_gemm_big(GemmArgs p, int ntn) {
               l[1] = (__bf16)(v.y - (float)h[1]);
               l[2] = (__bf16)(v.z - (float)h[2]);
               l[3] = (__bf16)(v.w - (float)h[3]);
-              __bf16* const rowp = (__bf16*)p.C + (int64_t)(te.row0 + r) * p.ldc;
+              __bf16* const rowp = (__bf16*)g.C + (int64_t)(te.row0 + r) * g.ldc;
               *(bf16x4*)(rowp + hi_col) = h;
               *(bf16x4*)(rowp + lo_col) = l;
             } else {
               if (!ok) continue;
-              *(float4*)(p.C + (int64_t)(te.row0 + r) * p.ldc + col) = v;
+              *(float4*)(g.C + (int64_t)(te.row0 + r) * g.ldc + col) = v;
             }
           }
         }
@@ -650,7 +663,33 @@ void k_gemm_big(GemmArgs p, int ntn) {
         emit(std::true_type{});
     }
     bar();  // the next item's loads overwrite the epilogue's LDS
+  };
+  for (int Lg = xbeg + (int)blockIdx.x / NXCD; Lg < xend; Lg += mx) {
+    // items [0, real1) are p's, the rest p2's
+    if constexpr (OUT2 >= 0) {
+      if (Lg >= real1)
+        item(p2, Lg - real1, ntn2, OutC<OUT2>{});
+      else
+        item(p, Lg, ntn, OutC<OUT>{});
+    } else {
+      item(p, Lg, ntn, OutC<OUT>{});
+    }
   }
+}
+
+template <int BM, int BN, int OUT, bool LO8 = false, bool F16 = false>
+__global__ __launch_bounds__((BigCfg<BM, BN>::NTHR), 1)
+__attribute__((amdgpu_waves_per_eu(BigCfg<BM, BN>::WPE, BigCfg<BM, BN>::WPE)))
+void k_gemm_big(GemmArgs p, int ntn) {
+  gemm_big_body<BM, BN, OUT, LO8, F16, -1>(p, ntn, p, 0);
+}
+
+// Two products in one persistent launch (see gemm_big_body).
+template <int BM, int BN, int OUT, int OUT2, bool F16>
+__global__ __launch_bounds__((BigCfg<BM, BN>::NTHR), 1)
+__attribute__((amdgpu_waves_per_eu(BigCfg<BM, BN>::WPE, BigCfg<BM, BN>::WPE)))
+void k_gemm_big2(GemmArgs p, int ntn, GemmArgs p2, int ntn2) {
+  gemm_big_body<BM, BN, OUT, false, F16, OUT2>(p, ntn, p2, ntn2);
 }
 
 // ---------------------------------------------------------------- segmented
@@ -1529,6 +1568,26 @@ hipError_t launch_gemm_f16(const GemmArgs& g, int bn, int ofmt, int grid_tiles, 
     hipLaunchKernelGGL((k_gemm_big<256, 256, OUT_X16, false, true>), dim3(grid), dim3(512), 0, s, g, ntn);
   else if (ofmt == OUT_F32 && bn == 256)
     hipLaunchKernelGGL((k_gemm_big<256, 256, OUT_F32, false, true>), dim3(grid), dim3(512), 0, s, g, ntn);
+  else
+    return hipErrorInvalidValue;
+  return hipGetLastError();
+}
+
+hipError_t launch_gemm_f16_pair(const GemmArgs& g0, int grid_tiles0, const GemmArgs& g1, int ofmt1,
+                                int grid_tiles1, hipStream_t s) {
+  if (!x16_shape_ok(g0, OUT_X16) || !x16_shape_ok(g1, ofmt1)) return hipErrorInvalidValue;
+  const int ntn0 = (g0.ncols[0] + g0.ncols[1] + 255) / 256;
+  const int ntn1 = (g1.ncols[0] + g1.ncols[1] + 255) / 256;
+  int grid = grid_tiles0 * ntn0 + grid_tiles1 * ntn1;
+  if (grid <= 0) return hipSuccess;
+  const int cap = grid_cap();
+  if (grid > cap) grid = cap;
+  if (ofmt1 == OUT_F16T)
+    hipLaunchKernelGGL((k_gemm_big2<256, 256, OUT_X16, OUT_F16T, true>), dim3(grid), dim3(512), 0, s, g0, ntn0, g1,
+                       ntn1);
+  else if (ofmt1 == OUT_X16)
+    hipLaunchKernelGGL((k_gemm_big2<256, 256, OUT_X16, OUT_X16, true>), dim3(grid), dim3(512), 0, s, g0, ntn0, g1,
+                       ntn1);
   else
     return hipErrorInvalidValue;
   return hipGetLastError();

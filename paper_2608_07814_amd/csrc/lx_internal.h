@@ -325,6 +325,12 @@ hipError_t launch_gemm_lo8(const GemmArgs& g, int ofmt, int grid_tiles, hipStrea
 // exponents (OUT_F16T).
 bool gemm_f16_ok(const GemmArgs& g, int bn, int ofmt, int64_t a_rows_total);
 hipError_t launch_gemm_f16(const GemmArgs& g, int bn, int ofmt, int grid_tiles, hipStream_t s);
+// Two independent fp16 products with 256 x 256 tiles in one persistent launch
+// (g0's work items, then g1's: one schedule and one tail for both); output
+// formats x16 for g0 and x16 or OUT_F16T for g1, each product as accepted by
+// gemm_f16_ok.
+hipError_t launch_gemm_f16_pair(const GemmArgs& g0, int grid_tiles0, const GemmArgs& g1, int ofmt1,
+                                int grid_tiles1, hipStream_t s);
 // Weights [n][per] bf16 -> fp16 [n][per] scaled per matrix i by 2^exps[i]
 // (exps[i] puts the matrix's largest magnitude in [2^14, 2^15); 0 for an
 // all-zero matrix).
