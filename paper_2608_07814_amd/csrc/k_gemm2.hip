@@ -733,7 +733,11 @@ void k_gemm_seg(GemmArgs p, SegArgs sg, int ntn) {
   // item's may still be read)
   __shared__ __attribute__((aligned(16))) int s_e[F16 ? 2 : 1][F16 ? kSegMax : 1][BM];
 
-  const int real = *p.n_tiles * ntn;
+  // work item = (row tile, group of ngrp consecutive column tiles of one
+  // part): the tile's setup (weight indices, row exponents) is done once per
+  // group, then each column tile of the group runs its K loop and epilogue
+  const int ngrp = sg.ngrp, nsg = ntn / ngrp;
+  const int real = *p.n_tiles * nsg;
   const int q = real / NXCD, rmd = real % NXCD;
   const int x = blockIdx.x % NXCD;
   const int xbeg = x * q + (x < rmd ? x : rmd);
@@ -761,9 +765,9 @@ void k_gemm_seg(GemmArgs p, SegArgs sg, int ntn) {
   uint32_t aoff[A_ROUNDS], boff[B_ROUNDS];
 
   auto setup = [&](int L_) {
-    const int ti = L_ / ntn, nt = L_ % ntn;
+    const int ti = L_ / nsg, grp = L_ % nsg;
     te = p.tiles[ti];
-    n0 = nt * BN;
+    n0 = grp * ngrp * BN;
     tpart = n0 < p.ncols[0] ? 0 : 1;
     nk = 0;
     cur = -1;
@@ -929,6 +933,7 @@ void k_gemm_seg(GemmArgs p, SegArgs sg, int ntn) {
   // once). Slabs 0 and 1 of an item are issued before the previous item's
   // epilogue.
   setup(Lg);
+  int gi = 0;  // column tile within the item's group
   for (int i = 0; i < 2 && i < nk; ++i) issue(i ? sA1 : sA0, i ? sB1 : sB0, i);
   while (true) {
     asm volatile("" : "+v"(tid));
@@ -965,14 +970,24 @@ void k_gemm_seg(GemmArgs p, SegArgs sg, int ntn) {
       if (aseg >= 0) rescale(eb, aseg, -1);
     }
 
-    // every wavefront is done with both stages: load the next item's first
-    // slabs, then store this item's outputs
+    // every wavefront is done with both stages: load the next column tile's
+    // first slabs (the group's next one, or the next item's first), then
+    // store this one's outputs
     const int row0 = te.row0, nrows = te.nrows, en0 = n0;
-    const int nLg = Lg + mx;
+    int nLg = Lg, ngi = gi + 1;
+    if (ngi == ngrp) {
+      ngi = 0;
+      nLg = Lg + mx;
+    }
     const bool more = nLg < xend;
     if (more) {
-      if constexpr (F16) eb ^= 1;
-      setup(nLg);
+      if (ngi == 0) {
+        if constexpr (F16) eb ^= 1;
+        setup(nLg);
+      } else {
+        n0 += BN;  // same rows, weights and exponents
+        cur = -1;
+      }
       for (int i = 0; i < 2 && i < nk; ++i) issue(i ? sA1 : sA0, i ? sB1 : sB0, i);
     }
 
@@ -1011,6 +1026,7 @@ void k_gemm_seg(GemmArgs p, SegArgs sg, int ntn) {
     }
     if (!more) break;
     Lg = nLg;
+    gi = ngi;
     cur = -1;  // the next issue recomputes the operand offsets (not kept live across the epilogue)
   }
 #undef LX_SCOMPUTE
@@ -1681,9 +1697,18 @@ bool gemm_seg_ok(const GemmArgs& g, const SegArgs& sa, int64_t out_rows) {
   return true;
 }
 
-hipError_t launch_gemm_seg(const GemmArgs& g, const SegArgs& sa, int grid_tiles, hipStream_t s) {
+hipError_t launch_gemm_seg(const GemmArgs& g, const SegArgs& sa_in, int grid_tiles, hipStream_t s) {
   const int ntn = (g.ncols[0] + g.ncols[1] + 255) / 256;
-  int grid = grid_tiles * ntn;
+  // column tiles per work item: 4 (or 2) when every part is a whole number of
+  // such groups, so a group never straddles the parts
+  SegArgs sa = sa_in;
+  sa.ngrp = 1;
+  for (const int gsz : {4, 2})
+    if (g.ncols[0] % (gsz * 256) == 0 && g.ncols[1] % (gsz * 256) == 0) {
+      sa.ngrp = gsz;
+      break;
+    }
+  int grid = grid_tiles * (ntn / sa.ngrp);
   if (grid <= 0) return hipSuccess;
   const int cap = grid_cap();
   if (grid > cap) grid = cap;

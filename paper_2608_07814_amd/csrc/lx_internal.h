@@ -373,6 +373,7 @@ struct SegDesc {
 struct SegArgs {
   int32_t nseg;
   int32_t f16;             // fp16 segments
+  int32_t ngrp;            // consecutive column tiles per work item (set by launch_gemm_seg)
   const int32_t* anc;      // [(L + 1) * E] ancestor of each expert per level
   SegDesc s[LX_MAX_LEVELS];
 };
