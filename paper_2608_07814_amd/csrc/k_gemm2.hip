@@ -203,16 +203,19 @@ __device__ __forceinline__ void gemm_big_body(const GemmArgs& p, int ntn, const 
   u16* const sA1 = smem + SA + SB;
   u16* const sB1 = smem + 2 * SA + SB;
 
-  // Work items (tile, n-tile) [0, real): XCD x owns the contiguous range
-  // [xbeg, xend); its mx workgroups take every mx-th item of it. The host
-  // launches either one workgroup per item or a multiple of 8 workgroups, so
-  // every XCD with items has at least one workgroup.
-  const int real1 = *p.n_tiles * ntn;
-  const int real = OUT2 >= 0 ? real1 + *p2.n_tiles * ntn2 : real1;
-  const int q = real / NXCD, rmd = real % NXCD;
+  // Work items (tile, n-tile) of each product: XCD x owns a contiguous range
+  // of p's items and one of p2's (each product split evenly over the XCDs, the
+  // remainders from opposite ends so that no XCD gets two extra items); its mx
+  // workgroups take every mx-th item of [its p items, then its p2 items]. The
+  // host launches either one workgroup per item or a multiple of 8
+  // workgroups, so every XCD with items has at least one workgroup.
+  const int n1 = *p.n_tiles * ntn;
+  const int n2 = OUT2 >= 0 ? *p2.n_tiles * ntn2 : 0;
   const int x = blockIdx.x % NXCD;
-  const int xbeg = x * q + (x < rmd ? x : rmd);
-  const int xend = xbeg + q + (x < rmd ? 1 : 0);
+  const int q1 = n1 / NXCD, r1 = n1 % NXCD;
+  const int b1 = x * q1 + (x < r1 ? x : r1), c1 = q1 + (x < r1 ? 1 : 0);
+  const int q2 = n2 / NXCD, r2 = n2 % NXCD, xr = NXCD - 1 - x;
+  const int b2 = xr * q2 + (xr < r2 ? xr : r2), c2 = q2 + (xr < r2 ? 1 : 0);
   const int mx = ((int)gridDim.x - x + NXCD - 1) / NXCD;
 
   // One work item of product g (item Li of its own list, ntn_i column tiles
@@ -227,7 +230,19 @@ __device__ __forceinline__ void gemm_big_body(const GemmArgs& p, int ntn, const 
     asm volatile("" : "+v"(tid));
     const int wave = tid >> 6, lane = tid & 63;
     const int wm = wave / WGN, wn = wave % WGN;
-    const int ti = Li / ntn_i, nt = Li % ntn_i;
+    // item -> (row tile, column tile): with more than 8 column tiles, in bands
+    // of 8 (band-major), so the 32 workgroups of an XCD that run together
+    // cover 4 row tiles x 8 column tiles and each weight slab is shared by 4
+    int ti, nt;
+    if (ntn_i > 8 && ntn_i % 8 == 0) {
+      const int per_band = *g.n_tiles * 8;
+      const int band = Li / per_band, rem = Li - band * per_band;
+      ti = rem >> 3;
+      nt = band * 8 + (rem & 7);
+    } else {
+      ti = Li / ntn_i;
+      nt = Li % ntn_i;
+    }
     const int ncol = g.ncols[0] + g.ncols[1];
     const int K = g.K;
     const int Kb = g.Kb > 0 ? g.Kb : K;
@@ -664,15 +679,14 @@ __device__ __forceinline__ void gemm_big_body(const GemmArgs& p, int ntn, const 
     }
     bar();  // the next item's loads overwrite the epilogue's LDS
   };
-  for (int Lg = xbeg + (int)blockIdx.x / NXCD; Lg < xend; Lg += mx) {
-    // items [0, real1) are p's, the rest p2's
+  for (int j = (int)blockIdx.x / NXCD; j < c1 + c2; j += mx) {
     if constexpr (OUT2 >= 0) {
-      if (Lg >= real1)
-        item(p2, Lg - real1, ntn2, OutC<OUT2>{});
+      if (j >= c1)
+        item(p2, b2 + j - c1, ntn2, OutC<OUT2>{});
       else
-        item(p, Lg, ntn, OutC<OUT>{});
+        item(p, b1 + j, ntn, OutC<OUT>{});
     } else {
-      item(p, Lg, ntn, OutC<OUT>{});
+      item(p, b1 + j, ntn, OutC<OUT>{});
     }
   }
 }

@@ -545,7 +545,7 @@ __global__ __launch_bounds__(kFastThr) void k_combine_fast(TokenArgs a) {
 // x16 rows, CPT (8 or 16) columns per thread: 16-byte mantissa loads and
 // one 2- or 4-byte exponent load per row (a fraction of the load
 // instructions of 4 columns per thread); otherwise as k_combine_fast.
-template <int NL, int CPT>
+template <int NL, int CPT, bool MERGED>
 __global__ __launch_bounds__(kFastThr) void k_combine_x16w(TokenArgs a) {
   constexpr int NG = CPT / 4;  // 4-value groups per thread
   const int t = blockIdx.x, k = a.k, d = a.d;
@@ -554,7 +554,9 @@ __global__ __launch_bounds__(kFastThr) void k_combine_x16w(TokenArgs a) {
   int row[NL + 1][kFastK], fl[NL + 1][kFastK];
   float w[kFastK];
   token_meta_fast<NL>(a, t, row, fl, w);
-  const bool merged = a.merged != 0;
+  // (a.merged, as a template argument: the intermediate levels' rows are
+  // never loaded and take no registers)
+  constexpr bool merged = MERGED;
   const int64_t rb = x16_row_bytes(d);
   uint4 mv[NL + 1][kFastK][NG / 2];
   uint32_t ev[NL + 1][kFastK];
@@ -679,11 +681,13 @@ hipError_t launch_combine(const TokenArgs& a, hipStream_t s) {
     const int thr = fast_threads(a.d * 4 / CPT, a.T);
     const dim3 grid(a.T, (a.d / CPT + thr - 1) / thr);
     if (a.L == 0)
-      hipLaunchKernelGGL((k_combine_x16w<0, CPT>), grid, dim3(thr), 0, s, a);
+      hipLaunchKernelGGL((k_combine_x16w<0, CPT, false>), grid, dim3(thr), 0, s, a);
     else if (a.L == 1)
-      hipLaunchKernelGGL((k_combine_x16w<1, CPT>), grid, dim3(thr), 0, s, a);
+      hipLaunchKernelGGL((k_combine_x16w<1, CPT, false>), grid, dim3(thr), 0, s, a);
+    else if (a.merged)
+      hipLaunchKernelGGL((k_combine_x16w<2, CPT, true>), grid, dim3(thr), 0, s, a);
     else
-      hipLaunchKernelGGL((k_combine_x16w<2, CPT>), grid, dim3(thr), 0, s, a);
+      hipLaunchKernelGGL((k_combine_x16w<2, CPT, false>), grid, dim3(thr), 0, s, a);
     return hipGetLastError();
   }
   if (a.k <= kFastK && a.L <= kFastL && fmt >= 0) {
