@@ -172,7 +172,7 @@ def clone_layer(dl):
     """Independent device copy of a DeviceLayer's weights (same routing structure)."""
     import dataclasses
     from paper_2608_07814_amd import lorex as lx
-    names = ("a_gate", "b_gate", "a_up", "b_up", "a_down", "b_down") + lx.FACTOR_F16
+    names = ("a_gate", "b_gate", "a_up", "b_up", "a_down", "b_down") + lx.FACTOR_F16 + lx.FACTOR_PAD
     levels = [dataclasses.replace(lv, **{n: getattr(lv, n).clone() for n in names if getattr(lv, n) is not None})
               for lv in dl.levels]
     copies = {n: getattr(dl, n).clone() for n in ("anchor_down_f8", "anchor_down_f8_scale", "anchor_down_f16",

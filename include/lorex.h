@@ -128,6 +128,17 @@ typedef struct lx_level {
   const int32_t* a_down_f16_exp;     /* [n_factors] */
   const void* b_down_f16;            /* [n_factors][rank][f] */
   const int32_t* b_down_f16_exp;     /* [n_factors] */
+  /* Padded rank of the fp16 copies (0: rank). The fp16 path needs the rank
+   * to be a multiple of 64; for another rank the copies can be made at
+   * rank_f16 = rank rounded up to a multiple of 64 (lx_convert_f16_padded),
+   * with zero columns (a_*_f16: [n_factors][f or d][rank_f16]) or zero rows
+   * (b_down_f16: [n_factors][rank_f16][f]) beyond rank, together with bf16
+   * copies of b_gate and b_up padded with zero rows (lx_pad_bf16). The
+   * padding holds exact zeros, so the products equal those of rank `rank`.
+   * rank_f16 > rank requires both pad copies; at most 128. */
+  int32_t rank_f16;
+  const void* b_gate_pad;            /* [n_factors][rank_f16][d] bf16 */
+  const void* b_up_pad;              /* [n_factors][rank_f16][d] bf16 */
 } lx_level;
 
 /* A BTExperts tree (Sec. 5): dense anchors, then n_levels correction levels;
@@ -186,6 +197,11 @@ typedef struct lx_flat_layer {
   const int32_t* a_down_f16_exp;
   const void* b_down_f16;
   const int32_t* b_down_f16_exp;
+  /* padded rank of the fp16 copies and the padded bf16 copies of b_gate and
+   * b_up, as rank_f16, b_gate_pad and b_up_pad of lx_level */
+  int32_t r_f16;
+  const void* b_gate_pad;              /* [M][r_f16][d] */
+  const void* b_up_pad;                /* [M][r_f16][d] */
 } lx_flat_layer;
 
 /* An uncompressed MoE layer (every expert stored in full): the comparator the
@@ -300,8 +316,9 @@ lx_status lx_quantize_f8(const void* w, int32_t n, int32_t rows, int32_t cols, v
  * the fp8 copy (if any) or the pair. With fp16 copies of a level's factors
  * too (lx_level), that level's correction products run the same way: its
  * activation sums as above, its rank-r intermediates fp16 with one
- * power-of-two scale per 256-row tile (rank a multiple of 64, at most 128;
- * levels with at most 64 rows per node keep the pair).
+ * power-of-two scale per 256-row tile (rank a multiple of 64, at most 128, or
+ * copies padded to such a rank: lx_convert_f16_padded; levels with at most 64
+ * rows per node keep the pair).
  *
  * w [n][rows][cols] bf16 -> w_f16 [n][rows][cols] fp16 equal to w * 2^e_i
  * for matrix i, rounded to nearest even, with exps[i] = e_i chosen so that
@@ -311,6 +328,25 @@ lx_status lx_quantize_f8(const void* w, int32_t n, int32_t rows, int32_t cols, v
  * (LX_ERR_INVALID_ARGUMENT). Asynchronous on `stream`. */
 lx_status lx_convert_f16(const void* w, int32_t n, int32_t rows, int32_t cols, void* w_f16, int32_t* exps,
                          void* stream);
+
+/* lx_convert_f16 into a larger zero-padded layout, for the factor copies of
+ * a level whose rank is not a multiple of 64 (lx_level::rank_f16).
+ *
+ * w [n][rows][cols] bf16 -> w_f16 [n][rows_out][cols_out] fp16: element
+ * (i, r, c) is w[i][r][c] * 2^exps[i] for r < rows and c < cols (the same
+ * values and exponents as lx_convert_f16) and 0 elsewhere. rows_out >= rows,
+ * cols_out >= cols, all positive (LX_ERR_INVALID_ARGUMENT); pointers as in
+ * lx_convert_f16. Asynchronous on `stream`. */
+lx_status lx_convert_f16_padded(const void* w, int32_t n, int32_t rows, int32_t cols, int32_t rows_out,
+                                int32_t cols_out, void* w_f16, int32_t* exps, void* stream);
+
+/* Zero-padded bf16 copy (the padded b_gate and b_up of lx_level::rank_f16):
+ * w [n][rows][cols] bf16 -> w_out [n][rows_out][cols_out] bf16, element
+ * (i, r, c) = w[i][r][c] for r < rows and c < cols, 0 elsewhere. rows_out >=
+ * rows, cols_out >= cols, all positive (LX_ERR_INVALID_ARGUMENT); w_out
+ * 16-byte aligned. Asynchronous on `stream`. */
+lx_status lx_pad_bf16(const void* w, int32_t n, int32_t rows, int32_t cols, int32_t rows_out, int32_t cols_out,
+                      void* w_out, void* stream);
 
 /* The model's unchanged top-k router on the GPU (Sec. 3 "Stage 1" and Fig.
  * overview: compression leaves the router as it is and every expert

@@ -94,6 +94,12 @@ struct Timed {
 // --------------------------------------------------------------- planning
 size_t align_up(size_t x) { return (x + 255) & ~size_t(255); }
 
+// Rank of a level's fp16 factor copies (padded to a multiple of 64 where the
+// copies were made that way) and the bf16 input factors the fp16 path reads.
+int rank16(const lx_level& v) { return v.rank_f16 > 0 ? v.rank_f16 : v.rank; }
+const void* b_gate16(const lx_level& v) { return rank16(v) > v.rank ? v.b_gate_pad : v.b_gate; }
+const void* b_up16(const lx_level& v) { return rank16(v) > v.rank ? v.b_up_pad : v.b_up; }
+
 struct LevelPlan {
   int N = 0, rank = 0, nfac = 0;
   int bm[kNumTab] = {};
@@ -205,8 +211,8 @@ Plan make_plan(const lx_tree_layer& t, int T, int k) {
       for (int l = 1; l <= p.L && p.cf16; ++l) {
         const lx_level& v = t.levels[l - 1];
         if (v.n_factors == 0) continue;
-        p.cf16 = v.a_gate_f16 && v.a_up_f16 && v.a_down_f16 && v.b_down_f16 && v.rank % 64 == 0 &&
-                 2 * v.rank <= 256 && !p.skinny[l];
+        p.cf16 = v.a_gate_f16 && v.a_up_f16 && v.a_down_f16 && v.b_down_f16 && rank16(v) % 64 == 0 &&
+                 2 * rank16(v) <= 256 && !p.skinny[l];
       }
     }
     // (batches of at most 64 tokens always run their fast levels on the
@@ -215,7 +221,7 @@ Plan make_plan(const lx_tree_layer& t, int T, int k) {
     for (int l = 1; l <= p.L && p.merged; ++l)
       p.merged = p.fast[l] && !p.skinny[l] && t.levels[l - 1].rank % 64 == 0;
     p.dmerge = p.cf16 && p.merged && p.L == 2 && t.levels[0].n_factors > 0 && t.levels[1].n_factors > 0 &&
-               t.levels[0].rank + t.levels[1].rank <= 256;
+               rank16(t.levels[0]) + rank16(t.levels[1]) <= 256;
   }
   p.flags = take(16);  // first: lx_read_device_status reads offset 0
   p.anc = take((size_t)(p.L + 1) * p.E * 4);
@@ -256,14 +262,16 @@ Plan make_plan(const lx_tree_layer& t, int T, int k) {
     const bool inter = p.merged && l > 0 && l < p.L;
     const bool leafm = p.merged && l == p.L;
     q.gu = take((work && !inter) || leafm ? R * 2 * p.f * 4 : 0);
-    q.z = take(l > 0 && work ? R * 2 * q.rank * 4 : 0);
+    // z and v rows: bf16 (hi, lo) pairs of the rank, or fp16 at the copies' rank
+    const size_t rf = l == 0 ? 0 : (size_t)rank16(t.levels[l - 1]);
+    q.z = take(l > 0 && work ? R * std::max<size_t>(2 * (size_t)q.rank * 4, 2 * rf * 2) : 0);
     q.hbar = take((work && !inter) || leafm ? R * p.f * 4 : 0);
     // merged trees: an intermediate level's down-in product runs on the leaf
     // rows (by linearity, the sum over a row's leaf rows of B_down h_leaf is
     // B_down of the row's sum), so its v has one row per leaf row
     const size_t Rv = inter ? (size_t)T * std::min(k, t.E) : R;
-    const size_t vrow = p.dmerge && l == 1 ? std::max<size_t>(q.rank * 4, (size_t)(q.rank + t.levels[1].rank) * 2)
-                                           : (size_t)q.rank * 4;
+    const size_t vrow = p.dmerge && l == 1 ? std::max<size_t>(q.rank * 4, (rf + rank16(t.levels[1])) * 2)
+                                           : std::max<size_t>((size_t)q.rank * 4, rf * 2);
     q.v = take(l > 0 && work ? Rv * vrow : 0);
     q.y = take((work && !inter) || leafm ? R * p.d * 4 : 0);
     if (p.cf16 && l > 0) {
@@ -337,6 +345,15 @@ lx_status check_layer(const lx_tree_layer* t) {
     if (nset != 0 && nset != 8)
       return fail(LX_ERR_INVALID_ARGUMENT, "fp16 factor copies and their exponents: all eight or none");
     if (nset && t->dtype != LX_BF16) return fail(LX_ERR_UNSUPPORTED, "fp16 factor copies need a bf16 layer");
+    if (v.rank_f16 != 0) {
+      if (v.rank_f16 < v.rank || v.rank_f16 % 64 || v.rank_f16 > 128)
+        return fail(LX_ERR_INVALID_ARGUMENT, "rank_f16 must be 0 or a multiple of 64 in [rank, 128]");
+      if (!nset) return fail(LX_ERR_INVALID_ARGUMENT, "rank_f16 is set without fp16 factor copies");
+    }
+    if (rank16(v) > v.rank) {
+      if (!v.b_gate_pad || !v.b_up_pad || !aligned(v.b_gate_pad, 16) || !aligned(v.b_up_pad, 16))
+        return fail(LX_ERR_INVALID_ARGUMENT, "rank_f16 > rank needs b_gate_pad and b_up_pad, 16-byte aligned");
+    }
   }
   return LX_OK;
 }
@@ -385,6 +402,9 @@ lx_tree_layer flat_to_tree(const lx_flat_layer& F) {
   v.a_down_f16_exp = F.a_down_f16_exp;
   v.b_down_f16 = F.b_down_f16;
   v.b_down_f16_exp = F.b_down_f16_exp;
+  v.rank_f16 = F.r_f16;
+  v.b_gate_pad = F.b_gate_pad;
+  v.b_up_pad = F.b_up_pad;
   return t;
 }
 
@@ -735,9 +755,16 @@ lx_status run(const lx_tree_layer& t, int T, int k, const void* x, const int32_t
     g.K = d;
     g.C = (float*)(W + q.z);
     if (fast[l] && P.cf16) {
-      g.ldc = 2 * (int64_t)r;  // [gate | up], fp16, one scale per tile
+      // [gate | up], fp16, one scale per tile, at the copies' rank (padded
+      // factor rows give zero columns)
+      const int rf = rank16(v);
+      g.B[0] = b_gate16(v);
+      g.B[1] = b_up16(v);
+      g.b_stride[0] = g.b_stride[1] = (int64_t)rf * d;
+      g.ncols[0] = g.ncols[1] = rf;
+      g.ldc = 2 * (int64_t)rf;
       g.c_row_exp = (int32_t*)(W + q.z_exp);
-      LX_TRY(big(kLowIn[l], g, l, kBigBM, 2 * r <= 128 ? 128 : 256, OUT_F16T, T));
+      LX_TRY(big(kLowIn[l], g, l, kBigBM, 2 * rf <= 128 ? 128 : 256, OUT_F16T, T));
     } else if (fast[l]) {
       g.ldc = 4 * (int64_t)r;  // [gate hi | gate lo | up hi | up lo], bf16
       LX_TRY(big(kLowIn[l], g, l, kBigBM, 2 * r <= 128 ? 128 : 256, OUT_HILO, T));
@@ -780,7 +807,8 @@ lx_status run(const lx_tree_layer& t, int T, int k, const void* x, const int32_t
       const lx_level& v = t.levels[l - 1];
       if (v.n_factors == 0) continue;
       const LevelPlan& q = P.lv[l];
-      const int r = v.rank;
+      // fp16: the copies' rank (padded columns of A and rows of B are zero)
+      const int r = P.cf16 ? rank16(v) : v.rank;
       SegDesc& sd = sa.s[sa.nseg++];
       sd.rank = r;
       sd.anc_off = l == L ? -1 : l * E;
@@ -810,8 +838,8 @@ lx_status run(const lx_tree_layer& t, int T, int k, const void* x, const int32_t
         if (P.dmerge) {  // [v1 | v2] rows of level 1's buffer, one exponent per row
           const LevelPlan& q1 = P.lv[1];
           sd.A = W + q1.v;
-          sd.lda = t.levels[0].rank + t.levels[1].rank;
-          sd.a_col0 = l == 1 ? 0 : t.levels[0].rank;
+          sd.lda = rank16(t.levels[0]) + rank16(t.levels[1]);
+          sd.a_col0 = l == 1 ? 0 : rank16(t.levels[0]);
           sd.a_exp = (const int32_t*)(W + q1.v_exp);
         }
       }
@@ -849,11 +877,13 @@ lx_status run(const lx_tree_layer& t, int T, int k, const void* x, const int32_t
     h.ldc = 2 * (int64_t)f;
     h.c_coloff[1] = f;
     if (fast[l] && P.cf16) {
+      const int rf = rank16(v);
       h.B[0] = v.a_gate_f16;
       h.B[1] = v.a_up_f16;
-      h.lda = 2 * (int64_t)r;  // [gate | up] fp16
-      h.a_koff[1] = r;
-      h.K = h.Kb = r;
+      h.b_stride[0] = h.b_stride[1] = (int64_t)f * rf;
+      h.lda = 2 * (int64_t)rf;  // [gate | up] fp16
+      h.a_koff[1] = rf;
+      h.K = h.Kb = rf;
       h.a_row_exp = (const int32_t*)(W + q.z_exp);
       h.b_exp = v.a_gate_f16_exp;
       h.b_exp1 = v.a_up_f16_exp;
@@ -974,10 +1004,10 @@ lx_status run(const lx_tree_layer& t, int T, int k, const void* x, const int32_t
     g.K = g.Kb = f;
     g.B[0] = v1.b_down_f16;
     g.B[1] = v2.b_down_f16;
-    g.b_stride[0] = (int64_t)v1.rank * f;
-    g.b_stride[1] = (int64_t)v2.rank * f;
-    g.ncols[0] = v1.rank;
-    g.ncols[1] = v2.rank;
+    g.b_stride[0] = (int64_t)rank16(v1) * f;
+    g.b_stride[1] = (int64_t)rank16(v2) * f;
+    g.ncols[0] = rank16(v1);
+    g.ncols[1] = rank16(v2);
     g.widx_anc = pa.anc + (size_t)1 * E;
     g.widx_fac = (const int32_t*)(W + P.lv[1].fac);
     g.widx_own1 = 1;
@@ -985,7 +1015,7 @@ lx_status run(const lx_tree_layer& t, int T, int k, const void* x, const int32_t
     g.b_exp = v1.b_down_f16_exp;
     g.b_exp1 = v2.b_down_f16_exp;
     g.C = (float*)(W + P.lv[1].v);
-    g.ldc = v1.rank + v2.rank;
+    g.ldc = rank16(v1) + rank16(v2);
     g.c_row_exp = (int32_t*)(W + P.lv[1].v_exp);
     if (pair_down) {
       g.tiles = ba.lv[L].tiles[kTabBig];
@@ -1020,14 +1050,17 @@ lx_status run(const lx_tree_layer& t, int T, int k, const void* x, const int32_t
         g.widx_anc = pa.anc + (size_t)l * E;
         g.widx_fac = (const int32_t*)(W + q.fac);
       }
+      const int rf = rank16(v);
       g.B[0] = v.b_down_f16;
+      g.b_stride[0] = (int64_t)rf * f;
+      g.ncols[0] = rf;
       g.lda = f;
       g.K = g.Kb = f;
-      g.ldc = r;
+      g.ldc = rf;
       g.a_row_exp = (const int32_t*)(W + qa.hbar_exp);
       g.b_exp = v.b_down_f16_exp;
       g.c_row_exp = (int32_t*)(W + q.v_exp);
-      LX_TRY(f16big(kDownIn[l], g, lt, r <= 64 ? 64 : 128, OUT_F16T, qa.rows_max));
+      LX_TRY(f16big(kDownIn[l], g, lt, rf <= 64 ? 64 : 128, OUT_F16T, qa.rows_max));
       continue;
     }
     if (P.merged) {
@@ -1075,9 +1108,11 @@ lx_status run(const lx_tree_layer& t, int T, int k, const void* x, const int32_t
     h.C = (float*)(W + q.y);
     h.ldc = d;
     if (fast[l] && P.cf16) {
+      const int rf = rank16(v);
       h.B[0] = v.a_down_f16;
-      h.lda = r;
-      h.K = h.Kb = r;
+      h.b_stride[0] = (int64_t)d * rf;
+      h.lda = rf;
+      h.K = h.Kb = rf;
       h.a_row_exp = (const int32_t*)(W + q.v_exp);
       h.b_exp = v.a_down_f16_exp;
       LX_TRY(f16big(kDownOut[l], h, l, 256, OUT_X16, q.rows_max));
@@ -1276,6 +1311,32 @@ lx_status lx_convert_f16(const void* w, int32_t n, int32_t rows, int32_t cols, v
     return fail(LX_ERR_INVALID_ARGUMENT, "null or misaligned pointer");
   const hipError_t e = launch_convert_f16(w, n, (int64_t)rows * cols, w_f16, exps, (hipStream_t)stream);
   if (e != hipSuccess) return fail(LX_ERR_HIP, std::string("lx_convert_f16: ") + hipGetErrorString(e));
+  return LX_OK;
+}
+
+lx_status lx_convert_f16_padded(const void* w, int32_t n, int32_t rows, int32_t cols, int32_t rows_out,
+                                int32_t cols_out, void* w_f16, int32_t* exps, void* stream) {
+  g_err.clear();
+  if (n < 1 || rows < 1 || cols < 1 || rows_out < rows || cols_out < cols)
+    return fail(LX_ERR_INVALID_ARGUMENT, "n, rows, cols positive; rows_out >= rows, cols_out >= cols");
+  if ((int64_t)rows_out * cols_out >= ((int64_t)1 << 31)) return fail(LX_ERR_UNSUPPORTED, "matrix too large");
+  if (!w || !w_f16 || !exps || !aligned(w, 2) || !aligned(w_f16, 16) || !aligned(exps, 4))
+    return fail(LX_ERR_INVALID_ARGUMENT, "null or misaligned pointer");
+  const hipError_t e = launch_copy_pad(w, n, rows, cols, rows_out, cols_out, w_f16, exps, (hipStream_t)stream);
+  if (e != hipSuccess) return fail(LX_ERR_HIP, std::string("lx_convert_f16_padded: ") + hipGetErrorString(e));
+  return LX_OK;
+}
+
+lx_status lx_pad_bf16(const void* w, int32_t n, int32_t rows, int32_t cols, int32_t rows_out, int32_t cols_out,
+                      void* w_out, void* stream) {
+  g_err.clear();
+  if (n < 1 || rows < 1 || cols < 1 || rows_out < rows || cols_out < cols)
+    return fail(LX_ERR_INVALID_ARGUMENT, "n, rows, cols positive; rows_out >= rows, cols_out >= cols");
+  if ((int64_t)rows_out * cols_out >= ((int64_t)1 << 31)) return fail(LX_ERR_UNSUPPORTED, "matrix too large");
+  if (!w || !w_out || !aligned(w, 2) || !aligned(w_out, 16))
+    return fail(LX_ERR_INVALID_ARGUMENT, "null or misaligned pointer");
+  const hipError_t e = launch_copy_pad(w, n, rows, cols, rows_out, cols_out, w_out, nullptr, (hipStream_t)stream);
+  if (e != hipSuccess) return fail(LX_ERR_HIP, std::string("lx_pad_bf16: ") + hipGetErrorString(e));
   return LX_OK;
 }
 

@@ -1541,6 +1541,29 @@ __global__ __launch_bounds__(256) void k_to_f16(const u16* __restrict__ w, int64
   }
 }
 
+// Zero-padded copy [n][rows][cols] -> [n][rows_out][cols_out]: fp16 scaled
+// as k_to_f16 (F16), or the bf16 values unchanged.
+template <bool F16>
+__global__ __launch_bounds__(256) void k_copy_pad(const u16* __restrict__ w, int rows, int cols, int rows_out,
+                                                  int cols_out, const uint32_t* __restrict__ mx,
+                                                  u16* __restrict__ out) {
+  const int i = blockIdx.y;
+  const int s = F16 ? f16_exp_for(mx[i]) : 0;
+  const int64_t per_out = (int64_t)rows_out * cols_out;
+  for (int64_t j = (int64_t)blockIdx.x * blockDim.x + threadIdx.x; j < per_out; j += (int64_t)gridDim.x * blockDim.x) {
+    const int r = (int)(j / cols_out), c = (int)(j - (int64_t)r * cols_out);
+    u16 v = 0;
+    if (r < rows && c < cols) {
+      const u16 b = w[((int64_t)i * rows + r) * cols + c];
+      if constexpr (F16)
+        v = __builtin_bit_cast(u16, (_Float16)ldexpf(__uint_as_float((uint32_t)b << 16), s));
+      else
+        v = b;
+    }
+    out[(int64_t)i * per_out + j] = v;
+  }
+}
+
 __global__ void k_f16_exps(uint32_t* __restrict__ mx, int n) {
   const int i = blockIdx.x * blockDim.x + threadIdx.x;
   if (i < n) mx[i] = (uint32_t)f16_exp_for(mx[i]);
@@ -1561,6 +1584,27 @@ hipError_t launch_convert_f16(const void* w, int n, int64_t per, void* w16, int3
   const int gx = (int)std::min<int64_t>((per + 255) / 256, 1024);
   hipLaunchKernelGGL(k_absmax_bits, dim3(gx, n), dim3(256), 0, s, (const u16*)w, per, n, mx);
   hipLaunchKernelGGL(k_to_f16, dim3(gx, n), dim3(256), 0, s, (const u16*)w, per, n, mx, (_Float16*)w16);
+  hipLaunchKernelGGL(k_f16_exps, dim3(g1), dim3(256), 0, s, mx, n);
+  return hipGetLastError();
+}
+
+hipError_t launch_copy_pad(const void* w, int n, int rows, int cols, int rows_out, int cols_out, void* out,
+                           int32_t* exps, hipStream_t s) {
+  if (n <= 0) return hipSuccess;
+  const int gx = (int)std::min<int64_t>(((int64_t)rows_out * cols_out + 255) / 256, 1024);
+  if (!exps) {
+    hipLaunchKernelGGL(k_copy_pad<false>, dim3(gx, n), dim3(256), 0, s, (const u16*)w, rows, cols, rows_out, cols_out,
+                       (const uint32_t*)nullptr, (u16*)out);
+    return hipGetLastError();
+  }
+  uint32_t* const mx = (uint32_t*)exps;
+  const int g1 = (n + 255) / 256;
+  const int64_t per = (int64_t)rows * cols;
+  hipLaunchKernelGGL(k_zero_u32, dim3(g1), dim3(256), 0, s, mx, n);
+  const int ga = (int)std::min<int64_t>((per + 255) / 256, 1024);
+  hipLaunchKernelGGL(k_absmax_bits, dim3(ga, n), dim3(256), 0, s, (const u16*)w, per, n, mx);
+  hipLaunchKernelGGL(k_copy_pad<true>, dim3(gx, n), dim3(256), 0, s, (const u16*)w, rows, cols, rows_out, cols_out,
+                     (const uint32_t*)mx, (u16*)out);
   hipLaunchKernelGGL(k_f16_exps, dim3(g1), dim3(256), 0, s, mx, n);
   return hipGetLastError();
 }

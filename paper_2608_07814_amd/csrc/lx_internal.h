@@ -335,6 +335,11 @@ hipError_t launch_gemm_f16_pair(const GemmArgs& g0, int grid_tiles0, const GemmA
 // (exps[i] puts the matrix's largest magnitude in [2^14, 2^15); 0 for an
 // all-zero matrix).
 hipError_t launch_convert_f16(const void* w, int n, int64_t per, void* w16, int32_t* exps, hipStream_t s);
+// Zero-padded copy [n][rows][cols] bf16 -> [n][rows_out][cols_out]: fp16 as
+// launch_convert_f16 (exps non-null; the exponents of the unpadded matrices)
+// or bf16 (exps null).
+hipError_t launch_copy_pad(const void* w, int n, int rows, int cols, int rows_out, int cols_out, void* out,
+                           int32_t* exps, hipStream_t s);
 // Weights [n][rows][cols] bf16 -> fp8 copy [n][rows][cols] and scale words
 // [n][rows][cols / 64] (cols a multiple of 64).
 hipError_t launch_quantize_f8(const void* w, int64_t n_rows, int cols, uint8_t* w8, uint32_t* sc, hipStream_t s);

@@ -36,11 +36,14 @@ class LxLevel(ctypes.Structure):
                 ("a_down", _c_void), ("b_down", _c_void),
                 ("a_gate_f16", _c_void), ("a_gate_f16_exp", _c_void), ("a_up_f16", _c_void),
                 ("a_up_f16_exp", _c_void), ("a_down_f16", _c_void), ("a_down_f16_exp", _c_void),
-                ("b_down_f16", _c_void), ("b_down_f16_exp", _c_void)]
+                ("b_down_f16", _c_void), ("b_down_f16_exp", _c_void),
+                ("rank_f16", _c_i32), ("b_gate_pad", _c_void), ("b_up_pad", _c_void)]
 
 # the optional fp16 factor copies of a level (lx_convert_f16), with exponents
 FACTOR_F16 = ("a_gate_f16", "a_gate_f16_exp", "a_up_f16", "a_up_f16_exp", "a_down_f16", "a_down_f16_exp",
               "b_down_f16", "b_down_f16_exp")
+# the zero-padded bf16 input factors that go with copies of a padded rank
+FACTOR_PAD = ("b_gate_pad", "b_up_pad")
 
 
 class LxTreeLayer(ctypes.Structure):
@@ -62,7 +65,8 @@ class LxFlatLayer(ctypes.Structure):
                 ("dom_down_f16", _c_void), ("dom_down_f16_exp", _c_void),
                 ("a_gate_f16", _c_void), ("a_gate_f16_exp", _c_void), ("a_up_f16", _c_void),
                 ("a_up_f16_exp", _c_void), ("a_down_f16", _c_void), ("a_down_f16_exp", _c_void),
-                ("b_down_f16", _c_void), ("b_down_f16_exp", _c_void)]
+                ("b_down_f16", _c_void), ("b_down_f16_exp", _c_void),
+                ("r_f16", _c_i32), ("b_gate_pad", _c_void), ("b_up_pad", _c_void)]
 
 
 class LxDenseLayer(ctypes.Structure):
@@ -95,6 +99,8 @@ EXPORTS = {
                            _c_void, _c_void, _c_void, ctypes.c_size_t, _c_void]),
     "lx_read_device_status": (_c_i32, [_c_void, _c_void, ctypes.POINTER(ctypes.c_uint32)]),
     "lx_convert_f16": (_c_i32, [_c_void, _c_i32, _c_i32, _c_i32, _c_void, _c_void, _c_void]),
+    "lx_convert_f16_padded": (_c_i32, [_c_void, _c_i32, _c_i32, _c_i32, _c_i32, _c_i32, _c_void, _c_void, _c_void]),
+    "lx_pad_bf16": (_c_i32, [_c_void, _c_i32, _c_i32, _c_i32, _c_i32, _c_i32, _c_void, _c_void]),
     "lx_quantize_f8": (_c_i32, [_c_void, _c_i32, _c_i32, _c_i32, _c_void, _c_void, _c_void]),
     "lx_route_workspace_bytes": (ctypes.c_size_t, [_c_i32, _c_i32, _c_i32]),
     "lx_coact_distance": (_c_i32, [_c_void, _c_i32, _c_i32, _c_i32, _c_void, _c_void, _c_void, _c_void]),
@@ -196,6 +202,11 @@ class DeviceLevel:
     a_down_f16_exp: Optional[torch.Tensor] = None
     b_down_f16: Optional[torch.Tensor] = None
     b_down_f16_exp: Optional[torch.Tensor] = None
+    # rank of the fp16 copies when padded to a multiple of 64 (0: rank), with
+    # the zero-padded bf16 b_gate / b_up [n_factors][rank_f16][d]
+    rank_f16: int = 0
+    b_gate_pad: Optional[torch.Tensor] = None
+    b_up_pad: Optional[torch.Tensor] = None
 
     @property
     def n_nodes(self) -> int:
@@ -250,8 +261,9 @@ class DeviceLayer:
             c.a_gate, c.b_gate, c.a_up, c.b_up, c.a_down, c.b_down = (
                 _ptr(lv.a_gate), _ptr(lv.b_gate), _ptr(lv.a_up), _ptr(lv.b_up),
                 _ptr(lv.a_down), _ptr(lv.b_down))
-            for n in FACTOR_F16:
+            for n in FACTOR_F16 + FACTOR_PAD:
                 setattr(c, n, _ptr(getattr(lv, n)))
+            c.rank_f16 = lv.rank_f16
         return s
 
     def flat_struct(self) -> LxFlatLayer:
@@ -269,8 +281,9 @@ class DeviceLayer:
         s.a_gate, s.b_gate, s.a_up, s.b_up, s.a_down, s.b_down = (
             _ptr(lv.a_gate), _ptr(lv.b_gate), _ptr(lv.a_up), _ptr(lv.b_up), _ptr(lv.a_down),
             _ptr(lv.b_down))
-        for n in FACTOR_F16:
+        for n in FACTOR_F16 + FACTOR_PAD:
             setattr(s, n, _ptr(getattr(lv, n)))
+        s.r_f16 = lv.rank_f16
         return s
 
     def dense_struct(self) -> LxDenseLayer:
@@ -456,6 +469,29 @@ def convert_f16(w: torch.Tensor, stream=None):
     return w16, ex
 
 
+def convert_f16_padded(w: torch.Tensor, rows_out: int, cols_out: int, stream=None):
+    """lx_convert_f16 into a zero-padded [n][rows_out][cols_out] layout
+    (lx_convert_f16_padded): returns (fp16 tensor, int32 exps [n])."""
+    if w.dtype != torch.bfloat16 or not w.is_contiguous() or w.dim() != 3:
+        raise ValueError("w must be a contiguous bf16 [n][rows][cols] tensor")
+    n, rows, cols = (int(v) for v in w.shape)
+    w16 = torch.empty(n, rows_out, cols_out, dtype=torch.float16, device=w.device)
+    ex = torch.empty(n, dtype=torch.int32, device=w.device)
+    _check(lib().lx_convert_f16_padded(_ptr(w), n, rows, cols, rows_out, cols_out, _ptr(w16), _ptr(ex),
+                                       _stream(stream)))
+    return w16, ex
+
+
+def pad_bf16(w: torch.Tensor, rows_out: int, cols_out: int, stream=None) -> torch.Tensor:
+    """Zero-padded copy [n][rows_out][cols_out] of bf16 weights (lx_pad_bf16)."""
+    if w.dtype != torch.bfloat16 or not w.is_contiguous() or w.dim() != 3:
+        raise ValueError("w must be a contiguous bf16 [n][rows][cols] tensor")
+    n, rows, cols = (int(v) for v in w.shape)
+    out = torch.empty(n, rows_out, cols_out, dtype=torch.bfloat16, device=w.device)
+    _check(lib().lx_pad_bf16(_ptr(w), n, rows, cols, rows_out, cols_out, _ptr(out), _stream(stream)))
+    return out
+
+
 def attach_down_f16(layer: "DeviceLayer") -> "DeviceLayer":
     """Give a bf16 layer the fp16 copy of its anchor down weights; a no-op
     for fp32 layers."""
@@ -467,15 +503,28 @@ def attach_down_f16(layer: "DeviceLayer") -> "DeviceLayer":
 def attach_factors_f16(layer: "DeviceLayer") -> "DeviceLayer":
     """Give every level of a bf16 layer the fp16 copies of its factors (used,
     with the anchor down fp16 copy, by the fp16 path of the correction
-    products); a no-op for fp32 layers and levels without factors."""
+    products); a rank that is not a multiple of 64 gets copies padded with
+    zeros to the next one (rank_f16, with padded bf16 b_gate / b_up); a no-op
+    for fp32 layers, levels without factors and padded ranks above 128."""
     if layer.dtype == "bf16":
         for lv in layer.levels:
             if lv.n_factors == 0:
                 continue
-            for n in ("a_gate", "a_up", "a_down", "b_down"):
-                w16, ex = convert_f16(getattr(lv, n))
+            r = lv.rank
+            rf = -(-r // 64) * 64  # the fp16 path takes ranks that are multiples of 64
+            if rf > 128:
+                continue
+            for n in ("a_gate", "a_up", "a_down"):  # [n][rows][r]: zero columns
+                w = getattr(lv, n)
+                w16, ex = convert_f16(w) if rf == r else convert_f16_padded(w, w.shape[1], rf)
                 setattr(lv, n + "_f16", w16)
                 setattr(lv, n + "_f16_exp", ex)
+            w = lv.b_down  # [n][r][f]: zero rows
+            lv.b_down_f16, lv.b_down_f16_exp = convert_f16(w) if rf == r else convert_f16_padded(w, rf, w.shape[2])
+            if rf > r:
+                lv.rank_f16 = rf
+                lv.b_gate_pad = pad_bf16(lv.b_gate, rf, lv.b_gate.shape[2])
+                lv.b_up_pad = pad_bf16(lv.b_up, rf, lv.b_up.shape[2])
     return layer
 
 

@@ -28,7 +28,7 @@ def _declared(root):
 
 def test_every_declared_symbol_is_exported(L, root):
     names = _declared(root)
-    assert len(names) == len(lx.EXPORTS) == 33
+    assert len(names) == len(lx.EXPORTS) == 35
     for n in names:
         assert hasattr(L, n), n
         assert n in lx.EXPORTS, n
@@ -354,3 +354,50 @@ def test_factor_f16_copies_validation(L):
     for n in names:
         setattr(f, n, FAKE)
     assert L.lx_moe_workspace_bytes(ctypes.byref(f), 64, 8) > 0
+
+
+def test_padded_rank_validation(L):
+    """rank_f16 (the padded rank of a level's fp16 copies): 0, or a multiple
+    of 64 in [rank, 128], only with the fp16 copies, and above the rank only
+    with both zero-padded bf16 input factors (checked on the host); the flat
+    layer carries it as r_f16; the padded-copy entry points check their
+    sizes and pointers."""
+    s = _tree(r=96)
+    lv = s.levels[0]
+    for n in lx.FACTOR_F16:
+        setattr(lv, n, FAKE)
+    assert L.lx_moe_tree_workspace_bytes(ctypes.byref(s), 64, 8) > 0
+    for bad in (100, 64, 192):  # not a multiple of 64, below the rank, above 128
+        lv.rank_f16 = bad
+        assert L.lx_moe_tree_workspace_bytes(ctypes.byref(s), 64, 8) == 0
+        assert "multiple of 64" in L.lx_last_error().decode()
+    lv.rank_f16 = 128
+    assert L.lx_moe_tree_workspace_bytes(ctypes.byref(s), 64, 8) == 0
+    assert "b_gate_pad" in L.lx_last_error().decode()
+    lv.b_gate_pad = FAKE
+    lv.b_up_pad = FAKE + 8  # not 16-byte aligned
+    assert L.lx_moe_tree_workspace_bytes(ctypes.byref(s), 64, 8) == 0
+    lv.b_up_pad = FAKE
+    assert L.lx_moe_tree_workspace_bytes(ctypes.byref(s), 64, 8) > 0
+    for n in lx.FACTOR_F16:
+        setattr(lv, n, None)
+    assert L.lx_moe_tree_workspace_bytes(ctypes.byref(s), 64, 8) == 0
+    assert "without fp16 factor copies" in L.lx_last_error().decode()
+    f = lx.LxFlatLayer()
+    f.E, f.C, f.d, f.f, f.r, f.M, f.dtype = 128, 16, 2048, 768, 96, 112, lx.LX_BF16
+    for n in ("cluster_of", "factor_of", "dom_gate", "dom_up", "dom_down", "a_gate", "b_gate",
+              "a_up", "b_up", "a_down", "b_down") + lx.FACTOR_F16:
+        setattr(f, n, FAKE)
+    f.r_f16 = 128
+    assert L.lx_moe_workspace_bytes(ctypes.byref(f), 64, 8) == 0
+    f.b_gate_pad = f.b_up_pad = FAKE
+    assert L.lx_moe_workspace_bytes(ctypes.byref(f), 64, 8) > 0
+    # entry points: sizes and pointers (no device work is queued)
+    E = lx.LX_ERR_INVALID_ARGUMENT
+    assert L.lx_convert_f16_padded(FAKE, 1, 96, 64, 64, 64, FAKE, FAKE, None) == E  # rows_out < rows
+    assert L.lx_convert_f16_padded(FAKE, 1, 96, 64, 128, 32, FAKE, FAKE, None) == E  # cols_out < cols
+    assert L.lx_convert_f16_padded(None, 1, 96, 64, 128, 64, FAKE, FAKE, None) == E
+    assert L.lx_convert_f16_padded(FAKE, 1, 96, 64, 128, 64, FAKE + 8, FAKE, None) == E
+    assert L.lx_pad_bf16(FAKE, 0, 96, 64, 128, 64, FAKE, None) == E
+    assert L.lx_pad_bf16(FAKE, 1, 96, 64, 128, 64, None, None) == E
+    assert L.lx_pad_bf16(FAKE, 1, 96, 64, 128, 64, FAKE + 8, None) == E

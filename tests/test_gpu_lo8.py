@@ -122,6 +122,30 @@ def test_convert_f16_exact():
         assert np.array_equal(got, wv[i]), i
 
 
+def test_padded_copies_exact():
+    """lx_convert_f16_padded equals lx_convert_f16 in the original rows and
+    columns (same values, same exponents) and is exactly zero in the padding;
+    lx_pad_bf16 copies the bf16 values unchanged and zero-fills the rest."""
+    require_gpu()
+    rng = np.random.default_rng(43)
+    w = (rng.standard_normal((3, 96, 200)) * 0.02).astype(np.float32)
+    w[1] *= 1e3
+    w[2] = 0.0
+    wt = torch.from_numpy(w).cuda().to(torch.bfloat16)
+    w16, ex = lx.convert_f16(wt)
+    for rows_out, cols_out in ((128, 200), (96, 256), (100, 264)):
+        p16, pex = lx.convert_f16_padded(wt, rows_out, cols_out)
+        pb = lx.pad_bf16(wt, rows_out, cols_out)
+        torch.cuda.synchronize()
+        assert torch.equal(pex, ex)
+        assert torch.equal(p16[:, :96, :200].view(torch.int16), w16.view(torch.int16))
+        assert torch.equal(pb[:, :96, :200].view(torch.int16), wt.view(torch.int16))
+        mask = torch.ones(rows_out, cols_out, dtype=torch.bool, device=wt.device)
+        mask[:96, :200] = False
+        assert int(p16.view(torch.int16)[:, mask].abs().max()) == 0 if mask.any() else True
+        assert int(pb.view(torch.int16)[:, mask].abs().max()) == 0 if mask.any() else True
+
+
 @pytest.mark.parametrize("cfg,T,kind", [(1, 1024, None), (4, 600, None), ("dense", 600, "dense")])
 def test_f16_forward(cfg, T, kind):
     """With the fp16 copy the anchor down projection multiplies fp16 sums
@@ -148,13 +172,13 @@ def test_f16_forward(cfg, T, kind):
     assert e16 <= TOL_DESIGN and e16 <= TOL_BF16
 
 
-@pytest.mark.parametrize("cfg,T,used", [(1, 2048, True), (4, 2304, True), (3, 2048, False)])
+@pytest.mark.parametrize("cfg,T,used", [(1, 2048, True), (4, 2304, True), (3, 2048, True)])
 def test_f16_correction_products(cfg, T, used):
     """With the fp16 copies of the factors every correction product runs once
     in fp16 (tile-scaled fp16 intermediates, token-scaled fp16 activation
     sums): a different result from the same layer without those copies (the
     path ran), and both meet the design bound against the oracle. Rank 96
-    (not a multiple of 64) keeps the bf16 pair products: identical results.
+    (not a multiple of 64) runs on copies padded with zeros to rank 128.
     (Sizes with more than 64 rows per expert at every level: smaller batches
     take the skinny kernel, which keeps the pairs.)"""
     require_gpu()
@@ -162,10 +186,13 @@ def test_f16_correction_products(cfg, T, used):
     ref = O.moe_forward(p.layer, p.x, p.routing.topk_ids, p.routing.topk_weights)
     full = lx.to_device(p.layer, lo8=True, f16=True)
     assert all(lv.b_down_f16 is not None for lv in full.levels if lv.n_factors > 0)
+    if cfg == 3:
+        assert all(lv.rank_f16 == 128 and lv.b_gate_pad is not None for lv in full.levels)
     anchor_only = lx.to_device(p.layer, lo8=True, f16=True)
     for lv in anchor_only.levels:
-        for n in lx.FACTOR_F16:
+        for n in lx.FACTOR_F16 + lx.FACTOR_PAD:
             setattr(lv, n, None)
+        lv.rank_f16 = 0
     g_full = gpu_forward(p, dev_layer=full)
     g_anchor = gpu_forward(p, dev_layer=anchor_only)
     e_full, e_anchor = err_ratio(g_full, ref), err_ratio(g_anchor, ref)
