@@ -218,38 +218,46 @@ __device__ inline int block_exscan(int v, int* s_wave, int& total) {
 
 // GEMM tile tables over the nodes that do work, in node order, one per tile
 // height. off / fac: the level's node offsets and validated factor indices
-// (global or LDS), complete and visible to the whole workgroup.
+// (global or LDS), complete and visible to the whole workgroup. Each thread
+// reads its nodes' offsets, work flags and weight indices once (at most
+// LX_MAX_NODES / 1024 nodes per thread), before the first table's stores.
 __device__ inline void build_tile_tables(const BucketLevel& lv, const int32_t* off, const int32_t* fac,
                                          int* s_wave) {
+  constexpr int kMaxChunk = (LX_MAX_NODES + 1023) / 1024;
   const int N = lv.n_nodes;
   const int nth = blockDim.x, tid = threadIdx.x;
   const int nchunk = (N + nth - 1) / nth;
   const int nb = tid * nchunk;
-  const int ne = nb + nchunk < N ? nb + nchunk : N;
+  int o_[kMaxChunk], cnt_[kMaxChunk], widx_[kMaxChunk];  // cnt_ 0: no tiles
+#pragma unroll
+  for (int u = 0; u < kMaxChunk; ++u) {
+    const int n = nb + u;
+    o_[u] = cnt_[u] = widx_[u] = 0;
+    if (u < nchunk && n < N) {
+      const bool work = lv.work_all || (lv.work_node ? lv.work_node[n] != 0 : fac[n] >= 0);
+      o_[u] = off[n];
+      cnt_[u] = work ? off[n + 1] - o_[u] : 0;
+      widx_[u] = lv.work_all ? n : fac[n];
+    }
+  }
   for (int tab = 0; tab < kNumTab; ++tab) {
     if (!((lv.tab_mask >> tab) & 1u)) continue;  // uniform across the workgroup
     const int bm = lv.tile_bm[tab];
     TileEntry* tiles = lv.tiles[tab];
     int my_tiles = 0;
-    for (int n = nb; n < ne; ++n) {
-      const bool work = lv.work_all || (lv.work_node ? lv.work_node[n] != 0 : fac[n] >= 0);
-      const int cnt = off[n + 1] - off[n];
-      if (work && cnt > 0) my_tiles += (cnt + bm - 1) / bm;
-    }
+#pragma unroll
+    for (int u = 0; u < kMaxChunk; ++u) my_tiles += (cnt_[u] + bm - 1) / bm;
     int ntiles = 0;
     int tpos = block_exscan(my_tiles, s_wave, ntiles);
-    for (int n = nb; n < ne; ++n) {
-      const bool work = lv.work_all || (lv.work_node ? lv.work_node[n] != 0 : fac[n] >= 0);
-      const int o = off[n];
-      const int cnt = off[n + 1] - o;
-      if (!work || cnt == 0) continue;
-      const int widx = lv.work_all ? n : fac[n];
+#pragma unroll
+    for (int u = 0; u < kMaxChunk; ++u) {
+      const int cnt = cnt_[u];
       for (int r = 0; r < cnt; r += bm) {
         TileEntry te;
-        te.widx = widx;
-        te.row0 = o + r;
+        te.widx = widx_[u];
+        te.row0 = o_[u] + r;
         te.nrows = cnt - r < bm ? cnt - r : bm;
-        te.node = n;
+        te.node = nb + u;
         tiles[tpos++] = te;
       }
     }
