@@ -1654,6 +1654,9 @@ hipError_t launch_gemm_f16_pair(const GemmArgs& g0, int grid_tiles0, const GemmA
   const int ntn1 = (g1.ncols[0] + g1.ncols[1] + 255) / 256;
   int grid = grid_tiles0 * ntn0 + grid_tiles1 * ntn1;
   if (grid <= 0) return hipSuccess;
+  // a multiple of 8: the second product's remainder items go to the XCDs
+  // from the last one down, so every XCD needs a workgroup
+  grid = (grid + NXCD - 1) / NXCD * NXCD;
   const int cap = grid_cap();
   if (grid > cap) grid = cap;
   if (ofmt1 == OUT_F16T)

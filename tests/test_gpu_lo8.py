@@ -10,7 +10,7 @@ import numpy as np
 import pytest
 import torch
 
-from lxsynth import make_problem
+from lxsynth import config, make_problem
 from oracle import moe as O
 from paper_2608_07814_amd import lorex as lx
 from gpu_util import TOL_BF16, TOL_DESIGN, require_gpu, say, gpu_forward, err_ratio, sample_tokens
@@ -120,6 +120,30 @@ def test_convert_f16_exact():
         assert ex[i] == want, (i, ex[i], want)
         got = w16[i].float().cpu().numpy().astype(np.float64) * 2.0 ** -int(ex[i])
         assert np.array_equal(got, wv[i]), i
+
+
+def test_paired_down_launch_small_grid():
+    """The tree's fp16 anchor down projection and merged down-in share one
+    persistent launch, whose schedule spreads the second product's items over
+    the XCDs from the last one down. With one anchor, one sub-node and two
+    leaves at T = 512, k = 1 the launch bound is 7 work items: the grid is
+    rounded up to a multiple of 8 so that every XCD has a workgroup. Every
+    output against the oracle, and the paired launch ran."""
+    require_gpu()
+    p = make_problem(config(4, E=2, d=256, f=256, n_roots=1, subs_per_root=1, r_sub=64, r_leaf=64, k=1), T=512)
+    ref = O.moe_forward(p.layer, p.x, p.routing.topk_ids, p.routing.topk_weights)
+    lx.profile_reset()
+    lx.profile_enable(True)
+    try:
+        got = gpu_forward(p)
+        names = lx.profile_read()
+    finally:
+        lx.profile_enable(False)
+        lx.profile_reset()
+    assert "anchor_down+lowrank_down_in_merged" in names, sorted(names)
+    e = err_ratio(got, ref)
+    say(f"small paired launch: err/RMS {e:.3e}")
+    assert e <= TOL_DESIGN
 
 
 def test_padded_copies_exact():
