@@ -354,7 +354,7 @@ def test_merged_tree_products(case):
     e = err_ratio(got, _oracle(p))
     say(f"  err/RMS = {e:.3e}")
     assert e <= TOL_BF16 and e <= TOL_DESIGN
-    # the same forward with the correction chains on the auxiliary stream
+    # a second call gives the same bits
     assert np.array_equal(got, gpu_forward(p))
 
 
