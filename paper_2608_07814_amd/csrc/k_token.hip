@@ -290,18 +290,6 @@ __device__ __forceinline__ void token_meta_fast(const TokenArgs& a, int t, int (
   }
 }
 
-// Between a kernel's load pass and its arithmetic pass the slot flags go
-// through an empty asm: the compiler then cannot merge the two passes'
-// branches on the same flag, which would put each row's first arithmetic
-// right after its loads (and a wait for them there, one row after another).
-template <int NL>
-__device__ __forceinline__ void opaque_flags(int (&fl)[NL + 1][kFastK]) {
-#pragma unroll
-  for (int l = 0; l <= NL; ++l)
-#pragma unroll
-    for (int j = 0; j < kFastK; ++j) asm volatile("" : "+s"(fl[l][j]));
-}
-
 // Raw row segment (4 values at column c): loaded in one pass, converted in a
 // later one, so every load of a thread is in flight before the first use.
 template <bool X16>
@@ -357,7 +345,6 @@ __global__ __launch_bounds__(kFastThr) void k_swiglu_fast(TokenArgs a) {
       uv[j][l] = ldraw<X16>(a.dgu[l], row[l][j], ld, f + c);
     }
   }
-  opaque_flags<NL>(fl);
   float4 h[kFastK];
 #pragma unroll
   for (int j = 0; j < kFastK; ++j) {
@@ -544,7 +531,6 @@ __global__ __launch_bounds__(kFastThr) void k_combine_fast(TokenArgs a) {
 #pragma unroll
     for (int j = 0; j < kFastK; ++j)
       if ((fl[l][j] & 3) == 3 && !(merged && l > 0 && l < NL)) v[l][j] = ldraw<X16>(a.y[l], row[l][j], d, c);
-  opaque_flags<NL>(fl);
   float4 acc = make_float4(0.f, 0.f, 0.f, 0.f);
 #pragma unroll
   for (int l = 0; l <= NL; ++l)
