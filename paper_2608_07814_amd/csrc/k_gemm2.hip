@@ -31,7 +31,8 @@
 //     neighbours that share A rows and weight slabs share one L2;
 //   * epilogue through LDS: each wavefront transposes its accumulator block
 //     so that every lane stores 4 consecutive columns of one row (16-byte
-//     fp32 or 8-byte bf16 stores).
+//     fp32 or 8-byte bf16 stores), 8 for x16 outputs (a 16-byte mantissa
+//     store and a 2-byte exponent store).
 #include "lx_internal.h"
 
 #include <algorithm>
@@ -557,7 +558,7 @@ __device__ __forceinline__ void gemm_big_body(const GemmArgs& p, int ntn, const 
     // Epilogue (output format O). 32x32 accumulator layout: lane holds column (lane & 31) and
     // rows 8*(i/4) + 4*(lane/32) + (i%4) for i = 0..15. Each wavefront writes
     // its 32 x WN block of one mi into its own LDS region (row pitch WN + 4
-    // floats), then reads it back as 4 consecutive columns per lane. All
+    // floats), then reads it back as 4 (x16: 8) consecutive columns per lane. All
     // stages are free here (every wavefront passed the barrier above).
     {
       constexpr int PITCH = WN + 4;
@@ -611,6 +612,13 @@ __device__ __forceinline__ void gemm_big_body(const GemmArgs& p, int ntn, const 
         }
       }
       X16Rows xr(g.C, g.ldc, te.row0 + wm * WM + lane / LPR, RPP, col);
+      // x16 output: 8 consecutive columns per lane (one 16-byte mantissa and
+      // one 2-byte exponent store per row)
+      constexpr int LPR8 = WN / 8, RPP8 = 64 / LPR8;
+      static_assert(WN % 8 == 0 && 32 % RPP8 == 0, "x16 epilogue layout");
+      const int c8 = (lane % LPR8) * 8;
+      const int col8 = n0 + wn * WN + c8;
+      X16Rows8 xr8(g.C, g.ldc, te.row0 + wm * WM + lane / LPR8, RPP8, col8);
       // full tiles store without per-row checks (a separate, branch-free copy)
       auto emit = [&](auto check) {
 #pragma unroll
@@ -620,6 +628,26 @@ __device__ __forceinline__ void gemm_big_body(const GemmArgs& p, int ntn, const 
 #pragma unroll
             for (int i = 0; i < 16; ++i)
               ep[(8 * (i >> 2) + 4 * (lane >> 5) + (i & 3)) * PITCH + ni * 32 + (lane & 31)] = acc[mi][ni][i];
+          if constexpr (O == OUT_X16) {
+#pragma unroll
+            for (int ps = 0; ps < 32 / RPP8; ++ps) {
+              const int rr = ps * RPP8 + lane / LPR8;
+              float4 va = *(const float4*)&ep[rr * PITCH + c8];
+              float4 vb = *(const float4*)&ep[rr * PITCH + c8 + 4];
+              const int r = wm * WM + mi * 32 + rr;
+              const bool ok = !decltype(check)::value || (r < te.nrows && col8 < ncol);
+              if constexpr (F16) {
+                if (ok) {
+                  const int e = -(s_rexp[r] + bexp);
+                  va = make_float4(ldexpf(va.x, e), ldexpf(va.y, e), ldexpf(va.z, e), ldexpf(va.w, e));
+                  vb = make_float4(ldexpf(vb.x, e), ldexpf(vb.y, e), ldexpf(vb.z, e), ldexpf(vb.w, e));
+                }
+              }
+              if (ok) xr8.store(va, vb);
+              xr8.next();
+            }
+            continue;
+          }
 #pragma unroll
           for (int ps = 0; ps < 32 / RPP; ++ps) {
             const int rr = ps * RPP + lane / LPR;
@@ -732,7 +760,9 @@ void k_gemm_seg(GemmArgs p, SegArgs sg, int ntn) {
   constexpr int MI = BM / 64, NI = BN / (32 * WGN), WM = BM / 2, WN = BN / WGN;
   constexpr int A_ROUNDS = BM * 8 / NTHR, B_ROUNDS = BN * 8 / NTHR, ROUNDS = A_ROUNDS + B_ROUNDS;
   constexpr int SA = BM * BK2, SB = BN * BK2;
-  constexpr int PITCH = WN + 4, LPR = WN / 4, RPP = 64 / LPR;  // epilogue
+  // epilogue: 8 consecutive columns per lane (LPR lanes per row, RPP rows per pass)
+  constexpr int PITCH = WN + 4, LPR = WN / 8, RPP = 64 / LPR;
+  static_assert(8 % RPP == 0, "epilogue rows");
   __shared__ __attribute__((aligned(1024))) u16 smem[2 * (SA + SB)];
   u16* const sA0 = smem;
   u16* const sB0 = smem + SA;
@@ -1006,12 +1036,12 @@ void k_gemm_seg(GemmArgs p, SegArgs sg, int ntn) {
     }
 
     // Epilogue (as k_gemm_big's x16 output): per-wavefront LDS transpose of
-    // 8 rows at a time, then 4 consecutive columns per lane.
+    // 8 rows at a time, then 8 consecutive columns per lane.
     {
       float* const ep = s_ep[wave];
-      const int c4 = (lane % LPR) * 4;
-      const int col = en0 + wn * WN + c4;
-      X16Rows xr(p.C, p.ldc, row0 + wm * WM + lane / LPR, RPP, col);
+      const int c8 = (lane % LPR) * 8;
+      const int col = en0 + wn * WN + c8;
+      X16Rows8 xr(p.C, p.ldc, row0 + wm * WM + lane / LPR, RPP, col);
       // full tiles store without per-row checks (a separate, branch-free copy)
       auto emit = [&](auto check) {
 #pragma unroll
@@ -1027,8 +1057,9 @@ void k_gemm_seg(GemmArgs p, SegArgs sg, int ntn) {
 #pragma unroll
             for (int ps = 0; ps < 8 / RPP; ++ps) {
               const int rr = ps * RPP + lane / LPR;
-              const float4 v = *(const float4*)&ep[rr * PITCH + c4];
-              if (!decltype(check)::value || (wm * WM + mi * 32 + 8 * qd + rr < nrows && col < ncol)) xr.store(v);
+              const float4 va = *(const float4*)&ep[rr * PITCH + c8];
+              const float4 vb = *(const float4*)&ep[rr * PITCH + c8 + 4];
+              if (!decltype(check)::value || (wm * WM + mi * 32 + 8 * qd + rr < nrows && col < ncol)) xr.store(va, vb);
               xr.next();
             }
           }
@@ -1622,9 +1653,14 @@ bool gemm_f16_ok(const GemmArgs& g, int bn, int ofmt, int64_t a_rows_total) {
 
 // x16 rows need a row length that keeps every 8-byte mantissa word aligned.
 static bool x16_shape_ok(const GemmArgs& g, int ofmt) { return ofmt != OUT_X16 || g.ldc % 32 == 0; }
+// x16 outputs of the large-tile kernels, 8 columns per lane: 16-byte aligned
+// rows (ldc a multiple of 64) and whole groups of 8 columns per part
+static bool x16_rows8_ok(const GemmArgs& g, int ofmt) {
+  return ofmt != OUT_X16 || (g.ldc % 64 == 0 && g.ncols[0] % 8 == 0 && g.ncols[1] % 8 == 0 && ((uintptr_t)g.C & 15) == 0);
+}
 
 hipError_t launch_gemm_f16(const GemmArgs& g, int bn, int ofmt, int grid_tiles, hipStream_t s) {
-  if (!x16_shape_ok(g, ofmt)) return hipErrorInvalidValue;
+  if (!x16_rows8_ok(g, ofmt)) return hipErrorInvalidValue;
   const int ntn = (g.ncols[0] + g.ncols[1] + bn - 1) / bn;
   int grid = grid_tiles * ntn;
   if (grid <= 0) return hipSuccess;
@@ -1649,7 +1685,7 @@ hipError_t launch_gemm_f16(const GemmArgs& g, int bn, int ofmt, int grid_tiles, 
 
 hipError_t launch_gemm_f16_pair(const GemmArgs& g0, int grid_tiles0, const GemmArgs& g1, int ofmt1,
                                 int grid_tiles1, hipStream_t s) {
-  if (!x16_shape_ok(g0, OUT_X16) || !x16_shape_ok(g1, ofmt1)) return hipErrorInvalidValue;
+  if (!x16_rows8_ok(g0, OUT_X16) || !x16_rows8_ok(g1, ofmt1)) return hipErrorInvalidValue;
   const int ntn0 = (g0.ncols[0] + g0.ncols[1] + 255) / 256;
   const int ntn1 = (g1.ncols[0] + g1.ncols[1] + 255) / 256;
   int grid = grid_tiles0 * ntn0 + grid_tiles1 * ntn1;
@@ -1717,7 +1753,7 @@ int grid_cap() {
 }  // namespace
 
 hipError_t launch_gemm_big(const GemmArgs& g, int bm, int bn, int ofmt, int grid_tiles, hipStream_t s) {
-  if (!x16_shape_ok(g, ofmt)) return hipErrorInvalidValue;
+  if (!x16_rows8_ok(g, ofmt)) return hipErrorInvalidValue;
   // fp16 output with one scale per tile: the tile spans whole rows
   if (ofmt == OUT_F16T && (!g.c_row_exp || g.ncols[0] + g.ncols[1] > bn || bm != 256 || bn < 128))
     return hipErrorInvalidValue;
@@ -1741,7 +1777,8 @@ bool gemm_seg_ok(const GemmArgs& g, const SegArgs& sa, int64_t out_rows) {
   const int ncol = g.ncols[0] + g.ncols[1];
   // tiles never straddle the two parts (their A columns differ)
   if (g.ncols[1] > 0 && g.ncols[0] % 256) return false;
-  if (g.ncols[0] % 4 || g.ncols[1] % 4 || g.ldc % 32 || g.ldc < ncol || ((uintptr_t)g.C & 7)) return false;
+  // (x16 output, 8 columns per lane: 16-byte aligned rows)
+  if (g.ncols[0] % 8 || g.ncols[1] % 8 || g.ldc % 64 || g.ldc < ncol || ((uintptr_t)g.C & 15)) return false;
   if (out_rows * g.ldc * 3 >= ((int64_t)1 << 40)) return false;
   for (int i = 0; i < sa.nseg; ++i) {
     const SegDesc& d = sa.s[i];
@@ -1781,7 +1818,7 @@ hipError_t launch_gemm_seg(const GemmArgs& g, const SegArgs& sa_in, int grid_til
 }
 
 hipError_t launch_gemm_lo8(const GemmArgs& g, int ofmt, int grid_tiles, hipStream_t s) {
-  if (!x16_shape_ok(g, ofmt)) return hipErrorInvalidValue;
+  if (!x16_rows8_ok(g, ofmt)) return hipErrorInvalidValue;
   const int ntn = (g.ncols[0] + 255) / 256;
   int grid = grid_tiles * ntn;
   if (grid <= 0) return hipSuccess;

@@ -80,6 +80,27 @@ struct X16Rows {
   __device__ __forceinline__ void next() { m += stride; }
 };
 
+// The same down a group of 8 columns [c, c + 8) (c a multiple of 8, n a
+// multiple of 64, base 16-byte aligned): one 16-byte mantissa store and one
+// 2-byte exponent store per row, half the store instructions of X16Rows.
+struct X16Rows8 {
+  uint8_t* m;
+  int64_t stride;
+  int32_t eoff;
+  __device__ __forceinline__ X16Rows8(void* base, int64_t n, int64_t row, int step, int64_t c) {
+    const int64_t rb = x16_row_bytes(n);
+    m = (uint8_t*)base + row * rb + 2 * c;
+    stride = rb * step;
+    eoff = (int32_t)(2 * n + (c >> 2) - 2 * c);
+  }
+  __device__ __forceinline__ void store(float4 a, float4 b) const {
+    const X16x4 wa = x16_pack(a), wb = x16_pack(b);
+    *(uint4*)m = make_uint4(wa.m.x, wa.m.y, wb.m.x, wb.m.y);
+    *(uint16_t*)(m + eoff) = (uint16_t)((wa.e & 0xFFu) | ((wb.e & 0xFFu) << 8));
+  }
+  __device__ __forceinline__ void next() { m += stride; }
+};
+
 __device__ __forceinline__ X16x4 x16_load_raw(const void* base, int64_t row, int64_t n, int64_t c) {
   const uint8_t* const rp = (const uint8_t*)base + row * x16_row_bytes(n);
   X16x4 w;
