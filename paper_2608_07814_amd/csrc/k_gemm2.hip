@@ -31,8 +31,7 @@
 //     neighbours that share A rows and weight slabs share one L2;
 //   * epilogue through LDS: each wavefront transposes its accumulator block
 //     so that every lane stores 4 consecutive columns of one row (16-byte
-//     fp32 or 8-byte bf16 stores), 8 for x16 outputs (a 16-byte mantissa
-//     store and a 2-byte exponent store).
+//     fp32 or 8-byte bf16 stores), 8 for x16 outputs (one 16-byte group).
 #include "lx_internal.h"
 
 #include <algorithm>
@@ -611,9 +610,8 @@ __device__ __forceinline__ void gemm_big_body(const GemmArgs& p, int ntn, const 
           tsh = tsh < -100 ? -100 : tsh > 100 ? 100 : tsh;
         }
       }
-      X16Rows xr(g.C, g.ldc, te.row0 + wm * WM + lane / LPR, RPP, col);
-      // x16 output: 8 consecutive columns per lane (one 16-byte mantissa and
-      // one 2-byte exponent store per row)
+      // x16 output: 8 consecutive columns per lane (one x16 group, one
+      // 16-byte store per row)
       constexpr int LPR8 = WN / 8, RPP8 = 64 / LPR8;
       static_assert(WN % 8 == 0 && 32 % RPP8 == 0, "x16 epilogue layout");
       const int c8 = (lane % LPR8) * 8;
@@ -660,10 +658,7 @@ __device__ __forceinline__ void gemm_big_body(const GemmArgs& p, int ntn, const 
                 v = make_float4(ldexpf(v.x, e), ldexpf(v.y, e), ldexpf(v.z, e), ldexpf(v.w, e));
               }
             }
-            if constexpr (O == OUT_X16) {
-              if (ok) xr.store(v);
-              xr.next();
-            } else if constexpr (O == OUT_F16T) {
+            if constexpr (O == OUT_F16T) {
               if (!ok) continue;
               typedef _Float16 h4 __attribute__((ext_vector_type(4)));
               h4 q;
@@ -1230,6 +1225,21 @@ __device__ __forceinline__ void sk_epilogue(const SkUnit& u, const f32x16& acc, 
       ep[r * PITCH + cc] = v;
     }
   }
+  if (u.ofmt == OUT_X16) {
+    // 8 consecutive columns per lane (one x16 group), 16 rows per pass
+    constexpr int LPR8 = 4, RPP8 = 16;
+    const int c8 = (lane % LPR8) * 8;
+    const int col8 = u.n0 + wave * 32 + c8;
+#pragma unroll
+    for (int ps = 0; ps < 32 / RPP8; ++ps) {
+      const int r = ps * RPP8 + lane / LPR8;
+      const float4 va = *(const float4*)&ep[r * PITCH + c8];
+      const float4 vb = *(const float4*)&ep[r * PITCH + c8 + 4];
+      if (r < te.nrows && col8 < u.ncol)
+        *(uint4*)((uint8_t*)p.C + ((int64_t)(te.row0 + r) * p.ldc + col8) * 2) = x16_pack8(va, vb);
+    }
+    return;
+  }
 #pragma unroll
   for (int ps = 0; ps < 32 / RPP; ++ps) {
     const int r = ps * RPP + lane / LPR;
@@ -1252,8 +1262,6 @@ __device__ __forceinline__ void sk_epilogue(const SkUnit& u, const f32x16& acc, 
       __bf16* const rowp = (__bf16*)p.C + (int64_t)(te.row0 + r) * p.ldc;
       *(bf16x4*)(rowp + hi_col) = h;
       *(bf16x4*)(rowp + lo_col) = l;
-    } else if (u.ofmt == OUT_X16) {
-      x16_store(p.C, te.row0 + r, p.ldc, col, v);
     } else {
       *(float4*)(p.C + (int64_t)(te.row0 + r) * p.ldc + col) = v;
     }
@@ -1652,15 +1660,13 @@ bool gemm_f16_ok(const GemmArgs& g, int bn, int ofmt, int64_t a_rows_total) {
 }
 
 // x16 rows need a row length that keeps every 8-byte mantissa word aligned.
-static bool x16_shape_ok(const GemmArgs& g, int ofmt) { return ofmt != OUT_X16 || g.ldc % 32 == 0; }
-// x16 outputs of the large-tile kernels, 8 columns per lane: 16-byte aligned
-// rows (ldc a multiple of 64) and whole groups of 8 columns per part
-static bool x16_rows8_ok(const GemmArgs& g, int ofmt) {
-  return ofmt != OUT_X16 || (g.ldc % 64 == 0 && g.ncols[0] % 8 == 0 && g.ncols[1] % 8 == 0 && ((uintptr_t)g.C & 15) == 0);
+// x16 outputs: whole 8-value groups per part, 16-byte aligned rows
+static bool x16_shape_ok(const GemmArgs& g, int ofmt) {
+  return ofmt != OUT_X16 || (g.ldc % 8 == 0 && g.ncols[0] % 8 == 0 && g.ncols[1] % 8 == 0 && ((uintptr_t)g.C & 15) == 0);
 }
 
 hipError_t launch_gemm_f16(const GemmArgs& g, int bn, int ofmt, int grid_tiles, hipStream_t s) {
-  if (!x16_rows8_ok(g, ofmt)) return hipErrorInvalidValue;
+  if (!x16_shape_ok(g, ofmt)) return hipErrorInvalidValue;
   const int ntn = (g.ncols[0] + g.ncols[1] + bn - 1) / bn;
   int grid = grid_tiles * ntn;
   if (grid <= 0) return hipSuccess;
@@ -1685,7 +1691,7 @@ hipError_t launch_gemm_f16(const GemmArgs& g, int bn, int ofmt, int grid_tiles, 
 
 hipError_t launch_gemm_f16_pair(const GemmArgs& g0, int grid_tiles0, const GemmArgs& g1, int ofmt1,
                                 int grid_tiles1, hipStream_t s) {
-  if (!x16_rows8_ok(g0, OUT_X16) || !x16_rows8_ok(g1, ofmt1)) return hipErrorInvalidValue;
+  if (!x16_shape_ok(g0, OUT_X16) || !x16_shape_ok(g1, ofmt1)) return hipErrorInvalidValue;
   const int ntn0 = (g0.ncols[0] + g0.ncols[1] + 255) / 256;
   const int ntn1 = (g1.ncols[0] + g1.ncols[1] + 255) / 256;
   int grid = grid_tiles0 * ntn0 + grid_tiles1 * ntn1;
@@ -1753,7 +1759,7 @@ int grid_cap() {
 }  // namespace
 
 hipError_t launch_gemm_big(const GemmArgs& g, int bm, int bn, int ofmt, int grid_tiles, hipStream_t s) {
-  if (!x16_rows8_ok(g, ofmt)) return hipErrorInvalidValue;
+  if (!x16_shape_ok(g, ofmt)) return hipErrorInvalidValue;
   // fp16 output with one scale per tile: the tile spans whole rows
   if (ofmt == OUT_F16T && (!g.c_row_exp || g.ncols[0] + g.ncols[1] > bn || bm != 256 || bn < 128))
     return hipErrorInvalidValue;
@@ -1778,7 +1784,7 @@ bool gemm_seg_ok(const GemmArgs& g, const SegArgs& sa, int64_t out_rows) {
   // tiles never straddle the two parts (their A columns differ)
   if (g.ncols[1] > 0 && g.ncols[0] % 256) return false;
   // (x16 output, 8 columns per lane: 16-byte aligned rows)
-  if (g.ncols[0] % 8 || g.ncols[1] % 8 || g.ldc % 64 || g.ldc < ncol || ((uintptr_t)g.C & 15)) return false;
+  if (g.ncols[0] % 8 || g.ncols[1] % 8 || g.ldc % 8 || g.ldc < ncol || ((uintptr_t)g.C & 15)) return false;
   if (out_rows * g.ldc * 3 >= ((int64_t)1 << 40)) return false;
   for (int i = 0; i < sa.nseg; ++i) {
     const SegDesc& d = sa.s[i];
@@ -1818,7 +1824,7 @@ hipError_t launch_gemm_seg(const GemmArgs& g, const SegArgs& sa_in, int grid_til
 }
 
 hipError_t launch_gemm_lo8(const GemmArgs& g, int ofmt, int grid_tiles, hipStream_t s) {
-  if (!x16_rows8_ok(g, ofmt)) return hipErrorInvalidValue;
+  if (!x16_shape_ok(g, ofmt)) return hipErrorInvalidValue;
   const int ntn = (g.ncols[0] + 255) / 256;
   int grid = grid_tiles * ntn;
   if (grid <= 0) return hipSuccess;

@@ -50,7 +50,7 @@ __device__ __forceinline__ float4 ld4(const float* p) { return *(const float4*)p
 // 4 consecutive values at column c of row `row` (row length ld values) of an
 // fp32 or x16 matrix.
 __device__ __forceinline__ float4 ldrow4(const float* base, bool x16, int64_t row, int64_t ld, int c) {
-  if (x16) return x16_unpack(x16_load_raw(base, row, ld, c));
+  if (x16) return x16_unpack4(x16_load8(base, row, ld, c), (c >> 2) & 1);
   return *(const float4*)(base + row * ld + c);
 }
 __device__ __forceinline__ void add4(float4& a, const float4& b) {
@@ -214,7 +214,7 @@ __global__ __launch_bounds__(kCombMaxThr) void k_combine(TokenArgs a) {
         if ((a.slot_flags[l][sl] & 3) == 3 && !(a.merged && l > 0 && l < L)) {
           take = true;
           x16 = a.x16[l] != 0;
-          ptr = (const uint8_t*)a.y[l] + (int64_t)row * (x16 ? x16_row_bytes(d) : (int64_t)d * 4);
+          ptr = (const uint8_t*)a.y[l] + (int64_t)row * d * (x16 ? 2 : 4);
         }
       }
       const uint64_t bal = __ballot(take);
@@ -236,7 +236,7 @@ __global__ __launch_bounds__(kCombMaxThr) void k_combine(TokenArgs a) {
 #pragma unroll
       for (int i = 0; i < 16; ++i)
         if (b + i < n)
-          v[i] = s_x16[b + i] ? x16_unpack(x16_load_raw(s_rows[b + i], 0, d, c))
+          v[i] = s_x16[b + i] ? x16_unpack4(*(const uint4*)(s_rows[b + i] + (c & ~7) * 2), (c >> 2) & 1)
                               : *(const float4*)(s_rows[b + i] + c * 4);
 #pragma unroll
       for (int i = 0; i < 16; ++i)
@@ -290,32 +290,33 @@ __device__ __forceinline__ void token_meta_fast(const TokenArgs& a, int t, int (
   }
 }
 
-// Raw row segment (4 values at column c): loaded in one pass, converted in a
-// later one, so every load of a thread is in flight before the first use.
+// Raw row segment (4 values at column c; x16: the 8-value group holding
+// them): loaded in one pass, converted in a later one, so every load of a
+// thread is in flight before the first use.
 template <bool X16>
 struct Raw4 {
-  using T = typename std::conditional<X16, X16x4, float4>::type;
+  using T = typename std::conditional<X16, uint4, float4>::type;
   T v;
 };
 template <bool X16>
 __device__ __forceinline__ Raw4<X16> ldraw(const float* base, int64_t row, int64_t ld, int c) {
   Raw4<X16> r;
   if constexpr (X16)
-    r.v = x16_load_raw(base, row, ld, c);
+    r.v = x16_load8(base, row, ld, c);
   else
     r.v = *(const float4*)(base + row * ld + c);
   return r;
 }
-// Conversion in the arithmetic pass. x16 words go through an empty asm
-// first: a row that is loaded only under a condition is otherwise merged with
-// the skipped path's placeholder after the unpacking's first operations, which
-// the compiler then performs in the load branch, right after the load (and
-// waits for it there).
+// Conversion in the arithmetic pass (c: the column the segment was loaded
+// at). x16 words go through an empty asm first: a row that is loaded only
+// under a condition is otherwise merged with the skipped path's placeholder
+// after the unpacking's first operations, which the compiler then performs in
+// the load branch, right after the load (and waits for it there).
 template <bool X16>
-__device__ __forceinline__ float4 cvt(Raw4<X16> r) {
+__device__ __forceinline__ float4 cvt(Raw4<X16> r, int c) {
   if constexpr (X16) {
-    asm volatile("" : "+v"(r.v.m.x), "+v"(r.v.m.y), "+v"(r.v.e));
-    return x16_unpack(r.v);
+    asm volatile("" : "+v"(r.v.x), "+v"(r.v.y), "+v"(r.v.z), "+v"(r.v.w));
+    return x16_unpack4(r.v, (c >> 2) & 1);
   } else {
     return r.v;
   }
@@ -350,12 +351,12 @@ __global__ __launch_bounds__(kFastThr) void k_swiglu_fast(TokenArgs a) {
   for (int j = 0; j < kFastK; ++j) {
     h[j] = make_float4(0.f, 0.f, 0.f, 0.f);
     if (!(fl[NL][j] & 1)) continue;
-    float4 g = cvt<X16>(gv[j][0]), u = cvt<X16>(uv[j][0]);
+    float4 g = cvt<X16>(gv[j][0], c), u = cvt<X16>(uv[j][0], f + c);
 #pragma unroll
     for (int l = 1; l <= NL; ++l) {
       if (!(fl[l][j] & 2) || (merged && l < NL)) continue;
-      add4(g, cvt<X16>(gv[j][l]));
-      add4(u, cvt<X16>(uv[j][l]));
+      add4(g, cvt<X16>(gv[j][l], c));
+      add4(u, cvt<X16>(uv[j][l], f + c));
     }
     h[j] = make_float4(w[j] * silu_mul(g.x, u.x), w[j] * silu_mul(g.y, u.y), w[j] * silu_mul(g.z, u.z),
                        w[j] * silu_mul(g.w, u.w));
@@ -403,8 +404,7 @@ __global__ __launch_bounds__(kFastThr) void k_swiglu_fast(TokenArgs a) {
 }
 
 // x16 gate|up rows and fp16 activation sums on every stored level, 8
-// columns per thread: one 16-byte mantissa load and one 2-byte exponent load
-// per row half (half the load instructions of k_swiglu_fast); whole rows per
+// columns per thread: one 16-byte load (an x16 group) per row half; whole rows per
 // workgroup (threads past f / 8 only join the token's scale reduction).
 // Same sums, in the same order, as k_swiglu_fast.
 template <int NL, bool MERGED>
@@ -412,30 +412,20 @@ __global__ __launch_bounds__(kFastThr) void k_swiglu_x16w(TokenArgs a) {
   const int t = blockIdx.x, f = a.f;
   const int c = threadIdx.x * 8;
   const bool act = c < f;
-  const int64_t rb = x16_row_bytes(2 * (int64_t)f);
+  const int64_t ld = 2 * (int64_t)f;  // values per gate|up row
   int row[NL + 1][kFastK], fl[NL + 1][kFastK];
   float w[kFastK];
   token_meta_fast<NL>(a, t, row, fl, w);
   constexpr bool merged = MERGED;  // (a.merged, as a template argument)
-  struct Raw8 {
-    uint4 m;
-    uint32_t e;
-  };
+  typedef uint4 Raw8;  // one x16 group
   auto ld8 = [&](const float* base, int r, int col) {
-    const uint8_t* rp = (const uint8_t*)base + (int64_t)r * rb;
-    Raw8 v;
-    v.m = *(const uint4*)(rp + 2 * col);
-    v.e = *(const uint16_t*)(rp + 4 * f + (col >> 2));
-    return v;
+    return *(const uint4*)((const uint8_t*)base + ((int64_t)r * ld + col) * 2);
   };
   auto add8 = [&](float4 (&acc)[2], const Raw8& v) {
-    X16x4 q0, q1;
-    q0.m = make_uint2(v.m.x, v.m.y);
-    q0.e = v.e & 0xFFu;
-    q1.m = make_uint2(v.m.z, v.m.w);
-    q1.e = v.e >> 8;
-    add4(acc[0], x16_unpack(q0));
-    add4(acc[1], x16_unpack(q1));
+    float4 va, vb;
+    x16_unpack8(v, va, vb);
+    add4(acc[0], va);
+    add4(acc[1], vb);
   };
   auto live = [&](int l, int j) { return (fl[l][j] & 2) && !(merged && l < NL); };
   Raw8 gv[kFastK][NL + 1], uv[kFastK][NL + 1];
@@ -536,7 +526,7 @@ __global__ __launch_bounds__(kFastThr) void k_combine_fast(TokenArgs a) {
   for (int l = 0; l <= NL; ++l)
 #pragma unroll
     for (int j = 0; j < kFastK; ++j)
-      if ((fl[l][j] & 3) == 3 && !(merged && l > 0 && l < NL)) add4(acc, cvt<X16>(v[l][j]));
+      if ((fl[l][j] & 3) == 3 && !(merged && l > 0 && l < NL)) add4(acc, cvt<X16>(v[l][j], c));
   if (a.out_dtype == LX_F32) {
     *(float4*)((float*)a.out + (int64_t)t * d + c) = acc;
   } else {
@@ -549,9 +539,9 @@ __global__ __launch_bounds__(kFastThr) void k_combine_fast(TokenArgs a) {
   }
 }
 
-// x16 rows, CPT (8 or 16) columns per thread: 16-byte mantissa loads and
-// one 2- or 4-byte exponent load per row (a fraction of the load
-// instructions of 4 columns per thread); otherwise as k_combine_fast.
+// x16 rows, CPT (8 or 16) columns per thread: one 16-byte load per x16 group
+// and row (a fraction of the load instructions of 4 columns per thread);
+// otherwise as k_combine_fast.
 template <int NL, int CPT, bool MERGED>
 __global__ __launch_bounds__(kFastThr) void k_combine_x16w(TokenArgs a) {
   constexpr int NG = CPT / 4;  // 4-value groups per thread
@@ -564,21 +554,15 @@ __global__ __launch_bounds__(kFastThr) void k_combine_x16w(TokenArgs a) {
   // (a.merged, as a template argument: the intermediate levels' rows are
   // never loaded and take no registers)
   constexpr bool merged = MERGED;
-  const int64_t rb = x16_row_bytes(d);
   uint4 mv[NL + 1][kFastK][NG / 2];
-  uint32_t ev[NL + 1][kFastK];
 #pragma unroll
   for (int l = 0; l <= NL; ++l)
 #pragma unroll
     for (int j = 0; j < kFastK; ++j)
       if ((fl[l][j] & 3) == 3 && !(merged && l > 0 && l < NL)) {
-        const uint8_t* rp = (const uint8_t*)a.y[l] + (int64_t)row[l][j] * rb;
+        const uint8_t* rp = (const uint8_t*)a.y[l] + ((int64_t)row[l][j] * d + c) * 2;
 #pragma unroll
-        for (int h = 0; h < NG / 2; ++h) mv[l][j][h] = *(const uint4*)(rp + 2 * c + 16 * h);
-        if constexpr (NG == 2)
-          ev[l][j] = *(const uint16_t*)(rp + 2 * d + (c >> 2));
-        else
-          ev[l][j] = *(const uint32_t*)(rp + 2 * d + (c >> 2));
+        for (int h = 0; h < NG / 2; ++h) mv[l][j][h] = *(const uint4*)(rp + 16 * h);
       }
   float4 acc[NG];
 #pragma unroll
@@ -589,12 +573,11 @@ __global__ __launch_bounds__(kFastThr) void k_combine_x16w(TokenArgs a) {
     for (int j = 0; j < kFastK; ++j)
       if ((fl[l][j] & 3) == 3 && !(merged && l > 0 && l < NL)) {
 #pragma unroll
-        for (int g = 0; g < NG; ++g) {
-          const uint4 m = mv[l][j][g >> 1];
-          X16x4 q;
-          q.m = (g & 1) ? make_uint2(m.z, m.w) : make_uint2(m.x, m.y);
-          q.e = (ev[l][j] >> (8 * g)) & 0xFFu;
-          add4(acc[g], x16_unpack(q));
+        for (int h = 0; h < NG / 2; ++h) {
+          float4 va, vb;
+          x16_unpack8(mv[l][j][h], va, vb);
+          add4(acc[2 * h], va);
+          add4(acc[2 * h + 1], vb);
         }
       }
   if (a.out_dtype == LX_F32) {

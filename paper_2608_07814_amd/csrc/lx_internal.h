@@ -11,103 +11,81 @@ namespace lx {
 
 // ---------------------------------------------------------------- x16 rows
 // Intermediates that only the elementwise kernels read back (gate|up
-// outputs, down outputs) are stored as groups of 4 consecutive values that
-// share one exponent: the biased exponent byte E of the group's largest
-// magnitude (mx in [2^(E-127), 2^(E-126))), and each value v as the 16-bit
-// signed normalized integer m = round(32767 * v * 2^(126 - E)) (|v| 2^(126-E)
-// < 1, so |m| <= 32767), i.e. v = m / 32767 * 2^(E - 126). The error of a
-// value is at most 2^-15 of the group's largest magnitude. One conversion
-// instruction (v_cvt_pknorm_i16_f32: clamp to [-1, 1], scale by 32767, round
-// to nearest) encodes two values. A row of n values (n a multiple of 32) is
-// 9n/4 bytes: the n mantissas (2n bytes), then the n/4 exponent bytes; a
-// lane's 4 values are one 8-byte word and one byte.
-struct X16x4 {
-  uint2 m;    // mantissas 0, 1 | 2, 3 (low half first)
-  uint32_t e; // exponent byte (low 8 bits)
-};
-
-__host__ __device__ __forceinline__ int64_t x16_row_bytes(int64_t n) { return n * 9 / 4; }
-
+// outputs, down outputs) are stored as groups of 8 consecutive values (a
+// group starts at a column that is a multiple of 8) in 16 bytes: eight
+// 16-bit slots. They share one exponent, the biased exponent byte E of the
+// group's largest magnitude (mx in [2^(E-127), 2^(E-126))). Slot i holds value
+// i as the 15-bit signed integer m = round(32767 * v * 2^(125 - E)) (|v|
+// 2^(125-E) < 1/2, so -16384 <= m <= 16383) in its bits 15..1, and bit i of E
+// in its bit 0: v = m / 32767 * 2^(E - 125). The error of a value is at most
+// half a step, 2^-15 of 2^(E-126), i.e. 2^-14 of the group's largest magnitude. One
+// conversion instruction (v_cvt_pknorm_i16_f32: clamp to [-1, 1], scale by
+// 32767, round to nearest) encodes two values. A row of n values (n a multiple
+// of 8) is 2n bytes; the exponent travels with the mantissas, so a group is
+// one 16-byte store and one 16-byte load.
 typedef short x16_short2 __attribute__((ext_vector_type(2)));
 
-__device__ __forceinline__ X16x4 x16_pack(float4 v) {
-  const float mx = fmaxf(fmaxf(fabsf(v.x), fabsf(v.y)), fmaxf(fabsf(v.z), fabsf(v.w)));
-  const int eb = (int)((__float_as_uint(mx) >> 23) & 0xFFu);
-  const int sh = 126 - eb;
-  const x16_short2 a = __builtin_amdgcn_cvt_pknorm_i16(ldexpf(v.x, sh), ldexpf(v.y, sh));
-  const x16_short2 b = __builtin_amdgcn_cvt_pknorm_i16(ldexpf(v.z, sh), ldexpf(v.w, sh));
-  X16x4 w;
-  w.m.x = __builtin_bit_cast(uint32_t, a);
-  w.m.y = __builtin_bit_cast(uint32_t, b);
-  w.e = (uint32_t)eb;
-  return w;
+// values [0, 4) = a, [4, 8) = b of a group
+__device__ __forceinline__ uint4 x16_pack8(float4 a, float4 b) {
+  const float mx = fmaxf(fmaxf(fmaxf(fabsf(a.x), fabsf(a.y)), fmaxf(fabsf(a.z), fabsf(a.w))),
+                         fmaxf(fmaxf(fabsf(b.x), fabsf(b.y)), fmaxf(fabsf(b.z), fabsf(b.w))));
+  const uint32_t e = (__float_as_uint(mx) >> 23) & 0xFFu;
+  const int sh = 125 - (int)e;
+  auto pk = [&](float u, float v, int k) {
+    const x16_short2 q = __builtin_amdgcn_cvt_pknorm_i16(ldexpf(u, sh), ldexpf(v, sh));
+    // exponent bits 2k, 2k + 1 at bit 0 of each 16-bit half
+    const uint32_t t = __builtin_amdgcn_ubfe(e, 2 * k, 2);
+    const uint32_t eb = (t | (t << 15)) & 0x10001u;
+    // each half shifted up by one (its top bit is a copy of the sign), the
+    // exponent bits into the freed low bits
+    return ((__builtin_bit_cast(uint32_t, q) << 1) & 0xFFFEFFFEu) | eb;
+  };
+  return make_uint4(pk(a.x, a.y, 0), pk(a.z, a.w, 1), pk(b.x, b.y, 2), pk(b.z, b.w, 3));
 }
 
-__device__ __forceinline__ float4 x16_unpack(X16x4 w) {
-  const int sh = (int)(w.e & 0xFFu) - 126;
-  constexpr float inv = 1.0f / 32767.0f;
-  auto d = [&](uint32_t h) { return ldexpf((float)(int32_t)(int16_t)(uint16_t)h * inv, sh); };
-  return make_float4(d(w.m.x & 0xFFFFu), d(w.m.x >> 16), d(w.m.y & 0xFFFFu), d(w.m.y >> 16));
+// the group's exponent byte from its slots' low bits
+__device__ __forceinline__ uint32_t x16_exp8(const uint4& w) {
+  return (w.x & 1u) | ((w.x >> 15) & 2u) | ((w.y & 1u) << 2) | ((w.y >> 13) & 8u) | ((w.z & 1u) << 4) |
+         ((w.z >> 11) & 32u) | ((w.w & 1u) << 6) | ((w.w >> 9) & 128u);
 }
 
-// Values [c, c + 4) of row `row` (n values per row) at base.
-__device__ __forceinline__ void x16_store(void* base, int64_t row, int64_t n, int64_t c, float4 v) {
-  uint8_t* const rp = (uint8_t*)base + row * x16_row_bytes(n);
-  const X16x4 w = x16_pack(v);
-  *(uint2*)(rp + 2 * c) = w.m;
-  rp[2 * n + (c >> 2)] = (uint8_t)w.e;
+// values 4 h .. 4 h + 3 of a group (h = 0 or 1)
+__device__ __forceinline__ float4 x16_unpack4(const uint4& w, int h) {
+  const float s = ldexpf(1.0f / 32767.0f, (int)x16_exp8(w) - 125);
+  const uint32_t p = h ? w.z : w.x, q = h ? w.w : w.y;
+  // (int32)(slot << 16) >> 17 and (int32)slot >> 17: the signed 15-bit value
+  return make_float4((float)((int32_t)(p << 16) >> 17) * s, (float)((int32_t)p >> 17) * s,
+                     (float)((int32_t)(q << 16) >> 17) * s, (float)((int32_t)q >> 17) * s);
 }
 
-// A lane's x16 stores down a column group: rows row, row + step, row + 2 step,
-// ... of a row-major x16 matrix with n values per row, columns [c, c + 4);
-// the row address advances by a constant stride instead of being multiplied
-// out per row.
-struct X16Rows {
-  uint8_t* m;        // mantissa word of the current row
-  int64_t stride;    // bytes between consecutive rows of this lane
-  int32_t eoff;      // exponent byte, relative to m
-  __device__ __forceinline__ X16Rows(void* base, int64_t n, int64_t row, int step, int64_t c) {
-    const int64_t rb = x16_row_bytes(n);
-    m = (uint8_t*)base + row * rb + 2 * c;
-    stride = rb * step;
-    eoff = (int32_t)(2 * n + (c >> 2) - 2 * c);
-  }
-  __device__ __forceinline__ void store(float4 v) const {
-    const X16x4 w = x16_pack(v);
-    *(uint2*)m = w.m;
-    m[eoff] = (uint8_t)w.e;
-  }
-  __device__ __forceinline__ void next() { m += stride; }
-};
+// all 8 values of a group
+__device__ __forceinline__ void x16_unpack8(const uint4& w, float4& a, float4& b) {
+  const float s = ldexpf(1.0f / 32767.0f, (int)x16_exp8(w) - 125);
+  auto lo = [](uint32_t u) { return (float)((int32_t)(u << 16) >> 17); };
+  auto hi = [](uint32_t u) { return (float)((int32_t)u >> 17); };
+  a = make_float4(lo(w.x) * s, hi(w.x) * s, lo(w.y) * s, hi(w.y) * s);
+  b = make_float4(lo(w.z) * s, hi(w.z) * s, lo(w.w) * s, hi(w.w) * s);
+}
 
-// The same down a group of 8 columns [c, c + 8) (c a multiple of 8, n a
-// multiple of 64, base 16-byte aligned): one 16-byte mantissa store and one
-// 2-byte exponent store per row, half the store instructions of X16Rows.
+// The group holding column c of row `row` (n values per row) at base.
+__device__ __forceinline__ uint4 x16_load8(const void* base, int64_t row, int64_t n, int64_t c) {
+  return *(const uint4*)((const uint8_t*)base + (row * n + (c & ~(int64_t)7)) * 2);
+}
+
+// A lane's x16 stores down a group of 8 columns [c, c + 8) (c a multiple of
+// 8): rows row, row + step, row + 2 step, ... of a row-major x16 matrix with
+// n values per row, one 16-byte store per row; the row address advances by a
+// constant stride instead of being multiplied out per row.
 struct X16Rows8 {
   uint8_t* m;
   int64_t stride;
-  int32_t eoff;
   __device__ __forceinline__ X16Rows8(void* base, int64_t n, int64_t row, int step, int64_t c) {
-    const int64_t rb = x16_row_bytes(n);
-    m = (uint8_t*)base + row * rb + 2 * c;
-    stride = rb * step;
-    eoff = (int32_t)(2 * n + (c >> 2) - 2 * c);
+    m = (uint8_t*)base + (row * n + c) * 2;
+    stride = n * step * 2;
   }
-  __device__ __forceinline__ void store(float4 a, float4 b) const {
-    const X16x4 wa = x16_pack(a), wb = x16_pack(b);
-    *(uint4*)m = make_uint4(wa.m.x, wa.m.y, wb.m.x, wb.m.y);
-    *(uint16_t*)(m + eoff) = (uint16_t)((wa.e & 0xFFu) | ((wb.e & 0xFFu) << 8));
-  }
+  __device__ __forceinline__ void store(float4 a, float4 b) const { *(uint4*)m = x16_pack8(a, b); }
   __device__ __forceinline__ void next() { m += stride; }
 };
-
-__device__ __forceinline__ X16x4 x16_load_raw(const void* base, int64_t row, int64_t n, int64_t c) {
-  const uint8_t* const rp = (const uint8_t*)base + row * x16_row_bytes(n);
-  X16x4 w;
-  w.m = *(const uint2*)(rp + 2 * c);
-  w.e = rp[2 * n + (c >> 2)];
-  return w;
-}
 
 // Output format of a GEMM: fp32, a bf16 (hi, lo) pair, x16, or OUT_F16T:
 // fp16 [rows][ldc] with one power-of-two scale per tile (the tile spans whole
@@ -330,7 +308,7 @@ hipError_t launch_gemm(const GemmArgs& g, lx_dtype dt, AMode am, int grid_x, hip
 // is bf16, K and Kb are multiples of 64, the parts either share A columns or
 // the part boundary is a multiple of BN, and A's element count fits in 31
 // bits. fp32 and x16 output is written at columns [0, ncols[0] + ncols[1]) of
-// C (the parts adjacent; ldc in values, an x16 row is 9 ldc / 4 bytes); bf16
+// C (the parts adjacent; ldc in values, an x16 row is 2 ldc bytes); bf16
 // (hi, lo) output writes part p's hi values at columns base_p + c and lo
 // values at base_p + ncols[p] + c, base_0 = 0, base_1 = 2 ncols[0] (ldc in
 // bf16 elements).
