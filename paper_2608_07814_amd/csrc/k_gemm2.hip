@@ -143,8 +143,12 @@ __device__ __forceinline__ void wait_slabs(int ahead) {
 // the other's MFMAs), else 4 (one per SIMD, a 2x2 grid).
 template <int BM, int BN>
 struct BigCfg {
-  static constexpr int NW = (BM == 256 && BN == 256) ? 8 : 4;
-  static constexpr int WGN = NW / 2;  // wavefronts along N
+  // 256 x 256 and 256 x 128 tiles: 8 wavefronts (two per SIMD), in a 2 x 4
+  // grid of 128 x 64 blocks and a 4 x 2 grid of 64 x 64 blocks; the others 4
+  // wavefronts in a 2 x 2 grid
+  static constexpr int NW = (BM == 256 && (BN == 256 || BN == 128)) ? 8 : 4;
+  static constexpr int WGN = (BM == 256 && BN == 256) ? 4 : 2;  // wavefronts along N
+  static constexpr int WGM = NW / WGN;                          // wavefronts along M
   static constexpr int NTHR = NW * 64;
   static constexpr int WPE = NW / 4;  // wavefronts per SIMD
 };
@@ -179,9 +183,9 @@ __device__ __forceinline__ void gemm_big_body(const GemmArgs& p, int ntn, const 
   static_assert(!LO8 || (BM == 256 && BN == 256), "fp8 lo: 256 x 256 tiles");
   static_assert(!(LO8 && F16), "one precision mode at a time");
   constexpr int NTHR = BigCfg<BM, BN>::NTHR, WGN = BigCfg<BM, BN>::WGN;
-  constexpr int MI = BM / 64;              // 32-row MFMA blocks per wavefront
-  constexpr int NI = BN / (32 * WGN);      // 32-column MFMA blocks per wavefront
-  constexpr int WM = BM / 2, WN = BN / WGN;
+  constexpr int WM = BM / BigCfg<BM, BN>::WGM, WN = BN / WGN;  // a wavefront's block
+  constexpr int MI = WM / 32;              // 32-row MFMA blocks per wavefront
+  constexpr int NI = WN / 32;              // 32-column MFMA blocks per wavefront
   constexpr int A_ROUNDS = BM * 8 / NTHR;  // 16-byte chunks per thread per slab
   constexpr int B_ROUNDS = BN * 8 / NTHR;
   constexpr int ROUNDS = A_ROUNDS + B_ROUNDS;
