@@ -3,7 +3,8 @@
 //
 //   * BM x BN output tile (BM = 128 or 256, BN = 64, 128 or 256); 256x256
 //     tiles use 8 wavefronts (2 x 4 grid of 128x64 blocks, two per SIMD),
-//     the others 4 (2 x 2 grid), each block as MFMA 32x32x16 sub-blocks;
+//     256x128 tiles 8 (4 x 2 grid of 64x64 blocks), the others 4 (2 x 2
+//     grid), each block as MFMA 32x32x16 sub-blocks;
 //   * both operands go HBM -> LDS with global_load_lds_dwordx4 (16 B per lane,
 //     no staging registers) into a 2-stage LDS ring, so the next K-slab
 //     streams in while the current one feeds the MFMAs; inside a slab the
