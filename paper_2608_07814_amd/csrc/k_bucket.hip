@@ -25,6 +25,25 @@ namespace {
 // correction levels together
 constexpr int kSmallMaxNodes = 1024, kSmallMaxTree = 1024;
 constexpr int kPlaceThr = 256;  // placement: threads per 64-token tile
+constexpr int kScanThr = 1024;  // scan: threads of the one workgroup per level
+
+// Inclusive prefix sum over the 64 lanes of a wavefront; every lane must be
+// active. Row shifts (DPP) scan each row of 16 lanes, then each row adds the
+// totals of the rows before it, read from lanes 15, 31 and 47.
+__device__ __forceinline__ int wave_incl_scan(int x) {
+  x += __builtin_amdgcn_update_dpp(0, x, 0x111, 0xf, 0xf, false);  // row_shr:1
+  x += __builtin_amdgcn_update_dpp(0, x, 0x112, 0xf, 0xf, false);  // row_shr:2
+  x += __builtin_amdgcn_update_dpp(0, x, 0x114, 0xf, 0xf, false);  // row_shr:4
+  x += __builtin_amdgcn_update_dpp(0, x, 0x118, 0xf, 0xf, false);  // row_shr:8
+  const int r0 = __builtin_amdgcn_readlane(x, 15), r1 = __builtin_amdgcn_readlane(x, 31),
+            r2 = __builtin_amdgcn_readlane(x, 47);
+  const int row = (threadIdx.x & 63) >> 4;
+  return x + (row >= 1 ? r0 : 0) + (row >= 2 ? r1 : 0) + (row >= 3 ? r2 : 0);
+}
+
+// Tile counts of a node: tile heights are powers of two (static_asserts at
+// their definitions), so the division is a shift.
+__device__ __forceinline__ int n_tiles_of(int cnt, int bm) { return (cnt + bm - 1) >> __builtin_ctz(bm); }
 
 // Workgroup barrier for LDS communication only: waits for this wave's LDS
 // operations, not for its global stores (which nothing in the workgroup
@@ -192,20 +211,12 @@ __global__ __launch_bounds__(kRouteHistThr) void k_bucket_hist_route(BucketArgs 
 __device__ inline int block_exscan(int v, int* s_wave, int& total) {
   const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
   const int nwaves = blockDim.x >> 6;
-  int incl = v;
-  for (int o = 1; o < 64; o <<= 1) {
-    const int u = __shfl_up(incl, o, 64);
-    if (lane >= o) incl += u;
-  }
+  const int incl = wave_incl_scan(v);
   if (lane == 63) s_wave[wave] = incl;
   lds_barrier();
   if (threadIdx.x < 64) {
-    int w = threadIdx.x < nwaves ? s_wave[threadIdx.x] : 0;
-    int wi = w;
-    for (int o = 1; o < 64; o <<= 1) {
-      const int u = __shfl_up(wi, o, 64);
-      if (threadIdx.x >= o) wi += u;
-    }
+    const int w = threadIdx.x < nwaves ? s_wave[threadIdx.x] : 0;
+    const int wi = wave_incl_scan(w);
     if (threadIdx.x < nwaves) s_wave[threadIdx.x] = wi - w;
     if (threadIdx.x == nwaves - 1) s_wave[63] = wi;
   }
@@ -246,7 +257,7 @@ __device__ inline void build_tile_tables(const BucketLevel& lv, const int32_t* o
     TileEntry* tiles = lv.tiles[tab];
     int my_tiles = 0;
 #pragma unroll
-    for (int u = 0; u < kMaxChunk; ++u) my_tiles += (cnt_[u] + bm - 1) / bm;
+    for (int u = 0; u < kMaxChunk; ++u) my_tiles += n_tiles_of(cnt_[u], bm);
     int ntiles = 0;
     int tpos = block_exscan(my_tiles, s_wave, ntiles);
 #pragma unroll
@@ -265,14 +276,18 @@ __device__ inline void build_tile_tables(const BucketLevel& lv, const int32_t* o
   }
 }
 
-__global__ __launch_bounds__(1024) void k_bucket_scan(BucketArgs a) {
+// CH: entries per thread kept in registers (8, 16 or 32, the smallest that
+// holds the largest level's chunk).
+template <int CH>
+__global__ __launch_bounds__(kScanThr) void k_bucket_scan(BucketArgs a) {
   __shared__ int s_wave[64];
   extern __shared__ int s_off[];  // [N + 1] node offsets
   const int l = blockIdx.x;
   const BucketLevel& lv = a.lv[l];
   const int N = lv.n_nodes, NT = a.n_tok_tiles;
   const int64_t total = (int64_t)N * NT;
-  const int nth = blockDim.x, tid = threadIdx.x;
+  constexpr int nth = kScanThr;
+  const int tid = threadIdx.x;
   for (int i = tid; i < lv.n_split_cnt; i += nth) lv.split_cnt[i] = 0u;
 
   // exclusive scan of hist in (node, tile) order, in place; entry (n, 0)
@@ -280,61 +295,94 @@ __global__ __launch_bounds__(1024) void k_bucket_scan(BucketArgs a) {
   // Each thread owns a chunk of consecutive entries (a multiple of 4, so it
   // is read and written as 16-byte vectors): up to CH entries stay in
   // registers between the two passes, all loaded at once; longer chunks are
-  // read CH at a time in both passes.
-  constexpr int CH = 32;
+  // read CH at a time in both passes. A block of CH entries handles only its
+  // m valid ones.
   const int64_t chunk = ((total + nth - 1) / nth + 3) & ~(int64_t)3;
   const int64_t b = (int64_t)tid * chunk;
   const int64_t e = b + chunk < total ? b + chunk : total;
+  auto valid = [&](int64_t c0) { return (int)(e - c0 < CH ? e - c0 : CH); };
   int v[CH];
+#pragma unroll
+  for (int u = 0; u < CH; ++u) v[u] = 0;
   auto load = [&](int64_t c0) {
+    const int m = valid(c0);
 #pragma unroll
     for (int u = 0; u < CH; u += 4) {
-      if (c0 + u + 4 <= e) {
+      if (u + 4 <= m) {
         const int4 q = *(const int4*)(lv.hist + c0 + u);
         v[u] = q.x;
         v[u + 1] = q.y;
         v[u + 2] = q.z;
         v[u + 3] = q.w;
-      } else {
+      } else if (u < m) {
 #pragma unroll
-        for (int w = 0; w < 4; ++w) v[u + w] = c0 + u + w < e ? lv.hist[c0 + u + w] : 0;
+        for (int w = 0; w < 4; ++w) v[u + w] = u + w < m ? lv.hist[c0 + u + w] : 0;
       }
     }
   };
   int local = 0;
   for (int64_t c0 = b; c0 < e; c0 += CH) {
     load(c0);
+    const int m = valid(c0);
 #pragma unroll
-    for (int u = 0; u < CH; ++u) local += v[u];
+    for (int u = 0; u < CH; ++u) local += u < m ? v[u] : 0;
   }
   int grand = 0;
   int run = block_exscan(local, s_wave, grand);
-  // (node, tile) of entry b, advanced incrementally (no division per entry)
-  int node = (int)(b / NT), tile = (int)(b - (int64_t)node * NT);
+  // next node start at or after b (its entries begin at nnode * NT)
+  int nnode = 0;  // at most N (LX_MAX_NODES)
+  if (b < e) {
+    if (b < ((int64_t)1 << 31)) {
+      const uint32_t q = (uint32_t)b / (uint32_t)NT;
+      nnode = (int)q + ((int64_t)q * NT != b ? 1 : 0);
+    } else {
+      nnode = (int)((b + NT - 1) / NT);
+    }
+  }
   for (int64_t c0 = b; c0 < e; c0 += CH) {
     if (e - b > CH) load(c0);  // chunk larger than the register cache: reload
+    const int m = valid(c0);
+    // position of the next node start within this block (CH: none)
+    const int64_t nx = (int64_t)nnode * NT - c0;
+    int nxt = nx < CH ? (int)nx : CH;
+    if (NT >= CH) {
+      // at most one node start in the block: its offset is selected, no
+      // branches per entry (entries past m are not stored)
+      int bval = 0;
 #pragma unroll
-    for (int u = 0; u < CH; ++u) {
-      const int64_t i = c0 + u;
-      const int cnt = v[u];
-      if (i < e) {
+      for (int u = 0; u < CH; ++u) {
+        const int cnt = u < m ? v[u] : 0;
         v[u] = run;
-        if (tile == 0) s_off[node] = run;
+        bval = u == nxt ? run : bval;
         run += cnt;
-        if (++tile == NT) {
-          tile = 0;
-          ++node;
+      }
+      if (nxt < m) {
+        s_off[nnode] = bval;
+        ++nnode;
+      }
+    } else {
+#pragma unroll
+      for (int u = 0; u < CH; ++u) {
+        if (u < m) {
+          const int cnt = v[u];
+          v[u] = run;
+          if (u == nxt) {
+            s_off[nnode] = run;
+            ++nnode;
+            nxt += NT;
+          }
+          run += cnt;
         }
       }
     }
 #pragma unroll
     for (int u = 0; u < CH; u += 4) {
-      if (c0 + u + 4 <= e) {
+      if (u + 4 <= m) {
         *(int4*)(lv.hist + c0 + u) = make_int4(v[u], v[u + 1], v[u + 2], v[u + 3]);
-      } else {
+      } else if (u < m) {
 #pragma unroll
         for (int w = 0; w < 4; ++w)
-          if (c0 + u + w < e) lv.hist[c0 + u + w] = v[u + w];
+          if (u + w < m) lv.hist[c0 + u + w] = v[u + w];
       }
     }
   }
@@ -439,13 +487,8 @@ __device__ inline int small_node(const SmallLds& S, const PrepareArgs& pa, int L
 
 
 __device__ inline int wave_exscan(int v, int& total) {
-  const int lane = threadIdx.x & 63;
-  int incl = v;
-  for (int o = 1; o < 64; o <<= 1) {
-    const int u = __shfl_up(incl, o, 64);
-    if (lane >= o) incl += u;
-  }
-  total = __shfl(incl, 63, 64);
+  const int incl = wave_incl_scan(v);
+  total = __builtin_amdgcn_readlane(incl, 63);
   return incl - v;
 }
 
@@ -544,7 +587,7 @@ __global__ __launch_bounds__(1024) void k_bucket_small(PrepareArgs pa, BucketArg
         int mine = 0;
         for (int n = nb; n < ne; ++n) {
           const int cnt = S.off[n + 1] - S.off[n];
-          if ((lv.work_all || S.fac[n] >= 0) && cnt > 0) mine += (cnt + bm - 1) / bm;
+          if ((lv.work_all || S.fac[n] >= 0) && cnt > 0) mine += n_tiles_of(cnt, bm);
         }
         int ntiles = 0;
         int tpos = wave_exscan(mine, ntiles);
@@ -655,8 +698,20 @@ hipError_t launch_bucket_hist(const BucketArgs& a, hipStream_t s) {
 
 hipError_t launch_bucket_scan(const BucketArgs& a, hipStream_t s) {
   int mx = 1;
-  for (int l = 0; l <= a.L; ++l) mx = a.lv[l].n_nodes > mx ? a.lv[l].n_nodes : mx;
-  hipLaunchKernelGGL(k_bucket_scan, dim3(a.L + 1), dim3(1024), (size_t)(mx + 1) * sizeof(int), s, a);
+  int64_t chunk = 0;  // the kernel's per-thread chunk at the largest level
+  for (int l = 0; l <= a.L; ++l) {
+    mx = a.lv[l].n_nodes > mx ? a.lv[l].n_nodes : mx;
+    const int64_t total = (int64_t)a.lv[l].n_nodes * a.n_tok_tiles;
+    const int64_t c = ((total + kScanThr - 1) / kScanThr + 3) & ~(int64_t)3;
+    chunk = c > chunk ? c : chunk;
+  }
+  const size_t lds = (size_t)(mx + 1) * sizeof(int);
+  if (chunk <= 8)
+    hipLaunchKernelGGL(k_bucket_scan<8>, dim3(a.L + 1), dim3(kScanThr), lds, s, a);
+  else if (chunk <= 16)
+    hipLaunchKernelGGL(k_bucket_scan<16>, dim3(a.L + 1), dim3(kScanThr), lds, s, a);
+  else
+    hipLaunchKernelGGL(k_bucket_scan<32>, dim3(a.L + 1), dim3(kScanThr), lds, s, a);
   return hipGetLastError();
 }
 

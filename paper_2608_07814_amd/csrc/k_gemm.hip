@@ -27,6 +27,7 @@ typedef float f32x16 __attribute__((ext_vector_type(16)));
 typedef uint16_t u16;
 
 constexpr int BM = 128, BN = 128, BK = 64, NTHR = 256;
+static_assert((BM & (BM - 1)) == 0, "tile heights are powers of two (bucketing shifts)");
 
 __device__ __forceinline__ int swz(int row) { return (row ^ (row >> 3)) & 7; }
 __device__ __forceinline__ int lds_off(int row, int kc) { return row * BK + ((kc ^ swz(row)) << 3); }
@@ -207,6 +208,7 @@ __global__ __launch_bounds__(NTHR) void k_gemm_bf16(GemmArgs p) {
 
 // ------------------------------------------------------------------ fp32 path
 constexpr int FBM = 64, FBN = 64, FBK = 16;
+static_assert((FBM & (FBM - 1)) == 0, "tile heights are powers of two (bucketing shifts)");
 
 __global__ __launch_bounds__(256) void k_gemm_f32(GemmArgs p) {
   if ((int)blockIdx.x >= *p.n_tiles) return;

@@ -313,6 +313,7 @@ hipError_t launch_gemm(const GemmArgs& g, lx_dtype dt, AMode am, int grid_x, hip
 // values at base_p + ncols[p] + c, base_0 = 0, base_1 = 2 ncols[0] (ldc in
 // bf16 elements).
 constexpr int kBigBM = 256;
+static_assert((kBigBM & (kBigBM - 1)) == 0, "tile heights are powers of two (bucketing shifts)");
 bool gemm_big_ok(const GemmArgs& g, int bn, int64_t a_rows_total);
 // The fp8-lo variant (256 x 256 tiles) of the large-tile kernel: hi slabs as
 // above, lo slabs from the fp8 copies with the block-scaled fp8 MFMA.
@@ -390,6 +391,7 @@ hipError_t launch_gemm_seg(const GemmArgs& g, const SegArgs& sa, int grid_tiles,
 // HBM rather than by MFMA work on padding rows. Same operand conventions and
 // applicability as the large-tile kernel (with bn = kSkinnyBN).
 constexpr int kSkinnyBM = 32, kSkinnyBN = 64;
+static_assert((kSkinnyBM & (kSkinnyBM - 1)) == 0, "tile heights are powers of two (bucketing shifts)");
 // Split-K: partial-tile slots per level (three 48 KB-LDS workgroups per
 // compute unit on 256 compute units) and the fewest weight slabs (64 K
 // values) a split covers.
