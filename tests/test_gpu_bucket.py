@@ -33,10 +33,15 @@ def _check(layer, ids, expect_flag=0):
     assert lx.read_device_status(ws) & lx.LX_DEVFLAG_BAD_ID == expect_flag
 
 
-@pytest.mark.parametrize("cfg,T", [(0, 16), (1, 4096), (2, 64), (3, 2000), (3, 16384), (4, 1000), (4, 8192)])
+@pytest.mark.parametrize("cfg,T", [(0, 16), (1, 4096), (2, 64), (3, 2000), (3, 16384), (4, 1000), (4, 4096),
+                                   (4, 8192), (4, 16384)])
 def test_bucket_configs(cfg, T):
-    """Full sizes included: cfg3 at T=16384 (256 token tiles x 32 nodes, the
-    scan's reload branch) and the cfg4 tree at T=8192."""
+    """Full sizes included: cfg3 at T=16384 and the cfg4 tree at T=8192. The
+    scan keeps 8, 16 or 32 histogram entries per thread in registers (the
+    largest level's entries / 1024 threads, rounded up to a multiple of 4):
+    cfg0 at T=16 has fewer token tiles than that block (several node starts
+    per block); the tree at T=4096 takes 16; the tree at T=16384 (256 leaves x
+    256 token tiles: 64 entries per thread) reads its chunk in two blocks."""
     say(f"bucket cfg{cfg} T={T}")
     p = make_problem(cfg, T=T)
     _check(p.layer, p.routing.topk_ids)
