@@ -459,18 +459,22 @@ __global__ __launch_bounds__(256) void k_leaf_maps(LeafMapArgs a) {
 //      wavefront-wide scans;
 //   C  every thread: slot placement, one thread per routing slot.
 // Same results as the four-pass path with one token tile.
+// Levels are processed in pairs (l0, l0 + 1): index q of the per-level
+// arrays is the level's place in its pair. Nodes and ids are below
+// kSmallMaxNodes, so 16 bits hold them (ids outside [0, E) are kept as -1).
 struct SmallLds {
-  unsigned long long mask[2][kSmallMaxNodes];  // alternate levels
-  int32_t off[kSmallMaxNodes + 1];
-  int32_t fac[kSmallMaxNodes];
+  unsigned long long mask[2][kSmallMaxNodes];
+  int32_t off[2][kSmallMaxNodes + 1];
+  int32_t fac[2][kSmallMaxNodes];
   int32_t par[kSmallMaxTree];   // parent arrays of levels 1..L, concatenated
   int32_t fo[kSmallMaxTree];    // factor_of arrays of levels 1..L, concatenated
-  int32_t node[kTokTile * LX_MAX_K];
-  int32_t ids[kTokTile * LX_MAX_K];
+  int16_t node[2][kTokTile * LX_MAX_K];
+  int16_t ids[kTokTile * LX_MAX_K];
   float w[kTokTile * LX_MAX_K];
   int32_t base[kMaxLvl];        // offset of level l's arrays in par / fo
   uint32_t bad;
 };
+static_assert(sizeof(SmallLds) <= 64 * 1024, "single-workgroup bucketing: default LDS limit");
 
 // Node of expert e at level l, or -1 (invalid id or broken path to the root).
 __device__ inline int small_node(const SmallLds& S, const PrepareArgs& pa, int L, int E, int e, int l) {
@@ -515,7 +519,7 @@ __global__ __launch_bounds__(1024) void k_bucket_small(PrepareArgs pa, BucketArg
   uint32_t bad = 0;
   for (int s = tid; s < TK; s += nth) {
     const int e = a.ids[s];
-    S.ids[s] = e;
+    S.ids[s] = (int16_t)(e >= 0 && e < E ? e : -1);
     S.w[s] = a.w ? a.w[s] : 0.f;
     if (e < -1 || e >= E) bad |= LX_DEVFLAG_BAD_ID;
   }
@@ -526,20 +530,20 @@ __global__ __launch_bounds__(1024) void k_bucket_small(PrepareArgs pa, BucketArg
       S.fo[S.base[l] + n] = pa.factor_of[l][n];
     }
   for (int n = tid; n < a.lv[0].n_nodes; n += nth) S.mask[0][n] = 0ull;
+  if (L >= 1)
+    for (int n = tid; n < a.lv[L >= 1 ? 1 : 0].n_nodes; n += nth) S.mask[1][n] = 0ull;
 #pragma unroll
   for (int l = 0; l <= L; ++l)
     for (int i = tid; i < a.lv[l].n_split_cnt; i += nth) a.lv[l].split_cnt[i] = 0u;
   lds_barrier();
 
-#pragma unroll
-  for (int l = 0; l <= L; ++l) {
-    const BucketLevel& lv = a.lv[l];
-    const int N = lv.n_nodes;
-    unsigned long long* const mask = S.mask[l & 1];
-    // A
+  // A: slot nodes, the level's token masks and validated factor indices
+  auto phase_a = [&](const int l, const int q) {
+    const int N = a.lv[l].n_nodes;
+    unsigned long long* const mask = S.mask[q];
     for (int s = tid; s < TK; s += nth) {
       const int n = small_node(S, pa, L, E, S.ids[s], l);
-      S.node[s] = n;
+      S.node[q][s] = (int16_t)n;
       if (n >= 0) atomicOr(&mask[n], 1ull << (s / k));
     }
     for (int n = tid; n < N; n += nth) {
@@ -551,92 +555,120 @@ __global__ __launch_bounds__(1024) void k_bucket_small(PrepareArgs pa, BucketArg
           m = -1;
         }
       }
-      S.fac[n] = m;
+      S.fac[q][n] = m;
     }
     if (l == 0)  // tree check of every expert, routed or not
       for (int e = tid; e < E; e += nth)
         if (L > 0 && small_node(S, pa, L, E, e, 0) < 0) bad |= LX_DEVFLAG_BAD_TREE;
-    lds_barrier();
-    // B
-    if (tid < 64) {
-      const int per = (N + 63) / 64;
-      const int nb = tid * per, ne = nb + per < N ? nb + per : N;
-      int local = 0;
-      for (int n = nb; n < ne; ++n) local += __popcll(mask[n]);
-      int total = 0;
-      int run = wave_exscan(local, total);
-      for (int n = nb; n < ne; ++n) {
-        S.off[n] = run;
-        lv.hist[n] = run;
-        lv.offsets[n] = run;
-        run += __popcll(mask[n]);
-      }
-      if (tid == 0) {
-        S.off[N] = total;
-        lv.offsets[N] = total;
-      }
-      // S.off[ne] is read below but written by the next lane: keep the
-      // compiler from hoisting reads above the writes (a wavefront's LDS
-      // accesses execute in program order)
-      asm volatile("" ::: "memory");
-      __builtin_amdgcn_wave_barrier();
-      asm volatile("" ::: "memory");
-      for (int tab = 0; tab < kNumTab; ++tab) {
-        if (!((lv.tab_mask >> tab) & 1u)) continue;
-        const int bm = lv.tile_bm[tab];
-        int mine = 0;
-        for (int n = nb; n < ne; ++n) {
-          const int cnt = S.off[n + 1] - S.off[n];
-          if ((lv.work_all || S.fac[n] >= 0) && cnt > 0) mine += n_tiles_of(cnt, bm);
-        }
-        int ntiles = 0;
-        int tpos = wave_exscan(mine, ntiles);
-        for (int n = nb; n < ne; ++n) {
-          const int o = S.off[n], cnt = S.off[n + 1] - o;
-          if (!(lv.work_all || S.fac[n] >= 0) || cnt == 0) continue;
-          const int widx = lv.work_all ? n : S.fac[n];
-          for (int r = 0; r < cnt; r += bm) {
-            TileEntry te;
-            te.widx = widx;
-            te.row0 = o + r;
-            te.nrows = cnt - r < bm ? cnt - r : bm;
-            te.node = n;
-            lv.tiles[tab][tpos++] = te;
-          }
-        }
-        if (tid == 0) *lv.n_tiles[tab] = ntiles;
-      }
+  };
+  // B (one wavefront): node offsets by a wavefront scan, then the tile tables
+  auto phase_b = [&](const int l, const int q) {
+    const BucketLevel& lv = a.lv[l];
+    const int N = lv.n_nodes;
+    const unsigned long long* const mask = S.mask[q];
+    int* const off = S.off[q];
+    const int* const fac = S.fac[q];
+    const int lane = tid & 63;
+    const int per = (N + 63) / 64;
+    const int nb = lane * per, ne = nb + per < N ? nb + per : N;
+    int local = 0;
+    for (int n = nb; n < ne; ++n) local += __popcll(mask[n]);
+    int total = 0;
+    int run = wave_exscan(local, total);
+    for (int n = nb; n < ne; ++n) {
+      off[n] = run;
+      lv.hist[n] = run;
+      lv.offsets[n] = run;
+      run += __popcll(mask[n]);
     }
-    lds_barrier();
-    // C
+    if (lane == 0) {
+      off[N] = total;
+      lv.offsets[N] = total;
+    }
+    // off[ne] is read below but written by the next lane: keep the
+    // compiler from hoisting reads above the writes (a wavefront's LDS
+    // accesses execute in program order)
+    asm volatile("" ::: "memory");
+    __builtin_amdgcn_wave_barrier();
+    asm volatile("" ::: "memory");
+    for (int tab = 0; tab < kNumTab; ++tab) {
+      if (!((lv.tab_mask >> tab) & 1u)) continue;
+      const int bm = lv.tile_bm[tab];
+      int mine = 0;
+      for (int n = nb; n < ne; ++n) {
+        const int cnt = off[n + 1] - off[n];
+        if ((lv.work_all || fac[n] >= 0) && cnt > 0) mine += n_tiles_of(cnt, bm);
+      }
+      int ntiles = 0;
+      int tpos = wave_exscan(mine, ntiles);
+      for (int n = nb; n < ne; ++n) {
+        const int o = off[n], cnt = off[n + 1] - o;
+        if (!(lv.work_all || fac[n] >= 0) || cnt == 0) continue;
+        const int widx = lv.work_all ? n : fac[n];
+        for (int r = 0; r < cnt; r += bm) {
+          TileEntry te;
+          te.widx = widx;
+          te.row0 = o + r;
+          te.nrows = cnt - r < bm ? cnt - r : bm;
+          te.node = n;
+          lv.tiles[tab][tpos++] = te;
+        }
+      }
+      if (lane == 0) *lv.n_tiles[tab] = ntiles;
+    }
+  };
+  // C: each slot's row, first-slot flags, row tokens, summed weights
+  auto phase_c = [&](const int l, const int q) {
+    const BucketLevel& lv = a.lv[l];
+    const unsigned long long* const mask = S.mask[q];
     for (int s = tid; s < TK; s += nth) {
       const int t = s / k, j = s - t * k;
-      const int n = S.node[s];
+      const int n = S.node[q][s];
       if (n < 0) {
         lv.slot_row[s] = -1;
         lv.slot_flags[s] = 0;
         if (l == L && a.w) a.slot_wsum[s] = 0.f;
         continue;
       }
-      const int row = S.off[n] + __popcll(mask[n] & ((1ull << t) - 1ull));
+      const int row = S.off[q][n] + __popcll(mask[n] & ((1ull << t) - 1ull));
       lv.slot_row[s] = row;
       bool first = true;
-      for (int j2 = 0; j2 < j; ++j2) first &= (S.node[t * k + j2] != n);
+      for (int j2 = 0; j2 < j; ++j2) first &= (S.node[q][t * k + j2] != n);
       if (first) lv.row_token[row] = t;
-      const bool work = lv.work_all || S.fac[n] >= 0;
+      const bool work = lv.work_all || S.fac[q][n] >= 0;
       lv.slot_flags[s] = (uint8_t)((first ? 1 : 0) | (work ? 2 : 0));
       // expert level: summed weight of each distinct expert, on its first slot
       if (l == L && a.w) {
         float ws = 0.f;
         if (first)
           for (int j2 = j; j2 < k; ++j2)
-            if (S.node[t * k + j2] == n) ws += S.w[t * k + j2];
+            if (S.node[q][t * k + j2] == n) ws += S.w[t * k + j2];
         a.slot_wsum[s] = ws;
       }
     }
-    if (l < L)  // the next level's mask buffer (last read two phases ago)
-      for (int n = tid; n < a.lv[l + 1].n_nodes; n += nth) S.mask[(l + 1) & 1][n] = 0ull;
+  };
+
+  // levels in pairs: both levels' A, then B on wavefronts 0 and 1, then both C
+#pragma unroll
+  for (int l0 = 0; l0 <= L; l0 += 2) {
+    const bool two = l0 + 1 <= L;
+    phase_a(l0, 0);
+    if (two) phase_a(l0 + 1, 1);
     lds_barrier();
+    if (tid < 64)
+      phase_b(l0, 0);
+    else if (two && tid < 128)
+      phase_b(l0 + 1, 1);
+    lds_barrier();
+    phase_c(l0, 0);
+    if (two) phase_c(l0 + 1, 1);
+    if (l0 + 2 <= L) {  // the next pair's masks (both read by the C phase above)
+      lds_barrier();
+      for (int n = tid; n < a.lv[l0 + 2].n_nodes; n += nth) S.mask[0][n] = 0ull;
+      if (l0 + 3 <= L)
+        for (int n = tid; n < a.lv[l0 + 3 <= L ? l0 + 3 : l0 + 2].n_nodes; n += nth) S.mask[1][n] = 0ull;
+      lds_barrier();
+    }
   }
   if (bad) atomicOr(&S.bad, bad);
   lds_barrier();
